@@ -1,0 +1,136 @@
+/*
+ * rmuscle.h: C ABI of the Action Cache sparse-FFN hot path on one AMD Instinct MI355X (gfx950).
+ *
+ * The paper's Action Cache (section 4.1, "Group-Shared Neuron Masks" and "Anchors with Mask Recomputation")
+ * keeps, per action-expert FFN layer, a mask of important intermediate neurons taken from a similar reference
+ * execution.  The mask is shared by the consecutive denoising steps of a group, and at each such step only
+ * the selected neurons' hidden activations h^M are computed and applied through their down-projection rows
+ * (Eq. 4).  This library implements that update with a zero anchor, i.e. the masked SwiGLU FFN
+ *
+ *     y[b,t,:] = x[b,t,:] + sum_{i < count[b]} h[b,t,i] * w_down[idx[b][i], :]
+ *     h[b,t,i] = SiLU(<w_gate[idx[b][i]], xn[b,t]>) * <w_up[idx[b][i]], xn[b,t]>
+ *     xn       = norm_g ? x / sqrt(mean(x^2) + norm_eps) * norm_g : x
+ *
+ * where only the listed rows of w_gate / w_up / w_down are read.
+ *
+ * Conventions shared by every call
+ *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every buffer and the stream; the
+ *     library allocates nothing, keeps no state except a thread-local error string, and never synchronizes.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the default stream).
+ *   - Every argument is validated on the host before anything is enqueued; on error nothing is enqueued and
+ *     the call returns a negative rm_status with a detail message in rm_last_error().
+ *   - Index lists are multisets: a neuron listed twice contributes twice.  Lists made by rm_mask_compact hold
+ *     no repeats.  An index outside [0, d_ff) is undefined behaviour (not checked on the device).
+ *   - Activations are float32.  Weights are float32 (RM_F32) or bfloat16 (RM_BF16); accumulation is float32.
+ *     On the bf16 path the FFN input xn and the activations h are rounded to bf16 before the matrix-core
+ *     products.
+ *   - The result is deterministic: no floating-point atomics; repeated calls give bitwise equal outputs.
+ */
+#ifndef RMUSCLE_H
+#define RMUSCLE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rm_status {
+    RM_OK = 0,
+    RM_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, bad enum value            */
+    RM_ERR_SHAPE = -2,       /* d not a multiple of 32, max_count outside [0, d_ff], ...    */
+    RM_ERR_DTYPE = -3,       /* unknown weight dtype                                        */
+    RM_ERR_ALIGN = -4,       /* a pointer is not 16-byte aligned                            */
+    RM_ERR_WORKSPACE = -5,   /* ws_bytes smaller than rm_workspace_size() asks for          */
+    RM_ERR_HIP = -6          /* the HIP runtime refused a launch (see rm_last_error())      */
+} rm_status;
+
+typedef enum rm_dtype { RM_F32 = 0, RM_BF16 = 1 } rm_dtype;
+
+/* Shape of one FFN layer.  d: model width (multiple of 32).  d_ff: intermediate neurons (>= 1).
+ * wdtype: an rm_dtype.  norm_eps: RMSNorm epsilon (1e-6 in the workloads); ignored without norm_g. */
+typedef struct rm_ffn_shape {
+    int32_t d;
+    int32_t d_ff;
+    int32_t wdtype;
+    float norm_eps;
+} rm_ffn_shape;
+
+/* Weights of one layer, all row-major [d_ff][d] in the dtype of rm_ffn_shape.wdtype.
+ * Row n of every matrix belongs to intermediate neuron n:
+ *   w_gate[n], w_up[n]: the gate and up projections (PyTorch nn.Linear weights of shape [d_ff][d]);
+ *   w_down[n]: the neuron's down-projection row, i.e. the row-vector form W^down of Eq. 4 (the transpose of a
+ *              PyTorch down_proj.weight of shape [d][d_ff]), so that a neuron's down weights are contiguous.
+ * norm_g: float32 [d] RMSNorm gain applied to the FFN input, or NULL for no norm.  All pointers 16-byte
+ * aligned.  Read-only. */
+typedef struct rm_ffn_layer_weights {
+    const void *w_gate;
+    const void *w_up;
+    const void *w_down;
+    const float *norm_g;
+} rm_ffn_layer_weights;
+
+/* Mask -> ascending active-neuron index list (section 4.1: a reference stores its selected neuron indices;
+ * section 5: one mask per layer and group).
+ *   mask:  uint8 [n_masks][d_ff], nonzero = active (a torch.bool tensor's storage qualifies).
+ *   idx:   int32 [n_masks][d_ff] out.  Row m holds the active positions of mask m in ascending order in its
+ *          first count[m] entries and -1 in the rest (the whole row is written).
+ *   count: int32 [n_masks] out, the number of active neurons of each mask.
+ * n_masks >= 1, d_ff >= 1.  idx and count must not overlap mask.  Errors: RM_ERR_INVALID_ARG for null
+ * pointers or non-positive sizes, RM_ERR_ALIGN if idx or count is not 4-byte aligned. */
+rm_status rm_mask_compact(const uint8_t *mask, int32_t n_masks, int32_t d_ff, int32_t *idx, int32_t *count,
+                          void *stream);
+
+/* Workspace bytes (written to *bytes, a host pointer) needed by rm_sparse_ffn_layer / rm_sparse_ffn_stack /
+ * rm_dense_ffn_ref for B samples of T tokens with at most max_count listed neurons per sample and layer
+ * (max_count = d_ff for the dense call).  The workspace is scratch owned by the caller: 256-byte aligned
+ * device memory, contents need not be initialized, reused by every layer of a call, and it must not be used by
+ * two calls that may run at the same time. */
+rm_status rm_workspace_size(const rm_ffn_shape *s, int32_t B, int32_t T, int32_t max_count, size_t *bytes);
+
+/* One masked FFN layer with residual (Eq. 4 with a zero anchor; see the file comment).
+ *   s, w:   host pointers to the shape and to the layer's weights.
+ *   x:      float32 [B][T][d] input.   y: float32 [B][T][d] output; y == x (in place) is allowed, any other
+ *           overlap is not.
+ *   idx:    int32 [B][d_ff]: sample b's list in idx[b][0 .. count[b]-1] (the rm_mask_compact layout).
+ *   count:  int32 [B], each in [0, max_count]; read on the device, so it may be produced by an earlier kernel.
+ *   max_count: host-side upper bound of count[], in [0, d_ff]; sizes the launch and the workspace.
+ *   ws, ws_bytes: workspace of at least rm_workspace_size(s, B, T, max_count) bytes.
+ * count[b] == 0 gives y[b] == x[b] bit for bit. */
+rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
+                              const float *x, float *y, const int32_t *idx, const int32_t *count,
+                              int32_t max_count, void *ws, size_t ws_bytes, void *stream);
+
+/* L masked FFN layers applied in order (the action expert's layer loop within one denoising step, sections
+ * 2.4 and 4.1): layer l reads layer l-1's output.  w is a host array of L weight structs.  idx is
+ * int32 [L][B][d_ff] and count int32 [L][B] (one rm_mask_compact call over L*B masks fills both); max_count
+ * bounds every count.  x, y, ws as for rm_sparse_ffn_layer (y == x allowed).  L >= 1. */
+rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
+                              int32_t T, const float *x, float *y, const int32_t *idx, const int32_t *count,
+                              int32_t max_count, void *ws, size_t ws_bytes, void *stream);
+
+/* The dense FFN layer with residual: every neuron active (the anchor step of a group, section 4.1, and the
+ * dense fallback of section 5).  Same arguments as rm_sparse_ffn_layer without the lists; the workspace is
+ * sized with max_count = d_ff. */
+rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
+                           const float *x, float *y, void *ws, size_t ws_bytes, void *stream);
+
+/* Measurement hook.  Arms two hipEvent_t (begin, end) to be recorded on the call's stream immediately before
+ * and after the next launch of the named kernel by this thread; the hook disarms after that launch.  Passing
+ * NULL events disarms it.  kernel: 0 = gate/up projection, 1 = down projection (with residual).  Recording
+ * events between kernels costs a few microseconds of queue time; leave the hook disarmed outside timing. */
+typedef enum rm_kernel_id { RM_KERNEL_GATEUP = 0, RM_KERNEL_DOWN = 1 } rm_kernel_id;
+rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end);
+
+/* Static description of a status code. */
+const char *rm_status_string(rm_status status);
+
+/* Detail of this thread's last failed call ("" if none). */
+const char *rm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RMUSCLE_H */

@@ -1,0 +1,254 @@
+"""Python binding of librmuscle.so, the Action Cache sparse-FFN hot path for MI355X (gfx950).
+
+Argument marshalling only: every function checks tensor devices, dtypes and shapes, turns them into raw
+device pointers plus the current HIP stream, and calls the C ABI function of the same name (declared in
+include/rmuscle.h).  All computation runs in the library's HIP kernels; there is no fallback.  If the library
+is not built, or no GPU is present, the calls raise.
+
+Layouts (see include/rmuscle.h for the full contract):
+  mask  uint8/bool [N][d_ff] -> idx int32 [N][d_ff] (ascending, -1 tail), count int32 [N]
+  x, y  float32 [B][T][d];  weights [d_ff][d] float32 or bfloat16, row n = neuron n (w_down neuron-major)
+  idx   int32 [B][d_ff] per layer ([L][B][d_ff] for a stack), count int32 [B] ([L][B])
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "librmuscle.so")
+
+RM_OK = 0
+RM_ERR_INVALID_ARG = -1
+RM_ERR_SHAPE = -2
+RM_ERR_DTYPE = -3
+RM_ERR_ALIGN = -4
+RM_ERR_WORKSPACE = -5
+RM_ERR_HIP = -6
+
+RM_F32 = 0
+RM_BF16 = 1
+RM_KERNEL_GATEUP = 0
+RM_KERNEL_DOWN = 1
+
+EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_stack",
+            "rm_dense_ffn_ref", "rm_profile_kernel_events", "rm_status_string", "rm_last_error")
+
+Layer = Tuple[torch.Tensor, torch.Tensor, torch.Tensor, Optional[torch.Tensor]]
+
+
+class RmError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        self.detail = detail
+        super().__init__(f"{status_string(status)}: {detail}")
+
+
+class FfnShape(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("d_ff", ctypes.c_int32), ("wdtype", ctypes.c_int32),
+                ("norm_eps", ctypes.c_float)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [("w_gate", ctypes.c_void_p), ("w_up", ctypes.c_void_p), ("w_down", ctypes.c_void_p),
+                ("norm_g", ctypes.c_void_p)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def library_path() -> str:
+    return LIB_PATH
+
+
+def load_library() -> ctypes.CDLL:
+    """Load librmuscle.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2609_19104_amd.build` "
+                           "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, vp, sz = ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+    sp, wp = ctypes.POINTER(FfnShape), ctypes.POINTER(LayerWeights)
+    sigs = {
+        "rm_mask_compact": [vp, i32, i32, vp, vp, vp],
+        "rm_workspace_size": [sp, i32, i32, i32, ctypes.POINTER(sz)],
+        "rm_sparse_ffn_layer": [sp, wp, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp],
+        "rm_sparse_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp],
+        "rm_dense_ffn_ref": [sp, wp, i32, i32, vp, vp, vp, sz, vp],
+        "rm_profile_kernel_events": [i32, vp, vp],
+        "rm_status_string": [i32],
+        "rm_last_error": [],
+    }
+    for name, args in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_char_p if name in ("rm_status_string", "rm_last_error") else ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().rm_status_string(status).decode()
+
+
+def last_error() -> str:
+    return load_library().rm_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != RM_OK:
+        raise RmError(status, last_error())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _need_cuda(name: str, t: torch.Tensor, dtypes, ndim: Optional[int] = None) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a HIP device, got {t.device}")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+
+
+def wdtype_of(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return RM_BF16
+    if t.dtype == torch.float32:
+        return RM_F32
+    raise ValueError(f"weights must be float32 or bfloat16, got {t.dtype}")
+
+
+def _shape(layer: Layer, eps: float) -> FfnShape:
+    wg = layer[0]
+    return FfnShape(int(wg.shape[1]), int(wg.shape[0]), wdtype_of(wg), float(eps))
+
+
+def _weights(layer: Layer) -> LayerWeights:
+    wg, wu, wd, g = layer
+    d_ff, d = wg.shape
+    for name, w in (("w_gate", wg), ("w_up", wu), ("w_down", wd)):
+        _need_cuda(name, w, (wg.dtype,), 2)
+        if tuple(w.shape) != (d_ff, d):
+            raise ValueError(f"{name} has shape {tuple(w.shape)}, expected {(d_ff, d)} (neuron-major)")
+    if g is not None:
+        _need_cuda("norm_g", g, (torch.float32,), 1)
+        if g.shape[0] != d:
+            raise ValueError("norm_g must have d entries")
+    return LayerWeights(wg.data_ptr(), wu.data_ptr(), wd.data_ptr(), _ptr(g))
+
+
+def _activations(x: torch.Tensor, y: torch.Tensor, d: int) -> Tuple[int, int]:
+    _need_cuda("x", x, (torch.float32,), 3)
+    _need_cuda("y", y, (torch.float32,), 3)
+    if x.shape != y.shape or x.shape[2] != d:
+        raise ValueError(f"x {tuple(x.shape)} and y {tuple(y.shape)} must both be [B][T][{d}]")
+    return int(x.shape[0]), int(x.shape[1])
+
+
+# ----------------------------------------------------------------------------------------------------------
+# The C ABI calls
+# ----------------------------------------------------------------------------------------------------------
+
+def rm_mask_compact(mask: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, stream=None) -> None:
+    """mask uint8/bool [N][d_ff] -> idx int32 [N][d_ff] (ascending, -1 tail) and count int32 [N]."""
+    _need_cuda("mask", mask, (torch.uint8, torch.bool), 2)
+    n, d_ff = mask.shape
+    _need_cuda("idx", idx, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    if idx.numel() != n * d_ff or count.numel() != n:
+        raise ValueError("idx must hold N*d_ff and count N entries")
+    _check(load_library().rm_mask_compact(mask.data_ptr(), n, d_ff, idx.data_ptr(), count.data_ptr(),
+                                          _stream(stream)))
+
+
+def rm_workspace_size(d: int, d_ff: int, wdtype: int, B: int, T: int, max_count: int, eps: float = 1e-6) -> int:
+    out = ctypes.c_size_t(0)
+    shape = FfnShape(d, d_ff, wdtype, eps)
+    _check(load_library().rm_workspace_size(ctypes.byref(shape), B, T, max_count, ctypes.byref(out)))
+    return int(out.value)
+
+
+def workspace(d: int, d_ff: int, wdtype: int, B: int, T: int, max_count: int, device="cuda") -> torch.Tensor:
+    """Allocate a workspace tensor (uint8) of the size rm_workspace_size asks for."""
+    return torch.empty(rm_workspace_size(d, d_ff, wdtype, B, T, max_count), dtype=torch.uint8, device=device)
+
+
+def _ws(ws: torch.Tensor) -> Tuple[int, int]:
+    _need_cuda("ws", ws, (torch.uint8,))
+    return ws.data_ptr(), ws.numel()
+
+
+def rm_sparse_ffn_layer(x: torch.Tensor, y: torch.Tensor, layer: Layer, idx: torch.Tensor, count: torch.Tensor,
+                        max_count: int, ws: torch.Tensor, eps: float = 1e-6, stream=None) -> None:
+    """y = x + masked SwiGLU FFN over the listed neurons (y may be x)."""
+    shape = _shape(layer, eps)
+    w = _weights(layer)
+    B, T = _activations(x, y, shape.d)
+    _need_cuda("idx", idx, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    if idx.numel() != B * shape.d_ff or count.numel() != B:
+        raise ValueError("idx must be [B][d_ff] and count [B]")
+    wp, wn = _ws(ws)
+    _check(load_library().rm_sparse_ffn_layer(ctypes.byref(shape), ctypes.byref(w), B, T, x.data_ptr(),
+                                              y.data_ptr(), idx.data_ptr(), count.data_ptr(), int(max_count),
+                                              wp, wn, _stream(stream)))
+
+
+def rm_sparse_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
+                        count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6,
+                        stream=None) -> None:
+    """L masked FFN layers in order; idx [L][B][d_ff], count [L][B]."""
+    L = len(layers)
+    if L == 0:
+        raise ValueError("at least one layer")
+    shape = _shape(layers[0], eps)
+    arr = (LayerWeights * L)()
+    for l, layer in enumerate(layers):
+        s = _shape(layer, eps)
+        if (s.d, s.d_ff, s.wdtype) != (shape.d, shape.d_ff, shape.wdtype):
+            raise ValueError("every layer of a stack must have the same shape and dtype")
+        arr[l] = _weights(layer)
+    B, T = _activations(x, y, shape.d)
+    _need_cuda("idx", idx, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    if idx.numel() != L * B * shape.d_ff or count.numel() != L * B:
+        raise ValueError("idx must be [L][B][d_ff] and count [L][B]")
+    wp, wn = _ws(ws)
+    _check(load_library().rm_sparse_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
+                                              idx.data_ptr(), count.data_ptr(), int(max_count), wp, wn,
+                                              _stream(stream)))
+
+
+def rm_dense_ffn_ref(x: torch.Tensor, y: torch.Tensor, layer: Layer, ws: torch.Tensor, eps: float = 1e-6,
+                     stream=None) -> None:
+    """y = x + dense SwiGLU FFN (every neuron)."""
+    shape = _shape(layer, eps)
+    w = _weights(layer)
+    B, T = _activations(x, y, shape.d)
+    wp, wn = _ws(ws)
+    _check(load_library().rm_dense_ffn_ref(ctypes.byref(shape), ctypes.byref(w), B, T, x.data_ptr(), y.data_ptr(),
+                                           wp, wn, _stream(stream)))
+
+
+def rm_profile_kernel_events(kernel: int, ev_begin: Optional[int], ev_end: Optional[int]) -> None:
+    """Arm raw hipEvent_t handles around the next launch of `kernel` (RM_KERNEL_GATEUP / RM_KERNEL_DOWN)."""
+    _check(load_library().rm_profile_kernel_events(kernel, ev_begin, ev_end))

@@ -1,0 +1,182 @@
+// float32 masked SwiGLU FFN on the vector ALU (for float32 weights; float32 end to end).
+//
+// With float32 weights the arithmetic intensity is T/2 FLOP per weight byte, a few FLOP/B at the small token
+// counts of an action chunk, so the vector ALU keeps up with HBM and no input rounding is needed.
+//
+// gate/up (gateup_f32_kernel): one wave per 8 listed neurons; 8 lanes per neuron row, each lane reading
+//   16 contiguous bytes (128 contiguous bytes per row per step).  8 tokens per register block; the 8 lanes'
+//   partial dot products are combined with a fixed xor butterfly, then lane j forms h for token j.
+// down + residual (down_f32_kernel): one wave per (256-column tile, K-slice of listed neurons, sample); a lane
+//   owns 4 columns, loops over its slice's neurons (one 1 KB coalesced row segment per neuron and wave) and
+//   keeps 8 tokens x 4 columns of float32 sums.  The slice's partial is finished by the ticket scheme of
+//   rm_finish.h (fixed-order sum over slices, + x, no float atomics).
+#include "rm_finish.h"
+#include "rm_internal.h"
+
+namespace {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int clamp_neuron(int n, int d_ff) { return n < 0 ? 0 : (n >= d_ff ? d_ff - 1 : n); }
+
+__global__ __launch_bounds__(kWave) void gateup_f32_kernel(
+    const float *__restrict__ wg, const float *__restrict__ wu, const float *__restrict__ xn,
+    const int32_t *__restrict__ idx, const int32_t *__restrict__ count, int max_count, int d_ff, int d, int T,
+    int tpad, float *__restrict__ H, int kcap) {
+    const int b = blockIdx.y;
+    const int slot0 = blockIdx.x * rm::kF32NeurPerBlk;
+    const int lane = threadIdx.x;
+    int cnt = idx ? count[b] : d_ff;
+    cnt = cnt < 0 ? 0 : (cnt > max_count ? max_count : cnt);
+    if (slot0 >= cnt) return;  // the down projection never reads slots past the list
+
+    const int r = lane >> 3;  // neuron of the block
+    const int cl = lane & 7;  // 16-byte column group of each 128-byte step
+    const int slot = slot0 + r;
+    const bool valid = slot < cnt;
+    const int n = valid ? (idx ? clamp_neuron(idx[static_cast<size_t>(b) * d_ff + slot], d_ff) : slot) : 0;
+    const float *grow = wg + static_cast<size_t>(n) * d;
+    const float *urow = wu + static_cast<size_t>(n) * d;
+    const float *xb = xn + static_cast<size_t>(b) * T * d;
+    float *Hb = H + static_cast<size_t>(b) * tpad * kcap;
+
+    for (int t0 = 0; t0 < T; t0 += rm::kF32TokBlock) {
+        const int nt = min(rm::kF32TokBlock, T - t0);
+        float ag[rm::kF32TokBlock], au[rm::kF32TokBlock];
+#pragma unroll
+        for (int t = 0; t < rm::kF32TokBlock; ++t) ag[t] = au[t] = 0.0f;
+        for (int c = cl * 4; c < d; c += 32) {
+            float4 g4 = make_float4(0.f, 0.f, 0.f, 0.f), u4 = g4;
+            if (valid) {
+                g4 = *reinterpret_cast<const float4 *>(grow + c);
+                u4 = *reinterpret_cast<const float4 *>(urow + c);
+            }
+#pragma unroll
+            for (int t = 0; t < rm::kF32TokBlock; ++t) {
+                if (t < nt) {
+                    const float4 xv = *reinterpret_cast<const float4 *>(xb + static_cast<size_t>(t0 + t) * d + c);
+                    ag[t] = fmaf(g4.x, xv.x, ag[t]);
+                    ag[t] = fmaf(g4.y, xv.y, ag[t]);
+                    ag[t] = fmaf(g4.z, xv.z, ag[t]);
+                    ag[t] = fmaf(g4.w, xv.w, ag[t]);
+                    au[t] = fmaf(u4.x, xv.x, au[t]);
+                    au[t] = fmaf(u4.y, xv.y, au[t]);
+                    au[t] = fmaf(u4.z, xv.z, au[t]);
+                    au[t] = fmaf(u4.w, xv.w, au[t]);
+                }
+            }
+        }
+        // Combine the 8 lanes of each neuron row (lanes 8r .. 8r+7): fixed butterfly.
+#pragma unroll
+        for (int t = 0; t < rm::kF32TokBlock; ++t) {
+#pragma unroll
+            for (int off = 1; off < 8; off <<= 1) {
+                ag[t] += __shfl_xor(ag[t], off);
+                au[t] += __shfl_xor(au[t], off);
+            }
+        }
+        float gs = 0.f, us = 0.f;
+#pragma unroll
+        for (int t = 0; t < rm::kF32TokBlock; ++t) {
+            if (t == cl) {
+                gs = ag[t];
+                us = au[t];
+            }
+        }
+        if (t0 + cl < tpad && valid) {
+            Hb[static_cast<size_t>(t0 + cl) * kcap + slot] = (cl < nt) ? rm_silu(gs) * us : 0.0f;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kWave) void down_f32_kernel(
+    const float *__restrict__ H, const float *__restrict__ wd, const int32_t *__restrict__ idx,
+    const int32_t *__restrict__ count, int max_count, int d_ff, int d, int T, int tpad, int kcap, int slices,
+    int slice_neurons, const float *x, float *y, float *__restrict__ part, int *__restrict__ tickets) {
+    const int ct = blockIdx.x;
+    const int s = blockIdx.y;
+    const int b = blockIdx.z;
+    const int ncol = gridDim.x;
+    const int lane = threadIdx.x;
+    int cnt = idx ? count[b] : d_ff;
+    cnt = cnt < 0 ? 0 : (cnt > max_count ? max_count : cnt);
+    const int used_slices = (cnt + slice_neurons - 1) / slice_neurons;
+    const int k_begin = s * slice_neurons;
+    const int k_end = min(k_begin + slice_neurons, cnt);
+    const int col0 = ct * rm::kF32ColTile;
+    const int c = col0 + lane * 4;
+    const bool colok = c < d;
+    const float *Hb = H + static_cast<size_t>(b) * tpad * kcap;
+    const int32_t *idxb = idx ? idx + static_cast<size_t>(b) * d_ff : nullptr;
+    float *part_tile = part + (static_cast<size_t>(b) * ncol + ct) * slices * static_cast<size_t>(T) * rm::kF32ColTile;
+    float *P = part_tile + static_cast<size_t>(s) * T * rm::kF32ColTile;
+
+    if (k_begin < k_end) {
+        for (int t0 = 0; t0 < T; t0 += rm::kF32TokBlock) {
+            const int nt = min(rm::kF32TokBlock, T - t0);
+            float4 acc[rm::kF32TokBlock];
+#pragma unroll
+            for (int t = 0; t < rm::kF32TokBlock; ++t) acc[t] = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int k = k_begin; k < k_end; ++k) {
+                const int n = idxb ? clamp_neuron(idxb[k], d_ff) : k;
+                float4 w4 = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (colok) w4 = *reinterpret_cast<const float4 *>(wd + static_cast<size_t>(n) * d + c);
+#pragma unroll
+                for (int t = 0; t < rm::kF32TokBlock; ++t) {
+                    const float h = Hb[static_cast<size_t>(t0 + t) * kcap + k];
+                    acc[t].x = fmaf(h, w4.x, acc[t].x);
+                    acc[t].y = fmaf(h, w4.y, acc[t].y);
+                    acc[t].z = fmaf(h, w4.z, acc[t].z);
+                    acc[t].w = fmaf(h, w4.w, acc[t].w);
+                }
+            }
+            if (colok) {
+#pragma unroll
+                for (int t = 0; t < rm::kF32TokBlock; ++t)
+                    if (t < nt)
+                        *reinterpret_cast<float4 *>(P + static_cast<size_t>(t0 + t) * rm::kF32ColTile + lane * 4) =
+                            acc[t];
+            }
+        }
+    }
+
+    rm_finish_column_tile<rm::kF32ColTile>(part_tile, slices, used_slices,
+                                           tickets + static_cast<size_t>(b) * ncol + ct,
+                                           x + static_cast<size_t>(b) * T * d, y + static_cast<size_t>(b) * T * d,
+                                           T, d, col0);
+}
+
+}  // namespace
+
+namespace rm {
+
+hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
+                             const int32_t *count, void *ws, hipStream_t st) {
+    char *base = static_cast<char *>(ws);
+    const float *xn = reinterpret_cast<const float *>(base + p.off_xn);
+    float *H = reinterpret_cast<float *>(base + p.off_h);
+    profile_before(RM_KERNEL_GATEUP, st);
+    hipLaunchKernelGGL(gateup_f32_kernel, dim3(p.gate_blocks, p.B), dim3(kWave), 0, st,
+                       static_cast<const float *>(w_gate), static_cast<const float *>(w_up), xn, idx, count,
+                       p.max_count, p.d_ff, p.d, p.T, p.tpad, H, p.kcap);
+    hipError_t e = hipGetLastError();
+    profile_after(RM_KERNEL_GATEUP, st);
+    return e;
+}
+
+hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
+                           const float *x, float *y, void *ws, hipStream_t st) {
+    char *base = static_cast<char *>(ws);
+    const float *H = reinterpret_cast<const float *>(base + p.off_h);
+    float *part = reinterpret_cast<float *>(base + p.off_part);
+    int *tickets = reinterpret_cast<int *>(base + p.off_ticket);
+    profile_before(RM_KERNEL_DOWN, st);
+    hipLaunchKernelGGL(down_f32_kernel, dim3(p.ncol, p.slices, p.B), dim3(kWave), 0, st, H,
+                       static_cast<const float *>(w_down), idx, count, p.max_count, p.d_ff, p.d, p.T, p.tpad,
+                       p.kcap, p.slices, p.slice_units, x, y, part, tickets);
+    hipError_t e = hipGetLastError();
+    profile_after(RM_KERNEL_DOWN, st);
+    return e;
+}
+
+}  // namespace rm

@@ -1,0 +1,80 @@
+// FFN input preparation: xn = x (or RMSNorm(x) * g) in the input dtype of the FFN kernels.
+//
+// The action expert normalizes the FFN input (paper section 4.1 names the FFN input after normalization; the
+// layer is x + FFN(RMSNorm(x))).  One workgroup per token row; the row's sum of squares is reduced in a fixed
+// order (lane butterfly, then waves 0..3), so the scale is deterministic.  The same launch clears the
+// per-column-tile tickets that the down projection counts with.
+#include "rm_internal.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+
+template <bool kBf16Out>
+__global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restrict__ x,
+                                                            const float *__restrict__ g, float eps, int d,
+                                                            void *__restrict__ xn, int *__restrict__ tickets,
+                                                            int ntickets) {
+    const int row = blockIdx.x;
+    const int tid = threadIdx.x;
+    for (int i = row * kThreads + tid; i < ntickets; i += gridDim.x * kThreads) tickets[i] = 0;
+
+    const float *xr = x + static_cast<size_t>(row) * d;
+    float scale = 1.0f;
+    if (g != nullptr) {
+        float ss = 0.0f;
+        for (int c = tid * 4; c < d; c += kThreads * 4) {
+            const float4 v = *reinterpret_cast<const float4 *>(xr + c);
+            ss = fmaf(v.x, v.x, ss);
+            ss = fmaf(v.y, v.y, ss);
+            ss = fmaf(v.z, v.z, ss);
+            ss = fmaf(v.w, v.w, ss);
+        }
+        for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+        __shared__ float wave_ss[kThreads / 64];
+        if ((tid & 63) == 0) wave_ss[tid >> 6] = ss;
+        __syncthreads();
+        const float total = (wave_ss[0] + wave_ss[1]) + (wave_ss[2] + wave_ss[3]);
+        scale = 1.0f / sqrtf(total / static_cast<float>(d) + eps);
+    }
+    for (int c = tid * 4; c < d; c += kThreads * 4) {
+        float4 v = *reinterpret_cast<const float4 *>(xr + c);
+        if (g != nullptr) {
+            const float4 gv = *reinterpret_cast<const float4 *>(g + c);
+            v.x = v.x * scale * gv.x;
+            v.y = v.y * scale * gv.y;
+            v.z = v.z * scale * gv.z;
+            v.w = v.w * scale * gv.w;
+        }
+        const size_t o = static_cast<size_t>(row) * d + c;
+        if constexpr (kBf16Out) {
+            uint2 packed;
+            packed.x = rm_f32_to_bf16_bits(v.x) | (rm_f32_to_bf16_bits(v.y) << 16);
+            packed.y = rm_f32_to_bf16_bits(v.z) | (rm_f32_to_bf16_bits(v.w) << 16);
+            *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(xn) + o) = packed;
+        } else {
+            *reinterpret_cast<float4 *>(static_cast<float *>(xn) + o) = v;
+        }
+    }
+}
+
+}  // namespace
+
+namespace rm {
+
+hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, void *ws, hipStream_t st) {
+    char *base = static_cast<char *>(ws);
+    void *xn = base + p.off_xn;
+    int *tickets = reinterpret_cast<int *>(base + p.off_ticket);
+    const int rows = p.B * p.T;
+    const int ntickets = p.B * p.ncol;
+    if (p.wdtype == RM_BF16)
+        hipLaunchKernelGGL(prologue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.eps, p.d, xn,
+                           tickets, ntickets);
+    else
+        hipLaunchKernelGGL(prologue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.eps, p.d, xn,
+                           tickets, ntickets);
+    return hipGetLastError();
+}
+
+}  // namespace rm

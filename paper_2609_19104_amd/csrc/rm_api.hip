@@ -1,0 +1,283 @@
+// C ABI entry points: argument validation, launch plan / workspace layout, and the layer and stack drivers.
+//
+// Per layer the driver enqueues three kernels on the caller's stream: the prologue (FFN input, optional
+// RMSNorm, ticket clear), the gathered gate/up projection (H), and the gathered down projection with the
+// residual.  A stack repeats them per layer in place on y, reading the next layer's list and weights.  Nothing
+// here synchronizes or allocates.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "rm_internal.h"
+
+#define RM_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+struct ProfileSlot {
+    hipEvent_t begin = nullptr;
+    hipEvent_t end = nullptr;
+};
+thread_local ProfileSlot g_profile[2];
+
+rm_status fail(rm_status st, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+rm_status ok() {
+    g_last_error[0] = '\0';
+    return RM_OK;
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+rm_status check_shape(const rm_ffn_shape *s) {
+    if (s == nullptr) return fail(RM_ERR_INVALID_ARG, "shape pointer is NULL");
+    if (s->d <= 0 || s->d_ff <= 0) return fail(RM_ERR_INVALID_ARG, "d=%d and d_ff=%d must be positive", s->d, s->d_ff);
+    if (s->d % 32 != 0) return fail(RM_ERR_SHAPE, "d=%d must be a multiple of 32", s->d);
+    if (s->wdtype != RM_F32 && s->wdtype != RM_BF16) return fail(RM_ERR_DTYPE, "unknown weight dtype %d", s->wdtype);
+    if (!(s->norm_eps >= 0.0f)) return fail(RM_ERR_INVALID_ARG, "norm_eps must be >= 0");
+    return RM_OK;
+}
+
+rm_status check_layer(const rm_ffn_layer_weights *w, int l) {
+    if (w == nullptr) return fail(RM_ERR_INVALID_ARG, "weights pointer is NULL");
+    if (!w->w_gate || !w->w_up || !w->w_down)
+        return fail(RM_ERR_INVALID_ARG, "layer %d: a weight pointer is NULL", l);
+    if (!aligned(w->w_gate, 16) || !aligned(w->w_up, 16) || !aligned(w->w_down, 16) ||
+        (w->norm_g && !aligned(w->norm_g, 16)))
+        return fail(RM_ERR_ALIGN, "layer %d: weight and gain pointers must be 16-byte aligned", l);
+    return RM_OK;
+}
+
+bool ranges_overlap(const void *a, size_t na, const void *b, size_t nb) {
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+    return pa < pb + nb && pb < pa + na;
+}
+
+// Common checks of a layer / stack / dense call; fills the plan.
+rm_status check_call(const rm_ffn_shape *s, int B, int T, const float *x, float *y, const int32_t *idx,
+                     const int32_t *count, bool sparse, int max_count, void *ws, size_t ws_bytes, rm::Plan *p) {
+    rm_status st = check_shape(s);
+    if (st != RM_OK) return st;
+    if (B <= 0 || T <= 0) return fail(RM_ERR_INVALID_ARG, "B=%d and T=%d must be positive", B, T);
+    if (B > 65535) return fail(RM_ERR_SHAPE, "B=%d exceeds 65535", B);
+    if (!x || !y) return fail(RM_ERR_INVALID_ARG, "x or y is NULL");
+    if (!aligned(x, 16) || !aligned(y, 16)) return fail(RM_ERR_ALIGN, "x and y must be 16-byte aligned");
+    const size_t act_bytes = static_cast<size_t>(B) * T * s->d * sizeof(float);
+    if (x != y && ranges_overlap(x, act_bytes, y, act_bytes))
+        return fail(RM_ERR_INVALID_ARG, "y overlaps x without being equal to it");
+    if (sparse) {
+        if (!idx || !count) return fail(RM_ERR_INVALID_ARG, "idx or count is NULL");
+        if (!aligned(idx, 4) || !aligned(count, 4)) return fail(RM_ERR_ALIGN, "idx and count must be 4-byte aligned");
+        if (max_count < 0 || max_count > s->d_ff)
+            return fail(RM_ERR_SHAPE, "max_count=%d outside [0, d_ff=%d]", max_count, s->d_ff);
+    }
+    st = rm::make_plan(s, B, T, sparse ? max_count : s->d_ff, p);
+    if (st != RM_OK) return st;
+    if (!ws) return fail(RM_ERR_INVALID_ARG, "workspace is NULL");
+    if (!aligned(ws, 16)) return fail(RM_ERR_ALIGN, "workspace must be 16-byte aligned");
+    if (ws_bytes < p->total)
+        return fail(RM_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, p->total);
+    if (ranges_overlap(ws, p->total, x, act_bytes) || ranges_overlap(ws, p->total, y, act_bytes))
+        return fail(RM_ERR_INVALID_ARG, "workspace overlaps x or y");
+    return RM_OK;
+}
+
+rm_status hip_fail(hipError_t e, const char *what) {
+    return fail(RM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+rm_status run_layer(const rm::Plan &p, const rm_ffn_layer_weights *w, const float *x, float *y, const int32_t *idx,
+                    const int32_t *count, void *ws, hipStream_t st) {
+    hipError_t e = rm::launch_prologue(p, x, w->norm_g, ws, st);
+    if (e != hipSuccess) return hip_fail(e, "prologue launch");
+    e = (p.wdtype == RM_BF16) ? rm::launch_gateup_bf16(p, w->w_gate, w->w_up, idx, count, ws, st)
+                              : rm::launch_gateup_f32(p, w->w_gate, w->w_up, idx, count, ws, st);
+    if (e != hipSuccess) return hip_fail(e, "gate/up launch");
+    e = (p.wdtype == RM_BF16) ? rm::launch_down_bf16(p, w->w_down, idx, count, x, y, ws, st)
+                              : rm::launch_down_f32(p, w->w_down, idx, count, x, y, ws, st);
+    if (e != hipSuccess) return hip_fail(e, "down launch");
+    return RM_OK;
+}
+
+}  // namespace
+
+namespace rm {
+
+rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p) {
+    Plan q;
+    q.d = s->d;
+    q.d_ff = s->d_ff;
+    q.wdtype = s->wdtype;
+    q.B = B;
+    q.T = T;
+    q.max_count = max_count;
+    q.eps = s->norm_eps;
+    const int kmax = max_count > 0 ? max_count : 1;
+    size_t xn_elem, h_elem;
+    // Aim for about two workgroups per compute unit (256 CUs) in the down projection.
+    constexpr int kTargetDownGroups = 512;
+    if (s->wdtype == RM_BF16) {
+        q.tpad = ceil_div(T, kBfTokBlock) * kBfTokBlock;
+        q.kcap = ceil_div(kmax, kBfChunk) * kBfChunk;
+        q.gate_blocks = q.kcap / kBfNeurPerBlk;
+        q.col_tile = kBfColTile;
+        q.ncol = ceil_div(s->d, kBfColTile);
+        const int nchunks = q.kcap / kBfChunk;
+        const int s_target = std::max(1, ceil_div(kTargetDownGroups, q.ncol * B));
+        int cps = ceil_div(nchunks, s_target);
+        cps = std::max(kBfWaves, ceil_div(cps, kBfWaves) * kBfWaves);
+        q.slice_units = cps;
+        q.slices = ceil_div(nchunks, cps);
+        xn_elem = 2;
+        h_elem = 2;
+    } else {
+        q.tpad = ceil_div(T, kF32TokBlock) * kF32TokBlock;
+        q.kcap = ceil_div(kmax, kF32NeurPerBlk) * kF32NeurPerBlk;
+        q.gate_blocks = q.kcap / kF32NeurPerBlk;
+        q.col_tile = kF32ColTile;
+        q.ncol = ceil_div(s->d, kF32ColTile);
+        const long long work = static_cast<long long>(kmax) * q.ncol * B;
+        const int su = static_cast<int>(std::max<long long>(kF32SliceNeur, (work + kTargetDownGroups - 1) / kTargetDownGroups));
+        q.slice_units = su;
+        q.slices = ceil_div(kmax, su);
+        xn_elem = 4;
+        h_elem = 4;
+    }
+    if (q.gate_blocks > 0x7fffffff || q.slices > 65535)
+        return fail(RM_ERR_SHAPE, "launch grid too large");
+    size_t off = 0;
+    q.off_xn = off;
+    off = align_up(off + static_cast<size_t>(B) * T * s->d * xn_elem, 256);
+    q.off_h = off;
+    off = align_up(off + static_cast<size_t>(B) * q.tpad * q.kcap * h_elem, 256);
+    q.off_part = off;
+    off = align_up(off + static_cast<size_t>(B) * q.ncol * q.slices * static_cast<size_t>(T) * q.col_tile * 4, 256);
+    q.off_ticket = off;
+    off = align_up(off + static_cast<size_t>(B) * q.ncol * sizeof(int), 256);
+    q.total = off;
+    *p = q;
+    return RM_OK;
+}
+
+void profile_before(int kernel, hipStream_t st) {
+    if (g_profile[kernel].begin) (void)hipEventRecord(g_profile[kernel].begin, st);
+}
+
+void profile_after(int kernel, hipStream_t st) {
+    if (g_profile[kernel].end) (void)hipEventRecord(g_profile[kernel].end, st);
+    g_profile[kernel] = ProfileSlot{};
+}
+
+}  // namespace rm
+
+// ---------------------------------------------------------------------------------------------------------
+// Exported C ABI
+// ---------------------------------------------------------------------------------------------------------
+
+RM_EXPORT rm_status rm_mask_compact(const uint8_t *mask, int32_t n_masks, int32_t d_ff, int32_t *idx, int32_t *count,
+                                    void *stream) {
+    if (!mask || !idx || !count) return fail(RM_ERR_INVALID_ARG, "mask, idx or count is NULL");
+    if (n_masks <= 0 || d_ff <= 0) return fail(RM_ERR_INVALID_ARG, "n_masks=%d and d_ff=%d must be positive", n_masks, d_ff);
+    if (!aligned(idx, 4) || !aligned(count, 4)) return fail(RM_ERR_ALIGN, "idx and count must be 4-byte aligned");
+    const size_t mbytes = static_cast<size_t>(n_masks) * d_ff;
+    if (ranges_overlap(mask, mbytes, idx, mbytes * 4) || ranges_overlap(mask, mbytes, count, n_masks * 4u) ||
+        ranges_overlap(idx, mbytes * 4, count, n_masks * 4u))
+        return fail(RM_ERR_INVALID_ARG, "mask, idx and count must not overlap");
+    const hipError_t e = rm::launch_mask_compact(mask, n_masks, d_ff, idx, count, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "mask compaction launch");
+    return ok();
+}
+
+RM_EXPORT rm_status rm_workspace_size(const rm_ffn_shape *s, int32_t B, int32_t T, int32_t max_count, size_t *bytes) {
+    if (!bytes) return fail(RM_ERR_INVALID_ARG, "bytes is NULL");
+    rm_status st = check_shape(s);
+    if (st != RM_OK) return st;
+    if (B <= 0 || T <= 0) return fail(RM_ERR_INVALID_ARG, "B=%d and T=%d must be positive", B, T);
+    if (max_count < 0 || max_count > s->d_ff)
+        return fail(RM_ERR_SHAPE, "max_count=%d outside [0, d_ff=%d]", max_count, s->d_ff);
+    rm::Plan p;
+    st = rm::make_plan(s, B, T, max_count, &p);
+    if (st != RM_OK) return st;
+    *bytes = p.total;
+    return ok();
+}
+
+RM_EXPORT rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
+                                        const float *x, float *y, const int32_t *idx, const int32_t *count,
+                                        int32_t max_count, void *ws, size_t ws_bytes, void *stream) {
+    rm::Plan p;
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    if (st != RM_OK) return st;
+    st = check_layer(w, 0);
+    if (st != RM_OK) return st;
+    st = run_layer(p, w, x, y, idx, count, ws, static_cast<hipStream_t>(stream));
+    return st == RM_OK ? ok() : st;
+}
+
+RM_EXPORT rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
+                                        int32_t T, const float *x, float *y, const int32_t *idx,
+                                        const int32_t *count, int32_t max_count, void *ws, size_t ws_bytes,
+                                        void *stream) {
+    if (L <= 0) return fail(RM_ERR_INVALID_ARG, "L=%d must be positive", L);
+    if (!w) return fail(RM_ERR_INVALID_ARG, "weights pointer is NULL");
+    rm::Plan p;
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    if (st != RM_OK) return st;
+    for (int l = 0; l < L; ++l) {
+        st = check_layer(&w[l], l);
+        if (st != RM_OK) return st;
+    }
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    const size_t list_stride = static_cast<size_t>(B) * s->d_ff;
+    for (int l = 0; l < L; ++l) {
+        st = run_layer(p, &w[l], l == 0 ? x : y, y, idx + l * list_stride, count + static_cast<size_t>(l) * B, ws, hs);
+        if (st != RM_OK) return st;
+    }
+    return ok();
+}
+
+RM_EXPORT rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
+                                     const float *x, float *y, void *ws, size_t ws_bytes, void *stream) {
+    rm::Plan p;
+    rm_status st = check_call(s, B, T, x, y, nullptr, nullptr, false, 0, ws, ws_bytes, &p);
+    if (st != RM_OK) return st;
+    st = check_layer(w, 0);
+    if (st != RM_OK) return st;
+    st = run_layer(p, w, x, y, nullptr, nullptr, ws, static_cast<hipStream_t>(stream));
+    return st == RM_OK ? ok() : st;
+}
+
+RM_EXPORT rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end) {
+    if (kernel != RM_KERNEL_GATEUP && kernel != RM_KERNEL_DOWN)
+        return fail(RM_ERR_INVALID_ARG, "unknown kernel id %d", kernel);
+    g_profile[kernel].begin = static_cast<hipEvent_t>(ev_begin);
+    g_profile[kernel].end = static_cast<hipEvent_t>(ev_end);
+    return ok();
+}
+
+RM_EXPORT const char *rm_status_string(rm_status status) {
+    switch (status) {
+        case RM_OK: return "RM_OK";
+        case RM_ERR_INVALID_ARG: return "RM_ERR_INVALID_ARG: invalid argument";
+        case RM_ERR_SHAPE: return "RM_ERR_SHAPE: unsupported shape";
+        case RM_ERR_DTYPE: return "RM_ERR_DTYPE: unsupported dtype";
+        case RM_ERR_ALIGN: return "RM_ERR_ALIGN: misaligned pointer";
+        case RM_ERR_WORKSPACE: return "RM_ERR_WORKSPACE: workspace too small";
+        case RM_ERR_HIP: return "RM_ERR_HIP: HIP runtime error";
+    }
+    return "unknown rm_status";
+}
+
+RM_EXPORT const char *rm_last_error(void) { return g_last_error; }

@@ -1,0 +1,91 @@
+// Internal declarations shared by the HIP sources of the rmuscle library (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "rmuscle.h"
+
+namespace rm {
+
+// ---------------------------------------------------------------------------------------------------------
+// Launch plan and workspace layout.  One plan is derived on the host from (shape, B, T, max_count); the same
+// function sizes the workspace and every launch, so they always agree.
+// ---------------------------------------------------------------------------------------------------------
+
+// bf16 path: 16x16x32 bf16 matrix-core tiles.
+constexpr int kBfTokBlock = 64;     // tokens per accumulator block (4 tiles of 16)
+constexpr int kBfNeurPerBlk = 8;    // neurons per gate/up workgroup (8 gate rows + 8 up rows = one 16-row tile)
+constexpr int kBfChunk = 32;        // neurons per down-projection matrix-core step (K of the 16x16x32 tile)
+constexpr int kBfColTile = 128;     // output columns per down workgroup (16 lanes x 8 columns)
+constexpr int kBfWaves = 4;
+
+// f32 path: vector ALU.
+constexpr int kF32TokBlock = 8;     // tokens per register block
+constexpr int kF32NeurPerBlk = 8;   // neurons per gate/up wave (8 lanes per neuron row)
+constexpr int kF32ColTile = 256;    // output columns per down wave (64 lanes x 4 columns)
+constexpr int kF32SliceNeur = 16;   // neurons per down K-slice
+
+struct Plan {
+    int d = 0, d_ff = 0, wdtype = 0, B = 0, T = 0, max_count = 0;
+    float eps = 1e-6f;
+    int tpad = 0;       // T rounded up to the token block (rows of H)
+    int kcap = 0;       // row length of H (neuron slots), max_count rounded up
+    int gate_blocks = 0;// gate/up workgroups per sample
+    int col_tile = 0;   // output columns per down workgroup
+    int ncol = 0;       // column tiles
+    int slices = 0;     // K-slices per column tile (down partial sums)
+    int slice_units = 0;// bf16: 32-neuron chunks per slice; f32: neurons per slice
+    size_t off_xn = 0, off_h = 0, off_part = 0, off_ticket = 0, total = 0;
+};
+
+rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p);
+
+// ---------------------------------------------------------------------------------------------------------
+// Launchers (enqueue only; all arguments already validated).
+// ---------------------------------------------------------------------------------------------------------
+
+hipError_t launch_mask_compact(const uint8_t *mask, int n_masks, int d_ff, int32_t *idx, int32_t *count,
+                               hipStream_t st);
+
+// x -> xn (optional RMSNorm, cast to the path's input dtype); also clears the down-projection tickets.
+hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, void *ws, hipStream_t st);
+
+// Gate/up projection of the listed neurons + SiLU * up -> H in the workspace (one launcher per weight dtype).
+hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
+                              const int32_t *count, void *ws, hipStream_t st);
+hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
+                             const int32_t *count, void *ws, hipStream_t st);
+
+// Down projection of the listed neurons + residual: y = x + H W_down[idx].
+hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
+                            const float *x, float *y, void *ws, hipStream_t st);
+hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
+                           const float *x, float *y, void *ws, hipStream_t st);
+
+// Profiling hook (thread-local events armed by rm_profile_kernel_events).
+void profile_before(int kernel, hipStream_t st);
+void profile_after(int kernel, hipStream_t st);
+
+}  // namespace rm
+
+// ---------------------------------------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------------------------------------
+
+typedef __bf16 rm_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float rm_f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t rm_u32x4 __attribute__((ext_vector_type(4)));
+
+// float -> bfloat16 bits, round to nearest even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint32_t rm_f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ float rm_bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// SiLU(z) = z / (1 + e^-z); e^-z overflows to +inf for very negative z, giving -0, never NaN.
+__device__ __forceinline__ float rm_silu(float z) { return z / (1.0f + expf(-z)); }

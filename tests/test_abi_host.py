@@ -1,0 +1,149 @@
+"""Host-side checks of the C ABI: the library loads, exports exactly what include/rmuscle.h declares, sizes
+workspaces, and rejects bad arguments before enqueuing anything (no GPU needed: every call here fails
+validation or is pure host arithmetic)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2609_19104_amd as rm
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "rmuscle.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:rm_status|const char \*)\s*(rm_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rm.LIB_PATH):
+        pytest.skip("librmuscle.so not built")
+    return rm.load_library()
+
+
+def test_header_declares_the_abi():
+    assert _declared() == sorted(rm.EXPORTED)
+
+
+def test_exports_match_header(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", rm.LIB_PATH], capture_output=True, text=True, check=True)
+    exported = sorted({l.split()[-1] for l in out.stdout.splitlines() if re.search(r"\brm_\w+$", l)})
+    assert exported == _declared()
+    for name in _declared():
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    for st in (rm.RM_OK, rm.RM_ERR_INVALID_ARG, rm.RM_ERR_SHAPE, rm.RM_ERR_DTYPE, rm.RM_ERR_ALIGN,
+               rm.RM_ERR_WORKSPACE, rm.RM_ERR_HIP):
+        assert rm.status_string(st).startswith("RM_")
+    assert "unknown" in rm.status_string(42)
+
+
+def _size(d, d_ff, wdtype, B, T, k):
+    out = ctypes.c_size_t(0)
+    s = rm.FfnShape(d, d_ff, wdtype, 1e-6)
+    st = rm.load_library().rm_workspace_size(ctypes.byref(s), B, T, k, ctypes.byref(out))
+    return st, out.value
+
+
+def test_workspace_size_values(lib):
+    # bf16, d=1024, d_ff=4096, T=51, K=1229: xn 51*1024*2, H 64 tokens x 1248 slots x 2, partials, tickets.
+    st, n = _size(1024, 4096, rm.RM_BF16, 1, 51, 1229)
+    assert st == rm.RM_OK
+    assert n >= 51 * 1024 * 2 + 64 * 1248 * 2 + 8 * 51 * 128 * 4
+    assert n % 256 == 0
+    # Monotone in every size argument.
+    assert _size(1024, 4096, rm.RM_BF16, 2, 51, 1229)[1] > n
+    assert _size(1024, 4096, rm.RM_BF16, 1, 52, 1229)[1] > n
+    assert _size(1024, 4096, rm.RM_BF16, 1, 51, 4096)[1] >= n
+    assert _size(256, 1024, rm.RM_F32, 1, 8, 256)[0] == rm.RM_OK
+    assert _size(1024, 4096, rm.RM_BF16, 1, 51, 0)[0] == rm.RM_OK
+
+
+@pytest.mark.parametrize("args,expected", [
+    ((1000, 4096, 1, 1, 51, 10), rm.RM_ERR_SHAPE),       # d not a multiple of 32
+    ((0, 4096, 1, 1, 51, 10), rm.RM_ERR_INVALID_ARG),
+    ((1024, 0, 1, 1, 51, 0), rm.RM_ERR_INVALID_ARG),
+    ((1024, 4096, 7, 1, 51, 10), rm.RM_ERR_DTYPE),
+    ((1024, 4096, 1, 0, 51, 10), rm.RM_ERR_INVALID_ARG),
+    ((1024, 4096, 1, 1, 0, 10), rm.RM_ERR_INVALID_ARG),
+    ((1024, 4096, 1, 1, 51, 4097), rm.RM_ERR_SHAPE),     # max_count > d_ff
+    ((1024, 4096, 1, 1, 51, -1), rm.RM_ERR_SHAPE),
+])
+def test_workspace_size_rejects(lib, args, expected):
+    st, _ = _size(*args)
+    assert st == expected
+    assert rm.last_error() != ""
+
+
+FAKE = 0x10000  # a 16-byte aligned address that is never dereferenced: validation fails first
+
+
+def _layer_call(lib, *, shape=(1024, 4096, 1), B=1, T=51, x=FAKE, y=FAKE, idx=FAKE, cnt=FAKE, k=100,
+                ws=FAKE * 16, ws_bytes=1 << 30, w=(FAKE, FAKE, FAKE, None)):
+    s = rm.FfnShape(shape[0], shape[1], shape[2], 1e-6)
+    lw = rm.LayerWeights(*w)
+    return lib.rm_sparse_ffn_layer(ctypes.byref(s), ctypes.byref(lw), B, T, x, y, idx, cnt, k, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,expected", [
+    (dict(x=None), rm.RM_ERR_INVALID_ARG),
+    (dict(idx=None), rm.RM_ERR_INVALID_ARG),
+    (dict(cnt=None), rm.RM_ERR_INVALID_ARG),
+    (dict(w=(None, FAKE, FAKE, None)), rm.RM_ERR_INVALID_ARG),
+    (dict(w=(FAKE + 2, FAKE, FAKE, None)), rm.RM_ERR_ALIGN),
+    (dict(w=(FAKE, FAKE, FAKE, FAKE + 4)), rm.RM_ERR_ALIGN),
+    (dict(x=FAKE + 4, y=FAKE + 4), rm.RM_ERR_ALIGN),
+    (dict(idx=FAKE + 2), rm.RM_ERR_ALIGN),
+    (dict(k=5000), rm.RM_ERR_SHAPE),
+    (dict(k=-3), rm.RM_ERR_SHAPE),
+    (dict(shape=(1000, 4096, 1)), rm.RM_ERR_SHAPE),
+    (dict(shape=(1024, 4096, 9)), rm.RM_ERR_DTYPE),
+    (dict(B=0), rm.RM_ERR_INVALID_ARG),
+    (dict(B=70000), rm.RM_ERR_SHAPE),
+    (dict(T=-1), rm.RM_ERR_INVALID_ARG),
+    (dict(ws=None), rm.RM_ERR_INVALID_ARG),
+    (dict(ws_bytes=100), rm.RM_ERR_WORKSPACE),
+    (dict(y=FAKE + 16), rm.RM_ERR_INVALID_ARG),               # y overlaps x without being x
+    (dict(ws=FAKE), rm.RM_ERR_INVALID_ARG),                   # workspace overlaps x
+])
+def test_layer_rejects_before_launch(lib, kw, expected):
+    assert _layer_call(lib, **kw) == expected
+    assert rm.last_error() != ""
+
+
+def test_stack_and_dense_reject(lib):
+    s = rm.FfnShape(1024, 4096, 1, 1e-6)
+    arr = (rm.LayerWeights * 2)(rm.LayerWeights(FAKE, FAKE, FAKE, None), rm.LayerWeights(FAKE, None, FAKE, None))
+    st = lib.rm_sparse_ffn_stack(ctypes.byref(s), arr, 2, 1, 51, FAKE, FAKE, FAKE, FAKE, 10, FAKE * 16, 1 << 30, None)
+    assert st == rm.RM_ERR_INVALID_ARG and "layer 1" in rm.last_error()
+    st = lib.rm_sparse_ffn_stack(ctypes.byref(s), arr, 0, 1, 51, FAKE, FAKE, FAKE, FAKE, 10, FAKE * 16, 1 << 30, None)
+    assert st == rm.RM_ERR_INVALID_ARG
+    lw = rm.LayerWeights(FAKE, FAKE, FAKE, None)
+    st = lib.rm_dense_ffn_ref(ctypes.byref(s), ctypes.byref(lw), 1, 51, FAKE, FAKE, FAKE * 16, 64, None)
+    assert st == rm.RM_ERR_WORKSPACE
+
+
+def test_mask_compact_rejects(lib):
+    assert lib.rm_mask_compact(None, 1, 16, FAKE, FAKE * 2, None) == rm.RM_ERR_INVALID_ARG
+    assert lib.rm_mask_compact(FAKE, 0, 16, FAKE * 2, FAKE * 3, None) == rm.RM_ERR_INVALID_ARG
+    assert lib.rm_mask_compact(FAKE, 1, 16, FAKE * 2 + 1, FAKE * 3, None) == rm.RM_ERR_ALIGN
+    assert lib.rm_mask_compact(FAKE, 4, 16, FAKE + 8, FAKE * 3, None) == rm.RM_ERR_INVALID_ARG  # idx overlaps mask
+
+
+def test_profile_hook_rejects_unknown_kernel(lib):
+    assert lib.rm_profile_kernel_events(5, None, None) == rm.RM_ERR_INVALID_ARG
+    assert lib.rm_profile_kernel_events(rm.RM_KERNEL_GATEUP, None, None) == rm.RM_OK
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(1, 4, 32)
+    with pytest.raises((ValueError, RuntimeError)):
+        rm.rm_dense_ffn_ref(x, x, (torch.zeros(8, 32), torch.zeros(8, 32), torch.zeros(8, 32), None),
+                            torch.zeros(16, dtype=torch.uint8))

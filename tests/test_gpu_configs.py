@@ -1,0 +1,100 @@
+"""GPU parity at the five workload configurations' full sizes, checked element by element against the float64
+oracle (every output of every config; the oracle finishes each in seconds).
+
+Score-based masks are picked by the oracle on the CPU (mean |SiLU(g) * u| on the reference input, ties to the
+lower index), so the GPU and the oracle evaluate exactly the same mask."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from gpu_helpers import (TOL_BF16, TOL_F32, compact, dev_weights, errors, run_dense, run_layer,  # noqa: E402
+                         run_stack)
+
+
+def _lists(masks):
+    idx, cnt = compact(masks)
+    torch.cuda.synchronize()
+    ref_idx, ref_cnt = oracle.compact_mask(masks)
+    assert np.array_equal(idx.cpu().numpy(), ref_idx) and np.array_equal(cnt.cpu().numpy(), ref_cnt)
+    return idx, cnt
+
+
+def _check(y, y_ref, x, tol, label):
+    ey, ed = errors(y, y_ref, x)
+    print(f"{label}: rel err y {ey:.3e} delta {ed:.3e}")
+    assert ey <= tol and ed <= tol, f"{label}: rel err y {ey:.3e}, delta {ed:.3e} > {tol}"
+
+
+def test_config1_fp32_single_layer():
+    w = wl.config1()
+    layer = w.layers[0]
+    mask = w.masks[0]
+    assert int(mask.sum()) == 256
+    idx, cnt = _lists(mask)
+    y = run_layer(dev_weights(layer), w.x, idx, cnt, w.k)
+    wg, wu, wd, g = layer.f64()
+    _check(y[0], oracle.masked_ffn(w.x[0], wg, wu, wd, mask[0].astype(float), g), w.x[0], TOL_F32, "config 1")
+
+
+def test_config2_action_expert_layer():
+    w = wl.config2()
+    layer = w.layers[0]
+    wg, wu, wd, g = layer.f64()
+    mask = oracle.topk_mask(oracle.mean_abs_activation(w.x_ref[0], wg, wu, g), w.k)[None]
+    assert int(mask.sum()) == 1229
+    idx, cnt = _lists(mask)
+    y = run_layer(dev_weights(layer), w.x, idx, cnt, w.k)
+    _check(y[0], oracle.masked_ffn(w.x[0], wg, wu, wd, mask[0].astype(float), g), w.x[0], TOL_BF16, "config 2")
+
+
+def test_config3_stack_schedule():
+    w = wl.config3()
+    layers64 = [l.f64() for l in w.layers]
+    lws = [dev_weights(l) for l in w.layers]
+    masks = None
+    for s, x in enumerate(w.x_steps):
+        if s == 0:
+            y = x
+            for lw in lws:
+                y = run_dense(lw, y)
+            ref = oracle.ffn_stack(x[0], layers64, [np.ones(w.d_ff)] * w.L)
+        else:
+            if s in w.refresh_steps:
+                masks = oracle.stack_masks_from_dense(w.x_steps[s - 1][0], layers64, w.k)
+                idx, cnt = _lists(masks)
+            y = run_stack(lws, x, idx, cnt, w.k)
+            ref = oracle.ffn_stack(x[0], layers64, [m.astype(float) for m in masks])
+        _check(y[0], ref, x[0], TOL_BF16, f"config 3 step {s}")
+
+
+def test_config4_density_sweep():
+    w = wl.config4()
+    layer = w.layers[0]
+    wg, wu, wd, g = layer.f64()
+    masks = oracle.nested_topk_masks(oracle.mean_abs_activation(w.x_ref[0], wg, wu, g), w.ks)
+    lw = dev_weights(layer)
+    for p, k, m in zip(w.percents, w.ks, masks):
+        idx, cnt = _lists(m[None])
+        y = run_layer(lw, w.x, idx, cnt, k)
+        _check(y[0], oracle.masked_ffn(w.x[0], wg, wu, wd, m.astype(float), g), w.x[0], TOL_BF16,
+               f"config 4 at {p}%")
+        if p == 100:
+            assert np.array_equal(y, run_dense(lw, w.x))
+
+
+def test_config5_batched_ragged_stack():
+    w = wl.config5()
+    layers64 = [l.f64() for l in w.layers]
+    idx, cnt = _lists(w.masks.reshape(w.L * w.B, w.d_ff))
+    y = run_stack([dev_weights(l) for l in w.layers], w.x, idx, cnt, w.k)
+    for b in range(w.B):
+        ref = oracle.ffn_stack(w.x[b], layers64, [w.masks[l, b].astype(float) for l in range(w.L)])
+        _check(y[b], ref, w.x[b], TOL_BF16, f"config 5 sample {b}")

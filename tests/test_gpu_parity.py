@@ -1,0 +1,224 @@
+"""GPU parity: the HIP library through its C ABI against the float64 CPU oracle, on the same seeded inputs.
+
+Bars: compaction bit-exact (idx including its -1 tail, and count); FFN outputs within max-abs relative error
+2e-2 (bf16 weights) or 1e-5 (float32 weights) of the oracle, on both y and the FFN delta y - x; the empty list
+gives y == x bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2609_19104_amd as rm  # noqa: E402
+from gpu_helpers import (TOL_BF16, TOL_F32, compact, dev_f32, dev_weights, errors, run_dense,  # noqa: E402
+                         run_layer, run_stack)
+
+
+def _oracle_layer(layer, x, mult):
+    wg, wu, wd, g = layer.f64()
+    return np.stack([oracle.masked_ffn(x[b], wg, wu, wd, mult[b], g) for b in range(x.shape[0])])
+
+
+def _masks_to_lists(masks):
+    idx, cnt = compact(masks)
+    torch.cuda.synchronize()
+    ref_idx, ref_cnt = oracle.compact_mask(masks)
+    assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
+    assert np.array_equal(idx.cpu().numpy(), ref_idx)
+    return idx, cnt
+
+
+def _check(y, y_ref, x, tol, label=""):
+    ey, ed = errors(y, y_ref, x)
+    print(f"{label} rel err y {ey:.3e} delta {ed:.3e}")
+    assert ey <= tol and ed <= tol, f"{label}: rel err y {ey:.3e}, delta {ed:.3e} > {tol}"
+
+
+# ------------------------------------------------------------------------------------------------ compaction
+
+@pytest.mark.parametrize("d_ff", [1, 3, 63, 64, 65, 1000, 1001, 1024, 4095, 4096, 16384])
+@pytest.mark.parametrize("p", [0.0, 0.02, 0.3, 0.97, 1.0])
+def test_compact_random_bit_exact(d_ff, p):
+    masks = wl.bernoulli_mask(np.random.default_rng(d_ff * 7 + int(p * 100)), (5, d_ff), p)
+    masks[masks == 1] = np.random.default_rng(1).integers(1, 256, size=int(masks.sum()), dtype=np.uint8)
+    _masks_to_lists(masks)
+
+
+def test_compact_edge_masks_bit_exact():
+    for d_ff in (1, 2, 255, 256, 257, 1023, 1025, 4096):
+        rows = [np.zeros(d_ff), np.ones(d_ff), np.eye(1, d_ff, 0)[0], np.eye(1, d_ff, d_ff - 1)[0],
+                (np.arange(d_ff) % 2 == 1), (np.arange(d_ff) % 64 == 63)]
+        _masks_to_lists(np.stack(rows).astype(np.uint8))
+
+
+def test_compact_bool_tensor_storage():
+    m = torch.from_numpy(wl.bernoulli_mask(np.random.default_rng(3), (4, 300), 0.4).astype(bool)).cuda()
+    idx = torch.empty((4, 300), dtype=torch.int32, device="cuda")
+    cnt = torch.empty(4, dtype=torch.int32, device="cuda")
+    rm.rm_mask_compact(m, idx, cnt)
+    ref_idx, ref_cnt = oracle.compact_mask(m.cpu().numpy().astype(np.uint8))
+    assert np.array_equal(idx.cpu().numpy(), ref_idx) and np.array_equal(cnt.cpu().numpy(), ref_cnt)
+
+
+def test_compact_config5_masks():
+    w = wl.config5()
+    _masks_to_lists(w.masks.reshape(-1, w.d_ff))
+
+
+# ------------------------------------------------------------------------------------------------ small layers
+
+BF16_CASES = [
+    # d, d_ff, T, k, norm
+    (256, 1000, 51, 333, "none"),
+    (256, 1000, 1, 1000, "random"),
+    (512, 777, 65, 500, "random"),
+    (128, 300, 130, 64, "none"),
+    (96, 64, 17, 1, "none"),
+    (160, 200, 64, 199, "ones"),
+    (1024, 4096, 51, 1229, "none"),
+]
+
+
+@pytest.mark.parametrize("d,d_ff,T,k,norm", BF16_CASES)
+def test_bf16_layer_parity(d, d_ff, T, k, norm):
+    layer = wl.make_layer(11, d, d, d_ff, "bf16", norm=norm)
+    x = wl.make_x(11, (1, T, d), d_ff, T)
+    mask = wl.uniform_mask(wl.rng(11, 4, d, d_ff, T), d_ff, k)[None]
+    idx, cnt = _masks_to_lists(mask)
+    y = run_layer(dev_weights(layer), x, idx, cnt, k)
+    _check(y, _oracle_layer(layer, x, mask.astype(np.float64)), x, TOL_BF16, f"bf16 {d}x{d_ff} T={T} k={k}")
+
+
+F32_CASES = [
+    (256, 1024, 8, 256, "none"),
+    (64, 100, 3, 37, "random"),
+    (288, 513, 17, 200, "none"),
+    (32, 16, 1, 16, "ones"),
+]
+
+
+@pytest.mark.parametrize("d,d_ff,T,k,norm", F32_CASES)
+def test_f32_layer_parity(d, d_ff, T, k, norm):
+    layer = wl.make_layer(12, d, d, d_ff, "f32", norm=norm)
+    x = wl.make_x(12, (1, T, d), d_ff, T)
+    mask = wl.uniform_mask(wl.rng(12, 4, d, d_ff, T), d_ff, k)[None]
+    idx, cnt = _masks_to_lists(mask)
+    y = run_layer(dev_weights(layer), x, idx, cnt, k)
+    _check(y, _oracle_layer(layer, x, mask.astype(np.float64)), x, TOL_F32, f"f32 {d}x{d_ff} T={T} k={k}")
+
+
+# ------------------------------------------------------------------------------------------------ invariants
+
+@pytest.mark.parametrize("wdtype", ["bf16", "f32"])
+def test_empty_list_is_bitwise_identity(wdtype):
+    layer = wl.make_layer(13, 0, 256, 512, wdtype, norm="random")
+    x = wl.make_x(13, (3, 20, 256), 0)
+    x[0, 0, :5] = -0.0
+    mask = np.zeros((3, 512), np.uint8)
+    idx, cnt = _masks_to_lists(mask)
+    y = run_layer(dev_weights(layer), x, idx, cnt, 100)
+    assert np.array_equal(y.view(np.uint32), x.view(np.uint32))
+    y0 = run_layer(dev_weights(layer), x, idx, cnt, 0)
+    assert np.array_equal(y0.view(np.uint32), x.view(np.uint32))
+
+
+@pytest.mark.parametrize("wdtype", ["bf16", "f32"])
+def test_all_ones_equals_dense_and_oracle(wdtype):
+    layer = wl.make_layer(14, 0, 256, 640, wdtype, norm="random")
+    x = wl.make_x(14, (2, 51, 256), 0)
+    mask = np.ones((2, 640), np.uint8)
+    idx, cnt = _masks_to_lists(mask)
+    lw = dev_weights(layer)
+    y_sparse = run_layer(lw, x, idx, cnt, 640)
+    y_dense = run_dense(lw, x)
+    assert np.array_equal(y_sparse, y_dense)
+    wg, wu, wd, g = layer.f64()
+    y_ref = np.stack([oracle.dense_ffn(x[b], wg, wu, wd, g) for b in range(2)])
+    _check(y_dense, y_ref, x, TOL_BF16 if wdtype == "bf16" else TOL_F32, f"dense {wdtype}")
+
+
+@pytest.mark.parametrize("wdtype", ["bf16", "f32"])
+def test_permuted_and_duplicated_lists(wdtype):
+    d, d_ff, T = 256, 700, 33
+    layer = wl.make_layer(15, 0, d, d_ff, wdtype)
+    x = wl.make_x(15, (1, T, d), 0)
+    r = np.random.default_rng(15)
+    lst = r.choice(d_ff, size=300, replace=False).astype(np.int32)  # not sorted
+    lst = np.concatenate([lst, lst[:40]])                             # 40 repeats: a multiset
+    idx = np.full((1, d_ff), -1, np.int32)
+    idx[0, : lst.size] = lst
+    idx_t = torch.from_numpy(idx).cuda()
+    cnt_t = torch.tensor([lst.size], dtype=torch.int32, device="cuda")
+    lw = dev_weights(layer)
+    y = run_layer(lw, x, idx_t, cnt_t, lst.size)
+    mult = oracle.multiplicity(lst, lst.size, d_ff)
+    tol = TOL_BF16 if wdtype == "bf16" else TOL_F32
+    _check(y, _oracle_layer(layer, x, mult[None]), x, tol, f"multiset {wdtype}")
+    idx_rev = idx.copy()
+    idx_rev[0, : lst.size] = lst[::-1]
+    y_rev = run_layer(lw, x, torch.from_numpy(idx_rev).cuda(), cnt_t, lst.size)
+    _check(y_rev, _oracle_layer(layer, x, mult[None]), x, tol, f"reversed {wdtype}")
+
+
+@pytest.mark.parametrize("wdtype", ["bf16", "f32"])
+def test_in_place_and_deterministic(wdtype):
+    layer = wl.make_layer(16, 0, 512, 1024, wdtype, norm="ones")
+    x = wl.make_x(16, (2, 51, 512), 0)
+    masks = np.stack([wl.uniform_mask(wl.rng(16, 4, b), 1024, 300) for b in range(2)])
+    idx, cnt = _masks_to_lists(masks)
+    lw = dev_weights(layer)
+    y1 = run_layer(lw, x, idx, cnt, 300)
+    y2 = run_layer(lw, x, idx, cnt, 300)
+    y3 = run_layer(lw, x, idx, cnt, 300, in_place=True)
+    assert np.array_equal(y1, y2) and np.array_equal(y1, y3)
+
+
+def test_ragged_batch_counts():
+    d, d_ff, T = 1024, 4096, 51
+    counts = [0, 1, 63, 64, 65, 1229, 4096]
+    layer = wl.make_layer(17, 0, d, d_ff, "bf16", norm="ones")
+    x = wl.make_x(17, (len(counts), T, d), 0)
+    masks = wl.ragged_masks(17, d_ff, counts)
+    idx, cnt = _masks_to_lists(masks)
+    y = run_layer(dev_weights(layer), x, idx, cnt, max(counts))
+    y_ref = _oracle_layer(layer, x, masks.astype(np.float64))
+    assert np.array_equal(y[0].view(np.uint32), x[0].view(np.uint32))
+    for b, c in enumerate(counts[1:], start=1):
+        _check(y[b], y_ref[b], x[b], TOL_BF16, f"ragged count {c}")
+
+
+def test_counts_above_max_count_are_clamped_not_read_past():
+    # count[b] larger than the host bound: only the first max_count listed neurons are applied.
+    d, d_ff, T = 256, 512, 16
+    layer = wl.make_layer(18, 0, d, d_ff, "bf16")
+    x = wl.make_x(18, (1, T, d), 0)
+    mask = wl.uniform_mask(wl.rng(18, 4), d_ff, 200)[None]
+    idx, cnt = _masks_to_lists(mask)
+    y = run_layer(dev_weights(layer), x, idx, cnt, 96)
+    first = np.zeros(d_ff)
+    first[oracle.compact_mask(mask)[0][0, :96]] = 1
+    _check(y, _oracle_layer(layer, x, first[None]), x, TOL_BF16, "clamped")
+
+
+def test_stack_equals_layer_sequence():
+    d, d_ff, T, L, B = 256, 512, 51, 3, 2
+    layers = [wl.make_layer(19, l, d, d_ff, "bf16", norm="random") for l in range(L)]
+    x = wl.make_x(19, (B, T, d), 0)
+    masks = np.stack([np.stack([wl.uniform_mask(wl.rng(19, 4, l, b), d_ff, 100 + 50 * l) for b in range(B)])
+                      for l in range(L)])
+    idx, cnt = compact(masks.reshape(L * B, d_ff))
+    lws = [dev_weights(l) for l in layers]
+    y_stack = run_stack(lws, x, idx, cnt, 200)
+    y = x
+    for l in range(L):
+        y = run_layer(lws[l], y, idx[l * B:(l + 1) * B].contiguous(), cnt[l * B:(l + 1) * B].contiguous(), 200)
+    assert np.array_equal(y_stack, y)
+    ref = np.stack([oracle.ffn_stack(x[b], [lay.f64() for lay in layers],
+                                     [masks[l, b].astype(np.float64) for l in range(L)]) for b in range(B)])
+    _check(y_stack, ref, x, TOL_BF16, "stack")

@@ -1,0 +1,279 @@
+"""Benchmark of the Action Cache sparse-FFN hot path on one MI355X.
+
+Workload (default): one pi0-style action-expert FFN layer, bf16 weights / float32 activations, d = 1024,
+d_ff = 4096, T = 51 tokens (50 actions + 1 state), mask = top 30% of neurons (K = 1229) by mean |SiLU(g) * u| on
+a reference input, evaluated on that input + 0.1 N(0,1).  One step is the whole hot path for one batch:
+rm_mask_compact of the layer's mask, then rm_sparse_ffn_layer.
+
+Weights are cold: every step reads a different one of R copies of the layer (>= 1 GiB together), so neither
+L2 nor the 256 MB Infinity Cache can serve them and the weight bytes come from HBM.  Activations, mask and
+index list are small and stay resident.
+
+The printed JSON line gives value = achieved GB/s on active weight bytes (3 K d * 2 B per step) over the timed
+steps, the roofline of the dominant kernel (its algorithmic bytes / its average duration from HIP events
+recorded around its launches by the library's measurement hook, on the launch stream), and the float64 CPU
+oracle timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2|c4-10|c4-30|c4-50|c4-100]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+COLD_BYTES = 1 << 30   # weight copies rotated through per timed run
+
+
+# ----------------------------------------------------------------------------------------------------------
+# Byte / FLOP accounting (algorithmic: active weights only)
+# ----------------------------------------------------------------------------------------------------------
+
+def projection_flops(tokens: int, d: int, d_ff: int) -> int:
+    """FLOPs of one dense projection between widths d and d_ff at `tokens` tokens (multiply + add)."""
+    return 2 * tokens * d * d_ff
+
+
+def matrix_bytes(d: int, d_ff: int, elem_bytes: int) -> int:
+    return d * d_ff * elem_bytes
+
+
+def gateup_bytes(k: int, d: int, elem_bytes: int) -> int:
+    """Active weight bytes of the gate/up kernel: two rows of d weights per listed neuron."""
+    return 2 * k * d * elem_bytes
+
+
+def down_bytes(k: int, d: int, elem_bytes: int) -> int:
+    """Active weight bytes of the down kernel: one neuron-major row of d weights per listed neuron."""
+    return k * d * elem_bytes
+
+
+def active_weight_bytes(k: int, d: int, elem_bytes: int) -> int:
+    return gateup_bytes(k, d, elem_bytes) + down_bytes(k, d, elem_bytes)
+
+
+# ----------------------------------------------------------------------------------------------------------
+# Workloads
+# ----------------------------------------------------------------------------------------------------------
+
+WORKLOADS = {
+    "c2": dict(name="pi0 action-expert FFN layer, bf16, d=1024 d_ff=4096 T=51, top-30% mask", cfg=2, percent=30),
+    "c4-10": dict(name="wide FFN layer, bf16, d=2048 d_ff=16384 T=51, top-10% mask", cfg=4, percent=10),
+    "c4-30": dict(name="wide FFN layer, bf16, d=2048 d_ff=16384 T=51, top-30% mask", cfg=4, percent=30),
+    "c4-50": dict(name="wide FFN layer, bf16, d=2048 d_ff=16384 T=51, top-50% mask", cfg=4, percent=50),
+    "c4-100": dict(name="wide FFN layer, bf16, d=2048 d_ff=16384 T=51, all neurons", cfg=4, percent=100),
+}
+
+
+def _bf16_tensor(bits, device):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(device)
+
+
+def score_mask_on_device(x_ref, wg, wu, k: int):
+    """Top-k neurons by mean |SiLU(x_ref Wg^T) * (x_ref Wu^T)| over tokens, float64 on the GPU (input setup).
+
+    Ties go to the lower neuron index (stable sort)."""
+    import torch
+    import torch.nn.functional as F
+    xr = x_ref.to(torch.float64)
+    h = F.silu(xr @ wg.to(torch.float64).T) * (xr @ wu.to(torch.float64).T)
+    score = h.abs().mean(dim=0)
+    order = torch.sort(score, descending=True, stable=True).indices
+    mask = torch.zeros(score.shape[0], dtype=torch.uint8, device=score.device)
+    mask[order[:k]] = 1
+    return mask
+
+
+class Setup:
+    """Device-resident inputs of a workload, with R rotating weight copies."""
+
+    def __init__(self, key: str, device, cold: bool = True):
+        import torch
+        import workloads as wl
+        import paper_2609_19104_amd as rm
+
+        spec = WORKLOADS[key]
+        w = wl.config2() if spec["cfg"] == 2 else wl.config4(percents=(spec["percent"],))
+        self.key, self.spec, self.wl = key, spec, w
+        layer = w.layers[0]
+        self.d, self.d_ff, self.T, self.B = w.d, w.d_ff, w.T, w.B
+        self.k = wl.count_for_percent(spec["percent"], w.d_ff)
+        self.layer_np = layer
+        base = (_bf16_tensor(layer.w_gate, device), _bf16_tensor(layer.w_up, device),
+                _bf16_tensor(layer.w_down, device), None)
+        self.x = torch.from_numpy(w.x.reshape(self.B, self.T, self.d)).to(device)
+        self.x_ref = torch.from_numpy(w.x_ref.reshape(self.B * self.T, self.d)).to(device)
+        self.mask = score_mask_on_device(self.x_ref, base[0], base[1], self.k).reshape(1, self.d_ff)
+        dense_bytes = 3 * matrix_bytes(self.d, self.d_ff, 2)
+        self.copies = max(2, math.ceil(COLD_BYTES / dense_bytes)) if cold else 1
+        self.layers = [base] + [tuple(t.clone() if t is not None else None for t in base)
+                                for _ in range(self.copies - 1)]
+        self.rotate = self.copies  # copies cycled through by step(); 1 = warm (same weights every step)
+        self.y = torch.empty_like(self.x)
+        self.idx = torch.empty((1, self.d_ff), dtype=torch.int32, device=device)
+        self.cnt = torch.empty((1,), dtype=torch.int32, device=device)
+        self.ws = rm.workspace(self.d, self.d_ff, rm.RM_BF16, self.B, self.T, self.k, device=device)
+        self.rm = rm
+
+    def step(self, i: int) -> None:
+        self.rm.rm_mask_compact(self.mask, self.idx, self.cnt)
+        self.rm.rm_sparse_ffn_layer(self.x, self.y, self.layers[i % self.rotate], self.idx, self.cnt, self.k, self.ws)
+
+    @property
+    def active_bytes(self) -> int:
+        return active_weight_bytes(self.k, self.d, 2)
+
+
+def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
+    """Time `steps` steps after `warmup` untimed ones.  With hook=True, also record HIP events around every
+    gate/up and down launch (on the launch stream) and return their average durations in microseconds."""
+    import torch
+    rm = setup.rm
+    for i in range(warmup):
+        setup.step(i)
+    torch.cuda.synchronize()
+    evs = None
+    if hook:
+        evs = {kk: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for _ in range(steps)] for kk in (rm.RM_KERNEL_GATEUP, rm.RM_KERNEL_DOWN)}
+        for pairs in evs.values():  # create the underlying events before handing them to the library
+            for a, b in pairs:
+                a.record()
+                b.record()
+        torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        if hook:
+            for kk, pairs in evs.items():
+                rm.rm_profile_kernel_events(kk, pairs[i][0].cuda_event, pairs[i][1].cuda_event)
+        setup.step(warmup + i)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    kern = None
+    if hook:
+        kern = {kk: float(np.mean([a.elapsed_time(b) for a, b in pairs])) * 1e3 for kk, pairs in evs.items()}
+    return ms, kern
+
+
+def cpu_baseline(setup: Setup, seconds: float):
+    """The float64 oracle on the same layer, mask and input, repeated for about `seconds` of CPU time."""
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    except Exception:  # threadpoolctl missing: report the affinity size NumPy's BLAS defaults to
+        threads = len(os.sched_getaffinity(0))
+    wg, wu, wd, g = setup.layer_np.f64()
+    mult = setup.mask.cpu().numpy()[0].astype(np.float64)
+    x = setup.x.cpu().numpy()[0]
+    oracle.masked_ffn(x, wg, wu, wd, mult, g)  # warm
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.masked_ffn(x, wg, wu, wd, mult, g)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds and reps >= 3:
+            break
+    per = el / reps
+    return {"value": round(setup.active_bytes / per / 1e9, 4), "unit": "GB/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{reps} float64 oracle evaluations of the same layer (dense SwiGLU over all {setup.d_ff} "
+                      f"neurons, inactive ones zeroed) on the same input and mask, {el:.1f} s; "
+                      f"{per * 1e3:.2f} ms per layer; value = active weight bytes / oracle time"}
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="run warmup + steps with no event hooks and no CPU leg (for rocprofv3)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(the hot path shards by sample with no communication; see the design notes).", file=sys.stderr)
+        return 2
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    setup = Setup(args.workload, dev, cold=True)
+
+    if args.profile_only:
+        time_steps(setup, args.steps, args.warmup)
+        print(json.dumps({"profile_only": True, "workload": args.workload, "steps": args.steps}))
+        return 0
+
+    ms, _ = time_steps(setup, args.steps, args.warmup)
+    _, kern = time_steps(setup, args.steps, 5, hook=True)
+    gu_us, dn_us = kern[setup.rm.RM_KERNEL_GATEUP], kern[setup.rm.RM_KERNEL_DOWN]
+    gu_bytes = gateup_bytes(setup.k, setup.d, 2)
+    dn_bytes = down_bytes(setup.k, setup.d, 2)
+    if gu_us >= dn_us:
+        dom, dom_bytes, dom_us = "gateup_bf16_kernel", gu_bytes, gu_us
+    else:
+        dom, dom_bytes, dom_us = "down_bf16_kernel", dn_bytes, dn_us
+    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
+    value = setup.active_bytes / (ms * 1e-3) / 1e9
+
+    setup.rotate = 1
+    warm_ms, _ = time_steps(setup, args.steps, args.warmup)
+    setup.rotate = setup.copies
+
+    out = {
+        "metric": "µs per sparse FFN layer + achieved HBM GB/s (% of peak) on active weights",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": setup.spec["name"], "d": setup.d, "d_ff": setup.d_ff, "T": setup.T, "B": setup.B,
+                   "active_neurons": setup.k, "layers": 1,
+                   "step": "rm_mask_compact + rm_sparse_ffn_layer",
+                   "weights": f"cold: {setup.copies} rotating copies ({setup.copies * 3 * setup.d * setup.d_ff * 2 / 2**30:.2f} GiB)"},
+        "us_per_layer": round(ms * 1e3, 3),
+        "pct_of_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "tokens_per_s": round(setup.B * setup.T / (ms * 1e-3), 1),
+        "active_weight_bytes": setup.active_bytes,
+        "warm_us_per_layer": round(warm_ms * 1e3, 3),
+        "kernel_us": {"gateup_bf16_kernel": round(gu_us, 3), "down_bf16_kernel": round(dn_us, 3)},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_us, 3)},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(setup, args.cpu_seconds)
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -6,11 +6,10 @@
 // gate/up (gateup_f32_kernel): one wave per 8 listed neurons; 8 lanes per neuron row, each lane reading
 //   16 contiguous bytes (128 contiguous bytes per row per step).  8 tokens per register block; the 8 lanes'
 //   partial dot products are combined with a fixed xor butterfly, then lane j forms h for token j.
-// down + residual (down_f32_kernel): one wave per (256-column tile, K-slice of listed neurons, sample); a lane
-//   owns 4 columns, loops over its slice's neurons (one 1 KB coalesced row segment per neuron and wave) and
-//   keeps 8 tokens x 4 columns of float32 sums.  The slice's partial is finished by the ticket scheme of
-//   rm_finish.h (fixed-order sum over slices, + x, no float atomics).
-#include "rm_finish.h"
+// down (down_f32_kernel): one wave per (256-column tile, K-slice of listed neurons, sample); a lane owns
+//   4 columns, loops over its slice's neurons (one 1 KB coalesced row segment per neuron and wave) and keeps
+//   8 tokens x 4 columns of float32 sums.  The slice's float32 partial is stored; the epilogue kernel adds the
+//   slices in order to the residual (no float atomics).
 #include "rm_internal.h"
 
 namespace {
@@ -92,15 +91,13 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
 __global__ __launch_bounds__(kWave) void down_f32_kernel(
     const float *__restrict__ H, const float *__restrict__ wd, const int32_t *__restrict__ idx,
     const int32_t *__restrict__ count, int max_count, int d_ff, int d, int T, int tpad, int kcap, int slices,
-    int slice_neurons, const float *x, float *y, float *__restrict__ part, int *__restrict__ tickets) {
+    int slice_neurons, float *__restrict__ part) {
     const int ct = blockIdx.x;
     const int s = blockIdx.y;
     const int b = blockIdx.z;
-    const int ncol = gridDim.x;
     const int lane = threadIdx.x;
     int cnt = idx ? count[b] : d_ff;
     cnt = cnt < 0 ? 0 : (cnt > max_count ? max_count : cnt);
-    const int used_slices = (cnt + slice_neurons - 1) / slice_neurons;
     const int k_begin = s * slice_neurons;
     const int k_end = min(k_begin + slice_neurons, cnt);
     const int col0 = ct * rm::kF32ColTile;
@@ -108,8 +105,7 @@ __global__ __launch_bounds__(kWave) void down_f32_kernel(
     const bool colok = c < d;
     const float *Hb = H + static_cast<size_t>(b) * tpad * kcap;
     const int32_t *idxb = idx ? idx + static_cast<size_t>(b) * d_ff : nullptr;
-    float *part_tile = part + (static_cast<size_t>(b) * ncol + ct) * slices * static_cast<size_t>(T) * rm::kF32ColTile;
-    float *P = part_tile + static_cast<size_t>(s) * T * rm::kF32ColTile;
+    float *P = part + (static_cast<size_t>(b) * slices + s) * static_cast<size_t>(T) * d;
 
     if (k_begin < k_end) {
         for (int t0 = 0; t0 < T; t0 += rm::kF32TokBlock) {
@@ -134,16 +130,10 @@ __global__ __launch_bounds__(kWave) void down_f32_kernel(
 #pragma unroll
                 for (int t = 0; t < rm::kF32TokBlock; ++t)
                     if (t < nt)
-                        *reinterpret_cast<float4 *>(P + static_cast<size_t>(t0 + t) * rm::kF32ColTile + lane * 4) =
-                            acc[t];
+                        *reinterpret_cast<float4 *>(P + static_cast<size_t>(t0 + t) * d + c) = acc[t];
             }
         }
     }
-
-    rm_finish_column_tile<rm::kF32ColTile>(part_tile, slices, used_slices,
-                                           tickets + static_cast<size_t>(b) * ncol + ct,
-                                           x + static_cast<size_t>(b) * T * d, y + static_cast<size_t>(b) * T * d,
-                                           T, d, col0);
 }
 
 }  // namespace
@@ -164,16 +154,15 @@ hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up
     return e;
 }
 
-hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
-                           const float *x, float *y, void *ws, hipStream_t st) {
+hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
+                           hipStream_t st) {
     char *base = static_cast<char *>(ws);
     const float *H = reinterpret_cast<const float *>(base + p.off_h);
     float *part = reinterpret_cast<float *>(base + p.off_part);
-    int *tickets = reinterpret_cast<int *>(base + p.off_ticket);
     profile_before(RM_KERNEL_DOWN, st);
     hipLaunchKernelGGL(down_f32_kernel, dim3(p.ncol, p.slices, p.B), dim3(kWave), 0, st, H,
                        static_cast<const float *>(w_down), idx, count, p.max_count, p.d_ff, p.d, p.T, p.tpad,
-                       p.kcap, p.slices, p.slice_units, x, y, part, tickets);
+                       p.kcap, p.slices, p.slice_units, part);
     hipError_t e = hipGetLastError();
     profile_after(RM_KERNEL_DOWN, st);
     return e;

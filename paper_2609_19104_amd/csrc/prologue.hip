@@ -2,8 +2,8 @@
 //
 // The action expert normalizes the FFN input (paper section 4.1 names the FFN input after normalization; the
 // layer is x + FFN(RMSNorm(x))).  One workgroup per token row; the row's sum of squares is reduced in a fixed
-// order (lane butterfly, then waves 0..3), so the scale is deterministic.  The same launch clears the
-// per-column-tile tickets that the down projection counts with.
+// order (lane butterfly, then waves 0..3), so the scale is deterministic.  Inside a stack the next layer's
+// input is produced by the previous layer's epilogue instead.
 #include "rm_internal.h"
 
 namespace {
@@ -13,11 +13,9 @@ constexpr int kThreads = 256;
 template <bool kBf16Out>
 __global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restrict__ x,
                                                             const float *__restrict__ g, float eps, int d,
-                                                            void *__restrict__ xn, int *__restrict__ tickets,
-                                                            int ntickets) {
+                                                            void *__restrict__ xn) {
     const int row = blockIdx.x;
     const int tid = threadIdx.x;
-    for (int i = row * kThreads + tid; i < ntickets; i += gridDim.x * kThreads) tickets[i] = 0;
 
     const float *xr = x + static_cast<size_t>(row) * d;
     float scale = 1.0f;
@@ -65,15 +63,11 @@ namespace rm {
 hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, void *ws, hipStream_t st) {
     char *base = static_cast<char *>(ws);
     void *xn = base + p.off_xn;
-    int *tickets = reinterpret_cast<int *>(base + p.off_ticket);
     const int rows = p.B * p.T;
-    const int ntickets = p.B * p.ncol;
     if (p.wdtype == RM_BF16)
-        hipLaunchKernelGGL(prologue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.eps, p.d, xn,
-                           tickets, ntickets);
+        hipLaunchKernelGGL(prologue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.eps, p.d, xn);
     else
-        hipLaunchKernelGGL(prologue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.eps, p.d, xn,
-                           tickets, ntickets);
+        hipLaunchKernelGGL(prologue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.eps, p.d, xn);
     return hipGetLastError();
 }
 

@@ -1,9 +1,9 @@
 // C ABI entry points: argument validation, launch plan / workspace layout, and the layer and stack drivers.
 //
-// Per layer the driver enqueues three kernels on the caller's stream: the prologue (FFN input, optional
-// RMSNorm, ticket clear), the gathered gate/up projection (H), and the gathered down projection with the
-// residual.  A stack repeats them per layer in place on y, reading the next layer's list and weights.  Nothing
-// here synchronizes or allocates.
+// A call enqueues on the caller's stream: the prologue (FFN input of the first layer, optional RMSNorm), then
+// per layer the gathered gate/up projection (H), the gathered down projection (per-K-slice partials) and the
+// epilogue (y = x + partials in slice order, plus the next layer's normalized input inside a stack).  Layers
+// after the first run in place on y.  Nothing here synchronizes or allocates.
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -98,16 +98,24 @@ rm_status hip_fail(hipError_t e, const char *what) {
     return fail(RM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-rm_status run_layer(const rm::Plan &p, const rm_ffn_layer_weights *w, const float *x, float *y, const int32_t *idx,
-                    const int32_t *count, void *ws, hipStream_t st) {
-    hipError_t e = rm::launch_prologue(p, x, w->norm_g, ws, st);
+// Layers 0..L-1 of one call; w[l] are the layers' weights, lists at idx + l * list_stride.
+rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, const float *x, float *y,
+                     const int32_t *idx, const int32_t *count, size_t list_stride, void *ws, hipStream_t st) {
+    hipError_t e = rm::launch_prologue(p, x, w[0].norm_g, ws, st);
     if (e != hipSuccess) return hip_fail(e, "prologue launch");
-    e = (p.wdtype == RM_BF16) ? rm::launch_gateup_bf16(p, w->w_gate, w->w_up, idx, count, ws, st)
-                              : rm::launch_gateup_f32(p, w->w_gate, w->w_up, idx, count, ws, st);
-    if (e != hipSuccess) return hip_fail(e, "gate/up launch");
-    e = (p.wdtype == RM_BF16) ? rm::launch_down_bf16(p, w->w_down, idx, count, x, y, ws, st)
-                              : rm::launch_down_f32(p, w->w_down, idx, count, x, y, ws, st);
-    if (e != hipSuccess) return hip_fail(e, "down launch");
+    for (int l = 0; l < L; ++l) {
+        const int32_t *il = idx ? idx + l * list_stride : nullptr;
+        const int32_t *cl = count ? count + static_cast<size_t>(l) * p.B : nullptr;
+        const bool bf = p.wdtype == RM_BF16;
+        e = bf ? rm::launch_gateup_bf16(p, w[l].w_gate, w[l].w_up, il, cl, ws, st)
+               : rm::launch_gateup_f32(p, w[l].w_gate, w[l].w_up, il, cl, ws, st);
+        if (e != hipSuccess) return hip_fail(e, "gate/up launch");
+        e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, cl, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
+        if (e != hipSuccess) return hip_fail(e, "down launch");
+        const bool next = l + 1 < L;
+        e = rm::launch_epilogue(p, cl, l == 0 ? x : y, y, next ? w[l + 1].norm_g : nullptr, next, ws, st);
+        if (e != hipSuccess) return hip_fail(e, "epilogue launch");
+    }
     return RM_OK;
 }
 
@@ -126,8 +134,8 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.eps = s->norm_eps;
     const int kmax = max_count > 0 ? max_count : 1;
     size_t xn_elem, h_elem;
-    // Aim for about two workgroups per compute unit (256 CUs) in the down projection.
-    constexpr int kTargetDownGroups = 512;
+    // Aim for about four down-projection workgroups per compute unit (256 CUs).
+    constexpr int kTargetDownGroups = 1024;
     if (s->wdtype == RM_BF16) {
         q.tpad = ceil_div(T, kBfTokBlock) * kBfTokBlock;
         q.kcap = ceil_div(kmax, kBfChunk) * kBfChunk;
@@ -140,6 +148,7 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         cps = std::max(kBfWaves, ceil_div(cps, kBfWaves) * kBfWaves);
         q.slice_units = cps;
         q.slices = ceil_div(nchunks, cps);
+        q.slice_neurons = cps * kBfChunk;
         xn_elem = 2;
         h_elem = 2;
     } else {
@@ -152,20 +161,18 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         const int su = static_cast<int>(std::max<long long>(kF32SliceNeur, (work + kTargetDownGroups - 1) / kTargetDownGroups));
         q.slice_units = su;
         q.slices = ceil_div(kmax, su);
+        q.slice_neurons = su;
         xn_elem = 4;
         h_elem = 4;
     }
-    if (q.gate_blocks > 0x7fffffff || q.slices > 65535)
-        return fail(RM_ERR_SHAPE, "launch grid too large");
+    if (q.slices > 65535) return fail(RM_ERR_SHAPE, "launch grid too large");
     size_t off = 0;
     q.off_xn = off;
     off = align_up(off + static_cast<size_t>(B) * T * s->d * xn_elem, 256);
     q.off_h = off;
     off = align_up(off + static_cast<size_t>(B) * q.tpad * q.kcap * h_elem, 256);
     q.off_part = off;
-    off = align_up(off + static_cast<size_t>(B) * q.ncol * q.slices * static_cast<size_t>(T) * q.col_tile * 4, 256);
-    q.off_ticket = off;
-    off = align_up(off + static_cast<size_t>(B) * q.ncol * sizeof(int), 256);
+    off = align_up(off + static_cast<size_t>(B) * q.slices * static_cast<size_t>(T) * s->d * 4, 256);
     q.total = off;
     *p = q;
     return RM_OK;
@@ -222,7 +229,7 @@ RM_EXPORT rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_laye
     if (st != RM_OK) return st;
     st = check_layer(w, 0);
     if (st != RM_OK) return st;
-    st = run_layer(p, w, x, y, idx, count, ws, static_cast<hipStream_t>(stream));
+    st = run_layers(p, w, 1, x, y, idx, count, 0, ws, static_cast<hipStream_t>(stream));
     return st == RM_OK ? ok() : st;
 }
 
@@ -239,13 +246,8 @@ RM_EXPORT rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
         st = check_layer(&w[l], l);
         if (st != RM_OK) return st;
     }
-    const hipStream_t hs = static_cast<hipStream_t>(stream);
-    const size_t list_stride = static_cast<size_t>(B) * s->d_ff;
-    for (int l = 0; l < L; ++l) {
-        st = run_layer(p, &w[l], l == 0 ? x : y, y, idx + l * list_stride, count + static_cast<size_t>(l) * B, ws, hs);
-        if (st != RM_OK) return st;
-    }
-    return ok();
+    st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, ws, static_cast<hipStream_t>(stream));
+    return st == RM_OK ? ok() : st;
 }
 
 RM_EXPORT rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
@@ -255,7 +257,7 @@ RM_EXPORT rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_w
     if (st != RM_OK) return st;
     st = check_layer(w, 0);
     if (st != RM_OK) return st;
-    st = run_layer(p, w, x, y, nullptr, nullptr, ws, static_cast<hipStream_t>(stream));
+    st = run_layers(p, w, 1, x, y, nullptr, nullptr, 0, ws, static_cast<hipStream_t>(stream));
     return st == RM_OK ? ok() : st;
 }
 

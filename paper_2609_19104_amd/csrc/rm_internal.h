@@ -18,7 +18,7 @@ namespace rm {
 constexpr int kBfTokBlock = 64;     // tokens per accumulator block (4 tiles of 16)
 constexpr int kBfNeurPerBlk = 8;    // neurons per gate/up workgroup (8 gate rows + 8 up rows = one 16-row tile)
 constexpr int kBfChunk = 32;        // neurons per down-projection matrix-core step (K of the 16x16x32 tile)
-constexpr int kBfColTile = 128;     // output columns per down workgroup (16 lanes x 8 columns)
+constexpr int kBfColTile = 64;      // output columns per down workgroup (16 lanes x 4 columns)
 constexpr int kBfWaves = 4;
 
 // f32 path: vector ALU.
@@ -35,9 +35,11 @@ struct Plan {
     int gate_blocks = 0;// gate/up workgroups per sample
     int col_tile = 0;   // output columns per down workgroup
     int ncol = 0;       // column tiles
-    int slices = 0;     // K-slices per column tile (down partial sums)
+    int slices = 0;     // K-slices (down projection partial sums, added by the epilogue)
     int slice_units = 0;// bf16: 32-neuron chunks per slice; f32: neurons per slice
-    size_t off_xn = 0, off_h = 0, off_part = 0, off_ticket = 0, total = 0;
+    int slice_neurons = 0; // listed neurons per slice
+    // Workspace: xn [B][T][d] (bf16 or f32), H [B][tpad][kcap] (bf16 or f32), partials f32 [B][slices][T][d].
+    size_t off_xn = 0, off_h = 0, off_part = 0, total = 0;
 };
 
 rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p);
@@ -49,7 +51,7 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
 hipError_t launch_mask_compact(const uint8_t *mask, int n_masks, int d_ff, int32_t *idx, int32_t *count,
                                hipStream_t st);
 
-// x -> xn (optional RMSNorm, cast to the path's input dtype); also clears the down-projection tickets.
+// x -> xn (optional RMSNorm, cast to the path's input dtype).
 hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, void *ws, hipStream_t st);
 
 // Gate/up projection of the listed neurons + SiLU * up -> H in the workspace (one launcher per weight dtype).
@@ -58,11 +60,16 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
 hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
                              const int32_t *count, void *ws, hipStream_t st);
 
-// Down projection of the listed neurons + residual: y = x + H W_down[idx].
-hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
-                            const float *x, float *y, void *ws, hipStream_t st);
-hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
-                           const float *x, float *y, void *ws, hipStream_t st);
+// Down projection of the listed neurons: per-K-slice float32 partials of H W_down[idx] in the workspace.
+hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
+                            hipStream_t st);
+hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
+                           hipStream_t st);
+
+// y = x + the slices' partials in slice order; if emit_xn, also the next layer's xn (RMSNorm with g_next when
+// g_next is not null).
+hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, float *y, const float *g_next,
+                           bool emit_xn, void *ws, hipStream_t st);
 
 // Profiling hook (thread-local events armed by rm_profile_kernel_events).
 void profile_before(int kernel, hipStream_t st);

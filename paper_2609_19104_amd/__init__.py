@@ -19,7 +19,8 @@ from typing import Optional, Sequence, Tuple
 import torch
 
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG_DIR, "librmuscle.so")
+# The in-tree build; RMUSCLE_LIB may name another build of the same library (e.g. for A/B timing).
+LIB_PATH = os.environ.get("RMUSCLE_LIB") or os.path.join(PKG_DIR, "librmuscle.so")
 
 RM_OK = 0
 RM_ERR_INVALID_ARG = -1

@@ -1,11 +1,13 @@
 // Layer epilogue: y = x + sum over K-slices of the down projection's partials, then (inside a stack) the next
-// layer's FFN input xn = RMSNorm(y) * g in the FFN kernels' input dtype.
+// layer's FFN input xn = y * g in the FFN kernels' input dtype and the row's sum of squares, from which the
+// next gate/up kernel forms the RMSNorm factor 1 / sqrt(mean(y^2) + eps).
 //
 // One workgroup per token row.  Each thread owns float4 groups of the row; the slices are added in slice order
-// 0, 1, 2, ... (loads issued four at a time, additions in order), so the result is bitwise reproducible.
+// 0, 1, 2, ... (loads issued sixteen at a time, additions in order), so the result is bitwise reproducible.
 // Slices past the end of a sample's list were not written by the down projection and are skipped; with no
-// listed neuron at all y = x exactly.  The row's sum of squares for the next RMSNorm is reduced in a fixed
-// order (lane butterfly, then the four waves in order).
+// listed neuron at all y = x exactly.  The row's sum of squares is reduced in a fixed order (lane butterfly,
+// then the four waves in order).  A separate launch, rather than the last K-slice workgroup of each column
+// tile, does this: a device-wide release from every such workgroup costs more than one kernel boundary.
 #include "rm_internal.h"
 
 namespace {
@@ -23,15 +25,14 @@ __device__ __forceinline__ float4 reduce_column(const float *P, size_t stride, i
     const float4 xv = ld4(xr + c);
     if (used == 0) return xv;
     float4 acc = ld4(P + c);
-    int s = 1;
-    for (; s + 4 <= used; s += 4) {
-        const float4 v1 = ld4(P + s * stride + c);
-        const float4 v2 = ld4(P + (s + 1) * stride + c);
-        const float4 v3 = ld4(P + (s + 2) * stride + c);
-        const float4 v4 = ld4(P + (s + 3) * stride + c);
-        acc = add4(add4(add4(add4(acc, v1), v2), v3), v4);
+    for (int s = 1; s < used; s += 16) {
+        float4 v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = (s + i < used) ? ld4(P + (s + i) * stride + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            if (s + i < used) acc = add4(acc, v[i]);
     }
-    for (; s < used; ++s) acc = add4(acc, ld4(P + s * stride + c));
     return add4(xv, acc);
 }
 
@@ -52,7 +53,8 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
                                                             int slice_neurons, const int32_t *__restrict__ count,
                                                             int max_count, int dense_count, const float *x,
                                                             float *y, int T, int d, void *__restrict__ xn_next,
-                                                            const float *__restrict__ g_next, float eps) {
+                                                            const float *__restrict__ g_next,
+                                                            float *__restrict__ ssq) {
     const int row = blockIdx.x;
     const int b = row / T;
     const int t = row - b * T;
@@ -93,14 +95,12 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
     }
     if (xn_next == nullptr) return;
 
-    float scale = 1.0f;
     if (g_next != nullptr) {
         for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
         __shared__ float wave_ss[kThreads / 64];
         if ((tid & 63) == 0) wave_ss[tid >> 6] = ss;
         __syncthreads();
-        const float total = (wave_ss[0] + wave_ss[1]) + (wave_ss[2] + wave_ss[3]);
-        scale = 1.0f / sqrtf(total / static_cast<float>(d) + eps);
+        if (tid == 0) ssq[row] = (wave_ss[0] + wave_ss[1]) + (wave_ss[2] + wave_ss[3]);
     }
     const size_t ro = static_cast<size_t>(row) * d;
 #pragma unroll
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
             float4 v = keep[k];
             if (g_next != nullptr) {
                 const float4 g = ld4(g_next + c);
-                v = make_float4(v.x * scale * g.x, v.y * scale * g.y, v.z * scale * g.z, v.w * scale * g.w);
+                v = make_float4(v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w);
             }
             store_xn<kBf16Xn>(xn_next, ro + c, v);
         }
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
         float4 v = ld4(yr + c);
         if (g_next != nullptr) {
             const float4 g = ld4(g_next + c);
-            v = make_float4(v.x * scale * g.x, v.y * scale * g.y, v.z * scale * g.z, v.w * scale * g.w);
+            v = make_float4(v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w);
         }
         store_xn<kBf16Xn>(xn_next, ro + c, v);
     }
@@ -134,13 +134,16 @@ hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, 
     char *base = static_cast<char *>(ws);
     const float *part = reinterpret_cast<const float *>(base + p.off_part);
     void *xn = emit_xn ? static_cast<void *>(base + p.off_xn) : nullptr;
+    float *ssq = reinterpret_cast<float *>(base + p.off_ssq);
     const int rows = p.B * p.T;
+    const int slice_neurons = p.wdtype == RM_BF16 ? p.slice_units * kBfChunk : p.slice_units;
+    const float *g = emit_xn ? g_next : nullptr;
     if (p.wdtype == RM_BF16)
-        hipLaunchKernelGGL(epilogue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, part, p.slices, p.slice_neurons,
-                           count, p.max_count, p.d_ff, x, y, p.T, p.d, xn, g_next, p.eps);
+        hipLaunchKernelGGL(epilogue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, part, p.slices, slice_neurons,
+                           count, p.max_count, p.d_ff, x, y, p.T, p.d, xn, g, ssq);
     else
-        hipLaunchKernelGGL(epilogue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, part, p.slices,
-                           p.slice_neurons, count, p.max_count, p.d_ff, x, y, p.T, p.d, xn, g_next, p.eps);
+        hipLaunchKernelGGL(epilogue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, part, p.slices, slice_neurons,
+                           count, p.max_count, p.d_ff, x, y, p.T, p.d, xn, g, ssq);
     return hipGetLastError();
 }
 

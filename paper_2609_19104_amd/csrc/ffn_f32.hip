@@ -8,8 +8,9 @@
 //   partial dot products are combined with a fixed xor butterfly, then lane j forms h for token j.
 // down (down_f32_kernel): one wave per (256-column tile, K-slice of listed neurons, sample); a lane owns
 //   4 columns, loops over its slice's neurons (one 1 KB coalesced row segment per neuron and wave) and keeps
-//   8 tokens x 4 columns of float32 sums.  The slice's float32 partial is stored; the epilogue kernel adds the
-//   slices in order to the residual (no float atomics).
+//   8 tokens x 4 columns of float32 sums.  The slice's float32 partial is stored; the epilogue kernel adds
+//   the slices in order to the residual (no float atomics).
+// The FFN input xn is x * g; the per-token RMSNorm factor multiplies the gate and up sums (see ffn_bf16.hip).
 #include "rm_internal.h"
 
 namespace {
@@ -21,7 +22,7 @@ __device__ __forceinline__ int clamp_neuron(int n, int d_ff) { return n < 0 ? 0 
 __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
     const float *__restrict__ wg, const float *__restrict__ wu, const float *__restrict__ xn,
     const int32_t *__restrict__ idx, const int32_t *__restrict__ count, int max_count, int d_ff, int d, int T,
-    int tpad, float *__restrict__ H, int kcap) {
+    int tpad, float *__restrict__ H, int kcap, const float *__restrict__ ssq, float eps) {
     const int b = blockIdx.y;
     const int slot0 = blockIdx.x * rm::kF32NeurPerBlk;
     const int lane = threadIdx.x;
@@ -83,7 +84,14 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
             }
         }
         if (t0 + cl < tpad && valid) {
-            Hb[static_cast<size_t>(t0 + cl) * kcap + slot] = (cl < nt) ? rm_silu(gs) * us : 0.0f;
+            float h = 0.0f;
+            if (cl < nt) {
+                float rn = 1.0f;
+                if (ssq != nullptr)
+                    rn = 1.0f / sqrtf(ssq[static_cast<size_t>(b) * T + t0 + cl] / static_cast<float>(d) + eps);
+                h = rm_silu(gs * rn) * (us * rn);
+            }
+            Hb[static_cast<size_t>(t0 + cl) * kcap + slot] = h;
         }
     }
 }
@@ -134,6 +142,7 @@ __global__ __launch_bounds__(kWave) void down_f32_kernel(
             }
         }
     }
+
 }
 
 }  // namespace
@@ -141,14 +150,15 @@ __global__ __launch_bounds__(kWave) void down_f32_kernel(
 namespace rm {
 
 hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
-                             const int32_t *count, void *ws, hipStream_t st) {
+                             const int32_t *count, bool norm, void *ws, hipStream_t st) {
     char *base = static_cast<char *>(ws);
     const float *xn = reinterpret_cast<const float *>(base + p.off_xn);
     float *H = reinterpret_cast<float *>(base + p.off_h);
+    const float *ssq = norm ? reinterpret_cast<const float *>(base + p.off_ssq) : nullptr;
     profile_before(RM_KERNEL_GATEUP, st);
     hipLaunchKernelGGL(gateup_f32_kernel, dim3(p.gate_blocks, p.B), dim3(kWave), 0, st,
                        static_cast<const float *>(w_gate), static_cast<const float *>(w_up), xn, idx, count,
-                       p.max_count, p.d_ff, p.d, p.T, p.tpad, H, p.kcap);
+                       p.max_count, p.d_ff, p.d, p.T, p.tpad, H, p.kcap, ssq, p.eps);
     hipError_t e = hipGetLastError();
     profile_after(RM_KERNEL_GATEUP, st);
     return e;

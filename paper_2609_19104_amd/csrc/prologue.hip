@@ -1,9 +1,10 @@
-// FFN input preparation: xn = x (or RMSNorm(x) * g) in the input dtype of the FFN kernels.
+// First layer's FFN input: xn = x * g (or x without a norm) in the FFN kernels' input dtype, plus the row's
+// sum of squares for the RMSNorm factor.
 //
-// The action expert normalizes the FFN input (paper section 4.1 names the FFN input after normalization; the
-// layer is x + FFN(RMSNorm(x))).  One workgroup per token row; the row's sum of squares is reduced in a fixed
-// order (lane butterfly, then waves 0..3), so the scale is deterministic.  Inside a stack the next layer's
-// input is produced by the previous layer's epilogue instead.
+// The action expert normalizes each FFN input (the layer is x + FFN(RMSNorm(x)) with RMSNorm(x) =
+// x / sqrt(mean(x^2) + eps) * g).  The per-token factor is applied by the gate/up kernel after its matrix-core
+// products, so xn itself stays unscaled; the row's sum of squares is reduced here in a fixed order (lane
+// butterfly, then waves 0..3).  One workgroup per token row.
 #include "rm_internal.h"
 
 namespace {
@@ -12,37 +13,25 @@ constexpr int kThreads = 256;
 
 template <bool kBf16Out>
 __global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restrict__ x,
-                                                            const float *__restrict__ g, float eps, int d,
-                                                            void *__restrict__ xn) {
+                                                            const float *__restrict__ g, int d,
+                                                            void *__restrict__ xn, float *__restrict__ ssq) {
     const int row = blockIdx.x;
     const int tid = threadIdx.x;
 
     const float *xr = x + static_cast<size_t>(row) * d;
-    float scale = 1.0f;
-    if (g != nullptr) {
-        float ss = 0.0f;
-        for (int c = tid * 4; c < d; c += kThreads * 4) {
-            const float4 v = *reinterpret_cast<const float4 *>(xr + c);
+    float ss = 0.0f;
+    for (int c = tid * 4; c < d; c += kThreads * 4) {
+        float4 v = *reinterpret_cast<const float4 *>(xr + c);
+        if (g != nullptr) {
             ss = fmaf(v.x, v.x, ss);
             ss = fmaf(v.y, v.y, ss);
             ss = fmaf(v.z, v.z, ss);
             ss = fmaf(v.w, v.w, ss);
-        }
-        for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-        __shared__ float wave_ss[kThreads / 64];
-        if ((tid & 63) == 0) wave_ss[tid >> 6] = ss;
-        __syncthreads();
-        const float total = (wave_ss[0] + wave_ss[1]) + (wave_ss[2] + wave_ss[3]);
-        scale = 1.0f / sqrtf(total / static_cast<float>(d) + eps);
-    }
-    for (int c = tid * 4; c < d; c += kThreads * 4) {
-        float4 v = *reinterpret_cast<const float4 *>(xr + c);
-        if (g != nullptr) {
             const float4 gv = *reinterpret_cast<const float4 *>(g + c);
-            v.x = v.x * scale * gv.x;
-            v.y = v.y * scale * gv.y;
-            v.z = v.z * scale * gv.z;
-            v.w = v.w * scale * gv.w;
+            v.x *= gv.x;
+            v.y *= gv.y;
+            v.z *= gv.z;
+            v.w *= gv.w;
         }
         const size_t o = static_cast<size_t>(row) * d + c;
         if constexpr (kBf16Out) {
@@ -54,6 +43,12 @@ __global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restr
             *reinterpret_cast<float4 *>(static_cast<float *>(xn) + o) = v;
         }
     }
+    if (g == nullptr) return;
+    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+    __shared__ float wave_ss[kThreads / 64];
+    if ((tid & 63) == 0) wave_ss[tid >> 6] = ss;
+    __syncthreads();
+    if (tid == 0) ssq[row] = (wave_ss[0] + wave_ss[1]) + (wave_ss[2] + wave_ss[3]);
 }
 
 }  // namespace
@@ -63,11 +58,12 @@ namespace rm {
 hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, void *ws, hipStream_t st) {
     char *base = static_cast<char *>(ws);
     void *xn = base + p.off_xn;
+    float *ssq = reinterpret_cast<float *>(base + p.off_ssq);
     const int rows = p.B * p.T;
     if (p.wdtype == RM_BF16)
-        hipLaunchKernelGGL(prologue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.eps, p.d, xn);
+        hipLaunchKernelGGL(prologue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.d, xn, ssq);
     else
-        hipLaunchKernelGGL(prologue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.eps, p.d, xn);
+        hipLaunchKernelGGL(prologue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.d, xn, ssq);
     return hipGetLastError();
 }
 

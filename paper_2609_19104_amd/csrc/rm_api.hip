@@ -1,8 +1,8 @@
 // C ABI entry points: argument validation, launch plan / workspace layout, and the layer and stack drivers.
 //
-// A call enqueues on the caller's stream: the prologue (FFN input of the first layer, optional RMSNorm), then
-// per layer the gathered gate/up projection (H), the gathered down projection (per-K-slice partials) and the
-// epilogue (y = x + partials in slice order, plus the next layer's normalized input inside a stack).  Layers
+// A call enqueues on the caller's stream: the prologue (the first layer's FFN input and its sums of squares),
+// then per layer the gathered gate/up projection (H), the gathered down projection (per-K-slice partials) and
+// the epilogue (y = x + the partials in slice order, plus the next layer's FFN input inside a stack).  Layers
 // after the first run in place on y.  Nothing here synchronizes or allocates.
 #include <stdarg.h>
 #include <stdio.h>
@@ -107,13 +107,16 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
         const int32_t *il = idx ? idx + l * list_stride : nullptr;
         const int32_t *cl = count ? count + static_cast<size_t>(l) * p.B : nullptr;
         const bool bf = p.wdtype == RM_BF16;
-        e = bf ? rm::launch_gateup_bf16(p, w[l].w_gate, w[l].w_up, il, cl, ws, st)
-               : rm::launch_gateup_f32(p, w[l].w_gate, w[l].w_up, il, cl, ws, st);
+        const bool norm = w[l].norm_g != nullptr;
+        e = bf ? rm::launch_gateup_bf16(p, w[l].w_gate, w[l].w_up, il, cl, norm, ws, st)
+               : rm::launch_gateup_f32(p, w[l].w_gate, w[l].w_up, il, cl, norm, ws, st);
         if (e != hipSuccess) return hip_fail(e, "gate/up launch");
+        const bool next = l + 1 < L;
+        const float *g_next = next ? w[l + 1].norm_g : nullptr;
+        const float *xin = l == 0 ? x : y;
         e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, cl, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
         if (e != hipSuccess) return hip_fail(e, "down launch");
-        const bool next = l + 1 < L;
-        e = rm::launch_epilogue(p, cl, l == 0 ? x : y, y, next ? w[l + 1].norm_g : nullptr, next, ws, st);
+        e = rm::launch_epilogue(p, cl, xin, y, g_next, next, ws, st);
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }
     return RM_OK;
@@ -135,20 +138,29 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     const int kmax = max_count > 0 ? max_count : 1;
     size_t xn_elem, h_elem;
     // Aim for about four down-projection workgroups per compute unit (256 CUs).
-    constexpr int kTargetDownGroups = 1024;
+    constexpr int kCUs = 256;
+    constexpr int kTargetDownGroups = 4 * kCUs;
     if (s->wdtype == RM_BF16) {
         q.tpad = ceil_div(T, kBfTokBlock) * kBfTokBlock;
-        q.kcap = ceil_div(kmax, kBfChunk) * kBfChunk;
-        q.gate_blocks = q.kcap / kBfNeurPerBlk;
+        // Gate/up: the widest workgroup (8 * NG neurons) that still gives every compute unit one workgroup.
+        const int k32 = ceil_div(kmax, kBfChunk) * kBfChunk;
+        q.gate_groups = 1;
+        for (int ng : {8, 4, 2}) {
+            if (static_cast<long long>(B) * ceil_div(k32, 8 * ng) >= kCUs) {
+                q.gate_groups = ng;
+                break;
+            }
+        }
+        q.kcap = ceil_div(k32, std::max(kBfChunk, 8 * q.gate_groups)) * std::max(kBfChunk, 8 * q.gate_groups);
+        q.gate_blocks = q.kcap / (8 * q.gate_groups);
         q.col_tile = kBfColTile;
-        q.ncol = ceil_div(s->d, kBfColTile);
+        q.ncol = ceil_div(s->d, q.col_tile);
         const int nchunks = q.kcap / kBfChunk;
         const int s_target = std::max(1, ceil_div(kTargetDownGroups, q.ncol * B));
         int cps = ceil_div(nchunks, s_target);
         cps = std::max(kBfWaves, ceil_div(cps, kBfWaves) * kBfWaves);
         q.slice_units = cps;
         q.slices = ceil_div(nchunks, cps);
-        q.slice_neurons = cps * kBfChunk;
         xn_elem = 2;
         h_elem = 2;
     } else {
@@ -161,7 +173,6 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         const int su = static_cast<int>(std::max<long long>(kF32SliceNeur, (work + kTargetDownGroups - 1) / kTargetDownGroups));
         q.slice_units = su;
         q.slices = ceil_div(kmax, su);
-        q.slice_neurons = su;
         xn_elem = 4;
         h_elem = 4;
     }
@@ -173,6 +184,8 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     off = align_up(off + static_cast<size_t>(B) * q.tpad * q.kcap * h_elem, 256);
     q.off_part = off;
     off = align_up(off + static_cast<size_t>(B) * q.slices * static_cast<size_t>(T) * s->d * 4, 256);
+    q.off_ssq = off;
+    off = align_up(off + static_cast<size_t>(B) * T * sizeof(float), 256);
     q.total = off;
     *p = q;
     return RM_OK;

@@ -30,16 +30,17 @@ constexpr int kF32SliceNeur = 16;   // neurons per down K-slice
 struct Plan {
     int d = 0, d_ff = 0, wdtype = 0, B = 0, T = 0, max_count = 0;
     float eps = 1e-6f;
-    int tpad = 0;       // T rounded up to the token block (rows of H)
-    int kcap = 0;       // row length of H (neuron slots), max_count rounded up
-    int gate_blocks = 0;// gate/up workgroups per sample
-    int col_tile = 0;   // output columns per down workgroup
-    int ncol = 0;       // column tiles
-    int slices = 0;     // K-slices (down projection partial sums, added by the epilogue)
-    int slice_units = 0;// bf16: 32-neuron chunks per slice; f32: neurons per slice
-    int slice_neurons = 0; // listed neurons per slice
-    // Workspace: xn [B][T][d] (bf16 or f32), H [B][tpad][kcap] (bf16 or f32), partials f32 [B][slices][T][d].
-    size_t off_xn = 0, off_h = 0, off_part = 0, total = 0;
+    int tpad = 0;        // T rounded up to the token block (rows of H)
+    int kcap = 0;        // row length of H (neuron slots), max_count rounded up
+    int gate_groups = 1; // bf16 gate/up: groups of 8 neurons per workgroup (1 = direct, 2/4/8 = LDS-staged)
+    int gate_blocks = 0; // gate/up workgroups per sample
+    int col_tile = 0;    // output columns per down workgroup
+    int ncol = 0;        // column tiles
+    int slices = 0;      // K-slices per column tile (down partial sums)
+    int slice_units = 0; // bf16: 32-neuron chunks per slice; f32: neurons per slice
+    // Workspace: xn [B][T][d] (bf16 or f32), H [B][tpad][kcap] (bf16 or f32), partials f32 [B][slices][T][d],
+    // ssq f32 [B][T] (per-token sums of squares of the FFN input, for the RMSNorm factor).
+    size_t off_xn = 0, off_h = 0, off_part = 0, off_ssq = 0, total = 0;
 };
 
 rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p);
@@ -51,14 +52,16 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
 hipError_t launch_mask_compact(const uint8_t *mask, int n_masks, int d_ff, int32_t *idx, int32_t *count,
                                hipStream_t st);
 
-// x -> xn (optional RMSNorm, cast to the path's input dtype).
+// First layer's FFN input: xn = x * g (or x) in the FFN input dtype, and (norm only) its per-token sums of
+// squares.
 hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, void *ws, hipStream_t st);
 
-// Gate/up projection of the listed neurons + SiLU * up -> H in the workspace (one launcher per weight dtype).
+// Gate/up projection of the listed neurons + SiLU * up -> H in the workspace.  norm: scale by the per-token
+// RMSNorm factor formed from the workspace's sums of squares.
 hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
-                              const int32_t *count, void *ws, hipStream_t st);
+                              const int32_t *count, bool norm, void *ws, hipStream_t st);
 hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
-                             const int32_t *count, void *ws, hipStream_t st);
+                             const int32_t *count, bool norm, void *ws, hipStream_t st);
 
 // Down projection of the listed neurons: per-K-slice float32 partials of H W_down[idx] in the workspace.
 hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
@@ -66,8 +69,8 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
 hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
                            hipStream_t st);
 
-// y = x + the slices' partials in slice order; if emit_xn, also the next layer's xn (RMSNorm with g_next when
-// g_next is not null).
+// y = x + the slices' partials in slice order; if emit_xn, also the next layer's FFN input (y * g_next, or y)
+// and, with g_next, its per-token sums of squares.
 hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, float *y, const float *g_next,
                            bool emit_xn, void *ws, hipStream_t st);
 

@@ -52,10 +52,10 @@ def _size(d, d_ff, wdtype, B, T, k):
 
 
 def test_workspace_size_values(lib):
-    # bf16, d=1024, d_ff=4096, T=51, K=1229: xn 51*1024*2, H 64 tokens x 1248 slots x 2, partials, tickets.
+    # bf16, d=1024, d_ff=4096, T=51, K=1229: at least xn (51 x 1024 bf16) and H (64 tokens x 1248 slots bf16).
     st, n = _size(1024, 4096, rm.RM_BF16, 1, 51, 1229)
     assert st == rm.RM_OK
-    assert n >= 51 * 1024 * 2 + 64 * 1248 * 2 + 8 * 51 * 128 * 4
+    assert n >= 51 * 1024 * 2 + 64 * 1248 * 2
     assert n % 256 == 0
     # Monotone in every size argument.
     assert _size(1024, 4096, rm.RM_BF16, 2, 51, 1229)[1] > n

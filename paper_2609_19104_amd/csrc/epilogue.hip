@@ -28,7 +28,7 @@ __device__ __forceinline__ float4 reduce_column(const float *P, size_t stride, i
     for (int s = 1; s < used; s += 16) {
         float4 v[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) v[i] = (s + i < used) ? ld4(P + (s + i) * stride + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int i = 0; i < 16; ++i) v[i] = ld4(P + min(s + i, used - 1) * stride + c);  // unconditional: no waits
 #pragma unroll
         for (int i = 0; i < 16; ++i)
             if (s + i < used) acc = add4(acc, v[i]);

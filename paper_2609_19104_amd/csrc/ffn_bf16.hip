@@ -2,9 +2,10 @@
 //
 // Eq. 4 of the paper, with a zero anchor: only the listed neurons' rows of W_gate / W_up and their rows of the
 // neuron-major W_down are read from HBM; the weights are gathered in place, row by row, with no compact copy.
-// Each wave issues its HBM weight loads before its first matrix-core instruction; the count and the index
-// list are loaded together, so a wave waits for two memory round trips (index, then weights) before it can
-// compute.
+// Every load is unconditional, from an address clamped into its buffer, and results that must not count are
+// masked where they are consumed: a load under a branch makes the compiler wait for all earlier loads before
+// the branch joins, which would serialize a wave's memory round trips.  A wave therefore issues all of a
+// chunk's loads back to back and waits once.
 //
 // FFN input.  xn holds bf16(x * g) (or bf16(x) without a norm); the per-token RMSNorm factor
 // r_t = 1 / sqrt(mean(x_t^2) + eps) multiplies each gate and up sum after the matrix cores, which is exact in
@@ -14,7 +15,8 @@
 // gate/up, 512 threads = 8 waves, one 16-row A tile per wave = 8 gate rows + 8 up rows of 8 listed neurons,
 // loaded straight from HBM (16 contiguous bytes per lane).  B = xn^T, 16 tokens per tile.
 //   gateup_direct:  1 group of 8 neurons per workgroup; the 8 waves split d; B is read from L2.  Used when the
-//                   list is short, so that there are enough workgroups for the 256 compute units.
+//                   list is short, so that there are enough workgroups for the 256 compute units (and d is
+//                   256, 512, 1024 or 2048).
 //   gateup_staged:  NG groups (16..64 neurons) per workgroup, 8 / NG waves per group splitting d; B is
 //                   staged in LDS in 256-column chunks (double-buffered) and shared by all NG groups, so each
 //                   byte of xn read from L2 serves NG times more neurons.
@@ -36,7 +38,6 @@ constexpr int kGuThreads = 512;
 constexpr int kGuWaves = kGuThreads / 64;
 constexpr int kDnThreads = 256;
 constexpr int kDnWaves = kDnThreads / 64;
-constexpr int kMaxSteps = 8;      // direct gate/up: K steps (of 32) whose weight loads are issued together
 constexpr int kChunkCols = 256;   // staged gate/up: xn columns per LDS chunk (8 K steps)
 constexpr int kChunkSteps = kChunkCols / 32;
 constexpr int kRowPitch = kChunkCols + 8;  // bf16 elements per LDS row (16 bytes of padding against conflicts)
@@ -102,35 +103,22 @@ __device__ __forceinline__ float group_h(const rm_f32x4 (*red)[NT][64], int ds, 
 
 // ------------------------------------------------------------------------------------------ gate / up, direct
 
+// Writes h for 8 neurons x 64 tokens of token block t0 from the summed tile; slots at or past the count and
+// tokens at or past T get h = 0 (their rows and columns were computed from clamped loads).
 template <int NT>
-struct GuX {
-    rm_u32x4 x[2][NT];
-};
-
-template <int NT>
-__device__ __forceinline__ void gu_load_x(GuX<NT> &c, const uint16_t *const *xr, const bool *xv, int s, int s_end) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const bool ok = s + i < s_end;
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) c.x[i][tt] = (ok && xv[tt]) ? load16(xr[tt] + (s + i) * 32) : zero16();
-    }
+__device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, const rm_f32x4 (*red)[NT][64], int ds,
+                                           int t0, int slot_base, int cnt, const float *rn) {
+    const int j = threadIdx.x & 7;
+    const int tok = threadIdx.x >> 3;
+    float h = group_h<NT>(red, ds, j, tok, rn);
+    if (slot_base + j >= cnt || t0 + tok >= a.T) h = 0.0f;
+    Hb[static_cast<size_t>(t0 + tok) * a.kcap + slot_base + j] = static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
 }
 
-template <int NT>
-__device__ __forceinline__ void gu_mma2(rm_u32x4 a0, rm_u32x4 a1, const GuX<NT> &c, int s, int s_end,
-                                        rm_f32x4 *acc) {
-    if (s < s_end) {
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) acc[tt] = mfma_bf16(a0, c.x[0][tt], acc[tt]);
-    }
-    if (s + 1 < s_end) {
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) acc[tt] = mfma_bf16(a1, c.x[1][tt], acc[tt]);
-    }
-}
-
-template <int NT>
+// SPW: K steps (of 32 columns) per wave, d = 8 * 32 * SPW.  Straight-line code: every weight load and the x
+// loads of the first half go out before the first matrix-core instruction, the second half's x loads right
+// after, so the compiler's wait counts are exact and a wave waits for memory about once.
+template <int NT, int SPW>
 __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
     const int b = blockIdx.y;
     const int slot0 = blockIdx.x * 8;
@@ -139,8 +127,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
     const int wave = tid >> 6;
     const int r = lane & 15;    // A row (0-7 gate, 8-15 up) and B column (token within the tile)
     const int grp = lane >> 4;  // which 8 of the 32 K values of a step this lane carries
-    const int slot = slot0 + (r & 7);
-    const int n = lane_neuron(a, b, slot);
+    const int n = lane_neuron(a, b, slot0 + (r & 7));
     const int cnt = a.idx ? clamp_count(a.count[b], a.max_count) : a.d_ff;
     uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
 
@@ -149,51 +136,44 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
             *reinterpret_cast<rm_u32x4 *>(Hb + static_cast<size_t>(t) * a.kcap + slot0) = zero16();
         return;
     }
-    const bool valid = slot < cnt;
-    const uint16_t *wrow = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(n) * a.d + grp * 8;
-    const int nsteps = a.d / 32;
-    const int s_begin = (nsteps * wave) / kGuWaves;
-    const int s_end = (nsteps * (wave + 1)) / kGuWaves;
+    const int c0 = wave * SPW * 32 + grp * 8;  // first column of this lane's K pieces
+    const uint16_t *wrow = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(n) * a.d + c0;
 
     __shared__ rm_f32x4 red[kGuWaves][NT][64];
     __shared__ float rn[64];
 
     for (int t0 = 0; t0 < a.T; t0 += rm::kBfTokBlock) {
-        load_rnorm(a, b, t0, rn);
-        rm_f32x4 acc[NT];
         const uint16_t *xr[NT];
-        bool xv[NT];
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) {
-            acc[tt] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
-            const int t = t0 + tt * 16 + r;
-            xv[tt] = t < a.T;
-            xr[tt] = a.xn + (static_cast<size_t>(b) * a.T + (xv[tt] ? t : 0)) * a.d + grp * 8;
+            const int t = min(t0 + tt * 16 + r, a.T - 1);  // tokens past T re-read the last token
+            xr[tt] = a.xn + (static_cast<size_t>(b) * a.T + t) * a.d + c0;
         }
-        for (int sb = s_begin; sb < s_end; sb += kMaxSteps) {
-            rm_u32x4 w[kMaxSteps];
+        constexpr int H1 = (SPW + 1) / 2;  // steps of the first half
+        rm_u32x4 w[SPW], x[SPW][NT];
 #pragma unroll
-            for (int i = 0; i < kMaxSteps; ++i) w[i] = (sb + i < s_end) ? load16(wrow + (sb + i) * 32) : zero16();
-            GuX<NT> x0, x1;
-            gu_load_x(x0, xr, xv, sb, s_end);
-            if (!valid) {
+        for (int i = 0; i < SPW; ++i) w[i] = load16(wrow + i * 32);
 #pragma unroll
-                for (int i = 0; i < kMaxSteps; ++i) w[i] = zero16();
-            }
+        for (int i = 0; i < H1; ++i)
 #pragma unroll
-            for (int i = 0; i < kMaxSteps; i += 4) {
-                if (sb + i + 2 < s_end) gu_load_x(x1, xr, xv, sb + i + 2, s_end);
-                gu_mma2(w[i], w[i + 1], x0, sb + i, s_end, acc);
-                if (sb + i + 4 < s_end && i + 4 < kMaxSteps) gu_load_x(x0, xr, xv, sb + i + 4, s_end);
-                gu_mma2(w[i + 2], w[i + 3], x1, sb + i + 2, s_end, acc);
-            }
-        }
+            for (int tt = 0; tt < NT; ++tt) x[i][tt] = load16(xr[tt] + i * 32);
+#pragma unroll
+        for (int i = H1; i < SPW; ++i)
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) x[i][tt] = load16(xr[tt] + i * 32);
+        rm_f32x4 acc[NT];
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) acc[tt] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < SPW; ++i)
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) acc[tt] = mfma_bf16(w[i], x[i][tt], acc[tt]);
+
+        load_rnorm(a, b, t0, rn);
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) red[wave][tt][lane] = acc[tt];
         __syncthreads();
-        const float h = group_h<NT>(red, kGuWaves, tid & 7, tid >> 3, rn);
-        Hb[static_cast<size_t>(t0 + (tid >> 3)) * a.kcap + slot0 + (tid & 7)] =
-            static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
+        gu_store_h<NT>(a, Hb, red, kGuWaves, t0, slot0, cnt, rn);
         __syncthreads();
     }
 }
@@ -214,8 +194,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
     const int r = lane & 15;
     const int grp = lane >> 4;
     const int slot0 = blk0 + g * 8;
-    const int slot = slot0 + (r & 7);
-    const int n = lane_neuron(a, b, slot);
+    const int n = lane_neuron(a, b, slot0 + (r & 7));
     const int cnt = a.idx ? clamp_count(a.count[b], a.max_count) : a.d_ff;
     uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
 
@@ -226,24 +205,24 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
         }
         return;
     }
-    const bool valid = slot < cnt;
     const uint16_t *wrow = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(n) * a.d + grp * 8;
     const int nchunks = (a.d + kChunkCols - 1) / kChunkCols;
+    const int last_col = a.d - 32;  // clamp target of out-of-range K steps (their products are skipped)
 
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][64 * kRowPitch];
     __shared__ rm_f32x4 red[NG][DS][NT][64];
     __shared__ float rn[64];
 
-    // Cooperative staging of one xn chunk: 64 rows x 256 columns, 16 bytes per thread and pass.
+    // Cooperative staging of one xn chunk: 64 rows x 256 columns, 16 bytes per thread and pass.  Rows past T
+    // and columns past d re-read clamped positions; they only feed outputs that are discarded.
     auto stage_load = [&](int t0, int c, rm_u32x4 *v) {
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
             const int e = tid + p * kGuThreads;  // 0 .. 2047
             const int row = e >> 5;              // 32 x 16 bytes per row
-            const int col = c * kChunkCols + (e & 31) * 8;
-            const int t = t0 + row;
-            v[p] = (row < NT * 16 && t < a.T && col < a.d) ? load16(a.xn + (static_cast<size_t>(b) * a.T + t) * a.d + col)
-                                                            : zero16();
+            const int col = min(c * kChunkCols + (e & 31) * 8, a.d - 8);
+            const int t = min(t0 + row, a.T - 1);
+            v[p] = load16(a.xn + (static_cast<size_t>(b) * a.T + t) * a.d + col);
         }
     };
     auto stage_store = [&](int buf, const rm_u32x4 *v) {
@@ -256,41 +235,34 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
     };
 
     for (int t0 = 0; t0 < a.T; t0 += rm::kBfTokBlock) {
-        load_rnorm(a, b, t0, rn);
         rm_f32x4 acc[NT];
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) acc[tt] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 
         rm_u32x4 xv[4], w0[SPW], w1[SPW];
-        stage_load(t0, 0, xv);
 #pragma unroll
-        for (int i = 0; i < SPW; ++i) {
-            const int s = part * SPW + i;
-            w0[i] = (s * 32 < a.d) ? load16(wrow + s * 32) : zero16();
-        }
+        for (int i = 0; i < SPW; ++i) w0[i] = load16(wrow + min((part * SPW + i) * 32, last_col));
+        stage_load(t0, 0, xv);
         stage_store(0, xv);
         __syncthreads();
         for (int c = 0; c < nchunks; ++c) {
             const int buf = c & 1;
             const bool more = c + 1 < nchunks;
             if (more) {
-                stage_load(t0, c + 1, xv);
 #pragma unroll
-                for (int i = 0; i < SPW; ++i) {
-                    const int col = (c + 1) * kChunkCols + (part * SPW + i) * 32;
-                    w1[i] = (col < a.d) ? load16(wrow + col) : zero16();
-                }
+                for (int i = 0; i < SPW; ++i)
+                    w1[i] = load16(wrow + min((c + 1) * kChunkCols + (part * SPW + i) * 32, last_col));
+                stage_load(t0, c + 1, xv);
             }
 #pragma unroll
             for (int i = 0; i < SPW; ++i) {
                 const int lc = (part * SPW + i) * 32;  // column within the chunk
                 if (c * kChunkCols + lc < a.d) {
-                    const rm_u32x4 aw = valid ? w0[i] : zero16();
 #pragma unroll
                     for (int tt = 0; tt < NT; ++tt) {
                         const rm_u32x4 bx =
                             *reinterpret_cast<const rm_u32x4 *>(&xs[buf][(tt * 16 + r) * kRowPitch + lc + grp * 8]);
-                        acc[tt] = mfma_bf16(aw, bx, acc[tt]);
+                        acc[tt] = mfma_bf16(w0[i], bx, acc[tt]);
                     }
                 }
             }
@@ -301,16 +273,107 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
             }
             __syncthreads();
         }
+        load_rnorm(a, b, t0, rn);
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) red[g][part][tt][lane] = acc[tt];
+        __syncthreads();
+        // Thread tid forms h for neuron (tid & 7) of each group and token tid >> 3.
+#pragma unroll
+        for (int gg = 0; gg < NG; ++gg) gu_store_h<NT>(a, Hb, red[gg], DS, t0, blk0 + gg * 8, cnt, rn);
+        __syncthreads();
+    }
+}
+
+// The same with NCH = ceil(d / 256) known at compile time (d <= 2048): fully unrolled, so the double buffer
+// (weights in registers, xn in LDS) is indexed at compile time and every wait count is exact.
+template <int NT, int NG, int NCH>
+__global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuArgs a) {
+    constexpr int DS = kGuWaves / NG;
+    constexpr int SPW = kChunkSteps / DS;
+    const int b = blockIdx.y;
+    const int blk0 = blockIdx.x * 8 * NG;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int g = wave / DS;
+    const int part = wave % DS;
+    const int r = lane & 15;
+    const int grp = lane >> 4;
+    const int slot0 = blk0 + g * 8;
+    const int n = lane_neuron(a, b, slot0 + (r & 7));
+    const int cnt = a.idx ? clamp_count(a.count[b], a.max_count) : a.d_ff;
+    uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
+
+    if (blk0 >= cnt) {
+        for (int e = tid; e < a.tpad * NG; e += kGuThreads) {
+            const int t = e / NG, gg = e % NG;
+            *reinterpret_cast<rm_u32x4 *>(Hb + static_cast<size_t>(t) * a.kcap + blk0 + gg * 8) = zero16();
+        }
+        return;
+    }
+    const uint16_t *wrow = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(n) * a.d + grp * 8;
+    const int last_col = a.d - 32;
+
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][64 * kRowPitch];
+    __shared__ rm_f32x4 red[NG][DS][NT][64];
+    __shared__ float rn[64];
+
+    for (int t0 = 0; t0 < a.T; t0 += rm::kBfTokBlock) {
+        auto stage_load = [&](int c, rm_u32x4 *v) {
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const int e = tid + p * kGuThreads;
+                const int row = e >> 5;
+                const int col = min(c * kChunkCols + (e & 31) * 8, a.d - 8);
+                const int t = min(t0 + row, a.T - 1);
+                v[p] = load16(a.xn + (static_cast<size_t>(b) * a.T + t) * a.d + col);
+            }
+        };
+        auto stage_store = [&](int buf, const rm_u32x4 *v) {
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const int e = tid + p * kGuThreads;
+                *reinterpret_cast<rm_u32x4 *>(&xs[buf][(e >> 5) * kRowPitch + (e & 31) * 8]) = v[p];
+            }
+        };
+        rm_f32x4 acc[NT];
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) acc[tt] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+        rm_u32x4 w[2][SPW], xv[4];
+#pragma unroll
+        for (int i = 0; i < SPW; ++i) w[0][i] = load16(wrow + min((part * SPW + i) * 32, last_col));
+        stage_load(0, xv);
+        stage_store(0, xv);
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            if (c + 1 < NCH) {
+#pragma unroll
+                for (int i = 0; i < SPW; ++i)
+                    w[(c + 1) & 1][i] = load16(wrow + min((c + 1) * kChunkCols + (part * SPW + i) * 32, last_col));
+                stage_load(c + 1, xv);
+            }
+#pragma unroll
+            for (int i = 0; i < SPW; ++i) {
+                const int lc = (part * SPW + i) * 32;
+                if (c * kChunkCols + lc < a.d) {
+#pragma unroll
+                    for (int tt = 0; tt < NT; ++tt) {
+                        const rm_u32x4 bx =
+                            *reinterpret_cast<const rm_u32x4 *>(&xs[c & 1][(tt * 16 + r) * kRowPitch + lc + grp * 8]);
+                        acc[tt] = mfma_bf16(w[c & 1][i], bx, acc[tt]);
+                    }
+                }
+            }
+            if (c + 1 < NCH) stage_store((c + 1) & 1, xv);
+            __syncthreads();
+        }
+        load_rnorm(a, b, t0, rn);
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) red[g][part][tt][lane] = acc[tt];
         __syncthreads();
 #pragma unroll
-        for (int gg = 0; gg < NG; ++gg) {
-            // Thread tid forms h for neuron (tid & 7) of group gg and token tid >> 3.
-            const float h = group_h<NT>(red[gg], DS, tid & 7, tid >> 3, rn);
-            Hb[static_cast<size_t>(t0 + (tid >> 3)) * a.kcap + blk0 + gg * 8 + (tid & 7)] =
-                static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
-        }
+        for (int gg = 0; gg < NG; ++gg) gu_store_h<NT>(a, Hb, red[gg], DS, t0, blk0 + gg * 8, cnt, rn);
         __syncthreads();
     }
 }
@@ -331,20 +394,18 @@ struct DnArgs {
 };
 
 template <int NT>
-__device__ __forceinline__ void dn_load(DnChunk<NT> &c, const DnArgs &a, const int32_t *idxb, const uint16_t *Hrow,
-                                        int kb, int col, bool colok) {
+__device__ __forceinline__ void dn_load(DnChunk<NT> &c, const DnArgs &a, const int *sidx, const uint16_t *Hrow,
+                                        int kb, int kb_local, int col) {
+    const int4 i0 = *reinterpret_cast<const int4 *>(sidx + kb_local);
+    const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb_local + 4);
+    const int n[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int slot = kb + j;
-        int n = slot < a.d_ff ? slot : 0;
-        if (idxb != nullptr) n = slot < a.d_ff ? clamp_neuron(idxb[slot], a.d_ff) : 0;
-        c.w[j] = colok ? load8(a.wd + static_cast<size_t>(n) * a.d + col) : make_uint2(0u, 0u);
-    }
+    for (int j = 0; j < 8; ++j) c.w[j] = load8(a.wd + static_cast<size_t>(n[j]) * a.d + col);
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) c.a[tt] = load16(Hrow + static_cast<size_t>(tt * 16) * a.kcap + kb);
 }
 
-// Slots at or past the count hold h = 0 in H, so their (clamped, loaded) weights contribute nothing.
+// Slots at or past the count hold h = 0 in H, so the weights loaded for them contribute nothing.
 template <int NT>
 __device__ __forceinline__ void dn_mma(const DnChunk<NT> &c, rm_f32x4 (*acc)[4]) {
 #pragma unroll
@@ -365,7 +426,8 @@ __device__ __forceinline__ void dn_mma(const DnChunk<NT> &c, rm_f32x4 (*acc)[4])
     }
 }
 
-template <int NT>
+// CPW: chunks per wave (a slice has 4 * CPW chunks); the chunk pipeline below is unrolled straight-line code.
+template <int NT, int CPW>
 __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
     const int ct = blockIdx.x;
     const int s = blockIdx.y;
@@ -375,88 +437,86 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
     const int wave = tid >> 6;
     const int grp = lane >> 4;  // K group: slots 8*grp .. 8*grp+7 of a chunk
     const int nn = lane & 15;   // A row (token in tile) and B column group (physical columns 4*nn + q)
-    const int col0 = ct * rm::kBfColTile;
-    const int col = col0 + nn * 4;
-    const bool colok = col < a.d;
-    const int32_t *idxb = a.idx ? a.idx + static_cast<size_t>(b) * a.d_ff : nullptr;
+    const int colw = ct * rm::kBfColTile + nn * 4;
+    const bool colok = colw < a.d;
+    const int col = min(colw, a.d - 4);  // columns past d re-read column d-4; those outputs are not stored
     const size_t stride = static_cast<size_t>(a.T) * a.d;
-    float *part_b = a.part + static_cast<size_t>(b) * a.slices * stride;
-    float *P = part_b + static_cast<size_t>(s) * stride;
-    const int c_begin = s * a.chunks_per_slice;
+    float *P = a.part + (static_cast<size_t>(b) * a.slices + s) * stride;
+    const int cps = a.chunks_per_slice;
+    const int c_begin = s * cps;
+    const int c_last = min(c_begin + cps, a.kcap / rm::kBfChunk) - 1;  // last chunk of the slice below kcap
 
-    // The first chunk of the first token block is loaded before the count is known (its slots are below
-    // kcap and its indices are clamped, so the loads stay in bounds); the count then trims the work.
-    DnChunk<NT> c0, c1;
-    const int c_first = c_begin + wave;
-    const bool first_loaded = c_first < min(c_begin + a.chunks_per_slice, a.kcap / rm::kBfChunk);
-    if (first_loaded)
-        dn_load(c0, a, idxb, a.H + (static_cast<size_t>(b) * a.tpad + nn) * a.kcap, c_first * rm::kBfChunk + grp * 8,
-                col, colok);
-
+    // The slice's neuron indices, clamped into [0, d_ff), staged once in LDS: the waves read them with LDS
+    // loads, which do not wait behind the weight loads in flight.
+    __shared__ __attribute__((aligned(16))) int sidx[rm::kBfMaxChunksPerSlice * rm::kBfChunk];
+    for (int i = tid; i < cps * rm::kBfChunk; i += kDnThreads) {
+        const int slot = min(c_begin * rm::kBfChunk + i, a.d_ff - 1);
+        sidx[i] = a.idx ? clamp_neuron(a.idx[static_cast<size_t>(b) * a.d_ff + slot], a.d_ff) : slot;
+    }
     const int cnt = a.idx ? clamp_count(a.count[b], a.max_count) : a.d_ff;
     const int nchunks = (cnt + rm::kBfChunk - 1) / rm::kBfChunk;
-    const int c_end = min(c_begin + a.chunks_per_slice, nchunks);
+    const int c_end = min(c_begin + cps, nchunks);
+    __syncthreads();
 
     __shared__ rm_f32x4 red[kDnWaves][NT][4][64];
+    if (c_begin >= c_end) return;  // no neuron of this sample falls in the slice; the epilogue skips it
 
-    if (c_begin < c_end) {
-        for (int t0 = 0; t0 < a.T; t0 += rm::kBfTokBlock) {
-            rm_f32x4 acc[NT][4];
+    for (int t0 = 0; t0 < a.T; t0 += rm::kBfTokBlock) {
+        rm_f32x4 acc[NT][4];
 #pragma unroll
-            for (int tt = 0; tt < NT; ++tt)
+        for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) acc[tt][q] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int q = 0; q < 4; ++q) acc[tt][q] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 
-            const uint16_t *Hrow = a.H + (static_cast<size_t>(b) * a.tpad + t0 + nn) * a.kcap;
-            int c = c_first;
-            if (c < c_end && !(t0 == 0 && first_loaded))
-                dn_load(c0, a, idxb, Hrow, c * rm::kBfChunk + grp * 8, col, colok);
-            for (; c < c_end; c += 2 * kDnWaves) {
-                const int cn = c + kDnWaves;
-                const bool more = cn < c_end;
-                if (more) dn_load(c1, a, idxb, Hrow, cn * rm::kBfChunk + grp * 8, col, colok);
-                dn_mma(c0, acc);
-                if (!more) break;
-                const int cnn = cn + kDnWaves;
-                if (cnn < c_end) dn_load(c0, a, idxb, Hrow, cnn * rm::kBfChunk + grp * 8, col, colok);
-                dn_mma(c1, acc);
+        const uint16_t *Hrow = a.H + (static_cast<size_t>(b) * a.tpad + t0 + nn) * a.kcap;
+        // Chunk loads are unconditional (chunk numbers clamped to the slice) and two deep: chunk k+2 is loaded
+        // into chunk k's registers right after chunk k's products are issued.
+        auto load_chunk = [&](DnChunk<NT> &cc, int k) {
+            const int ce = min(c_begin + wave + k * kDnWaves, c_last);
+            dn_load(cc, a, sidx, Hrow, ce * rm::kBfChunk + grp * 8, (ce - c_begin) * rm::kBfChunk + grp * 8, col);
+        };
+        DnChunk<NT> cb[2];
+        load_chunk(cb[0], 0);
+        if (CPW > 1) load_chunk(cb[1], 1);
+#pragma unroll
+        for (int k = 0; k < CPW; ++k) {
+            if (c_begin + wave + k * kDnWaves < c_end) dn_mma(cb[k & 1], acc);
+            if (k + 2 < CPW) load_chunk(cb[k & 1], k + 2);
+        }
+
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) red[wave][tt][q][lane] = acc[tt][q];
+        __syncthreads();
+        // Wave w sums token tile w over the four waves (order 0, 1, 2, 3) and stores it.
+        if (wave < NT) {
+            const int tt = wave;
+            rm_f32x4 v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                v[q] = red[0][tt][q][lane];
+#pragma unroll
+                for (int w = 1; w < kDnWaves; ++w) v[q] += red[w][tt][q][lane];
             }
-
+            // lane L, register i: token 4*(L/16)+i of the tile, physical column 4*(L%16) + q.
+            if (colok) {
 #pragma unroll
-            for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) red[wave][tt][q][lane] = acc[tt][q];
-            __syncthreads();
-            // Wave w sums token tile w over the four waves (order 0, 1, 2, 3) and stores it.
-            if (wave < NT) {
-                const int tt = wave;
-                rm_f32x4 v[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    v[q] = red[0][tt][q][lane];
-#pragma unroll
-                    for (int w = 1; w < kDnWaves; ++w) v[q] += red[w][tt][q][lane];
-                }
-                // lane L, register i: token 4*(L/16)+i of the tile, physical column 4*(L%16) + q.
-                if (colok) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int t = t0 + tt * 16 + grp * 4 + i;
-                        if (t < a.T) {
-                            float4 o;
-                            o.x = v[0][i];
-                            o.y = v[1][i];
-                            o.z = v[2][i];
-                            o.w = v[3][i];
-                            *reinterpret_cast<float4 *>(P + static_cast<size_t>(t) * a.d + col) = o;
-                        }
+                for (int i = 0; i < 4; ++i) {
+                    const int t = t0 + tt * 16 + grp * 4 + i;
+                    if (t < a.T) {
+                        float4 o;
+                        o.x = v[0][i];
+                        o.y = v[1][i];
+                        o.z = v[2][i];
+                        o.w = v[3][i];
+                        *reinterpret_cast<float4 *>(P + static_cast<size_t>(t) * a.d + colw) = o;
                     }
                 }
             }
-            __syncthreads();
         }
+        __syncthreads();
     }
-
 }
 
 int token_tiles(int T) {
@@ -468,12 +528,37 @@ template <int NT>
 void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
     const dim3 block(kGuThreads);
     const dim3 grid(p.gate_blocks, p.B);
-    switch (p.gate_groups) {
-        case 1: hipLaunchKernelGGL(gateup_direct_kernel<NT>, grid, block, 0, st, a); break;
-        case 2: hipLaunchKernelGGL((gateup_staged_kernel<NT, 2>), grid, block, 0, st, a); break;
-        case 4: hipLaunchKernelGGL((gateup_staged_kernel<NT, 4>), grid, block, 0, st, a); break;
-        default: hipLaunchKernelGGL((gateup_staged_kernel<NT, 8>), grid, block, 0, st, a); break;
+    if (p.gate_groups == 1) {
+        switch (p.d / 256) {  // the plan picks the direct kernel only for d = 256, 512, 1024, 2048
+            case 1: hipLaunchKernelGGL((gateup_direct_kernel<NT, 1>), grid, block, 0, st, a); break;
+            case 2: hipLaunchKernelGGL((gateup_direct_kernel<NT, 2>), grid, block, 0, st, a); break;
+            case 4: hipLaunchKernelGGL((gateup_direct_kernel<NT, 4>), grid, block, 0, st, a); break;
+            default: hipLaunchKernelGGL((gateup_direct_kernel<NT, 8>), grid, block, 0, st, a); break;
+        }
+        return;
     }
+    const int nch = (p.d + kChunkCols - 1) / kChunkCols;
+#define RM_STAGED(NG)                                                                                          \
+    switch (nch) {                                                                                             \
+        case 1: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 1>), grid, block, 0, st, a); break; \
+        case 2: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 2>), grid, block, 0, st, a); break; \
+        case 3: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 3>), grid, block, 0, st, a); break; \
+        case 4: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 4>), grid, block, 0, st, a); break; \
+        case 8:                                                                                                \
+            if (NG < 8) {                                                                                      \
+                hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 8>), grid, block, 0, st, a);        \
+                break;                                                                                         \
+            }                                                                                                  \
+            hipLaunchKernelGGL((gateup_staged_kernel<NT, NG>), grid, block, 0, st, a);                        \
+            break; /* 8 chunks x 8 groups: the unrolled form spills */                                         \
+        default: hipLaunchKernelGGL((gateup_staged_kernel<NT, NG>), grid, block, 0, st, a); break;            \
+    }
+    switch (p.gate_groups) {
+        case 2: RM_STAGED(2) break;
+        case 4: RM_STAGED(4) break;
+        default: RM_STAGED(8) break;
+    }
+#undef RM_STAGED
 }
 
 }  // namespace
@@ -529,12 +614,19 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
     a.part = reinterpret_cast<float *>(base + p.off_part);
     const dim3 grid(p.ncol, p.slices, p.B), block(kDnThreads);
     profile_before(RM_KERNEL_DOWN, st);
-    switch (token_tiles(p.T)) {
-        case 1: hipLaunchKernelGGL(down_bf16_kernel<1>, grid, block, 0, st, a); break;
-        case 2: hipLaunchKernelGGL(down_bf16_kernel<2>, grid, block, 0, st, a); break;
-        case 3: hipLaunchKernelGGL(down_bf16_kernel<3>, grid, block, 0, st, a); break;
-        default: hipLaunchKernelGGL(down_bf16_kernel<4>, grid, block, 0, st, a); break;
+#define RM_DOWN(NT)                                                                                 \
+    switch (p.slice_units / kDnWaves) {                                                            \
+        case 1: hipLaunchKernelGGL((down_bf16_kernel<NT, 1>), grid, block, 0, st, a); break;       \
+        case 2: hipLaunchKernelGGL((down_bf16_kernel<NT, 2>), grid, block, 0, st, a); break;       \
+        default: hipLaunchKernelGGL((down_bf16_kernel<NT, 4>), grid, block, 0, st, a); break;      \
     }
+    switch (token_tiles(p.T)) {
+        case 1: RM_DOWN(1) break;
+        case 2: RM_DOWN(2) break;
+        case 3: RM_DOWN(3) break;
+        default: RM_DOWN(4) break;
+    }
+#undef RM_DOWN
     hipError_t e = hipGetLastError();
     profile_after(RM_KERNEL_DOWN, st);
     return e;

@@ -144,7 +144,8 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         q.tpad = ceil_div(T, kBfTokBlock) * kBfTokBlock;
         // Gate/up: the widest workgroup (8 * NG neurons) that still gives every compute unit one workgroup.
         const int k32 = ceil_div(kmax, kBfChunk) * kBfChunk;
-        q.gate_groups = 1;
+        const bool direct_ok = s->d == 256 || s->d == 512 || s->d == 1024 || s->d == 2048;
+        q.gate_groups = direct_ok ? 1 : 2;
         for (int ng : {8, 4, 2}) {
             if (static_cast<long long>(B) * ceil_div(k32, 8 * ng) >= kCUs) {
                 q.gate_groups = ng;
@@ -156,9 +157,11 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         q.col_tile = kBfColTile;
         q.ncol = ceil_div(s->d, q.col_tile);
         const int nchunks = q.kcap / kBfChunk;
+        // Chunks per slice: 4, 8 or 16 (1, 2 or 4 per wave), the fewest that keep the slice count near the
+        // target; longer lists get more slices.
         const int s_target = std::max(1, ceil_div(kTargetDownGroups, q.ncol * B));
-        int cps = ceil_div(nchunks, s_target);
-        cps = std::max(kBfWaves, ceil_div(cps, kBfWaves) * kBfWaves);
+        int cps = kBfWaves;
+        while (cps < 4 * kBfWaves && ceil_div(nchunks, cps) > s_target) cps *= 2;
         q.slice_units = cps;
         q.slices = ceil_div(nchunks, cps);
         xn_elem = 2;

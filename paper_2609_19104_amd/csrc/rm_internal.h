@@ -20,6 +20,7 @@ constexpr int kBfNeurPerBlk = 8;    // neurons per gate/up workgroup (8 gate row
 constexpr int kBfChunk = 32;        // neurons per down-projection matrix-core step (K of the 16x16x32 tile)
 constexpr int kBfColTile = 64;      // output columns per down workgroup (16 lanes x 4 columns)
 constexpr int kBfWaves = 4;
+constexpr int kBfMaxChunksPerSlice = 16;  // down: a slice's indices (16 x 32) are staged in 2 KB of LDS
 
 // f32 path: vector ALU.
 constexpr int kF32TokBlock = 8;     // tokens per register block

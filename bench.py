@@ -37,6 +37,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_2609_19104_amd", "csrc")
 COLD_BYTES = 1 << 30   # weight copies rotated through per timed run
 
 
@@ -215,6 +217,37 @@ def time_graph(setup: Setup, steps: int, warmup: int):
     return start.elapsed_time(end) / steps
 
 
+def kernel_source_digest() -> str:
+    """sha256 over the HIP sources (names and contents, sorted): identifies the kernels a counter run measured."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def counted_traffic(workload: str, kernel_key: str):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 counter summary of this workload
+    (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter reads for a plain copy of known size), or None
+    when there is no summary or the kernels have changed since it was taken."""
+    path = os.path.join(PROFILES, f"pmc_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].strip().split(": ", 1)
+                fields[k.strip("`")] = v.strip().strip("`")
+    if fields.get("kernel_source_sha256") != kernel_source_digest():
+        return None
+    v = fields.get(f"traffic_bytes_per_launch.{kernel_key}")
+    return int(float(v)) if v else None
+
+
 def cpu_baseline(setup: Setup, seconds: float):
     """The float64 oracle on the same layer, mask and input, repeated for about `seconds` of CPU time."""
     import oracle
@@ -253,6 +286,9 @@ def main(argv=None) -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + steps with no event hooks and no CPU leg (for rocprofv3)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run `steps` device-to-device copies of MIB MiB (the plain copy kernel whose "
+                         "FETCH_SIZE / WRITE_SIZE counters scale the hot path's)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -265,6 +301,15 @@ def main(argv=None) -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "copies": args.steps}))
+        return 0
     setup = Setup(args.workload, dev, cold=True)
 
     if args.profile_only:
@@ -279,9 +324,9 @@ def main(argv=None) -> int:
     gu_bytes = gateup_bytes(setup.k, setup.d, 2)
     dn_bytes = down_bytes(setup.k, setup.d, 2)
     if gu_us >= dn_us:
-        dom, dom_bytes, dom_us = "gate/up projection (gateup_direct_kernel or gateup_staged_kernel)", gu_bytes, gu_us
+        dom, dom_key, dom_bytes, dom_us = "gate/up projection (gateup_*_kernel)", "gateup", gu_bytes, gu_us
     else:
-        dom, dom_bytes, dom_us = "down projection (down_bf16_kernel)", dn_bytes, dn_us
+        dom, dom_key, dom_bytes, dom_us = "down projection (down_bf16_kernel)", "down", dn_bytes, dn_us
     achieved = dom_bytes / (dom_us * 1e-6) / 1e9
     value = setup.active_bytes / (ms * 1e-3) / 1e9
 
@@ -314,8 +359,10 @@ def main(argv=None) -> int:
         "warm_us_per_layer": round(warm_ms * 1e3, 3),
         "kernel_us": {"gateup": round(gu_us, 3), "down": round(dn_us, 3)},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_us, 3)},
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": counted_traffic(args.workload, dom_key),
+                     "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_us, 3),
+                     "traffic_unit": "bytes per launch (HBM, from rocprofv3 counters)"},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(setup, args.cpu_seconds)

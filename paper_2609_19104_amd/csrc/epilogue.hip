@@ -51,7 +51,7 @@ __device__ __forceinline__ void store_xn(void *xn, size_t o, float4 v) {
 template <bool kBf16Xn>
 __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restrict__ part, int slices,
                                                             int slice_neurons, const int32_t *__restrict__ count,
-                                                            int max_count, int dense_count, const float *x,
+                                                            int max_count, const float *x,
                                                             float *y, int T, int d, void *__restrict__ xn_next,
                                                             const float *__restrict__ g_next,
                                                             float *__restrict__ ssq) {
@@ -59,11 +59,8 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
     const int b = row / T;
     const int t = row - b * T;
     const int tid = threadIdx.x;
-    int cnt = dense_count;
-    if (count != nullptr) {
-        cnt = count[b];
-        cnt = cnt < 0 ? 0 : (cnt > max_count ? max_count : cnt);
-    }
+    int cnt = count[b];
+    cnt = cnt < 0 ? 0 : (cnt > max_count ? max_count : cnt);
     const int used = (cnt + slice_neurons - 1) / slice_neurons;
     const size_t stride = static_cast<size_t>(T) * d;
     const float *P = part + static_cast<size_t>(b) * slices * stride + static_cast<size_t>(t) * d;
@@ -140,10 +137,10 @@ hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, 
     const float *g = emit_xn ? g_next : nullptr;
     if (p.wdtype == RM_BF16)
         hipLaunchKernelGGL(epilogue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, part, p.slices, slice_neurons,
-                           count, p.max_count, p.d_ff, x, y, p.T, p.d, xn, g, ssq);
+                           count, p.max_count, x, y, p.T, p.d, xn, g, ssq);
     else
         hipLaunchKernelGGL(epilogue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, part, p.slices, slice_neurons,
-                           count, p.max_count, p.d_ff, x, y, p.T, p.d, xn, g, ssq);
+                           count, p.max_count, x, y, p.T, p.d, xn, g, ssq);
     return hipGetLastError();
 }
 

@@ -74,52 +74,68 @@ __device__ __forceinline__ void load_rnorm(const GuArgs &a, int b, int t0, float
     }
 }
 
-// The neuron index of this lane's row, loaded without waiting for the count (slots beyond the list are
-// masked once the count is known; their index entries are only clamped into range).
+// The neuron index of this lane's row (slot clamped into the list; entries past the count are only clamped
+// into range, their h is masked when stored).
 __device__ __forceinline__ int lane_neuron(const GuArgs &a, int b, int slot) {
-    if (a.idx == nullptr) return slot < a.d_ff ? slot : 0;
-    return slot < a.d_ff ? clamp_neuron(a.idx[static_cast<size_t>(b) * a.d_ff + slot], a.d_ff) : 0;
-}
-
-// h for 8 neurons x 64 tokens from the summed gate/up tile in LDS; one value per thread of a 512-thread group.
-// red: [ds][NT][64 lanes] f32x4 tiles of one neuron group (lane L, register i = row 4*(L/16)+i, token L%16).
-template <int NT>
-__device__ __forceinline__ float group_h(const rm_f32x4 (*red)[NT][64], int ds, int j, int tok, const float *rn) {
-    const int tt = tok >> 4;
-    if (tt >= NT) return 0.0f;
-    const int tc = tok & 15;
-    const int lg = (j >> 2) * 16 + tc;
-    const int lu = ((j + 8) >> 2) * 16 + tc;
-    const int reg = j & 3;
-    float gsum = red[0][tt][lg][reg];
-    float usum = red[0][tt][lu][reg];
-    for (int w = 1; w < ds; ++w) {
-        gsum += red[w][tt][lg][reg];
-        usum += red[w][tt][lu][reg];
-    }
-    const float r = rn[tok];
-    return rm_silu(gsum * r) * (usum * r);
+    return clamp_neuron(a.idx[static_cast<size_t>(b) * a.d_ff + min(slot, a.d_ff - 1)], a.d_ff);
 }
 
 // ------------------------------------------------------------------------------------------ gate / up, direct
 
 // Writes h for 8 neurons x 64 tokens of token block t0 from the summed tile; slots at or past the count and
-// tokens at or past T get h = 0 (their rows and columns were computed from clamped loads).
-template <int NT>
-__device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, const rm_f32x4 (*red)[NT][64], int ds,
-                                           int t0, int slot_base, int cnt, const float *rn) {
+// tokens at or past T get h = 0 (their rows and columns were computed from clamped loads).  H is chunk-major
+// (32-slot chunks, then tokens), so the 8 slots of a token are 16 contiguous bytes.
+// red(w, tt, lane) is d-part w's tile tt (lane L, register i = row 4 (L / 16) + i, token L % 16).
+template <int NT, typename RedAt>
+__device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, RedAt red, int ds, int t0, int slot_base,
+                                           int cnt, const float *rn) {
     const int j = threadIdx.x & 7;
     const int tok = threadIdx.x >> 3;
-    float h = group_h<NT>(red, ds, j, tok, rn);
-    if (slot_base + j >= cnt || t0 + tok >= a.T) h = 0.0f;
-    Hb[static_cast<size_t>(t0 + tok) * a.kcap + slot_base + j] = static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
+    const int tt = tok >> 4, tc = tok & 15;
+    float h = 0.0f;
+    if (tt < NT) {
+        const int lg = (j >> 2) * 16 + tc;        // gate row j of the tile: lane 16 (j / 4) + token, register j % 4
+        const int lu = ((j + 8) >> 2) * 16 + tc;  // up row j + 8
+        const int reg = j & 3;
+        float gsum = red(0, tt, lg)[reg];
+        float usum = red(0, tt, lu)[reg];
+        for (int w = 1; w < ds; ++w) {
+            gsum += red(w, tt, lg)[reg];
+            usum += red(w, tt, lu)[reg];
+        }
+        const float r = rn[tok];
+        h = rm_silu(gsum * r) * (usum * r);
+    }
+    const int slot = slot_base + j;
+    if (slot >= cnt || t0 + tok >= a.T) h = 0.0f;
+    Hb[(static_cast<size_t>(slot >> 5) * a.tpad + t0 + tok) * rm::kBfChunk + (slot & 31)] =
+        static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
 }
 
-// SPW: K steps (of 32 columns) per wave, d = 8 * 32 * SPW.  Straight-line code: every weight load and the x
-// loads of the first half go out before the first matrix-core instruction, the second half's x loads right
-// after, so the compiler's wait counts are exact and a wave waits for memory about once.
-template <int NT, int SPW>
+// Geometry of the direct kernel's per-wave column slice: SPW K steps of 32 columns, staged in sub-slices of at
+// most 4 steps (256 bytes per token row) through the wave's own LDS region.
+template <int SPW>
+struct DirGeom {
+    static constexpr int kSubSteps = SPW < 4 ? SPW : 4;
+    static constexpr int kSubs = SPW / kSubSteps;
+    static constexpr int kRowBytes = kSubSteps * 64;
+    static constexpr int kPieces = kRowBytes / 16;   // 16-byte pieces per token row = loads per lane per sub-slice
+    static constexpr int kPitch = kRowBytes + 16;    // LDS row pitch: 16 bytes of padding against bank conflicts
+    static constexpr int kRegion = 64 * kPitch;      // bytes per wave: 64 token rows
+};
+
+// One group of 8 listed neurons per workgroup; wave w takes columns [w * 32 SPW, (w + 1) * 32 SPW) of d = 256 SPW.
+// The wave copies its slice of the FFN input (64 token rows) into its own LDS region with whole-line loads
+// (each instruction covers 4 rows x 256 bytes), then reads it back in matrix-core fragment order.  Loading the
+// fragments straight from memory would touch sixteen half-used lines per instruction, which moves the same
+// bytes about three times slower.  Every load of a wave is issued before its first wait: the neuron index, the
+// input slice, then the weights (which need the index); the scheduling barrier keeps the compiler from
+// interleaving loads with the matrix-core work, so the wave waits for memory once.  No early exit on the count:
+// the count only masks the stored h, and its load is not waited for until then.
+// kOneBlock: T <= 64, the token-block loop runs once (and compiles away, with its conservative waits).
+template <int NT, int SPW, bool kOneBlock>
 __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
+    using G = DirGeom<SPW>;
     const int b = blockIdx.y;
     const int slot0 = blockIdx.x * 8;
     const int tid = threadIdx.x;
@@ -127,54 +143,73 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
     const int wave = tid >> 6;
     const int r = lane & 15;    // A row (0-7 gate, 8-15 up) and B column (token within the tile)
     const int grp = lane >> 4;  // which 8 of the 32 K values of a step this lane carries
-    const int n = lane_neuron(a, b, slot0 + (r & 7));
-    const int cnt = a.idx ? clamp_count(a.count[b], a.max_count) : a.d_ff;
+    const int cnt = clamp_count(a.count[b], a.max_count);  // used only when h is stored
+    const int raw_n = a.idx[static_cast<size_t>(b) * a.d_ff + min(slot0 + (r & 7), a.d_ff - 1)];
     uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
+    const int col0 = wave * SPW * 32;
 
-    if (slot0 >= cnt) {
-        for (int t = tid; t < a.tpad; t += kGuThreads)
-            *reinterpret_cast<rm_u32x4 *>(Hb + static_cast<size_t>(t) * a.kcap + slot0) = zero16();
-        return;
-    }
-    const int c0 = wave * SPW * 32 + grp * 8;  // first column of this lane's K pieces
-    const uint16_t *wrow = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(n) * a.d + c0;
-
-    __shared__ rm_f32x4 red[kGuWaves][NT][64];
+    __shared__ __attribute__((aligned(16))) unsigned char lds[kGuWaves * G::kRegion];
     __shared__ float rn[64];
+    unsigned char *region = lds + wave * G::kRegion;
+    auto red = [&](int w, int tt, int l) -> const rm_f32x4 & {
+        return *reinterpret_cast<const rm_f32x4 *>(lds + w * G::kRegion + (tt * 64 + l) * 16);
+    };
 
-    for (int t0 = 0; t0 < a.T; t0 += rm::kBfTokBlock) {
-        const uint16_t *xr[NT];
+    // Input slice of token block t0: piece e = j * 64 + lane is row e / kPieces, 16-byte piece e % kPieces.
+    auto load_x = [&](int t0, rm_u32x4 (&xv)[G::kSubs][G::kPieces]) {
 #pragma unroll
-        for (int tt = 0; tt < NT; ++tt) {
-            const int t = min(t0 + tt * 16 + r, a.T - 1);  // tokens past T re-read the last token
-            xr[tt] = a.xn + (static_cast<size_t>(b) * a.T + t) * a.d + c0;
-        }
-        constexpr int H1 = (SPW + 1) / 2;  // steps of the first half
-        rm_u32x4 w[SPW], x[SPW][NT];
+        for (int s = 0; s < G::kSubs; ++s)
+#pragma unroll
+            for (int j = 0; j < G::kPieces; ++j) {
+                const int e = j * 64 + lane;
+                const int t = min(t0 + e / G::kPieces, a.T - 1);  // rows past T repeat the last token
+                xv[s][j] = load16(a.xn + (static_cast<size_t>(b) * a.T + t) * a.d + col0 + s * G::kSubSteps * 32 +
+                                  (e % G::kPieces) * 8);
+            }
+    };
+    rm_u32x4 xv[G::kSubs][G::kPieces];
+    load_x(0, xv);
+    __builtin_amdgcn_sched_barrier(0);  // the input loads go out before the wait for the index
+    rm_u32x4 w[SPW];
+    {
+        const int n = clamp_neuron(raw_n, a.d_ff);
+        const uint16_t *wrow = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(n) * a.d + col0 + grp * 8;
 #pragma unroll
         for (int i = 0; i < SPW; ++i) w[i] = load16(wrow + i * 32);
-#pragma unroll
-        for (int i = 0; i < H1; ++i)
-#pragma unroll
-            for (int tt = 0; tt < NT; ++tt) x[i][tt] = load16(xr[tt] + i * 32);
-#pragma unroll
-        for (int i = H1; i < SPW; ++i)
-#pragma unroll
-            for (int tt = 0; tt < NT; ++tt) x[i][tt] = load16(xr[tt] + i * 32);
+    }
+    for (int t0 = 0;;) {
+        __builtin_amdgcn_sched_barrier(0);
         rm_f32x4 acc[NT];
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) acc[tt] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int i = 0; i < SPW; ++i)
+        for (int s = 0; s < G::kSubs; ++s) {
+            // The wave's own region: its LDS operations run in order, so no barrier is needed between the
+            // previous sub-slice's fragment reads and these writes.
 #pragma unroll
-            for (int tt = 0; tt < NT; ++tt) acc[tt] = mfma_bf16(w[i], x[i][tt], acc[tt]);
-
+            for (int j = 0; j < G::kPieces; ++j) {
+                const int e = j * 64 + lane;
+                *reinterpret_cast<rm_u32x4 *>(region + (e / G::kPieces) * G::kPitch + (e % G::kPieces) * 16) = xv[s][j];
+            }
+#pragma unroll
+            for (int i = 0; i < G::kSubSteps; ++i)
+#pragma unroll
+                for (int tt = 0; tt < NT; ++tt) {
+                    const rm_u32x4 bx =
+                        *reinterpret_cast<const rm_u32x4 *>(region + (tt * 16 + r) * G::kPitch + i * 64 + grp * 16);
+                    acc[tt] = mfma_bf16(w[s * G::kSubSteps + i], bx, acc[tt]);
+                }
+        }
+        // The summed tile goes into the wave's region (its fragment reads precede these writes).
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) *reinterpret_cast<rm_f32x4 *>(region + (tt * 64 + lane) * 16) = acc[tt];
         load_rnorm(a, b, t0, rn);
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) red[wave][tt][lane] = acc[tt];
         __syncthreads();
         gu_store_h<NT>(a, Hb, red, kGuWaves, t0, slot0, cnt, rn);
-        __syncthreads();
+        t0 += rm::kBfTokBlock;
+        if (kOneBlock || t0 >= a.T) break;
+        __syncthreads();  // every wave has read the tiles before the regions are refilled
+        load_x(t0, xv);
     }
 }
 
@@ -195,13 +230,14 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
     const int grp = lane >> 4;
     const int slot0 = blk0 + g * 8;
     const int n = lane_neuron(a, b, slot0 + (r & 7));
-    const int cnt = a.idx ? clamp_count(a.count[b], a.max_count) : a.d_ff;
+    const int cnt = clamp_count(a.count[b], a.max_count);
     uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
 
-    if (blk0 >= cnt) {
+    if (blk0 >= cnt) {  // the whole group is past the list: h = 0
         for (int e = tid; e < a.tpad * NG; e += kGuThreads) {
-            const int t = e / NG, gg = e % NG;
-            *reinterpret_cast<rm_u32x4 *>(Hb + static_cast<size_t>(t) * a.kcap + blk0 + gg * 8) = zero16();
+            const int t = e / NG, slot = blk0 + (e % NG) * 8;
+            *reinterpret_cast<rm_u32x4 *>(Hb + (static_cast<size_t>(slot >> 5) * a.tpad + t) * rm::kBfChunk +
+                                          (slot & 31)) = zero16();
         }
         return;
     }
@@ -279,7 +315,9 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
         __syncthreads();
         // Thread tid forms h for neuron (tid & 7) of each group and token tid >> 3.
 #pragma unroll
-        for (int gg = 0; gg < NG; ++gg) gu_store_h<NT>(a, Hb, red[gg], DS, t0, blk0 + gg * 8, cnt, rn);
+        for (int gg = 0; gg < NG; ++gg)
+            gu_store_h<NT>(a, Hb, [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; }, DS, t0,
+                           blk0 + gg * 8, cnt, rn);
         __syncthreads();
     }
 }
@@ -301,13 +339,14 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
     const int grp = lane >> 4;
     const int slot0 = blk0 + g * 8;
     const int n = lane_neuron(a, b, slot0 + (r & 7));
-    const int cnt = a.idx ? clamp_count(a.count[b], a.max_count) : a.d_ff;
+    const int cnt = clamp_count(a.count[b], a.max_count);
     uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
 
-    if (blk0 >= cnt) {
+    if (blk0 >= cnt) {  // the whole group is past the list: h = 0
         for (int e = tid; e < a.tpad * NG; e += kGuThreads) {
-            const int t = e / NG, gg = e % NG;
-            *reinterpret_cast<rm_u32x4 *>(Hb + static_cast<size_t>(t) * a.kcap + blk0 + gg * 8) = zero16();
+            const int t = e / NG, slot = blk0 + (e % NG) * 8;
+            *reinterpret_cast<rm_u32x4 *>(Hb + (static_cast<size_t>(slot >> 5) * a.tpad + t) * rm::kBfChunk +
+                                          (slot & 31)) = zero16();
         }
         return;
     }
@@ -373,7 +412,9 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
         for (int tt = 0; tt < NT; ++tt) red[g][part][tt][lane] = acc[tt];
         __syncthreads();
 #pragma unroll
-        for (int gg = 0; gg < NG; ++gg) gu_store_h<NT>(a, Hb, red[gg], DS, t0, blk0 + gg * 8, cnt, rn);
+        for (int gg = 0; gg < NG; ++gg)
+            gu_store_h<NT>(a, Hb, [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; }, DS, t0,
+                           blk0 + gg * 8, cnt, rn);
         __syncthreads();
     }
 }
@@ -388,24 +429,14 @@ struct DnChunk {
 
 struct DnArgs {
     const uint16_t *H, *wd;
-    const int32_t *idx, *count;
-    int max_count, d_ff, d, T, tpad, kcap, slices, chunks_per_slice;
+    const int32_t *idx;
+    int d_ff, d, T, tpad, kcap, slices, chunks_per_slice;
     float *part;
 };
 
-template <int NT>
-__device__ __forceinline__ void dn_load(DnChunk<NT> &c, const DnArgs &a, const int *sidx, const uint16_t *Hrow,
-                                        int kb, int kb_local, int col) {
-    const int4 i0 = *reinterpret_cast<const int4 *>(sidx + kb_local);
-    const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb_local + 4);
-    const int n[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
-#pragma unroll
-    for (int j = 0; j < 8; ++j) c.w[j] = load8(a.wd + static_cast<size_t>(n[j]) * a.d + col);
-#pragma unroll
-    for (int tt = 0; tt < NT; ++tt) c.a[tt] = load16(Hrow + static_cast<size_t>(tt * 16) * a.kcap + kb);
-}
-
-// Slots at or past the count hold h = 0 in H, so the weights loaded for them contribute nothing.
+// Slots at or past the count hold h = 0 in H (the gate/up kernels write every slot below kcap), so the products
+// of their chunks are exact zeros and the kernel does not read the count; the epilogue skips whole slices past
+// it, so an empty list still gives y = x bit for bit.
 template <int NT>
 __device__ __forceinline__ void dn_mma(const DnChunk<NT> &c, rm_f32x4 (*acc)[4]) {
 #pragma unroll
@@ -427,7 +458,9 @@ __device__ __forceinline__ void dn_mma(const DnChunk<NT> &c, rm_f32x4 (*acc)[4])
 }
 
 // CPW: chunks per wave (a slice has 4 * CPW chunks); the chunk pipeline below is unrolled straight-line code.
-template <int NT, int CPW>
+// Load order: the slice's neuron indices, then the first chunks' H tiles (which do not depend on the indices),
+// then, once the indices are in LDS, the weights; the wave waits for memory once per pipeline stage.
+template <int NT, int CPW, bool kOneBlock>
 __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
     const int ct = blockIdx.x;
     const int s = blockIdx.y;
@@ -445,43 +478,68 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
     const int cps = a.chunks_per_slice;
     const int c_begin = s * cps;
     const int c_last = min(c_begin + cps, a.kcap / rm::kBfChunk) - 1;  // last chunk of the slice below kcap
+    const uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
 
-    // The slice's neuron indices, clamped into [0, d_ff), staged once in LDS: the waves read them with LDS
+    // The slice's neuron indices, clamped into [0, d_ff), are staged once in LDS: the waves read them with LDS
     // loads, which do not wait behind the weight loads in flight.
+    constexpr int kIdxPerThread = rm::kBfMaxChunksPerSlice * rm::kBfChunk / kDnThreads;
     __shared__ __attribute__((aligned(16))) int sidx[rm::kBfMaxChunksPerSlice * rm::kBfChunk];
-    for (int i = tid; i < cps * rm::kBfChunk; i += kDnThreads) {
-        const int slot = min(c_begin * rm::kBfChunk + i, a.d_ff - 1);
-        sidx[i] = a.idx ? clamp_neuron(a.idx[static_cast<size_t>(b) * a.d_ff + slot], a.d_ff) : slot;
+    int iv[kIdxPerThread];
+#pragma unroll
+    for (int q = 0; q < kIdxPerThread; ++q) {
+        const int i = min(tid + q * kDnThreads, cps * rm::kBfChunk - 1);
+        iv[q] = a.idx[static_cast<size_t>(b) * a.d_ff + min(c_begin * rm::kBfChunk + i, a.d_ff - 1)];
     }
-    const int cnt = a.idx ? clamp_count(a.count[b], a.max_count) : a.d_ff;
-    const int nchunks = (cnt + rm::kBfChunk - 1) / rm::kBfChunk;
-    const int c_end = min(c_begin + cps, nchunks);
+    __builtin_amdgcn_sched_barrier(0);  // the index loads go out first
+
+    // Chunk k of this wave is chunk c_begin + wave + 4 k of the slice, clamped to the slice (unconditional
+    // loads; the matrix-core step of a chunk past the list is skipped).
+    auto chunk_of = [&](int k) { return min(c_begin + wave + k * kDnWaves, c_last); };
+    auto load_h = [&](DnChunk<NT> &cc, int k, int t0) {
+        const int ce = chunk_of(k);
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)  // chunk-major H: 16 tokens x 64 bytes, one contiguous kilobyte
+            cc.a[tt] = load16(Hb + (static_cast<size_t>(ce) * a.tpad + t0 + tt * 16 + nn) * rm::kBfChunk + grp * 8);
+    };
+    auto load_w = [&](DnChunk<NT> &cc, int k) {
+        const int kb = (chunk_of(k) - c_begin) * rm::kBfChunk + grp * 8;
+        const int4 i0 = *reinterpret_cast<const int4 *>(sidx + kb);
+        const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb + 4);
+        const int n[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cc.w[j] = load8(a.wd + static_cast<size_t>(n[j]) * a.d + col);
+    };
+
+    DnChunk<NT> cb[2];
+    load_h(cb[0], 0, 0);
+    if (CPW > 1) load_h(cb[1], 1, 0);
+    __builtin_amdgcn_sched_barrier(0);  // then the H tiles, before the wait for the indices
+#pragma unroll
+    for (int q = 0; q < kIdxPerThread; ++q) {
+        const int i = tid + q * kDnThreads;
+        if (i < cps * rm::kBfChunk) sidx[i] = clamp_neuron(iv[q], a.d_ff);
+    }
     __syncthreads();
 
     __shared__ rm_f32x4 red[kDnWaves][NT][4][64];
-    if (c_begin >= c_end) return;  // no neuron of this sample falls in the slice; the epilogue skips it
-
-    for (int t0 = 0; t0 < a.T; t0 += rm::kBfTokBlock) {
+    for (int t0 = 0;;) {
         rm_f32x4 acc[NT][4];
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
             for (int q = 0; q < 4; ++q) acc[tt][q] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 
-        const uint16_t *Hrow = a.H + (static_cast<size_t>(b) * a.tpad + t0 + nn) * a.kcap;
-        // Chunk loads are unconditional (chunk numbers clamped to the slice) and two deep: chunk k+2 is loaded
-        // into chunk k's registers right after chunk k's products are issued.
-        auto load_chunk = [&](DnChunk<NT> &cc, int k) {
-            const int ce = min(c_begin + wave + k * kDnWaves, c_last);
-            dn_load(cc, a, sidx, Hrow, ce * rm::kBfChunk + grp * 8, (ce - c_begin) * rm::kBfChunk + grp * 8, col);
-        };
-        DnChunk<NT> cb[2];
-        load_chunk(cb[0], 0);
-        if (CPW > 1) load_chunk(cb[1], 1);
+        // Two chunks in flight: chunk k + 2 is loaded into chunk k's registers right after chunk k's products.
+        load_w(cb[0], 0);
+        if (CPW > 1) load_w(cb[1], 1);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int k = 0; k < CPW; ++k) {
-            if (c_begin + wave + k * kDnWaves < c_end) dn_mma(cb[k & 1], acc);
-            if (k + 2 < CPW) load_chunk(cb[k & 1], k + 2);
+            if (c_begin + wave + k * kDnWaves <= c_last) dn_mma(cb[k & 1], acc);
+            if (k + 2 < CPW) {
+                load_h(cb[k & 1], k + 2, t0);
+                load_w(cb[k & 1], k + 2);
+            }
         }
 
 #pragma unroll
@@ -515,7 +573,11 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
                 }
             }
         }
+        t0 += rm::kBfTokBlock;
+        if (kOneBlock || t0 >= a.T) break;
         __syncthreads();
+        load_h(cb[0], 0, t0);
+        if (CPW > 1) load_h(cb[1], 1, t0);
     }
 }
 
@@ -529,11 +591,20 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
     const dim3 block(kGuThreads);
     const dim3 grid(p.gate_blocks, p.B);
     if (p.gate_groups == 1) {
-        switch (p.d / 256) {  // the plan picks the direct kernel only for d = 256, 512, 1024, 2048
-            case 1: hipLaunchKernelGGL((gateup_direct_kernel<NT, 1>), grid, block, 0, st, a); break;
-            case 2: hipLaunchKernelGGL((gateup_direct_kernel<NT, 2>), grid, block, 0, st, a); break;
-            case 4: hipLaunchKernelGGL((gateup_direct_kernel<NT, 4>), grid, block, 0, st, a); break;
-            default: hipLaunchKernelGGL((gateup_direct_kernel<NT, 8>), grid, block, 0, st, a); break;
+        if (p.T <= rm::kBfTokBlock) {
+            switch (p.d / 256) {  // the plan picks the direct kernel only for d = 256, 512, 1024, 2048
+                case 1: hipLaunchKernelGGL((gateup_direct_kernel<NT, 1, true>), grid, block, 0, st, a); break;
+                case 2: hipLaunchKernelGGL((gateup_direct_kernel<NT, 2, true>), grid, block, 0, st, a); break;
+                case 4: hipLaunchKernelGGL((gateup_direct_kernel<NT, 4, true>), grid, block, 0, st, a); break;
+                default: hipLaunchKernelGGL((gateup_direct_kernel<NT, 8, true>), grid, block, 0, st, a); break;
+            }
+        } else {
+            switch (p.d / 256) {
+                case 1: hipLaunchKernelGGL((gateup_direct_kernel<NT, 1, false>), grid, block, 0, st, a); break;
+                case 2: hipLaunchKernelGGL((gateup_direct_kernel<NT, 2, false>), grid, block, 0, st, a); break;
+                case 4: hipLaunchKernelGGL((gateup_direct_kernel<NT, 4, false>), grid, block, 0, st, a); break;
+                default: hipLaunchKernelGGL((gateup_direct_kernel<NT, 8, false>), grid, block, 0, st, a); break;
+            }
         }
         return;
     }
@@ -595,15 +666,12 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
     return e;
 }
 
-hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
-                            hipStream_t st) {
+hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, void *ws, hipStream_t st) {
     char *base = static_cast<char *>(ws);
     DnArgs a;
     a.H = reinterpret_cast<const uint16_t *>(base + p.off_h);
     a.wd = static_cast<const uint16_t *>(w_down);
     a.idx = idx;
-    a.count = count;
-    a.max_count = p.max_count;
     a.d_ff = p.d_ff;
     a.d = p.d;
     a.T = p.T;
@@ -614,11 +682,17 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
     a.part = reinterpret_cast<float *>(base + p.off_part);
     const dim3 grid(p.ncol, p.slices, p.B), block(kDnThreads);
     profile_before(RM_KERNEL_DOWN, st);
-#define RM_DOWN(NT)                                                                                 \
-    switch (p.slice_units / kDnWaves) {                                                            \
-        case 1: hipLaunchKernelGGL((down_bf16_kernel<NT, 1>), grid, block, 0, st, a); break;       \
-        case 2: hipLaunchKernelGGL((down_bf16_kernel<NT, 2>), grid, block, 0, st, a); break;       \
-        default: hipLaunchKernelGGL((down_bf16_kernel<NT, 4>), grid, block, 0, st, a); break;      \
+#define RM_DOWN_CPW(NT, ONE)                                                                              \
+    switch (p.slice_units / kDnWaves) {                                                                  \
+        case 1: hipLaunchKernelGGL((down_bf16_kernel<NT, 1, ONE>), grid, block, 0, st, a); break;        \
+        case 2: hipLaunchKernelGGL((down_bf16_kernel<NT, 2, ONE>), grid, block, 0, st, a); break;        \
+        default: hipLaunchKernelGGL((down_bf16_kernel<NT, 4, ONE>), grid, block, 0, st, a); break;       \
+    }
+#define RM_DOWN(NT)                          \
+    if (p.T <= rm::kBfTokBlock) {            \
+        RM_DOWN_CPW(NT, true)                \
+    } else {                                 \
+        RM_DOWN_CPW(NT, false)               \
     }
     switch (token_tiles(p.T)) {
         case 1: RM_DOWN(1) break;
@@ -627,6 +701,7 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
         default: RM_DOWN(4) break;
     }
 #undef RM_DOWN
+#undef RM_DOWN_CPW
     hipError_t e = hipGetLastError();
     profile_after(RM_KERNEL_DOWN, st);
     return e;

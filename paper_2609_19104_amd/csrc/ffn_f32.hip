@@ -26,7 +26,7 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
     const int b = blockIdx.y;
     const int slot0 = blockIdx.x * rm::kF32NeurPerBlk;
     const int lane = threadIdx.x;
-    int cnt = idx ? count[b] : d_ff;
+    int cnt = count[b];
     cnt = cnt < 0 ? 0 : (cnt > max_count ? max_count : cnt);
     if (slot0 >= cnt) return;  // the down projection never reads slots past the list
 
@@ -34,7 +34,7 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
     const int cl = lane & 7;  // 16-byte column group of each 128-byte step
     const int slot = slot0 + r;
     const bool valid = slot < cnt;
-    const int n = valid ? (idx ? clamp_neuron(idx[static_cast<size_t>(b) * d_ff + slot], d_ff) : slot) : 0;
+    const int n = valid ? clamp_neuron(idx[static_cast<size_t>(b) * d_ff + slot], d_ff) : 0;
     const float *grow = wg + static_cast<size_t>(n) * d;
     const float *urow = wu + static_cast<size_t>(n) * d;
     const float *xb = xn + static_cast<size_t>(b) * T * d;
@@ -104,7 +104,7 @@ __global__ __launch_bounds__(kWave) void down_f32_kernel(
     const int s = blockIdx.y;
     const int b = blockIdx.z;
     const int lane = threadIdx.x;
-    int cnt = idx ? count[b] : d_ff;
+    int cnt = count[b];
     cnt = cnt < 0 ? 0 : (cnt > max_count ? max_count : cnt);
     const int k_begin = s * slice_neurons;
     const int k_end = min(k_begin + slice_neurons, cnt);
@@ -112,7 +112,7 @@ __global__ __launch_bounds__(kWave) void down_f32_kernel(
     const int c = col0 + lane * 4;
     const bool colok = c < d;
     const float *Hb = H + static_cast<size_t>(b) * tpad * kcap;
-    const int32_t *idxb = idx ? idx + static_cast<size_t>(b) * d_ff : nullptr;
+    const int32_t *idxb = idx + static_cast<size_t>(b) * d_ff;
     float *P = part + (static_cast<size_t>(b) * slices + s) * static_cast<size_t>(T) * d;
 
     if (k_begin < k_end) {
@@ -122,7 +122,7 @@ __global__ __launch_bounds__(kWave) void down_f32_kernel(
 #pragma unroll
             for (int t = 0; t < rm::kF32TokBlock; ++t) acc[t] = make_float4(0.f, 0.f, 0.f, 0.f);
             for (int k = k_begin; k < k_end; ++k) {
-                const int n = idxb ? clamp_neuron(idxb[k], d_ff) : k;
+                const int n = clamp_neuron(idxb[k], d_ff);
                 float4 w4 = make_float4(0.f, 0.f, 0.f, 0.f);
                 if (colok) w4 = *reinterpret_cast<const float4 *>(wd + static_cast<size_t>(n) * d + c);
 #pragma unroll

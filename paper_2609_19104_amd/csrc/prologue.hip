@@ -1,10 +1,13 @@
 // First layer's FFN input: xn = x * g (or x without a norm) in the FFN kernels' input dtype, plus the row's
-// sum of squares for the RMSNorm factor.
+// sum of squares for the RMSNorm factor.  Also the identity index lists with which the dense reference runs the
+// sparse kernels.
 //
 // The action expert normalizes each FFN input (the layer is x + FFN(RMSNorm(x)) with RMSNorm(x) =
 // x / sqrt(mean(x^2) + eps) * g).  The per-token factor is applied by the gate/up kernel after its matrix-core
 // products, so xn itself stays unscaled; the row's sum of squares is reduced here in a fixed order (lane
 // butterfly, then waves 0..3).  One workgroup per token row.
+#include <algorithm>
+
 #include "rm_internal.h"
 
 namespace {
@@ -51,9 +54,28 @@ __global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restr
     if (tid == 0) ssq[row] = (wave_ss[0] + wave_ss[1]) + (wave_ss[2] + wave_ss[3]);
 }
 
+__global__ __launch_bounds__(kThreads) void identity_lists_kernel(int32_t *idx, int32_t *count, int d_ff, int B) {
+    const size_t n = static_cast<size_t>(B) * d_ff;
+    for (size_t i = static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x; i < n;
+         i += static_cast<size_t>(gridDim.x) * kThreads)
+        idx[i] = static_cast<int32_t>(i % d_ff);
+    if (blockIdx.x == 0 && threadIdx.x < B) count[threadIdx.x] = d_ff;
+    for (int b = kThreads + threadIdx.x; blockIdx.x == 0 && b < B; b += kThreads) count[b] = d_ff;
+}
+
 }  // namespace
 
 namespace rm {
+
+hipError_t launch_identity_lists(const Plan &p, void *ws, hipStream_t st) {
+    char *base = static_cast<char *>(ws);
+    int32_t *idx = reinterpret_cast<int32_t *>(base + p.off_ident);
+    int32_t *count = reinterpret_cast<int32_t *>(base + p.off_ident_count);
+    const size_t n = static_cast<size_t>(p.B) * p.d_ff;
+    const int blocks = static_cast<int>(std::min<size_t>((n + kThreads - 1) / kThreads, 1024));
+    hipLaunchKernelGGL(identity_lists_kernel, dim3(blocks), dim3(kThreads), 0, st, idx, count, p.d_ff, p.B);
+    return hipGetLastError();
+}
 
 hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, void *ws, hipStream_t st) {
     char *base = static_cast<char *>(ws);

@@ -104,8 +104,8 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
     hipError_t e = rm::launch_prologue(p, x, w[0].norm_g, ws, st);
     if (e != hipSuccess) return hip_fail(e, "prologue launch");
     for (int l = 0; l < L; ++l) {
-        const int32_t *il = idx ? idx + l * list_stride : nullptr;
-        const int32_t *cl = count ? count + static_cast<size_t>(l) * p.B : nullptr;
+        const int32_t *il = idx + l * list_stride;
+        const int32_t *cl = count + static_cast<size_t>(l) * p.B;
         const bool bf = p.wdtype == RM_BF16;
         const bool norm = w[l].norm_g != nullptr;
         e = bf ? rm::launch_gateup_bf16(p, w[l].w_gate, w[l].w_up, il, cl, norm, ws, st)
@@ -114,7 +114,7 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
         const bool next = l + 1 < L;
         const float *g_next = next ? w[l + 1].norm_g : nullptr;
         const float *xin = l == 0 ? x : y;
-        e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, cl, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
+        e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
         if (e != hipSuccess) return hip_fail(e, "down launch");
         e = rm::launch_epilogue(p, cl, xin, y, g_next, next, ws, st);
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
@@ -189,6 +189,10 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     off = align_up(off + static_cast<size_t>(B) * q.slices * static_cast<size_t>(T) * s->d * 4, 256);
     q.off_ssq = off;
     off = align_up(off + static_cast<size_t>(B) * T * sizeof(float), 256);
+    q.off_ident = off;
+    off = align_up(off + static_cast<size_t>(B) * s->d_ff * sizeof(int32_t), 256);
+    q.off_ident_count = off;
+    off = align_up(off + static_cast<size_t>(B) * sizeof(int32_t), 256);
     q.total = off;
     *p = q;
     return RM_OK;
@@ -273,7 +277,12 @@ RM_EXPORT rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_w
     if (st != RM_OK) return st;
     st = check_layer(w, 0);
     if (st != RM_OK) return st;
-    st = run_layers(p, w, 1, x, y, nullptr, nullptr, 0, ws, static_cast<hipStream_t>(stream));
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    const hipError_t e = rm::launch_identity_lists(p, ws, hs);
+    if (e != hipSuccess) return hip_fail(e, "identity list launch");
+    char *base = static_cast<char *>(ws);
+    st = run_layers(p, w, 1, x, y, reinterpret_cast<const int32_t *>(base + p.off_ident),
+                    reinterpret_cast<const int32_t *>(base + p.off_ident_count), 0, ws, hs);
     return st == RM_OK ? ok() : st;
 }
 

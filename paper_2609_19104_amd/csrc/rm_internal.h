@@ -39,9 +39,11 @@ struct Plan {
     int ncol = 0;        // column tiles
     int slices = 0;      // K-slices per column tile (down partial sums)
     int slice_units = 0; // bf16: 32-neuron chunks per slice; f32: neurons per slice
-    // Workspace: xn [B][T][d] (bf16 or f32), H [B][tpad][kcap] (bf16 or f32), partials f32 [B][slices][T][d],
-    // ssq f32 [B][T] (per-token sums of squares of the FFN input, for the RMSNorm factor).
-    size_t off_xn = 0, off_h = 0, off_part = 0, off_ssq = 0, total = 0;
+    // Workspace: xn [B][T][d] (bf16 or f32); H (bf16: [B][kcap / 32][tpad][32], chunk-major; f32:
+    // [B][tpad][kcap]); partials f32 [B][slices][T][d]; ssq f32 [B][T] (per-token sums of squares of the FFN
+    // input, for the RMSNorm factor); and, for the dense reference, the lists 0 .. d_ff-1 int32 [B][d_ff] and
+    // their counts int32 [B].
+    size_t off_xn = 0, off_h = 0, off_part = 0, off_ssq = 0, off_ident = 0, off_ident_count = 0, total = 0;
 };
 
 rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p);
@@ -52,6 +54,10 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
 
 hipError_t launch_mask_compact(const uint8_t *mask, int n_masks, int d_ff, int32_t *idx, int32_t *count,
                                hipStream_t st);
+
+// Index lists 0 .. d_ff-1 and counts d_ff for every sample in the workspace (the dense reference runs the
+// sparse kernels on them).
+hipError_t launch_identity_lists(const Plan &p, void *ws, hipStream_t st);
 
 // First layer's FFN input: xn = x * g (or x) in the FFN input dtype, and (norm only) its per-token sums of
 // squares.
@@ -64,9 +70,9 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
 hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
                              const int32_t *count, bool norm, void *ws, hipStream_t st);
 
-// Down projection of the listed neurons: per-K-slice float32 partials of H W_down[idx] in the workspace.
-hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
-                            hipStream_t st);
+// Down projection of the listed neurons: per-K-slice float32 partials of H W_down[idx] in the workspace.  The
+// bf16 form needs no count: H is zero in every slot past the list.
+hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, void *ws, hipStream_t st);
 hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
                            hipStream_t st);
 

@@ -419,6 +419,97 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
     }
 }
 
+// ------------------------------------------------------------------------------------------ gate / up, pipelined
+
+// For long lists (T <= 64, d = 256 NCH with NCH in {1, 2, 4, 8}).  NG groups of 8 neurons per workgroup as in the staged
+// kernel; chunk c of the FFN input (64 token rows x 256 columns) is shared by the groups through LDS.  Every
+// wave loads its share of chunk c's input (whole 512-byte rows) together with its weights for chunk c, P
+// chunks ahead, input first.  A wave's memory counter completes in issue order, so waiting for chunk c leaves
+// chunks c+1 .. c+P-1 in flight; and the input of a chunk never waits behind weights of later chunks, whose
+// deep queue would otherwise delay it by their whole transfer time.  The input goes through registers into a
+// double-buffered LDS tile, with one barrier per chunk.
+template <int NG, int NCH>
+__global__ __launch_bounds__(kGuThreads) void gateup_pipe_kernel(GuArgs a) {
+    constexpr int NT = 4;
+    constexpr int DS = kGuWaves / NG;                      // waves per neuron group (d split within a chunk)
+    constexpr int SPW = kChunkSteps / DS;                  // K steps per wave and chunk
+    constexpr int P0 = NG == 8 ? 3 : (NG == 4 ? 4 : 6);  // chunks in flight (registers: P (16 + 4 SPW))
+    constexpr int P = P0 < NCH ? P0 : NCH;
+    const int b = blockIdx.y;
+    const int blk0 = blockIdx.x * 8 * NG;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int g = wave / DS;
+    const int part = wave % DS;
+    const int r = lane & 15;
+    const int grp = lane >> 4;
+    const int n = lane_neuron(a, b, blk0 + g * 8 + (r & 7));
+    const int cnt = clamp_count(a.count[b], a.max_count);
+    uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
+    const uint16_t *wrow = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(n) * a.d + part * SPW * 32 + grp * 8;
+
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][64 * kRowPitch];
+    __shared__ float rn[64];
+    static_assert(sizeof(rm_f32x4) * NG * DS * NT * 64 <= sizeof(xs), "reduction tiles must fit the input tile");
+    auto red = [&](int gg, int w2, int tt, int l) -> rm_f32x4 & {
+        return reinterpret_cast<rm_f32x4 *>(&xs[0][0])[((gg * DS + w2) * NT + tt) * 64 + l];
+    };
+
+    // Step c processes column chunk (c + blockIdx.x) mod NCH: if every workgroup swept the chunks in the same
+    // order, all of them would read the same 512-byte window of their rows at once and load a few memory
+    // channels only (measured: about a quarter less bandwidth than with rotated orders).
+    const int rot = blockIdx.x & (NCH - 1);
+    // Step c into register slot c % P: the input pieces e = tid + 512 q (row e / 32, 16-byte piece e % 32),
+    // then the weights.
+    rm_u32x4 xv[P][4], w[P][SPW];
+    auto load_chunk = [&](int c) {
+        const int col = ((c + rot) & (NCH - 1)) * kChunkCols;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = tid + q * kGuThreads;
+            const int t = min(e >> 5, a.T - 1);  // rows past T repeat the last token
+            xv[c % P][q] = load16(a.xn + (static_cast<size_t>(b) * a.T + t) * a.d + col + (e & 31) * 8);
+        }
+#pragma unroll
+        for (int i = 0; i < SPW; ++i) w[c % P][i] = load16(wrow + col + i * 32);
+    };
+#pragma unroll
+    for (int c = 0; c < P; ++c) load_chunk(c);
+
+    rm_f32x4 acc[NT];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) acc[tt] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        // Buffer c & 1 was last read in chunk c - 2, before every wave passed chunk c - 1's barrier.
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = tid + q * kGuThreads;
+            *reinterpret_cast<rm_u32x4 *>(&xs[c & 1][(e >> 5) * kRowPitch + (e & 31) * 8]) = xv[c % P][q];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < SPW; ++i)
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) {
+                const rm_u32x4 bx = *reinterpret_cast<const rm_u32x4 *>(
+                    &xs[c & 1][(tt * 16 + r) * kRowPitch + (part * SPW + i) * 32 + grp * 8]);
+                acc[tt] = mfma_bf16(w[c % P][i], bx, acc[tt]);
+            }
+        if (c + P < NCH) load_chunk(c + P);
+    }
+    load_rnorm(a, b, 0, rn);
+    __syncthreads();  // every wave is done with the input tiles before they hold the reduction
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) red(g, part, tt, lane) = acc[tt];
+    __syncthreads();
+#pragma unroll
+    for (int gg = 0; gg < NG; ++gg)
+        gu_store_h<NT>(a, Hb, [&](int w2, int tt, int l) -> const rm_f32x4 & { return red(gg, w2, tt, l); }, DS, 0,
+                       blk0 + gg * 8, cnt, rn);
+}
+
 // ------------------------------------------------------------------------------------------ down
 
 template <int NT>
@@ -609,6 +700,22 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
         return;
     }
     const int nch = (p.d + kChunkCols - 1) / kChunkCols;
+    if (p.T <= rm::kBfTokBlock && p.d % kChunkCols == 0 && (nch == 1 || nch == 2 || nch == 4 || nch == 8)) {
+#define RM_PIPE(NG)                                                                                  \
+    switch (nch) {                                                                                   \
+        case 1: hipLaunchKernelGGL((gateup_pipe_kernel<NG, 1>), grid, block, 0, st, a); break;      \
+        case 2: hipLaunchKernelGGL((gateup_pipe_kernel<NG, 2>), grid, block, 0, st, a); break;      \
+        case 4: hipLaunchKernelGGL((gateup_pipe_kernel<NG, 4>), grid, block, 0, st, a); break;      \
+        default: hipLaunchKernelGGL((gateup_pipe_kernel<NG, 8>), grid, block, 0, st, a); break;     \
+    }
+        switch (p.gate_groups) {
+            case 2: RM_PIPE(2) break;
+            case 4: RM_PIPE(4) break;
+            default: RM_PIPE(8) break;
+        }
+#undef RM_PIPE
+        return;
+    }
 #define RM_STAGED(NG)                                                                                          \
     switch (nch) {                                                                                             \
         case 1: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 1>), grid, block, 0, st, a); break; \

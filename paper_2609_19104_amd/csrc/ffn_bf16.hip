@@ -57,7 +57,7 @@ __device__ __forceinline__ int clamp_count(int c, int max_count) { return c < 0 
 struct GuArgs {
     const uint16_t *wg, *wu, *xn;
     const int32_t *idx, *count;
-    const float *ssq;  // [B][T] per-token sums of squares, or null (no norm)
+    const float *ssq;  // [B][T][d / 256] per-token partial sums of squares, or null (no norm)
     float eps;
     int max_count, d_ff, d, T, tpad, kcap;
     uint16_t *H;
@@ -68,8 +68,7 @@ __device__ __forceinline__ void load_rnorm(const GuArgs &a, int b, int t0, float
     const int t = t0 + static_cast<int>(threadIdx.x);
     if (threadIdx.x < 64) {
         float r = 1.0f;
-        if (a.ssq != nullptr && t < a.T)
-            r = 1.0f / sqrtf(a.ssq[static_cast<size_t>(b) * a.T + t] / static_cast<float>(a.d) + a.eps);
+        if (a.ssq != nullptr && t < a.T) r = rm_token_rnorm(a.ssq, b * a.T + t, a.d, a.eps);
         rn[threadIdx.x] = r;
     }
 }
@@ -421,19 +420,21 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
 
 // ------------------------------------------------------------------------------------------ gate / up, pipelined
 
-// For long lists (T <= 64, d = 256 NCH with NCH in {1, 2, 4, 8}).  NG groups of 8 neurons per workgroup as in the staged
-// kernel; chunk c of the FFN input (64 token rows x 256 columns) is shared by the groups through LDS.  Every
-// wave loads its share of chunk c's input (whole 512-byte rows) together with its weights for chunk c, P
-// chunks ahead, input first.  A wave's memory counter completes in issue order, so waiting for chunk c leaves
-// chunks c+1 .. c+P-1 in flight; and the input of a chunk never waits behind weights of later chunks, whose
-// deep queue would otherwise delay it by their whole transfer time.  The input goes through registers into a
-// double-buffered LDS tile, with one barrier per chunk.
+// For long lists (T <= 64, d = 256 NCH with NCH in {1, 2, 4, 8}).  NG groups of 8 neurons per workgroup as
+// in the staged kernel; column chunk c of the FFN input (64 token rows x 256 columns) is shared by the groups
+// through LDS.  Every wave loads its share of chunk c's input (whole 512-byte rows) together with its weights
+// for chunk c, P chunks ahead, input first.  A wave's memory counter completes in issue order, so waiting for
+// chunk c leaves chunks c+1 .. c+P-1 in flight; and the input of a chunk never waits behind weights of later
+// chunks, whose deep queue would otherwise delay it by their whole transfer time.  The input goes through
+// registers into a double-buffered LDS tile, with one barrier per chunk.  With NG = 2 (more workgroups than
+// compute units) the register budget allows two workgroups per compute unit (4 waves per SIMD), so the second
+// half of the grid does not wait for the first.
 template <int NG, int NCH>
-__global__ __launch_bounds__(kGuThreads) void gateup_pipe_kernel(GuArgs a) {
+__global__ __launch_bounds__(kGuThreads, NG == 2 ? 4 : 2) void gateup_pipe_kernel(GuArgs a) {
     constexpr int NT = 4;
     constexpr int DS = kGuWaves / NG;                      // waves per neuron group (d split within a chunk)
     constexpr int SPW = kChunkSteps / DS;                  // K steps per wave and chunk
-    constexpr int P0 = NG == 8 ? 3 : (NG == 4 ? 4 : 6);  // chunks in flight (registers: P (16 + 4 SPW))
+    constexpr int P0 = NG == 8 ? 3 : (NG == 4 ? 4 : 3);  // chunks in flight (registers: P (16 + 4 SPW))
     constexpr int P = P0 < NCH ? P0 : NCH;
     const int b = blockIdx.y;
     const int blk0 = blockIdx.x * 8 * NG;

@@ -87,8 +87,7 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
             float h = 0.0f;
             if (cl < nt) {
                 float rn = 1.0f;
-                if (ssq != nullptr)
-                    rn = 1.0f / sqrtf(ssq[static_cast<size_t>(b) * T + t0 + cl] / static_cast<float>(d) + eps);
+                if (ssq != nullptr) rn = rm_token_rnorm(ssq, b * T + t0 + cl, d, eps);
                 h = rm_silu(gs * rn) * (us * rn);
             }
             Hb[static_cast<size_t>(t0 + cl) * kcap + slot] = h;

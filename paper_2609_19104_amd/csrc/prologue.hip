@@ -1,30 +1,31 @@
 // First layer's FFN input: xn = x * g (or x without a norm) in the FFN kernels' input dtype, plus the row's
-// sum of squares for the RMSNorm factor.  Also the identity index lists with which the dense reference runs the
+// sums of squares for the RMSNorm factor.  Also the identity index lists with which the dense reference runs the
 // sparse kernels.
 //
 // The action expert normalizes each FFN input (the layer is x + FFN(RMSNorm(x)) with RMSNorm(x) =
 // x / sqrt(mean(x^2) + eps) * g).  The per-token factor is applied by the gate/up kernel after its matrix-core
-// products, so xn itself stays unscaled; the row's sum of squares is reduced here in a fixed order (lane
-// butterfly, then waves 0..3).  One workgroup per token row.
+// products, so xn itself stays unscaled.  One wave per (token row, block of 256 columns), each lane a float4:
+// the row's sum of squares is kept as one partial per column block (lane butterfly, fixed order), which the
+// gate/up kernel adds in block order.
 #include <algorithm>
 
 #include "rm_internal.h"
 
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 64;
 
 template <bool kBf16Out>
 __global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restrict__ x,
-                                                            const float *__restrict__ g, int d,
+                                                            const float *__restrict__ g, int d, int nblk,
                                                             void *__restrict__ xn, float *__restrict__ ssq) {
-    const int row = blockIdx.x;
-    const int tid = threadIdx.x;
-
-    const float *xr = x + static_cast<size_t>(row) * d;
+    const int row = blockIdx.x / nblk;
+    const int blk = blockIdx.x - row * nblk;
+    const int c = blk * rm::kRowBlock + static_cast<int>(threadIdx.x) * 4;
+    const size_t o = static_cast<size_t>(row) * d + c;
     float ss = 0.0f;
-    for (int c = tid * 4; c < d; c += kThreads * 4) {
-        float4 v = *reinterpret_cast<const float4 *>(xr + c);
+    if (c < d) {
+        float4 v = *reinterpret_cast<const float4 *>(x + o);
         if (g != nullptr) {
             ss = fmaf(v.x, v.x, ss);
             ss = fmaf(v.y, v.y, ss);
@@ -36,7 +37,6 @@ __global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restr
             v.z *= gv.z;
             v.w *= gv.w;
         }
-        const size_t o = static_cast<size_t>(row) * d + c;
         if constexpr (kBf16Out) {
             uint2 packed;
             packed.x = rm_f32_to_bf16_bits(v.x) | (rm_f32_to_bf16_bits(v.y) << 16);
@@ -48,19 +48,15 @@ __global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restr
     }
     if (g == nullptr) return;
     for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-    __shared__ float wave_ss[kThreads / 64];
-    if ((tid & 63) == 0) wave_ss[tid >> 6] = ss;
-    __syncthreads();
-    if (tid == 0) ssq[row] = (wave_ss[0] + wave_ss[1]) + (wave_ss[2] + wave_ss[3]);
+    if (threadIdx.x == 0) ssq[blockIdx.x] = ss;  // [row][blk]
 }
 
-__global__ __launch_bounds__(kThreads) void identity_lists_kernel(int32_t *idx, int32_t *count, int d_ff, int B) {
+__global__ __launch_bounds__(256) void identity_lists_kernel(int32_t *idx, int32_t *count, int d_ff, int B) {
     const size_t n = static_cast<size_t>(B) * d_ff;
-    for (size_t i = static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x; i < n;
-         i += static_cast<size_t>(gridDim.x) * kThreads)
+    const size_t step = static_cast<size_t>(gridDim.x) * 256;
+    for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += step)
         idx[i] = static_cast<int32_t>(i % d_ff);
-    if (blockIdx.x == 0 && threadIdx.x < B) count[threadIdx.x] = d_ff;
-    for (int b = kThreads + threadIdx.x; blockIdx.x == 0 && b < B; b += kThreads) count[b] = d_ff;
+    for (int b = threadIdx.x; blockIdx.x == 0 && b < B; b += 256) count[b] = d_ff;
 }
 
 }  // namespace
@@ -72,8 +68,8 @@ hipError_t launch_identity_lists(const Plan &p, void *ws, hipStream_t st) {
     int32_t *idx = reinterpret_cast<int32_t *>(base + p.off_ident);
     int32_t *count = reinterpret_cast<int32_t *>(base + p.off_ident_count);
     const size_t n = static_cast<size_t>(p.B) * p.d_ff;
-    const int blocks = static_cast<int>(std::min<size_t>((n + kThreads - 1) / kThreads, 1024));
-    hipLaunchKernelGGL(identity_lists_kernel, dim3(blocks), dim3(kThreads), 0, st, idx, count, p.d_ff, p.B);
+    const int blocks = static_cast<int>(std::min<size_t>((n + 255) / 256, 1024));
+    hipLaunchKernelGGL(identity_lists_kernel, dim3(blocks), dim3(256), 0, st, idx, count, p.d_ff, p.B);
     return hipGetLastError();
 }
 
@@ -81,11 +77,12 @@ hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, v
     char *base = static_cast<char *>(ws);
     void *xn = base + p.off_xn;
     float *ssq = reinterpret_cast<float *>(base + p.off_ssq);
-    const int rows = p.B * p.T;
+    const int nblk = (p.d + kRowBlock - 1) / kRowBlock;
+    const dim3 grid(p.B * p.T * nblk);
     if (p.wdtype == RM_BF16)
-        hipLaunchKernelGGL(prologue_kernel<true>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.d, xn, ssq);
+        hipLaunchKernelGGL(prologue_kernel<true>, grid, dim3(kThreads), 0, st, x, norm_g, p.d, nblk, xn, ssq);
     else
-        hipLaunchKernelGGL(prologue_kernel<false>, dim3(rows), dim3(kThreads), 0, st, x, norm_g, p.d, xn, ssq);
+        hipLaunchKernelGGL(prologue_kernel<false>, grid, dim3(kThreads), 0, st, x, norm_g, p.d, nblk, xn, ssq);
     return hipGetLastError();
 }
 

@@ -180,6 +180,8 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         h_elem = 4;
     }
     if (q.slices > 65535) return fail(RM_ERR_SHAPE, "launch grid too large");
+    if (static_cast<long long>(B) * T * ceil_div(s->d, kRowBlock) > 0x7fffffffLL)
+        return fail(RM_ERR_SHAPE, "B=%d x T=%d rows are too many for one launch", B, T);
     size_t off = 0;
     q.off_xn = off;
     off = align_up(off + static_cast<size_t>(B) * T * s->d * xn_elem, 256);
@@ -188,7 +190,7 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.off_part = off;
     off = align_up(off + static_cast<size_t>(B) * q.slices * static_cast<size_t>(T) * s->d * 4, 256);
     q.off_ssq = off;
-    off = align_up(off + static_cast<size_t>(B) * T * sizeof(float), 256);
+    off = align_up(off + static_cast<size_t>(B) * T * ceil_div(s->d, kRowBlock) * sizeof(float), 256);
     q.off_ident = off;
     off = align_up(off + static_cast<size_t>(B) * s->d_ff * sizeof(int32_t), 256);
     q.off_ident_count = off;
@@ -218,6 +220,8 @@ RM_EXPORT rm_status rm_mask_compact(const uint8_t *mask, int32_t n_masks, int32_
     if (!mask || !idx || !count) return fail(RM_ERR_INVALID_ARG, "mask, idx or count is NULL");
     if (n_masks <= 0 || d_ff <= 0) return fail(RM_ERR_INVALID_ARG, "n_masks=%d and d_ff=%d must be positive", n_masks, d_ff);
     if (!aligned(idx, 4) || !aligned(count, 4)) return fail(RM_ERR_ALIGN, "idx and count must be 4-byte aligned");
+    if (static_cast<long long>(n_masks) * ((d_ff + 1023) / 1024) > 0x7fffffffLL)
+        return fail(RM_ERR_SHAPE, "n_masks=%d x d_ff=%d is too large for one launch", n_masks, d_ff);
     const size_t mbytes = static_cast<size_t>(n_masks) * d_ff;
     if (ranges_overlap(mask, mbytes, idx, mbytes * 4) || ranges_overlap(mask, mbytes, count, n_masks * 4u) ||
         ranges_overlap(idx, mbytes * 4, count, n_masks * 4u))

@@ -22,6 +22,10 @@ constexpr int kBfColTile = 64;      // output columns per down workgroup (16 lan
 constexpr int kBfWaves = 4;
 constexpr int kBfMaxChunksPerSlice = 16;  // down: a slice's indices (16 x 32) are staged in 2 KB of LDS
 
+// Prologue / epilogue: one wave per (token row, block of 256 columns); the per-token sums of squares of the FFN
+// input are kept as one partial sum per column block.
+constexpr int kRowBlock = 256;
+
 // f32 path: vector ALU.
 constexpr int kF32TokBlock = 8;     // tokens per register block
 constexpr int kF32NeurPerBlk = 8;   // neurons per gate/up wave (8 lanes per neuron row)
@@ -40,9 +44,9 @@ struct Plan {
     int slices = 0;      // K-slices per column tile (down partial sums)
     int slice_units = 0; // bf16: 32-neuron chunks per slice; f32: neurons per slice
     // Workspace: xn [B][T][d] (bf16 or f32); H (bf16: [B][kcap / 32][tpad][32], chunk-major; f32:
-    // [B][tpad][kcap]); partials f32 [B][slices][T][d]; ssq f32 [B][T] (per-token sums of squares of the FFN
-    // input, for the RMSNorm factor); and, for the dense reference, the lists 0 .. d_ff-1 int32 [B][d_ff] and
-    // their counts int32 [B].
+    // [B][tpad][kcap]); partials f32 [B][slices][T][d]; ssq f32 [B][T][ceil(d / 256)] (per-token sums of squares
+    // of the FFN input by column block, for the RMSNorm factor); and, for the dense reference, the lists
+    // 0 .. d_ff-1 int32 [B][d_ff] and their counts int32 [B].
     size_t off_xn = 0, off_h = 0, off_part = 0, off_ssq = 0, off_ident = 0, off_ident_count = 0, total = 0;
 };
 
@@ -103,6 +107,16 @@ __device__ __forceinline__ uint32_t rm_f32_to_bf16_bits(float f) {
 }
 
 __device__ __forceinline__ float rm_bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// RMSNorm factor of token row `row` (= b * T + t): 1 / sqrt(mean of squares + eps), from the row's partial sums
+// of squares by 256-column block, added in block order.
+__device__ __forceinline__ float rm_token_rnorm(const float *ssq, int row, int d, float eps) {
+    const int nblk = (d + rm::kRowBlock - 1) / rm::kRowBlock;
+    const float *p = ssq + static_cast<size_t>(row) * nblk;
+    float s = p[0];
+    for (int k = 1; k < nblk; ++k) s += p[k];
+    return 1.0f / sqrtf(s / static_cast<float>(d) + eps);
+}
 
 // SiLU(z) = z / (1 + e^-z); e^-z overflows to +inf for very negative z, giving -0, never NaN.
 __device__ __forceinline__ float rm_silu(float z) { return z / (1.0f + expf(-z)); }

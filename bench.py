@@ -143,8 +143,9 @@ class Setup:
 
 
 def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
-    """Time `steps` steps after `warmup` untimed ones.  With hook=True, also record HIP events around every
-    gate/up and down launch (on the launch stream) and return their average durations in microseconds."""
+    """Time `steps` steps after `warmup` untimed ones.  With hook=True, also hand the library a pair of HIP events
+    for every gate/up and down launch (it launches them with hipExtLaunchKernel, which stamps the kernel's own
+    start and end on its stream) and return their average durations in microseconds."""
     import torch
     rm = setup.rm
     for i in range(warmup):

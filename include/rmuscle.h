@@ -116,10 +116,10 @@ rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights 
 rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
                            const float *x, float *y, void *ws, size_t ws_bytes, void *stream);
 
-/* Measurement hook.  Arms two hipEvent_t (begin, end) to be recorded on the call's stream immediately before
- * and after the next launch of the named kernel by this thread; the hook disarms after that launch.  Passing
- * NULL events disarms it.  kernel: 0 = gate/up projection, 1 = down projection (with residual).  Recording
- * events between kernels costs a few microseconds of queue time; leave the hook disarmed outside timing. */
+/* Measurement hook.  Arms two hipEvent_t (begin, end, created by the caller) for the next launch of the named
+ * kernel by this thread: that launch goes through hipExtLaunchKernel, which stamps the events with the
+ * kernel's own start and end, the interval a kernel trace reports.  The hook disarms after that launch;
+ * passing NULL events disarms it.  kernel: 0 = gate/up projection, 1 = down projection. */
 typedef enum rm_kernel_id { RM_KERNEL_GATEUP = 0, RM_KERNEL_DOWN = 1 } rm_kernel_id;
 rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end);
 

@@ -34,6 +34,8 @@
 
 namespace {
 
+using rm::launch_timed;
+
 constexpr int kGuThreads = 512;
 constexpr int kGuWaves = kGuThreads / 64;
 constexpr int kDnThreads = 256;
@@ -685,17 +687,17 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
     if (p.gate_groups == 1) {
         if (p.T <= rm::kBfTokBlock) {
             switch (p.d / 256) {  // the plan picks the direct kernel only for d = 256, 512, 1024, 2048
-                case 1: hipLaunchKernelGGL((gateup_direct_kernel<NT, 1, true>), grid, block, 0, st, a); break;
-                case 2: hipLaunchKernelGGL((gateup_direct_kernel<NT, 2, true>), grid, block, 0, st, a); break;
-                case 4: hipLaunchKernelGGL((gateup_direct_kernel<NT, 4, true>), grid, block, 0, st, a); break;
-                default: hipLaunchKernelGGL((gateup_direct_kernel<NT, 8, true>), grid, block, 0, st, a); break;
+                case 1: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 1, true>, grid, block, st, a); break;
+                case 2: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 2, true>, grid, block, st, a); break;
+                case 4: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 4, true>, grid, block, st, a); break;
+                default: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 8, true>, grid, block, st, a); break;
             }
         } else {
             switch (p.d / 256) {
-                case 1: hipLaunchKernelGGL((gateup_direct_kernel<NT, 1, false>), grid, block, 0, st, a); break;
-                case 2: hipLaunchKernelGGL((gateup_direct_kernel<NT, 2, false>), grid, block, 0, st, a); break;
-                case 4: hipLaunchKernelGGL((gateup_direct_kernel<NT, 4, false>), grid, block, 0, st, a); break;
-                default: hipLaunchKernelGGL((gateup_direct_kernel<NT, 8, false>), grid, block, 0, st, a); break;
+                case 1: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 1, false>, grid, block, st, a); break;
+                case 2: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 2, false>, grid, block, st, a); break;
+                case 4: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 4, false>, grid, block, st, a); break;
+                default: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 8, false>, grid, block, st, a); break;
             }
         }
         return;
@@ -704,10 +706,10 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
     if (p.T <= rm::kBfTokBlock && p.d % kChunkCols == 0 && (nch == 1 || nch == 2 || nch == 4 || nch == 8)) {
 #define RM_PIPE(NG)                                                                                  \
     switch (nch) {                                                                                   \
-        case 1: hipLaunchKernelGGL((gateup_pipe_kernel<NG, 1>), grid, block, 0, st, a); break;      \
-        case 2: hipLaunchKernelGGL((gateup_pipe_kernel<NG, 2>), grid, block, 0, st, a); break;      \
-        case 4: hipLaunchKernelGGL((gateup_pipe_kernel<NG, 4>), grid, block, 0, st, a); break;      \
-        default: hipLaunchKernelGGL((gateup_pipe_kernel<NG, 8>), grid, block, 0, st, a); break;     \
+        case 1: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 1>, grid, block, st, a); break;      \
+        case 2: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 2>, grid, block, st, a); break;      \
+        case 4: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 4>, grid, block, st, a); break;      \
+        default: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 8>, grid, block, st, a); break;     \
     }
         switch (p.gate_groups) {
             case 2: RM_PIPE(2) break;
@@ -717,20 +719,23 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
 #undef RM_PIPE
         return;
     }
-#define RM_STAGED(NG)                                                                                          \
-    switch (nch) {                                                                                             \
-        case 1: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 1>), grid, block, 0, st, a); break; \
-        case 2: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 2>), grid, block, 0, st, a); break; \
-        case 3: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 3>), grid, block, 0, st, a); break; \
-        case 4: hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 4>), grid, block, 0, st, a); break; \
-        case 8:                                                                                                \
-            if (NG < 8) {                                                                                      \
-                hipLaunchKernelGGL((gateup_staged_unrolled_kernel<NT, NG, 8>), grid, block, 0, st, a);        \
-                break;                                                                                         \
-            }                                                                                                  \
-            hipLaunchKernelGGL((gateup_staged_kernel<NT, NG>), grid, block, 0, st, a);                        \
-            break; /* 8 chunks x 8 groups: the unrolled form spills */                                         \
-        default: hipLaunchKernelGGL((gateup_staged_kernel<NT, NG>), grid, block, 0, st, a); break;            \
+#define RM_STAGED(NG)                                                                                    \
+    switch (nch) {                                                                                       \
+        case 1: launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 1>, grid, block, st, a); \
+            break;                                                                                       \
+        case 2: launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 2>, grid, block, st, a); \
+            break;                                                                                       \
+        case 3: launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 3>, grid, block, st, a); \
+            break;                                                                                       \
+        case 4: launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 4>, grid, block, st, a); \
+            break;                                                                                       \
+        case 8: /* 8 chunks x 8 groups: the unrolled form spills */                                      \
+            if (NG < 8)                                                                                  \
+                launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 8>, grid, block, st, a); \
+            else                                                                                         \
+                launch_timed(RM_KERNEL_GATEUP, gateup_staged_kernel<NT, NG>, grid, block, st, a);        \
+            break;                                                                                       \
+        default: launch_timed(RM_KERNEL_GATEUP, gateup_staged_kernel<NT, NG>, grid, block, st, a); break; \
     }
     switch (p.gate_groups) {
         case 2: RM_STAGED(2) break;
@@ -762,7 +767,6 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
     a.tpad = p.tpad;
     a.kcap = p.kcap;
     a.H = reinterpret_cast<uint16_t *>(base + p.off_h);
-    profile_before(RM_KERNEL_GATEUP, st);
     switch (token_tiles(p.T)) {
         case 1: launch_gateup_nt<1>(p, a, st); break;
         case 2: launch_gateup_nt<2>(p, a, st); break;
@@ -770,7 +774,6 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
         default: launch_gateup_nt<4>(p, a, st); break;
     }
     hipError_t e = hipGetLastError();
-    profile_after(RM_KERNEL_GATEUP, st);
     return e;
 }
 
@@ -789,12 +792,11 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
     a.chunks_per_slice = p.slice_units;
     a.part = reinterpret_cast<float *>(base + p.off_part);
     const dim3 grid(p.ncol, p.slices, p.B), block(kDnThreads);
-    profile_before(RM_KERNEL_DOWN, st);
 #define RM_DOWN_CPW(NT, ONE)                                                                              \
     switch (p.slice_units / kDnWaves) {                                                                  \
-        case 1: hipLaunchKernelGGL((down_bf16_kernel<NT, 1, ONE>), grid, block, 0, st, a); break;        \
-        case 2: hipLaunchKernelGGL((down_bf16_kernel<NT, 2, ONE>), grid, block, 0, st, a); break;        \
-        default: hipLaunchKernelGGL((down_bf16_kernel<NT, 4, ONE>), grid, block, 0, st, a); break;       \
+        case 1: launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 1, ONE>, grid, block, st, a); break;        \
+        case 2: launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 2, ONE>, grid, block, st, a); break;        \
+        default: launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 4, ONE>, grid, block, st, a); break;       \
     }
 #define RM_DOWN(NT)                          \
     if (p.T <= rm::kBfTokBlock) {            \
@@ -811,7 +813,6 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
 #undef RM_DOWN
 #undef RM_DOWN_CPW
     hipError_t e = hipGetLastError();
-    profile_after(RM_KERNEL_DOWN, st);
     return e;
 }
 

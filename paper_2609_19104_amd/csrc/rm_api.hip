@@ -173,7 +173,8 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         q.col_tile = kF32ColTile;
         q.ncol = ceil_div(s->d, kF32ColTile);
         const long long work = static_cast<long long>(kmax) * q.ncol * B;
-        const int su = static_cast<int>(std::max<long long>(kF32SliceNeur, (work + kTargetDownGroups - 1) / kTargetDownGroups));
+        const int su =
+            static_cast<int>(std::max<long long>(kF32SliceNeur, (work + kTargetDownGroups - 1) / kTargetDownGroups));
         q.slice_units = su;
         q.slices = ceil_div(kmax, su);
         xn_elem = 4;
@@ -200,12 +201,9 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     return RM_OK;
 }
 
-void profile_before(int kernel, hipStream_t st) {
-    if (g_profile[kernel].begin) (void)hipEventRecord(g_profile[kernel].begin, st);
-}
-
-void profile_after(int kernel, hipStream_t st) {
-    if (g_profile[kernel].end) (void)hipEventRecord(g_profile[kernel].end, st);
+void profile_take(int kernel, hipEvent_t *begin, hipEvent_t *end) {
+    *begin = g_profile[kernel].begin;
+    *end = g_profile[kernel].end;
     g_profile[kernel] = ProfileSlot{};
 }
 
@@ -218,7 +216,8 @@ void profile_after(int kernel, hipStream_t st) {
 RM_EXPORT rm_status rm_mask_compact(const uint8_t *mask, int32_t n_masks, int32_t d_ff, int32_t *idx, int32_t *count,
                                     void *stream) {
     if (!mask || !idx || !count) return fail(RM_ERR_INVALID_ARG, "mask, idx or count is NULL");
-    if (n_masks <= 0 || d_ff <= 0) return fail(RM_ERR_INVALID_ARG, "n_masks=%d and d_ff=%d must be positive", n_masks, d_ff);
+    if (n_masks <= 0 || d_ff <= 0)
+        return fail(RM_ERR_INVALID_ARG, "n_masks=%d and d_ff=%d must be positive", n_masks, d_ff);
     if (!aligned(idx, 4) || !aligned(count, 4)) return fail(RM_ERR_ALIGN, "idx and count must be 4-byte aligned");
     if (static_cast<long long>(n_masks) * ((d_ff + 1023) / 1024) > 0x7fffffffLL)
         return fail(RM_ERR_SHAPE, "n_masks=%d x d_ff=%d is too large for one launch", n_masks, d_ff);

@@ -1,9 +1,12 @@
 // Internal declarations shared by the HIP sources of the rmuscle library (gfx950 only).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
+
+#include <tuple>
 
 #include "rmuscle.h"
 
@@ -85,9 +88,28 @@ hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx
 hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, float *y, const float *g_next,
                            bool emit_xn, void *ws, hipStream_t st);
 
-// Profiling hook (thread-local events armed by rm_profile_kernel_events).
-void profile_before(int kernel, hipStream_t st);
-void profile_after(int kernel, hipStream_t st);
+// Profiling hook: the events armed by rm_profile_kernel_events for the next launch of `kernel` by this thread
+// (null when disarmed), which are disarmed by taking them.
+void profile_take(int kernel, hipEvent_t *begin, hipEvent_t *end);
+
+// Launch of a gate/up or down kernel: with armed events through hipExtLaunchKernel, which records the kernel's
+// own start and end time (the interval a kernel trace reports), else a plain launch.
+template <typename... Params, typename... Args>
+inline hipError_t launch_timed(int kernel, void (*fn)(Params...), dim3 grid, dim3 block, hipStream_t st,
+                               Args... args) {
+    static_assert(sizeof...(Params) == sizeof...(Args), "kernel argument count");
+    hipEvent_t b = nullptr, e = nullptr;
+    profile_take(kernel, &b, &e);
+    std::tuple<Params...> conv{args...};  // the kernel's own parameter types
+    return std::apply(
+        [&](auto &...v) {
+            void *argv[] = {static_cast<void *>(&v)...};
+            if (b != nullptr || e != nullptr)
+                return hipExtLaunchKernel(reinterpret_cast<const void *>(fn), grid, block, argv, 0, st, b, e, 0);
+            return hipLaunchKernel(reinterpret_cast<const void *>(fn), grid, block, argv, 0, st);
+        },
+        conv);
+}
 
 }  // namespace rm
 

@@ -162,6 +162,10 @@ def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
         torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    if hook:
+        # A spin kernel ahead of the hooked steps keeps the device busy while the host enqueues them, so the
+        # steps then run back to back as in the graph replay instead of one kernel per host call.
+        torch.cuda._sleep(int(2e6) * steps)
     start.record()
     for i in range(steps):
         if hook:
@@ -173,7 +177,10 @@ def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
     ms = start.elapsed_time(end) / steps
     kern = None
     if hook:
-        kern = {kk: float(np.mean([a.elapsed_time(b) for a, b in pairs])) * 1e3 for kk, pairs in evs.items()}
+        kern = {}
+        for kk, pairs in evs.items():
+            us = np.array([a.elapsed_time(b) for a, b in pairs]) * 1e3
+            kern[kk] = {"mean": float(us.mean()), "median": float(np.median(us)), "min": float(us.min())}
     return ms, kern
 
 
@@ -321,7 +328,8 @@ def main(argv=None) -> int:
     eager_ms, _ = time_steps(setup, args.steps, args.warmup)
     _, kern = time_steps(setup, args.steps, 5, hook=True)
     ms = time_graph(setup, args.steps, args.warmup)
-    gu_us, dn_us = kern[setup.rm.RM_KERNEL_GATEUP], kern[setup.rm.RM_KERNEL_DOWN]
+    gu_t, dn_t = kern[setup.rm.RM_KERNEL_GATEUP], kern[setup.rm.RM_KERNEL_DOWN]
+    gu_us, dn_us = gu_t["mean"], dn_t["mean"]  # average launch duration (kernel start to end)
     gu_bytes = gateup_bytes(setup.k, setup.d, 2)
     dn_bytes = down_bytes(setup.k, setup.d, 2)
     if gu_us >= dn_us:
@@ -358,7 +366,9 @@ def main(argv=None) -> int:
         "tokens_per_s": round(setup.B * setup.T / (ms * 1e-3), 1),
         "active_weight_bytes": setup.active_bytes,
         "warm_us_per_layer": round(warm_ms * 1e3, 3),
-        "kernel_us": {"gateup": round(gu_us, 3), "down": round(dn_us, 3)},
+        "kernel_us": {"gateup": round(gu_us, 3), "down": round(dn_us, 3),
+                      "gateup_median": round(gu_t["median"], 3), "gateup_min": round(gu_t["min"], 3),
+                      "down_median": round(dn_t["median"], 3), "down_min": round(dn_t["min"], 3)},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": counted_traffic(args.workload, dom_key),

@@ -207,7 +207,8 @@ def time_graph(setup: Setup, steps: int, warmup: int):
     import torch
     for i in range(warmup):
         setup.step(i)
-    per = setup.rotate
+    # Graphs of a whole number of rotations and at least 32 steps, so one replay's launch is spread over many steps.
+    per = setup.rotate * max(1, math.ceil(32 / setup.rotate))
     full, tail = divmod(steps, per)
     g_full = _capture(setup, 0, per) if full else None
     g_tail = _capture(setup, 0, tail) if tail else None

@@ -19,7 +19,11 @@ steps, the roofline of the dominant kernel (its algorithmic bytes / its average 
 recorded around its launches by the library's measurement hook, on the launch stream), and the float64 CPU
 oracle timed on a bounded sample of the same workload.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2|c4-10|c4-30|c4-50|c4-100]
+Other workloads (--workload): the wide layer d = 2048, d_ff = 16384 at 10/30/50/100% (c4-*); the 18-layer stack
+run through a 10-step denoising schedule, one step of the benchmark being the whole sequence (c3); and 16
+independent executions through the stack with per-sample lists (c5).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c5]
 """
 from __future__ import annotations
 
@@ -79,6 +83,20 @@ WORKLOADS = {
     "c4-30": dict(name="wide FFN layer, bf16, d=2048 d_ff=16384 T=51, top-30% mask", cfg=4, percent=30),
     "c4-50": dict(name="wide FFN layer, bf16, d=2048 d_ff=16384 T=51, top-50% mask", cfg=4, percent=50),
     "c4-100": dict(name="wide FFN layer, bf16, d=2048 d_ff=16384 T=51, all neurons", cfg=4, percent=100),
+    "c3": dict(name="action-expert FFN stack, 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, 10 denoising steps "
+                    "(step 0 dense; top-30% masks refreshed at steps 1, 3, 5, 7, 9)", cfg=3, percent=30),
+    "c5": dict(name="16 independent executions x 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, per-sample top-30% "
+                    "masks (18% shared core + random remainder)", cfg=5, percent=30),
+}
+
+
+STEP_TEXT = {
+    "c2": "rm_mask_compact + rm_sparse_ffn_layer, replayed from HIP graphs",
+    "c4": "rm_mask_compact + rm_sparse_ffn_layer, replayed from HIP graphs",
+    "c3": "one 10-step sequence: 18 rm_dense_ffn_ref + 9 rm_sparse_ffn_stack (L=18) + 5 rm_mask_compact (18 masks), "
+          "replayed from HIP graphs; us_per_layer = sequence time / 180",
+    "c5": "rm_mask_compact (288 masks) + rm_sparse_ffn_stack (L=18, B=16), replayed from HIP graphs; "
+          "us_per_layer = step time / 18; value on the union of the samples' rows, per_sample_value on all rows",
 }
 
 
@@ -132,6 +150,7 @@ class Setup:
         self.cnt = torch.empty((1,), dtype=torch.int32, device=device)
         self.ws = rm.workspace(self.d, self.d_ff, rm.RM_BF16, self.B, self.T, self.k, device=device)
         self.rm = rm
+        self.L, self.layer_steps = 1, 1
 
     def step(self, i: int) -> None:
         self.rm.rm_mask_compact(self.mask, self.idx, self.cnt)
@@ -140,6 +159,119 @@ class Setup:
     @property
     def active_bytes(self) -> int:
         return active_weight_bytes(self.k, self.d, 2)
+
+    def hooked_bytes(self):
+        return gateup_bytes(self.k, self.d, 2), down_bytes(self.k, self.d, 2)
+
+
+def _stack_copies(layers, device, cold: bool):
+    """Device weights of every layer ((w_gate, w_up, w_down, g) per layer), repeated in enough copies to rotate
+    over >= 1 GiB when cold."""
+    import torch
+    base = [(_bf16_tensor(l.w_gate, device), _bf16_tensor(l.w_up, device), _bf16_tensor(l.w_down, device),
+             torch.from_numpy(l.norm_g).to(device) if l.norm_g is not None else None) for l in layers]
+    dense = sum(3 * matrix_bytes(l.d, l.d_ff, 2) for l in layers)
+    copies = max(2, math.ceil(COLD_BYTES / dense)) if cold else 1
+    return [base] + [[tuple(t.clone() if t is not None else None for t in lw) for lw in base]
+                     for _ in range(copies - 1)], copies
+
+
+class StackSetup5:
+    """Config 5: B = 16 executions through an 18-layer stack, each with its own list per layer.  One step is
+    the compaction of all L B masks plus one rm_sparse_ffn_stack call."""
+
+    def __init__(self, key: str, device, cold: bool = True):
+        import torch
+        import workloads as wl
+        import paper_2609_19104_amd as rm
+        w = wl.config5()
+        self.key, self.spec, self.rm = key, WORKLOADS[key], rm
+        self.d, self.d_ff, self.T, self.B, self.L, self.k = w.d, w.d_ff, w.T, w.B, w.L, w.k
+        self.layer_copies, self.copies = _stack_copies(w.layers, device, cold)
+        self.rotate = self.copies
+        self.mask = torch.from_numpy(w.masks.reshape(self.L * self.B, self.d_ff)).to(device)
+        self.idx = torch.empty((self.L * self.B, self.d_ff), dtype=torch.int32, device=device)
+        self.cnt = torch.empty((self.L * self.B,), dtype=torch.int32, device=device)
+        self.x = torch.from_numpy(w.x).to(device)
+        self.y = torch.empty_like(self.x)
+        self.ws = rm.workspace(self.d, self.d_ff, rm.RM_BF16, self.B, self.T, self.k, device=device)
+        self.union = [int((w.masks[l] != 0).any(axis=0).sum()) for l in range(self.L)]
+        self.layer_steps = self.L
+
+    def step(self, i: int) -> None:
+        self.rm.rm_mask_compact(self.mask, self.idx, self.cnt)
+        self.rm.rm_sparse_ffn_stack(self.x, self.y, self.layer_copies[i % self.rotate], self.idx, self.cnt, self.k,
+                                    self.ws)
+
+    @property
+    def active_bytes(self) -> int:  # distinct rows per layer call (the union of the samples' lists)
+        return sum(active_weight_bytes(u, self.d, 2) for u in self.union)
+
+    @property
+    def per_sample_bytes(self) -> int:
+        return self.L * self.B * active_weight_bytes(self.k, self.d, 2)
+
+    def hooked_bytes(self):  # the first gate/up and down launches of a step: layer 0, all samples
+        return gateup_bytes(self.union[0], self.d, 2), down_bytes(self.union[0], self.d, 2)
+
+
+class StackSetup3:
+    """Config 3: one step is a whole 10-step denoising sequence through the 18-layer stack: step 0 dense
+    (rm_dense_ffn_ref layer by layer), steps 1..9 sparse (rm_sparse_ffn_stack), with the 18 per-layer masks
+    compacted at steps 1, 3, 5, 7, 9 and shared with the following step.  The masks are the top-30% neurons by
+    mean |SiLU(g) u| of a float32 dense pass on the previous step's input (input setup, on the GPU)."""
+
+    def __init__(self, key: str, device, cold: bool = True):
+        import torch
+        import torch.nn.functional as F
+        import workloads as wl
+        import paper_2609_19104_amd as rm
+        w = wl.config3()
+        self.key, self.spec, self.rm = key, WORKLOADS[key], rm
+        self.d, self.d_ff, self.T, self.B, self.L, self.k = w.d, w.d_ff, w.T, 1, w.L, w.k
+        self.steps, self.refresh = w.steps, list(w.refresh_steps)
+        self.layer_copies, self.copies = _stack_copies(w.layers, device, cold)
+        self.rotate = self.copies
+        self.xs = [torch.from_numpy(x).to(device) for x in w.x_steps]
+        masks = []
+        base = self.layer_copies[0]
+        for s in self.refresh:
+            xl = self.xs[s - 1][0].to(torch.float32)
+            m = []
+            for (wg, wu, wd, g) in base:
+                xn = xl * torch.rsqrt((xl * xl).mean(dim=-1, keepdim=True) + 1e-6) * g
+                h = F.silu(xn @ wg.float().T) * (xn @ wu.float().T)
+                order = torch.sort(h.abs().mean(dim=0), descending=True, stable=True).indices
+                mk = torch.zeros(self.d_ff, dtype=torch.uint8, device=device)
+                mk[order[:self.k]] = 1
+                m.append(mk)
+                xl = xl + h @ wd.float()
+            masks.append(torch.stack(m))
+        self.masks = masks  # [refreshes] x [L][d_ff]
+        self.idx = [torch.empty((self.L, self.d_ff), dtype=torch.int32, device=device) for _ in self.refresh]
+        self.cnt = [torch.empty((self.L,), dtype=torch.int32, device=device) for _ in self.refresh]
+        self.y = torch.empty_like(self.xs[0])
+        self.ws = rm.workspace(self.d, self.d_ff, rm.RM_BF16, 1, self.T, self.k, device=device)
+        self.ws_dense = rm.workspace(self.d, self.d_ff, rm.RM_BF16, 1, self.T, self.d_ff, device=device)
+        self.layer_steps = self.steps * self.L
+
+    def step(self, i: int) -> None:
+        rm, layers = self.rm, self.layer_copies[i % self.rotate]
+        for l in range(self.L):
+            rm.rm_dense_ffn_ref(self.xs[0] if l == 0 else self.y, self.y, layers[l], self.ws_dense)
+        for s in range(1, self.steps):
+            r = (s - 1) // 2
+            if s in self.refresh:
+                rm.rm_mask_compact(self.masks[r], self.idx[r], self.cnt[r])
+            rm.rm_sparse_ffn_stack(self.xs[s], self.y, layers, self.idx[r], self.cnt[r], self.k, self.ws)
+
+    @property
+    def active_bytes(self) -> int:  # dense step + sparse steps
+        return self.L * (active_weight_bytes(self.d_ff, self.d, 2)
+                         + (self.steps - 1) * active_weight_bytes(self.k, self.d, 2))
+
+    def hooked_bytes(self):  # the first gate/up and down launches of a step: layer 0 of the dense step
+        return gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2)
 
 
 def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
@@ -207,8 +339,9 @@ def time_graph(setup: Setup, steps: int, warmup: int):
     import torch
     for i in range(warmup):
         setup.step(i)
-    # Graphs of a whole number of rotations and at least 32 steps, so one replay's launch is spread over many steps.
-    per = setup.rotate * max(1, math.ceil(32 / setup.rotate))
+    # Graphs of a whole number of rotations and, for single-layer steps, at least 32 steps, so that one replay's
+    # launch is spread over many steps (a stack step is long enough by itself).
+    per = setup.rotate * (max(1, math.ceil(32 / setup.rotate)) if setup.layer_steps == 1 else 1)
     full, tail = divmod(steps, per)
     g_full = _capture(setup, 0, per) if full else None
     g_tail = _capture(setup, 0, tail) if tail else None
@@ -319,7 +452,7 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "copies": args.steps}))
         return 0
-    setup = Setup(args.workload, dev, cold=True)
+    setup = {"c3": StackSetup3, "c5": StackSetup5}.get(args.workload, Setup)(args.workload, dev, cold=True)
 
     if args.profile_only:
         time_graph(setup, args.steps, args.warmup)
@@ -331,8 +464,7 @@ def main(argv=None) -> int:
     ms = time_graph(setup, args.steps, args.warmup)
     gu_t, dn_t = kern[setup.rm.RM_KERNEL_GATEUP], kern[setup.rm.RM_KERNEL_DOWN]
     gu_us, dn_us = gu_t["mean"], dn_t["mean"]  # average launch duration (kernel start to end)
-    gu_bytes = gateup_bytes(setup.k, setup.d, 2)
-    dn_bytes = down_bytes(setup.k, setup.d, 2)
+    gu_bytes, dn_bytes = setup.hooked_bytes()
     if gu_us >= dn_us:
         dom, dom_key, dom_bytes, dom_us = "gate/up projection (gateup_*_kernel)", "gateup", gu_bytes, gu_us
     else:
@@ -358,15 +490,15 @@ def main(argv=None) -> int:
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": setup.spec["name"], "d": setup.d, "d_ff": setup.d_ff, "T": setup.T, "B": setup.B,
-                   "active_neurons": setup.k, "layers": 1,
-                   "step": "rm_mask_compact + rm_sparse_ffn_layer, replayed from HIP graphs",
-                   "weights": f"cold: {setup.copies} rotating copies ({setup.copies * 3 * setup.d * setup.d_ff * 2 / 2**30:.2f} GiB)"},
-        "us_per_layer": round(ms * 1e3, 3),
-        "eager_us_per_layer": round(eager_ms * 1e3, 3),
+                   "active_neurons": setup.k, "layers": setup.L, "step": STEP_TEXT[setup.key[:2]],
+                   "weights": f"cold: {setup.copies} rotating copies "
+                              f"({setup.copies * setup.L * 3 * setup.d * setup.d_ff * 2 / 2**30:.2f} GiB)"},
+        "us_per_layer": round(ms * 1e3 / setup.layer_steps, 3),
+        "eager_us_per_layer": round(eager_ms * 1e3 / setup.layer_steps, 3),
         "pct_of_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
-        "tokens_per_s": round(setup.B * setup.T / (ms * 1e-3), 1),
+        "tokens_per_s": round(setup.B * setup.T * setup.layer_steps / (ms * 1e-3), 1),
         "active_weight_bytes": setup.active_bytes,
-        "warm_us_per_layer": round(warm_ms * 1e3, 3),
+        "warm_us_per_layer": round(warm_ms * 1e3 / setup.layer_steps, 3),
         "kernel_us": {"gateup": round(gu_us, 3), "down": round(dn_us, 3),
                       "gateup_median": round(gu_t["median"], 3), "gateup_min": round(gu_t["min"], 3),
                       "down_median": round(dn_t["median"], 3), "down_min": round(dn_t["min"], 3)},
@@ -376,7 +508,10 @@ def main(argv=None) -> int:
                      "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_us, 3),
                      "traffic_unit": "bytes per launch (HBM, from rocprofv3 counters)"},
     }
-    if not args.no_cpu_baseline:
+    if isinstance(setup, StackSetup5):
+        out["per_sample_weight_bytes"] = setup.per_sample_bytes
+        out["per_sample_value"] = round(setup.per_sample_bytes / (ms * 1e-3) / 1e9, 2)
+    if not args.no_cpu_baseline and isinstance(setup, Setup):
         out["cpu_baseline"] = cpu_baseline(setup, args.cpu_seconds)
     print(json.dumps(out))
     return 0

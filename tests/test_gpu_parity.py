@@ -82,6 +82,13 @@ BF16_CASES = [
     (96, 64, 17, 1, "none"),
     (160, 200, 64, 199, "ones"),
     (1024, 4096, 51, 1229, "none"),
+    # long lists: the pipelined gate/up kernel with 2, 4 and 8 neuron groups per workgroup and 1 or 2 column
+    # chunks; the staged kernel for a chunk count it does not cover and for T > 64
+    (256, 8192, 40, 4096, "random"),
+    (512, 8192, 51, 8192, "none"),
+    (512, 16384, 64, 16384, "ones"),
+    (768, 4096, 33, 2048, "none"),
+    (256, 8192, 100, 4096, "none"),
 ]
 
 

@@ -56,12 +56,22 @@ __device__ __forceinline__ rm_u32x4 zero16() { return rm_u32x4{0u, 0u, 0u, 0u}; 
 __device__ __forceinline__ int clamp_neuron(int n, int d_ff) { return n < 0 ? 0 : (n >= d_ff ? d_ff - 1 : n); }
 __device__ __forceinline__ int clamp_count(int c, int max_count) { return c < 0 ? 0 : (c > max_count ? max_count : c); }
 
+// Workgroups are dispatched to the 8 XCDs in turn (workgroup i to XCD i mod 8), each XCD with its own L2.  The
+// logical index of workgroup `id` of `n` numbers the workgroups so that logical indices [k a, (k + 1) a) (about
+// n / 8 of them) run on XCD k: consecutive logical indices share an L2.  The kernels put the samples of one
+// neuron block (gate/up) or of one column tile and K-slice (down) at consecutive logical indices: the lists of
+// different samples overlap, and their common rows are then fetched once per L2 instead of once per sample.
+__device__ __forceinline__ int xcd_logical(int id, int n) {
+    const int a = n >> 3, r = n & 7, x = id & 7;
+    return x * a + min(x, r) + (id >> 3);
+}
+
 struct GuArgs {
     const uint16_t *wg, *wu, *xn;
     const int32_t *idx, *count;
     const float *ssq;  // [B][T][d / 256] per-token partial sums of squares, or null (no norm)
     float eps;
-    int max_count, d_ff, d, T, tpad, kcap;
+    int max_count, d_ff, d, T, tpad, kcap, B;
     uint16_t *H;
 };
 
@@ -137,8 +147,9 @@ struct DirGeom {
 template <int NT, int SPW, bool kOneBlock>
 __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
     using G = DirGeom<SPW>;
-    const int b = blockIdx.y;
-    const int slot0 = blockIdx.x * 8;
+    const int q = xcd_logical(blockIdx.x, gridDim.x);  // = block * B + sample
+    const int b = q % a.B;
+    const int slot0 = (q / a.B) * 8;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -220,8 +231,9 @@ template <int NT, int NG>
 __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
     constexpr int DS = kGuWaves / NG;            // waves per neuron group (d split)
     constexpr int SPW = kChunkSteps / DS;        // K steps per wave and chunk
-    const int b = blockIdx.y;
-    const int blk0 = blockIdx.x * 8 * NG;        // first slot of the workgroup
+    const int q = xcd_logical(blockIdx.x, gridDim.x);  // = block * B + sample
+    const int b = q % a.B;
+    const int blk0 = (q / a.B) * 8 * NG;         // first slot of the workgroup
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -329,8 +341,9 @@ template <int NT, int NG, int NCH>
 __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuArgs a) {
     constexpr int DS = kGuWaves / NG;
     constexpr int SPW = kChunkSteps / DS;
-    const int b = blockIdx.y;
-    const int blk0 = blockIdx.x * 8 * NG;
+    const int q = xcd_logical(blockIdx.x, gridDim.x);  // = block * B + sample
+    const int b = q % a.B;
+    const int blk0 = (q / a.B) * 8 * NG;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -428,18 +441,19 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
 // for chunk c, P chunks ahead, input first.  A wave's memory counter completes in issue order, so waiting for
 // chunk c leaves chunks c+1 .. c+P-1 in flight; and the input of a chunk never waits behind weights of later
 // chunks, whose deep queue would otherwise delay it by their whole transfer time.  The input goes through
-// registers into a double-buffered LDS tile, with one barrier per chunk.  With NG = 2 (more workgroups than
-// compute units) the register budget allows two workgroups per compute unit (4 waves per SIMD), so the second
-// half of the grid does not wait for the first.
-template <int NG, int NCH>
-__global__ __launch_bounds__(kGuThreads, NG == 2 ? 4 : 2) void gateup_pipe_kernel(GuArgs a) {
+// registers into a double-buffered LDS tile, with one barrier per chunk.
+// kTwoPerCU: for grids larger than the compute unit count, a register budget for two workgroups per compute
+// unit (two chunks in flight), so that the whole grid is resident at once instead of running in two rounds.
+template <int NG, int NCH, bool kTwoPerCU>
+__global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void gateup_pipe_kernel(GuArgs a) {
     constexpr int NT = 4;
-    constexpr int DS = kGuWaves / NG;                      // waves per neuron group (d split within a chunk)
-    constexpr int SPW = kChunkSteps / DS;                  // K steps per wave and chunk
-    constexpr int P0 = NG == 8 ? 3 : (NG == 4 ? 4 : 3);  // chunks in flight (registers: P (16 + 4 SPW))
+    constexpr int DS = kGuWaves / NG;  // waves per neuron group (d split within a chunk)
+    constexpr int SPW = kChunkSteps / DS;  // K steps per wave and chunk
+    constexpr int P0 = kTwoPerCU ? (NG == 2 ? 3 : 2) : (NG == 8 ? 3 : (NG == 4 ? 4 : 3));  // chunks in flight
     constexpr int P = P0 < NCH ? P0 : NCH;
-    const int b = blockIdx.y;
-    const int blk0 = blockIdx.x * 8 * NG;
+    const int q = xcd_logical(blockIdx.x, gridDim.x);  // = block * B + sample
+    const int b = q % a.B;
+    const int blk0 = (q / a.B) * 8 * NG;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -459,10 +473,10 @@ __global__ __launch_bounds__(kGuThreads, NG == 2 ? 4 : 2) void gateup_pipe_kerne
         return reinterpret_cast<rm_f32x4 *>(&xs[0][0])[((gg * DS + w2) * NT + tt) * 64 + l];
     };
 
-    // Step c processes column chunk (c + blockIdx.x) mod NCH: if every workgroup swept the chunks in the same
+    // Step c processes column chunk (c + block) mod NCH: if every workgroup swept the chunks in the same
     // order, all of them would read the same 512-byte window of their rows at once and load a few memory
     // channels only (measured: about a quarter less bandwidth than with rotated orders).
-    const int rot = blockIdx.x & (NCH - 1);
+    const int rot = (q / a.B) & (NCH - 1);
     // Step c into register slot c % P: the input pieces e = tid + 512 q (row e / 32, 16-byte piece e % 32),
     // then the weights.
     rm_u32x4 xv[P][4], w[P][SPW];
@@ -524,7 +538,7 @@ struct DnChunk {
 struct DnArgs {
     const uint16_t *H, *wd;
     const int32_t *idx;
-    int d_ff, d, T, tpad, kcap, slices, chunks_per_slice;
+    int d_ff, d, T, tpad, kcap, slices, chunks_per_slice, B, ncol;
     float *part;
 };
 
@@ -556,9 +570,10 @@ __device__ __forceinline__ void dn_mma(const DnChunk<NT> &c, rm_f32x4 (*acc)[4])
 // then, once the indices are in LDS, the weights; the wave waits for memory once per pipeline stage.
 template <int NT, int CPW, bool kOneBlock>
 __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
-    const int ct = blockIdx.x;
-    const int s = blockIdx.y;
-    const int b = blockIdx.z;
+    const int q = xcd_logical(blockIdx.x, gridDim.x);  // = (slice * ncol + column tile) * B + sample
+    const int b = q % a.B;
+    const int ct = (q / a.B) % a.ncol;
+    const int s = (q / a.B) / a.ncol;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -683,7 +698,7 @@ int token_tiles(int T) {
 template <int NT>
 void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
     const dim3 block(kGuThreads);
-    const dim3 grid(p.gate_blocks, p.B);
+    const dim3 grid(p.gate_blocks * p.B);
     if (p.gate_groups == 1) {
         if (p.T <= rm::kBfTokBlock) {
             switch (p.d / 256) {  // the plan picks the direct kernel only for d = 256, 512, 1024, 2048
@@ -704,17 +719,22 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
     }
     const int nch = (p.d + kChunkCols - 1) / kChunkCols;
     if (p.T <= rm::kBfTokBlock && p.d % kChunkCols == 0 && (nch == 1 || nch == 2 || nch == 4 || nch == 8)) {
-#define RM_PIPE(NG)                                                                                  \
-    switch (nch) {                                                                                   \
-        case 1: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 1>, grid, block, st, a); break;      \
-        case 2: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 2>, grid, block, st, a); break;      \
-        case 4: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 4>, grid, block, st, a); break;      \
-        default: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 8>, grid, block, st, a); break;     \
+#define RM_PIPE(NG, TWO)                                                                                    \
+    switch (nch) {                                                                                          \
+        case 1: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 1, TWO>, grid, block, st, a); break;  \
+        case 2: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 2, TWO>, grid, block, st, a); break;  \
+        case 4: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 4, TWO>, grid, block, st, a); break;  \
+        default: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 8, TWO>, grid, block, st, a); break; \
     }
+        const bool two = static_cast<long long>(p.gate_blocks) * p.B > 256;  // more workgroups than compute units
         switch (p.gate_groups) {
-            case 2: RM_PIPE(2) break;
-            case 4: RM_PIPE(4) break;
-            default: RM_PIPE(8) break;
+            case 2: RM_PIPE(2, true) break;
+            case 4:
+                if (two) RM_PIPE(4, true) else RM_PIPE(4, false)
+                break;
+            default:
+                if (two) RM_PIPE(8, true) else RM_PIPE(8, false)
+                break;
         }
 #undef RM_PIPE
         return;
@@ -766,6 +786,7 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
     a.T = p.T;
     a.tpad = p.tpad;
     a.kcap = p.kcap;
+    a.B = p.B;
     a.H = reinterpret_cast<uint16_t *>(base + p.off_h);
     switch (token_tiles(p.T)) {
         case 1: launch_gateup_nt<1>(p, a, st); break;
@@ -790,8 +811,10 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
     a.kcap = p.kcap;
     a.slices = p.slices;
     a.chunks_per_slice = p.slice_units;
+    a.B = p.B;
+    a.ncol = p.ncol;
     a.part = reinterpret_cast<float *>(base + p.off_part);
-    const dim3 grid(p.ncol, p.slices, p.B), block(kDnThreads);
+    const dim3 grid(p.ncol * p.slices * p.B), block(kDnThreads);
 #define RM_DOWN_CPW(NT, ONE)                                                                              \
     switch (p.slice_units / kDnWaves) {                                                                  \
         case 1: launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 1, ONE>, grid, block, st, a); break;        \

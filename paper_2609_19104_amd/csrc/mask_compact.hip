@@ -46,34 +46,51 @@ __global__ __launch_bounds__(kThreads) void mask_compact_kernel(const uint8_t *_
     const int seg0 = s * kSeg;
     const int seg1 = min(seg0 + kSeg, d_ff);
     __shared__ int lds[kThreads / 64];
+    // This segment's mask bytes, kept as they pass through step 1.
+    __shared__ __attribute__((aligned(16))) uint32_t seg_bytes[kSeg / 4];
 
     // 1. Active neurons before the segment and in the whole mask.
     int before = 0, total = 0;
     const bool al16 = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
     const int n16 = al16 ? d_ff / 16 : 0;  // whole 16-byte units (they never straddle a segment boundary)
-    for (int u = tid; u < n16; u += kThreads) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(row + u * 16);
-        const int c = __popc(nonzero_bytes(v.x)) + __popc(nonzero_bytes(v.y)) + __popc(nonzero_bytes(v.z)) +
-                      __popc(nonzero_bytes(v.w));
-        total += c;
-        if (u * 16 < seg0) before += c;
+    // Four units per thread are loaded before any is counted (one wait per 16 KB of mask); units past the end
+    // re-read the last unit and are not counted.
+    constexpr int kBatch = 4;
+    for (int u0 = tid; u0 < n16; u0 += kBatch * kThreads) {
+        uint4 v[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i)
+            v[i] = *reinterpret_cast<const uint4 *>(row + min(u0 + i * kThreads, n16 - 1) * 16);
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            const int u = u0 + i * kThreads;
+            const int c = __popc(nonzero_bytes(v[i].x)) + __popc(nonzero_bytes(v[i].y)) +
+                          __popc(nonzero_bytes(v[i].z)) + __popc(nonzero_bytes(v[i].w));
+            if (u < n16) {
+                total += c;
+                if (u * 16 < seg0) before += c;
+                if (u * 16 >= seg0 && u * 16 < seg1)
+                    *reinterpret_cast<uint4 *>(&seg_bytes[(u * 16 - seg0) / 4]) = v[i];
+            }
+        }
     }
     for (int p = n16 * 16 + tid; p < d_ff; p += kThreads) {  // unaligned rows and the ragged end, bytewise
-        const int c = row[p] != 0;
+        const uint8_t m8 = row[p];
+        const int c = m8 != 0;
         total += c;
         if (p < seg0) before += c;
+        if (p >= seg0 && p < seg1) reinterpret_cast<uint8_t *>(seg_bytes)[p - seg0] = m8;
     }
     before = block_sum(before, lds);
     total = block_sum(total, lds);
 
-    // 2. This thread's 4 neurons of the segment, their exclusive prefix within the segment, and the writes.
+    // 2. This thread's 4 neurons of the segment (from LDS: every byte of [seg0, seg1) was stored in step 1, and
+    //    block_sum's barriers made it visible), their exclusive prefix within the segment, and the writes.
     const int p0 = seg0 + 4 * tid;
     uint32_t bits = 0;
-    if (al16 && p0 + 4 <= seg1) {
-        bits = nonzero_bytes(*reinterpret_cast<const uint32_t *>(row + p0));
-    } else {
-        for (int j = 0; j < 4; ++j)
-            if (p0 + j < seg1 && row[p0 + j] != 0) bits |= 1u << j;
+    if (p0 < seg1) {
+        bits = nonzero_bytes(seg_bytes[tid]);
+        if (p0 + 4 > seg1) bits &= (1u << (seg1 - p0)) - 1u;  // bytes past the mask are not neurons
     }
     const int mine = __popc(bits);
     int incl = mine;

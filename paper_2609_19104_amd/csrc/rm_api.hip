@@ -180,7 +180,9 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         xn_elem = 4;
         h_elem = 4;
     }
-    if (q.slices > 65535) return fail(RM_ERR_SHAPE, "launch grid too large");
+    if (q.slices > 65535 || static_cast<long long>(q.gate_blocks) * B > 0x7fffffffLL ||
+        static_cast<long long>(q.ncol) * q.slices * B > 0x7fffffffLL)
+        return fail(RM_ERR_SHAPE, "launch grid too large");
     if (static_cast<long long>(B) * T * ceil_div(s->d, kRowBlock) > 0x7fffffffLL)
         return fail(RM_ERR_SHAPE, "B=%d x T=%d rows are too many for one launch", B, T);
     size_t off = 0;

@@ -5,13 +5,18 @@
  * keeps, per action-expert FFN layer, a mask of important intermediate neurons taken from a similar reference
  * execution.  The mask is shared by the consecutive denoising steps of a group, and at each such step only
  * the selected neurons' hidden activations h^M are computed and applied through their down-projection rows
- * (Eq. 4).  This library implements that update with a zero anchor, i.e. the masked SwiGLU FFN
+ * (Eq. 4).  The core call is that update with a zero anchor, i.e. the masked SwiGLU FFN
  *
  *     y[b,t,:] = x[b,t,:] + sum_{i < count[b]} h[b,t,i] * w_down[idx[b][i], :]
  *     h[b,t,i] = SiLU(<w_gate[idx[b][i]], xn[b,t]>) * <w_up[idx[b][i]], xn[b,t]>
  *     xn       = norm_g ? x / sqrt(mean(x^2) + norm_eps) * norm_g : x
  *
- * where only the listed rows of w_gate / w_up / w_down are read.
+ * where only the listed rows of w_gate / w_up / w_down are read.  Eq. 4 itself, with the group's dense
+ * anchor, is the pair rm_anchor_ffn_stack (the anchor step) / rm_delta_ffn_stack (the other steps):
+ *
+ *     y[b,t,:] = x[b,t,:] + y_a[b,t,:] + sum_{i < count[b]} (h[b,t,i] - h_a[b,i,t]) * w_down[idx[b][i], :]
+ *
+ * with y_a the anchor's FFN output (before the residual) and h_a its activations of the listed neurons.
  *
  * Conventions shared by every call
  *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every buffer and the stream; the
@@ -115,6 +120,38 @@ rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights 
  * sized with max_count = d_ff. */
 rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
                            const float *x, float *y, void *ws, size_t ws_bytes, void *stream);
+
+/* The anchor step of a group with Eq. 4 (section 4.1, "Anchors with Mask Recomputation"): L dense FFN layers
+ * applied in order, as rm_dense_ffn_ref for each layer (norm, residual, layer l reading layer l-1's output),
+ * which also keep what the group's later steps reuse:
+ *   y_anchor: float32 [L][B][T][d] out, each layer's dense FFN output y_a before the residual (its y minus
+ *             its input, as summed before the residual add);
+ *   h_anchor: float32 [L][B][max_count][T] out, h_anchor[l][b][i][t] = the dense activation h of neuron
+ *             idx[l][b][i] at token t, for i < count[l][b] (later entries are not written); may be NULL
+ *             when max_count is 0.
+ *   idx, count, max_count: the group's lists, as for rm_sparse_ffn_stack ([L][B][d_ff] and [L][B]).
+ * x, y, w as for rm_sparse_ffn_stack.  The workspace is sized with max_count = d_ff
+ * (rm_workspace_size(s, B, T, s->d_ff, ...)).  The h values kept are computed by the same kernel, with the
+ * same launch geometry and summation order, as the h of rm_delta_ffn_stack with the same lists, so a delta
+ * step at the anchor's own input reproduces the anchor's y bit for bit.  y_anchor and h_anchor must not
+ * overlap each other, x, y or the workspace.  Errors as for rm_sparse_ffn_stack; RM_ERR_ALIGN if y_anchor is
+ * not 16-byte or h_anchor not 4-byte aligned. */
+rm_status rm_anchor_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
+                              int32_t T, const float *x, float *y, const int32_t *idx, const int32_t *count,
+                              int32_t max_count, float *y_anchor, float *h_anchor, void *ws, size_t ws_bytes,
+                              void *stream);
+
+/* A non-anchor step of the group with Eq. 4 (section 4.1): L layers, layer l computing
+ *     y = x + (y_anchor[l] + sum_{i < count[l][b]} (h - h_anchor[l][b][i]) * w_down[idx[l][b][i]])
+ * with h the current activations of the listed neurons.  The difference h - h_anchor is formed in float32 and
+ * then rounded once (to bf16 on the bf16 path) for the down projection.  y_anchor and h_anchor are what
+ * rm_anchor_ffn_stack wrote for the same lists (read only).  With an empty list the layer returns
+ * x + y_anchor; with the anchor taken at the same input the layer returns the anchor's y.  Arguments and
+ * errors as for rm_sparse_ffn_stack, plus those of rm_anchor_ffn_stack for y_anchor and h_anchor; the
+ * workspace is sized with the call's max_count. */
+rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B, int32_t T,
+                             const float *x, float *y, const int32_t *idx, const int32_t *count, int32_t max_count,
+                             const float *y_anchor, const float *h_anchor, void *ws, size_t ws_bytes, void *stream);
 
 /* Measurement hook.  Arms two hipEvent_t (begin, end, created by the caller) for the next launch of the named
  * kernel by this thread: that launch goes through hipExtLaunchKernel, which stamps the events with the

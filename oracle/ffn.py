@@ -139,6 +139,36 @@ def local_update(y_anchor: np.ndarray, h_t: np.ndarray, h_anchor: np.ndarray, mu
     return np.asarray(y_anchor, np.float64) + dh @ np.asarray(w_down, np.float64)
 
 
+def anchor_stack(x: np.ndarray, layers: Sequence[tuple], eps: float = RMS_EPS):
+    """The anchor step of a group (section 4.1, "Anchors with Mask Recomputation"): the dense layers in order.
+
+    Returns (y, y_a, h_a): the last layer's output, and per layer the dense FFN output before the residual
+    (y_a, [L][..][T][d]) and the dense activations (h_a, [L][..][T][d_ff]) that the group's later steps reuse.
+    """
+    y = np.asarray(x, dtype=np.float64)
+    ya, ha = [], []
+    for wg, wu, wd, g in layers:
+        h = hidden(y, wg, wu, g, eps)
+        f = h @ np.asarray(wd, np.float64)
+        ya.append(f)
+        ha.append(h)
+        y = y + f
+    return y, np.stack(ya), np.stack(ha)
+
+
+def delta_stack(x: np.ndarray, layers: Sequence[tuple], mults: Sequence[np.ndarray], y_anchor: np.ndarray,
+                h_anchor: np.ndarray, eps: float = RMS_EPS) -> np.ndarray:
+    """A non-anchor step of the group: at each layer the FFN output is Eq. 4's estimate from the anchor's y_a and
+    h_a (as returned by anchor_stack) and this step's activations of the masked neurons, followed by the
+    residual addition; layer l reads layer l-1's output.
+    """
+    y = np.asarray(x, dtype=np.float64)
+    for l, ((wg, wu, wd, g), m) in enumerate(zip(layers, mults)):
+        h_t = hidden(y, wg, wu, g, eps)
+        y = y + local_update(y_anchor[l], h_t, h_anchor[l], m, wd)
+    return y
+
+
 # ----------------------------------------------------------------------------------------------------------
 # Picking masks by activation score (test-input preparation)
 # ----------------------------------------------------------------------------------------------------------

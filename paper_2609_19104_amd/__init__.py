@@ -9,6 +9,7 @@ Layouts (see include/rmuscle.h for the full contract):
   mask  uint8/bool [N][d_ff] -> idx int32 [N][d_ff] (ascending, -1 tail), count int32 [N]
   x, y  float32 [B][T][d];  weights [d_ff][d] float32 or bfloat16, row n = neuron n (w_down neuron-major)
   idx   int32 [B][d_ff] per layer ([L][B][d_ff] for a stack), count int32 [B] ([L][B])
+  Eq. 4 anchor state: y_anchor float32 [L][B][T][d], h_anchor float32 [L][B][max_count][T]
 """
 from __future__ import annotations
 
@@ -36,7 +37,8 @@ RM_KERNEL_GATEUP = 0
 RM_KERNEL_DOWN = 1
 
 EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_stack",
-            "rm_dense_ffn_ref", "rm_profile_kernel_events", "rm_status_string", "rm_last_error")
+            "rm_dense_ffn_ref", "rm_anchor_ffn_stack", "rm_delta_ffn_stack", "rm_profile_kernel_events",
+            "rm_status_string", "rm_last_error")
 
 Layer = Tuple[torch.Tensor, torch.Tensor, torch.Tensor, Optional[torch.Tensor]]
 
@@ -82,6 +84,8 @@ def load_library() -> ctypes.CDLL:
         "rm_sparse_ffn_layer": [sp, wp, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp],
         "rm_sparse_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp],
         "rm_dense_ffn_ref": [sp, wp, i32, i32, vp, vp, vp, sz, vp],
+        "rm_anchor_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
+        "rm_delta_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
         "rm_profile_kernel_events": [i32, vp, vp],
         "rm_status_string": [i32],
         "rm_last_error": [],
@@ -214,10 +218,8 @@ def rm_sparse_ffn_layer(x: torch.Tensor, y: torch.Tensor, layer: Layer, idx: tor
                                               wp, wn, _stream(stream)))
 
 
-def rm_sparse_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
-                        count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6,
-                        stream=None) -> None:
-    """L masked FFN layers in order; idx [L][B][d_ff], count [L][B]."""
+def _stack_args(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
+                count: torch.Tensor, eps: float):
     L = len(layers)
     if L == 0:
         raise ValueError("at least one layer")
@@ -233,10 +235,53 @@ def rm_sparse_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer
     _need_cuda("count", count, (torch.int32,))
     if idx.numel() != L * B * shape.d_ff or count.numel() != L * B:
         raise ValueError("idx must be [L][B][d_ff] and count [L][B]")
+    return shape, arr, L, B, T
+
+
+def _anchor_state(y_anchor: torch.Tensor, h_anchor: torch.Tensor, L: int, B: int, T: int, d: int,
+                  max_count: int) -> None:
+    _need_cuda("y_anchor", y_anchor, (torch.float32,))
+    _need_cuda("h_anchor", h_anchor, (torch.float32,))
+    if tuple(y_anchor.shape) != (L, B, T, d):
+        raise ValueError(f"y_anchor has shape {tuple(y_anchor.shape)}, expected {(L, B, T, d)}")
+    if tuple(h_anchor.shape) != (L, B, max_count, T):
+        raise ValueError(f"h_anchor has shape {tuple(h_anchor.shape)}, expected {(L, B, max_count, T)}")
+
+
+def rm_sparse_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
+                        count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6,
+                        stream=None) -> None:
+    """L masked FFN layers in order; idx [L][B][d_ff], count [L][B]."""
+    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps)
     wp, wn = _ws(ws)
     _check(load_library().rm_sparse_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
                                               idx.data_ptr(), count.data_ptr(), int(max_count), wp, wn,
                                               _stream(stream)))
+
+
+def rm_anchor_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
+                        count: torch.Tensor, max_count: int, y_anchor: torch.Tensor, h_anchor: torch.Tensor,
+                        ws: torch.Tensor, eps: float = 1e-6, stream=None) -> None:
+    """Eq. 4 anchor step: L dense layers; keeps y_a [L][B][T][d] and h_a of the group's lists [L][B][max_count][T].
+    The workspace is sized with max_count = d_ff."""
+    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps)
+    _anchor_state(y_anchor, h_anchor, L, B, T, shape.d, int(max_count))
+    wp, wn = _ws(ws)
+    _check(load_library().rm_anchor_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
+                                              idx.data_ptr(), count.data_ptr(), int(max_count),
+                                              y_anchor.data_ptr(), h_anchor.data_ptr(), wp, wn, _stream(stream)))
+
+
+def rm_delta_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
+                       count: torch.Tensor, max_count: int, y_anchor: torch.Tensor, h_anchor: torch.Tensor,
+                       ws: torch.Tensor, eps: float = 1e-6, stream=None) -> None:
+    """Eq. 4 non-anchor step: y = x + y_a + (h - h_a) W_down over the listed neurons, per layer."""
+    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps)
+    _anchor_state(y_anchor, h_anchor, L, B, T, shape.d, int(max_count))
+    wp, wn = _ws(ws)
+    _check(load_library().rm_delta_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
+                                             idx.data_ptr(), count.data_ptr(), int(max_count),
+                                             y_anchor.data_ptr(), h_anchor.data_ptr(), wp, wn, _stream(stream)))
 
 
 def rm_dense_ffn_ref(x: torch.Tensor, y: torch.Tensor, layer: Layer, ws: torch.Tensor, eps: float = 1e-6,

@@ -26,7 +26,8 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
                                                             int max_count, const float *x, float *y, int T, int d,
                                                             int nblk, void *__restrict__ xn_next,
                                                             const float *__restrict__ g_next,
-                                                            float *__restrict__ ssq) {
+                                                            float *__restrict__ ssq, const float *__restrict__ ya_in,
+                                                            float *__restrict__ ya_out) {
     const int row = blockIdx.x / nblk;
     const int blk = blockIdx.x - row * nblk;
     const int b = row / T;
@@ -42,8 +43,9 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
     const size_t ro = static_cast<size_t>(row) * d + cc;
 
     float4 out = ld4(x + ro);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     if (used > 0) {
-        float4 acc = ld4(P);
+        acc = ld4(P);
         for (int s = 1; s < used; s += 16) {
             float4 v[16];
 #pragma unroll
@@ -52,9 +54,16 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
             for (int i = 0; i < 16; ++i)
                 if (s + i < used) acc = add4(acc, v[i]);
         }
+    }
+    if (ya_in != nullptr) {  // Eq. 4: y = x + (y_a + (h - h_a) W_down)
+        out = add4(out, add4(ld4(ya_in + ro), acc));
+    } else if (used > 0) {
         out = add4(out, acc);
     }
-    if (ok) *reinterpret_cast<float4 *>(y + ro) = out;
+    if (ok) {
+        *reinterpret_cast<float4 *>(y + ro) = out;
+        if (ya_out != nullptr) *reinterpret_cast<float4 *>(ya_out + ro) = acc;
+    }
     if (xn_next == nullptr) return;
 
     if (g_next != nullptr) {
@@ -86,7 +95,7 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
 namespace rm {
 
 hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, float *y, const float *g_next,
-                           bool emit_xn, void *ws, hipStream_t st) {
+                           bool emit_xn, const float *ya_in, float *ya_out, void *ws, hipStream_t st) {
     char *base = static_cast<char *>(ws);
     const float *part = reinterpret_cast<const float *>(base + p.off_part);
     void *xn = emit_xn ? static_cast<void *>(base + p.off_xn) : nullptr;
@@ -97,10 +106,10 @@ hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, 
     const float *g = emit_xn ? g_next : nullptr;
     if (p.wdtype == RM_BF16)
         hipLaunchKernelGGL(epilogue_kernel<true>, grid, dim3(kThreads), 0, st, part, p.slices, slice_neurons, count,
-                           p.max_count, x, y, p.T, p.d, nblk, xn, g, ssq);
+                           p.max_count, x, y, p.T, p.d, nblk, xn, g, ssq, ya_in, ya_out);
     else
         hipLaunchKernelGGL(epilogue_kernel<false>, grid, dim3(kThreads), 0, st, part, p.slices, slice_neurons,
-                           count, p.max_count, x, y, p.T, p.d, nblk, xn, g, ssq);
+                           count, p.max_count, x, y, p.T, p.d, nblk, xn, g, ssq, ya_in, ya_out);
     return hipGetLastError();
 }
 

@@ -73,6 +73,10 @@ struct GuArgs {
     float eps;
     int max_count, d_ff, d, T, tpad, kcap, B;
     uint16_t *H;
+    // Eq. 4 (optional, [B][max_count][T] float32): h_anchor is subtracted from h before it is rounded into H
+    // (the delta step); with h_out the kernel writes h there in float32 instead of writing H (the anchor step).
+    const float *h_anchor;
+    float *h_out;
 };
 
 // Per-token RMSNorm factors of tokens t0 .. t0+63 into LDS (1 without a norm).
@@ -98,8 +102,8 @@ __device__ __forceinline__ int lane_neuron(const GuArgs &a, int b, int slot) {
 // (32-slot chunks, then tokens), so the 8 slots of a token are 16 contiguous bytes.
 // red(w, tt, lane) is d-part w's tile tt (lane L, register i = row 4 (L / 16) + i, token L % 16).
 template <int NT, typename RedAt>
-__device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, RedAt red, int ds, int t0, int slot_base,
-                                           int cnt, const float *rn) {
+__device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, int b, RedAt red, int ds, int t0,
+                                           int slot_base, int cnt, const float *rn) {
     const int j = threadIdx.x & 7;
     const int tok = threadIdx.x >> 3;
     const int tt = tok >> 4, tc = tok & 15;
@@ -118,8 +122,16 @@ __device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, RedAt 
         h = rm_silu(gsum * r) * (usum * r);
     }
     const int slot = slot_base + j;
-    if (slot >= cnt || t0 + tok >= a.T) h = 0.0f;
-    Hb[(static_cast<size_t>(slot >> 5) * a.tpad + t0 + tok) * rm::kBfChunk + (slot & 31)] =
+    const int t = t0 + tok;
+    const bool live = slot < cnt && t < a.T;
+    const size_t ai = (static_cast<size_t>(b) * a.max_count + slot) * a.T + t;  // [b][slot][t] when live
+    if (a.h_out != nullptr) {  // anchor capture: float32 h of the listed slots, H untouched
+        if (live) a.h_out[ai] = h;
+        return;
+    }
+    if (a.h_anchor != nullptr && live) h -= a.h_anchor[ai];  // Eq. 4: h_t - h_a, rounded once
+    if (!live) h = 0.0f;
+    Hb[(static_cast<size_t>(slot >> 5) * a.tpad + t) * rm::kBfChunk + (slot & 31)] =
         static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
 }
 
@@ -217,7 +229,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
         for (int tt = 0; tt < NT; ++tt) *reinterpret_cast<rm_f32x4 *>(region + (tt * 64 + lane) * 16) = acc[tt];
         load_rnorm(a, b, t0, rn);
         __syncthreads();
-        gu_store_h<NT>(a, Hb, red, kGuWaves, t0, slot0, cnt, rn);
+        gu_store_h<NT>(a, Hb, b, red, kGuWaves, t0, slot0, cnt, rn);
         t0 += rm::kBfTokBlock;
         if (kOneBlock || t0 >= a.T) break;
         __syncthreads();  // every wave has read the tiles before the regions are refilled
@@ -246,7 +258,8 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
     const int cnt = clamp_count(a.count[b], a.max_count);
     uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
 
-    if (blk0 >= cnt) {  // the whole group is past the list: h = 0
+    if (blk0 >= cnt) {  // the whole group is past the list: h = 0 (nothing to capture for an anchor)
+        if (a.h_out != nullptr) return;
         for (int e = tid; e < a.tpad * NG; e += kGuThreads) {
             const int t = e / NG, slot = blk0 + (e % NG) * 8;
             *reinterpret_cast<rm_u32x4 *>(Hb + (static_cast<size_t>(slot >> 5) * a.tpad + t) * rm::kBfChunk +
@@ -329,7 +342,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
         // Thread tid forms h for neuron (tid & 7) of each group and token tid >> 3.
 #pragma unroll
         for (int gg = 0; gg < NG; ++gg)
-            gu_store_h<NT>(a, Hb, [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; }, DS, t0,
+            gu_store_h<NT>(a, Hb, b, [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; }, DS, t0,
                            blk0 + gg * 8, cnt, rn);
         __syncthreads();
     }
@@ -356,7 +369,8 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
     const int cnt = clamp_count(a.count[b], a.max_count);
     uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
 
-    if (blk0 >= cnt) {  // the whole group is past the list: h = 0
+    if (blk0 >= cnt) {  // the whole group is past the list: h = 0 (nothing to capture for an anchor)
+        if (a.h_out != nullptr) return;
         for (int e = tid; e < a.tpad * NG; e += kGuThreads) {
             const int t = e / NG, slot = blk0 + (e % NG) * 8;
             *reinterpret_cast<rm_u32x4 *>(Hb + (static_cast<size_t>(slot >> 5) * a.tpad + t) * rm::kBfChunk +
@@ -427,7 +441,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
         __syncthreads();
 #pragma unroll
         for (int gg = 0; gg < NG; ++gg)
-            gu_store_h<NT>(a, Hb, [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; }, DS, t0,
+            gu_store_h<NT>(a, Hb, b, [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; }, DS, t0,
                            blk0 + gg * 8, cnt, rn);
         __syncthreads();
     }
@@ -523,7 +537,7 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
     __syncthreads();
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg)
-        gu_store_h<NT>(a, Hb, [&](int w2, int tt, int l) -> const rm_f32x4 & { return red(gg, w2, tt, l); }, DS, 0,
+        gu_store_h<NT>(a, Hb, b, [&](int w2, int tt, int l) -> const rm_f32x4 & { return red(gg, w2, tt, l); }, DS, 0,
                        blk0 + gg * 8, cnt, rn);
 }
 
@@ -770,7 +784,8 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
 namespace rm {
 
 hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
-                              const int32_t *count, bool norm, void *ws, hipStream_t st) {
+                              const int32_t *count, bool norm, const float *h_anchor, float *h_out, void *ws,
+                              hipStream_t st) {
     char *base = static_cast<char *>(ws);
     GuArgs a;
     a.wg = static_cast<const uint16_t *>(w_gate);
@@ -788,6 +803,8 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
     a.kcap = p.kcap;
     a.B = p.B;
     a.H = reinterpret_cast<uint16_t *>(base + p.off_h);
+    a.h_anchor = h_anchor;
+    a.h_out = h_out;
     switch (token_tiles(p.T)) {
         case 1: launch_gateup_nt<1>(p, a, st); break;
         case 2: launch_gateup_nt<2>(p, a, st); break;

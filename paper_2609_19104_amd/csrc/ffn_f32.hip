@@ -22,7 +22,8 @@ __device__ __forceinline__ int clamp_neuron(int n, int d_ff) { return n < 0 ? 0 
 __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
     const float *__restrict__ wg, const float *__restrict__ wu, const float *__restrict__ xn,
     const int32_t *__restrict__ idx, const int32_t *__restrict__ count, int max_count, int d_ff, int d, int T,
-    int tpad, float *__restrict__ H, int kcap, const float *__restrict__ ssq, float eps) {
+    int tpad, float *__restrict__ H, int kcap, const float *__restrict__ ssq, float eps,
+    const float *__restrict__ h_anchor, float *__restrict__ h_out) {
     const int b = blockIdx.y;
     const int slot0 = blockIdx.x * rm::kF32NeurPerBlk;
     const int lane = threadIdx.x;
@@ -90,7 +91,14 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
                 if (ssq != nullptr) rn = rm_token_rnorm(ssq, b * T + t0 + cl, d, eps);
                 h = rm_silu(gs * rn) * (us * rn);
             }
-            Hb[static_cast<size_t>(t0 + cl) * kcap + slot] = h;
+            // Eq. 4: the anchor step keeps h of the listed slots; a delta step stores h - h_anchor.
+            const size_t ai = (static_cast<size_t>(b) * max_count + slot) * T + t0 + cl;
+            if (h_out != nullptr) {
+                if (cl < nt) h_out[ai] = h;
+            } else {
+                if (h_anchor != nullptr && cl < nt) h -= h_anchor[ai];
+                Hb[static_cast<size_t>(t0 + cl) * kcap + slot] = h;
+            }
         }
     }
 }
@@ -149,14 +157,15 @@ __global__ __launch_bounds__(kWave) void down_f32_kernel(
 namespace rm {
 
 hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
-                             const int32_t *count, bool norm, void *ws, hipStream_t st) {
+                             const int32_t *count, bool norm, const float *h_anchor, float *h_out, void *ws,
+                             hipStream_t st) {
     char *base = static_cast<char *>(ws);
     const float *xn = reinterpret_cast<const float *>(base + p.off_xn);
     float *H = reinterpret_cast<float *>(base + p.off_h);
     const float *ssq = norm ? reinterpret_cast<const float *>(base + p.off_ssq) : nullptr;
     launch_timed(RM_KERNEL_GATEUP, gateup_f32_kernel, dim3(p.gate_blocks, p.B), dim3(kWave), st,
-                       static_cast<const float *>(w_gate), static_cast<const float *>(w_up), xn, idx, count,
-                       p.max_count, p.d_ff, p.d, p.T, p.tpad, H, p.kcap, ssq, p.eps);
+                 static_cast<const float *>(w_gate), static_cast<const float *>(w_up), xn, idx, count, p.max_count,
+                 p.d_ff, p.d, p.T, p.tpad, H, p.kcap, ssq, p.eps, h_anchor, h_out);
     hipError_t e = hipGetLastError();
     return e;
 }

@@ -98,25 +98,82 @@ rm_status hip_fail(hipError_t e, const char *what) {
     return fail(RM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Layers 0..L-1 of one call; w[l] are the layers' weights, lists at idx + l * list_stride.
+// Checks shared by the anchor and delta stacks: L, weights, the anchor buffers' sizes and overlaps.
+rm_status check_anchor_buffers(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int L, int B, int T,
+                               const float *x, float *y, int max_count, const void *y_anchor, const void *h_anchor,
+                               const void *ws, size_t ws_bytes) {
+    if (L <= 0) return fail(RM_ERR_INVALID_ARG, "L=%d must be positive", L);
+    if (!w) return fail(RM_ERR_INVALID_ARG, "weights pointer is NULL");
+    for (int l = 0; l < L; ++l) {
+        const rm_status st = check_layer(&w[l], l);
+        if (st != RM_OK) return st;
+    }
+    if (!y_anchor) return fail(RM_ERR_INVALID_ARG, "y_anchor is NULL");
+    if (!h_anchor && max_count > 0) return fail(RM_ERR_INVALID_ARG, "h_anchor is NULL with max_count=%d", max_count);
+    if (!aligned(y_anchor, 16) || !aligned(h_anchor, 4))
+        return fail(RM_ERR_ALIGN, "y_anchor must be 16-byte and h_anchor 4-byte aligned");
+    const size_t act = static_cast<size_t>(B) * T * s->d * sizeof(float);
+    const size_t ya_bytes = act * L;
+    const size_t ha_bytes = static_cast<size_t>(L) * B * max_count * T * sizeof(float);
+    if (ranges_overlap(y_anchor, ya_bytes, h_anchor, ha_bytes) || ranges_overlap(y_anchor, ya_bytes, x, act) ||
+        ranges_overlap(y_anchor, ya_bytes, y, act) || ranges_overlap(h_anchor, ha_bytes, x, act) ||
+        ranges_overlap(h_anchor, ha_bytes, y, act) || ranges_overlap(y_anchor, ya_bytes, ws, ws_bytes) ||
+        ranges_overlap(h_anchor, ha_bytes, ws, ws_bytes))
+        return fail(RM_ERR_INVALID_ARG, "y_anchor and h_anchor must not overlap each other, x, y or the workspace");
+    return RM_OK;
+}
+
+// Eq. 4 terms of an anchor or delta stack (all null for a plain call).  Per layer l:
+//   ya_in  + l * B T d: y_a, added to the masked sum (delta step);
+//   ya_out + l * B T d: receives the FFN output before the residual (anchor step);
+//   ha_in  + l * h_stride: h_a^M, subtracted from h (delta step);
+//   ha_out + l * h_stride: receives h^M of the lists cap_idx / cap_count (anchor step), computed with cap_plan,
+//          which sizes the lists (its max_count) and shares the call's FFN input and sums of squares.
+struct AnchorTerms {
+    const float *ya_in = nullptr;
+    float *ya_out = nullptr;
+    const float *ha_in = nullptr;
+    float *ha_out = nullptr;
+    const int32_t *cap_idx = nullptr;
+    const int32_t *cap_count = nullptr;
+    const rm::Plan *cap_plan = nullptr;
+    size_t h_stride = 0;
+};
+
+// Layers 0..L-1 of one call; w[l] are the layers' weights, lists at idx + l * list_stride and counts at
+// count + l * count_stride (both strides 0 when every layer uses the same lists, as the dense calls do).
 rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, const float *x, float *y,
-                     const int32_t *idx, const int32_t *count, size_t list_stride, void *ws, hipStream_t st) {
+                     const int32_t *idx, const int32_t *count, size_t list_stride, size_t count_stride, void *ws,
+                     hipStream_t st, const AnchorTerms &at = AnchorTerms{}) {
     hipError_t e = rm::launch_prologue(p, x, w[0].norm_g, ws, st);
     if (e != hipSuccess) return hip_fail(e, "prologue launch");
+    const bool bf = p.wdtype == RM_BF16;
+    const size_t y_stride = static_cast<size_t>(p.B) * p.T * p.d;
     for (int l = 0; l < L; ++l) {
         const int32_t *il = idx + l * list_stride;
-        const int32_t *cl = count + static_cast<size_t>(l) * p.B;
-        const bool bf = p.wdtype == RM_BF16;
+        const int32_t *cl = count + l * count_stride;
         const bool norm = w[l].norm_g != nullptr;
-        e = bf ? rm::launch_gateup_bf16(p, w[l].w_gate, w[l].w_up, il, cl, norm, ws, st)
-               : rm::launch_gateup_f32(p, w[l].w_gate, w[l].w_up, il, cl, norm, ws, st);
+        const float *ha = at.ha_in ? at.ha_in + l * at.h_stride : nullptr;
+        e = bf ? rm::launch_gateup_bf16(p, w[l].w_gate, w[l].w_up, il, cl, norm, ha, nullptr, ws, st)
+               : rm::launch_gateup_f32(p, w[l].w_gate, w[l].w_up, il, cl, norm, ha, nullptr, ws, st);
         if (e != hipSuccess) return hip_fail(e, "gate/up launch");
+        if (at.ha_out != nullptr) {  // the anchor keeps h^M of the group's lists (same input, same norm)
+            const rm::Plan &q = *at.cap_plan;
+            const int32_t *ci = at.cap_idx + static_cast<size_t>(l) * p.B * p.d_ff;
+            const int32_t *cc = at.cap_count + static_cast<size_t>(l) * p.B;
+            float *ho = at.ha_out + l * at.h_stride;
+            e = bf ? rm::launch_gateup_bf16(q, w[l].w_gate, w[l].w_up, ci, cc, norm, nullptr, ho, ws, st)
+                   : rm::launch_gateup_f32(q, w[l].w_gate, w[l].w_up, ci, cc, norm, nullptr, ho, ws, st);
+            if (e != hipSuccess) return hip_fail(e, "anchor h capture launch");
+        }
         const bool next = l + 1 < L;
         const float *g_next = next ? w[l + 1].norm_g : nullptr;
         const float *xin = l == 0 ? x : y;
         e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
         if (e != hipSuccess) return hip_fail(e, "down launch");
-        e = rm::launch_epilogue(p, cl, xin, y, g_next, next, ws, st);
+        const float *ya_in = at.ya_in ? at.ya_in + l * y_stride : nullptr;
+        float *ya_out = at.ya_out ? at.ya_out + l * y_stride : nullptr;
+        e = rm::launch_epilogue(p, cl, xin, y, g_next, next, ya_in, ya_out, ws, st);
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }
     return RM_OK;
@@ -254,7 +311,7 @@ RM_EXPORT rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_laye
     if (st != RM_OK) return st;
     st = check_layer(w, 0);
     if (st != RM_OK) return st;
-    st = run_layers(p, w, 1, x, y, idx, count, 0, ws, static_cast<hipStream_t>(stream));
+    st = run_layers(p, w, 1, x, y, idx, count, 0, 0, ws, static_cast<hipStream_t>(stream));
     return st == RM_OK ? ok() : st;
 }
 
@@ -271,7 +328,8 @@ RM_EXPORT rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
         st = check_layer(&w[l], l);
         if (st != RM_OK) return st;
     }
-    st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, ws, static_cast<hipStream_t>(stream));
+    st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
+                    static_cast<hipStream_t>(stream));
     return st == RM_OK ? ok() : st;
 }
 
@@ -287,7 +345,57 @@ RM_EXPORT rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_w
     if (e != hipSuccess) return hip_fail(e, "identity list launch");
     char *base = static_cast<char *>(ws);
     st = run_layers(p, w, 1, x, y, reinterpret_cast<const int32_t *>(base + p.off_ident),
-                    reinterpret_cast<const int32_t *>(base + p.off_ident_count), 0, ws, hs);
+                    reinterpret_cast<const int32_t *>(base + p.off_ident_count), 0, 0, ws, hs);
+    return st == RM_OK ? ok() : st;
+}
+
+RM_EXPORT rm_status rm_anchor_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
+                                        int32_t T, const float *x, float *y, const int32_t *idx,
+                                        const int32_t *count, int32_t max_count, float *y_anchor, float *h_anchor,
+                                        void *ws, size_t ws_bytes, void *stream) {
+    rm::Plan p, q;
+    rm_status st = check_call(s, B, T, x, y, nullptr, nullptr, false, 0, ws, ws_bytes, &p);  // dense layers
+    if (st != RM_OK) return st;
+    st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &q);  // the group's lists
+    if (st != RM_OK) return st;
+    st = check_anchor_buffers(s, w, L, B, T, x, y, max_count, y_anchor, h_anchor, ws, ws_bytes);
+    if (st != RM_OK) return st;
+    // The capture reads the dense layers' FFN input and sums of squares from the dense workspace layout; it
+    // writes nothing else there.
+    q.off_xn = p.off_xn;
+    q.off_ssq = p.off_ssq;
+    q.off_h = p.off_h;  // not written by a capture
+    AnchorTerms at;
+    at.ya_out = y_anchor;
+    at.ha_out = max_count > 0 ? h_anchor : nullptr;  // nothing to keep from empty lists
+    at.cap_idx = idx;
+    at.cap_count = count;
+    at.cap_plan = &q;
+    at.h_stride = static_cast<size_t>(B) * max_count * T;
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    const hipError_t e = rm::launch_identity_lists(p, ws, hs);
+    if (e != hipSuccess) return hip_fail(e, "identity list launch");
+    char *base = static_cast<char *>(ws);
+    st = run_layers(p, w, L, x, y, reinterpret_cast<const int32_t *>(base + p.off_ident),
+                    reinterpret_cast<const int32_t *>(base + p.off_ident_count), 0, 0, ws, hs, at);
+    return st == RM_OK ? ok() : st;
+}
+
+RM_EXPORT rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
+                                       int32_t T, const float *x, float *y, const int32_t *idx, const int32_t *count,
+                                       int32_t max_count, const float *y_anchor, const float *h_anchor, void *ws,
+                                       size_t ws_bytes, void *stream) {
+    rm::Plan p;
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    if (st != RM_OK) return st;
+    st = check_anchor_buffers(s, w, L, B, T, x, y, max_count, y_anchor, h_anchor, ws, ws_bytes);
+    if (st != RM_OK) return st;
+    AnchorTerms at;
+    at.ya_in = y_anchor;
+    at.ha_in = max_count > 0 ? h_anchor : nullptr;
+    at.h_stride = static_cast<size_t>(B) * max_count * T;
+    st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
+                    static_cast<hipStream_t>(stream), at);
     return st == RM_OK ? ok() : st;
 }
 

@@ -72,10 +72,14 @@ hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, v
 
 // Gate/up projection of the listed neurons + SiLU * up -> H in the workspace.  norm: scale by the per-token
 // RMSNorm factor formed from the workspace's sums of squares.
+// Eq. 4 (both optional, [B][max_count][T] float32): h_anchor is subtracted from h before it goes into H (a
+// delta step); with h_out, h of the listed slots is written there instead of H (capturing an anchor's h^M).
 hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
-                              const int32_t *count, bool norm, void *ws, hipStream_t st);
+                              const int32_t *count, bool norm, const float *h_anchor, float *h_out, void *ws,
+                              hipStream_t st);
 hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
-                             const int32_t *count, bool norm, void *ws, hipStream_t st);
+                             const int32_t *count, bool norm, const float *h_anchor, float *h_out, void *ws,
+                             hipStream_t st);
 
 // Down projection of the listed neurons: per-K-slice float32 partials of H W_down[idx] in the workspace.  The
 // bf16 form needs no count: H is zero in every slot past the list.
@@ -84,9 +88,10 @@ hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx
                            hipStream_t st);
 
 // y = x + the slices' partials in slice order; if emit_xn, also the next layer's FFN input (y * g_next, or y)
-// and, with g_next, its per-token sums of squares.
+// and, with g_next, its per-token sums of squares.  Eq. 4 (optional, [B][T][d] float32): y = x + (ya_in +
+// partials) on a delta step; ya_out receives the partials' sum (the FFN output) on an anchor step.
 hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, float *y, const float *g_next,
-                           bool emit_xn, void *ws, hipStream_t st);
+                           bool emit_xn, const float *ya_in, float *ya_out, void *ws, hipStream_t st);
 
 // Profiling hook: the events armed by rm_profile_kernel_events for the next launch of `kernel` by this thread
 // (null when disarmed), which are disarmed by taking them.

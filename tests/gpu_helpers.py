@@ -97,3 +97,39 @@ def errors(y: np.ndarray, y_ref: np.ndarray, x: np.ndarray):
     num = float(np.max(excess)) if excess.size else 0.0
     ed = (0.0 if num == 0.0 else float("inf")) if den == 0.0 else num / den
     return oracle.rel_err(y, y_ref), ed
+
+
+H_SENTINEL = -12345.0  # h_anchor entries past a list's count must keep it
+
+
+def run_anchor(layers_dev, x: np.ndarray, idx: torch.Tensor, cnt: torch.Tensor, max_count: int):
+    """Eq. 4 anchor step through rm_anchor_ffn_stack -> (y, y_anchor [L][B][T][d], h_anchor [L][B][max_count][T])
+    as device tensors (the anchor state stays on the device for the delta steps)."""
+    wg = layers_dev[0][0]
+    d_ff, d = wg.shape
+    B, T, _ = x.shape
+    L = len(layers_dev)
+    xt = dev_f32(x)
+    yt = torch.full_like(xt, float("nan"))
+    ya = torch.full((L, B, T, d), float("nan"), dtype=torch.float32, device=DEV)
+    ha = torch.full((L, B, max_count, T), H_SENTINEL, dtype=torch.float32, device=DEV)
+    ws = rm.workspace(d, d_ff, rm.wdtype_of(wg), B, T, d_ff, device=DEV)
+    ws.fill_(0x6B)
+    rm.rm_anchor_ffn_stack(xt, yt, layers_dev, idx, cnt, max_count, ya, ha, ws)
+    torch.cuda.synchronize()
+    return yt, ya, ha
+
+
+def run_delta(layers_dev, x: np.ndarray, idx: torch.Tensor, cnt: torch.Tensor, max_count: int,
+              ya: torch.Tensor, ha: torch.Tensor) -> np.ndarray:
+    """Eq. 4 non-anchor step through rm_delta_ffn_stack."""
+    wg = layers_dev[0][0]
+    d_ff, d = wg.shape
+    B, T, _ = x.shape
+    xt = dev_f32(x)
+    yt = torch.full_like(xt, float("nan"))
+    ws = rm.workspace(d, d_ff, rm.wdtype_of(wg), B, T, max_count, device=DEV)
+    ws.fill_(0x2C)
+    rm.rm_delta_ffn_stack(xt, yt, layers_dev, idx, cnt, max_count, ya, ha, ws)
+    torch.cuda.synchronize()
+    return yt.cpu().numpy()

@@ -332,6 +332,80 @@ def test_local_update_special_cases():
     assert np.max(np.abs(got - (oracle.masked_ffn(xt, wg, wu, wd, m) - xt))) < 1e-14
 
 
+def _torch_dense_chain(x, layers):
+    outs = [np.asarray(x, np.float64)]
+    for wg, wu, wd, g in layers:
+        outs.append(_torch_swiglu(outs[-1], wg, wu, wd, g))
+    return outs
+
+
+def test_anchor_stack_keeps_dense_outputs_and_activations():
+    layers = [_rand_layer(40 + l, 8, 12, True) for l in range(3)]
+    x = np.random.default_rng(43).standard_normal((2, 5, 8))
+    y, ya, ha = oracle.anchor_stack(x, layers)
+    outs = _torch_dense_chain(x, layers)
+    assert np.max(np.abs(y - outs[-1])) < 1e-12
+    for l, (wg, wu, wd, g) in enumerate(layers):
+        # y_a is the layer's FFN output before the residual; h_a its activations at the layer's input.
+        assert np.max(np.abs(ya[l] - (outs[l + 1] - outs[l]))) < 1e-12
+        xn = F.rms_norm(torch.tensor(outs[l]), (8,), weight=torch.tensor(g), eps=1e-6)
+        h = (F.silu(F.linear(xn, torch.tensor(wg))) * F.linear(xn, torch.tensor(wu))).numpy()
+        assert np.max(np.abs(ha[l] - h)) < 1e-12
+
+
+def _brute_eq4_layer(x, layer, mask, ya, ha, eps=1e-6):
+    """Eq. 4 for one layer by scalar loops: x + y_a + sum over masked n of (h_t[n] - h_a[n]) W_down[n]."""
+    wg, wu, wd, g = layer
+    T, d = len(x), len(x[0])
+    out = []
+    for t in range(T):
+        ms = sum(x[t][j] * x[t][j] for j in range(d)) / d
+        xn = [x[t][j] / math.sqrt(ms + eps) * g[j] for j in range(d)]
+        row = []
+        for c in range(d):
+            acc = ya[t][c]
+            for n in range(len(wg)):
+                if mask[n]:
+                    a = sum(wg[n][j] * xn[j] for j in range(d))
+                    u = sum(wu[n][j] * xn[j] for j in range(d))
+                    h = a / (1.0 + math.exp(-a)) * u
+                    acc += (h - ha[t][n]) * wd[n][c]
+            row.append(x[t][c] + acc)
+        out.append(row)
+    return np.array(out)
+
+
+def test_delta_stack_matches_brute_force_eq4():
+    layer = _rand_layer(44, 3, 5, True)
+    r = np.random.default_rng(45)
+    xa, xt = r.standard_normal((2, 3)), r.standard_normal((2, 3))
+    _, ya, ha = oracle.anchor_stack(xa, [layer])
+    mask = np.array([1, 0, 1, 1, 0])
+    got = oracle.delta_stack(xt, [layer], [mask.astype(float)], ya, ha)
+    ref = _brute_eq4_layer(xt.tolist(), layer, mask, ya[0].tolist(), ha[0].tolist())
+    assert np.max(np.abs(got - ref)) < 1e-13
+
+
+def test_delta_stack_special_cases():
+    layers = [_rand_layer(46 + l, 8, 12, True) for l in range(3)]
+    r = np.random.default_rng(49)
+    xa = r.standard_normal((4, 8))
+    xt = xa + 0.05 * r.standard_normal((4, 8))
+    y_anchor, ya, ha = oracle.anchor_stack(xa, layers)
+    masks = [wl.bernoulli_mask(r, (12,), 0.4).astype(float) for _ in range(3)]
+    # At the anchor's own input every layer reproduces the anchor, whatever the masks.
+    assert np.array_equal(oracle.delta_stack(xa, layers, masks, ya, ha), y_anchor)
+    # Every neuron selected: the dense stack at the current input.
+    full = oracle.delta_stack(xt, layers, [np.ones(12)] * 3, ya, ha)
+    assert np.max(np.abs(full - _torch_dense_chain(xt, layers)[-1])) < 1e-12
+    # No neuron selected: each layer adds its anchor output to its own input.
+    empty = oracle.delta_stack(xt, layers, [np.zeros(12)] * 3, ya, ha)
+    assert np.array_equal(empty, ((xt + ya[0]) + ya[1]) + ya[2])
+    # Zero anchor: the masked stack.
+    zero = oracle.delta_stack(xt, layers, masks, np.zeros_like(ya), np.zeros_like(ha))
+    assert np.max(np.abs(zero - oracle.ffn_stack(xt, layers, masks))) < 1e-12
+
+
 # ------------------------------------------------------------------------------------------------ stacks
 
 def test_stack_reduces_to_layers_and_identity():

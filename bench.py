@@ -3,7 +3,8 @@
 Workload (default): one pi0-style action-expert FFN layer, bf16 weights / float32 activations, d = 1024,
 d_ff = 4096, T = 51 tokens (50 actions + 1 state), mask = top 30% of neurons (K = 1229) by mean |SiLU(g) * u| on
 a reference input, evaluated on that input + 0.1 N(0,1).  One step is the whole hot path for one batch:
-rm_mask_compact of the layer's mask, then rm_sparse_ffn_layer.
+rm_masked_ffn_layer, i.e. the compaction of the layer's mask into its index list (in the launch of the layer's
+first kernel) and the masked layer.
 
 Weights are cold: every step reads a different one of R copies of the layer (>= 1 GiB together), so neither
 L2 nor the 256 MB Infinity Cache can serve them and the weight bytes come from HBM.  Activations, mask and
@@ -20,10 +21,12 @@ recorded around its launches by the library's measurement hook, on the launch st
 oracle timed on a bounded sample of the same workload.
 
 Other workloads (--workload): the wide layer d = 2048, d_ff = 16384 at 10/30/50/100% (c4-*); the 18-layer stack
-run through a 10-step denoising schedule, one step of the benchmark being the whole sequence (c3); and 16
-independent executions through the stack with per-sample lists (c5).
+run through a 10-step denoising schedule, one step of the benchmark being the whole sequence (c3); the same
+sequence with Eq. 4's dense anchors at steps 0 and 5 and anchor-delta updates at the other steps (c3-eq4); and
+16 independent executions through the stack with per-sample lists (c5).
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c5]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+                       [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c3-eq4|c5]
 """
 from __future__ import annotations
 
@@ -85,17 +88,24 @@ WORKLOADS = {
     "c4-100": dict(name="wide FFN layer, bf16, d=2048 d_ff=16384 T=51, all neurons", cfg=4, percent=100),
     "c3": dict(name="action-expert FFN stack, 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, 10 denoising steps "
                     "(step 0 dense; top-30% masks refreshed at steps 1, 3, 5, 7, 9)", cfg=3, percent=30),
+    "c3-eq4": dict(name="action-expert FFN stack, 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, 10 denoising steps "
+                        "with Eq. 4: dense anchors at steps 0 and 5, each shared by the next 4 steps with top-30% "
+                        "group masks", cfg=3, percent=30),
     "c5": dict(name="16 independent executions x 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, per-sample top-30% "
                     "masks (18% shared core + random remainder)", cfg=5, percent=30),
 }
 
 
 STEP_TEXT = {
-    "c2": "rm_mask_compact + rm_sparse_ffn_layer, replayed from HIP graphs",
-    "c4": "rm_mask_compact + rm_sparse_ffn_layer, replayed from HIP graphs",
-    "c3": "one 10-step sequence: 18 rm_dense_ffn_ref + 9 rm_sparse_ffn_stack (L=18) + 5 rm_mask_compact (18 masks), "
-          "replayed from HIP graphs; us_per_layer = sequence time / 180",
-    "c5": "rm_mask_compact (288 masks) + rm_sparse_ffn_stack (L=18, B=16), replayed from HIP graphs; "
+    "c2": "rm_masked_ffn_layer (mask compaction + layer), replayed from HIP graphs",
+    "c4": "rm_masked_ffn_layer (mask compaction + layer), replayed from HIP graphs",
+    "c3": "one 10-step sequence: 18 rm_dense_ffn_ref, then 5 rm_masked_ffn_stack (L=18, compacting the refreshed "
+          "18 masks) alternating with 4 rm_sparse_ffn_stack (L=18), replayed from HIP graphs; "
+          "us_per_layer = sequence time / 180",
+    "c3-eq4": "one 10-step sequence: per group (anchors 0 and 5) rm_mask_compact (18 masks) + "
+              "rm_anchor_ffn_stack (L=18) + 4 rm_delta_ffn_stack (L=18), replayed from HIP graphs; "
+              "us_per_layer = sequence time / 180",
+    "c5": "rm_masked_ffn_stack (L=18, B=16: compaction of the 288 masks + the stack), replayed from HIP graphs; "
           "us_per_layer = step time / 18; value on the union of the samples' rows, per_sample_value on all rows",
 }
 
@@ -153,8 +163,8 @@ class Setup:
         self.L, self.layer_steps = 1, 1
 
     def step(self, i: int) -> None:
-        self.rm.rm_mask_compact(self.mask, self.idx, self.cnt)
-        self.rm.rm_sparse_ffn_layer(self.x, self.y, self.layers[i % self.rotate], self.idx, self.cnt, self.k, self.ws)
+        self.rm.rm_masked_ffn_layer(self.x, self.y, self.layers[i % self.rotate], self.mask, self.idx, self.cnt,
+                                    self.k, self.ws)
 
     @property
     def active_bytes(self) -> int:
@@ -177,8 +187,8 @@ def _stack_copies(layers, device, cold: bool):
 
 
 class StackSetup5:
-    """Config 5: B = 16 executions through an 18-layer stack, each with its own list per layer.  One step is
-    the compaction of all L B masks plus one rm_sparse_ffn_stack call."""
+    """Config 5: B = 16 executions through an 18-layer stack, each with its own list per layer.  One step is one
+    rm_masked_ffn_stack call: the compaction of all L B masks and the stack."""
 
     def __init__(self, key: str, device, cold: bool = True):
         import torch
@@ -199,9 +209,8 @@ class StackSetup5:
         self.layer_steps = self.L
 
     def step(self, i: int) -> None:
-        self.rm.rm_mask_compact(self.mask, self.idx, self.cnt)
-        self.rm.rm_sparse_ffn_stack(self.x, self.y, self.layer_copies[i % self.rotate], self.idx, self.cnt, self.k,
-                                    self.ws)
+        self.rm.rm_masked_ffn_stack(self.x, self.y, self.layer_copies[i % self.rotate], self.mask, self.idx, self.cnt,
+                                    self.k, self.ws)
 
     @property
     def active_bytes(self) -> int:  # distinct rows per layer call (the union of the samples' lists)
@@ -217,8 +226,8 @@ class StackSetup5:
 
 class StackSetup3:
     """Config 3: one step is a whole 10-step denoising sequence through the 18-layer stack: step 0 dense
-    (rm_dense_ffn_ref layer by layer), steps 1..9 sparse (rm_sparse_ffn_stack), with the 18 per-layer masks
-    compacted at steps 1, 3, 5, 7, 9 and shared with the following step.  The masks are the top-30% neurons by
+    (rm_dense_ffn_ref layer by layer), steps 1..9 sparse, with the 18 per-layer masks compacted at steps 1, 3,
+    5, 7, 9 (rm_masked_ffn_stack) and their lists reused by the following step (rm_sparse_ffn_stack).  The masks are the top-30% neurons by
     mean |SiLU(g) u| of a float32 dense pass on the previous step's input (input setup, on the GPU)."""
 
     def __init__(self, key: str, device, cold: bool = True):
@@ -262,8 +271,10 @@ class StackSetup3:
         for s in range(1, self.steps):
             r = (s - 1) // 2
             if s in self.refresh:
-                rm.rm_mask_compact(self.masks[r], self.idx[r], self.cnt[r])
-            rm.rm_sparse_ffn_stack(self.xs[s], self.y, layers, self.idx[r], self.cnt[r], self.k, self.ws)
+                rm.rm_masked_ffn_stack(self.xs[s], self.y, layers, self.masks[r], self.idx[r], self.cnt[r], self.k,
+                                       self.ws)
+            else:
+                rm.rm_sparse_ffn_stack(self.xs[s], self.y, layers, self.idx[r], self.cnt[r], self.k, self.ws)
 
     @property
     def active_bytes(self) -> int:  # dense step + sparse steps
@@ -271,6 +282,72 @@ class StackSetup3:
                          + (self.steps - 1) * active_weight_bytes(self.k, self.d, 2))
 
     def hooked_bytes(self):  # the first gate/up and down launches of a step: layer 0 of the dense step
+        return gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2)
+
+
+class StackSetupEq4:
+    """The paper's anchored schedule (section 4.1) on the config-3 stack: one step is a 10-step sequence of two
+    groups.  Each group compacts its 18 layer masks, runs its anchor step densely with rm_anchor_ffn_stack
+    (keeping y_a and the listed h_a) and its 4 later steps with rm_delta_ffn_stack (Eq. 4).  A group's masks
+    are the top-30% neurons by mean |SiLU(g) u| of a float32 dense pass on a similar input (the anchor input +
+    0.1 N(0,1)), computed on the GPU at set-up."""
+
+    ANCHORS = (0, 5)
+
+    def __init__(self, key: str, device, cold: bool = True):
+        import torch
+        import torch.nn.functional as F
+        import workloads as wl
+        import paper_2609_19104_amd as rm
+        w = wl.config3()
+        self.key, self.spec, self.rm = key, WORKLOADS[key], rm
+        self.d, self.d_ff, self.T, self.B, self.L, self.k = w.d, w.d_ff, w.T, 1, w.L, w.k
+        self.steps = w.steps
+        self.layer_copies, self.copies = _stack_copies(w.layers, device, cold)
+        self.rotate = self.copies
+        self.xs = [torch.from_numpy(x).to(device) for x in w.x_steps]
+        base = self.layer_copies[0]
+        self.masks = []
+        for xr in wl.group_reference_inputs(w, self.ANCHORS):
+            xl = torch.from_numpy(xr[0]).to(device)
+            m = []
+            for (wg, wu, wd, g) in base:
+                xn = xl * torch.rsqrt((xl * xl).mean(dim=-1, keepdim=True) + 1e-6) * g
+                h = F.silu(xn @ wg.float().T) * (xn @ wu.float().T)
+                order = torch.sort(h.abs().mean(dim=0), descending=True, stable=True).indices
+                mk = torch.zeros(self.d_ff, dtype=torch.uint8, device=device)
+                mk[order[:self.k]] = 1
+                m.append(mk)
+                xl = xl + h @ wd.float()
+            self.masks.append(torch.stack(m))
+        self.idx = [torch.empty((self.L, self.d_ff), dtype=torch.int32, device=device) for _ in self.ANCHORS]
+        self.cnt = [torch.empty((self.L,), dtype=torch.int32, device=device) for _ in self.ANCHORS]
+        self.ya = torch.empty((self.L, 1, self.T, self.d), dtype=torch.float32, device=device)
+        self.ha = torch.empty((self.L, 1, self.k, self.T), dtype=torch.float32, device=device)
+        self.y = torch.empty_like(self.xs[0])
+        self.ws = rm.workspace(self.d, self.d_ff, rm.RM_BF16, 1, self.T, self.k, device=device)
+        self.ws_dense = rm.workspace(self.d, self.d_ff, rm.RM_BF16, 1, self.T, self.d_ff, device=device)
+        self.layer_steps = self.steps * self.L
+
+    def step(self, i: int) -> None:
+        rm, layers = self.rm, self.layer_copies[i % self.rotate]
+        for s in range(self.steps):
+            if s in self.ANCHORS:
+                g = self.ANCHORS.index(s)
+                rm.rm_mask_compact(self.masks[g], self.idx[g], self.cnt[g])
+                rm.rm_anchor_ffn_stack(self.xs[s], self.y, layers, self.idx[g], self.cnt[g], self.k, self.ya,
+                                       self.ha, self.ws_dense)
+            else:
+                rm.rm_delta_ffn_stack(self.xs[s], self.y, layers, self.idx[g], self.cnt[g], self.k, self.ya,
+                                      self.ha, self.ws)
+
+    @property
+    def active_bytes(self) -> int:  # anchors read every row, later steps the listed rows
+        n_anchor = len(self.ANCHORS)
+        return self.L * (n_anchor * active_weight_bytes(self.d_ff, self.d, 2)
+                         + (self.steps - n_anchor) * active_weight_bytes(self.k, self.d, 2))
+
+    def hooked_bytes(self):  # the first gate/up and down launches of a step: layer 0 of the first anchor
         return gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2)
 
 
@@ -452,7 +529,8 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "copies": args.steps}))
         return 0
-    setup = {"c3": StackSetup3, "c5": StackSetup5}.get(args.workload, Setup)(args.workload, dev, cold=True)
+    setup = {"c3": StackSetup3, "c3-eq4": StackSetupEq4, "c5": StackSetup5}.get(args.workload, Setup)(
+        args.workload, dev, cold=True)
 
     if args.profile_only:
         time_graph(setup, args.steps, args.warmup)
@@ -490,7 +568,8 @@ def main(argv=None) -> int:
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": setup.spec["name"], "d": setup.d, "d_ff": setup.d_ff, "T": setup.T, "B": setup.B,
-                   "active_neurons": setup.k, "layers": setup.L, "step": STEP_TEXT[setup.key[:2]],
+                   "active_neurons": setup.k, "layers": setup.L,
+                   "step": STEP_TEXT.get(setup.key, STEP_TEXT[setup.key[:2]]),
                    "weights": f"cold: {setup.copies} rotating copies "
                               f"({setup.copies * setup.L * 3 * setup.d * setup.d_ff * 2 / 2**30:.2f} GiB)"},
         "us_per_layer": round(ms * 1e3 / setup.layer_steps, 3),

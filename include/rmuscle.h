@@ -87,8 +87,8 @@ typedef struct rm_ffn_layer_weights {
 rm_status rm_mask_compact(const uint8_t *mask, int32_t n_masks, int32_t d_ff, int32_t *idx, int32_t *count,
                           void *stream);
 
-/* Workspace bytes (written to *bytes, a host pointer) needed by rm_sparse_ffn_layer / rm_sparse_ffn_stack /
- * rm_dense_ffn_ref for B samples of T tokens with at most max_count listed neurons per sample and layer
+/* Workspace bytes (written to *bytes, a host pointer) needed by the FFN calls (rm_sparse_ffn_*, rm_masked_ffn_*,
+ * rm_dense_ffn_ref, rm_anchor_ffn_stack, rm_delta_ffn_stack) for B samples of T tokens with at most max_count listed neurons per sample and layer
  * (max_count = d_ff for the dense call).  The workspace is scratch owned by the caller: 256-byte aligned
  * device memory, contents need not be initialized, reused by every layer of a call, and it must not be used by
  * two calls that may run at the same time. */
@@ -114,6 +114,27 @@ rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_layer_weights 
 rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
                               int32_t T, const float *x, float *y, const int32_t *idx, const int32_t *count,
                               int32_t max_count, void *ws, size_t ws_bytes, void *stream);
+
+/* rm_mask_compact followed by rm_sparse_ffn_layer, with the compaction run in the same launch as the layer's
+ * first kernel (the two are independent), for a step that takes a freshly retrieved mask (section 4.1: the
+ * reference's mask is compacted into its index list; section 5: one mask per layer and group).
+ *   mask:  uint8 [B][d_ff], nonzero = active.
+ *   idx, count: out, int32 [B][d_ff] and [B], written exactly as rm_mask_compact writes them, so that the
+ *          group's later steps can call rm_sparse_ffn_layer with them.
+ *   max_count: in [0, d_ff], at least the number of active neurons of every mask (d_ff is always safe); a mask
+ *          with more active neurons than max_count contributes only its first max_count neurons.
+ * Other arguments, the workspace size and the errors as for rm_sparse_ffn_layer; idx and count must not
+ * overlap the masks, x, y, the workspace or each other. */
+rm_status rm_masked_ffn_layer(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
+                              const float *x, float *y, const uint8_t *mask, int32_t *idx, int32_t *count,
+                              int32_t max_count, void *ws, size_t ws_bytes, void *stream);
+
+/* rm_mask_compact of L * B masks followed by rm_sparse_ffn_stack, the compaction in the launch of the stack's
+ * first kernel.  mask: uint8 [L][B][d_ff]; idx int32 [L][B][d_ff] and count int32 [L][B] out.  Otherwise as
+ * rm_masked_ffn_layer and rm_sparse_ffn_stack. */
+rm_status rm_masked_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
+                              int32_t T, const float *x, float *y, const uint8_t *mask, int32_t *idx,
+                              int32_t *count, int32_t max_count, void *ws, size_t ws_bytes, void *stream);
 
 /* The dense FFN layer with residual: every neuron active (the anchor step of a group, section 4.1, and the
  * dense fallback of section 5).  Same arguments as rm_sparse_ffn_layer without the lists; the workspace is

@@ -37,7 +37,7 @@ RM_KERNEL_GATEUP = 0
 RM_KERNEL_DOWN = 1
 
 EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_stack",
-            "rm_dense_ffn_ref", "rm_anchor_ffn_stack", "rm_delta_ffn_stack", "rm_profile_kernel_events",
+            "rm_masked_ffn_layer", "rm_masked_ffn_stack", "rm_dense_ffn_ref", "rm_anchor_ffn_stack", "rm_delta_ffn_stack", "rm_profile_kernel_events",
             "rm_status_string", "rm_last_error")
 
 Layer = Tuple[torch.Tensor, torch.Tensor, torch.Tensor, Optional[torch.Tensor]]
@@ -83,6 +83,8 @@ def load_library() -> ctypes.CDLL:
         "rm_workspace_size": [sp, i32, i32, i32, ctypes.POINTER(sz)],
         "rm_sparse_ffn_layer": [sp, wp, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp],
         "rm_sparse_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp],
+        "rm_masked_ffn_layer": [sp, wp, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp],
+        "rm_masked_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp],
         "rm_dense_ffn_ref": [sp, wp, i32, i32, vp, vp, vp, sz, vp],
         "rm_anchor_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
         "rm_delta_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
@@ -257,6 +259,40 @@ def rm_sparse_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer
     _check(load_library().rm_sparse_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
                                               idx.data_ptr(), count.data_ptr(), int(max_count), wp, wn,
                                               _stream(stream)))
+
+
+def _masks(mask: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, n: int, d_ff: int) -> None:
+    _need_cuda("mask", mask, (torch.uint8, torch.bool))
+    _need_cuda("idx", idx, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    if mask.numel() != n * d_ff or idx.numel() != n * d_ff or count.numel() != n:
+        raise ValueError(f"mask and idx must hold {n} x d_ff={d_ff} and count {n} entries")
+
+
+def rm_masked_ffn_layer(x: torch.Tensor, y: torch.Tensor, layer: Layer, mask: torch.Tensor, idx: torch.Tensor,
+                        count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6,
+                        stream=None) -> None:
+    """rm_mask_compact(mask -> idx, count) + rm_sparse_ffn_layer, the compaction inside the layer's first launch."""
+    shape = _shape(layer, eps)
+    w = _weights(layer)
+    B, T = _activations(x, y, shape.d)
+    _masks(mask, idx, count, B, shape.d_ff)
+    wp, wn = _ws(ws)
+    _check(load_library().rm_masked_ffn_layer(ctypes.byref(shape), ctypes.byref(w), B, T, x.data_ptr(),
+                                              y.data_ptr(), mask.data_ptr(), idx.data_ptr(), count.data_ptr(),
+                                              int(max_count), wp, wn, _stream(stream)))
+
+
+def rm_masked_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], mask: torch.Tensor,
+                        idx: torch.Tensor, count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6,
+                        stream=None) -> None:
+    """rm_mask_compact of [L][B] masks + rm_sparse_ffn_stack, the compaction inside the stack's first launch."""
+    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps)
+    _masks(mask, idx, count, L * B, shape.d_ff)
+    wp, wn = _ws(ws)
+    _check(load_library().rm_masked_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
+                                              mask.data_ptr(), idx.data_ptr(), count.data_ptr(), int(max_count),
+                                              wp, wn, _stream(stream)))
 
 
 def rm_anchor_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,

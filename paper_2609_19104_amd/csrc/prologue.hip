@@ -1,6 +1,6 @@
 // First layer's FFN input: xn = x * g (or x without a norm) in the FFN kernels' input dtype, plus the row's
 // sums of squares for the RMSNorm factor.  Also the identity index lists with which the dense reference runs the
-// sparse kernels.
+// sparse kernels, and the launch that runs the mask compaction beside the prologue (the calls that take masks).
 //
 // The action expert normalizes each FFN input (the layer is x + FFN(RMSNorm(x)) with RMSNorm(x) =
 // x / sqrt(mean(x^2) + eps) * g).  The per-token factor is applied by the gate/up kernel after its matrix-core
@@ -9,7 +9,7 @@
 // gate/up kernel adds in block order.
 #include <algorithm>
 
-#include "rm_internal.h"
+#include "rm_units.h"
 
 namespace {
 
@@ -19,36 +19,24 @@ template <bool kBf16Out>
 __global__ __launch_bounds__(kThreads) void prologue_kernel(const float *__restrict__ x,
                                                             const float *__restrict__ g, int d, int nblk,
                                                             void *__restrict__ xn, float *__restrict__ ssq) {
-    const int row = blockIdx.x / nblk;
-    const int blk = blockIdx.x - row * nblk;
-    const int c = blk * rm::kRowBlock + static_cast<int>(threadIdx.x) * 4;
-    const size_t o = static_cast<size_t>(row) * d + c;
-    float ss = 0.0f;
-    if (c < d) {
-        float4 v = *reinterpret_cast<const float4 *>(x + o);
-        if (g != nullptr) {
-            ss = fmaf(v.x, v.x, ss);
-            ss = fmaf(v.y, v.y, ss);
-            ss = fmaf(v.z, v.z, ss);
-            ss = fmaf(v.w, v.w, ss);
-            const float4 gv = *reinterpret_cast<const float4 *>(g + c);
-            v.x *= gv.x;
-            v.y *= gv.y;
-            v.z *= gv.z;
-            v.w *= gv.w;
-        }
-        if constexpr (kBf16Out) {
-            uint2 packed;
-            packed.x = rm_f32_to_bf16_bits(v.x) | (rm_f32_to_bf16_bits(v.y) << 16);
-            packed.y = rm_f32_to_bf16_bits(v.z) | (rm_f32_to_bf16_bits(v.w) << 16);
-            *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(xn) + o) = packed;
-        } else {
-            *reinterpret_cast<float4 *>(static_cast<float *>(xn) + o) = v;
-        }
+    rm_units::prologue_unit<kBf16Out>(x, g, d, nblk, xn, ssq, blockIdx.x, threadIdx.x);
+}
+
+// Compaction and prologue in one launch (they are independent): workgroups [0, n_compact) each compact one
+// (mask, segment) unit; each later workgroup runs the prologue of four (row, column block) units, one per wave.
+template <bool kBf16Out>
+__global__ __launch_bounds__(rm_units::kCompactThreads) void compact_prologue_kernel(
+    const uint8_t *__restrict__ mask, int d_ff, int nseg, int n_compact, int32_t *__restrict__ idx,
+    int32_t *__restrict__ count, const float *__restrict__ x, const float *__restrict__ g, int d, int nblk,
+    int units, void *__restrict__ xn, float *__restrict__ ssq) {
+    const int w = static_cast<int>(blockIdx.x);
+    if (w < n_compact) {
+        const int m = w / nseg;
+        rm_units::compact_segment(mask, d_ff, m, w - m * nseg, idx, count);
+        return;
     }
-    if (g == nullptr) return;
-    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-    if (threadIdx.x == 0) ssq[blockIdx.x] = ss;  // [row][blk]
+    const int unit = (w - n_compact) * (rm_units::kCompactThreads / 64) + static_cast<int>(threadIdx.x >> 6);
+    if (unit < units) rm_units::prologue_unit<kBf16Out>(x, g, d, nblk, xn, ssq, unit, threadIdx.x & 63);
 }
 
 __global__ __launch_bounds__(256) void identity_lists_kernel(int32_t *idx, int32_t *count, int d_ff, int B) {
@@ -70,6 +58,27 @@ hipError_t launch_identity_lists(const Plan &p, void *ws, hipStream_t st) {
     const size_t n = static_cast<size_t>(p.B) * p.d_ff;
     const int blocks = static_cast<int>(std::min<size_t>((n + 255) / 256, 1024));
     hipLaunchKernelGGL(identity_lists_kernel, dim3(blocks), dim3(256), 0, st, idx, count, p.d_ff, p.B);
+    return hipGetLastError();
+}
+
+hipError_t launch_compact_prologue(const Plan &p, const uint8_t *mask, int n_masks, int32_t *idx, int32_t *count,
+                                   const float *x, const float *norm_g, void *ws, hipStream_t st) {
+    char *base = static_cast<char *>(ws);
+    void *xn = base + p.off_xn;
+    float *ssq = reinterpret_cast<float *>(base + p.off_ssq);
+    const int nblk = (p.d + kRowBlock - 1) / kRowBlock;
+    const int nseg = (p.d_ff + rm_units::kSeg - 1) / rm_units::kSeg;
+    const int n_compact = nseg * n_masks;
+    const int units = p.B * p.T * nblk;
+    const int per = rm_units::kCompactThreads / 64;
+    const dim3 grid(n_compact + (units + per - 1) / per);
+    const dim3 block(rm_units::kCompactThreads);
+    if (p.wdtype == RM_BF16)
+        hipLaunchKernelGGL(compact_prologue_kernel<true>, grid, block, 0, st, mask, p.d_ff, nseg, n_compact, idx,
+                           count, x, norm_g, p.d, nblk, units, xn, ssq);
+    else
+        hipLaunchKernelGGL(compact_prologue_kernel<false>, grid, block, 0, st, mask, p.d_ff, nseg, n_compact, idx,
+                           count, x, norm_g, p.d, nblk, units, xn, ssq);
     return hipGetLastError();
 }
 

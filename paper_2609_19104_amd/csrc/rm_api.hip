@@ -142,10 +142,14 @@ struct AnchorTerms {
 
 // Layers 0..L-1 of one call; w[l] are the layers' weights, lists at idx + l * list_stride and counts at
 // count + l * count_stride (both strides 0 when every layer uses the same lists, as the dense calls do).
+// A non-null mask ([n_masks][d_ff]) is compacted into idx / count in the prologue's launch.
 rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, const float *x, float *y,
                      const int32_t *idx, const int32_t *count, size_t list_stride, size_t count_stride, void *ws,
-                     hipStream_t st, const AnchorTerms &at = AnchorTerms{}) {
-    hipError_t e = rm::launch_prologue(p, x, w[0].norm_g, ws, st);
+                     hipStream_t st, const AnchorTerms &at = AnchorTerms{}, const uint8_t *mask = nullptr,
+                     int n_masks = 0) {
+    hipError_t e = mask ? rm::launch_compact_prologue(p, mask, n_masks, const_cast<int32_t *>(idx),
+                                                      const_cast<int32_t *>(count), x, w[0].norm_g, ws, st)
+                        : rm::launch_prologue(p, x, w[0].norm_g, ws, st);
     if (e != hipSuccess) return hip_fail(e, "prologue launch");
     const bool bf = p.wdtype == RM_BF16;
     const size_t y_stride = static_cast<size_t>(p.B) * p.T * p.d;
@@ -330,6 +334,62 @@ RM_EXPORT rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
     }
     st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
                     static_cast<hipStream_t>(stream));
+    return st == RM_OK ? ok() : st;
+}
+
+// Checks of the masks of a call that compacts them (n_masks = L * B masks of d_ff bytes into idx / count).
+static rm_status check_masks(const rm_ffn_shape *s, int n_masks, int B, int T, const uint8_t *mask, const int32_t *idx,
+                      const int32_t *count, const float *x, const float *y, const void *ws, size_t ws_bytes) {
+    if (!mask) return fail(RM_ERR_INVALID_ARG, "mask is NULL");
+    const int nseg = ceil_div(s->d_ff, 1024);
+    const long long units = static_cast<long long>(B) * T * ceil_div(s->d, rm::kRowBlock);
+    if (static_cast<long long>(n_masks) * nseg + (units + 3) / 4 > 0x7fffffffLL)
+        return fail(RM_ERR_SHAPE, "%d masks of d_ff=%d and B x T = %d x %d rows are too many for one launch",
+                    n_masks, s->d_ff, B, T);
+    const size_t mbytes = static_cast<size_t>(n_masks) * s->d_ff;
+    const size_t act = static_cast<size_t>(B) * T * s->d * sizeof(float);
+    const void *outs[2] = {idx, count};
+    const size_t out_bytes[2] = {mbytes * 4, static_cast<size_t>(n_masks) * 4};
+    for (int i = 0; i < 2; ++i)
+        if (ranges_overlap(outs[i], out_bytes[i], mask, mbytes) || ranges_overlap(outs[i], out_bytes[i], x, act) ||
+            ranges_overlap(outs[i], out_bytes[i], y, act) || ranges_overlap(outs[i], out_bytes[i], ws, ws_bytes))
+            return fail(RM_ERR_INVALID_ARG, "idx and count must not overlap the masks, x, y or the workspace");
+    if (ranges_overlap(idx, out_bytes[0], count, out_bytes[1]))
+        return fail(RM_ERR_INVALID_ARG, "idx and count must not overlap");
+    return RM_OK;
+}
+
+RM_EXPORT rm_status rm_masked_ffn_layer(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
+                                        const float *x, float *y, const uint8_t *mask, int32_t *idx, int32_t *count,
+                                        int32_t max_count, void *ws, size_t ws_bytes, void *stream) {
+    rm::Plan p;
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    if (st != RM_OK) return st;
+    st = check_layer(w, 0);
+    if (st != RM_OK) return st;
+    st = check_masks(s, B, B, T, mask, idx, count, x, y, ws, ws_bytes);
+    if (st != RM_OK) return st;
+    st = run_layers(p, w, 1, x, y, idx, count, 0, 0, ws, static_cast<hipStream_t>(stream), AnchorTerms{}, mask, B);
+    return st == RM_OK ? ok() : st;
+}
+
+RM_EXPORT rm_status rm_masked_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
+                                        int32_t T, const float *x, float *y, const uint8_t *mask, int32_t *idx,
+                                        int32_t *count, int32_t max_count, void *ws, size_t ws_bytes, void *stream) {
+    if (L <= 0) return fail(RM_ERR_INVALID_ARG, "L=%d must be positive", L);
+    if (!w) return fail(RM_ERR_INVALID_ARG, "weights pointer is NULL");
+    rm::Plan p;
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    if (st != RM_OK) return st;
+    for (int l = 0; l < L; ++l) {
+        st = check_layer(&w[l], l);
+        if (st != RM_OK) return st;
+    }
+    if (static_cast<long long>(L) * B > 0x7fffffffLL) return fail(RM_ERR_SHAPE, "L x B is too large");
+    st = check_masks(s, L * B, B, T, mask, idx, count, x, y, ws, ws_bytes);
+    if (st != RM_OK) return st;
+    st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
+                    static_cast<hipStream_t>(stream), AnchorTerms{}, mask, L * B);
     return st == RM_OK ? ok() : st;
 }
 

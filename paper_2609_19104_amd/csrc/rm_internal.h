@@ -70,6 +70,10 @@ hipError_t launch_identity_lists(const Plan &p, void *ws, hipStream_t st);
 // squares.
 hipError_t launch_prologue(const Plan &p, const float *x, const float *norm_g, void *ws, hipStream_t st);
 
+// rm_mask_compact of n_masks masks and launch_prologue in one launch.
+hipError_t launch_compact_prologue(const Plan &p, const uint8_t *mask, int n_masks, int32_t *idx, int32_t *count,
+                                   const float *x, const float *norm_g, void *ws, hipStream_t st);
+
 // Gate/up projection of the listed neurons + SiLU * up -> H in the workspace.  norm: scale by the per-token
 // RMSNorm factor formed from the workspace's sums of squares.
 // Eq. 4 (both optional, [B][max_count][T] float32): h_anchor is subtracted from h before it goes into H (a

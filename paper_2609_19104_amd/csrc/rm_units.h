@@ -1,0 +1,148 @@
+// Device bodies shared by the mask-compaction, prologue and fused compaction + prologue kernels: one
+// workgroup's compaction of a (mask, segment) unit and one wave's prologue of a (token row, column block) unit.
+// See mask_compact.hip and prologue.hip for what they compute.
+#pragma once
+
+#include "rm_internal.h"
+
+namespace rm_units {
+
+constexpr int kCompactThreads = 256;
+constexpr int kSeg = 4 * kCompactThreads;  // neurons per compaction workgroup
+
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t v) {
+    return ((v & 0x000000ffu) ? 1u : 0u) | ((v & 0x0000ff00u) ? 2u : 0u) | ((v & 0x00ff0000u) ? 4u : 0u) |
+           ((v & 0xff000000u) ? 8u : 0u);
+}
+
+// Sum of v over the workgroup (kCompactThreads threads).
+__device__ __forceinline__ int block_sum(int v, int *lds) {
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    const int wave = threadIdx.x >> 6;
+    __syncthreads();  // lds may still be read by a previous call
+    if ((threadIdx.x & 63) == 0) lds[wave] = v;
+    __syncthreads();
+    return lds[0] + lds[1] + lds[2] + lds[3];
+}
+
+// Mask m, segment s (neurons [s * kSeg, (s + 1) * kSeg)) -> the segment's part of idx[m] and, for s == 0,
+// count[m].  All kCompactThreads threads of the workgroup take part.
+__device__ __forceinline__ void compact_segment(const uint8_t *__restrict__ mask, int d_ff, int m, int s,
+                                                int32_t *__restrict__ idx, int32_t *__restrict__ count) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const uint8_t *row = mask + static_cast<size_t>(m) * d_ff;
+    int32_t *out = idx + static_cast<size_t>(m) * d_ff;
+    const int seg0 = s * kSeg;
+    const int seg1 = min(seg0 + kSeg, d_ff);
+    __shared__ int lds[kCompactThreads / 64];
+    // This segment's mask bytes, kept as they pass through step 1.
+    __shared__ __attribute__((aligned(16))) uint32_t seg_bytes[kSeg / 4];
+
+    // 1. Active neurons before the segment and in the whole mask.
+    int before = 0, total = 0;
+    const bool al16 = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
+    const int n16 = al16 ? d_ff / 16 : 0;  // whole 16-byte units (they never straddle a segment boundary)
+    // Four units per thread are loaded before any is counted (one wait per 16 KB of mask); units past the end
+    // re-read the last unit and are not counted.
+    constexpr int kBatch = 4;
+    for (int u0 = tid; u0 < n16; u0 += kBatch * kCompactThreads) {
+        uint4 v[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i)
+            v[i] = *reinterpret_cast<const uint4 *>(row + min(u0 + i * kCompactThreads, n16 - 1) * 16);
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            const int u = u0 + i * kCompactThreads;
+            const int c = __popc(nonzero_bytes(v[i].x)) + __popc(nonzero_bytes(v[i].y)) +
+                          __popc(nonzero_bytes(v[i].z)) + __popc(nonzero_bytes(v[i].w));
+            if (u < n16) {
+                total += c;
+                if (u * 16 < seg0) before += c;
+                if (u * 16 >= seg0 && u * 16 < seg1)
+                    *reinterpret_cast<uint4 *>(&seg_bytes[(u * 16 - seg0) / 4]) = v[i];
+            }
+        }
+    }
+    for (int p = n16 * 16 + tid; p < d_ff; p += kCompactThreads) {  // unaligned rows, the ragged end: bytewise
+        const uint8_t m8 = row[p];
+        const int c = m8 != 0;
+        total += c;
+        if (p < seg0) before += c;
+        if (p >= seg0 && p < seg1) reinterpret_cast<uint8_t *>(seg_bytes)[p - seg0] = m8;
+    }
+    before = block_sum(before, lds);
+    total = block_sum(total, lds);
+
+    // 2. This thread's 4 neurons of the segment (from LDS: every byte of [seg0, seg1) was stored in step 1, and
+    //    block_sum's barriers made it visible), their exclusive prefix within the segment, and the writes.
+    const int p0 = seg0 + 4 * tid;
+    uint32_t bits = 0;
+    if (p0 < seg1) {
+        bits = nonzero_bytes(seg_bytes[tid]);
+        if (p0 + 4 > seg1) bits &= (1u << (seg1 - p0)) - 1u;  // bytes past the mask are not neurons
+    }
+    const int mine = __popc(bits);
+    int incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off);
+        if (lane >= off) incl += v;
+    }
+    __syncthreads();  // lds was read by block_sum
+    if (lane == 63) lds[wave] = incl;
+    __syncthreads();
+    int before_wave = 0;
+#pragma unroll
+    for (int w = 0; w < kCompactThreads / 64; ++w) before_wave += (w < wave) ? lds[w] : 0;
+    int pos = before + before_wave + incl - mine;
+    while (bits) {
+        const int j = __builtin_ctz(bits);
+        out[pos++] = p0 + j;
+        bits &= bits - 1;
+    }
+
+    // 3. The -1 tail inside this workgroup's index range, and the count.
+    for (int p = max(total, seg0) + tid; p < seg1; p += kCompactThreads) out[p] = -1;
+    if (s == 0 && tid == 0) count[m] = total;
+}
+
+// Prologue of unit = row * nblk + blk (token row, block of 256 columns) by one wave; lane = the thread's lane.
+template <bool kBf16Out>
+__device__ __forceinline__ void prologue_unit(const float *__restrict__ x, const float *__restrict__ g, int d,
+                                              int nblk, void *__restrict__ xn, float *__restrict__ ssq, int unit,
+                                              int lane) {
+    const int row = unit / nblk;
+    const int blk = unit - row * nblk;
+    const int c = blk * rm::kRowBlock + lane * 4;
+    const size_t o = static_cast<size_t>(row) * d + c;
+    float ss = 0.0f;
+    if (c < d) {
+        float4 v = *reinterpret_cast<const float4 *>(x + o);
+        if (g != nullptr) {
+            ss = fmaf(v.x, v.x, ss);
+            ss = fmaf(v.y, v.y, ss);
+            ss = fmaf(v.z, v.z, ss);
+            ss = fmaf(v.w, v.w, ss);
+            const float4 gv = *reinterpret_cast<const float4 *>(g + c);
+            v.x *= gv.x;
+            v.y *= gv.y;
+            v.z *= gv.z;
+            v.w *= gv.w;
+        }
+        if constexpr (kBf16Out) {
+            uint2 packed;
+            packed.x = rm_f32_to_bf16_bits(v.x) | (rm_f32_to_bf16_bits(v.y) << 16);
+            packed.y = rm_f32_to_bf16_bits(v.z) | (rm_f32_to_bf16_bits(v.w) << 16);
+            *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(xn) + o) = packed;
+        } else {
+            *reinterpret_cast<float4 *>(static_cast<float *>(xn) + o) = v;
+        }
+    }
+    if (g == nullptr) return;
+    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+    if (lane == 0) ssq[unit] = ss;  // [row][blk]
+}
+
+}  // namespace rm_units

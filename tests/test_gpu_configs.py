@@ -15,8 +15,8 @@ pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 if not torch.cuda.is_available():
     pytest.skip("needs a GPU", allow_module_level=True)
 
-from gpu_helpers import (TOL_BF16, TOL_F32, compact, dev_weights, errors, run_dense, run_layer,  # noqa: E402
-                         run_stack)
+from gpu_helpers import (TOL_BF16, TOL_F32, compact, dev_weights, errors, run_anchor, run_delta,  # noqa: E402
+                         run_dense, run_layer, run_stack)
 
 
 def _lists(masks):
@@ -73,6 +73,27 @@ def test_config3_stack_schedule():
             y = run_stack(lws, x, idx, cnt, w.k)
             ref = oracle.ffn_stack(x[0], layers64, [m.astype(float) for m in masks])
         _check(y[0], ref, x[0], TOL_BF16, f"config 3 step {s}")
+
+
+def test_config3_anchored_eq4_schedule():
+    # The config-3 stack and inputs under the paper's schedule: dense anchors at steps 0 and 5, Eq. 4 at the
+    # other steps, with each group's masks scored on a similar input (anchor input + 0.1 N(0,1)).
+    w = wl.config3()
+    layers64 = [l.f64() for l in w.layers]
+    lws = [dev_weights(l) for l in w.layers]
+    anchors = (0, 5)
+    refs = wl.group_reference_inputs(w, anchors)
+    for s, x in enumerate(w.x_steps):
+        if s in anchors:
+            masks = oracle.stack_masks_from_dense(refs[anchors.index(s)][0], layers64, w.k)
+            idx, cnt = _lists(masks)
+            y, ya, ha = run_anchor(lws, x, idx, cnt, w.k)
+            y = y.cpu().numpy()
+            ref, ya_ref, ha_ref = oracle.anchor_stack(x[0], layers64)
+        else:
+            y = run_delta(lws, x, idx, cnt, w.k, ya, ha)
+            ref = oracle.delta_stack(x[0], layers64, [m.astype(float) for m in masks], ya_ref, ha_ref)
+        _check(y[0], ref, x[0], TOL_BF16, f"config 3, Eq. 4 schedule, step {s}")
 
 
 def test_config4_density_sweep():

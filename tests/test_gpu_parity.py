@@ -229,3 +229,43 @@ def test_stack_equals_layer_sequence():
     ref = np.stack([oracle.ffn_stack(x[b], [lay.f64() for lay in layers],
                                      [masks[l, b].astype(np.float64) for l in range(L)]) for b in range(B)])
     _check(y_stack, ref, x, TOL_BF16, "stack")
+
+
+# ------------------------------------------------------------------------------------------------ masks in
+
+MASKED_CASES = [
+    # d, d_ff, L, B, T, p (mask density), wdtype, norm
+    (256, 1000, 1, 3, 51, 0.3, "bf16", "random"),
+    (1024, 4096, 1, 1, 51, 0.3, "bf16", "none"),
+    (512, 4095, 2, 2, 17, 0.5, "bf16", "ones"),
+    (256, 16384, 1, 2, 8, 0.1, "bf16", "none"),
+    (128, 300, 3, 2, 9, 0.6, "f32", "random"),
+]
+
+
+@pytest.mark.parametrize("d,d_ff,L,B,T,p,wdtype,norm", MASKED_CASES)
+def test_masked_calls_equal_compaction_then_lists(d, d_ff, L, B, T, p, wdtype, norm):
+    # rm_masked_ffn_layer / _stack = rm_mask_compact + rm_sparse_ffn_layer / _stack, bit for bit, and their
+    # lists are the oracle's.
+    layers = [wl.make_layer(71, l, d, d_ff, wdtype, norm=norm) for l in range(L)]
+    lws = [dev_weights(l) for l in layers]
+    x = wl.make_x(71, (B, T, d), d_ff, T)
+    masks = wl.bernoulli_mask(wl.rng(71, 4, d_ff, L), (L * B, d_ff), p)
+    max_count = int(masks.sum(axis=1).max())
+    idx_ref, cnt_ref = oracle.compact_mask(masks)
+    xt = torch.from_numpy(x).cuda()
+    mt = torch.from_numpy(masks).cuda()
+    idx = torch.full((L * B, d_ff), 777, dtype=torch.int32, device="cuda")
+    cnt = torch.full((L * B,), -3, dtype=torch.int32, device="cuda")
+    y = torch.full_like(xt, float("nan"))
+    ws = rm.workspace(d, d_ff, rm.wdtype_of(lws[0][0]), B, T, max_count)
+    ws.fill_(0x4D)
+    if L == 1:
+        rm.rm_masked_ffn_layer(xt, y, lws[0], mt, idx, cnt, max_count, ws)
+    else:
+        rm.rm_masked_ffn_stack(xt, y, lws, mt, idx, cnt, max_count, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), idx_ref) and np.array_equal(cnt.cpu().numpy(), cnt_ref)
+    i2, c2 = _masks_to_lists(masks)
+    y2 = run_layer(lws[0], x, i2, c2, max_count) if L == 1 else run_stack(lws, x, i2, c2, max_count)
+    assert np.array_equal(y.cpu().numpy().view(np.uint32), y2.view(np.uint32))

@@ -247,6 +247,13 @@ def config3(L: int = 18, d: int = 1024, d_ff: int = 4096, T: int = 51, steps: in
                     k=count_for_percent(30, d_ff), steps=steps, refresh_steps=list(range(1, steps, 2)))
 
 
+def group_reference_inputs(w: Workload, anchors: Sequence[int], scale: float = 0.1) -> List[np.ndarray]:
+    """For the anchored schedule on a config-3 stack: per group, a similar execution's input (the group's anchor
+    input + scale N(0,1)) on which the group's masks are scored (section 4.1 takes them from a reference)."""
+    return [perturb(w.x_steps[a], make_noise(w.cfg, w.x_steps[a].shape, 100 + g, scale=scale))
+            for g, a in enumerate(anchors)]
+
+
 def config4(d: int = 2048, d_ff: int = 16384, T: int = 51, percents: Sequence[int] = (10, 30, 50, 100)) -> Workload:
     """Wide FFN density sweep; nested top-k masks of one score vector computed on x_ref."""
     cfg = 4

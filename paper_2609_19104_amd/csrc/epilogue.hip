@@ -66,18 +66,15 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
     }
     if (xn_next == nullptr) return;
 
-    if (g_next != nullptr) {
-        float ss = 0.0f;
+    if (g_next != nullptr) {  // partial sums of squares of the row's 64-column blocks (lane 16 j: block 4 blk + j)
+        const float ss = rm_ssq64(out, ok);
+        const int part = blk * 4 + static_cast<int>(threadIdx.x >> 4);
+        if ((threadIdx.x & 15) == 0 && part < rm::ssq_parts(d))
+            ssq[static_cast<size_t>(row) * rm::ssq_stride(d) + part] = ss;
         if (ok) {
-            ss = fmaf(out.x, out.x, ss);
-            ss = fmaf(out.y, out.y, ss);
-            ss = fmaf(out.z, out.z, ss);
-            ss = fmaf(out.w, out.w, ss);
             const float4 g = ld4(g_next + cc);
             out = make_float4(out.x * g.x, out.y * g.y, out.z * g.z, out.w * g.w);
         }
-        for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-        if (threadIdx.x == 0) ssq[blockIdx.x] = ss;  // [row][blk]
     }
     if (!ok) return;
     if constexpr (kBf16Xn) {

@@ -40,6 +40,7 @@ constexpr int kGuThreads = 512;
 constexpr int kGuWaves = kGuThreads / 64;
 constexpr int kDnThreads = 256;
 constexpr int kDnWaves = kDnThreads / 64;
+constexpr int kDfThreads = rm::kDfWaves * 64;
 constexpr int kChunkCols = 256;   // staged gate/up: xn columns per LDS chunk (8 K steps)
 constexpr int kChunkSteps = kChunkCols / 32;
 constexpr int kRowPitch = kChunkCols + 8;  // bf16 elements per LDS row (16 bytes of padding against conflicts)
@@ -704,6 +705,133 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
     }
 }
 
+// Down projection with the epilogue fused, for lists of at most kDfMaxChunks chunks.  Workgroup: one column
+// tile of 64 columns, one tile of 16 tokens, one sample; its 8 waves take the list's chunks in turn (chunk
+// wave + 8 k, k < CPW: every load is issued before the first product), each keeping a 16 x 64 fp32 tile, and
+// the 8 tiles are summed in wave order through LDS.  Then y = x + acc (x + (y_a + acc) for Eq. 4), y_a = acc on
+// an anchor step, and inside a stack the next layer's input xn = y * g in bf16 with the row's partial sum of
+// squares for this 64-column block.  No partials leave the workgroup, so no epilogue launch follows.
+struct DfArgs {
+    const uint16_t *H, *wd;
+    const int32_t *idx, *count;
+    int d_ff, d, T, tpad, kcap, max_count, B, ncol, ntt;
+    const float *x;
+    float *y;
+    const float *ya_in;
+    float *ya_out;
+    const float *g_next;  // with xn_next: the next layer's norm gain, or null for no norm
+    uint16_t *xn_next;    // the next layer's FFN input, or null
+    float *ssq;
+};
+
+template <int CPW>
+__global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
+    const int q = xcd_logical(blockIdx.x, gridDim.x);  // = (sample * ncol + column tile) * ntt + token tile
+    const int tt = q % a.ntt;
+    const int ct = (q / a.ntt) % a.ncol;
+    const int b = q / (a.ntt * a.ncol);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int grp = lane >> 4;  // K group: slots 8*grp .. 8*grp+7 of a chunk
+    const int nn = lane & 15;   // A row (token in tile) and B column group (physical columns 4*nn + q)
+    const int colw = ct * rm::kBfColTile + nn * 4;
+    const bool colok = colw < a.d;
+    const int col = min(colw, a.d - 4);  // columns past d re-read column d-4; those outputs are not stored
+    const int nchunks = a.kcap / rm::kBfChunk;
+    const int t0 = tt * 16;
+    const uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
+
+    // The list's neuron indices (clamped into [0, d_ff)) are staged once in LDS.
+    constexpr int kIdxPerThread = rm::kDfMaxChunks * rm::kBfChunk / kDfThreads;
+    __shared__ __attribute__((aligned(16))) int sidx[rm::kDfMaxChunks * rm::kBfChunk];
+    int iv[kIdxPerThread];
+#pragma unroll
+    for (int i = 0; i < kIdxPerThread; ++i)
+        iv[i] = a.idx[static_cast<size_t>(b) * a.d_ff + min(min(tid + i * kDfThreads, a.kcap - 1), a.d_ff - 1)];
+    int cnt = a.count[b];
+    __builtin_amdgcn_sched_barrier(0);  // the index loads go out first
+
+    auto chunk_of = [&](int k) { return min(wave + k * rm::kDfWaves, nchunks - 1); };
+    DnChunk<1> cb[CPW];
+#pragma unroll
+    for (int k = 0; k < CPW; ++k)  // chunk-major H: 16 tokens x 64 bytes, one contiguous kilobyte
+        cb[k].a[0] = load16(Hb + (static_cast<size_t>(chunk_of(k)) * a.tpad + t0 + nn) * rm::kBfChunk + grp * 8);
+    __builtin_amdgcn_sched_barrier(0);  // then the H tiles, before the wait for the indices
+#pragma unroll
+    for (int i = 0; i < kIdxPerThread; ++i) {
+        const int s = tid + i * kDfThreads;
+        if (s < a.kcap) sidx[s] = clamp_neuron(iv[i], a.d_ff);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < CPW; ++k) {
+        const int kb = chunk_of(k) * rm::kBfChunk + grp * 8;
+        const int4 i0 = *reinterpret_cast<const int4 *>(sidx + kb);
+        const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb + 4);
+        const int n[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cb[k].w[j] = load8(a.wd + static_cast<size_t>(n[j]) * a.d + col);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    rm_f32x4 acc[1][4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[0][c] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < CPW; ++k)
+        if (wave + k * rm::kDfWaves < nchunks) dn_mma(cb[k], acc);
+
+    __shared__ rm_f32x4 red[rm::kDfWaves][4][64];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) red[wave][c][lane] = acc[0][c];
+    __syncthreads();
+    if (wave >= 4) return;
+
+    // Wave i finishes token 4 * grp + i of the tile (lane L, register i of a tile: token 4*(L/16)+i, physical
+    // column 4*(L%16) + q of call q): the 8 waves' sums in wave order.
+    const int i = wave;
+    float v[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        v[c] = red[0][c][lane][i];
+#pragma unroll
+        for (int w = 1; w < rm::kDfWaves; ++w) v[c] += red[w][c][lane][i];
+    }
+    const int t = t0 + grp * 4 + i;
+    const bool live = t < a.T;
+    const size_t ro = (static_cast<size_t>(b) * a.T + min(t, a.T - 1)) * a.d + col;
+    const float4 acc4 = make_float4(v[0], v[1], v[2], v[3]);
+    float4 out = *reinterpret_cast<const float4 *>(a.x + ro);
+    cnt = cnt < 0 ? 0 : (cnt > a.max_count ? a.max_count : cnt);
+    if (a.ya_in != nullptr) {  // Eq. 4: y = x + (y_a + (h - h_a) W_down)
+        const float4 ya = *reinterpret_cast<const float4 *>(a.ya_in + ro);
+        out = make_float4(out.x + (ya.x + acc4.x), out.y + (ya.y + acc4.y), out.z + (ya.z + acc4.z),
+                          out.w + (ya.w + acc4.w));
+    } else if (cnt > 0) {  // an empty list leaves y = x bit for bit
+        out = make_float4(out.x + acc4.x, out.y + acc4.y, out.z + acc4.z, out.w + acc4.w);
+    }
+    const bool st = live && colok;
+    if (st) {
+        *reinterpret_cast<float4 *>(a.y + ro) = out;
+        if (a.ya_out != nullptr) *reinterpret_cast<float4 *>(a.ya_out + ro) = acc4;
+    }
+    if (a.xn_next == nullptr) return;
+    if (a.g_next != nullptr) {
+        const float ss = rm_ssq64(out, colok);
+        const int row = b * a.T + t;
+        if (nn == 0 && live) a.ssq[static_cast<size_t>(row) * rm::ssq_stride(a.d) + ct] = ss;
+        const float4 g = *reinterpret_cast<const float4 *>(a.g_next + col);
+        out = make_float4(out.x * g.x, out.y * g.y, out.z * g.z, out.w * g.w);
+    }
+    if (st) {
+        uint2 packed;
+        packed.x = rm_f32_to_bf16_bits(out.x) | (rm_f32_to_bf16_bits(out.y) << 16);
+        packed.y = rm_f32_to_bf16_bits(out.z) | (rm_f32_to_bf16_bits(out.w) << 16);
+        *reinterpret_cast<uint2 *>(a.xn_next + ro) = packed;
+    }
+}
+
 int token_tiles(int T) {
     const int tiles = (T + 15) / 16;
     return tiles >= 4 ? 4 : tiles;
@@ -813,6 +941,46 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
     }
     hipError_t e = hipGetLastError();
     return e;
+}
+
+hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
+                             const float *x, float *y, const float *g_next, bool emit_xn, const float *ya_in,
+                             float *ya_out, void *ws, hipStream_t st) {
+    char *base = static_cast<char *>(ws);
+    DfArgs a;
+    a.H = reinterpret_cast<const uint16_t *>(base + p.off_h);
+    a.wd = static_cast<const uint16_t *>(w_down);
+    a.idx = idx;
+    a.count = count;
+    a.d_ff = p.d_ff;
+    a.d = p.d;
+    a.T = p.T;
+    a.tpad = p.tpad;
+    a.kcap = p.kcap;
+    a.max_count = p.max_count;
+    a.B = p.B;
+    a.ncol = p.ncol;
+    a.ntt = p.ntt;
+    a.x = x;
+    a.y = y;
+    a.ya_in = ya_in;
+    a.ya_out = ya_out;
+    a.g_next = emit_xn ? g_next : nullptr;
+    a.xn_next = emit_xn ? reinterpret_cast<uint16_t *>(base + p.off_xn) : nullptr;
+    a.ssq = reinterpret_cast<float *>(base + p.off_ssq);
+    const dim3 grid(p.ncol * p.ntt * p.B);
+    const dim3 block(kDfThreads);
+    switch (p.dn_cpw) {
+        case 1: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<1>, grid, block, st, a); break;
+        case 2: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<2>, grid, block, st, a); break;
+        case 3: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<3>, grid, block, st, a); break;
+        case 4: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<4>, grid, block, st, a); break;
+        case 5: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<5>, grid, block, st, a); break;
+        case 6: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<6>, grid, block, st, a); break;
+        case 7: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7>, grid, block, st, a); break;
+        default: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8>, grid, block, st, a); break;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, void *ws, hipStream_t st) {

@@ -153,6 +153,10 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
     if (e != hipSuccess) return hip_fail(e, "prologue launch");
     const bool bf = p.wdtype == RM_BF16;
     const size_t y_stride = static_cast<size_t>(p.B) * p.T * p.d;
+    // The fused down projection sums the whole list in each workgroup: fewer, longer workgroups than the split
+    // over K.  On MI355X that pays where the epilogue it replaces is heavy (inside a stack, where it also forms
+    // the next layer's input, or at d >= 2048) and costs a little on a single narrower layer.
+    const bool fused = p.fused_down && (L > 1 || p.d >= 2048);
     for (int l = 0; l < L; ++l) {
         const int32_t *il = idx + l * list_stride;
         const int32_t *cl = count + l * count_stride;
@@ -173,10 +177,15 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
         const bool next = l + 1 < L;
         const float *g_next = next ? w[l + 1].norm_g : nullptr;
         const float *xin = l == 0 ? x : y;
-        e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
-        if (e != hipSuccess) return hip_fail(e, "down launch");
         const float *ya_in = at.ya_in ? at.ya_in + l * y_stride : nullptr;
         float *ya_out = at.ya_out ? at.ya_out + l * y_stride : nullptr;
+        if (fused) {  // down projection and epilogue in one launch
+            e = rm::launch_down_fused(p, w[l].w_down, il, cl, xin, y, g_next, next, ya_in, ya_out, ws, st);
+            if (e != hipSuccess) return hip_fail(e, "down launch");
+            continue;
+        }
+        e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
+        if (e != hipSuccess) return hip_fail(e, "down launch");
         e = rm::launch_epilogue(p, cl, xin, y, g_next, next, ya_in, ya_out, ws, st);
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }
@@ -225,6 +234,10 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         while (cps < 4 * kBfWaves && ceil_div(nchunks, cps) > s_target) cps *= 2;
         q.slice_units = cps;
         q.slices = ceil_div(nchunks, cps);
+        // Short lists of one sample: one workgroup per (column tile, 16-token tile) can sum the whole list.
+        q.fused_down = B == 1 && nchunks <= kDfMaxChunks;
+        q.dn_cpw = ceil_div(nchunks, kDfWaves);
+        q.ntt = ceil_div(T, 16);
         xn_elem = 2;
         h_elem = 2;
     } else {
@@ -242,7 +255,8 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         h_elem = 4;
     }
     if (q.slices > 65535 || static_cast<long long>(q.gate_blocks) * B > 0x7fffffffLL ||
-        static_cast<long long>(q.ncol) * q.slices * B > 0x7fffffffLL)
+        static_cast<long long>(q.ncol) * q.slices * B > 0x7fffffffLL ||
+        static_cast<long long>(q.ncol) * ceil_div(T, 16) * B > 0x7fffffffLL)
         return fail(RM_ERR_SHAPE, "launch grid too large");
     if (static_cast<long long>(B) * T * ceil_div(s->d, kRowBlock) > 0x7fffffffLL)
         return fail(RM_ERR_SHAPE, "B=%d x T=%d rows are too many for one launch", B, T);
@@ -254,7 +268,7 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.off_part = off;
     off = align_up(off + static_cast<size_t>(B) * q.slices * static_cast<size_t>(T) * s->d * 4, 256);
     q.off_ssq = off;
-    off = align_up(off + static_cast<size_t>(B) * T * ceil_div(s->d, kRowBlock) * sizeof(float), 256);
+    off = align_up(off + static_cast<size_t>(B) * T * ssq_stride(s->d) * sizeof(float), 256);
     q.off_ident = off;
     off = align_up(off + static_cast<size_t>(B) * s->d_ff * sizeof(int32_t), 256);
     q.off_ident_count = off;

@@ -24,10 +24,17 @@ constexpr int kBfChunk = 32;        // neurons per down-projection matrix-core s
 constexpr int kBfColTile = 64;      // output columns per down workgroup (16 lanes x 4 columns)
 constexpr int kBfWaves = 4;
 constexpr int kBfMaxChunksPerSlice = 16;  // down: a slice's indices (16 x 32) are staged in 2 KB of LDS
+constexpr int kDfWaves = 8;        // fused down: waves per workgroup
+constexpr int kDfMaxCpw = 8;       // fused down: at most 8 chunks per wave
+constexpr int kDfMaxChunks = kDfWaves * kDfMaxCpw;  // lists of up to 64 chunks (2048 neurons)
 
-// Prologue / epilogue: one wave per (token row, block of 256 columns); the per-token sums of squares of the FFN
-// input are kept as one partial sum per column block.
+// Prologue / epilogue: one wave per (token row, block of 256 columns).
 constexpr int kRowBlock = 256;
+// RMSNorm sums of squares are kept as partial sums over blocks of kSsqCols columns, [row][ssq_stride(d)] with
+// ssq_parts(d) partials per row (the rest of the row is padding, never read into a sum).
+constexpr int kSsqCols = 64;
+__host__ __device__ constexpr int ssq_parts(int d) { return (d + kSsqCols - 1) / kSsqCols; }
+__host__ __device__ constexpr int ssq_stride(int d) { return (ssq_parts(d) + 3) / 4 * 4; }
 
 // f32 path: vector ALU.
 constexpr int kF32TokBlock = 8;     // tokens per register block
@@ -46,10 +53,16 @@ struct Plan {
     int ncol = 0;        // column tiles
     int slices = 0;      // K-slices per column tile (down partial sums)
     int slice_units = 0; // bf16: 32-neuron chunks per slice; f32: neurons per slice
+    // bf16, one sample, lists of at most kDfMaxChunks chunks: the down projection may run fused (one workgroup
+    // per column tile and 16-token tile sums the whole list and applies the residual itself: no partials, no
+    // epilogue launch); the layer driver decides.
+    bool fused_down = false;
+    int dn_cpw = 0;      // fused down: chunks per wave (the kernel's unrolled pipeline depth)
+    int ntt = 0;         // fused down: 16-token tiles
     // Workspace: xn [B][T][d] (bf16 or f32); H (bf16: [B][kcap / 32][tpad][32], chunk-major; f32:
-    // [B][tpad][kcap]); partials f32 [B][slices][T][d]; ssq f32 [B][T][ceil(d / 256)] (per-token sums of squares
-    // of the FFN input by column block, for the RMSNorm factor); and, for the dense reference, the lists
-    // 0 .. d_ff-1 int32 [B][d_ff] and their counts int32 [B].
+    // [B][tpad][kcap]); partials f32 [B][slices][T][d]; ssq f32 [B][T][ssq_stride(d)]
+    // (per-token sums of squares of the FFN input by 64-column block, for the RMSNorm factor); and, for the dense
+    // reference, the lists 0 .. d_ff-1 int32 [B][d_ff] and their counts int32 [B].
     size_t off_xn = 0, off_h = 0, off_part = 0, off_ssq = 0, off_ident = 0, off_ident_count = 0, total = 0;
 };
 
@@ -88,6 +101,11 @@ hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up
 // Down projection of the listed neurons: per-K-slice float32 partials of H W_down[idx] in the workspace.  The
 // bf16 form needs no count: H is zero in every slot past the list.
 hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, void *ws, hipStream_t st);
+// With p.fused_down: the down projection and the epilogue's work in one launch (same results as
+// launch_down_bf16 + launch_epilogue up to the order of the K sum).
+hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
+                             const float *x, float *y, const float *g_next, bool emit_xn, const float *ya_in,
+                             float *ya_out, void *ws, hipStream_t st);
 hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
                            hipStream_t st);
 
@@ -142,11 +160,39 @@ __device__ __forceinline__ float rm_bf16_bits_to_f32(uint32_t b) { return __uint
 // RMSNorm factor of token row `row` (= b * T + t): 1 / sqrt(mean of squares + eps), from the row's partial sums
 // of squares by 256-column block, added in block order.
 __device__ __forceinline__ float rm_token_rnorm(const float *ssq, int row, int d, float eps) {
-    const int nblk = (d + rm::kRowBlock - 1) / rm::kRowBlock;
-    const float *p = ssq + static_cast<size_t>(row) * nblk;
-    float s = p[0];
-    for (int k = 1; k < nblk; ++k) s += p[k];
+    const int n = rm::ssq_parts(d);
+    const int stride4 = rm::ssq_stride(d) / 4;
+    const float4 *p = reinterpret_cast<const float4 *>(ssq + static_cast<size_t>(row) * rm::ssq_stride(d));
+    float s = 0.0f;
+    for (int k0 = 0; k0 < n; k0 += 32) {  // eight float4 loads in flight, then the in-order sum
+        float4 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = p[min(k0 / 4 + i, stride4 - 1)];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int k = k0 + 4 * i;
+            if (k < n) s += v[i].x;
+            if (k + 1 < n) s += v[i].y;
+            if (k + 2 < n) s += v[i].z;
+            if (k + 3 < n) s += v[i].w;
+        }
+    }
     return 1.0f / sqrtf(s / static_cast<float>(d) + eps);
+}
+
+// Sum of squares of 4 columns (one lane's float4), then the sum over the 16 lanes of a lane group (lanes
+// 16 g .. 16 g + 15 hold 64 consecutive columns): a fixed order shared by every kernel that writes the partials,
+// so that a layer's norm factors do not depend on which kernel produced its input.
+__device__ __forceinline__ float rm_ssq64(float4 v, bool ok) {
+    float ss = 0.0f;
+    if (ok) {
+        ss = fmaf(v.x, v.x, ss);
+        ss = fmaf(v.y, v.y, ss);
+        ss = fmaf(v.z, v.z, ss);
+        ss = fmaf(v.w, v.w, ss);
+    }
+    for (int off = 1; off < 16; off <<= 1) ss += __shfl_xor(ss, off);
+    return ss;
 }
 
 // SiLU(z) = z / (1 + e^-z); e^-z overflows to +inf for very negative z, giving -0, never NaN.

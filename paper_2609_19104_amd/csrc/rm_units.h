@@ -117,14 +117,16 @@ __device__ __forceinline__ void prologue_unit(const float *__restrict__ x, const
     const int blk = unit - row * nblk;
     const int c = blk * rm::kRowBlock + lane * 4;
     const size_t o = static_cast<size_t>(row) * d + c;
-    float ss = 0.0f;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (c < d) v = *reinterpret_cast<const float4 *>(x + o);
+    if (g != nullptr) {  // partial sums of squares of the row's 64-column blocks (lane 16 j: block 4 blk + j)
+        const float ss = rm_ssq64(v, c < d);
+        const int part = blk * 4 + (lane >> 4);
+        if ((lane & 15) == 0 && part < rm::ssq_parts(d))
+            ssq[static_cast<size_t>(row) * rm::ssq_stride(d) + part] = ss;
+    }
     if (c < d) {
-        float4 v = *reinterpret_cast<const float4 *>(x + o);
         if (g != nullptr) {
-            ss = fmaf(v.x, v.x, ss);
-            ss = fmaf(v.y, v.y, ss);
-            ss = fmaf(v.z, v.z, ss);
-            ss = fmaf(v.w, v.w, ss);
             const float4 gv = *reinterpret_cast<const float4 *>(g + c);
             v.x *= gv.x;
             v.y *= gv.y;
@@ -140,9 +142,6 @@ __device__ __forceinline__ void prologue_unit(const float *__restrict__ x, const
             *reinterpret_cast<float4 *>(static_cast<float *>(xn) + o) = v;
         }
     }
-    if (g == nullptr) return;
-    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-    if (lane == 0) ssq[unit] = ss;  // [row][blk]
 }
 
 }  // namespace rm_units

@@ -269,3 +269,39 @@ def test_masked_calls_equal_compaction_then_lists(d, d_ff, L, B, T, p, wdtype, n
     i2, c2 = _masks_to_lists(masks)
     y2 = run_layer(lws[0], x, i2, c2, max_count) if L == 1 else run_stack(lws, x, i2, c2, max_count)
     assert np.array_equal(y.cpu().numpy().view(np.uint32), y2.view(np.uint32))
+
+
+# ------------------------------------------------------------------------------------------------ one-sample stacks
+# A single sample's stack (and a single layer at d >= 2048) with a list of at most 2048 neurons runs the down
+# projection fused with the epilogue: one workgroup per (64-column tile, 16-token tile) sums the whole list.
+
+FUSED_CASES = [
+    # d, d_ff, L, T, k, norm
+    (96, 200, 3, 17, 150, "random"),    # a partial column tile, 5 chunks
+    (160, 512, 2, 70, 300, "none"),     # five token tiles (T > 64)
+    (2048, 4096, 1, 51, 1500, "random"),  # one layer at d = 2048
+    (1024, 4096, 2, 1, 2048, "ones"),   # T = 1, 64 chunks (8 per wave)
+    (256, 2048, 3, 64, 1999, "random"),
+]
+
+
+@pytest.mark.parametrize("d,d_ff,L,T,k,norm", FUSED_CASES)
+def test_single_sample_stack_parity(d, d_ff, L, T, k, norm):
+    layers = [wl.make_layer(81, l, d, d_ff, "bf16", norm=norm) for l in range(L)]
+    x = wl.make_x(81, (1, T, d), d_ff, T)
+    masks = np.stack([wl.uniform_mask(wl.rng(81, 4, l, d_ff), d_ff, k - 37 * l) for l in range(L)])
+    idx, cnt = _masks_to_lists(masks)
+    lws = [dev_weights(l) for l in layers]
+    y = run_stack(lws, x, idx, cnt, k)
+    ref = oracle.ffn_stack(x[0], [lay.f64() for lay in layers], [m.astype(np.float64) for m in masks])
+    _check(y[0], ref, x[0], TOL_BF16, f"one-sample stack {d}x{d_ff} L={L} T={T} k={k}")
+
+
+def test_single_sample_stack_empty_lists_are_identity():
+    d, d_ff, L, T = 256, 512, 3, 20
+    layers = [wl.make_layer(82, l, d, d_ff, "bf16", norm="random") for l in range(L)]
+    x = wl.make_x(82, (1, T, d), 0)
+    x[0, 0, :7] = -0.0
+    idx, cnt = _masks_to_lists(np.zeros((L, d_ff), np.uint8))
+    y = run_stack([dev_weights(l) for l in layers], x, idx, cnt, 64)
+    assert np.array_equal(y.view(np.uint32), x.view(np.uint32))

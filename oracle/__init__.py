@@ -6,8 +6,9 @@ package.  It shares no code with the GPU library and never calls it.
 from .ffn import (RMS_EPS, anchor_stack, ceil_budget, compact_mask, contribution_score, delta_stack, dense_ffn,
                   ffn_input, ffn_stack, hidden, local_update, mask_multiplicity, masked_ffn, mean_abs_activation,
                   multiplicity, nested_topk_masks, rel_err, rms_norm, silu, stack_masks_from_dense, topk_mask)
+from . import group_masks
 
 __all__ = ["RMS_EPS", "anchor_stack", "ceil_budget", "compact_mask", "contribution_score", "delta_stack",
            "dense_ffn", "ffn_input", "ffn_stack", "hidden", "local_update", "mask_multiplicity", "masked_ffn",
            "mean_abs_activation", "multiplicity", "nested_topk_masks", "rel_err", "rms_norm", "silu",
-           "stack_masks_from_dense", "topk_mask"]
+           "stack_masks_from_dense", "topk_mask", "group_masks"]

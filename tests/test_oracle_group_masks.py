@@ -1,0 +1,99 @@
+"""Pins for the group-mask oracle (section 5, "Constructing Group Neuron Masks"; Eq. 1 of section 3.4).
+
+Each pin checks the oracle against something fixed independently of it: a library norm, the float64 Eq. 1
+score, exhaustive search over subsets, or a small example worked out by hand."""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import group_masks as gm
+
+
+def test_neuron_norms_match_library_norm():
+    w = np.random.default_rng(1).standard_normal((37, 300)).astype(np.float32) * 0.02
+    ref = np.linalg.norm(w.astype(np.float64), axis=1)
+    got = gm.neuron_norms(w).astype(np.float64)
+    assert np.max(np.abs(got - ref) / ref) < 1e-5
+
+
+def test_scores_match_float64_eq1():
+    r = np.random.default_rng(2)
+    h = r.standard_normal((50, 17)).astype(np.float32)  # [d_ff][T]
+    wd = r.standard_normal((50, 64)).astype(np.float32)
+    got = gm.contribution_scores(h, gm.neuron_norms(wd)).astype(np.float64)
+    ref = oracle.contribution_score(h.T.astype(np.float64), wd.astype(np.float64))  # h as [T][d_ff]
+    assert np.max(np.abs(got - ref) / ref) < 1e-5
+
+
+def test_top_k_matches_stable_sort_and_breaks_ties_low():
+    s = np.array([3, 1, 3, 2, 3, 0], np.float32)
+    assert np.flatnonzero(gm.top_k(s, 2)).tolist() == [0, 2]
+    assert np.flatnonzero(gm.top_k(s, 4)).tolist() == [0, 2, 3, 4]
+    assert gm.top_k(s, 0).sum() == 0 and gm.top_k(s, 9).sum() == 6
+    r = np.random.default_rng(3)
+    for _ in range(20):
+        v = r.integers(0, 5, size=40).astype(np.float32)
+        k = int(r.integers(0, 41))
+        ref = np.zeros(40, bool)
+        ref[np.argsort(-v, kind="stable")[:k]] = True
+        assert np.array_equal(gm.top_k(v, k), ref)
+
+
+def test_worked_example():
+    # Two steps, five neurons, two actions, K = 2, unit down-projection rows (norm 1).
+    # Step 0 sums |h| = [3, 4, 1, 0, 2] -> candidates {1, 0}; step 1 sums = [0, 1, 5, 4, 2] -> {2, 3}.
+    # Summed over the steps: [3, 5, 6, 4, 4]; among the union {0, 1, 2, 3} the top two are 2 (6) and 1 (5).
+    h = np.array([[[1, -2], [4, 0], [0, 1], [0, 0], [1, 1]],
+                  [[0, 0], [-1, 0], [2, 3], [4, 0], [1, -1]]], np.float32)
+    norms = np.ones(5, np.float32)
+    assert np.flatnonzero(gm.group_mask(h, norms, 2)).tolist() == [1, 2]
+    # K = 3: step 0's top 3 = {1, 0, 4}, step 1's = {2, 3, 4}, so the union is all five neurons;
+    # summed top 3 = 2 (6), 1 (5), then 3 and 4 tie at 4 -> the lower index, 3.
+    assert np.flatnonzero(gm.group_mask(h, norms, 3)).tolist() == [1, 2, 3]
+
+
+def _brute_group_mask(c_steps, k):
+    """Exhaustive form: the K-subset of the union with the largest summed score (distinct sums)."""
+    n = c_steps.shape[1]
+    union = set()
+    for c in c_steps:
+        best = max(itertools.combinations(range(n), k), key=lambda sub: sum(float(c[i]) for i in sub))
+        union |= set(best)
+    tot = c_steps.astype(np.float64).sum(axis=0)
+    best = max(itertools.combinations(sorted(union), k), key=lambda sub: sum(tot[i] for i in sub))
+    m = np.zeros(n, np.uint8)
+    m[list(best)] = 1
+    return m
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_group_mask_matches_exhaustive_search(seed):
+    r = np.random.default_rng(10 + seed)
+    S, n, T, k = int(r.integers(1, 4)), 8, 3, int(r.integers(1, 5))
+    h = r.standard_normal((S, n, T)).astype(np.float32)
+    norms = (0.5 + r.random(n)).astype(np.float32)
+    c = np.stack([gm.contribution_scores(hs, norms) for hs in h])
+    assert np.array_equal(gm.group_mask(h, norms, k), _brute_group_mask(c, k))
+
+
+def test_group_mask_special_cases():
+    r = np.random.default_rng(20)
+    h = r.standard_normal((1, 64, 5)).astype(np.float32)
+    norms = (0.5 + r.random(64)).astype(np.float32)
+    c = gm.contribution_scores(h[0], norms)
+    # One step: the group mask is that step's top K.
+    assert np.array_equal(gm.group_mask(h, norms, 20).astype(bool), gm.top_k(c, 20))
+    # Identical steps: the same.
+    assert np.array_equal(gm.group_mask(np.repeat(h, 4, axis=0), norms, 20).astype(bool), gm.top_k(c, 20))
+    # K = 0 and K = d_ff.
+    assert gm.group_mask(h, norms, 0).sum() == 0 and gm.group_mask(h, norms, 64).sum() == 64
+    # Always exactly K neurons, all of them some step's candidate.
+    hs = r.standard_normal((3, 64, 5)).astype(np.float32)
+    m = gm.group_mask(hs, norms, 17)
+    assert m.sum() == 17
+    cand = np.zeros(64, bool)
+    for x in hs:
+        cand |= gm.top_k(gm.contribution_scores(x, norms), 17)
+    assert np.all(cand[m != 0])

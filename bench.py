@@ -23,10 +23,11 @@ oracle timed on a bounded sample of the same workload.
 Other workloads (--workload): the wide layer d = 2048, d_ff = 16384 at 10/30/50/100% (c4-*); the 18-layer stack
 run through a 10-step denoising schedule, one step of the benchmark being the whole sequence (c3); the same
 sequence with Eq. 4's dense anchors at steps 0 and 5 and anchor-delta updates at the other steps (c3-eq4); and
-16 independent executions through the stack with per-sample lists (c5).
+16 independent executions through the stack with per-sample lists (c5); and the construction of one group's
+neuron masks from 5 reference steps of the stack (gm).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c3-eq4|c5]
+                       [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c3-eq4|c5|gm]
 """
 from __future__ import annotations
 
@@ -91,6 +92,8 @@ WORKLOADS = {
     "c3-eq4": dict(name="action-expert FFN stack, 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, 10 denoising steps "
                         "with Eq. 4: dense anchors at steps 0 and 5, each shared by the next 4 steps with top-30% "
                         "group masks", cfg=3, percent=30),
+    "gm": dict(name="group neuron masks for the config-3 stack: 5 reference steps x 18 layers, d_ff=4096, T=51, "
+                    "K=1229 (top 30%)", cfg=3, percent=30),
     "c5": dict(name="16 independent executions x 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, per-sample top-30% "
                     "masks (18% shared core + random remainder)", cfg=5, percent=30),
 }
@@ -105,9 +108,18 @@ STEP_TEXT = {
     "c3-eq4": "one 10-step sequence: per group (anchors 0 and 5) rm_mask_compact (18 masks) + "
               "rm_anchor_ffn_stack (L=18) + 4 rm_delta_ffn_stack (L=18), replayed from HIP graphs; "
               "us_per_layer = sequence time / 180",
+    "gm": "rm_group_masks: Eq. 1 scores of 5 steps x 18 layers from their dense activations (float32 "
+          "[5][18][4096][51], written by rm_anchor_ffn_stack with identity lists at set-up), per-step top-K, union "
+          "and rerank; replayed from HIP graphs; us_per_layer = step time / 18",
     "c5": "rm_masked_ffn_stack (L=18, B=16: compaction of the 288 masks + the stack), replayed from HIP graphs; "
           "us_per_layer = step time / 18; value on the union of the samples' rows, per_sample_value on all rows",
 }
+
+
+def ffn_hooks(rm, gu_bytes: int, dn_bytes: int):
+    """The kernels a FFN step's timing hook follows: (kernel id, description, key, algorithmic bytes per launch)."""
+    return [(rm.RM_KERNEL_GATEUP, "gate/up projection (gateup_*_kernel)", "gateup", gu_bytes),
+            (rm.RM_KERNEL_DOWN, "down projection (down_*_kernel)", "down", dn_bytes)]
 
 
 def _bf16_tensor(bits, device):
@@ -170,8 +182,8 @@ class Setup:
     def active_bytes(self) -> int:
         return active_weight_bytes(self.k, self.d, 2)
 
-    def hooked_bytes(self):
-        return gateup_bytes(self.k, self.d, 2), down_bytes(self.k, self.d, 2)
+    def hooks(self):
+        return ffn_hooks(self.rm, gateup_bytes(self.k, self.d, 2), down_bytes(self.k, self.d, 2))
 
 
 def _stack_copies(layers, device, cold: bool):
@@ -220,15 +232,16 @@ class StackSetup5:
     def per_sample_bytes(self) -> int:
         return self.L * self.B * active_weight_bytes(self.k, self.d, 2)
 
-    def hooked_bytes(self):  # the first gate/up and down launches of a step: layer 0, all samples
-        return gateup_bytes(self.union[0], self.d, 2), down_bytes(self.union[0], self.d, 2)
+    def hooks(self):  # the first gate/up and down launches of a step: layer 0, all samples
+        return ffn_hooks(self.rm, gateup_bytes(self.union[0], self.d, 2), down_bytes(self.union[0], self.d, 2))
 
 
 class StackSetup3:
     """Config 3: one step is a whole 10-step denoising sequence through the 18-layer stack: step 0 dense
     (rm_dense_ffn_ref layer by layer), steps 1..9 sparse, with the 18 per-layer masks compacted at steps 1, 3,
-    5, 7, 9 (rm_masked_ffn_stack) and their lists reused by the following step (rm_sparse_ffn_stack).  The masks are the top-30% neurons by
-    mean |SiLU(g) u| of a float32 dense pass on the previous step's input (input setup, on the GPU)."""
+    5, 7, 9 (rm_masked_ffn_stack) and their lists reused by the following step (rm_sparse_ffn_stack).  The masks
+    are the top-30% neurons by mean |SiLU(g) u| of a float32 dense pass on the previous step's input (input
+    setup, on the GPU)."""
 
     def __init__(self, key: str, device, cold: bool = True):
         import torch
@@ -281,8 +294,8 @@ class StackSetup3:
         return self.L * (active_weight_bytes(self.d_ff, self.d, 2)
                          + (self.steps - 1) * active_weight_bytes(self.k, self.d, 2))
 
-    def hooked_bytes(self):  # the first gate/up and down launches of a step: layer 0 of the dense step
-        return gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2)
+    def hooks(self):  # the first gate/up and down launches of a step: layer 0 of the dense step
+        return ffn_hooks(self.rm, gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2))
 
 
 class StackSetupEq4:
@@ -347,8 +360,64 @@ class StackSetupEq4:
         return self.L * (n_anchor * active_weight_bytes(self.d_ff, self.d, 2)
                          + (self.steps - n_anchor) * active_weight_bytes(self.k, self.d, 2))
 
-    def hooked_bytes(self):  # the first gate/up and down launches of a step: layer 0 of the first anchor
-        return gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2)
+    def hooks(self):  # the first gate/up and down launches of a step: layer 0 of the first anchor
+        return ffn_hooks(self.rm, gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2))
+
+
+class GroupMaskSetup:
+    """Group-mask construction (section 5) for one group of the config-3 stack: the dense activations of 5
+    reference steps (inputs x_0 .. x_4 of config 3, each run through rm_anchor_ffn_stack with the identity lists,
+    at set-up) -> rm_group_masks.  The activations rotate over copies (>= 1 GiB) so the timed reads are cold."""
+
+    STEPS = 5
+
+    def __init__(self, key: str, device, cold: bool = True):
+        import torch
+        import workloads as wl
+        import paper_2609_19104_amd as rm
+        w = wl.config3()
+        self.key, self.spec, self.rm = key, WORKLOADS[key], rm
+        self.d, self.d_ff, self.T, self.B, self.L, self.k = w.d, w.d_ff, w.T, 1, w.L, w.k
+        layers, _ = _stack_copies(w.layers, device, cold=False)
+        layers = layers[0]
+        idx = torch.arange(self.d_ff, dtype=torch.int32, device=device).repeat(self.L, 1).contiguous()
+        cnt = torch.full((self.L,), self.d_ff, dtype=torch.int32, device=device)
+        ws = rm.workspace(self.d, self.d_ff, rm.RM_BF16, 1, self.T, self.d_ff, device=device)
+        h = torch.empty((self.STEPS, self.L, self.d_ff, self.T), dtype=torch.float32, device=device)
+        ya = torch.empty((self.L, 1, self.T, self.d), dtype=torch.float32, device=device)
+        ha = torch.empty((self.L, 1, self.d_ff, self.T), dtype=torch.float32, device=device)
+        for s in range(self.STEPS):
+            x = torch.from_numpy(w.x_steps[s]).to(device)
+            rm.rm_anchor_ffn_stack(x, torch.empty_like(x), layers, idx, cnt, self.d_ff, ya, ha, ws)
+            h[s] = ha[:, 0]
+        self.norms = torch.empty((self.L, self.d_ff), dtype=torch.float32, device=device)
+        for l in range(self.L):
+            rm.rm_neuron_norms(layers[l][2], self.norms[l])
+        torch.cuda.synchronize()
+        del layers, ws
+        self.h_bytes = h.numel() * 4
+        self.copies = max(2, math.ceil(COLD_BYTES / self.h_bytes)) if cold else 1
+        self.hs = [h] + [h.clone() for _ in range(self.copies - 1)]
+        self.rotate = self.copies
+        self.cold_text = (f"cold: {self.copies} rotating copies of the activations "
+                          f"({self.copies * self.h_bytes / 2**30:.2f} GiB)")
+        self.scores = torch.empty((self.STEPS, self.L, self.d_ff), dtype=torch.float32, device=device)
+        self.mask = torch.empty((self.L, self.d_ff), dtype=torch.uint8, device=device)
+        self.layer_steps = self.L
+
+    def step(self, i: int) -> None:
+        self.rm.rm_group_masks(self.hs[i % self.rotate], self.norms, self.k, self.scores, self.mask)
+
+    @property
+    def active_bytes(self) -> int:  # the activations read (the norms, scores and masks are < 2% more)
+        return self.h_bytes
+
+    def hooks(self):
+        rm, sl = self.rm, self.STEPS * self.L
+        score_bytes = self.h_bytes + 4 * self.L * self.d_ff + 4 * sl * self.d_ff
+        select_bytes = 4 * sl * self.d_ff + self.L * self.d_ff
+        return [(rm.RM_KERNEL_SCORES, "Eq. 1 scores (scores_kernel)", "scores", score_bytes),
+                (rm.RM_KERNEL_GROUP_SELECT, "top-K, union and rerank (group_select_kernel)", "select", select_bytes)]
 
 
 def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
@@ -363,7 +432,7 @@ def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
     evs = None
     if hook:
         evs = {kk: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                    for _ in range(steps)] for kk in (rm.RM_KERNEL_GATEUP, rm.RM_KERNEL_DOWN)}
+                    for _ in range(steps)] for kk, _, _, _ in setup.hooks()}
         for pairs in evs.values():  # create the underlying events before handing them to the library
             for a, b in pairs:
                 a.record()
@@ -529,7 +598,8 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "copies": args.steps}))
         return 0
-    setup = {"c3": StackSetup3, "c3-eq4": StackSetupEq4, "c5": StackSetup5}.get(args.workload, Setup)(
+    setup = {"c3": StackSetup3, "c3-eq4": StackSetupEq4, "c5": StackSetup5, "gm": GroupMaskSetup}.get(
+        args.workload, Setup)(
         args.workload, dev, cold=True)
 
     if args.profile_only:
@@ -540,13 +610,10 @@ def main(argv=None) -> int:
     eager_ms, _ = time_steps(setup, args.steps, args.warmup)
     _, kern = time_steps(setup, args.steps, 5, hook=True)
     ms = time_graph(setup, args.steps, args.warmup)
-    gu_t, dn_t = kern[setup.rm.RM_KERNEL_GATEUP], kern[setup.rm.RM_KERNEL_DOWN]
-    gu_us, dn_us = gu_t["mean"], dn_t["mean"]  # average launch duration (kernel start to end)
-    gu_bytes, dn_bytes = setup.hooked_bytes()
-    if gu_us >= dn_us:
-        dom, dom_key, dom_bytes, dom_us = "gate/up projection (gateup_*_kernel)", "gateup", gu_bytes, gu_us
-    else:
-        dom, dom_key, dom_bytes, dom_us = "down projection (down_bf16_kernel)", "down", dn_bytes, dn_us
+    # The dominant kernel: the hooked kernel with the longest average launch duration (kernel start to end).
+    hooks = setup.hooks()
+    dom_id, dom, dom_key, dom_bytes = max(hooks, key=lambda h: kern[h[0]]["mean"])
+    dom_us = kern[dom_id]["mean"]
     achieved = dom_bytes / (dom_us * 1e-6) / 1e9
     value = setup.active_bytes / (ms * 1e-3) / 1e9
 
@@ -570,7 +637,8 @@ def main(argv=None) -> int:
         "config": {"workload": setup.spec["name"], "d": setup.d, "d_ff": setup.d_ff, "T": setup.T, "B": setup.B,
                    "active_neurons": setup.k, "layers": setup.L,
                    "step": STEP_TEXT.get(setup.key, STEP_TEXT[setup.key[:2]]),
-                   "weights": f"cold: {setup.copies} rotating copies "
+                   "weights": getattr(setup, "cold_text", None) or
+                              f"cold: {setup.copies} rotating copies "
                               f"({setup.copies * setup.L * 3 * setup.d * setup.d_ff * 2 / 2**30:.2f} GiB)"},
         "us_per_layer": round(ms * 1e3 / setup.layer_steps, 3),
         "eager_us_per_layer": round(eager_ms * 1e3 / setup.layer_steps, 3),
@@ -578,9 +646,8 @@ def main(argv=None) -> int:
         "tokens_per_s": round(setup.B * setup.T * setup.layer_steps / (ms * 1e-3), 1),
         "active_weight_bytes": setup.active_bytes,
         "warm_us_per_layer": round(warm_ms * 1e3 / setup.layer_steps, 3),
-        "kernel_us": {"gateup": round(gu_us, 3), "down": round(dn_us, 3),
-                      "gateup_median": round(gu_t["median"], 3), "gateup_min": round(gu_t["min"], 3),
-                      "down_median": round(dn_t["median"], 3), "down_min": round(dn_t["min"], 3)},
+        "kernel_us": {f"{key}{suffix}": round(kern[kid][stat], 3) for kid, _, key, _ in hooks
+                      for suffix, stat in (("", "mean"), ("_median", "median"), ("_min", "min"))},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": counted_traffic(args.workload, dom_key),

@@ -88,10 +88,10 @@ rm_status rm_mask_compact(const uint8_t *mask, int32_t n_masks, int32_t d_ff, in
                           void *stream);
 
 /* Workspace bytes (written to *bytes, a host pointer) needed by the FFN calls (rm_sparse_ffn_*, rm_masked_ffn_*,
- * rm_dense_ffn_ref, rm_anchor_ffn_stack, rm_delta_ffn_stack) for B samples of T tokens with at most max_count listed neurons per sample and layer
- * (max_count = d_ff for the dense call).  The workspace is scratch owned by the caller: 256-byte aligned
- * device memory, contents need not be initialized, reused by every layer of a call, and it must not be used by
- * two calls that may run at the same time. */
+ * rm_dense_ffn_ref, rm_anchor_ffn_stack, rm_delta_ffn_stack) for B samples of T tokens with at most max_count
+ * listed neurons per sample and layer (max_count = d_ff for the dense and anchor calls).  The workspace is
+ * scratch owned by the caller: 256-byte aligned device memory, contents need not be initialized, reused by every
+ * layer of a call, and it must not be used by two calls that may run at the same time. */
 rm_status rm_workspace_size(const rm_ffn_shape *s, int32_t B, int32_t T, int32_t max_count, size_t *bytes);
 
 /* One masked FFN layer with residual (Eq. 4 with a zero anchor; see the file comment).
@@ -174,11 +174,41 @@ rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *
                              const float *x, float *y, const int32_t *idx, const int32_t *count, int32_t max_count,
                              const float *y_anchor, const float *h_anchor, void *ws, size_t ws_bytes, void *stream);
 
+/* Down-projection row norms ||W_down[n]||_2 of one layer (the weight factor of Eq. 1, section 3.4), float32.
+ *   w_down: [d_ff][d] in wdtype (the layout of rm_ffn_layer_weights.w_down), 16-byte aligned; d a multiple of 32.
+ *   norms:  float32 [d_ff] out.
+ * Each norm is the correctly rounded square root of the float32 sum of the row's squares, added in column order
+ * with every square and sum rounded to float32 (the order rm_group_masks' selections are defined with). */
+rm_status rm_neuron_norms(const void *w_down, int32_t d_ff, int32_t d, int32_t wdtype, float *norms, void *stream);
+
+/* Group neuron masks from the reference activations of a group of S denoising steps (section 5, "Constructing
+ * Group Neuron Masks"): per layer, Eq. 1's score c[s][l][n] = (sum over t of |h[s][l][n][t]|) * norms[l][n] for
+ * every step, each step's K best neurons as candidates, and as the mask the K candidates with the largest score
+ * summed over the steps.
+ *   h:      float32 [S][L][d_ff][T], neuron-major per step and layer (rm_anchor_ffn_stack run with the identity
+ *           lists 0 .. d_ff-1 writes one step's [L][1][d_ff][T] as its h_anchor).
+ *   norms:  float32 [L][d_ff] (rm_neuron_norms of each layer's w_down).
+ *   K:      neurons per mask, in [0, d_ff] (section 5 takes K = ceil(rho_n * d_ff)).
+ *   scores: float32 [S][L][d_ff] out, the Eq. 1 scores.
+ *   mask:   uint8 [L][d_ff] out, 1 for the layer's K selected neurons, else 0 (the input of rm_mask_compact and
+ *           rm_masked_ffn_*).
+ * Sums run in index order in float32 with one rounding per operation; ties at the K-th place go to the lower
+ * neuron index.  d_ff <= 16384, S * L <= 65535.  scores and mask must not overlap each other, h or norms.
+ * Errors: RM_ERR_INVALID_ARG (null pointer, non-positive size, overlap), RM_ERR_SHAPE (d_ff, K or S * L out of
+ * range), RM_ERR_ALIGN. */
+rm_status rm_group_masks(const float *h, int32_t S, int32_t L, int32_t d_ff, int32_t T, const float *norms,
+                         int32_t K, float *scores, uint8_t *mask, void *stream);
+
 /* Measurement hook.  Arms two hipEvent_t (begin, end, created by the caller) for the next launch of the named
  * kernel by this thread: that launch goes through hipExtLaunchKernel, which stamps the events with the
  * kernel's own start and end, the interval a kernel trace reports.  The hook disarms after that launch;
- * passing NULL events disarms it.  kernel: 0 = gate/up projection, 1 = down projection. */
-typedef enum rm_kernel_id { RM_KERNEL_GATEUP = 0, RM_KERNEL_DOWN = 1 } rm_kernel_id;
+ * passing NULL events disarms it.  kernel: an rm_kernel_id. */
+typedef enum rm_kernel_id {
+    RM_KERNEL_GATEUP = 0,      /* gate/up projection of the FFN calls                          */
+    RM_KERNEL_DOWN = 1,        /* down projection of the FFN calls                             */
+    RM_KERNEL_SCORES = 2,      /* Eq. 1 scores of rm_group_masks                               */
+    RM_KERNEL_GROUP_SELECT = 3 /* top-K selection, union and rerank of rm_group_masks          */
+} rm_kernel_id;
 rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end);
 
 /* Static description of a status code. */

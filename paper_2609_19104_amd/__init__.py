@@ -35,9 +35,12 @@ RM_F32 = 0
 RM_BF16 = 1
 RM_KERNEL_GATEUP = 0
 RM_KERNEL_DOWN = 1
+RM_KERNEL_SCORES = 2
+RM_KERNEL_GROUP_SELECT = 3
 
 EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_stack",
-            "rm_masked_ffn_layer", "rm_masked_ffn_stack", "rm_dense_ffn_ref", "rm_anchor_ffn_stack", "rm_delta_ffn_stack", "rm_profile_kernel_events",
+            "rm_masked_ffn_layer", "rm_masked_ffn_stack", "rm_dense_ffn_ref", "rm_anchor_ffn_stack",
+            "rm_delta_ffn_stack", "rm_neuron_norms", "rm_group_masks", "rm_profile_kernel_events",
             "rm_status_string", "rm_last_error")
 
 Layer = Tuple[torch.Tensor, torch.Tensor, torch.Tensor, Optional[torch.Tensor]]
@@ -88,6 +91,8 @@ def load_library() -> ctypes.CDLL:
         "rm_dense_ffn_ref": [sp, wp, i32, i32, vp, vp, vp, sz, vp],
         "rm_anchor_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
         "rm_delta_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
+        "rm_neuron_norms": [vp, i32, i32, i32, vp, vp],
+        "rm_group_masks": [vp, i32, i32, i32, i32, vp, i32, vp, vp, vp],
         "rm_profile_kernel_events": [i32, vp, vp],
         "rm_status_string": [i32],
         "rm_last_error": [],
@@ -331,6 +336,32 @@ def rm_dense_ffn_ref(x: torch.Tensor, y: torch.Tensor, layer: Layer, ws: torch.T
                                            wp, wn, _stream(stream)))
 
 
+def rm_neuron_norms(w_down: torch.Tensor, norms: torch.Tensor, stream=None) -> None:
+    """||W_down[n]||_2 per neuron (Eq. 1's weight factor): w_down [d_ff][d] -> norms float32 [d_ff]."""
+    _need_cuda("w_down", w_down, (torch.float32, torch.bfloat16), 2)
+    d_ff, d = w_down.shape
+    _need_cuda("norms", norms, (torch.float32,))
+    if norms.numel() != d_ff:
+        raise ValueError(f"norms must hold d_ff={d_ff} entries")
+    _check(load_library().rm_neuron_norms(w_down.data_ptr(), d_ff, d, wdtype_of(w_down), norms.data_ptr(),
+                                          _stream(stream)))
+
+
+def rm_group_masks(h: torch.Tensor, norms: torch.Tensor, k: int, scores: torch.Tensor, mask: torch.Tensor,
+                   stream=None) -> None:
+    """Group masks (section 5): h float32 [S][L][d_ff][T], norms [L][d_ff] -> scores float32 [S][L][d_ff] and
+    mask uint8 [L][d_ff]."""
+    _need_cuda("h", h, (torch.float32,), 4)
+    S, L, d_ff, T = h.shape
+    _need_cuda("norms", norms, (torch.float32,))
+    _need_cuda("scores", scores, (torch.float32,))
+    _need_cuda("mask", mask, (torch.uint8, torch.bool))
+    if norms.numel() != L * d_ff or scores.numel() != S * L * d_ff or mask.numel() != L * d_ff:
+        raise ValueError("norms must be [L][d_ff], scores [S][L][d_ff] and mask [L][d_ff]")
+    _check(load_library().rm_group_masks(h.data_ptr(), S, L, d_ff, T, norms.data_ptr(), int(k), scores.data_ptr(),
+                                         mask.data_ptr(), _stream(stream)))
+
+
 def rm_profile_kernel_events(kernel: int, ev_begin: Optional[int], ev_end: Optional[int]) -> None:
-    """Arm raw hipEvent_t handles around the next launch of `kernel` (RM_KERNEL_GATEUP / RM_KERNEL_DOWN)."""
+    """Arm raw hipEvent_t handles around the next launch of `kernel` (an RM_KERNEL_* id)."""
     _check(load_library().rm_profile_kernel_events(kernel, ev_begin, ev_end))

@@ -343,8 +343,8 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
         // Thread tid forms h for neuron (tid & 7) of each group and token tid >> 3.
 #pragma unroll
         for (int gg = 0; gg < NG; ++gg)
-            gu_store_h<NT>(a, Hb, b, [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; }, DS, t0,
-                           blk0 + gg * 8, cnt, rn);
+            auto red_g = [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; };
+            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8, cnt, rn);
         __syncthreads();
     }
 }
@@ -442,8 +442,8 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
         __syncthreads();
 #pragma unroll
         for (int gg = 0; gg < NG; ++gg)
-            gu_store_h<NT>(a, Hb, b, [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; }, DS, t0,
-                           blk0 + gg * 8, cnt, rn);
+            auto red_g = [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; };
+            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8, cnt, rn);
         __syncthreads();
     }
 }

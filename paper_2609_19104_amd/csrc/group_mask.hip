@@ -1,0 +1,307 @@
+// Group neuron masks from reference activations (paper section 5, "Constructing Group Neuron Masks", with the
+// contribution score of Eq. 1 from section 3.4).
+//
+// Per layer l of a group of S steps: c[s][n] = (sum over t of |h[s][n][t]|) * ||W_down[n]||_2 (Eq. 1); each
+// step's K best neurons are candidates; the mask is the K candidates with the largest sum over the steps of c.
+// Top-K is an integer decision on floating-point scores, so every sum here has a fixed order and single
+// rounding per operation (no contraction into fused multiply-adds): |h| over t = 0 .. T-1, w^2 over columns
+// j = 0 .. d-1 (each square rounded), the steps' scores over s = 0 .. S-1, a correctly rounded square root and
+// a rounded product.  Ties at the K-th place go to the lower neuron index.
+//
+// Kernels:
+//   neuron_norms_kernel:  one wave per 64 neurons; a 64 x 64 weight tile at a time goes through LDS (coalesced
+//                         row loads), then each lane adds its own row's 64 squares in column order.
+//   scores_kernel:        one wave per (step, layer, 64 neurons): the rows go through LDS with coalesced loads,
+//                         then lane n adds row n in token order.
+//   step_select_kernel:   one 1024-thread workgroup per (step, layer), 16 neurons per thread (d_ff <= 16384): the
+//                         step's top K sets the layer's mask bytes (their union over the steps).
+//   group_rerank_kernel:  one 1024-thread workgroup per layer: the union's top K by summed score.
+// Top K is an MSB-first radix select over the scores' bit patterns (non-negative floats order like their bits):
+// four 8-bit passes, each a histogram (per-wave LDS histograms with integer atomics, so the counts are exact,
+// then added) and a suffix scan that finds the digit of the K-th largest key; then the keys above that
+// threshold plus the lowest-index keys equal to it, found with a workgroup prefix sum.
+#include "rm_internal.h"
+
+namespace {
+
+// a * b rounded to float32 on its own: the empty asm statement hides the product from the optimizer, so it
+// cannot be fused with the sum it feeds into one multiply-add (HIP compiles with contraction allowed).
+__device__ __forceinline__ float mul_rounded(float a, float b) {
+    float p = a * b;
+    asm volatile("" : "+v"(p));
+    return p;
+}
+
+constexpr int kSelThreads = 1024;
+constexpr int kSelPerThread = 16;  // neurons per thread: d_ff <= 16384
+
+// ------------------------------------------------------------------------------------------ norms
+
+template <bool kBf16>
+__global__ __launch_bounds__(64) void neuron_norms_kernel(const void *__restrict__ w, int d_ff, int d,
+                                                          float *__restrict__ norms) {
+    __shared__ float tile[64][65];  // 64 rows x 64 columns, padded: lane n reads row n without bank conflicts
+    const int lane = threadIdx.x;
+    const int n0 = blockIdx.x * 64;
+    float s = 0.0f;
+    for (int c0 = 0; c0 < d; c0 += 64) {
+        // 64 rows x 64 columns: each lane loads 8 pieces of 8 columns, 8 lanes per row.
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int piece = lane + 64 * k;  // 0 .. 511
+            const int r = piece >> 3;
+            const int cc = (piece & 7) * 8;
+            const int row = min(n0 + r, d_ff - 1);
+            float v[8];
+            if (c0 + cc < d) {  // d is a multiple of 32, so a piece is wholly inside or outside the row
+                if constexpr (kBf16) {
+                    const uint4 p = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(w) +
+                                                                     static_cast<size_t>(row) * d + c0 + cc);
+                    const uint32_t q[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        v[2 * i] = __uint_as_float(q[i] << 16);
+                        v[2 * i + 1] = __uint_as_float(q[i] & 0xffff0000u);
+                    }
+                } else {
+                    const float *src = static_cast<const float *>(w) + static_cast<size_t>(row) * d + c0 + cc;
+                    const float4 a = *reinterpret_cast<const float4 *>(src);
+                    const float4 b = *reinterpret_cast<const float4 *>(src + 4);
+                    v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) v[i] = 0.0f;  // adds +0 to a non-negative sum: no change
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) tile[r][cc + i] = v[i];
+        }
+        __syncthreads();
+        for (int j = 0; j < 64; ++j) s = __fadd_rn(s, mul_rounded(tile[lane][j], tile[lane][j]));
+        __syncthreads();
+    }
+    if (n0 + lane < d_ff) norms[n0 + lane] = __fsqrt_rn(s);
+}
+
+// ------------------------------------------------------------------------------------------ scores
+
+// One wave per (step and layer, 64 neurons).  The 64 rows of T floats are contiguous in h: the wave loads them
+// (or 64-token slices of them) with consecutive lanes on consecutive addresses into LDS, then lane n adds |h| of
+// row n in token order.  The mask bytes of the layer are cleared here (step 0), before the selections set them.
+constexpr int kScoreRows = 64;
+constexpr int kScoreChunk = 64;
+
+__global__ __launch_bounds__(64) void scores_kernel(const float *__restrict__ h, int d_ff, int T,
+                                                    const float *__restrict__ norms, int L,
+                                                    float *__restrict__ scores, uint8_t *__restrict__ mask) {
+    __shared__ float tile[kScoreRows * (kScoreChunk + 1)];
+    const int lane = threadIdx.x;
+    const int n0 = blockIdx.x * kScoreRows;
+    const int sl = blockIdx.y;  // step * L + layer
+    const int rows = min(kScoreRows, d_ff - n0);
+    const float *base = h + (static_cast<size_t>(sl) * d_ff + n0) * T;
+    float s = 0.0f;
+    for (int t0 = 0; t0 < T; t0 += kScoreChunk) {
+        const int C = min(kScoreChunk, T - t0);
+        const int stride = C | 1;  // odd row pitch: lane n's reads of row n fall in distinct banks
+        const int total = rows * C;
+#pragma unroll 8
+        for (int e = lane; e < total; e += 64) {
+            const int r = e / C;
+            const int t = e - r * C;
+            tile[r * stride + t] = fabsf(base[static_cast<size_t>(r) * T + t0 + t]);
+        }
+        __syncthreads();
+        if (lane < rows)
+            for (int t = 0; t < C; ++t) s = __fadd_rn(s, tile[lane * stride + t]);
+        __syncthreads();
+    }
+    if (lane < rows) {
+        const int l = sl % L;
+        const float nrm = norms[static_cast<size_t>(l) * d_ff + n0 + lane];
+        scores[static_cast<size_t>(sl) * d_ff + n0 + lane] = __fmul_rn(s, nrm);
+        if (sl < L) mask[static_cast<size_t>(l) * d_ff + n0 + lane] = 0;
+    }
+}
+
+// ------------------------------------------------------------------------------------------ selection
+
+struct SelLds {
+    uint32_t whist[kSelThreads / 64][256];  // one histogram per wave: atomics only contend within a wave
+    uint32_t hist[256];
+    int wave_sum[kSelThreads / 64];
+    int digit, need;
+};
+
+// Exclusive prefix sum of v over the workgroup, in thread order.
+__device__ __forceinline__ int block_excl_scan(int v, SelLds &l) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int u = __shfl_up(incl, off);
+        if (lane >= off) incl += u;
+    }
+    __syncthreads();  // wave_sum may still be read by a previous call
+    if (lane == 63) l.wave_sum[wave] = incl;
+    __syncthreads();
+    int before = 0;
+    for (int w = 0; w < wave; ++w) before += l.wave_sum[w];
+    return before + incl - v;
+}
+
+// Selection bits (bit i: neuron tid * 16 + i) of the k largest keys among the thread's valid ones (bit i of
+// `valid`), ties to the lower neuron index.  0 <= k; every thread of the workgroup calls it.
+__device__ uint32_t select_top_k(const uint32_t (&key)[kSelPerThread], uint32_t valid, int k, int n_valid,
+                                 SelLds &l) {
+    if (k <= 0) return 0u;
+    if (k >= n_valid) return valid;
+    const int tid = threadIdx.x;
+    uint32_t prefix = 0, hi = 0;
+    int need = k;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        const int wave = tid >> 6;
+        for (int b = tid & 63; b < 256; b += 64) l.whist[wave][b] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kSelPerThread; ++i)
+            if (((valid >> i) & 1u) && (key[i] & hi) == prefix)
+                atomicAdd(&l.whist[wave][(key[i] >> shift) & 255u], 1u);
+        __syncthreads();
+        if (tid < 256) {
+            uint32_t c = 0;
+#pragma unroll
+            for (int w = 0; w < kSelThreads / 64; ++w) c += l.whist[w][tid];
+            l.hist[tid] = c;
+        }
+        __syncthreads();
+        if (tid < 64) {  // lane j holds digits 4j .. 4j+3; find the digit holding the need-th largest key
+            const int j = tid;
+            const uint32_t b0 = l.hist[4 * j], b1 = l.hist[4 * j + 1], b2 = l.hist[4 * j + 2], b3 = l.hist[4 * j + 3];
+            const int own = static_cast<int>(b0 + b1 + b2 + b3);
+            int above = own;  // inclusive suffix sum over lanes j .. 63, then made exclusive
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int u = __shfl_down(above, off);
+                if (j + off < 64) above += u;
+            }
+            above -= own;  // keys in digits above 4j + 3
+            const uint32_t b[4] = {b0, b1, b2, b3};
+            int cum = above;
+#pragma unroll
+            for (int q = 3; q >= 0; --q) {
+                const int c = static_cast<int>(b[q]);
+                if (cum < need && cum + c >= need) {
+                    l.digit = 4 * j + q;
+                    l.need = need - cum;
+                }
+                cum += c;
+            }
+        }
+        __syncthreads();
+        prefix |= static_cast<uint32_t>(l.digit) << shift;
+        hi |= 255u << shift;
+        need = l.need;
+        __syncthreads();  // l.digit / l.need are rewritten by the next pass
+    }
+    // prefix is the k-th largest key; take every larger key and the `need` lowest-index keys equal to it.
+    uint32_t sel = 0, eq = 0;
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i) {
+        if (!((valid >> i) & 1u)) continue;
+        if (key[i] > prefix) sel |= 1u << i;
+        if (key[i] == prefix) eq |= 1u << i;
+    }
+    int rank = block_excl_scan(__popc(eq), l);
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i) {
+        if ((eq >> i) & 1u) {
+            if (rank < need) sel |= 1u << i;
+            ++rank;
+        }
+    }
+    return sel;
+}
+
+// Each step's K best neurons of one layer (workgroup = step * L + layer) set their mask bytes to 1: the mask
+// holds the union of the steps' candidates when the rerank runs.
+__global__ __launch_bounds__(kSelThreads) void step_select_kernel(const float *__restrict__ scores, int L, int d_ff,
+                                                                  int k, uint8_t *__restrict__ mask) {
+    __shared__ SelLds l;
+    const int sl = blockIdx.x;
+    const int n0 = threadIdx.x * kSelPerThread;
+    const float *c = scores + static_cast<size_t>(sl) * d_ff;
+    uint32_t valid = 0, key[kSelPerThread];
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i) {
+        const bool ok = n0 + i < d_ff;
+        if (ok) valid |= 1u << i;
+        key[i] = ok ? __float_as_uint(c[n0 + i]) : 0u;  // c >= 0: its bits order like its value
+    }
+    const uint32_t sel = select_top_k(key, valid, k, d_ff, l);
+    uint8_t *m = mask + static_cast<size_t>(sl % L) * d_ff;
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i)
+        if ((sel >> i) & 1u) m[n0 + i] = 1;  // several steps may set the same byte to the same value
+}
+
+// The layer's mask: the K members of the union (mask bytes set by step_select_kernel) with the largest score
+// summed over the steps in step order.  Neurons outside the union get the smallest key and are never taken
+// (the union holds at least K neurons).
+__global__ __launch_bounds__(kSelThreads) void group_rerank_kernel(const float *__restrict__ scores, int S, int L,
+                                                                   int d_ff, int k, uint8_t *__restrict__ mask) {
+    __shared__ SelLds l;
+    const int layer = blockIdx.x;
+    const int n0 = threadIdx.x * kSelPerThread;
+    uint8_t *m = mask + static_cast<size_t>(layer) * d_ff;
+    uint32_t valid = 0, key[kSelPerThread];
+    float summed[kSelPerThread];
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i) {
+        summed[i] = 0.0f;
+        if (n0 + i < d_ff) valid |= 1u << i;
+    }
+    for (int s = 0; s < S; ++s) {
+        const float *c = scores + (static_cast<size_t>(s) * L + layer) * d_ff;
+#pragma unroll
+        for (int i = 0; i < kSelPerThread; ++i)
+            if ((valid >> i) & 1u) summed[i] = __fadd_rn(summed[i], c[n0 + i]);
+    }
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i)
+        key[i] = ((valid >> i) & 1u) && m[n0 + i] != 0 ? __float_as_uint(summed[i]) + 1u : 0u;
+    const uint32_t sel = select_top_k(key, valid, k, d_ff, l);
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i)
+        if ((valid >> i) & 1u) m[n0 + i] = static_cast<uint8_t>((sel >> i) & 1u);
+}
+
+}  // namespace
+
+namespace rm {
+
+hipError_t launch_neuron_norms(const void *w_down, int d_ff, int d, int wdtype, float *norms, hipStream_t st) {
+    const dim3 grid((d_ff + 63) / 64);
+    if (wdtype == RM_BF16)
+        hipLaunchKernelGGL(neuron_norms_kernel<true>, grid, dim3(64), 0, st, w_down, d_ff, d, norms);
+    else
+        hipLaunchKernelGGL(neuron_norms_kernel<false>, grid, dim3(64), 0, st, w_down, d_ff, d, norms);
+    return hipGetLastError();
+}
+
+hipError_t launch_group_masks(const float *h, int S, int L, int d_ff, int T, const float *norms, int k,
+                              float *scores, uint8_t *mask, hipStream_t st) {
+    launch_timed(RM_KERNEL_SCORES, scores_kernel, dim3((d_ff + kScoreRows - 1) / kScoreRows, S * L), dim3(64), st,
+                 h, d_ff, T, norms, L, scores, mask);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const float *sc = scores;
+    launch_timed(RM_KERNEL_GROUP_SELECT, step_select_kernel, dim3(S * L), dim3(kSelThreads), st, sc, L, d_ff, k,
+                 mask);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(group_rerank_kernel, dim3(L), dim3(kSelThreads), 0, st, sc, S, L, d_ff, k, mask);
+    return hipGetLastError();
+}
+
+}  // namespace rm

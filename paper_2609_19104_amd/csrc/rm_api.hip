@@ -22,7 +22,7 @@ struct ProfileSlot {
     hipEvent_t begin = nullptr;
     hipEvent_t end = nullptr;
 };
-thread_local ProfileSlot g_profile[2];
+thread_local ProfileSlot g_profile[4];
 
 rm_status fail(rm_status st, const char *fmt, ...) {
     va_list ap;
@@ -473,8 +473,46 @@ RM_EXPORT rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer
     return st == RM_OK ? ok() : st;
 }
 
+RM_EXPORT rm_status rm_neuron_norms(const void *w_down, int32_t d_ff, int32_t d, int32_t wdtype, float *norms,
+                                    void *stream) {
+    if (!w_down || !norms) return fail(RM_ERR_INVALID_ARG, "w_down or norms is NULL");
+    if (d <= 0 || d_ff <= 0) return fail(RM_ERR_INVALID_ARG, "d=%d and d_ff=%d must be positive", d, d_ff);
+    if (d % 32 != 0) return fail(RM_ERR_SHAPE, "d=%d must be a multiple of 32", d);
+    if (wdtype != RM_F32 && wdtype != RM_BF16) return fail(RM_ERR_DTYPE, "unknown weight dtype %d", wdtype);
+    if (!aligned(w_down, 16) || !aligned(norms, 4))
+        return fail(RM_ERR_ALIGN, "w_down must be 16-byte and norms 4-byte aligned");
+    const size_t wbytes = static_cast<size_t>(d_ff) * d * (wdtype == RM_BF16 ? 2 : 4);
+    if (ranges_overlap(w_down, wbytes, norms, static_cast<size_t>(d_ff) * 4))
+        return fail(RM_ERR_INVALID_ARG, "norms overlaps w_down");
+    const hipError_t e = rm::launch_neuron_norms(w_down, d_ff, d, wdtype, norms, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "neuron norm launch");
+    return ok();
+}
+
+RM_EXPORT rm_status rm_group_masks(const float *h, int32_t S, int32_t L, int32_t d_ff, int32_t T, const float *norms,
+                                   int32_t K, float *scores, uint8_t *mask, void *stream) {
+    if (!h || !norms || !scores || !mask) return fail(RM_ERR_INVALID_ARG, "h, norms, scores or mask is NULL");
+    if (S <= 0 || L <= 0 || d_ff <= 0 || T <= 0)
+        return fail(RM_ERR_INVALID_ARG, "S=%d, L=%d, d_ff=%d and T=%d must be positive", S, L, d_ff, T);
+    if (d_ff > rm::kGroupMaxDff) return fail(RM_ERR_SHAPE, "d_ff=%d exceeds %d", d_ff, rm::kGroupMaxDff);
+    if (K < 0 || K > d_ff) return fail(RM_ERR_SHAPE, "K=%d outside [0, d_ff=%d]", K, d_ff);
+    if (static_cast<long long>(S) * L > 65535) return fail(RM_ERR_SHAPE, "S x L = %d x %d exceeds 65535", S, L);
+    if (!aligned(h, 4) || !aligned(norms, 4) || !aligned(scores, 4))
+        return fail(RM_ERR_ALIGN, "h, norms and scores must be 4-byte aligned");
+    const size_t sl = static_cast<size_t>(S) * L;
+    const size_t hb = sl * d_ff * T * 4, nb = static_cast<size_t>(L) * d_ff * 4, sb = sl * d_ff * 4;
+    const size_t mb = static_cast<size_t>(L) * d_ff;
+    if (ranges_overlap(scores, sb, h, hb) || ranges_overlap(scores, sb, norms, nb) ||
+        ranges_overlap(scores, sb, mask, mb) || ranges_overlap(mask, mb, h, hb) || ranges_overlap(mask, mb, norms, nb))
+        return fail(RM_ERR_INVALID_ARG, "scores and mask must not overlap each other, h or norms");
+    const hipError_t e = rm::launch_group_masks(h, S, L, d_ff, T, norms, K, scores, mask,
+                                                static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "group mask launch");
+    return ok();
+}
+
 RM_EXPORT rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end) {
-    if (kernel != RM_KERNEL_GATEUP && kernel != RM_KERNEL_DOWN)
+    if (kernel < RM_KERNEL_GATEUP || kernel > RM_KERNEL_GROUP_SELECT)
         return fail(RM_ERR_INVALID_ARG, "unknown kernel id %d", kernel);
     g_profile[kernel].begin = static_cast<hipEvent_t>(ev_begin);
     g_profile[kernel].end = static_cast<hipEvent_t>(ev_end);

@@ -75,6 +75,12 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
 hipError_t launch_mask_compact(const uint8_t *mask, int n_masks, int d_ff, int32_t *idx, int32_t *count,
                                hipStream_t st);
 
+// Group neuron masks (group_mask.hip): the down rows' norms, and Eq. 1 scores + per-step top-K + union + rerank.
+constexpr int kGroupMaxDff = 16384;
+hipError_t launch_neuron_norms(const void *w_down, int d_ff, int d, int wdtype, float *norms, hipStream_t st);
+hipError_t launch_group_masks(const float *h, int S, int L, int d_ff, int T, const float *norms, int k,
+                              float *scores, uint8_t *mask, hipStream_t st);
+
 // Index lists 0 .. d_ff-1 and counts d_ff for every sample in the workspace (the dense reference runs the
 // sparse kernels on them).
 hipError_t launch_identity_lists(const Plan &p, void *ws, hipStream_t st);

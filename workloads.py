@@ -33,6 +33,7 @@ _TAG_X = 2
 _TAG_NOISE = 3
 _TAG_MASK = 4
 _TAG_GAIN = 5
+_TAG_ACT = 6
 
 
 def seed_sequence(cfg: int, *path: int) -> np.random.SeedSequence:
@@ -245,6 +246,24 @@ def config3(L: int = 18, d: int = 1024, d_ff: int = 4096, T: int = 51, steps: in
         xs.append(perturb(xs[-1], make_noise(cfg, xs[-1].shape, s, scale=0.05)))
     return Workload(cfg, "action-expert FFN stack", d, d_ff, T, 1, "bf16", layers, x_steps=xs,
                     k=count_for_percent(30, d_ff), steps=steps, refresh_steps=list(range(1, steps, 2)))
+
+
+def activation_like(cfg: int, shape: Sequence[int], *path: int, quantum: float = 0.0) -> np.ndarray:
+    """float32 stand-ins for post-GLU activations h[..][n][t] (neuron-major rows): standard normal values scaled
+    per neuron by a lognormal factor (a few neurons carry most of the magnitude, as in section 3.4's coverage
+    curve).  quantum > 0 rounds every value to a multiple of it, which makes equal scores (ties) common."""
+    r = rng(cfg, _TAG_ACT, *path)
+    h = r.standard_normal(tuple(shape))
+    scale = np.exp(r.standard_normal(tuple(shape[:-1]) + (1,)))
+    h = h * scale
+    if quantum > 0:
+        h = np.round(h / quantum) * quantum
+    return h.astype(np.float32)
+
+
+def positive_norms(cfg: int, shape: Sequence[int], *path: int) -> np.ndarray:
+    """float32 stand-ins for down-projection row norms: 0.5 .. 1.5."""
+    return (0.5 + rng(cfg, _TAG_ACT, 1, *path).random(tuple(shape))).astype(np.float32)
 
 
 def group_reference_inputs(w: Workload, anchors: Sequence[int], scale: float = 0.1) -> List[np.ndarray]:

@@ -342,9 +342,10 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
         __syncthreads();
         // Thread tid forms h for neuron (tid & 7) of each group and token tid >> 3.
 #pragma unroll
-        for (int gg = 0; gg < NG; ++gg)
+        for (int gg = 0; gg < NG; ++gg) {
             auto red_g = [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; };
             gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8, cnt, rn);
+        }
         __syncthreads();
     }
 }
@@ -441,9 +442,10 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
         for (int tt = 0; tt < NT; ++tt) red[g][part][tt][lane] = acc[tt];
         __syncthreads();
 #pragma unroll
-        for (int gg = 0; gg < NG; ++gg)
+        for (int gg = 0; gg < NG; ++gg) {
             auto red_g = [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; };
             gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8, cnt, rn);
+        }
         __syncthreads();
     }
 }

@@ -39,6 +39,16 @@ def silu(z: np.ndarray) -> np.ndarray:
     return out
 
 
+def gelu_tanh(z: np.ndarray) -> np.ndarray:
+    """GELU in its tanh form, 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))), the gate activation of a GeGLU FFN
+    (section 3.4 names the scored activations post-GeGLU)."""
+    z = np.asarray(z, dtype=np.float64)
+    return 0.5 * z * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * (z + 0.044715 * z * z * z)))
+
+
+ACTIVATIONS = {"silu": silu, "gelu_tanh": gelu_tanh}
+
+
 def rms_norm(x: np.ndarray, g: np.ndarray, eps: float = RMS_EPS) -> np.ndarray:
     """RMSNorm over the last axis: x / sqrt(mean(x^2) + eps) * g.
 
@@ -90,39 +100,49 @@ def ffn_input(x: np.ndarray, norm_g: Optional[np.ndarray], eps: float = RMS_EPS)
 
 
 def hidden(x: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray, norm_g: Optional[np.ndarray] = None,
-           eps: float = RMS_EPS) -> np.ndarray:
-    """Dense post-GLU activations h[t,n] = SiLU(xn_t . W_gate[n]) * (xn_t . W_up[n]) for every neuron."""
+           eps: float = RMS_EPS, act: str = "silu") -> np.ndarray:
+    """Dense post-GLU activations h[t,n] = act(xn_t . W_gate[n]) * (xn_t . W_up[n]) for every neuron
+    (act = SiLU for SwiGLU, GELU-tanh for GeGLU)."""
     xn = ffn_input(x, norm_g, eps)
-    return silu(xn @ np.asarray(w_gate, np.float64).T) * (xn @ np.asarray(w_up, np.float64).T)
+    return ACTIVATIONS[act](xn @ np.asarray(w_gate, np.float64).T) * (xn @ np.asarray(w_up, np.float64).T)
+
+
+def _gated(f: np.ndarray, gate: Optional[np.ndarray]) -> np.ndarray:
+    """The adaptive output gate (section 4.1: the FFN output goes through the model's adaptive gate before the
+    residual addition): f * gate, gate broadcast over tokens ([d] per sample), or f without a gate."""
+    return f if gate is None else f * np.asarray(gate, np.float64)
 
 
 def masked_ffn(x: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray, mult: np.ndarray,
-               norm_g: Optional[np.ndarray] = None, eps: float = RMS_EPS) -> np.ndarray:
-    """y = x + (h * mult) W_down: the dense FFN with inactive neurons zeroed, plus the residual.
+               norm_g: Optional[np.ndarray] = None, eps: float = RMS_EPS, act: str = "silu",
+               gate: Optional[np.ndarray] = None) -> np.ndarray:
+    """y = x + gate * ((h * mult) W_down): the dense FFN with inactive neurons zeroed, plus the residual.
 
-    x: [T][d] (any leading batch axes); weights [d_ff][d]; mult [d_ff] (0/1 for a mask, counts for a multiset).
-    The residual adds the un-normalized x (pre-norm block).  Eq. 4 with y_a = 0 and h_a = 0.
+    x: [T][d] (any leading batch axes); weights [d_ff][d]; mult [d_ff] (0/1 for a mask, counts for a multiset);
+    gate: [d] (or None).  The residual adds the un-normalized x (pre-norm block).  Eq. 4 with y_a = 0, h_a = 0.
     """
     x64 = np.asarray(x, dtype=np.float64)
-    h = hidden(x64, w_gate, w_up, norm_g, eps) * np.asarray(mult, np.float64)
-    return x64 + h @ np.asarray(w_down, np.float64)
+    h = hidden(x64, w_gate, w_up, norm_g, eps, act) * np.asarray(mult, np.float64)
+    return x64 + _gated(h @ np.asarray(w_down, np.float64), gate)
 
 
-def dense_ffn(x, w_gate, w_up, w_down, norm_g=None, eps: float = RMS_EPS) -> np.ndarray:
-    """Dense SwiGLU FFN + residual (the anchor step, section 4.1): every neuron active."""
-    return masked_ffn(x, w_gate, w_up, w_down, np.ones(np.asarray(w_gate).shape[0]), norm_g, eps)
+def dense_ffn(x, w_gate, w_up, w_down, norm_g=None, eps: float = RMS_EPS, act: str = "silu",
+              gate=None) -> np.ndarray:
+    """Dense GLU FFN + residual (the anchor step, section 4.1): every neuron active."""
+    return masked_ffn(x, w_gate, w_up, w_down, np.ones(np.asarray(w_gate).shape[0]), norm_g, eps, act, gate)
 
 
 def ffn_stack(x: np.ndarray, layers: Sequence[tuple], mults: Sequence[np.ndarray], eps: float = RMS_EPS,
-              return_all: bool = False):
+              return_all: bool = False, act: str = "silu", gates: Optional[Sequence] = None):
     """Apply layers in order, feeding each layer's output to the next.
 
-    layers: sequence of (w_gate, w_up, w_down, norm_g) float64 tuples; mults: one multiplicity per layer.
+    layers: sequence of (w_gate, w_up, w_down, norm_g) float64 tuples; mults: one multiplicity per layer;
+    gates: one output gate ([d] or None) per layer, or None.
     """
     y = np.asarray(x, dtype=np.float64)
     outs = []
-    for (wg, wu, wd, g), m in zip(layers, mults):
-        y = masked_ffn(y, wg, wu, wd, m, g, eps)
+    for l, ((wg, wu, wd, g), m) in enumerate(zip(layers, mults)):
+        y = masked_ffn(y, wg, wu, wd, m, g, eps, act, None if gates is None else gates[l])
         outs.append(y)
     return outs if return_all else y
 
@@ -139,33 +159,36 @@ def local_update(y_anchor: np.ndarray, h_t: np.ndarray, h_anchor: np.ndarray, mu
     return np.asarray(y_anchor, np.float64) + dh @ np.asarray(w_down, np.float64)
 
 
-def anchor_stack(x: np.ndarray, layers: Sequence[tuple], eps: float = RMS_EPS):
+def anchor_stack(x: np.ndarray, layers: Sequence[tuple], eps: float = RMS_EPS, act: str = "silu",
+                 gates: Optional[Sequence] = None):
     """The anchor step of a group (section 4.1, "Anchors with Mask Recomputation"): the dense layers in order.
 
-    Returns (y, y_a, h_a): the last layer's output, and per layer the dense FFN output before the residual
-    (y_a, [L][..][T][d]) and the dense activations (h_a, [L][..][T][d_ff]) that the group's later steps reuse.
+    Returns (y, y_a, h_a): the last layer's output, and per layer the dense FFN output before the adaptive gate
+    and the residual (y_a, [L][..][T][d]) and the dense activations (h_a, [L][..][T][d_ff]) that the group's
+    later steps reuse.
     """
     y = np.asarray(x, dtype=np.float64)
     ya, ha = [], []
-    for wg, wu, wd, g in layers:
-        h = hidden(y, wg, wu, g, eps)
+    for l, (wg, wu, wd, g) in enumerate(layers):
+        h = hidden(y, wg, wu, g, eps, act)
         f = h @ np.asarray(wd, np.float64)
         ya.append(f)
         ha.append(h)
-        y = y + f
+        y = y + _gated(f, None if gates is None else gates[l])
     return y, np.stack(ya), np.stack(ha)
 
 
 def delta_stack(x: np.ndarray, layers: Sequence[tuple], mults: Sequence[np.ndarray], y_anchor: np.ndarray,
-                h_anchor: np.ndarray, eps: float = RMS_EPS) -> np.ndarray:
+                h_anchor: np.ndarray, eps: float = RMS_EPS, act: str = "silu",
+                gates: Optional[Sequence] = None) -> np.ndarray:
     """A non-anchor step of the group: at each layer the FFN output is Eq. 4's estimate from the anchor's y_a and
-    h_a (as returned by anchor_stack) and this step's activations of the masked neurons, followed by the
-    residual addition; layer l reads layer l-1's output.
+    h_a (as returned by anchor_stack) and this step's activations of the masked neurons, then the adaptive gate
+    of this step and the residual addition; layer l reads layer l-1's output.
     """
     y = np.asarray(x, dtype=np.float64)
     for l, ((wg, wu, wd, g), m) in enumerate(zip(layers, mults)):
-        h_t = hidden(y, wg, wu, g, eps)
-        y = y + local_update(y_anchor[l], h_t, h_anchor[l], m, wd)
+        h_t = hidden(y, wg, wu, g, eps, act)
+        y = y + _gated(local_update(y_anchor[l], h_t, h_anchor[l], m, wd), None if gates is None else gates[l])
     return y
 
 

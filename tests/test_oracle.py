@@ -25,8 +25,9 @@ def _rand_layer(seed, d, d_ff, norm=False):
     return wg, wu, wd, g
 
 
-def _torch_swiglu(x, wg, wu, wd, g=None, eps=1e-6, zero_down_rows=None, zero_up_rows=None):
-    """Textbook SwiGLU FFN + residual through torch's float64 library ops (an independent implementation)."""
+def _torch_swiglu(x, wg, wu, wd, g=None, eps=1e-6, zero_down_rows=None, zero_up_rows=None, act="silu", gate=None):
+    """Textbook SwiGLU (or GeGLU) FFN + residual through torch's float64 library ops (an independent
+    implementation); gate multiplies the FFN output before the residual."""
     xt = torch.tensor(x, dtype=torch.float64)
     wg_t = torch.tensor(wg, dtype=torch.float64)
     wu_t = torch.tensor(wu, dtype=torch.float64)
@@ -38,9 +39,67 @@ def _torch_swiglu(x, wg, wu, wd, g=None, eps=1e-6, zero_down_rows=None, zero_up_
     xn = xt
     if g is not None:
         xn = F.rms_norm(xt, (xt.shape[-1],), weight=torch.tensor(g, dtype=torch.float64), eps=eps)
-    h = F.silu(F.linear(xn, wg_t)) * F.linear(xn, wu_t)
+    a = F.linear(xn, wg_t)
+    h = (F.silu(a) if act == "silu" else F.gelu(a, approximate="tanh")) * F.linear(xn, wu_t)
     # nn.Linear convention: down_proj.weight is [d][d_ff] = transpose of the neuron-major rows.
-    return (xt + F.linear(h, wd_t.T.contiguous())).numpy()
+    f = F.linear(h, wd_t.T.contiguous())
+    if gate is not None:
+        f = f * torch.tensor(gate, dtype=torch.float64)
+    return (xt + f).numpy()
+
+
+# ------------------------------------------------------------------------------------------------ GeGLU, gate
+
+def test_gelu_tanh_matches_library_and_closed_forms():
+    z = np.concatenate([np.linspace(-12, 12, 2001), [-80.0, 80.0, 0.0, 1e-9]])
+    ref = F.gelu(torch.tensor(z, dtype=torch.float64), approximate="tanh").numpy()
+    assert np.max(np.abs(oracle.gelu_tanh(z) - ref)) < 1e-14
+    assert oracle.gelu_tanh(np.array([0.0]))[0] == 0.0
+    # tanh is odd, so gelu(z) - gelu(-z) = z.
+    assert np.max(np.abs(oracle.gelu_tanh(z) - oracle.gelu_tanh(-z) - z)) < 1e-12
+
+
+@pytest.mark.parametrize("norm", [False, True])
+def test_geglu_and_gate_match_torch(norm):
+    wg, wu, wd, g = _rand_layer(50, 16, 40, norm)
+    r = np.random.default_rng(51)
+    x = r.standard_normal((5, 16))
+    gate = 1.0 + 0.5 * r.standard_normal(16)
+    m = wl.bernoulli_mask(r, (40,), 0.5)
+    off = np.flatnonzero(m == 0)
+    got = oracle.masked_ffn(x, wg, wu, wd, m.astype(float), g, act="gelu_tanh", gate=gate)
+    ref = _torch_swiglu(x, wg, wu, wd, g, zero_down_rows=off, act="gelu_tanh", gate=gate)
+    assert np.max(np.abs(got - ref)) < 1e-13
+    # The gate scales the FFN part only: all ones is no gate, zeros leave the residual, and it is linear.
+    plain = oracle.masked_ffn(x, wg, wu, wd, m.astype(float), g)
+    assert np.array_equal(oracle.masked_ffn(x, wg, wu, wd, m.astype(float), g, gate=np.ones(16)), plain)
+    assert np.array_equal(oracle.masked_ffn(x, wg, wu, wd, m.astype(float), g, gate=np.zeros(16)), x)
+    twice = oracle.masked_ffn(x, wg, wu, wd, m.astype(float), g, gate=2 * np.ones(16))
+    assert np.max(np.abs((twice - x) - 2 * (plain - x))) < 1e-13
+
+
+def test_gated_geglu_anchor_and_delta_stacks():
+    layers = [_rand_layer(52 + l, 8, 12, True) for l in range(3)]
+    r = np.random.default_rng(55)
+    xa = r.standard_normal((4, 8))
+    xt = xa + 0.05 * r.standard_normal((4, 8))
+    ga = [1.0 + 0.3 * r.standard_normal(8) for _ in range(3)]  # the anchor step's gates
+    gt = [1.0 + 0.3 * r.standard_normal(8) for _ in range(3)]  # a later step's gates (another timestep)
+    y_anchor, ya, ha = oracle.anchor_stack(xa, layers, act="gelu_tanh", gates=ga)
+    ref = xa
+    for (wg, wu, wd, g), gg in zip(layers, ga):
+        ref = _torch_swiglu(ref, wg, wu, wd, g, act="gelu_tanh", gate=gg)
+    assert np.max(np.abs(y_anchor - ref)) < 1e-12
+    # Every neuron selected: the dense gated stack at the current input with the current gates, since y_a is
+    # kept before the gate.
+    full = oracle.delta_stack(xt, layers, [np.ones(12)] * 3, ya, ha, act="gelu_tanh", gates=gt)
+    ref = xt
+    for (wg, wu, wd, g), gg in zip(layers, gt):
+        ref = _torch_swiglu(ref, wg, wu, wd, g, act="gelu_tanh", gate=gg)
+    assert np.max(np.abs(full - ref)) < 1e-12
+    # No neuron selected: each layer adds its gated anchor output.
+    empty = oracle.delta_stack(xt, layers, [np.zeros(12)] * 3, ya, ha, act="gelu_tanh", gates=gt)
+    assert np.array_equal(empty, ((xt + ya[0] * gt[0]) + ya[1] * gt[1]) + ya[2] * gt[2])
 
 
 # ------------------------------------------------------------------------------------------------ SiLU

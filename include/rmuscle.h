@@ -8,7 +8,7 @@
  * (Eq. 4).  The core call is that update with a zero anchor, i.e. the masked SwiGLU FFN
  *
  *     y[b,t,:] = x[b,t,:] + sum_{i < count[b]} h[b,t,i] * w_down[idx[b][i], :]
- *     h[b,t,i] = SiLU(<w_gate[idx[b][i]], xn[b,t]>) * <w_up[idx[b][i]], xn[b,t]>
+ *     h[b,t,i] = act(<w_gate[idx[b][i]], xn[b,t]>) * <w_up[idx[b][i]], xn[b,t]>   (act: SiLU or GELU-tanh)
  *     xn       = norm_g ? x / sqrt(mean(x^2) + norm_eps) * norm_g : x
  *
  * where only the listed rows of w_gate / w_up / w_down are read.  Eq. 4 itself, with the group's dense
@@ -16,7 +16,9 @@
  *
  *     y[b,t,:] = x[b,t,:] + y_a[b,t,:] + sum_{i < count[b]} (h[b,t,i] - h_a[b,i,t]) * w_down[idx[b][i], :]
  *
- * with y_a the anchor's FFN output (before the residual) and h_a its activations of the listed neurons.
+ * with y_a the anchor's FFN output (before the residual) and h_a its activations of the listed neurons.  With an
+ * output gate (rm_ffn_layer_weights.out_gate) the FFN part of each formula is multiplied by it before the
+ * residual is added, and y_a is kept before the gate.
  *
  * Conventions shared by every call
  *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every buffer and the stream; the
@@ -53,13 +55,20 @@ typedef enum rm_status {
 
 typedef enum rm_dtype { RM_F32 = 0, RM_BF16 = 1 } rm_dtype;
 
+/* Activation of the gated linear unit: h = act(<w_gate, xn>) * <w_up, xn>.  SiLU makes the FFN a SwiGLU, the
+ * tanh form of GELU, 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))), a GeGLU (section 3.4 scores post-GeGLU
+ * activations). */
+typedef enum rm_act { RM_ACT_SILU = 0, RM_ACT_GELU_TANH = 1 } rm_act;
+
 /* Shape of one FFN layer.  d: model width (multiple of 32).  d_ff: intermediate neurons (>= 1).
- * wdtype: an rm_dtype.  norm_eps: RMSNorm epsilon (1e-6 in the workloads); ignored without norm_g. */
+ * wdtype: an rm_dtype.  norm_eps: RMSNorm epsilon (1e-6 in the workloads); ignored without norm_g.
+ * act: an rm_act. */
 typedef struct rm_ffn_shape {
     int32_t d;
     int32_t d_ff;
     int32_t wdtype;
     float norm_eps;
+    int32_t act;
 } rm_ffn_shape;
 
 /* Weights of one layer, all row-major [d_ff][d] in the dtype of rm_ffn_shape.wdtype.
@@ -67,13 +76,17 @@ typedef struct rm_ffn_shape {
  *   w_gate[n], w_up[n]: the gate and up projections (PyTorch nn.Linear weights of shape [d_ff][d]);
  *   w_down[n]: the neuron's down-projection row, i.e. the row-vector form W^down of Eq. 4 (the transpose of a
  *              PyTorch down_proj.weight of shape [d][d_ff]), so that a neuron's down weights are contiguous.
- * norm_g: float32 [d] RMSNorm gain applied to the FFN input, or NULL for no norm.  All pointers 16-byte
- * aligned.  Read-only. */
+ * norm_g: float32 [d] RMSNorm gain applied to the FFN input, or NULL for no norm.
+ * out_gate: float32 [B][d], the adaptive output gate of each sample for this layer and step (section 4.1: the
+ *           FFN output goes through the model's adaptive gate before the residual addition), or NULL for none:
+ *           y = x + out_gate[b] * FFN(x) elementwise over columns, for every token of sample b.
+ * All pointers 16-byte aligned.  Read-only. */
 typedef struct rm_ffn_layer_weights {
     const void *w_gate;
     const void *w_up;
     const void *w_down;
     const float *norm_g;
+    const float *out_gate;
 } rm_ffn_layer_weights;
 
 /* Mask -> ascending active-neuron index list (section 4.1: a reference stores its selected neuron indices;

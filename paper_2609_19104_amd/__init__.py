@@ -33,6 +33,9 @@ RM_ERR_HIP = -6
 
 RM_F32 = 0
 RM_BF16 = 1
+RM_ACT_SILU = 0
+RM_ACT_GELU_TANH = 1
+ACTS = {"silu": RM_ACT_SILU, "gelu_tanh": RM_ACT_GELU_TANH}
 RM_KERNEL_GATEUP = 0
 RM_KERNEL_DOWN = 1
 RM_KERNEL_SCORES = 2
@@ -43,7 +46,8 @@ EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_s
             "rm_delta_ffn_stack", "rm_neuron_norms", "rm_group_masks", "rm_profile_kernel_events",
             "rm_status_string", "rm_last_error")
 
-Layer = Tuple[torch.Tensor, torch.Tensor, torch.Tensor, Optional[torch.Tensor]]
+# (w_gate, w_up, w_down, norm_g) or (w_gate, w_up, w_down, norm_g, out_gate); norm_g and out_gate may be None.
+Layer = Tuple[Optional[torch.Tensor], ...]
 
 
 class RmError(RuntimeError):
@@ -55,12 +59,12 @@ class RmError(RuntimeError):
 
 class FfnShape(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("d_ff", ctypes.c_int32), ("wdtype", ctypes.c_int32),
-                ("norm_eps", ctypes.c_float)]
+                ("norm_eps", ctypes.c_float), ("act", ctypes.c_int32)]
 
 
 class LayerWeights(ctypes.Structure):
     _fields_ = [("w_gate", ctypes.c_void_p), ("w_up", ctypes.c_void_p), ("w_down", ctypes.c_void_p),
-                ("norm_g", ctypes.c_void_p)]
+                ("norm_g", ctypes.c_void_p), ("out_gate", ctypes.c_void_p)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -149,13 +153,18 @@ def wdtype_of(t: torch.Tensor) -> int:
     raise ValueError(f"weights must be float32 or bfloat16, got {t.dtype}")
 
 
-def _shape(layer: Layer, eps: float) -> FfnShape:
+def _shape(layer: Layer, eps: float, act: str = "silu") -> FfnShape:
     wg = layer[0]
-    return FfnShape(int(wg.shape[1]), int(wg.shape[0]), wdtype_of(wg), float(eps))
+    if act not in ACTS:
+        raise ValueError(f"act must be one of {sorted(ACTS)}, got {act!r}")
+    return FfnShape(int(wg.shape[1]), int(wg.shape[0]), wdtype_of(wg), float(eps), ACTS[act])
 
 
-def _weights(layer: Layer) -> LayerWeights:
-    wg, wu, wd, g = layer
+def _weights(layer: Layer, B: Optional[int] = None) -> LayerWeights:
+    if len(layer) not in (4, 5):
+        raise ValueError("a layer is (w_gate, w_up, w_down, norm_g[, out_gate])")
+    wg, wu, wd, g = layer[:4]
+    gate = layer[4] if len(layer) == 5 else None
     d_ff, d = wg.shape
     for name, w in (("w_gate", wg), ("w_up", wu), ("w_down", wd)):
         _need_cuda(name, w, (wg.dtype,), 2)
@@ -165,7 +174,11 @@ def _weights(layer: Layer) -> LayerWeights:
         _need_cuda("norm_g", g, (torch.float32,), 1)
         if g.shape[0] != d:
             raise ValueError("norm_g must have d entries")
-    return LayerWeights(wg.data_ptr(), wu.data_ptr(), wd.data_ptr(), _ptr(g))
+    if gate is not None:
+        _need_cuda("out_gate", gate, (torch.float32,))
+        if B is not None and gate.numel() != B * d:
+            raise ValueError(f"out_gate must be [B][d] = [{B}][{d}]")
+    return LayerWeights(wg.data_ptr(), wu.data_ptr(), wd.data_ptr(), _ptr(g), _ptr(gate))
 
 
 def _activations(x: torch.Tensor, y: torch.Tensor, d: int) -> Tuple[int, int]:
@@ -210,11 +223,11 @@ def _ws(ws: torch.Tensor) -> Tuple[int, int]:
 
 
 def rm_sparse_ffn_layer(x: torch.Tensor, y: torch.Tensor, layer: Layer, idx: torch.Tensor, count: torch.Tensor,
-                        max_count: int, ws: torch.Tensor, eps: float = 1e-6, stream=None) -> None:
-    """y = x + masked SwiGLU FFN over the listed neurons (y may be x)."""
-    shape = _shape(layer, eps)
-    w = _weights(layer)
+                        max_count: int, ws: torch.Tensor, eps: float = 1e-6, act: str = "silu", stream=None) -> None:
+    """y = x + masked GLU FFN over the listed neurons (y may be x); act "silu" (SwiGLU) or "gelu_tanh" (GeGLU)."""
+    shape = _shape(layer, eps, act)
     B, T = _activations(x, y, shape.d)
+    w = _weights(layer, B)
     _need_cuda("idx", idx, (torch.int32,))
     _need_cuda("count", count, (torch.int32,))
     if idx.numel() != B * shape.d_ff or count.numel() != B:
@@ -226,18 +239,18 @@ def rm_sparse_ffn_layer(x: torch.Tensor, y: torch.Tensor, layer: Layer, idx: tor
 
 
 def _stack_args(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
-                count: torch.Tensor, eps: float):
+                count: torch.Tensor, eps: float, act: str):
     L = len(layers)
     if L == 0:
         raise ValueError("at least one layer")
-    shape = _shape(layers[0], eps)
+    shape = _shape(layers[0], eps, act)
+    B, T = _activations(x, y, shape.d)
     arr = (LayerWeights * L)()
     for l, layer in enumerate(layers):
-        s = _shape(layer, eps)
+        s = _shape(layer, eps, act)
         if (s.d, s.d_ff, s.wdtype) != (shape.d, shape.d_ff, shape.wdtype):
             raise ValueError("every layer of a stack must have the same shape and dtype")
-        arr[l] = _weights(layer)
-    B, T = _activations(x, y, shape.d)
+        arr[l] = _weights(layer, B)
     _need_cuda("idx", idx, (torch.int32,))
     _need_cuda("count", count, (torch.int32,))
     if idx.numel() != L * B * shape.d_ff or count.numel() != L * B:
@@ -256,10 +269,10 @@ def _anchor_state(y_anchor: torch.Tensor, h_anchor: torch.Tensor, L: int, B: int
 
 
 def rm_sparse_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
-                        count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6,
+                        count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6, act: str = "silu",
                         stream=None) -> None:
     """L masked FFN layers in order; idx [L][B][d_ff], count [L][B]."""
-    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps)
+    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps, act)
     wp, wn = _ws(ws)
     _check(load_library().rm_sparse_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
                                               idx.data_ptr(), count.data_ptr(), int(max_count), wp, wn,
@@ -275,12 +288,12 @@ def _masks(mask: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, n: int, d
 
 
 def rm_masked_ffn_layer(x: torch.Tensor, y: torch.Tensor, layer: Layer, mask: torch.Tensor, idx: torch.Tensor,
-                        count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6,
+                        count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6, act: str = "silu",
                         stream=None) -> None:
     """rm_mask_compact(mask -> idx, count) + rm_sparse_ffn_layer, the compaction inside the layer's first launch."""
-    shape = _shape(layer, eps)
-    w = _weights(layer)
+    shape = _shape(layer, eps, act)
     B, T = _activations(x, y, shape.d)
+    w = _weights(layer, B)
     _masks(mask, idx, count, B, shape.d_ff)
     wp, wn = _ws(ws)
     _check(load_library().rm_masked_ffn_layer(ctypes.byref(shape), ctypes.byref(w), B, T, x.data_ptr(),
@@ -290,9 +303,9 @@ def rm_masked_ffn_layer(x: torch.Tensor, y: torch.Tensor, layer: Layer, mask: to
 
 def rm_masked_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], mask: torch.Tensor,
                         idx: torch.Tensor, count: torch.Tensor, max_count: int, ws: torch.Tensor, eps: float = 1e-6,
-                        stream=None) -> None:
+                        act: str = "silu", stream=None) -> None:
     """rm_mask_compact of [L][B] masks + rm_sparse_ffn_stack, the compaction inside the stack's first launch."""
-    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps)
+    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps, act)
     _masks(mask, idx, count, L * B, shape.d_ff)
     wp, wn = _ws(ws)
     _check(load_library().rm_masked_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
@@ -302,10 +315,10 @@ def rm_masked_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer
 
 def rm_anchor_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
                         count: torch.Tensor, max_count: int, y_anchor: torch.Tensor, h_anchor: torch.Tensor,
-                        ws: torch.Tensor, eps: float = 1e-6, stream=None) -> None:
+                        ws: torch.Tensor, eps: float = 1e-6, act: str = "silu", stream=None) -> None:
     """Eq. 4 anchor step: L dense layers; keeps y_a [L][B][T][d] and h_a of the group's lists [L][B][max_count][T].
     The workspace is sized with max_count = d_ff."""
-    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps)
+    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps, act)
     _anchor_state(y_anchor, h_anchor, L, B, T, shape.d, int(max_count))
     wp, wn = _ws(ws)
     _check(load_library().rm_anchor_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
@@ -315,9 +328,9 @@ def rm_anchor_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer
 
 def rm_delta_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,
                        count: torch.Tensor, max_count: int, y_anchor: torch.Tensor, h_anchor: torch.Tensor,
-                       ws: torch.Tensor, eps: float = 1e-6, stream=None) -> None:
+                       ws: torch.Tensor, eps: float = 1e-6, act: str = "silu", stream=None) -> None:
     """Eq. 4 non-anchor step: y = x + y_a + (h - h_a) W_down over the listed neurons, per layer."""
-    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps)
+    shape, arr, L, B, T = _stack_args(x, y, layers, idx, count, eps, act)
     _anchor_state(y_anchor, h_anchor, L, B, T, shape.d, int(max_count))
     wp, wn = _ws(ws)
     _check(load_library().rm_delta_ffn_stack(ctypes.byref(shape), arr, L, B, T, x.data_ptr(), y.data_ptr(),
@@ -326,11 +339,11 @@ def rm_delta_ffn_stack(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer]
 
 
 def rm_dense_ffn_ref(x: torch.Tensor, y: torch.Tensor, layer: Layer, ws: torch.Tensor, eps: float = 1e-6,
-                     stream=None) -> None:
-    """y = x + dense SwiGLU FFN (every neuron)."""
-    shape = _shape(layer, eps)
-    w = _weights(layer)
+                     act: str = "silu", stream=None) -> None:
+    """y = x + dense GLU FFN (every neuron)."""
+    shape = _shape(layer, eps, act)
     B, T = _activations(x, y, shape.d)
+    w = _weights(layer, B)
     wp, wn = _ws(ws)
     _check(load_library().rm_dense_ffn_ref(ctypes.byref(shape), ctypes.byref(w), B, T, x.data_ptr(), y.data_ptr(),
                                            wp, wn, _stream(stream)))

@@ -27,7 +27,8 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
                                                             int nblk, void *__restrict__ xn_next,
                                                             const float *__restrict__ g_next,
                                                             float *__restrict__ ssq, const float *__restrict__ ya_in,
-                                                            float *__restrict__ ya_out) {
+                                                            float *__restrict__ ya_out,
+                                                            const float *__restrict__ out_gate) {
     const int row = blockIdx.x / nblk;
     const int blk = blockIdx.x - row * nblk;
     const int b = row / T;
@@ -55,10 +56,14 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
                 if (s + i < used) acc = add4(acc, v[i]);
         }
     }
-    if (ya_in != nullptr) {  // Eq. 4: y = x + (y_a + (h - h_a) W_down)
-        out = add4(out, add4(ld4(ya_in + ro), acc));
-    } else if (used > 0) {
-        out = add4(out, acc);
+    if (ya_in != nullptr || used > 0) {  // an empty list without an anchor leaves y = x bit for bit
+        float4 f = acc;
+        if (ya_in != nullptr) f = add4(ld4(ya_in + ro), acc);  // Eq. 4: the FFN output is y_a + (h - h_a) W_down
+        if (out_gate != nullptr) {  // the adaptive output gate, before the residual
+            const float4 g = ld4(out_gate + static_cast<size_t>(b) * d + cc);
+            f = make_float4(f.x * g.x, f.y * g.y, f.z * g.z, f.w * g.w);
+        }
+        out = add4(out, f);
     }
     if (ok) {
         *reinterpret_cast<float4 *>(y + ro) = out;
@@ -92,7 +97,8 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
 namespace rm {
 
 hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, float *y, const float *g_next,
-                           bool emit_xn, const float *ya_in, float *ya_out, void *ws, hipStream_t st) {
+                           bool emit_xn, const float *ya_in, float *ya_out, const float *out_gate, void *ws,
+                           hipStream_t st) {
     char *base = static_cast<char *>(ws);
     const float *part = reinterpret_cast<const float *>(base + p.off_part);
     void *xn = emit_xn ? static_cast<void *>(base + p.off_xn) : nullptr;
@@ -103,10 +109,10 @@ hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, 
     const float *g = emit_xn ? g_next : nullptr;
     if (p.wdtype == RM_BF16)
         hipLaunchKernelGGL(epilogue_kernel<true>, grid, dim3(kThreads), 0, st, part, p.slices, slice_neurons, count,
-                           p.max_count, x, y, p.T, p.d, nblk, xn, g, ssq, ya_in, ya_out);
+                           p.max_count, x, y, p.T, p.d, nblk, xn, g, ssq, ya_in, ya_out, out_gate);
     else
         hipLaunchKernelGGL(epilogue_kernel<false>, grid, dim3(kThreads), 0, st, part, p.slices, slice_neurons,
-                           count, p.max_count, x, y, p.T, p.d, nblk, xn, g, ssq, ya_in, ya_out);
+                           count, p.max_count, x, y, p.T, p.d, nblk, xn, g, ssq, ya_in, ya_out, out_gate);
     return hipGetLastError();
 }
 

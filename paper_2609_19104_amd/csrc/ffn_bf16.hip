@@ -72,7 +72,7 @@ struct GuArgs {
     const int32_t *idx, *count;
     const float *ssq;  // [B][T][d / 256] per-token partial sums of squares, or null (no norm)
     float eps;
-    int max_count, d_ff, d, T, tpad, kcap, B;
+    int max_count, d_ff, d, T, tpad, kcap, B, act;
     uint16_t *H;
     // Eq. 4 (optional, [B][max_count][T] float32): h_anchor is subtracted from h before it is rounded into H
     // (the delta step); with h_out the kernel writes h there in float32 instead of writing H (the anchor step).
@@ -120,7 +120,7 @@ __device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, int b,
             usum += red(w, tt, lu)[reg];
         }
         const float r = rn[tok];
-        h = rm_silu(gsum * r) * (usum * r);
+        h = rm_glu_act(a.act, gsum * r) * (usum * r);
     }
     const int slot = slot_base + j;
     const int t = t0 + tok;
@@ -721,7 +721,8 @@ struct DfArgs {
     float *y;
     const float *ya_in;
     float *ya_out;
-    const float *g_next;  // with xn_next: the next layer's norm gain, or null for no norm
+    const float *out_gate;  // [B][d] adaptive output gate, or null
+    const float *g_next;    // with xn_next: the next layer's norm gain, or null for no norm
     uint16_t *xn_next;    // the next layer's FFN input, or null
     float *ssq;
 };
@@ -806,12 +807,17 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     const float4 acc4 = make_float4(v[0], v[1], v[2], v[3]);
     float4 out = *reinterpret_cast<const float4 *>(a.x + ro);
     cnt = cnt < 0 ? 0 : (cnt > a.max_count ? a.max_count : cnt);
-    if (a.ya_in != nullptr) {  // Eq. 4: y = x + (y_a + (h - h_a) W_down)
-        const float4 ya = *reinterpret_cast<const float4 *>(a.ya_in + ro);
-        out = make_float4(out.x + (ya.x + acc4.x), out.y + (ya.y + acc4.y), out.z + (ya.z + acc4.z),
-                          out.w + (ya.w + acc4.w));
-    } else if (cnt > 0) {  // an empty list leaves y = x bit for bit
-        out = make_float4(out.x + acc4.x, out.y + acc4.y, out.z + acc4.z, out.w + acc4.w);
+    if (a.ya_in != nullptr || cnt > 0) {  // an empty list without an anchor leaves y = x bit for bit
+        float4 f = acc4;
+        if (a.ya_in != nullptr) {  // Eq. 4: the FFN output is y_a + (h - h_a) W_down
+            const float4 ya = *reinterpret_cast<const float4 *>(a.ya_in + ro);
+            f = make_float4(ya.x + acc4.x, ya.y + acc4.y, ya.z + acc4.z, ya.w + acc4.w);
+        }
+        if (a.out_gate != nullptr) {  // the adaptive output gate, before the residual
+            const float4 g = *reinterpret_cast<const float4 *>(a.out_gate + static_cast<size_t>(b) * a.d + col);
+            f = make_float4(f.x * g.x, f.y * g.y, f.z * g.z, f.w * g.w);
+        }
+        out = make_float4(out.x + f.x, out.y + f.y, out.z + f.z, out.w + f.w);
     }
     const bool st = live && colok;
     if (st) {
@@ -932,6 +938,7 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
     a.tpad = p.tpad;
     a.kcap = p.kcap;
     a.B = p.B;
+    a.act = p.act;
     a.H = reinterpret_cast<uint16_t *>(base + p.off_h);
     a.h_anchor = h_anchor;
     a.h_out = h_out;
@@ -947,7 +954,7 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
 
 hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
                              const float *x, float *y, const float *g_next, bool emit_xn, const float *ya_in,
-                             float *ya_out, void *ws, hipStream_t st) {
+                             float *ya_out, const float *out_gate, void *ws, hipStream_t st) {
     char *base = static_cast<char *>(ws);
     DfArgs a;
     a.H = reinterpret_cast<const uint16_t *>(base + p.off_h);
@@ -967,6 +974,7 @@ hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *i
     a.y = y;
     a.ya_in = ya_in;
     a.ya_out = ya_out;
+    a.out_gate = out_gate;
     a.g_next = emit_xn ? g_next : nullptr;
     a.xn_next = emit_xn ? reinterpret_cast<uint16_t *>(base + p.off_xn) : nullptr;
     a.ssq = reinterpret_cast<float *>(base + p.off_ssq);

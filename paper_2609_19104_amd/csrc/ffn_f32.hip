@@ -23,7 +23,7 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
     const float *__restrict__ wg, const float *__restrict__ wu, const float *__restrict__ xn,
     const int32_t *__restrict__ idx, const int32_t *__restrict__ count, int max_count, int d_ff, int d, int T,
     int tpad, float *__restrict__ H, int kcap, const float *__restrict__ ssq, float eps,
-    const float *__restrict__ h_anchor, float *__restrict__ h_out) {
+    const float *__restrict__ h_anchor, float *__restrict__ h_out, int act) {
     const int b = blockIdx.y;
     const int slot0 = blockIdx.x * rm::kF32NeurPerBlk;
     const int lane = threadIdx.x;
@@ -89,7 +89,7 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
             if (cl < nt) {
                 float rn = 1.0f;
                 if (ssq != nullptr) rn = rm_token_rnorm(ssq, b * T + t0 + cl, d, eps);
-                h = rm_silu(gs * rn) * (us * rn);
+                h = rm_glu_act(act, gs * rn) * (us * rn);
             }
             // Eq. 4: the anchor step keeps h of the listed slots; a delta step stores h - h_anchor.
             const size_t ai = (static_cast<size_t>(b) * max_count + slot) * T + t0 + cl;
@@ -165,7 +165,7 @@ hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up
     const float *ssq = norm ? reinterpret_cast<const float *>(base + p.off_ssq) : nullptr;
     launch_timed(RM_KERNEL_GATEUP, gateup_f32_kernel, dim3(p.gate_blocks, p.B), dim3(kWave), st,
                  static_cast<const float *>(w_gate), static_cast<const float *>(w_up), xn, idx, count, p.max_count,
-                 p.d_ff, p.d, p.T, p.tpad, H, p.kcap, ssq, p.eps, h_anchor, h_out);
+                 p.d_ff, p.d, p.T, p.tpad, H, p.kcap, ssq, p.eps, h_anchor, h_out, p.act);
     hipError_t e = hipGetLastError();
     return e;
 }

@@ -47,6 +47,7 @@ rm_status check_shape(const rm_ffn_shape *s) {
     if (s->d % 32 != 0) return fail(RM_ERR_SHAPE, "d=%d must be a multiple of 32", s->d);
     if (s->wdtype != RM_F32 && s->wdtype != RM_BF16) return fail(RM_ERR_DTYPE, "unknown weight dtype %d", s->wdtype);
     if (!(s->norm_eps >= 0.0f)) return fail(RM_ERR_INVALID_ARG, "norm_eps must be >= 0");
+    if (s->act != RM_ACT_SILU && s->act != RM_ACT_GELU_TANH) return fail(RM_ERR_INVALID_ARG, "unknown act %d", s->act);
     return RM_OK;
 }
 
@@ -55,8 +56,8 @@ rm_status check_layer(const rm_ffn_layer_weights *w, int l) {
     if (!w->w_gate || !w->w_up || !w->w_down)
         return fail(RM_ERR_INVALID_ARG, "layer %d: a weight pointer is NULL", l);
     if (!aligned(w->w_gate, 16) || !aligned(w->w_up, 16) || !aligned(w->w_down, 16) ||
-        (w->norm_g && !aligned(w->norm_g, 16)))
-        return fail(RM_ERR_ALIGN, "layer %d: weight and gain pointers must be 16-byte aligned", l);
+        (w->norm_g && !aligned(w->norm_g, 16)) || (w->out_gate && !aligned(w->out_gate, 16)))
+        return fail(RM_ERR_ALIGN, "layer %d: weight, gain and gate pointers must be 16-byte aligned", l);
     return RM_OK;
 }
 
@@ -147,6 +148,10 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
                      const int32_t *idx, const int32_t *count, size_t list_stride, size_t count_stride, void *ws,
                      hipStream_t st, const AnchorTerms &at = AnchorTerms{}, const uint8_t *mask = nullptr,
                      int n_masks = 0) {
+    const size_t act_bytes = static_cast<size_t>(p.B) * p.T * p.d * sizeof(float);
+    for (int l = 0; l < L; ++l)  // checked before anything is enqueued
+        if (w[l].out_gate && ranges_overlap(w[l].out_gate, static_cast<size_t>(p.B) * p.d * sizeof(float), y, act_bytes))
+            return fail(RM_ERR_INVALID_ARG, "layer %d: out_gate overlaps y", l);
     hipError_t e = mask ? rm::launch_compact_prologue(p, mask, n_masks, const_cast<int32_t *>(idx),
                                                       const_cast<int32_t *>(count), x, w[0].norm_g, ws, st)
                         : rm::launch_prologue(p, x, w[0].norm_g, ws, st);
@@ -180,13 +185,14 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
         const float *ya_in = at.ya_in ? at.ya_in + l * y_stride : nullptr;
         float *ya_out = at.ya_out ? at.ya_out + l * y_stride : nullptr;
         if (fused) {  // down projection and epilogue in one launch
-            e = rm::launch_down_fused(p, w[l].w_down, il, cl, xin, y, g_next, next, ya_in, ya_out, ws, st);
+            e = rm::launch_down_fused(p, w[l].w_down, il, cl, xin, y, g_next, next, ya_in, ya_out, w[l].out_gate,
+                                      ws, st);
             if (e != hipSuccess) return hip_fail(e, "down launch");
             continue;
         }
         e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
         if (e != hipSuccess) return hip_fail(e, "down launch");
-        e = rm::launch_epilogue(p, cl, xin, y, g_next, next, ya_in, ya_out, ws, st);
+        e = rm::launch_epilogue(p, cl, xin, y, g_next, next, ya_in, ya_out, w[l].out_gate, ws, st);
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }
     return RM_OK;
@@ -205,6 +211,7 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.T = T;
     q.max_count = max_count;
     q.eps = s->norm_eps;
+    q.act = s->act;
     const int kmax = max_count > 0 ? max_count : 1;
     size_t xn_elem, h_elem;
     // Aim for about four down-projection workgroups per compute unit (256 CUs).

@@ -43,7 +43,7 @@ constexpr int kF32ColTile = 256;    // output columns per down wave (64 lanes x 
 constexpr int kF32SliceNeur = 16;   // neurons per down K-slice
 
 struct Plan {
-    int d = 0, d_ff = 0, wdtype = 0, B = 0, T = 0, max_count = 0;
+    int d = 0, d_ff = 0, wdtype = 0, B = 0, T = 0, max_count = 0, act = RM_ACT_SILU;
     float eps = 1e-6f;
     int tpad = 0;        // T rounded up to the token block (rows of H)
     int kcap = 0;        // row length of H (neuron slots), max_count rounded up
@@ -111,15 +111,17 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
 // launch_down_bf16 + launch_epilogue up to the order of the K sum).
 hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
                              const float *x, float *y, const float *g_next, bool emit_xn, const float *ya_in,
-                             float *ya_out, void *ws, hipStream_t st);
+                             float *ya_out, const float *out_gate, void *ws, hipStream_t st);
 hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
                            hipStream_t st);
 
 // y = x + the slices' partials in slice order; if emit_xn, also the next layer's FFN input (y * g_next, or y)
 // and, with g_next, its per-token sums of squares.  Eq. 4 (optional, [B][T][d] float32): y = x + (ya_in +
-// partials) on a delta step; ya_out receives the partials' sum (the FFN output) on an anchor step.
+// partials) on a delta step; ya_out receives the partials' sum (the FFN output) on an anchor step.  out_gate
+// (optional, [B][d]) multiplies the FFN part before the residual.
 hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, float *y, const float *g_next,
-                           bool emit_xn, const float *ya_in, float *ya_out, void *ws, hipStream_t st);
+                           bool emit_xn, const float *ya_in, float *ya_out, const float *out_gate, void *ws,
+                           hipStream_t st);
 
 // Profiling hook: the events armed by rm_profile_kernel_events for the next launch of `kernel` by this thread
 // (null when disarmed), which are disarmed by taking them.
@@ -203,3 +205,13 @@ __device__ __forceinline__ float rm_ssq64(float4 v, bool ok) {
 
 // SiLU(z) = z / (1 + e^-z); e^-z overflows to +inf for very negative z, giving -0, never NaN.
 __device__ __forceinline__ float rm_silu(float z) { return z / (1.0f + expf(-z)); }
+
+// GELU, tanh form: 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))); tanh saturates, so large |z| gives z or -0.
+__device__ __forceinline__ float rm_gelu_tanh(float z) {
+    return 0.5f * z * (1.0f + tanhf(0.7978845608028654f * (z + 0.044715f * z * z * z)));
+}
+
+// The gated linear unit's activation (act: an rm_act).
+__device__ __forceinline__ float rm_glu_act(int act, float z) {
+    return act == RM_ACT_GELU_TANH ? rm_gelu_tanh(z) : rm_silu(z);
+}

@@ -22,12 +22,13 @@ oracle timed on a bounded sample of the same workload.
 
 Other workloads (--workload): the wide layer d = 2048, d_ff = 16384 at 10/30/50/100% (c4-*); the 18-layer stack
 run through a 10-step denoising schedule, one step of the benchmark being the whole sequence (c3); the same
-sequence with Eq. 4's dense anchors at steps 0 and 5 and anchor-delta updates at the other steps (c3-eq4); and
+sequence with Eq. 4's dense anchors at steps 0 and 5 and anchor-delta updates at the other steps (c3-eq4), also
+with the group's rows copied into compact buffers first (c3-eq4-compact); and
 16 independent executions through the stack with per-sample lists (c5); and the construction of one group's
 neuron masks from 5 reference steps of the stack (gm).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c3-eq4|c5|gm]
+                       [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c3-eq4|c3-eq4-compact|c5|gm]
 """
 from __future__ import annotations
 
@@ -92,6 +93,9 @@ WORKLOADS = {
     "c3-eq4": dict(name="action-expert FFN stack, 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, 10 denoising steps "
                         "with Eq. 4: dense anchors at steps 0 and 5, each shared by the next 4 steps with top-30% "
                         "group masks", cfg=3, percent=30),
+    "c3-eq4-compact": dict(name="the c3-eq4 sequence with the group's selected rows copied into compact buffers "
+                                "(on a side stream, during the anchor step) and the delta steps run on them",
+                           cfg=3, percent=30),
     "gm": dict(name="group neuron masks for the config-3 stack: 5 reference steps x 18 layers, d_ff=4096, T=51, "
                     "K=1229 (top 30%)", cfg=3, percent=30),
     "c5": dict(name="16 independent executions x 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, per-sample top-30% "
@@ -108,6 +112,10 @@ STEP_TEXT = {
     "c3-eq4": "one 10-step sequence: per group (anchors 0 and 5) rm_mask_compact (18 masks) + "
               "rm_anchor_ffn_stack (L=18) + 4 rm_delta_ffn_stack (L=18), replayed from HIP graphs; "
               "us_per_layer = sequence time / 180",
+    "c3-eq4-compact": "one 10-step sequence: per group rm_mask_compact (18 masks), then rm_gather_stack_rows "
+                      "(18 layers x 3 matrices) on a side stream beside rm_anchor_ffn_stack (L=18), then 4 "
+                      "rm_delta_ffn_stack (L=18) on the compact layers; replayed from HIP graphs; "
+                      "us_per_layer = sequence time / 180",
     "gm": "rm_group_masks: Eq. 1 scores of 5 steps x 18 layers from their dense activations (float32 "
           "[5][18][4096][51], written by rm_anchor_ffn_stack with identity lists at set-up), per-step top-K, union "
           "and rerank; replayed from HIP graphs; us_per_layer = step time / 18",
@@ -364,6 +372,43 @@ class StackSetupEq4:
         return ffn_hooks(self.rm, gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2))
 
 
+class StackSetupEq4Compact(StackSetupEq4):
+    """The anchored schedule with section 4.1's compact buffers: each group's selected rows of the 18 layers are
+    copied once (rm_gather_stack_rows, on a side stream while the main stream runs the dense anchor step) and the
+    group's delta steps read those contiguous rows through the identity lists."""
+
+    def __init__(self, key: str, device, cold: bool = True):
+        import torch
+        super().__init__(key, device, cold)
+        # One compact buffer per group (the two groups' copies would alternate in a deployment; here each group
+        # keeps its own so that replays need no ordering between them).
+        self.compact = [torch.empty((self.L, 3, self.k, self.d), dtype=torch.bfloat16, device=device)
+                        for _ in self.ANCHORS]
+        self.ident = torch.arange(self.k, dtype=torch.int32, device=device).repeat(self.L, 1).contiguous()
+        self.ws_c = self.rm.workspace(self.d, self.k, self.rm.RM_BF16, 1, self.T, self.k, device=device)
+        self.side = torch.cuda.Stream(device=device)
+
+    def step(self, i: int) -> None:
+        import torch
+        rm, layers = self.rm, self.layer_copies[i % self.rotate]
+        main = torch.cuda.current_stream()
+        for s in range(self.steps):
+            if s in self.ANCHORS:
+                g = self.ANCHORS.index(s)
+                rm.rm_mask_compact(self.masks[g], self.idx[g], self.cnt[g])
+                self.side.wait_stream(main)
+                with torch.cuda.stream(self.side):
+                    rm.rm_gather_stack_rows(layers, self.idx[g], self.cnt[g], self.k, self.compact[g])
+                rm.rm_anchor_ffn_stack(self.xs[s], self.y, layers, self.idx[g], self.cnt[g], self.k, self.ya,
+                                       self.ha, self.ws_dense)
+                main.wait_stream(self.side)
+                clayers = [(self.compact[g][l, 0], self.compact[g][l, 1], self.compact[g][l, 2], layers[l][3])
+                           for l in range(self.L)]
+            else:
+                rm.rm_delta_ffn_stack(self.xs[s], self.y, clayers, self.ident, self.cnt[g], self.k, self.ya,
+                                      self.ha, self.ws_c)
+
+
 class GroupMaskSetup:
     """Group-mask construction (section 5) for one group of the config-3 stack: the dense activations of 5
     reference steps (inputs x_0 .. x_4 of config 3, each run through rm_anchor_ffn_stack with the identity lists,
@@ -598,7 +643,8 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "copies": args.steps}))
         return 0
-    setup = {"c3": StackSetup3, "c3-eq4": StackSetupEq4, "c5": StackSetup5, "gm": GroupMaskSetup}.get(
+    setup = {"c3": StackSetup3, "c3-eq4": StackSetupEq4, "c3-eq4-compact": StackSetupEq4Compact, "c5": StackSetup5,
+             "gm": GroupMaskSetup}.get(
         args.workload, Setup)(
         args.workload, dev, cold=True)
 

@@ -187,6 +187,20 @@ rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *
                              const float *x, float *y, const int32_t *idx, const int32_t *count, int32_t max_count,
                              const float *y_anchor, const float *h_anchor, void *ws, size_t ws_bytes, void *stream);
 
+/* Compact copies of a group's selected weight rows (section 4.1: the selected weights are prepared in shared
+ * compact buffers reused across the group's steps).  For every layer l of a stack and its list (one list per
+ * layer, the group's mask: idx int32 [L][d_ff], count int32 [L], the rm_mask_compact layout with B = 1):
+ *     out[l][0][i] = w[l].w_gate[idx[l][i]],  out[l][1][i] = w[l].w_up[idx[l][i]],
+ *     out[l][2][i] = w[l].w_down[idx[l][i]]
+ * for i < count[l] (clamped to max_count), and zero rows for count[l] <= i < max_count.
+ *   out: [L][3][max_count][d] in the weights' dtype, 16-byte aligned, must not overlap the weights, idx or count.
+ *   max_count in [1, d_ff].
+ * Layer l's compact rows form an FFN layer of d_ff' = max_count neurons (w_gate = out[l][0] and so on) that the
+ * FFN calls run with the identity lists 0 .. max_count-1 and the same counts, in the same slot order as the
+ * original lists (so Eq. 4's h_anchor slots still match). */
+rm_status rm_gather_stack_rows(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, const int32_t *idx,
+                               const int32_t *count, int32_t max_count, void *out, void *stream);
+
 /* Down-projection row norms ||W_down[n]||_2 of one layer (the weight factor of Eq. 1, section 3.4), float32.
  *   w_down: [d_ff][d] in wdtype (the layout of rm_ffn_layer_weights.w_down), 16-byte aligned; d a multiple of 32.
  *   norms:  float32 [d_ff] out.

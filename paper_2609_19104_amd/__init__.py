@@ -43,7 +43,8 @@ RM_KERNEL_GROUP_SELECT = 3
 
 EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_stack",
             "rm_masked_ffn_layer", "rm_masked_ffn_stack", "rm_dense_ffn_ref", "rm_anchor_ffn_stack",
-            "rm_delta_ffn_stack", "rm_neuron_norms", "rm_group_masks", "rm_profile_kernel_events",
+            "rm_delta_ffn_stack", "rm_gather_stack_rows", "rm_neuron_norms", "rm_group_masks",
+            "rm_profile_kernel_events",
             "rm_status_string", "rm_last_error")
 
 # (w_gate, w_up, w_down, norm_g) or (w_gate, w_up, w_down, norm_g, out_gate); norm_g and out_gate may be None.
@@ -95,6 +96,7 @@ def load_library() -> ctypes.CDLL:
         "rm_dense_ffn_ref": [sp, wp, i32, i32, vp, vp, vp, sz, vp],
         "rm_anchor_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
         "rm_delta_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
+        "rm_gather_stack_rows": [sp, wp, i32, vp, vp, i32, vp, vp],
         "rm_neuron_norms": [vp, i32, i32, i32, vp, vp],
         "rm_group_masks": [vp, i32, i32, i32, i32, vp, i32, vp, vp, vp],
         "rm_profile_kernel_events": [i32, vp, vp],
@@ -347,6 +349,26 @@ def rm_dense_ffn_ref(x: torch.Tensor, y: torch.Tensor, layer: Layer, ws: torch.T
     wp, wn = _ws(ws)
     _check(load_library().rm_dense_ffn_ref(ctypes.byref(shape), ctypes.byref(w), B, T, x.data_ptr(), y.data_ptr(),
                                            wp, wn, _stream(stream)))
+
+
+def rm_gather_stack_rows(layers: Sequence[Layer], idx: torch.Tensor, count: torch.Tensor, max_count: int,
+                         out: torch.Tensor, stream=None) -> None:
+    """Compact copies of each layer's listed rows: out [L][3][max_count][d] (w_gate, w_up, w_down rows), rows past
+    a layer's count zero; idx [L][d_ff], count [L] (one list per layer)."""
+    L = len(layers)
+    if L == 0:
+        raise ValueError("at least one layer")
+    shape = _shape(layers[0], 1e-6)
+    arr = (LayerWeights * L)()
+    for l, layer in enumerate(layers):
+        arr[l] = _weights(layer)
+    _need_cuda("idx", idx, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    _need_cuda("out", out, (layers[0][0].dtype,))
+    if idx.numel() != L * shape.d_ff or count.numel() != L or out.numel() != L * 3 * max_count * shape.d:
+        raise ValueError("idx must be [L][d_ff], count [L] and out [L][3][max_count][d]")
+    _check(load_library().rm_gather_stack_rows(ctypes.byref(shape), arr, L, idx.data_ptr(), count.data_ptr(),
+                                               int(max_count), out.data_ptr(), _stream(stream)))
 
 
 def rm_neuron_norms(w_down: torch.Tensor, norms: torch.Tensor, stream=None) -> None:

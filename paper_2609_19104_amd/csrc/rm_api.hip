@@ -150,7 +150,8 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
                      int n_masks = 0) {
     const size_t act_bytes = static_cast<size_t>(p.B) * p.T * p.d * sizeof(float);
     for (int l = 0; l < L; ++l)  // checked before anything is enqueued
-        if (w[l].out_gate && ranges_overlap(w[l].out_gate, static_cast<size_t>(p.B) * p.d * sizeof(float), y, act_bytes))
+        if (w[l].out_gate &&
+            ranges_overlap(w[l].out_gate, static_cast<size_t>(p.B) * p.d * sizeof(float), y, act_bytes))
             return fail(RM_ERR_INVALID_ARG, "layer %d: out_gate overlaps y", l);
     hipError_t e = mask ? rm::launch_compact_prologue(p, mask, n_masks, const_cast<int32_t *>(idx),
                                                       const_cast<int32_t *>(count), x, w[0].norm_g, ws, st)
@@ -478,6 +479,38 @@ RM_EXPORT rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer
     st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
                     static_cast<hipStream_t>(stream), at);
     return st == RM_OK ? ok() : st;
+}
+
+RM_EXPORT rm_status rm_gather_stack_rows(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L,
+                                         const int32_t *idx, const int32_t *count, int32_t max_count, void *out,
+                                         void *stream) {
+    rm_status st = check_shape(s);
+    if (st != RM_OK) return st;
+    if (L <= 0) return fail(RM_ERR_INVALID_ARG, "L=%d must be positive", L);
+    if (!w) return fail(RM_ERR_INVALID_ARG, "weights pointer is NULL");
+    for (int l = 0; l < L; ++l) {
+        st = check_layer(&w[l], l);
+        if (st != RM_OK) return st;
+    }
+    if (!idx || !count || !out) return fail(RM_ERR_INVALID_ARG, "idx, count or out is NULL");
+    if (!aligned(idx, 4) || !aligned(count, 4) || !aligned(out, 16))
+        return fail(RM_ERR_ALIGN, "idx and count must be 4-byte and out 16-byte aligned");
+    if (max_count <= 0 || max_count > s->d_ff)
+        return fail(RM_ERR_SHAPE, "max_count=%d outside [1, d_ff=%d]", max_count, s->d_ff);
+    const size_t eb = s->wdtype == RM_BF16 ? 2 : 4;
+    const size_t out_bytes = static_cast<size_t>(L) * 3 * max_count * s->d * eb;
+    const size_t wbytes = static_cast<size_t>(s->d_ff) * s->d * eb;
+    for (int l = 0; l < L; ++l)
+        if (ranges_overlap(out, out_bytes, w[l].w_gate, wbytes) || ranges_overlap(out, out_bytes, w[l].w_up, wbytes) ||
+            ranges_overlap(out, out_bytes, w[l].w_down, wbytes))
+            return fail(RM_ERR_INVALID_ARG, "out overlaps layer %d's weights", l);
+    if (ranges_overlap(out, out_bytes, idx, static_cast<size_t>(L) * s->d_ff * 4) ||
+        ranges_overlap(out, out_bytes, count, static_cast<size_t>(L) * 4))
+        return fail(RM_ERR_INVALID_ARG, "out overlaps idx or count");
+    const hipError_t e = rm::launch_gather_rows(w, idx, count, s->d_ff, s->d, s->wdtype, max_count, L, out,
+                                                static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "row gather launch");
+    return ok();
 }
 
 RM_EXPORT rm_status rm_neuron_norms(const void *w_down, int32_t d_ff, int32_t d, int32_t wdtype, float *norms,

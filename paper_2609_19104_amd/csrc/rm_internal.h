@@ -75,6 +75,10 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
 hipError_t launch_mask_compact(const uint8_t *mask, int n_masks, int d_ff, int32_t *idx, int32_t *count,
                                hipStream_t st);
 
+// Compact copies of the listed rows of L layers' three matrices: out [L][3][max_count][d] (gather_rows.hip).
+hipError_t launch_gather_rows(const rm_ffn_layer_weights *w, const int32_t *idx, const int32_t *count, int d_ff,
+                              int d, int wdtype, int max_count, int L, void *out, hipStream_t st);
+
 // Group neuron masks (group_mask.hip): the down rows' norms, and Eq. 1 scores + per-step top-K + union + rerank.
 constexpr int kGroupMaxDff = 16384;
 hipError_t launch_neuron_norms(const void *w_down, int d_ff, int d, int wdtype, float *norms, hipStream_t st);

@@ -201,6 +201,44 @@ rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *
 rm_status rm_gather_stack_rows(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, const int32_t *idx,
                                const int32_t *count, int32_t max_count, void *out, void *stream);
 
+/* Context Cache, the rows to recompute (section 4.1, "Visual-Token Recomputation", Eq. 2).  Over a layer's N
+ * token rows, of which rows [v0, v0 + P) are visual tokens:
+ *   drift[p] = RMS(x[v0+p] - x_ref[v0+p]) / max(RMS(x[v0+p]), 1e-6), the Eq. 2 drift of each visual token, with
+ *              x the current FFN input (after RMSNorm) and x_ref the reference execution's, both float32 [N][d];
+ *   rows:      int32 [N] out: in its first count[0] entries, ascending, every non-visual row (instruction and
+ *              robot-state rows are always recomputed) and the k visual rows with the largest drift (ties to the
+ *              lower token); k = ceil(rho_p * P) in the paper;
+ *   count:     int32 [1] out, (N - P) + k.
+ * The drift is float32 in a fixed order (lane j of a wave adds the squares of columns j, j + 64, ...; the lanes'
+ * sums are folded 32, 16, ..., 1 apart; rounded division and correctly rounded square roots), since the row
+ * selection depends on it.  N <= 16384, 0 <= v0, v0 + P <= N, 0 <= k <= P; drift may be NULL when P = 0.
+ * drift, rows and count must not overlap each other, x or x_ref.  Errors: RM_ERR_INVALID_ARG, RM_ERR_SHAPE,
+ * RM_ERR_ALIGN (4-byte alignment). */
+rm_status rm_context_select(const float *x, const float *x_ref, int32_t n_tok, int32_t d, int32_t v0, int32_t P,
+                            int32_t k, float *drift, int32_t *rows, int32_t *count, void *stream);
+
+/* Workspace bytes (written to *bytes, host pointer) of rm_context_ffn for n_tok rows with at most max_rows
+ * recomputed. */
+rm_status rm_context_workspace_size(const rm_ffn_shape *s, int32_t n_tok, int32_t max_rows, size_t *bytes);
+
+/* Context Cache, the update of Eq. 3: the listed rows of y are replaced by F(x) of those rows, every other row
+ * keeps the reference output the caller put there.  F(x) = (act(x W_gate^T) * (x W_up^T)) W_down, the VLM FFN
+ * on its normalized input (no norm inside, no residual).
+ *   s:        d and d_ff multiples of 64, wdtype RM_BF16, act (GeGLU for the Gemma VLM of pi0.5); norm_eps unused.
+ *   w_gate, w_up: bf16 [d_ff][d]; w_down_t: bf16 [d][d_ff], the nn.Linear layout of the down projection (this
+ *             dense FFN reads every neuron, so both of its products take K-contiguous operands).
+ *   x:        float32 [n_tok][d], the FFN input of every row (rounded to bf16 for the matrix cores).
+ *   rows, count: the recomputed rows and their number (rm_context_select's outputs, read on the device);
+ *             count is clamped to [0, max_rows] and rows outside [0, n_tok) to it.
+ *   max_rows: host bound of count, in [1, n_tok]; sizes the launch and the workspace.
+ *   y:        float32 [n_tok][d], in/out: the reference outputs on entry.
+ *   ws, ws_bytes: at least rm_context_workspace_size(s, n_tok, max_rows) bytes, 16-byte aligned.
+ * x, y and the workspace must not overlap.  Errors: RM_ERR_INVALID_ARG, RM_ERR_SHAPE, RM_ERR_DTYPE, RM_ERR_ALIGN,
+ * RM_ERR_WORKSPACE, RM_ERR_HIP. */
+rm_status rm_context_ffn(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
+                         int32_t n_tok, const float *x, const int32_t *rows, const int32_t *count, int32_t max_rows,
+                         float *y, void *ws, size_t ws_bytes, void *stream);
+
 /* Down-projection row norms ||W_down[n]||_2 of one layer (the weight factor of Eq. 1, section 3.4), float32.
  *   w_down: [d_ff][d] in wdtype (the layout of rm_ffn_layer_weights.w_down), 16-byte aligned; d a multiple of 32.
  *   norms:  float32 [d_ff] out.

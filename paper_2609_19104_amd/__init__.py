@@ -43,7 +43,8 @@ RM_KERNEL_GROUP_SELECT = 3
 
 EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_stack",
             "rm_masked_ffn_layer", "rm_masked_ffn_stack", "rm_dense_ffn_ref", "rm_anchor_ffn_stack",
-            "rm_delta_ffn_stack", "rm_gather_stack_rows", "rm_neuron_norms", "rm_group_masks",
+            "rm_delta_ffn_stack", "rm_gather_stack_rows", "rm_context_select", "rm_context_workspace_size",
+            "rm_context_ffn", "rm_neuron_norms", "rm_group_masks",
             "rm_profile_kernel_events",
             "rm_status_string", "rm_last_error")
 
@@ -97,6 +98,9 @@ def load_library() -> ctypes.CDLL:
         "rm_anchor_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
         "rm_delta_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp],
         "rm_gather_stack_rows": [sp, wp, i32, vp, vp, i32, vp, vp],
+        "rm_context_select": [vp, vp, i32, i32, i32, i32, i32, vp, vp, vp, vp],
+        "rm_context_workspace_size": [sp, i32, i32, ctypes.POINTER(sz)],
+        "rm_context_ffn": [sp, vp, vp, vp, i32, vp, vp, vp, i32, vp, vp, sz, vp],
         "rm_neuron_norms": [vp, i32, i32, i32, vp, vp],
         "rm_group_masks": [vp, i32, i32, i32, i32, vp, i32, vp, vp, vp],
         "rm_profile_kernel_events": [i32, vp, vp],
@@ -369,6 +373,62 @@ def rm_gather_stack_rows(layers: Sequence[Layer], idx: torch.Tensor, count: torc
         raise ValueError("idx must be [L][d_ff], count [L] and out [L][3][max_count][d]")
     _check(load_library().rm_gather_stack_rows(ctypes.byref(shape), arr, L, idx.data_ptr(), count.data_ptr(),
                                                int(max_count), out.data_ptr(), _stream(stream)))
+
+
+def rm_context_select(x: torch.Tensor, x_ref: torch.Tensor, v0: int, P: int, k: int, drift: Optional[torch.Tensor],
+                      rows: torch.Tensor, count: torch.Tensor, stream=None) -> None:
+    """Eq. 2 drift of the visual rows [v0, v0 + P) of x [N][d] against x_ref, and the rows to recompute: every
+    non-visual row plus the k visual rows of largest drift (ascending, in rows[:count[0]])."""
+    _need_cuda("x", x, (torch.float32,), 2)
+    _need_cuda("x_ref", x_ref, (torch.float32,), 2)
+    if x.shape != x_ref.shape:
+        raise ValueError("x and x_ref must have the same shape")
+    n_tok, d = x.shape
+    if drift is not None:
+        _need_cuda("drift", drift, (torch.float32,))
+        if drift.numel() < P:
+            raise ValueError("drift must hold P entries")
+    _need_cuda("rows", rows, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    if rows.numel() < n_tok or count.numel() < 1:
+        raise ValueError("rows must hold N entries and count one")
+    _check(load_library().rm_context_select(x.data_ptr(), x_ref.data_ptr(), n_tok, d, int(v0), int(P), int(k),
+                                            _ptr(drift), rows.data_ptr(), count.data_ptr(), _stream(stream)))
+
+
+def context_workspace(d: int, d_ff: int, n_tok: int, max_rows: int, act: str = "gelu_tanh", device="cuda"):
+    """A workspace tensor (uint8) of the size rm_context_workspace_size asks for."""
+    out = ctypes.c_size_t(0)
+    shape = FfnShape(d, d_ff, RM_BF16, 1e-6, ACTS[act])
+    _check(load_library().rm_context_workspace_size(ctypes.byref(shape), n_tok, max_rows, ctypes.byref(out)))
+    return torch.empty(int(out.value), dtype=torch.uint8, device=device)
+
+
+def rm_context_ffn(x: torch.Tensor, y: torch.Tensor, w_gate: torch.Tensor, w_up: torch.Tensor,
+                   w_down_t: torch.Tensor, rows: torch.Tensor, count: torch.Tensor, max_rows: int, ws: torch.Tensor,
+                   act: str = "gelu_tanh", stream=None) -> None:
+    """Eq. 3: y[rows[:count]] = F(x[rows[:count]]); other rows of y (the reference outputs) are left as they are.
+    w_gate, w_up bf16 [d_ff][d]; w_down_t bf16 [d][d_ff] (nn.Linear layout)."""
+    _need_cuda("x", x, (torch.float32,), 2)
+    _need_cuda("y", y, (torch.float32,), 2)
+    if x.shape != y.shape:
+        raise ValueError("x and y must have the same shape")
+    n_tok, d = x.shape
+    _need_cuda("w_gate", w_gate, (torch.bfloat16,), 2)
+    d_ff = w_gate.shape[0]
+    for name, w, shp in (("w_gate", w_gate, (d_ff, d)), ("w_up", w_up, (d_ff, d)), ("w_down_t", w_down_t, (d, d_ff))):
+        _need_cuda(name, w, (torch.bfloat16,), 2)
+        if tuple(w.shape) != shp:
+            raise ValueError(f"{name} has shape {tuple(w.shape)}, expected {shp}")
+    _need_cuda("rows", rows, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    if act not in ACTS:
+        raise ValueError(f"act must be one of {sorted(ACTS)}")
+    shape = FfnShape(d, d_ff, RM_BF16, 1e-6, ACTS[act])
+    wp, wn = _ws(ws)
+    _check(load_library().rm_context_ffn(ctypes.byref(shape), w_gate.data_ptr(), w_up.data_ptr(),
+                                         w_down_t.data_ptr(), n_tok, x.data_ptr(), rows.data_ptr(), count.data_ptr(),
+                                         int(max_rows), y.data_ptr(), wp, wn, _stream(stream)))
 
 
 def rm_neuron_norms(w_down: torch.Tensor, norms: torch.Tensor, stream=None) -> None:

@@ -20,20 +20,15 @@
 // four 8-bit passes, each a histogram (per-wave LDS histograms with integer atomics, so the counts are exact,
 // then added) and a suffix scan that finds the digit of the K-th largest key; then the keys above that
 // threshold plus the lowest-index keys equal to it, found with a workgroup prefix sum.
-#include "rm_internal.h"
+#include "rm_select.h"
 
 namespace {
 
-// a * b rounded to float32 on its own: the empty asm statement hides the product from the optimizer, so it
-// cannot be fused with the sum it feeds into one multiply-add (HIP compiles with contraction allowed).
-__device__ __forceinline__ float mul_rounded(float a, float b) {
-    float p = a * b;
-    asm volatile("" : "+v"(p));
-    return p;
-}
-
-constexpr int kSelThreads = 1024;
-constexpr int kSelPerThread = 16;  // neurons per thread: d_ff <= 16384
+using rm_sel::kSelPerThread;
+using rm_sel::kSelThreads;
+using rm_sel::mul_rounded;
+using rm_sel::select_top_k;
+using rm_sel::SelLds;
 
 // ------------------------------------------------------------------------------------------ norms
 
@@ -80,7 +75,7 @@ __global__ __launch_bounds__(64) void neuron_norms_kernel(const void *__restrict
         for (int j = 0; j < 64; ++j) s = __fadd_rn(s, mul_rounded(tile[lane][j], tile[lane][j]));
         __syncthreads();
     }
-    if (n0 + lane < d_ff) norms[n0 + lane] = __fsqrt_rn(s);
+    if (n0 + lane < d_ff) norms[n0 + lane] = __builtin_sqrtf(s);
 }
 
 // ------------------------------------------------------------------------------------------ scores
@@ -125,103 +120,6 @@ __global__ __launch_bounds__(64) void scores_kernel(const float *__restrict__ h,
 }
 
 // ------------------------------------------------------------------------------------------ selection
-
-struct SelLds {
-    uint32_t whist[kSelThreads / 64][256];  // one histogram per wave: atomics only contend within a wave
-    uint32_t hist[256];
-    int wave_sum[kSelThreads / 64];
-    int digit, need;
-};
-
-// Exclusive prefix sum of v over the workgroup, in thread order.
-__device__ __forceinline__ int block_excl_scan(int v, SelLds &l) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int incl = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int u = __shfl_up(incl, off);
-        if (lane >= off) incl += u;
-    }
-    __syncthreads();  // wave_sum may still be read by a previous call
-    if (lane == 63) l.wave_sum[wave] = incl;
-    __syncthreads();
-    int before = 0;
-    for (int w = 0; w < wave; ++w) before += l.wave_sum[w];
-    return before + incl - v;
-}
-
-// Selection bits (bit i: neuron tid * 16 + i) of the k largest keys among the thread's valid ones (bit i of
-// `valid`), ties to the lower neuron index.  0 <= k; every thread of the workgroup calls it.
-__device__ uint32_t select_top_k(const uint32_t (&key)[kSelPerThread], uint32_t valid, int k, int n_valid,
-                                 SelLds &l) {
-    if (k <= 0) return 0u;
-    if (k >= n_valid) return valid;
-    const int tid = threadIdx.x;
-    uint32_t prefix = 0, hi = 0;
-    int need = k;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        const int wave = tid >> 6;
-        for (int b = tid & 63; b < 256; b += 64) l.whist[wave][b] = 0u;
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < kSelPerThread; ++i)
-            if (((valid >> i) & 1u) && (key[i] & hi) == prefix)
-                atomicAdd(&l.whist[wave][(key[i] >> shift) & 255u], 1u);
-        __syncthreads();
-        if (tid < 256) {
-            uint32_t c = 0;
-#pragma unroll
-            for (int w = 0; w < kSelThreads / 64; ++w) c += l.whist[w][tid];
-            l.hist[tid] = c;
-        }
-        __syncthreads();
-        if (tid < 64) {  // lane j holds digits 4j .. 4j+3; find the digit holding the need-th largest key
-            const int j = tid;
-            const uint32_t b0 = l.hist[4 * j], b1 = l.hist[4 * j + 1], b2 = l.hist[4 * j + 2], b3 = l.hist[4 * j + 3];
-            const int own = static_cast<int>(b0 + b1 + b2 + b3);
-            int above = own;  // inclusive suffix sum over lanes j .. 63, then made exclusive
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int u = __shfl_down(above, off);
-                if (j + off < 64) above += u;
-            }
-            above -= own;  // keys in digits above 4j + 3
-            const uint32_t b[4] = {b0, b1, b2, b3};
-            int cum = above;
-#pragma unroll
-            for (int q = 3; q >= 0; --q) {
-                const int c = static_cast<int>(b[q]);
-                if (cum < need && cum + c >= need) {
-                    l.digit = 4 * j + q;
-                    l.need = need - cum;
-                }
-                cum += c;
-            }
-        }
-        __syncthreads();
-        prefix |= static_cast<uint32_t>(l.digit) << shift;
-        hi |= 255u << shift;
-        need = l.need;
-        __syncthreads();  // l.digit / l.need are rewritten by the next pass
-    }
-    // prefix is the k-th largest key; take every larger key and the `need` lowest-index keys equal to it.
-    uint32_t sel = 0, eq = 0;
-#pragma unroll
-    for (int i = 0; i < kSelPerThread; ++i) {
-        if (!((valid >> i) & 1u)) continue;
-        if (key[i] > prefix) sel |= 1u << i;
-        if (key[i] == prefix) eq |= 1u << i;
-    }
-    int rank = block_excl_scan(__popc(eq), l);
-#pragma unroll
-    for (int i = 0; i < kSelPerThread; ++i) {
-        if ((eq >> i) & 1u) {
-            if (rank < need) sel |= 1u << i;
-            ++rank;
-        }
-    }
-    return sel;
-}
 
 // Each step's K best neurons of one layer (workgroup = step * L + layer) set their mask bytes to 1: the mask
 // holds the union of the steps' candidates when the rerank runs.

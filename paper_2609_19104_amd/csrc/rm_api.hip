@@ -10,7 +10,7 @@
 
 #include <algorithm>
 
-#include "rm_internal.h"
+#include "rm_select.h"
 
 #define RM_EXPORT extern "C" __attribute__((visibility("default")))
 
@@ -510,6 +510,93 @@ RM_EXPORT rm_status rm_gather_stack_rows(const rm_ffn_shape *s, const rm_ffn_lay
     const hipError_t e = rm::launch_gather_rows(w, idx, count, s->d_ff, s->d, s->wdtype, max_count, L, out,
                                                 static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "row gather launch");
+    return ok();
+}
+
+RM_EXPORT rm_status rm_context_select(const float *x, const float *x_ref, int32_t n_tok, int32_t d, int32_t v0,
+                                      int32_t P, int32_t k, float *drift, int32_t *rows, int32_t *count,
+                                      void *stream) {
+    if (!x || !x_ref || !rows || !count) return fail(RM_ERR_INVALID_ARG, "x, x_ref, rows or count is NULL");
+    if (n_tok <= 0 || d <= 0) return fail(RM_ERR_INVALID_ARG, "n_tok=%d and d=%d must be positive", n_tok, d);
+    if (n_tok > rm_sel::kSelThreads * rm_sel::kSelPerThread)
+        return fail(RM_ERR_SHAPE, "n_tok=%d exceeds %d", n_tok, rm_sel::kSelThreads * rm_sel::kSelPerThread);
+    if (v0 < 0 || P < 0 || static_cast<long long>(v0) + P > n_tok)
+        return fail(RM_ERR_SHAPE, "visual rows [%d, %d + %d) outside [0, n_tok=%d)", v0, v0, P, n_tok);
+    if (k < 0 || k > P) return fail(RM_ERR_SHAPE, "k=%d outside [0, P=%d]", k, P);
+    if (P > 0 && !drift) return fail(RM_ERR_INVALID_ARG, "drift is NULL");
+    if (!aligned(x, 4) || !aligned(x_ref, 4) || !aligned(rows, 4) || !aligned(count, 4) ||
+        (drift && !aligned(drift, 4)))
+        return fail(RM_ERR_ALIGN, "pointers must be 4-byte aligned");
+    const size_t xb = static_cast<size_t>(n_tok) * d * 4;
+    const void *outs[3] = {drift, rows, count};
+    const size_t ob[3] = {static_cast<size_t>(P) * 4, static_cast<size_t>(n_tok) * 4, 4};
+    for (int i = 0; i < 3; ++i) {
+        if (!outs[i]) continue;
+        if (ranges_overlap(outs[i], ob[i], x, xb) || ranges_overlap(outs[i], ob[i], x_ref, xb))
+            return fail(RM_ERR_INVALID_ARG, "drift, rows and count must not overlap x or x_ref");
+        for (int j = i + 1; j < 3; ++j)
+            if (outs[j] && ranges_overlap(outs[i], ob[i], outs[j], ob[j]))
+                return fail(RM_ERR_INVALID_ARG, "drift, rows and count must not overlap each other");
+    }
+    const hipError_t e = rm::launch_context_select(x, x_ref, n_tok, d, v0, P, k, drift, rows, count,
+                                                   static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "context selection launch");
+    return ok();
+}
+
+static rm_status context_plan(const rm_ffn_shape *s, int n_tok, int max_rows, rm::ContextPlan *p) {
+    rm_status st = check_shape(s);
+    if (st != RM_OK) return st;
+    if (s->wdtype != RM_BF16) return fail(RM_ERR_DTYPE, "the context FFN takes bf16 weights");
+    if (s->d % 64 != 0 || s->d_ff % 64 != 0)
+        return fail(RM_ERR_SHAPE, "d=%d and d_ff=%d must be multiples of 64", s->d, s->d_ff);
+    if (n_tok <= 0 || max_rows <= 0 || max_rows > n_tok)
+        return fail(RM_ERR_SHAPE, "need 1 <= max_rows=%d <= n_tok=%d", max_rows, n_tok);
+    rm::ContextPlan q;
+    q.d = s->d;
+    q.d_ff = s->d_ff;
+    q.act = s->act;
+    q.n_tok = n_tok;
+    q.max_rows = max_rows;
+    q.m_pad = ceil_div(max_rows, rm::kCtxGluBM) * rm::kCtxGluBM;
+    const long long tiles = static_cast<long long>(q.m_pad / rm::kCtxDownBM) * (s->d_ff / rm::kCtxGluBN);
+    if (tiles > 0x7fffffffLL) return fail(RM_ERR_SHAPE, "launch grid too large");
+    q.off_a = 0;
+    q.off_h = align_up(static_cast<size_t>(q.m_pad) * s->d * 2, 256);
+    q.total = align_up(q.off_h + static_cast<size_t>(q.m_pad) * s->d_ff * 2, 256);
+    *p = q;
+    return RM_OK;
+}
+
+RM_EXPORT rm_status rm_context_workspace_size(const rm_ffn_shape *s, int32_t n_tok, int32_t max_rows, size_t *bytes) {
+    if (!bytes) return fail(RM_ERR_INVALID_ARG, "bytes is NULL");
+    rm::ContextPlan p;
+    const rm_status st = context_plan(s, n_tok, max_rows, &p);
+    if (st != RM_OK) return st;
+    *bytes = p.total;
+    return ok();
+}
+
+RM_EXPORT rm_status rm_context_ffn(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
+                                   int32_t n_tok, const float *x, const int32_t *rows, const int32_t *count,
+                                   int32_t max_rows, float *y, void *ws, size_t ws_bytes, void *stream) {
+    rm::ContextPlan p;
+    rm_status st = context_plan(s, n_tok, max_rows, &p);
+    if (st != RM_OK) return st;
+    if (!w_gate || !w_up || !w_down_t || !x || !rows || !count || !y || !ws)
+        return fail(RM_ERR_INVALID_ARG, "a pointer is NULL");
+    if (!aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(w_down_t, 16) || !aligned(x, 16) ||
+        !aligned(y, 4) || !aligned(rows, 4) || !aligned(count, 4) || !aligned(ws, 16))
+        return fail(RM_ERR_ALIGN, "weights, x and the workspace must be 16-byte aligned, the rest 4-byte");
+    if (ws_bytes < p.total)
+        return fail(RM_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, p.total);
+    const size_t act_bytes = static_cast<size_t>(n_tok) * s->d * 4;
+    if (ranges_overlap(x, act_bytes, y, act_bytes) || ranges_overlap(ws, p.total, x, act_bytes) ||
+        ranges_overlap(ws, p.total, y, act_bytes))
+        return fail(RM_ERR_INVALID_ARG, "x, y and the workspace must not overlap");
+    const hipError_t e = rm::launch_context_ffn(p, w_gate, w_up, w_down_t, x, rows, count, y, ws,
+                                                static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "context FFN launch");
     return ok();
 }
 

@@ -1,0 +1,127 @@
+"""GPU parity of the Context Cache's visual-token recomputation (section 4.1, Eq. 2 and Eq. 3) against the oracle
+(oracle.context_cache) on the same seeded inputs.
+
+Bars: the Eq. 2 drift and the recomputed row list bit-exact (both sides take the top-k decision on the same
+float32 values); the recomputed rows of y within max-abs relative error 2e-2 of the float64 FFN (bf16 weights,
+inputs rounded to bf16, float32 accumulation); every other row of y left bit for bit as the reference output."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import context_cache as cc
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2609_19104_amd as rm  # noqa: E402
+from gpu_helpers import TOL_BF16, dev_f32  # noqa: E402
+
+
+def _bf16(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _select(x, x_ref, v0, P, k):
+    n_tok = x.shape[0]
+    drift = torch.full((max(P, 1),), float("nan"), device="cuda")
+    rows = torch.full((n_tok,), -5, dtype=torch.int32, device="cuda")
+    count = torch.full((1,), -5, dtype=torch.int32, device="cuda")
+    rm.rm_context_select(dev_f32(x), dev_f32(x_ref), v0, P, k, drift if P > 0 else None, rows, count)
+    torch.cuda.synchronize()
+    c = int(count.item())
+    return drift.cpu().numpy()[:P], rows.cpu().numpy()[:c], c
+
+
+SELECT_CASES = [
+    # n_tok, d, v0, P, k, quantum (> 0: rounded differences, so tied drifts)
+    (850, 2048, 0, 768, 308, 0.0),
+    (100, 64, 10, 80, 0, 0.0),
+    (100, 64, 10, 80, 80, 0.0),
+    (33, 96, 0, 33, 5, 0.0),
+    (50, 128, 40, 0, 0, 0.0),
+    (300, 256, 20, 256, 103, 0.5),
+    (16384, 32, 0, 16384, 4000, 0.0),
+]
+
+
+@pytest.mark.parametrize("n_tok,d,v0,P,k,quantum", SELECT_CASES)
+def test_drift_and_row_selection_bit_exact(n_tok, d, v0, P, k, quantum):
+    r = np.random.default_rng(n_tok + d)
+    x_ref = r.standard_normal((n_tok, d)).astype(np.float32)
+    delta = r.standard_normal((n_tok, d)) * np.exp(r.standard_normal((n_tok, 1)))
+    if quantum > 0:
+        delta = np.round(delta / quantum) * quantum
+        delta[::3] = 0.0  # rows without drift: exact zeros, tied
+    x = (x_ref + delta).astype(np.float32)
+    drift, rows, count = _select(x, x_ref, v0, P, k)
+    ref = cc.drift(x[v0:v0 + P], x_ref[v0:v0 + P])
+    assert np.array_equal(drift.view(np.uint32), ref.view(np.uint32))
+    ref_rows = cc.recomputed_rows(ref, n_tok, v0, k)
+    assert count == len(ref_rows) == n_tok - P + k
+    assert np.array_equal(rows, ref_rows)
+
+
+def _run_ffn(w, x, y_ref, rows, count, max_rows, act):
+    xt, yt = dev_f32(x), dev_f32(y_ref)
+    rt = torch.from_numpy(np.concatenate([rows, np.full(w.n_tok - len(rows), -1)]).astype(np.int32)).cuda()
+    ct = torch.tensor([count], dtype=torch.int32, device="cuda")
+    ws = rm.context_workspace(w.d, w.d_ff, w.n_tok, max_rows, act=act)
+    ws.fill_(0x7F)  # the path must not rely on a cleared workspace
+    rm.rm_context_ffn(xt, yt, _bf16(w.layer.w_gate), _bf16(w.layer.w_up), _bf16(w.w_down_t), rt, ct, max_rows, ws,
+                      act=act)
+    torch.cuda.synchronize()
+    return yt.cpu().numpy()
+
+
+def _check_update(w, x, y_ref, y, rows, act, sample=None):
+    keep = np.setdiff1d(np.arange(w.n_tok), rows)
+    assert np.array_equal(y[keep].view(np.uint32), y_ref[keep].view(np.uint32))
+    chk = rows if sample is None else rows[np.linspace(0, len(rows) - 1, sample).astype(int)]
+    if len(chk) == 0:
+        return
+    wg, wu, _, _ = w.layer.f64()
+    wdt = wl.storage_to_f64(w.w_down_t)
+    ref = cc.ffn_out(x[chk], wg, wu, wdt, act)
+    err = np.max(np.abs(y[chk] - ref)) / np.max(np.abs(ref))
+    print(f"recomputed rows: rel err {err:.3e} over {len(chk)} rows")
+    assert err <= TOL_BF16
+
+
+FFN_CASES = [
+    # d, d_ff, n_tok, v0, P, k, max_rows, act
+    (128, 256, 70, 5, 60, 20, 40, "gelu_tanh"),
+    (512, 2048, 300, 0, 256, 100, 160, "silu"),
+    (256, 1024, 200, 0, 200, 199, 200, "gelu_tanh"),
+    (64, 128, 30, 0, 30, 0, 5, "gelu_tanh"),
+]
+
+
+@pytest.mark.parametrize("d,d_ff,n_tok,v0,P,k,max_rows,act", FFN_CASES)
+def test_context_ffn_parity(d, d_ff, n_tok, v0, P, k, max_rows, act):
+    w = wl.context_workload(n_tok=n_tok, v0=v0, P=P, d=d, d_ff=d_ff, seed=7 + d)
+    drift = cc.drift(w.x[v0:v0 + P], w.x_ref[v0:v0 + P])
+    rows = cc.recomputed_rows(drift, n_tok, v0, k)
+    count = min(len(rows), max_rows)  # rows past max_rows are not recomputed
+    y = _run_ffn(w, w.x, w.y_ref, rows, count, max_rows, act)
+    _check_update(w, w.x, w.y_ref, y, rows[:count], act)
+
+
+def test_context_ffn_with_no_rows_leaves_y():
+    w = wl.context_workload(n_tok=40, v0=0, P=40, d=128, d_ff=256, seed=9)
+    y = _run_ffn(w, w.x, w.y_ref, np.zeros(0, np.int32), 0, 8, "gelu_tanh")
+    assert np.array_equal(y.view(np.uint32), w.y_ref.view(np.uint32))
+
+
+def test_context_cache_full_size_end_to_end():
+    # The VLM layer of a pi0.5-style model: 850 rows (768 visual), rho_p = 0.4 -> 308 + 82 rows recomputed,
+    # d = 2048, d_ff = 16384, GeGLU.  Selection on the GPU, checked bit for bit; the FFN checked on 48 sampled
+    # recomputed rows and on every kept row.
+    w = wl.context_workload()
+    drift, rows, count = _select(w.x, w.x_ref, w.v0, w.P, w.k)
+    ref_rows = cc.recomputed_rows(cc.drift(w.x[w.v0:w.v0 + w.P], w.x_ref[w.v0:w.v0 + w.P]), w.n_tok, w.v0, w.k)
+    assert np.array_equal(rows, ref_rows)
+    y = _run_ffn(w, w.x, w.y_ref, ref_rows, count, count, "gelu_tanh")
+    _check_update(w, w.x, w.y_ref, y, ref_rows, "gelu_tanh", sample=48)

@@ -266,6 +266,41 @@ def positive_norms(cfg: int, shape: Sequence[int], *path: int) -> np.ndarray:
     return (0.5 + rng(cfg, _TAG_ACT, 1, *path).random(tuple(shape))).astype(np.float32)
 
 
+@dataclass
+class ContextWorkload:
+    """One VLM FFN layer of the Context Cache (section 4.1, "Visual-Token Recomputation"): n_tok token rows, the
+    visual tokens in rows [v0, v0 + P), the current FFN inputs x and the reference execution's x_ref and y_ref
+    (all float32 [n_tok][d]), bf16 weights with the down projection in nn.Linear's [d][d_ff] layout, and k visual
+    rows to recompute."""
+    d: int
+    d_ff: int
+    n_tok: int
+    v0: int
+    P: int
+    k: int
+    layer: Layer
+    w_down_t: np.ndarray
+    x: np.ndarray
+    x_ref: np.ndarray
+    y_ref: np.ndarray
+
+
+def context_workload(n_tok: int = 850, v0: int = 0, P: int = 768, d: int = 2048, d_ff: int = 16384,
+                     rho_num: int = 2, rho_den: int = 5, seed: int = 6) -> ContextWorkload:
+    """The VLM prefill FFN of a pi0.5-style model (d = 2048, d_ff = 16384; 3 camera views x 256 visual tokens
+    first, then 82 instruction and state rows: 850 rows as in Table 1), rho_p = 0.4 (the paper's default).  x_ref
+    is N(0, 1) (a normalized input); x drifts from it by a per-token scale drawn lognormally, so that a minority
+    of tokens carries most of the change; y_ref is N(0, 0.1^2)."""
+    layer = make_layer(seed, 0, d, d_ff, "bf16")
+    x_ref = make_x(seed, (n_tok, d), 1)
+    r = rng(seed, _TAG_NOISE, 7)
+    scale = 0.05 * np.exp(1.5 * r.standard_normal((n_tok, 1)))
+    x = (x_ref + scale * r.standard_normal((n_tok, d))).astype(np.float32)
+    y_ref = (0.1 * rng(seed, _TAG_X, 2).standard_normal((n_tok, d))).astype(np.float32)
+    k = -(-rho_num * P // rho_den)
+    return ContextWorkload(d, d_ff, n_tok, v0, P, k, layer, np.ascontiguousarray(layer.w_down.T), x, x_ref, y_ref)
+
+
 def group_reference_inputs(w: Workload, anchors: Sequence[int], scale: float = 0.1) -> List[np.ndarray]:
     """For the anchored schedule on a config-3 stack: per group, a similar execution's input (the group's anchor
     input + scale N(0,1)) on which the group's masks are scored (section 4.1 takes them from a reference)."""

@@ -25,10 +25,11 @@ run through a 10-step denoising schedule, one step of the benchmark being the wh
 sequence with Eq. 4's dense anchors at steps 0 and 5 and anchor-delta updates at the other steps (c3-eq4), also
 with the group's rows copied into compact buffers first (c3-eq4-compact); and
 16 independent executions through the stack with per-sample lists (c5); and the construction of one group's
-neuron masks from 5 reference steps of the stack (gm).
+neuron masks from 5 reference steps of the stack (gm); and the Context Cache's token recomputation on one VLM
+FFN layer (cc).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c3-eq4|c3-eq4-compact|c5|gm]
+                       [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c3-eq4|c3-eq4-compact|c5|gm|cc]
 """
 from __future__ import annotations
 
@@ -46,6 +47,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix cores (no sparsity)
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2609_19104_amd", "csrc")
 COLD_BYTES = 1 << 30   # weight copies rotated through per timed run
@@ -96,6 +98,8 @@ WORKLOADS = {
     "c3-eq4-compact": dict(name="the c3-eq4 sequence with the group's selected rows copied into compact buffers "
                                 "(on a side stream, during the anchor step) and the delta steps run on them",
                            cfg=3, percent=30),
+    "cc": dict(name="Context Cache, one VLM FFN layer: 850 rows (768 visual), d=2048 d_ff=16384, GeGLU, bf16, "
+                    "rho_p=0.4 (308 visual + 82 other rows recomputed)", cfg=6, percent=40),
     "gm": dict(name="group neuron masks for the config-3 stack: 5 reference steps x 18 layers, d_ff=4096, T=51, "
                     "K=1229 (top 30%)", cfg=3, percent=30),
     "c5": dict(name="16 independent executions x 18 layers, RMSNorm, d=1024 d_ff=4096 T=51, per-sample top-30% "
@@ -116,6 +120,9 @@ STEP_TEXT = {
                       "(18 layers x 3 matrices) on a side stream beside rm_anchor_ffn_stack (L=18), then 4 "
                       "rm_delta_ffn_stack (L=18) on the compact layers; replayed from HIP graphs; "
                       "us_per_layer = sequence time / 180",
+    "cc": "rm_context_select (Eq. 2 drift of the 768 visual rows, top 308 + the 82 other rows) + rm_context_ffn "
+          "(gathered rows through the gate/up and down GEMMs, scattered into the reference outputs), replayed from "
+          "HIP graphs",
     "gm": "rm_group_masks: Eq. 1 scores of 5 steps x 18 layers from their dense activations (float32 "
           "[5][18][4096][51], written by rm_anchor_ffn_stack with identity lists at set-up), per-step top-K, union "
           "and rerank; replayed from HIP graphs; us_per_layer = step time / 18",
@@ -409,6 +416,54 @@ class StackSetupEq4Compact(StackSetupEq4):
                                       self.ha, self.ws_c)
 
 
+class ContextSetup:
+    """The Context Cache step (section 4.1, Eq. 2 and Eq. 3) on one VLM FFN layer: select the rows to recompute
+    from the drift of the current FFN inputs against the reference's, then recompute them (all weights read;
+    the copies rotate over >= 1 GiB so the reads are cold)."""
+
+    bound = "mfma"
+
+    def __init__(self, key: str, device, cold: bool = True):
+        import torch
+        import workloads as wl
+        import paper_2609_19104_amd as rm
+        w = wl.context_workload()
+        self.key, self.spec, self.rm, self.w = key, WORKLOADS[key], rm, w
+        self.d, self.d_ff, self.T, self.B, self.L, self.k = w.d, w.d_ff, w.n_tok, 1, 1, w.k
+        self.rows_max = w.n_tok - w.P + w.k
+        base = (_bf16_tensor(w.layer.w_gate, device), _bf16_tensor(w.layer.w_up, device),
+                _bf16_tensor(w.w_down_t, device))
+        self.copies = max(2, math.ceil(COLD_BYTES / (3 * matrix_bytes(self.d, self.d_ff, 2)))) if cold else 1
+        self.weights = [base] + [tuple(t.clone() for t in base) for _ in range(self.copies - 1)]
+        self.rotate = self.copies
+        self.x = torch.from_numpy(w.x).to(device)
+        self.x_ref = torch.from_numpy(w.x_ref).to(device)
+        self.y = torch.from_numpy(w.y_ref).to(device)
+        self.drift = torch.empty((w.P,), dtype=torch.float32, device=device)
+        self.rows = torch.empty((w.n_tok,), dtype=torch.int32, device=device)
+        self.count = torch.empty((1,), dtype=torch.int32, device=device)
+        self.ws = rm.context_workspace(self.d, self.d_ff, w.n_tok, self.rows_max, device=device)
+        self.layer_steps = 1
+        self.cold_text = (f"cold: {self.copies} rotating copies of the layer's weights "
+                          f"({self.copies * 3 * matrix_bytes(self.d, self.d_ff, 2) / 2**30:.2f} GiB)")
+
+    def step(self, i: int) -> None:
+        w, (wg, wu, wdt) = self.w, self.weights[i % self.rotate]
+        self.rm.rm_context_select(self.x, self.x_ref, w.v0, w.P, w.k, self.drift, self.rows, self.count)
+        self.rm.rm_context_ffn(self.x, self.y, wg, wu, wdt, self.rows, self.count, self.rows_max, self.ws)
+
+    @property
+    def active_bytes(self) -> int:  # every weight of the layer is read
+        return 3 * matrix_bytes(self.d, self.d_ff, 2)
+
+    def hooks(self):  # matrix-core FLOPs of the two GEMMs over the recomputed rows
+        rm, r = self.rm, self.rows_max
+        return [(rm.RM_KERNEL_GATEUP, "gate/up GEMM over the gathered rows (gemm_nt_kernel, GLU)", "gateup",
+                 2 * projection_flops(r, self.d, self.d_ff)),
+                (rm.RM_KERNEL_DOWN, "down GEMM with the scatter (gemm_nt_kernel, scatter)", "down",
+                 projection_flops(r, self.d, self.d_ff))]
+
+
 class GroupMaskSetup:
     """Group-mask construction (section 5) for one group of the config-3 stack: the dense activations of 5
     reference steps (inputs x_0 .. x_4 of config 3, each run through rm_anchor_ffn_stack with the identity lists,
@@ -644,7 +699,7 @@ def main(argv=None) -> int:
         print(json.dumps({"copy_calibration_bytes": n, "copies": args.steps}))
         return 0
     setup = {"c3": StackSetup3, "c3-eq4": StackSetupEq4, "c3-eq4-compact": StackSetupEq4Compact, "c5": StackSetup5,
-             "gm": GroupMaskSetup}.get(
+             "gm": GroupMaskSetup, "cc": ContextSetup}.get(
         args.workload, Setup)(
         args.workload, dev, cold=True)
 
@@ -658,9 +713,13 @@ def main(argv=None) -> int:
     ms = time_graph(setup, args.steps, args.warmup)
     # The dominant kernel: the hooked kernel with the longest average launch duration (kernel start to end).
     hooks = setup.hooks()
-    dom_id, dom, dom_key, dom_bytes = max(hooks, key=lambda h: kern[h[0]]["mean"])
+    dom_id, dom, dom_key, dom_bytes = max(hooks, key=lambda h: kern[h[0]]["mean"])[:4]
     dom_us = kern[dom_id]["mean"]
-    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
+    bound = getattr(setup, "bound", "hbm")
+    if bound == "mfma":  # the dominant kernel's amount is FLOPs: matrix-core roofline
+        achieved, peak, unit = dom_bytes / (dom_us * 1e-6) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        achieved, peak, unit = dom_bytes / (dom_us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s"
     value = setup.active_bytes / (ms * 1e-3) / 1e9
 
     setup.rotate = 1
@@ -694,10 +753,11 @@ def main(argv=None) -> int:
         "warm_us_per_layer": round(warm_ms * 1e3 / setup.layer_steps, 3),
         "kernel_us": {f"{key}{suffix}": round(kern[kid][stat], 3) for kid, _, key, _ in hooks
                       for suffix, stat in (("", "mean"), ("_median", "median"), ("_min", "min"))},
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "roofline": {"bound": bound, "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
+                     "unit": unit, "frac": round(achieved / peak, 4),
                      "traffic": counted_traffic(args.workload, dom_key),
-                     "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_us, 3),
+                     ("flops_per_launch" if bound == "mfma" else "bytes_per_launch"): dom_bytes,
+                     "avg_launch_us": round(dom_us, 3),
                      "traffic_unit": "bytes per launch (HBM, from rocprofv3 counters)"},
     }
     if isinstance(setup, StackSetup5):

@@ -13,6 +13,9 @@
 //   gemm_nt_kernel<GLU>:   H = act(A W_gate^T) * (A W_up^T), bf16 [rows][d_ff].
 //   gemm_nt_kernel<SCAT>:  y[row_i] = H_i W_down^T (W_down as nn.Linear's [d][d_ff]): Eq. 3's recomputed rows
 //                          written into the caller's buffer, which holds the reference outputs everywhere else.
+//                          With K = d_ff long and few output tiles, the down product is split over K instead
+//                          (<PART>: float32 partials per K slice) and reduce_scatter_kernel adds the slices in
+//                          order into the listed rows of y (no atomics).
 //
 // The two projections are dense contractions with enough reuse for the matrix cores (about 400 rows against
 // 2048 x 16384 weights: 390 FLOP per weight byte, above the bf16 ridge of MI355X), so both run on
@@ -134,7 +137,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const float *__restric
 
 // ------------------------------------------------------------------------------------------ GEMM
 
-enum { kEpiGlu = 0, kEpiScatter = 1 };
+enum { kEpiGlu = 0, kEpiScatter = 1, kEpiPartial = 2 };
 
 struct GemmArgs {
     const uint16_t *A;       // bf16 [m_pad][K]
@@ -146,6 +149,8 @@ struct GemmArgs {
     float *y;                // kEpiScatter: float32 [n_tok][N], row rows[i] receives output row i
     const int32_t *rows;
     int n_tok;
+    int splits;              // K slices (workgroups per output tile); kEpiPartial: slice s writes part[s]
+    float *part;             // kEpiPartial: float32 [splits][m_pad][N]
 };
 
 constexpr int kKt = 64;          // K per LDS stage (two matrix-core steps)
@@ -161,9 +166,12 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t Bs[2][NB * BN * kPitch];
 
     const int mt = a.m_pad / BM;
-    const int q = xcd_order(blockIdx.x, gridDim.x);  // = n tile * mt + m tile: one weight tile per XCD run
+    const int q = xcd_order(blockIdx.x, gridDim.x);  // = (n tile * splits + K slice) * mt + m tile
     const int m0 = (q % mt) * BM;
-    const int n0 = (q / mt) * BN;
+    const int ks_id = (q / mt) % a.splits;
+    const int n0 = (q / mt / a.splits) * BN;
+    const int k_len = a.K / a.splits;  // a multiple of kKt
+    const int k_base = ks_id * k_len;
     const int cnt = min(max(a.count[0], 0), a.max_rows);
     if (m0 >= cnt) return;  // the whole tile is past the rows in use
 
@@ -178,7 +186,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
 #pragma unroll
         for (int p = 0; p < A_PIECES; ++p) {
             const int e = tid + p * 256;
-            ra[p] = *reinterpret_cast<const rm_u32x4 *>(a.A + static_cast<size_t>(m0 + (e >> 3)) * a.K + k0 +
+            ra[p] = *reinterpret_cast<const rm_u32x4 *>(a.A + static_cast<size_t>(m0 + (e >> 3)) * a.K + k_base + k0 +
                                                        (e & 7) * 8);
         }
 #pragma unroll
@@ -187,7 +195,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
             const int nb = e / (BN * 8);
             const int rem = e - nb * BN * 8;
             const uint16_t *B = nb ? a.B1 : a.B0;
-            rb[p] = *reinterpret_cast<const rm_u32x4 *>(B + static_cast<size_t>(n0 + (rem >> 3)) * a.K + k0 +
+            rb[p] = *reinterpret_cast<const rm_u32x4 *>(B + static_cast<size_t>(n0 + (rem >> 3)) * a.K + k_base + k0 +
                                                        (rem & 7) * 8);
         }
     };
@@ -212,7 +220,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) acc[nb][tm][tn] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nk = a.K / kKt;
+    const int nk = k_len / kKt;
     load_stage(0);
     store_stage(0);
     __syncthreads();
@@ -257,6 +265,8 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
                 if constexpr (EPI == kEpiGlu) {
                     const float h = rm_glu_act(a.act, acc[0][tm][tn][i]) * acc[NB - 1][tm][tn][i];
                     a.H[static_cast<size_t>(m) * a.N + n] = static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
+                } else if constexpr (EPI == kEpiPartial) {
+                    a.part[(static_cast<size_t>(ks_id) * a.m_pad + m) * a.N + n] = acc[0][tm][tn][i];
                 } else {
                     const int row = min(max(a.rows[m], 0), a.n_tok - 1);
                     a.y[static_cast<size_t>(row) * a.N + n] = acc[0][tm][tn][i];
@@ -264,6 +274,26 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
             }
         }
     }
+}
+
+// y[rows[i]] = the K slices' partials of output row i, added in slice order (one thread per 4 columns).
+__global__ __launch_bounds__(256) void reduce_scatter_kernel(const float *__restrict__ part, int splits, int m_pad,
+                                                             int N, const int32_t *__restrict__ rows,
+                                                             const int32_t *__restrict__ count, int max_rows,
+                                                             int n_tok, float *__restrict__ y) {
+    const int cnt = min(max(count[0], 0), max_rows);
+    const int per_row = N / 4;
+    const long long e = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x;
+    const int i = static_cast<int>(e / per_row);
+    if (i >= cnt) return;
+    const int c = static_cast<int>(e - static_cast<long long>(i) * per_row) * 4;
+    float4 s = *reinterpret_cast<const float4 *>(part + static_cast<size_t>(i) * N + c);
+    for (int k = 1; k < splits; ++k) {
+        const float4 v = *reinterpret_cast<const float4 *>(part + (static_cast<size_t>(k) * m_pad + i) * N + c);
+        s = make_float4(s.x + v.x, s.y + v.y, s.z + v.z, s.w + v.w);
+    }
+    const int row = min(max(rows[i], 0), n_tok - 1);
+    *reinterpret_cast<float4 *>(y + static_cast<size_t>(row) * N + c) = s;
 }
 
 }  // namespace
@@ -304,6 +334,7 @@ hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const vo
     g.max_rows = p.max_rows;
     g.act = p.act;
     g.H = H;
+    g.splits = 1;
     launch_timed(RM_KERNEL_GATEUP, gemm_nt_kernel<kCtxGluBM, kCtxGluBN, 2, kEpiGlu>,
                  dim3((p.m_pad / kCtxGluBM) * (p.d_ff / kCtxGluBN)), dim3(256), st, g);
     e = hipGetLastError();
@@ -321,8 +352,21 @@ hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const vo
     o.y = y;
     o.rows = rows;
     o.n_tok = p.n_tok;
-    launch_timed(RM_KERNEL_DOWN, gemm_nt_kernel<kCtxDownBM, kCtxDownBN, 1, kEpiScatter>,
-                 dim3((p.m_pad / kCtxDownBM) * (p.d / kCtxDownBN)), dim3(256), st, o);
+    o.splits = p.down_splits;
+    const dim3 grid((p.m_pad / kCtxDownBM) * (p.d / kCtxDownBN) * p.down_splits);
+    if (p.down_splits == 1) {
+        launch_timed(RM_KERNEL_DOWN, gemm_nt_kernel<kCtxDownBM, kCtxDownBN, 1, kEpiScatter>, grid, dim3(256), st, o);
+        return hipGetLastError();
+    }
+    // Split over K: the slices' float32 partials, then their ordered sum scattered into y.
+    o.part = reinterpret_cast<float *>(base + p.off_part);
+    launch_timed(RM_KERNEL_DOWN, gemm_nt_kernel<kCtxDownBM, kCtxDownBN, 1, kEpiPartial>, grid, dim3(256), st, o);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const long long n4 = static_cast<long long>(p.max_rows) * (p.d / 4);
+    hipLaunchKernelGGL(reduce_scatter_kernel, dim3(static_cast<unsigned>((n4 + 255) / 256)), dim3(256), 0, st,
+                       static_cast<const float *>(o.part), p.down_splits, p.m_pad, p.d, rows, count, p.max_rows,
+                       p.n_tok, y);
     return hipGetLastError();
 }
 

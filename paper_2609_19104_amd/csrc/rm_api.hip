@@ -561,9 +561,18 @@ static rm_status context_plan(const rm_ffn_shape *s, int n_tok, int max_rows, rm
     q.m_pad = ceil_div(max_rows, rm::kCtxGluBM) * rm::kCtxGluBM;
     const long long tiles = static_cast<long long>(q.m_pad / rm::kCtxDownBM) * (s->d_ff / rm::kCtxGluBN);
     if (tiles > 0x7fffffffLL) return fail(RM_ERR_SHAPE, "launch grid too large");
+    // The down GEMM splits K until it has about 1024 workgroups (four per compute unit), keeping slices of at
+    // least 1024 along K.
+    const int out_tiles = ceil_div(max_rows, rm::kCtxDownBM) * (s->d / rm::kCtxDownBN);
+    q.down_splits = 1;
+    while (q.down_splits < 16 && out_tiles * q.down_splits < 1024 && s->d_ff % (2 * q.down_splits * 64) == 0 &&
+           s->d_ff / (2 * q.down_splits) >= 1024)
+        q.down_splits *= 2;
     q.off_a = 0;
     q.off_h = align_up(static_cast<size_t>(q.m_pad) * s->d * 2, 256);
-    q.total = align_up(q.off_h + static_cast<size_t>(q.m_pad) * s->d_ff * 2, 256);
+    q.off_part = align_up(q.off_h + static_cast<size_t>(q.m_pad) * s->d_ff * 2, 256);
+    const size_t part = q.down_splits > 1 ? static_cast<size_t>(q.down_splits) * q.m_pad * s->d * 4 : 0;
+    q.total = align_up(q.off_part + part, 256);
     *p = q;
     return RM_OK;
 }

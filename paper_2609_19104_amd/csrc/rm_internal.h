@@ -80,12 +80,14 @@ hipError_t launch_gather_rows(const rm_ffn_layer_weights *w, const int32_t *idx,
                               int d, int wdtype, int max_count, int L, void *out, hipStream_t st);
 
 // Context Cache (context_cache.hip): tile sizes of its two matrix-core GEMMs, and the workspace plan (the
-// gathered rows as bf16 [m_pad][d], then H bf16 [m_pad][d_ff]; m_pad = max_rows rounded up to the gate/up tile).
+// gathered rows as bf16 [m_pad][d], then H bf16 [m_pad][d_ff], then the down GEMM's K-slice partials; m_pad =
+// max_rows rounded up to the gate/up tile).
 constexpr int kCtxGluBM = 128, kCtxGluBN = 64;   // gate/up: 128 rows x 64 neurons (x 2 matrices)
 constexpr int kCtxDownBM = 64, kCtxDownBN = 64;  // down: 64 rows x 64 columns
 struct ContextPlan {
     int d = 0, d_ff = 0, act = 0, n_tok = 0, max_rows = 0, m_pad = 0;
-    size_t off_a = 0, off_h = 0, total = 0;
+    int down_splits = 1;  // K slices of the down GEMM (float32 partials [splits][m_pad][d] when > 1)
+    size_t off_a = 0, off_h = 0, off_part = 0, total = 0;
 };
 hipError_t launch_context_select(const float *x, const float *x_ref, int n_tok, int d, int v0, int P, int k,
                                  float *drift, int32_t *rows, int32_t *count, hipStream_t st);

@@ -55,11 +55,22 @@ __global__ __launch_bounds__(64) void drift_kernel(const float *__restrict__ x, 
     const float *xa = x + static_cast<size_t>(v0 + p) * d;
     const float *xb = xr + static_cast<size_t>(v0 + p) * d;
     float sd = 0.0f, sx = 0.0f;
-    for (int c = lane; c < d; c += 64) {
-        const float a = xa[c];
-        const float diff = __fsub_rn(a, xb[c]);
-        sd = __fadd_rn(sd, mul_rounded(diff, diff));
-        sx = __fadd_rn(sx, mul_rounded(a, a));
+    // Eight columns of each input in flight per lane before the in-order sums (columns past d are not added).
+    for (int c0 = lane; c0 < d; c0 += 8 * 64) {
+        float va[8], vb[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int c = min(c0 + u * 64, d - 1);
+            va[u] = xa[c];
+            vb[u] = xb[c];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (c0 + u * 64 >= d) break;
+            const float diff = __fsub_rn(va[u], vb[u]);
+            sd = __fadd_rn(sd, mul_rounded(diff, diff));
+            sx = __fadd_rn(sx, mul_rounded(va[u], va[u]));
+        }
     }
     for (int off = 32; off >= 1; off >>= 1) {
         sd = __fadd_rn(sd, __shfl_xor(sd, off));

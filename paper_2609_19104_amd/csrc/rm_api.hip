@@ -99,6 +99,16 @@ rm_status hip_fail(hipError_t e, const char *what) {
     return fail(RM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// The layers' output gates must not overlap y (they are read while y is written); checked by every FFN entry
+// point before it enqueues anything.
+rm_status check_gates(const rm_ffn_layer_weights *w, int L, int B, int T, int d, const float *y) {
+    const size_t act_bytes = static_cast<size_t>(B) * T * d * sizeof(float);
+    for (int l = 0; l < L; ++l)
+        if (w[l].out_gate && ranges_overlap(w[l].out_gate, static_cast<size_t>(B) * d * sizeof(float), y, act_bytes))
+            return fail(RM_ERR_INVALID_ARG, "layer %d: out_gate overlaps y", l);
+    return RM_OK;
+}
+
 // Checks shared by the anchor and delta stacks: L, weights, the anchor buffers' sizes and overlaps.
 rm_status check_anchor_buffers(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int L, int B, int T,
                                const float *x, float *y, int max_count, const void *y_anchor, const void *h_anchor,
@@ -109,6 +119,8 @@ rm_status check_anchor_buffers(const rm_ffn_shape *s, const rm_ffn_layer_weights
         const rm_status st = check_layer(&w[l], l);
         if (st != RM_OK) return st;
     }
+    const rm_status sg = check_gates(w, L, B, T, s->d, y);
+    if (sg != RM_OK) return sg;
     if (!y_anchor) return fail(RM_ERR_INVALID_ARG, "y_anchor is NULL");
     if (!h_anchor && max_count > 0) return fail(RM_ERR_INVALID_ARG, "h_anchor is NULL with max_count=%d", max_count);
     if (!aligned(y_anchor, 16) || !aligned(h_anchor, 4))
@@ -148,11 +160,6 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
                      const int32_t *idx, const int32_t *count, size_t list_stride, size_t count_stride, void *ws,
                      hipStream_t st, const AnchorTerms &at = AnchorTerms{}, const uint8_t *mask = nullptr,
                      int n_masks = 0) {
-    const size_t act_bytes = static_cast<size_t>(p.B) * p.T * p.d * sizeof(float);
-    for (int l = 0; l < L; ++l)  // checked before anything is enqueued
-        if (w[l].out_gate &&
-            ranges_overlap(w[l].out_gate, static_cast<size_t>(p.B) * p.d * sizeof(float), y, act_bytes))
-            return fail(RM_ERR_INVALID_ARG, "layer %d: out_gate overlaps y", l);
     hipError_t e = mask ? rm::launch_compact_prologue(p, mask, n_masks, const_cast<int32_t *>(idx),
                                                       const_cast<int32_t *>(count), x, w[0].norm_g, ws, st)
                         : rm::launch_prologue(p, x, w[0].norm_g, ws, st);
@@ -337,6 +344,8 @@ RM_EXPORT rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_laye
     if (st != RM_OK) return st;
     st = check_layer(w, 0);
     if (st != RM_OK) return st;
+    st = check_gates(w, 1, B, T, s->d, y);
+    if (st != RM_OK) return st;
     st = run_layers(p, w, 1, x, y, idx, count, 0, 0, ws, static_cast<hipStream_t>(stream));
     return st == RM_OK ? ok() : st;
 }
@@ -354,6 +363,8 @@ RM_EXPORT rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
         st = check_layer(&w[l], l);
         if (st != RM_OK) return st;
     }
+    st = check_gates(w, L, B, T, s->d, y);
+    if (st != RM_OK) return st;
     st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
                     static_cast<hipStream_t>(stream));
     return st == RM_OK ? ok() : st;
@@ -391,6 +402,8 @@ RM_EXPORT rm_status rm_masked_ffn_layer(const rm_ffn_shape *s, const rm_ffn_laye
     if (st != RM_OK) return st;
     st = check_masks(s, B, B, T, mask, idx, count, x, y, ws, ws_bytes);
     if (st != RM_OK) return st;
+    st = check_gates(w, 1, B, T, s->d, y);
+    if (st != RM_OK) return st;
     st = run_layers(p, w, 1, x, y, idx, count, 0, 0, ws, static_cast<hipStream_t>(stream), AnchorTerms{}, mask, B);
     return st == RM_OK ? ok() : st;
 }
@@ -410,6 +423,8 @@ RM_EXPORT rm_status rm_masked_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
     if (static_cast<long long>(L) * B > 0x7fffffffLL) return fail(RM_ERR_SHAPE, "L x B is too large");
     st = check_masks(s, L * B, B, T, mask, idx, count, x, y, ws, ws_bytes);
     if (st != RM_OK) return st;
+    st = check_gates(w, L, B, T, s->d, y);
+    if (st != RM_OK) return st;
     st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
                     static_cast<hipStream_t>(stream), AnchorTerms{}, mask, L * B);
     return st == RM_OK ? ok() : st;
@@ -421,6 +436,8 @@ RM_EXPORT rm_status rm_dense_ffn_ref(const rm_ffn_shape *s, const rm_ffn_layer_w
     rm_status st = check_call(s, B, T, x, y, nullptr, nullptr, false, 0, ws, ws_bytes, &p);
     if (st != RM_OK) return st;
     st = check_layer(w, 0);
+    if (st != RM_OK) return st;
+    st = check_gates(w, 1, B, T, s->d, y);
     if (st != RM_OK) return st;
     const hipStream_t hs = static_cast<hipStream_t>(stream);
     const hipError_t e = rm::launch_identity_lists(p, ws, hs);

@@ -147,3 +147,111 @@ def test_binding_refuses_cpu_tensors():
     with pytest.raises((ValueError, RuntimeError)):
         rm.rm_dense_ffn_ref(x, x, (torch.zeros(8, 32), torch.zeros(8, 32), torch.zeros(8, 32), None),
                             torch.zeros(16, dtype=torch.uint8))
+
+
+def test_profile_hook_accepts_every_kernel_id(lib):
+    for k in (rm.RM_KERNEL_GATEUP, rm.RM_KERNEL_DOWN, rm.RM_KERNEL_SCORES, rm.RM_KERNEL_GROUP_SELECT):
+        assert lib.rm_profile_kernel_events(k, None, None) == rm.RM_OK
+    assert lib.rm_profile_kernel_events(4, None, None) == rm.RM_ERR_INVALID_ARG
+    assert lib.rm_profile_kernel_events(-1, None, None) == rm.RM_ERR_INVALID_ARG
+
+
+def test_activation_and_gate_are_validated(lib):
+    s = rm.FfnShape(1024, 4096, 1, 1e-6, 7)  # unknown activation
+    lw = rm.LayerWeights(FAKE, FAKE, FAKE, None, None)
+    st = lib.rm_sparse_ffn_layer(ctypes.byref(s), ctypes.byref(lw), 1, 51, FAKE, FAKE, FAKE, FAKE, 100, FAKE * 16,
+                                 1 << 30, None)
+    assert st == rm.RM_ERR_INVALID_ARG and "act" in rm.last_error()
+    s = rm.FfnShape(1024, 4096, 1, 1e-6, rm.RM_ACT_GELU_TANH)
+    lw = rm.LayerWeights(FAKE, FAKE, FAKE, None, FAKE + 4)  # misaligned gate
+    st = lib.rm_sparse_ffn_layer(ctypes.byref(s), ctypes.byref(lw), 1, 51, FAKE, FAKE, FAKE, FAKE, 100, FAKE * 16,
+                                 1 << 30, None)
+    assert st == rm.RM_ERR_ALIGN
+    lw = rm.LayerWeights(FAKE, FAKE, FAKE, None, FAKE)  # gate overlapping y (x == y == FAKE)
+    st = lib.rm_sparse_ffn_layer(ctypes.byref(s), ctypes.byref(lw), 1, 51, FAKE, FAKE, FAKE * 2, FAKE * 3, 100,
+                                 FAKE * 16, 1 << 30, None)
+    assert st == rm.RM_ERR_INVALID_ARG and "out_gate" in rm.last_error()
+
+
+def test_masked_calls_reject(lib):
+    s = rm.FfnShape(1024, 4096, 1, 1e-6)
+    lw = rm.LayerWeights(FAKE, FAKE, FAKE, None)
+    base = dict(B=1, T=51, x=FAKE, y=FAKE, mask=FAKE * 64, idx=FAKE * 128, cnt=FAKE * 256, k=100)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return lib.rm_masked_ffn_layer(ctypes.byref(s), ctypes.byref(lw), a["B"], a["T"], a["x"], a["y"], a["mask"],
+                                       a["idx"], a["cnt"], a["k"], FAKE * 1024, 1 << 30, None)
+    assert call(mask=None) == rm.RM_ERR_INVALID_ARG
+    assert call(idx=FAKE * 64 + 8) == rm.RM_ERR_INVALID_ARG   # idx overlaps the mask
+    assert call(cnt=FAKE * 128 + 4) == rm.RM_ERR_INVALID_ARG  # count overlaps idx
+    arr = (rm.LayerWeights * 2)(lw, lw)
+    assert lib.rm_masked_ffn_stack(ctypes.byref(s), arr, 0, 1, 51, FAKE, FAKE, FAKE * 64, FAKE * 128, FAKE * 256, 100,
+                                   FAKE * 1024, 1 << 30, None) == rm.RM_ERR_INVALID_ARG
+
+
+def test_anchor_and_delta_reject(lib):
+    s = rm.FfnShape(1024, 4096, 1, 1e-6)
+    arr = (rm.LayerWeights * 2)(rm.LayerWeights(FAKE, FAKE, FAKE, None), rm.LayerWeights(FAKE, FAKE, FAKE, None))
+    args = (FAKE, FAKE, FAKE * 64, FAKE * 128, 100)
+
+    def anchor(ya, ha, ws_bytes=1 << 30, k=100):
+        return lib.rm_anchor_ffn_stack(ctypes.byref(s), arr, 2, 1, 51, *args[:4], k, ya, ha, FAKE * 4096, ws_bytes,
+                                       None)
+    assert anchor(None, FAKE * 512) == rm.RM_ERR_INVALID_ARG
+    assert anchor(FAKE * 512 + 4, FAKE * 1024) == rm.RM_ERR_ALIGN
+    assert anchor(FAKE * 512, None) == rm.RM_ERR_INVALID_ARG            # h_anchor needed when max_count > 0
+    assert anchor(FAKE * 512, FAKE * 512 + 64) == rm.RM_ERR_INVALID_ARG  # y_anchor and h_anchor overlap
+    ws_sparse = _size(1024, 4096, rm.RM_BF16, 1, 51, 100)[1]
+    assert anchor(FAKE * 512, FAKE * 1024, ws_bytes=ws_sparse) == rm.RM_ERR_WORKSPACE  # anchors need the dense size
+    st = lib.rm_delta_ffn_stack(ctypes.byref(s), arr, 2, 1, 51, *args[:4], 100, None, FAKE * 1024, FAKE * 4096,
+                                1 << 30, None)
+    assert st == rm.RM_ERR_INVALID_ARG
+
+
+def test_gather_norms_and_group_masks_reject(lib):
+    s = rm.FfnShape(1024, 4096, 1, 1e-6)
+    arr = (rm.LayerWeights * 1)(rm.LayerWeights(FAKE, FAKE, FAKE, None))
+    assert lib.rm_gather_stack_rows(ctypes.byref(s), arr, 1, FAKE * 64, FAKE * 128, 0, FAKE * 256,
+                                    None) == rm.RM_ERR_SHAPE
+    assert lib.rm_gather_stack_rows(ctypes.byref(s), arr, 1, FAKE * 64, FAKE * 128, 100, FAKE,
+                                    None) == rm.RM_ERR_INVALID_ARG  # out overlaps the weights
+    assert lib.rm_neuron_norms(FAKE, 4096, 1000, rm.RM_BF16, FAKE * 64, None) == rm.RM_ERR_SHAPE
+    assert lib.rm_neuron_norms(FAKE, 4096, 1024, 3, FAKE * 64, None) == rm.RM_ERR_DTYPE
+    assert lib.rm_neuron_norms(FAKE, 4096, 1024, rm.RM_BF16, FAKE, None) == rm.RM_ERR_INVALID_ARG  # overlap
+    gm = lib.rm_group_masks
+    assert gm(FAKE, 5, 18, 20000, 51, FAKE * 64, 100, FAKE * 128, FAKE * 256, None) == rm.RM_ERR_SHAPE
+    assert gm(FAKE, 5, 18, 4096, 51, FAKE * 64, 4097, FAKE * 128, FAKE * 256, None) == rm.RM_ERR_SHAPE
+    assert gm(FAKE, 300, 300, 4096, 51, FAKE * 64, 100, FAKE * 128, FAKE * 256, None) == rm.RM_ERR_SHAPE
+    assert gm(FAKE, 5, 18, 4096, 51, FAKE * 64, 100, FAKE * 128, FAKE * 128 + 4, None) == rm.RM_ERR_INVALID_ARG
+    assert gm(None, 5, 18, 4096, 51, FAKE * 64, 100, FAKE * 128, FAKE * 256, None) == rm.RM_ERR_INVALID_ARG
+
+
+def _ctx_size(d, d_ff, n_tok, max_rows, wdtype=rm.RM_BF16):
+    out = ctypes.c_size_t(0)
+    s = rm.FfnShape(d, d_ff, wdtype, 1e-6, rm.RM_ACT_GELU_TANH)
+    return rm.load_library().rm_context_workspace_size(ctypes.byref(s), n_tok, max_rows, ctypes.byref(out)), out.value
+
+
+def test_context_calls_validate(lib):
+    st, n = _ctx_size(2048, 16384, 850, 390)
+    assert st == rm.RM_OK and n >= 512 * 2048 * 2 + 512 * 16384 * 2 and n % 256 == 0
+    assert _ctx_size(2048, 16384, 850, 391)[1] >= n
+    assert _ctx_size(2048, 16384, 850, 900)[0] == rm.RM_ERR_SHAPE     # max_rows > n_tok
+    assert _ctx_size(2048, 16384, 850, 390, rm.RM_F32)[0] == rm.RM_ERR_DTYPE
+    assert _ctx_size(2080, 16384, 850, 390)[0] == rm.RM_ERR_SHAPE     # d not a multiple of 64
+    sel = lib.rm_context_select
+    assert sel(FAKE, FAKE * 64, 850, 2048, 0, 768, 769, FAKE * 128, FAKE * 256, FAKE * 512, None) == rm.RM_ERR_SHAPE
+    assert sel(FAKE, FAKE * 64, 850, 2048, 100, 768, 10, FAKE * 128, FAKE * 256, FAKE * 512, None) == rm.RM_ERR_SHAPE
+    assert sel(FAKE, FAKE * 64, 20000, 32, 0, 10, 1, FAKE * 128, FAKE * 256, FAKE * 512, None) == rm.RM_ERR_SHAPE
+    assert sel(FAKE, FAKE * 64, 850, 2048, 0, 768, 10, None, FAKE * 256, FAKE * 512, None) == rm.RM_ERR_INVALID_ARG
+    assert sel(FAKE, FAKE * 64, 850, 2048, 0, 768, 10, FAKE * 128, FAKE * 128 + 64, FAKE * 512,
+               None) == rm.RM_ERR_INVALID_ARG  # rows overlap drift
+    s = rm.FfnShape(2048, 16384, rm.RM_BF16, 1e-6, rm.RM_ACT_GELU_TANH)
+    ffn = lib.rm_context_ffn
+    assert ffn(ctypes.byref(s), FAKE, FAKE, FAKE, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 512,
+               FAKE * 4096, 100, None) == rm.RM_ERR_WORKSPACE
+    assert ffn(ctypes.byref(s), FAKE, FAKE, FAKE, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 64,
+               FAKE * 4096, 1 << 30, None) == rm.RM_ERR_INVALID_ARG  # y is x
+    assert ffn(ctypes.byref(s), None, FAKE, FAKE, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 512,
+               FAKE * 4096, 1 << 30, None) == rm.RM_ERR_INVALID_ARG

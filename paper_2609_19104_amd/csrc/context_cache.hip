@@ -10,8 +10,8 @@
 //   select_rows_kernel:    one 1024-thread workgroup: the k visual rows with the largest drift (radix select, ties
 //                          to the lower token) plus every non-visual row, as an ascending row list and its count.
 //   gather_rows_kernel:    the listed rows of x as bf16 into the workspace, zero rows up to the padded count.
-//   gemm_nt_kernel<GLU>:   H = act(A W_gate^T) * (A W_up^T), bf16 [rows][d_ff].
-//   gemm_nt_kernel<SCAT>:  y[row_i] = H_i W_down^T (W_down as nn.Linear's [d][d_ff]): Eq. 3's recomputed rows
+//   gemm_dma_kernel<GLU>:  H = act(A W_gate^T) * (A W_up^T), bf16 [rows][d_ff].
+//   gemm_dma_kernel<SCAT>: y[row_i] = H_i W_down^T (W_down as nn.Linear's [d][d_ff]): Eq. 3's recomputed rows
 //                          written into the caller's buffer, which holds the reference outputs everywhere else.
 //                          With K = d_ff long and few output tiles, the down product is split over K instead
 //                          (<PART>: float32 partials per K slice) and reduce_scatter_kernel adds the slices in
@@ -19,10 +19,11 @@
 //
 // The two projections are dense contractions with enough reuse for the matrix cores (about 400 rows against
 // 2048 x 16384 weights: 390 FLOP per weight byte, above the bf16 ridge of MI355X), so both run on
-// v_mfma_f32_16x16x32_bf16 with both operands contiguous along K: a workgroup of 4 waves owns a BM x BN tile,
-// stages 64-wide K slices of A and B through double-buffered LDS (16-byte loads, padded rows), and each wave
-// accumulates a (BM/2) x (BN/2) quarter (for the gate/up product, one accumulator set per matrix).  Workgroups
-// that share a weight tile are numbered onto one XCD so that its L2 serves the re-reads.
+// v_mfma_f32_16x16x32_bf16 with both operands contiguous along K.  On this shape the limit is how fast a compute
+// unit pulls tiles out of L2, not the matrix cores, so the tiles are as large as one workgroup per compute unit
+// allows: 256 rows by 128 columns of each weight matrix (2 MB read per gate/up workgroup over K = 2048), 8 waves
+// each accumulating 64 x 64 per matrix, K staged 64 wide (one cache line per row) straight from memory into LDS.
+// Workgroups that share a weight tile are numbered onto one XCD so that its L2 serves the re-reads.
 #include "rm_select.h"
 
 namespace {
@@ -164,24 +165,69 @@ struct GemmArgs {
     float *part;             // kEpiPartial: float32 [splits][m_pad][N]
 };
 
-constexpr int kKt = 64;          // K per LDS stage (two matrix-core steps)
-constexpr int kPitch = kKt + 8;  // bf16 per LDS row: 16 bytes of padding against bank conflicts
+// ------------------------------------------------------------------------------------------ DMA-staged GEMM
 
-template <int BM, int BN, int NB, int EPI>
-__global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
-    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
-    constexpr int A_PIECES = BM * kKt / 8 / 256;       // 16-byte pieces per thread and stage
-    constexpr int B_PIECES = NB * BN * kKt / 8 / 256;
-    static_assert(A_PIECES >= 1 && B_PIECES >= 1, "tile too small for 256 threads");
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * kPitch];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][NB * BN * kPitch];
+// The tiles are moved by the load unit straight into LDS (global_load_lds_dwordx4), with no register staging:
+// STAGES buffers, all but one in flight.  A stage is KT wide along K (KT = 32: one matrix-core step, 64 bytes per
+// row; KT = 64: two steps, 128 bytes = one cache line per row); a load instruction fills 1 KB of consecutive rows,
+// lane l writing bytes [16 l, 16 l + 16).  The 16-byte pieces of a row are permuted (piece c of row r sits at
+// position c ^ swz(r)) so that the fragment reads of 16 rows at one piece hit distinct LDS banks, with 32 banks
+// and 8 lanes per cycle as well as with 64 banks and 16 lanes (the counters show no conflicts).
+template <int KT>
+__device__ __forceinline__ int dma_swz(int r) {
+    if constexpr (KT == 32)
+        return ((r >> 1) ^ (r >> 2)) & 3;
+    else
+        return (r ^ (r >> 3)) & 7;
+}
+
+// One load of 16 bytes per lane into LDS at lds + 16 lane (M0 holds the wave's LDS base).  Issued as inline
+// assembly so that the compiler, which cannot tell the stage buffers apart, adds no wait of its own for it before
+// the LDS reads: the waits are the explicit ones below.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// Wait until at most N of this wave's vector-memory operations are in flight and all its LDS operations are
+// done, then the workgroup barrier.  The compiler may not move memory accesses across it.
+template <int N>
+__device__ __forceinline__ void dma_wait_barrier() {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t *p) {
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t *)p));
+}
+
+// Waves per SIMD that the stage buffers allow (160 KB of LDS per compute unit), at most 2: the register budget
+// follows from it.
+constexpr int dma_waves_per_simd(int lds_bytes, int waves) {
+    return (163840 / lds_bytes) * waves / 4 >= 2 ? 2 : 1;
+}
+
+template <int TM, int TN, int NB, int KT, int STAGES, int WAVES_M, int EPI>
+__global__ __launch_bounds__(128 * WAVES_M,
+                             dma_waves_per_simd(STAGES * (16 * WAVES_M * TM + NB * 32 * TN) * KT * 2, 2 * WAVES_M))
+void gemm_dma_kernel(GemmArgs a) {
+    constexpr int WAVES = 2 * WAVES_M;             // WAVES_M x 2 waves, each (16 TM) x (16 TN) per matrix
+    constexpr int BM = 16 * WAVES_M * TM, BN = 32 * TN;
+    constexpr int ROWS = BM + NB * BN;             // a stage: BM rows of A, then BN rows of each B matrix
+    constexpr int RB = KT * 2;                     // bytes per row and stage
+    constexpr int RPB = 1024 / RB;                 // rows per 1 KB load block
+    constexpr int PIECES = RB / 16;
+    static_assert(KT == 32 || KT == 64, "stage width");
+    static_assert(ROWS % (WAVES * RPB) == 0, "load blocks must split evenly over the waves");
+    constexpr int BPW = ROWS / RPB / WAVES;        // load blocks per wave and stage
+    static_assert(STAGES >= 2 && BPW * (STAGES - 2) <= 63, "vmcnt range");
+    constexpr int STAGE = ROWS * RB;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[STAGES][STAGE];
 
     const int mt = a.m_pad / BM;
     const int q = xcd_order(blockIdx.x, gridDim.x);  // = (n tile * splits + K slice) * mt + m tile
     const int m0 = (q % mt) * BM;
     const int ks_id = (q / mt) % a.splits;
     const int n0 = (q / mt / a.splits) * BN;
-    const int k_len = a.K / a.splits;  // a multiple of kKt
+    const int k_len = a.K / a.splits;  // a multiple of KT
     const int k_base = ks_id * k_len;
     const int cnt = min(max(a.count[0], 0), a.max_rows);
     if (m0 >= cnt) return;  // the whole tile is past the rows in use
@@ -189,38 +235,33 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % WAVES_M, wn = wave / WAVES_M;
     const int r = lane & 15, grp = lane >> 4;
 
-    rm_u32x4 ra[A_PIECES], rb[B_PIECES];
-    auto load_stage = [&](int k0) {
+    // Source of this lane's 16 bytes in each of the wave's load blocks (block wave + WAVES j), at K offset 0.
+    const uint8_t *src[BPW];
 #pragma unroll
-        for (int p = 0; p < A_PIECES; ++p) {
-            const int e = tid + p * 256;
-            ra[p] = *reinterpret_cast<const rm_u32x4 *>(a.A + static_cast<size_t>(m0 + (e >> 3)) * a.K + k_base + k0 +
-                                                       (e & 7) * 8);
+    for (int j = 0; j < BPW; ++j) {
+        const int row = (wave + WAVES * j) * RPB + lane / PIECES;
+        const int piece = (lane % PIECES) ^ dma_swz<KT>(row & 15);
+        const uint16_t *base;
+        if (row < BM) {
+            base = a.A + static_cast<size_t>(m0 + row) * a.K;
+        } else {
+            const int rb = row - BM;
+            const int nb = rb / BN;
+            base = (nb ? a.B1 : a.B0) + static_cast<size_t>(n0 + rb - nb * BN) * a.K;
         }
+        src[j] = reinterpret_cast<const uint8_t *>(base + k_base + piece * 8);
+    }
+    const uint32_t lds0 = lds_addr(&lds[0][0]);
+    const int nk = k_len / KT;
+    auto issue = [&](int kt) {
+        const size_t koff = static_cast<size_t>(kt) * RB;
+        const uint32_t buf = lds0 + (kt % STAGES) * STAGE;
 #pragma unroll
-        for (int p = 0; p < B_PIECES; ++p) {
-            const int e = tid + p * 256;
-            const int nb = e / (BN * 8);
-            const int rem = e - nb * BN * 8;
-            const uint16_t *B = nb ? a.B1 : a.B0;
-            rb[p] = *reinterpret_cast<const rm_u32x4 *>(B + static_cast<size_t>(n0 + (rem >> 3)) * a.K + k_base + k0 +
-                                                       (rem & 7) * 8);
-        }
-    };
-    auto store_stage = [&](int buf) {
-#pragma unroll
-        for (int p = 0; p < A_PIECES; ++p) {
-            const int e = tid + p * 256;
-            *reinterpret_cast<rm_u32x4 *>(&As[buf][(e >> 3) * kPitch + (e & 7) * 8]) = ra[p];
-        }
-#pragma unroll
-        for (int p = 0; p < B_PIECES; ++p) {
-            const int e = tid + p * 256;
-            *reinterpret_cast<rm_u32x4 *>(&Bs[buf][(e >> 3) * kPitch + (e & 7) * 8]) = rb[p];
-        }
+        for (int j = 0; j < BPW; ++j)
+            dma16(src[j] + koff, __builtin_amdgcn_readfirstlane(buf + (wave + WAVES * j) * 1024));
     };
 
     rm_f32x4 acc[NB][TM][TN];
@@ -231,36 +272,55 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) acc[nb][tm][tn] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nk = k_len / kKt;
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) load_stage((kt + 1) * kKt);  // in flight while this stage's products run
+    // Fragment reads: row r of a 16-row tile, piece 4 ks + grp (K elements 32 ks + 8 grp ..) at its permuted place.
+    auto compute = [&](const uint8_t *buf) {
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
+        for (int ks = 0; ks < KT / 32; ++ks) {
+            const int frag = r * RB + (((ks * 4 + grp) ^ dma_swz<KT>(r)) << 4);
             rm_u32x4 af[TM], bf[NB][TN];
 #pragma unroll
             for (int tm = 0; tm < TM; ++tm)
-                af[tm] = *reinterpret_cast<const rm_u32x4 *>(
-                    &As[buf][(wm * WM + tm * 16 + r) * kPitch + ks * 32 + grp * 8]);
+                af[tm] = *reinterpret_cast<const rm_u32x4 *>(buf + (wm * TM * 16 + tm * 16) * RB + frag);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
                 for (int tn = 0; tn < TN; ++tn)
                     bf[nb][tn] = *reinterpret_cast<const rm_u32x4 *>(
-                        &Bs[buf][(nb * BN + wn * WN + tn * 16 + r) * kPitch + ks * 32 + grp * 8]);
+                        buf + (BM + nb * BN + wn * TN * 16 + tn * 16) * RB + frag);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
                 for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-                    for (int tn = 0; tn < TN; ++tn) acc[nb][tm][tn] = mfma16(af[tm], bf[nb][tn], acc[nb][tm][tn]);
+                    for (int tn = 0; tn < TN; ++tn)
+                        acc[nb][tm][tn] = mfma16(af[tm], bf[nb][tn], acc[nb][tm][tn]);
         }
-        if (more) store_stage(buf ^ 1);  // buf ^ 1 was last read before the previous barrier
-        __syncthreads();
+    };
+    // Stage kt: wait for its loads (later stages' may stay in flight), barrier (every wave is also done with the
+    // buffer read at stage kt - 1), refill that buffer with stage kt + STAGES - 1, compute stage kt.
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < nk) issue(s);
+    for (int kt = 0; kt < nk; ++kt) {
+        const int later = min(nk - 1 - kt, STAGES - 2);  // stages issued after kt, still allowed in flight
+        if constexpr (STAGES >= 4) {
+            if (later >= 2) {
+                dma_wait_barrier<BPW * (STAGES >= 4 ? STAGES - 2 : 0)>();
+            } else if (later == 1) {
+                dma_wait_barrier<BPW>();
+            } else {
+                dma_wait_barrier<0>();
+            }
+        } else if constexpr (STAGES == 3) {
+            if (later == 1)
+                dma_wait_barrier<BPW>();
+            else
+                dma_wait_barrier<0>();
+        } else {
+            dma_wait_barrier<0>();
+        }
+        if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+        compute(&lds[kt % STAGES][0]);
     }
 
     // Lane (grp, r), register i of a tile: row 4 grp + i, column r.
@@ -268,11 +328,11 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
     for (int tm = 0; tm < TM; ++tm) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int m = m0 + wm * WM + tm * 16 + grp * 4 + i;
+            const int m = m0 + wm * TM * 16 + tm * 16 + grp * 4 + i;
             if (m >= cnt) continue;
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) {
-                const int n = n0 + wn * WN + tn * 16 + r;
+                const int n = n0 + wn * TN * 16 + tn * 16 + r;
                 if constexpr (EPI == kEpiGlu) {
                     const float h = rm_glu_act(a.act, acc[0][tm][tn][i]) * acc[NB - 1][tm][tn][i];
                     a.H[static_cast<size_t>(m) * a.N + n] = static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
@@ -346,9 +406,11 @@ hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const vo
     g.act = p.act;
     g.H = H;
     g.splits = 1;
-    launch_timed(RM_KERNEL_GATEUP, gemm_nt_kernel<kCtxGluBM, kCtxGluBN, 2, kEpiGlu>,
-                 dim3((p.m_pad / kCtxGluBM) * (p.d_ff / kCtxGluBN)), dim3(256), st, g);
-    e = hipGetLastError();
+    constexpr int kWavesM = kCtxBM / 64;
+    static_assert(kCtxGluBN == 128, "gate/up tiles of 4 x 16 neurons per wave");
+    e = launch_timed(RM_KERNEL_GATEUP, gemm_dma_kernel<4, 4, 2, 64, RM_CTX_GLU_STAGES, kWavesM, kEpiGlu>,
+                     dim3((p.m_pad / kCtxBM) * (p.d_ff / kCtxGluBN)), dim3(128 * kWavesM), st, g);
+    if (e == hipSuccess) e = hipGetLastError();
     if (e != hipSuccess) return e;
 
     GemmArgs o{};
@@ -364,15 +426,20 @@ hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const vo
     o.rows = rows;
     o.n_tok = p.n_tok;
     o.splits = p.down_splits;
-    const dim3 grid((p.m_pad / kCtxDownBM) * (p.d / kCtxDownBN) * p.down_splits);
+    o.part = reinterpret_cast<float *>(base + p.off_part);  // used when split
+    const dim3 grid((p.m_pad / kCtxBM) * (p.d / p.down_bn) * p.down_splits), block(128 * kWavesM);
+    constexpr int S = RM_CTX_DOWN_STAGES;
     if (p.down_splits == 1) {
-        launch_timed(RM_KERNEL_DOWN, gemm_nt_kernel<kCtxDownBM, kCtxDownBN, 1, kEpiScatter>, grid, dim3(256), st, o);
-        return hipGetLastError();
+        e = p.down_bn == 128
+                ? launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 4, 1, 64, S, kWavesM, kEpiScatter>, grid, block, st, o)
+                : launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 2, 1, 64, S, kWavesM, kEpiScatter>, grid, block, st, o);
+        return e != hipSuccess ? e : hipGetLastError();
     }
     // Split over K: the slices' float32 partials, then their ordered sum scattered into y.
-    o.part = reinterpret_cast<float *>(base + p.off_part);
-    launch_timed(RM_KERNEL_DOWN, gemm_nt_kernel<kCtxDownBM, kCtxDownBN, 1, kEpiPartial>, grid, dim3(256), st, o);
-    e = hipGetLastError();
+    e = p.down_bn == 128
+            ? launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 4, 1, 64, S, kWavesM, kEpiPartial>, grid, block, st, o)
+            : launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 2, 1, 64, S, kWavesM, kEpiPartial>, grid, block, st, o);
+    if (e == hipSuccess) e = hipGetLastError();
     if (e != hipSuccess) return e;
     const long long n4 = static_cast<long long>(p.max_rows) * (p.d / 4);
     hipLaunchKernelGGL(reduce_scatter_kernel, dim3(static_cast<unsigned>((n4 + 255) / 256)), dim3(256), 0, st,

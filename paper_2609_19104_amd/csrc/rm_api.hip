@@ -565,8 +565,8 @@ static rm_status context_plan(const rm_ffn_shape *s, int n_tok, int max_rows, rm
     rm_status st = check_shape(s);
     if (st != RM_OK) return st;
     if (s->wdtype != RM_BF16) return fail(RM_ERR_DTYPE, "the context FFN takes bf16 weights");
-    if (s->d % 64 != 0 || s->d_ff % 64 != 0)
-        return fail(RM_ERR_SHAPE, "d=%d and d_ff=%d must be multiples of 64", s->d, s->d_ff);
+    if (s->d % 64 != 0 || s->d_ff % rm::kCtxGluBN != 0)
+        return fail(RM_ERR_SHAPE, "d=%d must be a multiple of 64 and d_ff=%d of %d", s->d, s->d_ff, rm::kCtxGluBN);
     if (n_tok <= 0 || max_rows <= 0 || max_rows > n_tok)
         return fail(RM_ERR_SHAPE, "need 1 <= max_rows=%d <= n_tok=%d", max_rows, n_tok);
     rm::ContextPlan q;
@@ -575,15 +575,16 @@ static rm_status context_plan(const rm_ffn_shape *s, int n_tok, int max_rows, rm
     q.act = s->act;
     q.n_tok = n_tok;
     q.max_rows = max_rows;
-    q.m_pad = ceil_div(max_rows, rm::kCtxGluBM) * rm::kCtxGluBM;
-    const long long tiles = static_cast<long long>(q.m_pad / rm::kCtxDownBM) * (s->d_ff / rm::kCtxGluBN);
+    q.m_pad = ceil_div(max_rows, rm::kCtxBM) * rm::kCtxBM;
+    q.down_bn = rm::ctx_down_bn(s->d);
+    const long long tiles = static_cast<long long>(q.m_pad / rm::kCtxBM) * (s->d_ff / rm::kCtxGluBN);
     if (tiles > 0x7fffffffLL) return fail(RM_ERR_SHAPE, "launch grid too large");
-    // The down GEMM splits K until it has about 1024 workgroups (four per compute unit), keeping slices of at
-    // least 1024 along K.
-    const int out_tiles = ceil_div(max_rows, rm::kCtxDownBM) * (s->d / rm::kCtxDownBN);
+    // The down GEMM splits K until it has about one workgroup per compute unit, keeping slices of at least 1024
+    // along K (a multiple of the 64-wide K stage).
+    const int out_tiles = (q.m_pad / rm::kCtxBM) * (s->d / q.down_bn);
     q.down_splits = 1;
-    while (q.down_splits < 16 && out_tiles * q.down_splits < 1024 && s->d_ff % (2 * q.down_splits * 64) == 0 &&
-           s->d_ff / (2 * q.down_splits) >= 1024)
+    while (q.down_splits < 16 && out_tiles * q.down_splits < rm::kCtxDownTarget &&
+           s->d_ff % (2 * q.down_splits * 64) == 0 && s->d_ff / (2 * q.down_splits) >= 1024)
         q.down_splits *= 2;
     q.off_a = 0;
     q.off_h = align_up(static_cast<size_t>(q.m_pad) * s->d * 2, 256);

@@ -82,10 +82,27 @@ hipError_t launch_gather_rows(const rm_ffn_layer_weights *w, const int32_t *idx,
 // Context Cache (context_cache.hip): tile sizes of its two matrix-core GEMMs, and the workspace plan (the
 // gathered rows as bf16 [m_pad][d], then H bf16 [m_pad][d_ff], then the down GEMM's K-slice partials; m_pad =
 // max_rows rounded up to the gate/up tile).
-constexpr int kCtxGluBM = 128, kCtxGluBN = 64;   // gate/up: 128 rows x 64 neurons (x 2 matrices)
-constexpr int kCtxDownBM = 64, kCtxDownBN = 64;  // down: 64 rows x 64 columns
+// The tile sizes can be set at build time (RM_CTX_GLU_BM and so on) for tuning sweeps.
+// Context Cache GEMM tiles (context_cache.hip): 256 rows by 8 waves (4 along the rows x 2 along the columns),
+// each wave 64 rows x 64 columns per weight matrix; the gate/up tile spans 128 neurons of both matrices, the down
+// tile 128 output columns (64 when d is not a multiple of 128).  The stage counts can be set at build time
+// (RM_CTX_GLU_STAGES, RM_CTX_DOWN_STAGES, RM_CTX_DOWN_TARGET) for tuning sweeps.
+#ifndef RM_CTX_GLU_STAGES
+#define RM_CTX_GLU_STAGES 2
+#endif
+#ifndef RM_CTX_DOWN_STAGES
+#define RM_CTX_DOWN_STAGES 3
+#endif
+#ifndef RM_CTX_DOWN_TARGET
+#define RM_CTX_DOWN_TARGET 256
+#endif
+constexpr int kCtxBM = 256;                         // rows per tile; the padded row count is a multiple
+constexpr int kCtxGluBN = 128;                      // gate/up: neurons per tile
+constexpr int kCtxDownTarget = RM_CTX_DOWN_TARGET;  // down: workgroups the K split aims for
+inline int ctx_down_bn(int d) { return d % 128 == 0 ? 128 : 64; }
 struct ContextPlan {
     int d = 0, d_ff = 0, act = 0, n_tok = 0, max_rows = 0, m_pad = 0;
+    int down_bn = 128;    // output columns per down tile
     int down_splits = 1;  // K slices of the down GEMM (float32 partials [splits][m_pad][d] when > 1)
     size_t off_a = 0, off_h = 0, off_part = 0, total = 0;
 };

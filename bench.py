@@ -120,9 +120,9 @@ STEP_TEXT = {
                       "(18 layers x 3 matrices) on a side stream beside rm_anchor_ffn_stack (L=18), then 4 "
                       "rm_delta_ffn_stack (L=18) on the compact layers; replayed from HIP graphs; "
                       "us_per_layer = sequence time / 180",
-    "cc": "rm_context_select (Eq. 2 drift of the 768 visual rows, top 308 + the 82 other rows) + rm_context_ffn "
-          "(gathered rows through the gate/up and down GEMMs, scattered into the reference outputs), replayed from "
-          "HIP graphs",
+    "cc": "rm_context_select (Eq. 2 drift of the 768 visual rows, top 308 + the 82 other rows) + "
+          "rm_context_ffn_packed (gathered rows through the gate/up and down GEMMs on the weights packed once by "
+          "rm_context_pack, scattered into the reference outputs), replayed from HIP graphs",
     "gm": "rm_group_masks: Eq. 1 scores of 5 steps x 18 layers from their dense activations (float32 "
           "[5][18][4096][51], written by rm_anchor_ffn_stack with identity lists at set-up), per-step top-K, union "
           "and rerank; replayed from HIP graphs; us_per_layer = step time / 18",
@@ -434,7 +434,12 @@ class ContextSetup:
         base = (_bf16_tensor(w.layer.w_gate, device), _bf16_tensor(w.layer.w_up, device),
                 _bf16_tensor(w.w_down_t, device))
         self.copies = max(2, math.ceil(COLD_BYTES / (3 * matrix_bytes(self.d, self.d_ff, 2)))) if cold else 1
-        self.weights = [base] + [tuple(t.clone() for t in base) for _ in range(self.copies - 1)]
+        # The weights packed once, as at model load (rm_context_pack: a layout change only); each copy is packed
+        # from its own clone so that no two copies share memory.
+        self.weights = [rm.rm_context_pack(*base)]
+        for _ in range(self.copies - 1):
+            self.weights.append(rm.rm_context_pack(*(t.clone() for t in base)))
+        del base
         self.rotate = self.copies
         self.x = torch.from_numpy(w.x).to(device)
         self.x_ref = torch.from_numpy(w.x_ref).to(device)
@@ -448,9 +453,9 @@ class ContextSetup:
                           f"({self.copies * 3 * matrix_bytes(self.d, self.d_ff, 2) / 2**30:.2f} GiB)")
 
     def step(self, i: int) -> None:
-        w, (wg, wu, wdt) = self.w, self.weights[i % self.rotate]
+        w, packed = self.w, self.weights[i % self.rotate]
         self.rm.rm_context_select(self.x, self.x_ref, w.v0, w.P, w.k, self.drift, self.rows, self.count)
-        self.rm.rm_context_ffn(self.x, self.y, wg, wu, wdt, self.rows, self.count, self.rows_max, self.ws)
+        self.rm.rm_context_ffn_packed(self.x, self.y, packed, self.rows, self.count, self.rows_max, self.ws)
 
     @property
     def active_bytes(self) -> int:  # every weight of the layer is read

@@ -224,7 +224,8 @@ rm_status rm_context_workspace_size(const rm_ffn_shape *s, int32_t n_tok, int32_
 /* Context Cache, the update of Eq. 3: the listed rows of y are replaced by F(x) of those rows, every other row
  * keeps the reference output the caller put there.  F(x) = (act(x W_gate^T) * (x W_up^T)) W_down, the VLM FFN
  * on its normalized input (no norm inside, no residual).
- *   s:        d and d_ff multiples of 64, wdtype RM_BF16, act (GeGLU for the Gemma VLM of pi0.5); norm_eps unused.
+ *   s:        d a multiple of 64 and d_ff of 128, wdtype RM_BF16, act (GeGLU for the Gemma VLM of pi0.5); norm_eps
+ *             unused.
  *   w_gate, w_up: bf16 [d_ff][d]; w_down_t: bf16 [d][d_ff], the nn.Linear layout of the down projection (this
  *             dense FFN reads every neuron, so both of its products take K-contiguous operands).
  *   x:        float32 [n_tok][d], the FFN input of every row (rounded to bf16 for the matrix cores).
@@ -238,6 +239,26 @@ rm_status rm_context_workspace_size(const rm_ffn_shape *s, int32_t n_tok, int32_
 rm_status rm_context_ffn(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
                          int32_t n_tok, const float *x, const int32_t *rows, const int32_t *count, int32_t max_rows,
                          float *y, void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes (written to *bytes, host pointer) of a layer's weights packed by rm_context_pack: 3 * d * d_ff * 2. */
+rm_status rm_context_pack_size(const rm_ffn_shape *s, size_t *bytes);
+
+/* The three matrices of one layer (the arguments of rm_context_ffn) copied into the blocked layout that
+ * rm_context_ffn_packed reads: each matrix as 64-row x 64-column bf16 blocks of 8 KB, the blocks of a 64-row tile
+ * consecutive along K, the 16-byte pieces of each block row permuted; w_gate, then w_up, then w_down_t.  Every
+ * K stage of a weight tile is then one contiguous read.  A layout change only (no arithmetic); run it once when
+ * the weights are loaded.
+ *   packed, packed_bytes: device buffer of at least rm_context_pack_size bytes, 16-byte aligned, owned by the
+ *             caller; it must not overlap the weights.
+ * Errors: as rm_context_ffn for the shape and pointers; RM_ERR_WORKSPACE if packed_bytes is too small. */
+rm_status rm_context_pack(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
+                          void *packed, size_t packed_bytes, void *stream);
+
+/* rm_context_ffn with the weights from rm_context_pack (same result bit for bit: only the weights' layout
+ * differs).  packed must not overlap y or the workspace. */
+rm_status rm_context_ffn_packed(const rm_ffn_shape *s, const void *packed, int32_t n_tok, const float *x,
+                                const int32_t *rows, const int32_t *count, int32_t max_rows, float *y, void *ws,
+                                size_t ws_bytes, void *stream);
 
 /* Down-projection row norms ||W_down[n]||_2 of one layer (the weight factor of Eq. 1, section 3.4), float32.
  *   w_down: [d_ff][d] in wdtype (the layout of rm_ffn_layer_weights.w_down), 16-byte aligned; d a multiple of 32.

@@ -44,7 +44,8 @@ RM_KERNEL_GROUP_SELECT = 3
 EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_stack",
             "rm_masked_ffn_layer", "rm_masked_ffn_stack", "rm_dense_ffn_ref", "rm_anchor_ffn_stack",
             "rm_delta_ffn_stack", "rm_gather_stack_rows", "rm_context_select", "rm_context_workspace_size",
-            "rm_context_ffn", "rm_neuron_norms", "rm_group_masks",
+            "rm_context_ffn", "rm_context_pack_size", "rm_context_pack", "rm_context_ffn_packed", "rm_neuron_norms",
+            "rm_group_masks",
             "rm_profile_kernel_events",
             "rm_status_string", "rm_last_error")
 
@@ -101,6 +102,9 @@ def load_library() -> ctypes.CDLL:
         "rm_context_select": [vp, vp, i32, i32, i32, i32, i32, vp, vp, vp, vp],
         "rm_context_workspace_size": [sp, i32, i32, ctypes.POINTER(sz)],
         "rm_context_ffn": [sp, vp, vp, vp, i32, vp, vp, vp, i32, vp, vp, sz, vp],
+        "rm_context_pack_size": [sp, ctypes.POINTER(sz)],
+        "rm_context_pack": [sp, vp, vp, vp, vp, sz, vp],
+        "rm_context_ffn_packed": [sp, vp, i32, vp, vp, vp, i32, vp, vp, sz, vp],
         "rm_neuron_norms": [vp, i32, i32, i32, vp, vp],
         "rm_group_masks": [vp, i32, i32, i32, i32, vp, i32, vp, vp, vp],
         "rm_profile_kernel_events": [i32, vp, vp],
@@ -429,6 +433,52 @@ def rm_context_ffn(x: torch.Tensor, y: torch.Tensor, w_gate: torch.Tensor, w_up:
     _check(load_library().rm_context_ffn(ctypes.byref(shape), w_gate.data_ptr(), w_up.data_ptr(),
                                          w_down_t.data_ptr(), n_tok, x.data_ptr(), rows.data_ptr(), count.data_ptr(),
                                          int(max_rows), y.data_ptr(), wp, wn, _stream(stream)))
+
+
+def rm_context_pack(w_gate: torch.Tensor, w_up: torch.Tensor, w_down_t: torch.Tensor, act: str = "gelu_tanh",
+                    stream=None) -> torch.Tensor:
+    """The layer's three matrices in the blocked layout rm_context_ffn_packed reads (a uint8 tensor of
+    3 * d * d_ff * 2 bytes, allocated here).  Run once per layer when the weights are loaded."""
+    _need_cuda("w_gate", w_gate, (torch.bfloat16,), 2)
+    d_ff, d = w_gate.shape
+    for name, w, shp in (("w_up", w_up, (d_ff, d)), ("w_down_t", w_down_t, (d, d_ff))):
+        _need_cuda(name, w, (torch.bfloat16,), 2)
+        if tuple(w.shape) != shp:
+            raise ValueError(f"{name} has shape {tuple(w.shape)}, expected {shp}")
+    if act not in ACTS:
+        raise ValueError(f"act must be one of {sorted(ACTS)}")
+    shape = FfnShape(d, d_ff, RM_BF16, 1e-6, ACTS[act])
+    n = ctypes.c_size_t(0)
+    lib = load_library()
+    _check(lib.rm_context_pack_size(ctypes.byref(shape), ctypes.byref(n)))
+    packed = torch.empty(int(n.value), dtype=torch.uint8, device=w_gate.device)
+    _check(lib.rm_context_pack(ctypes.byref(shape), w_gate.data_ptr(), w_up.data_ptr(), w_down_t.data_ptr(),
+                               packed.data_ptr(), packed.numel(), _stream(stream)))
+    return packed
+
+
+def rm_context_ffn_packed(x: torch.Tensor, y: torch.Tensor, packed: torch.Tensor, rows: torch.Tensor,
+                          count: torch.Tensor, max_rows: int, ws: torch.Tensor, act: str = "gelu_tanh",
+                          stream=None) -> None:
+    """rm_context_ffn with the weights from rm_context_pack (d_ff follows from the packed size)."""
+    _need_cuda("x", x, (torch.float32,), 2)
+    _need_cuda("y", y, (torch.float32,), 2)
+    if x.shape != y.shape:
+        raise ValueError("x and y must have the same shape")
+    n_tok, d = x.shape
+    _need_cuda("packed", packed, (torch.uint8,))
+    if packed.numel() % (6 * d) != 0:
+        raise ValueError("packed does not hold the three matrices of a layer with this d")
+    d_ff = packed.numel() // (6 * d)
+    _need_cuda("rows", rows, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    if act not in ACTS:
+        raise ValueError(f"act must be one of {sorted(ACTS)}")
+    shape = FfnShape(d, d_ff, RM_BF16, 1e-6, ACTS[act])
+    wp, wn = _ws(ws)
+    _check(load_library().rm_context_ffn_packed(ctypes.byref(shape), packed.data_ptr(), n_tok, x.data_ptr(),
+                                                rows.data_ptr(), count.data_ptr(), int(max_rows), y.data_ptr(), wp,
+                                                wn, _stream(stream)))
 
 
 def rm_neuron_norms(w_down: torch.Tensor, norms: torch.Tensor, stream=None) -> None:

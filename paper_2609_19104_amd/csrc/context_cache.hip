@@ -121,8 +121,50 @@ __global__ __launch_bounds__(kSelThreads) void select_rows_kernel(const float *_
     if (tid == kSelThreads - 1) count[0] = pos;  // the last thread's end is the total
 }
 
+// ------------------------------------------------------------------------------------------ blocked layout
+
+// The GEMM operands live in a blocked layout: a bf16 matrix [R][K] (R and K multiples of 64) as 64-row x 64-column
+// blocks of 8 KB, the blocks of one 64-row tile consecutive along K.  Inside a block, row r holds its 64 columns
+// (128 bytes) as eight 16-byte pieces, piece p at position p ^ swz(r): a block is the exact image of its rows in
+// the GEMM's LDS stage, so one K stage of a tile is one contiguous read.  swz permutes the pieces so that the
+// matrix-core fragment reads (16 rows at one piece) hit distinct LDS banks, both with 32 banks served 8 lanes a
+// cycle and with 64 banks served 16 lanes a cycle (the counters show no conflicts).
+#ifndef RM_CTX_KT
+#define RM_CTX_KT 64
+#endif
+constexpr int kStageK = RM_CTX_KT;                // K per stage and per block column
+constexpr int kRowBytes = kStageK * 2;
+constexpr int kBlockElems = 64 * kStageK;
+static_assert(kStageK == 64 || kStageK == 32, "stage width");
+
+__device__ __forceinline__ int ctx_swz(int r) {  // r: row mod 16
+    if constexpr (kStageK == 64)
+        return (r ^ (r >> 3)) & 7;
+    else
+        return ((r >> 1) ^ (r >> 2)) & 3;
+}
+
+__device__ __forceinline__ size_t blocked_offset(int row, int col, int K) {  // element offset of (row, col)
+    const int r = row & 63, piece = (col % kStageK) >> 3;
+    return (static_cast<size_t>(row >> 6) * (K / kStageK) + col / kStageK) * kBlockElems + r * kStageK +
+           ((piece ^ ctx_swz(r & 15)) << 3) + (col & 7);
+}
+
+// Weight packing: one thread per 16-byte piece of a row-major [R][K] matrix.
+__global__ __launch_bounds__(256) void pack_blocked_kernel(const uint16_t *__restrict__ src, int R, int K,
+                                                           uint16_t *__restrict__ dst) {
+    const long long e = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x;
+    const int per_row = K >> 3;
+    if (e >= static_cast<long long>(R) * per_row) return;
+    const int row = static_cast<int>(e / per_row);
+    const int col = static_cast<int>(e - static_cast<long long>(row) * per_row) * 8;
+    *reinterpret_cast<rm_u32x4 *>(dst + blocked_offset(row, col, K)) =
+        *reinterpret_cast<const rm_u32x4 *>(src + static_cast<size_t>(row) * K + col);
+}
+
 // ------------------------------------------------------------------------------------------ gather
 
+// The listed rows of x as bf16 in the blocked layout [m_pad][d]; rows from the count up to m_pad are zero.
 __global__ __launch_bounds__(256) void gather_rows_kernel(const float *__restrict__ x, int d,
                                                           const int32_t *__restrict__ rows,
                                                           const int32_t *__restrict__ count, int max_rows, int m_pad,
@@ -131,9 +173,9 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const float *__restric
     const int lane = threadIdx.x & 63;
     if (i >= m_pad) return;
     const int cnt = min(max(count[0], 0), max_rows);
-    uint16_t *dst = A + static_cast<size_t>(i) * d;
     if (i >= cnt) {
-        for (int c = lane * 4; c < d; c += 256) *reinterpret_cast<uint2 *>(dst + c) = make_uint2(0u, 0u);
+        for (int c = lane * 4; c < d; c += 256)
+            *reinterpret_cast<uint2 *>(A + blocked_offset(i, c, d)) = make_uint2(0u, 0u);
         return;
     }
     const int r = min(max(rows[i], 0), n_tok - 1);
@@ -143,7 +185,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const float *__restric
         uint2 packed;
         packed.x = rm_f32_to_bf16_bits(v.x) | (rm_f32_to_bf16_bits(v.y) << 16);
         packed.y = rm_f32_to_bf16_bits(v.z) | (rm_f32_to_bf16_bits(v.w) << 16);
-        *reinterpret_cast<uint2 *>(dst + c) = packed;
+        *reinterpret_cast<uint2 *>(A + blocked_offset(i, c, d)) = packed;
     }
 }
 
@@ -152,12 +194,12 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const float *__restric
 enum { kEpiGlu = 0, kEpiScatter = 1, kEpiPartial = 2 };
 
 struct GemmArgs {
-    const uint16_t *A;       // bf16 [m_pad][K]
-    const uint16_t *B0, *B1; // bf16 [N][K] (B1: the up matrix of the gate/up product)
+    const uint16_t *A;       // bf16 [m_pad][K], blocked
+    const uint16_t *B0, *B1; // bf16 [N][K], row-major or blocked (B1: the up matrix of the gate/up product)
     int K, N, m_pad;
     const int32_t *count;    // rows of A in use (device), clamped to [0, max_rows]
     int max_rows, act;
-    uint16_t *H;             // kEpiGlu: bf16 [m_pad][N]
+    uint16_t *H;             // kEpiGlu: bf16 [m_pad][N], blocked
     float *y;                // kEpiScatter: float32 [n_tok][N], row rows[i] receives output row i
     const int32_t *rows;
     int n_tok;
@@ -168,24 +210,23 @@ struct GemmArgs {
 // ------------------------------------------------------------------------------------------ DMA-staged GEMM
 
 // The tiles are moved by the load unit straight into LDS (global_load_lds_dwordx4), with no register staging:
-// STAGES buffers, all but one in flight.  A stage is KT wide along K (KT = 32: one matrix-core step, 64 bytes per
-// row; KT = 64: two steps, 128 bytes = one cache line per row); a load instruction fills 1 KB of consecutive rows,
-// lane l writing bytes [16 l, 16 l + 16).  The 16-byte pieces of a row are permuted (piece c of row r sits at
-// position c ^ swz(r)) so that the fragment reads of 16 rows at one piece hit distinct LDS banks, with 32 banks
-// and 8 lanes per cycle as well as with 64 banks and 16 lanes (the counters show no conflicts).
-template <int KT>
-__device__ __forceinline__ int dma_swz(int r) {
-    if constexpr (KT == 32)
-        return ((r >> 1) ^ (r >> 2)) & 3;
-    else
-        return (r ^ (r >> 3)) & 7;
-}
+// STAGES buffers, all but one in flight.  A stage is 64 wide along K (two matrix-core steps, 128 bytes per row) and
+// holds the tile's BM rows of A, then BN rows of each B matrix, in the blocked layout's row image; a load
+// instruction fills 1 KB = 8 rows, lane l writing bytes [16 l, 16 l + 16).  A (and B when B_BLOCKED) come blocked,
+// so each load reads 1 KB of consecutive memory; a row-major B is read 128 bytes per row, each lane taking the
+// piece that belongs at its position.
 
-// One load of 16 bytes per lane into LDS at lds + 16 lane (M0 holds the wave's LDS base).  Issued as inline
-// assembly so that the compiler, which cannot tell the stage buffers apart, adds no wait of its own for it before
-// the LDS reads: the waits are the explicit ones below.
+// One load of 16 bytes per lane into LDS at lds + 16 lane (M0 holds the wave's LDS base while it issues; M0 is
+// the compiler's register, so its value is kept and put back).  Issued as inline assembly so that the compiler,
+// which cannot tell the stage buffers apart, adds no wait of its own for it before the LDS reads: the waits are
+// the explicit ones below.
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+    uint32_t keep;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+        : "=&s"(keep)
+        : "v"(g), "s"(lds)
+        : "memory");
 }
 
 // Wait until at most N of this wave's vector-memory operations are in flight and all its LDS operations are
@@ -205,29 +246,31 @@ constexpr int dma_waves_per_simd(int lds_bytes, int waves) {
     return (163840 / lds_bytes) * waves / 4 >= 2 ? 2 : 1;
 }
 
-template <int TM, int TN, int NB, int KT, int STAGES, int WAVES_M, int EPI>
+template <int TM, int TN, int NB, int STAGES, int WAVES_M, bool B_BLOCKED, int EPI>
 __global__ __launch_bounds__(128 * WAVES_M,
-                             dma_waves_per_simd(STAGES * (16 * WAVES_M * TM + NB * 32 * TN) * KT * 2, 2 * WAVES_M))
+                             dma_waves_per_simd(STAGES * (16 * WAVES_M * TM + NB * 32 * TN) * kRowBytes, 2 * WAVES_M))
 void gemm_dma_kernel(GemmArgs a) {
     constexpr int WAVES = 2 * WAVES_M;             // WAVES_M x 2 waves, each (16 TM) x (16 TN) per matrix
     constexpr int BM = 16 * WAVES_M * TM, BN = 32 * TN;
     constexpr int ROWS = BM + NB * BN;             // a stage: BM rows of A, then BN rows of each B matrix
-    constexpr int RB = KT * 2;                     // bytes per row and stage
-    constexpr int RPB = 1024 / RB;                 // rows per 1 KB load block
-    constexpr int PIECES = RB / 16;
-    static_assert(KT == 32 || KT == 64, "stage width");
-    static_assert(ROWS % (WAVES * RPB) == 0, "load blocks must split evenly over the waves");
+    constexpr int RPB = 1024 / kRowBytes;          // rows per 1 KB load block
+    static_assert(ROWS % (WAVES * RPB) == 0 && BM % (WAVES * RPB) == 0, "load blocks must split evenly");
+    static_assert(BM % 64 == 0 && BN % 64 == 0, "tiles of whole 64-row blocks");
     constexpr int BPW = ROWS / RPB / WAVES;        // load blocks per wave and stage
-    static_assert(STAGES >= 2 && BPW * (STAGES - 2) <= 63, "vmcnt range");
-    constexpr int STAGE = ROWS * RB;
+    constexpr int JA = BM / RPB / WAVES;           // the wave's first JA load blocks are rows of A
+    static_assert(STAGES >= 2 && STAGES <= 4 && BPW * (STAGES - 2) <= 63, "vmcnt range");
+    constexpr int STAGE = ROWS * kRowBytes;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[STAGES][STAGE];
 
     const int mt = a.m_pad / BM;
-    const int q = xcd_order(blockIdx.x, gridDim.x);  // = (n tile * splits + K slice) * mt + m tile
+    const int ntl = a.N / BN;
+    // q = (K slice * ntl + n tile) * mt + m tile: the tiles of one K slice share an XCD (so its L2 holds the slice
+    // of A that they all read), and the m tiles of one n tile are neighbours (sharing the weight rows).
+    const int q = xcd_order(blockIdx.x, gridDim.x);
     const int m0 = (q % mt) * BM;
-    const int ks_id = (q / mt) % a.splits;
-    const int n0 = (q / mt / a.splits) * BN;
-    const int k_len = a.K / a.splits;  // a multiple of KT
+    const int n0 = ((q / mt) % ntl) * BN;
+    const int ks_id = q / mt / ntl;
+    const int k_len = a.K / a.splits;  // a multiple of kStageK
     const int k_base = ks_id * k_len;
     const int cnt = min(max(a.count[0], 0), a.max_rows);
     if (m0 >= cnt) return;  // the whole tile is past the rows in use
@@ -238,30 +281,42 @@ void gemm_dma_kernel(GemmArgs a) {
     const int wm = wave % WAVES_M, wn = wave / WAVES_M;
     const int r = lane & 15, grp = lane >> 4;
 
-    // Source of this lane's 16 bytes in each of the wave's load blocks (block wave + WAVES j), at K offset 0.
-    const uint8_t *src[BPW];
+    // Source of this lane's 16 bytes in each of the wave's load blocks (block wave + WAVES j) at stage 0; a
+    // blocked operand advances one 8 KB block per stage, a row-major one 128 bytes.
+    const size_t kblocks = static_cast<size_t>(a.K / kStageK), kb0 = static_cast<size_t>(k_base / kStageK);
+    const uint16_t *src[BPW];
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
-        const int row = (wave + WAVES * j) * RPB + lane / PIECES;
-        const int piece = (lane % PIECES) ^ dma_swz<KT>(row & 15);
+        const int row = (wave + WAVES * j) * RPB;  // first stage row of the block
         const uint16_t *base;
-        if (row < BM) {
-            base = a.A + static_cast<size_t>(m0 + row) * a.K;
+        int mrow;
+        if (j < JA) {
+            base = a.A;
+            mrow = m0 + row;
         } else {
             const int rb = row - BM;
             const int nb = rb / BN;
-            base = (nb ? a.B1 : a.B0) + static_cast<size_t>(n0 + rb - nb * BN) * a.K;
+            base = nb ? a.B1 : a.B0;
+            mrow = n0 + rb - nb * BN;
         }
-        src[j] = reinterpret_cast<const uint8_t *>(base + k_base + piece * 8);
+        if (j < JA || B_BLOCKED) {
+            src[j] = base + ((mrow >> 6) * kblocks + kb0) * kBlockElems + (mrow & 63) * kStageK + lane * 8;
+        } else {
+            constexpr int kPieces = kStageK / 8;
+            const int rr = mrow + lane / kPieces;  // row of this lane's piece
+            const int piece = (lane % kPieces) ^ ctx_swz(rr & 15);
+            src[j] = base + static_cast<size_t>(rr) * a.K + k_base + piece * 8;
+        }
     }
     const uint32_t lds0 = lds_addr(&lds[0][0]);
-    const int nk = k_len / KT;
     auto issue = [&](int kt) {
-        const size_t koff = static_cast<size_t>(kt) * RB;
         const uint32_t buf = lds0 + (kt % STAGES) * STAGE;
 #pragma unroll
-        for (int j = 0; j < BPW; ++j)
-            dma16(src[j] + koff, __builtin_amdgcn_readfirstlane(buf + (wave + WAVES * j) * 1024));
+        for (int j = 0; j < BPW; ++j) {
+            const size_t step = (j < JA || B_BLOCKED) ? kBlockElems : kStageK;
+            dma16(src[j] + static_cast<size_t>(kt) * step,
+                  __builtin_amdgcn_readfirstlane(buf + (wave + WAVES * j) * 1024));
+        }
     };
 
     rm_f32x4 acc[NB][TM][TN];
@@ -275,18 +330,18 @@ void gemm_dma_kernel(GemmArgs a) {
     // Fragment reads: row r of a 16-row tile, piece 4 ks + grp (K elements 32 ks + 8 grp ..) at its permuted place.
     auto compute = [&](const uint8_t *buf) {
 #pragma unroll
-        for (int ks = 0; ks < KT / 32; ++ks) {
-            const int frag = r * RB + (((ks * 4 + grp) ^ dma_swz<KT>(r)) << 4);
+        for (int ks = 0; ks < kStageK / 32; ++ks) {
+            const int frag = r * kRowBytes + (((ks * 4 + grp) ^ ctx_swz(r)) << 4);
             rm_u32x4 af[TM], bf[NB][TN];
 #pragma unroll
             for (int tm = 0; tm < TM; ++tm)
-                af[tm] = *reinterpret_cast<const rm_u32x4 *>(buf + (wm * TM * 16 + tm * 16) * RB + frag);
+                af[tm] = *reinterpret_cast<const rm_u32x4 *>(buf + (wm * TM * 16 + tm * 16) * kRowBytes + frag);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
                 for (int tn = 0; tn < TN; ++tn)
                     bf[nb][tn] = *reinterpret_cast<const rm_u32x4 *>(
-                        buf + (BM + nb * BN + wn * TN * 16 + tn * 16) * RB + frag);
+                        buf + (BM + nb * BN + wn * TN * 16 + tn * 16) * kRowBytes + frag);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -296,29 +351,20 @@ void gemm_dma_kernel(GemmArgs a) {
                         acc[nb][tm][tn] = mfma16(af[tm], bf[nb][tn], acc[nb][tm][tn]);
         }
     };
-    // Stage kt: wait for its loads (later stages' may stay in flight), barrier (every wave is also done with the
-    // buffer read at stage kt - 1), refill that buffer with stage kt + STAGES - 1, compute stage kt.
+    // Stage kt: wait for its loads (the later stages' may stay in flight), barrier (every wave is also done with
+    // the buffer read at stage kt - 1), refill that buffer with stage kt + STAGES - 1, compute stage kt.
+    const int nk = k_len / kStageK;
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
         if (s < nk) issue(s);
     for (int kt = 0; kt < nk; ++kt) {
-        const int later = min(nk - 1 - kt, STAGES - 2);  // stages issued after kt, still allowed in flight
-        if constexpr (STAGES >= 4) {
-            if (later >= 2) {
-                dma_wait_barrier<BPW * (STAGES >= 4 ? STAGES - 2 : 0)>();
-            } else if (later == 1) {
-                dma_wait_barrier<BPW>();
-            } else {
-                dma_wait_barrier<0>();
-            }
-        } else if constexpr (STAGES == 3) {
-            if (later == 1)
-                dma_wait_barrier<BPW>();
-            else
-                dma_wait_barrier<0>();
-        } else {
+        const int later = min(nk - 1 - kt, STAGES - 2);  // stages issued after kt
+        if (STAGES >= 4 && later >= 2)
+            dma_wait_barrier<(STAGES >= 4 ? 2 : 0) * BPW>();
+        else if (STAGES >= 3 && later == 1)
+            dma_wait_barrier<BPW>();
+        else
             dma_wait_barrier<0>();
-        }
         if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
         compute(&lds[kt % STAGES][0]);
     }
@@ -335,7 +381,7 @@ void gemm_dma_kernel(GemmArgs a) {
                 const int n = n0 + wn * TN * 16 + tn * 16 + r;
                 if constexpr (EPI == kEpiGlu) {
                     const float h = rm_glu_act(a.act, acc[0][tm][tn][i]) * acc[NB - 1][tm][tn][i];
-                    a.H[static_cast<size_t>(m) * a.N + n] = static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
+                    a.H[blocked_offset(m, n, a.N)] = static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
                 } else if constexpr (EPI == kEpiPartial) {
                     a.part[(static_cast<size_t>(ks_id) * a.m_pad + m) * a.N + n] = acc[0][tm][tn][i];
                 } else {
@@ -383,21 +429,17 @@ hipError_t launch_context_select(const float *x, const float *x_ref, int n_tok, 
     return hipGetLastError();
 }
 
-hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const void *w_up, const void *w_down_t,
-                              const float *x, const int32_t *rows, const int32_t *count, float *y, void *ws,
-                              hipStream_t st) {
-    char *base = static_cast<char *>(ws);
-    uint16_t *A = reinterpret_cast<uint16_t *>(base + p.off_a);
+template <bool B_BLOCKED>
+static hipError_t context_gemms(const ContextPlan &p, const uint16_t *w_gate, const uint16_t *w_up,
+                                const uint16_t *w_down_t, const int32_t *rows, const int32_t *count, float *y,
+                                char *base, hipStream_t st) {
+    constexpr int kWavesM = kCtxBM / 64;
+    static_assert(kCtxGluBN == 128, "gate/up tiles of 4 x 16 neurons per wave");
     uint16_t *H = reinterpret_cast<uint16_t *>(base + p.off_h);
-    hipLaunchKernelGGL(gather_rows_kernel, dim3((p.m_pad + 3) / 4), dim3(256), 0, st, x, p.d, rows, count,
-                       p.max_rows, p.m_pad, p.n_tok, A);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-
     GemmArgs g{};
-    g.A = A;
-    g.B0 = static_cast<const uint16_t *>(w_gate);
-    g.B1 = static_cast<const uint16_t *>(w_up);
+    g.A = reinterpret_cast<const uint16_t *>(base + p.off_a);
+    g.B0 = w_gate;
+    g.B1 = w_up;
     g.K = p.d;
     g.N = p.d_ff;
     g.m_pad = p.m_pad;
@@ -406,17 +448,16 @@ hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const vo
     g.act = p.act;
     g.H = H;
     g.splits = 1;
-    constexpr int kWavesM = kCtxBM / 64;
-    static_assert(kCtxGluBN == 128, "gate/up tiles of 4 x 16 neurons per wave");
-    e = launch_timed(RM_KERNEL_GATEUP, gemm_dma_kernel<4, 4, 2, 64, RM_CTX_GLU_STAGES, kWavesM, kEpiGlu>,
+    hipError_t e =
+        launch_timed(RM_KERNEL_GATEUP, gemm_dma_kernel<4, 4, 2, RM_CTX_GLU_STAGES, kWavesM, B_BLOCKED, kEpiGlu>,
                      dim3((p.m_pad / kCtxBM) * (p.d_ff / kCtxGluBN)), dim3(128 * kWavesM), st, g);
     if (e == hipSuccess) e = hipGetLastError();
     if (e != hipSuccess) return e;
 
     GemmArgs o{};
     o.A = H;
-    o.B0 = static_cast<const uint16_t *>(w_down_t);
-    o.B1 = o.B0;
+    o.B0 = w_down_t;
+    o.B1 = w_down_t;
     o.K = p.d_ff;
     o.N = p.d;
     o.m_pad = p.m_pad;
@@ -429,22 +470,47 @@ hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const vo
     o.part = reinterpret_cast<float *>(base + p.off_part);  // used when split
     const dim3 grid((p.m_pad / kCtxBM) * (p.d / p.down_bn) * p.down_splits), block(128 * kWavesM);
     constexpr int S = RM_CTX_DOWN_STAGES;
+    const bool wide = p.down_bn == 128;
     if (p.down_splits == 1) {
-        e = p.down_bn == 128
-                ? launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 4, 1, 64, S, kWavesM, kEpiScatter>, grid, block, st, o)
-                : launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 2, 1, 64, S, kWavesM, kEpiScatter>, grid, block, st, o);
+        e = wide ? launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 4, 1, S, kWavesM, B_BLOCKED, kEpiScatter>, grid,
+                                block, st, o)
+                 : launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 2, 1, S, kWavesM, B_BLOCKED, kEpiScatter>, grid,
+                                block, st, o);
         return e != hipSuccess ? e : hipGetLastError();
     }
     // Split over K: the slices' float32 partials, then their ordered sum scattered into y.
-    e = p.down_bn == 128
-            ? launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 4, 1, 64, S, kWavesM, kEpiPartial>, grid, block, st, o)
-            : launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 2, 1, 64, S, kWavesM, kEpiPartial>, grid, block, st, o);
+    e = wide ? launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 4, 1, S, kWavesM, B_BLOCKED, kEpiPartial>, grid, block,
+                            st, o)
+             : launch_timed(RM_KERNEL_DOWN, gemm_dma_kernel<4, 2, 1, S, kWavesM, B_BLOCKED, kEpiPartial>, grid, block,
+                            st, o);
     if (e == hipSuccess) e = hipGetLastError();
     if (e != hipSuccess) return e;
     const long long n4 = static_cast<long long>(p.max_rows) * (p.d / 4);
     hipLaunchKernelGGL(reduce_scatter_kernel, dim3(static_cast<unsigned>((n4 + 255) / 256)), dim3(256), 0, st,
                        static_cast<const float *>(o.part), p.down_splits, p.m_pad, p.d, rows, count, p.max_rows,
                        p.n_tok, y);
+    return hipGetLastError();
+}
+
+hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const void *w_up, const void *w_down_t,
+                              bool blocked, const float *x, const int32_t *rows, const int32_t *count, float *y,
+                              void *ws, hipStream_t st) {
+    char *base = static_cast<char *>(ws);
+    hipLaunchKernelGGL(gather_rows_kernel, dim3((p.m_pad + 3) / 4), dim3(256), 0, st, x, p.d, rows, count,
+                       p.max_rows, p.m_pad, p.n_tok, reinterpret_cast<uint16_t *>(base + p.off_a));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const auto *wg = static_cast<const uint16_t *>(w_gate);
+    const auto *wu = static_cast<const uint16_t *>(w_up);
+    const auto *wd = static_cast<const uint16_t *>(w_down_t);
+    return blocked ? context_gemms<true>(p, wg, wu, wd, rows, count, y, base, st)
+                   : context_gemms<false>(p, wg, wu, wd, rows, count, y, base, st);
+}
+
+hipError_t launch_pack_blocked(const void *src, int R, int K, void *dst, hipStream_t st) {
+    const long long pieces = static_cast<long long>(R) * (K / 8);
+    hipLaunchKernelGGL(pack_blocked_kernel, dim3(static_cast<unsigned>((pieces + 255) / 256)), dim3(256), 0, st,
+                       static_cast<const uint16_t *>(src), R, K, static_cast<uint16_t *>(dst));
     return hipGetLastError();
 }
 

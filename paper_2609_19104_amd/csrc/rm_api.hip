@@ -604,9 +604,9 @@ RM_EXPORT rm_status rm_context_workspace_size(const rm_ffn_shape *s, int32_t n_t
     return ok();
 }
 
-RM_EXPORT rm_status rm_context_ffn(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
-                                   int32_t n_tok, const float *x, const int32_t *rows, const int32_t *count,
-                                   int32_t max_rows, float *y, void *ws, size_t ws_bytes, void *stream) {
+static rm_status context_ffn(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
+                             bool blocked, int32_t n_tok, const float *x, const int32_t *rows, const int32_t *count,
+                             int32_t max_rows, float *y, void *ws, size_t ws_bytes, void *stream) {
     rm::ContextPlan p;
     rm_status st = context_plan(s, n_tok, max_rows, &p);
     if (st != RM_OK) return st;
@@ -621,10 +621,65 @@ RM_EXPORT rm_status rm_context_ffn(const rm_ffn_shape *s, const void *w_gate, co
     if (ranges_overlap(x, act_bytes, y, act_bytes) || ranges_overlap(ws, p.total, x, act_bytes) ||
         ranges_overlap(ws, p.total, y, act_bytes))
         return fail(RM_ERR_INVALID_ARG, "x, y and the workspace must not overlap");
-    const hipError_t e = rm::launch_context_ffn(p, w_gate, w_up, w_down_t, x, rows, count, y, ws,
+    const hipError_t e = rm::launch_context_ffn(p, w_gate, w_up, w_down_t, blocked, x, rows, count, y, ws,
                                                 static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "context FFN launch");
     return ok();
+}
+
+RM_EXPORT rm_status rm_context_ffn(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
+                                   int32_t n_tok, const float *x, const int32_t *rows, const int32_t *count,
+                                   int32_t max_rows, float *y, void *ws, size_t ws_bytes, void *stream) {
+    return context_ffn(s, w_gate, w_up, w_down_t, false, n_tok, x, rows, count, max_rows, y, ws, ws_bytes, stream);
+}
+
+static size_t context_matrix_bytes(const rm_ffn_shape *s) { return static_cast<size_t>(s->d) * s->d_ff * 2; }
+
+RM_EXPORT rm_status rm_context_pack_size(const rm_ffn_shape *s, size_t *bytes) {
+    if (!bytes) return fail(RM_ERR_INVALID_ARG, "bytes is NULL");
+    rm::ContextPlan p;
+    const rm_status st = context_plan(s, 1, 1, &p);
+    if (st != RM_OK) return st;
+    *bytes = 3 * context_matrix_bytes(s);
+    return ok();
+}
+
+RM_EXPORT rm_status rm_context_pack(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
+                                    void *packed, size_t packed_bytes, void *stream) {
+    rm::ContextPlan p;
+    const rm_status st = context_plan(s, 1, 1, &p);
+    if (st != RM_OK) return st;
+    if (!w_gate || !w_up || !w_down_t || !packed) return fail(RM_ERR_INVALID_ARG, "a pointer is NULL");
+    if (!aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(w_down_t, 16) || !aligned(packed, 16))
+        return fail(RM_ERR_ALIGN, "weights and the packed buffer must be 16-byte aligned");
+    const size_t mb = context_matrix_bytes(s);
+    if (packed_bytes < 3 * mb)
+        return fail(RM_ERR_WORKSPACE, "packed buffer of %zu bytes is smaller than the %zu required", packed_bytes,
+                    3 * mb);
+    if (ranges_overlap(packed, 3 * mb, w_gate, mb) || ranges_overlap(packed, 3 * mb, w_up, mb) ||
+        ranges_overlap(packed, 3 * mb, w_down_t, mb))
+        return fail(RM_ERR_INVALID_ARG, "the packed buffer must not overlap the weights");
+    const auto hs = static_cast<hipStream_t>(stream);
+    char *out = static_cast<char *>(packed);
+    hipError_t e = rm::launch_pack_blocked(w_gate, s->d_ff, s->d, out, hs);
+    if (e == hipSuccess) e = rm::launch_pack_blocked(w_up, s->d_ff, s->d, out + mb, hs);
+    if (e == hipSuccess) e = rm::launch_pack_blocked(w_down_t, s->d, s->d_ff, out + 2 * mb, hs);
+    if (e != hipSuccess) return hip_fail(e, "context weight packing launch");
+    return ok();
+}
+
+RM_EXPORT rm_status rm_context_ffn_packed(const rm_ffn_shape *s, const void *packed, int32_t n_tok, const float *x,
+                                          const int32_t *rows, const int32_t *count, int32_t max_rows, float *y,
+                                          void *ws, size_t ws_bytes, void *stream) {
+    if (!packed) return fail(RM_ERR_INVALID_ARG, "packed is NULL");
+    rm::ContextPlan p;
+    const rm_status st = context_plan(s, n_tok, max_rows, &p);
+    if (st != RM_OK) return st;
+    const size_t mb = context_matrix_bytes(s);
+    const char *w = static_cast<const char *>(packed);
+    if (ranges_overlap(w, 3 * mb, y, static_cast<size_t>(n_tok) * s->d * 4) || ranges_overlap(w, 3 * mb, ws, ws_bytes))
+        return fail(RM_ERR_INVALID_ARG, "the packed weights must not overlap y or the workspace");
+    return context_ffn(s, w, w + mb, w + 2 * mb, true, n_tok, x, rows, count, max_rows, y, ws, ws_bytes, stream);
 }
 
 RM_EXPORT rm_status rm_neuron_norms(const void *w_down, int32_t d_ff, int32_t d, int32_t wdtype, float *norms,

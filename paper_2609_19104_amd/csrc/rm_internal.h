@@ -79,14 +79,12 @@ hipError_t launch_mask_compact(const uint8_t *mask, int n_masks, int d_ff, int32
 hipError_t launch_gather_rows(const rm_ffn_layer_weights *w, const int32_t *idx, const int32_t *count, int d_ff,
                               int d, int wdtype, int max_count, int L, void *out, hipStream_t st);
 
-// Context Cache (context_cache.hip): tile sizes of its two matrix-core GEMMs, and the workspace plan (the
-// gathered rows as bf16 [m_pad][d], then H bf16 [m_pad][d_ff], then the down GEMM's K-slice partials; m_pad =
-// max_rows rounded up to the gate/up tile).
-// The tile sizes can be set at build time (RM_CTX_GLU_BM and so on) for tuning sweeps.
-// Context Cache GEMM tiles (context_cache.hip): 256 rows by 8 waves (4 along the rows x 2 along the columns),
-// each wave 64 rows x 64 columns per weight matrix; the gate/up tile spans 128 neurons of both matrices, the down
-// tile 128 output columns (64 when d is not a multiple of 128).  The stage counts can be set at build time
-// (RM_CTX_GLU_STAGES, RM_CTX_DOWN_STAGES, RM_CTX_DOWN_TARGET) for tuning sweeps.
+// Context Cache (context_cache.hip).  Workspace plan: the gathered rows as bf16 [m_pad][d], then H bf16
+// [m_pad][d_ff] (both in the GEMMs' blocked layout), then the down GEMM's K-slice partials; m_pad = max_rows
+// rounded up to the row tile.  GEMM tiles: 256 rows by 8 waves (4 along the rows x 2 along the columns), each wave
+// 64 rows x 64 columns per weight matrix; the gate/up tile spans 128 neurons of both matrices, the down tile 128
+// output columns (64 when d is not a multiple of 128).  The stage counts and the down GEMM's workgroup target can
+// be set at build time (RM_CTX_GLU_STAGES, RM_CTX_DOWN_STAGES, RM_CTX_DOWN_TARGET) for tuning sweeps.
 #ifndef RM_CTX_GLU_STAGES
 #define RM_CTX_GLU_STAGES 2
 #endif
@@ -108,9 +106,12 @@ struct ContextPlan {
 };
 hipError_t launch_context_select(const float *x, const float *x_ref, int n_tok, int d, int v0, int P, int k,
                                  float *drift, int32_t *rows, int32_t *count, hipStream_t st);
+// blocked: the three weight matrices come in the blocked layout written by launch_pack_blocked.
 hipError_t launch_context_ffn(const ContextPlan &p, const void *w_gate, const void *w_up, const void *w_down_t,
-                              const float *x, const int32_t *rows, const int32_t *count, float *y, void *ws,
-                              hipStream_t st);
+                              bool blocked, const float *x, const int32_t *rows, const int32_t *count, float *y,
+                              void *ws, hipStream_t st);
+// A row-major bf16 [R][K] matrix (R, K multiples of 64) into the blocked layout of the context GEMMs.
+hipError_t launch_pack_blocked(const void *src, int R, int K, void *dst, hipStream_t st);
 
 // Group neuron masks (group_mask.hip): the down rows' norms, and Eq. 1 scores + per-step top-K + union + rerank.
 constexpr int kGroupMaxDff = 16384;

@@ -240,6 +240,7 @@ def test_context_calls_validate(lib):
     assert _ctx_size(2048, 16384, 850, 900)[0] == rm.RM_ERR_SHAPE     # max_rows > n_tok
     assert _ctx_size(2048, 16384, 850, 390, rm.RM_F32)[0] == rm.RM_ERR_DTYPE
     assert _ctx_size(2080, 16384, 850, 390)[0] == rm.RM_ERR_SHAPE     # d not a multiple of 64
+    assert _ctx_size(2048, 16320, 850, 390)[0] == rm.RM_ERR_SHAPE     # d_ff not a multiple of 128
     sel = lib.rm_context_select
     assert sel(FAKE, FAKE * 64, 850, 2048, 0, 768, 769, FAKE * 128, FAKE * 256, FAKE * 512, None) == rm.RM_ERR_SHAPE
     assert sel(FAKE, FAKE * 64, 850, 2048, 100, 768, 10, FAKE * 128, FAKE * 256, FAKE * 512, None) == rm.RM_ERR_SHAPE
@@ -255,3 +256,30 @@ def test_context_calls_validate(lib):
                FAKE * 4096, 1 << 30, None) == rm.RM_ERR_INVALID_ARG  # y is x
     assert ffn(ctypes.byref(s), None, FAKE, FAKE, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 512,
                FAKE * 4096, 1 << 30, None) == rm.RM_ERR_INVALID_ARG
+
+
+def test_context_pack_calls_validate(lib):
+    s = rm.FfnShape(2048, 16384, rm.RM_BF16, 1e-6, rm.RM_ACT_GELU_TANH)
+    n = ctypes.c_size_t(0)
+    assert lib.rm_context_pack_size(ctypes.byref(s), ctypes.byref(n)) == rm.RM_OK
+    assert n.value == 3 * 2048 * 16384 * 2
+    odd = rm.FfnShape(2048, 16320, rm.RM_BF16, 1e-6, rm.RM_ACT_GELU_TANH)  # d_ff not a multiple of 128
+    assert lib.rm_context_pack_size(ctypes.byref(odd), ctypes.byref(n)) == rm.RM_ERR_SHAPE
+    assert lib.rm_context_pack_size(ctypes.byref(s), None) == rm.RM_ERR_INVALID_ARG
+    big = 3 * 2048 * 16384 * 2
+    pack = lib.rm_context_pack
+    W = 1 << 32  # the packed buffer, well away from the fake weights
+    assert pack(ctypes.byref(s), None, FAKE, FAKE, W, big, None) == rm.RM_ERR_INVALID_ARG
+    assert pack(ctypes.byref(s), FAKE, FAKE, FAKE, W, big - 1, None) == rm.RM_ERR_WORKSPACE
+    assert pack(ctypes.byref(s), FAKE + 8, FAKE, FAKE, W, big, None) == rm.RM_ERR_ALIGN
+    assert pack(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, big, None) == rm.RM_ERR_INVALID_ARG  # packed over w_gate
+    assert pack(ctypes.byref(odd), FAKE, FAKE, FAKE, W, big, None) == rm.RM_ERR_SHAPE
+    fp = lib.rm_context_ffn_packed
+    assert fp(ctypes.byref(s), None, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 512, FAKE * 4096, 1 << 30,
+              None) == rm.RM_ERR_INVALID_ARG
+    assert fp(ctypes.byref(s), W, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, W + 64, FAKE * 4096, 1 << 30,
+              None) == rm.RM_ERR_INVALID_ARG  # y inside the packed weights
+    assert fp(ctypes.byref(s), W, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 512, FAKE * 4096, 100,
+              None) == rm.RM_ERR_WORKSPACE
+    assert fp(ctypes.byref(odd), W, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 512, FAKE * 4096, 1 << 30,
+              None) == rm.RM_ERR_SHAPE

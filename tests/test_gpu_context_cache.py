@@ -64,14 +64,18 @@ def test_drift_and_row_selection_bit_exact(n_tok, d, v0, P, k, quantum):
     assert np.array_equal(rows, ref_rows)
 
 
-def _run_ffn(w, x, y_ref, rows, count, max_rows, act):
+def _run_ffn(w, x, y_ref, rows, count, max_rows, act, packed=False):
     xt, yt = dev_f32(x), dev_f32(y_ref)
     rt = torch.from_numpy(np.concatenate([rows, np.full(w.n_tok - len(rows), -1)]).astype(np.int32)).cuda()
     ct = torch.tensor([count], dtype=torch.int32, device="cuda")
     ws = rm.context_workspace(w.d, w.d_ff, w.n_tok, max_rows, act=act)
     ws.fill_(0x7F)  # the path must not rely on a cleared workspace
-    rm.rm_context_ffn(xt, yt, _bf16(w.layer.w_gate), _bf16(w.layer.w_up), _bf16(w.w_down_t), rt, ct, max_rows, ws,
-                      act=act)
+    wg, wu, wd = _bf16(w.layer.w_gate), _bf16(w.layer.w_up), _bf16(w.w_down_t)
+    if packed:
+        pk = rm.rm_context_pack(wg, wu, wd, act=act)
+        rm.rm_context_ffn_packed(xt, yt, pk, rt, ct, max_rows, ws, act=act)
+    else:
+        rm.rm_context_ffn(xt, yt, wg, wu, wd, rt, ct, max_rows, ws, act=act)
     torch.cuda.synchronize()
     return yt.cpu().numpy()
 
@@ -99,14 +103,49 @@ FFN_CASES = [
 ]
 
 
+@pytest.mark.parametrize("packed", [False, True], ids=["row-major", "packed"])
 @pytest.mark.parametrize("d,d_ff,n_tok,v0,P,k,max_rows,act", FFN_CASES)
-def test_context_ffn_parity(d, d_ff, n_tok, v0, P, k, max_rows, act):
+def test_context_ffn_parity(d, d_ff, n_tok, v0, P, k, max_rows, act, packed):
     w = wl.context_workload(n_tok=n_tok, v0=v0, P=P, d=d, d_ff=d_ff, seed=7 + d)
     drift = cc.drift(w.x[v0:v0 + P], w.x_ref[v0:v0 + P])
     rows = cc.recomputed_rows(drift, n_tok, v0, k)
     count = min(len(rows), max_rows)  # rows past max_rows are not recomputed
-    y = _run_ffn(w, w.x, w.y_ref, rows, count, max_rows, act)
+    y = _run_ffn(w, w.x, w.y_ref, rows, count, max_rows, act, packed=packed)
     _check_update(w, w.x, w.y_ref, y, rows[:count], act)
+
+
+def _blocked_reference(m):
+    """The documented blocked layout, written out with NumPy: 64 x 64 blocks, row tiles outermost, the blocks of a
+    tile consecutive along K; in a block, row r's eight 16-byte pieces with piece p at position p ^ swz(r % 16),
+    swz(r) = (r ^ (r >> 3)) & 7."""
+    R, K = m.shape
+    out = np.empty(R * K, dtype=m.dtype)
+    swz = lambda r: (r ^ (r >> 3)) & 7  # noqa: E731
+    for t in range(R // 64):
+        for kb in range(K // 64):
+            blk = m[t * 64:(t + 1) * 64, kb * 64:(kb + 1) * 64].reshape(64, 8, 8)
+            img = np.empty_like(blk)
+            for r in range(64):
+                for p in range(8):
+                    img[r, p ^ swz(r % 16)] = blk[r, p]
+            base = (t * (K // 64) + kb) * 4096
+            out[base:base + 4096] = img.reshape(-1)
+    return out
+
+
+def test_context_pack_layout_and_packed_matches_row_major_bit_for_bit():
+    d, d_ff = 192, 256  # d not a multiple of 128: the down product runs 64-column tiles
+    w = wl.context_workload(n_tok=90, v0=10, P=70, d=d, d_ff=d_ff, seed=21)
+    wg, wu, wd = _bf16(w.layer.w_gate), _bf16(w.layer.w_up), _bf16(w.w_down_t)
+    pk = rm.rm_context_pack(wg, wu, wd).cpu().numpy().view(np.uint16)
+    mats = [w.layer.w_gate, w.layer.w_up, w.w_down_t]
+    ref = np.concatenate([_blocked_reference(np.ascontiguousarray(m).view(np.uint16)) for m in mats])
+    assert np.array_equal(pk, ref)
+    rows = cc.recomputed_rows(cc.drift(w.x[10:80], w.x_ref[10:80]), 90, 10, 30)
+    y_row = _run_ffn(w, w.x, w.y_ref, rows, len(rows), len(rows), "gelu_tanh")
+    y_pk = _run_ffn(w, w.x, w.y_ref, rows, len(rows), len(rows), "gelu_tanh", packed=True)
+    assert np.array_equal(y_row.view(np.uint32), y_pk.view(np.uint32))
+    _check_update(w, w.x, w.y_ref, y_pk, rows, "gelu_tanh")
 
 
 def test_context_ffn_with_no_rows_leaves_y():

@@ -56,21 +56,25 @@ __global__ __launch_bounds__(64) void drift_kernel(const float *__restrict__ x, 
     const float *xa = x + static_cast<size_t>(v0 + p) * d;
     const float *xb = xr + static_cast<size_t>(v0 + p) * d;
     float sd = 0.0f, sx = 0.0f;
-    // Eight columns of each input in flight per lane before the in-order sums (columns past d are not added).
-    for (int c0 = lane; c0 < d; c0 += 8 * 64) {
-        float va[8], vb[8];
+    // kDriftCols columns of each input in flight per lane (all of a 2048-wide row in one round trip) before the
+    // in-order sums; columns past d are not added.
+    constexpr int kDriftCols = 32;
+    for (int c0 = lane; c0 < d; c0 += kDriftCols * 64) {
+        float va[kDriftCols], vb[kDriftCols];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < kDriftCols; ++u) {
             const int c = min(c0 + u * 64, d - 1);
             va[u] = xa[c];
             vb[u] = xb[c];
         }
+        // No branch between the loads and the sums (a branch lets the compiler sink each load to its use, one
+        // round trip per column): a column past d adds +0, which leaves the non-negative sums unchanged.
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            if (c0 + u * 64 >= d) break;
+        for (int u = 0; u < kDriftCols; ++u) {
+            const bool in = c0 + u * 64 < d;
             const float diff = __fsub_rn(va[u], vb[u]);
-            sd = __fadd_rn(sd, mul_rounded(diff, diff));
-            sx = __fadd_rn(sx, mul_rounded(va[u], va[u]));
+            sd = __fadd_rn(sd, in ? mul_rounded(diff, diff) : 0.0f);
+            sx = __fadd_rn(sx, in ? mul_rounded(va[u], va[u]) : 0.0f);
         }
     }
     for (int off = 32; off >= 1; off >>= 1) {

@@ -7,8 +7,9 @@
 //                          per row.  The top-k decision below depends on it, so it has a fixed float32 order: lane j
 //                          adds the squares of columns j, j + 64, ... one rounding per operation, the 64 lane sums
 //                          are folded 32, 16, ..., 1 apart, then rounded division and correctly rounded roots.
-//   select_rows_kernel:    one 1024-thread workgroup: the k visual rows with the largest drift (radix select, ties
-//                          to the lower token) plus every non-visual row, as an ascending row list and its count.
+//   select_rows_kernel:    one workgroup (256 threads up to 4096 rows, else 1024): the k visual rows with the
+//                          largest drift (radix select, ties to the lower token) plus every non-visual row, as an
+//                          ascending row list and its count.
 //   gather_rows_kernel:    the listed rows of x as bf16 into the workspace, zero rows up to the padded count.
 //   gemm_dma_kernel<GLU>:  H = act(A W_gate^T) * (A W_up^T), bf16 [rows][d_ff].
 //   gemm_dma_kernel<SCAT>: y[row_i] = H_i W_down^T (W_down as nn.Linear's [d][d_ff]): Eq. 3's recomputed rows
@@ -30,6 +31,7 @@ namespace {
 
 using rm_sel::kSelPerThread;
 using rm_sel::kSelThreads;
+using rm_sel::kSelThreadsSmall;
 using rm_sel::mul_rounded;
 using rm_sel::select_top_k;
 using rm_sel::SelLds;
@@ -91,11 +93,12 @@ __global__ __launch_bounds__(64) void drift_kernel(const float *__restrict__ x, 
 
 // ------------------------------------------------------------------------------------------ row selection
 
-__global__ __launch_bounds__(kSelThreads) void select_rows_kernel(const float *__restrict__ drift, int n_tok, int v0,
-                                                                  int P, int k, int32_t *__restrict__ rows,
-                                                                  int32_t *__restrict__ count) {
-    __shared__ SelLds l;
-    __shared__ uint8_t chosen[kSelThreads * kSelPerThread];
+template <int kThreads>
+__global__ __launch_bounds__(kThreads) void select_rows_kernel(const float *__restrict__ drift, int n_tok, int v0,
+                                                               int P, int k, int32_t *__restrict__ rows,
+                                                               int32_t *__restrict__ count) {
+    __shared__ SelLds<kThreads> l;
+    __shared__ uint8_t chosen[kThreads * kSelPerThread];
     const int tid = threadIdx.x;
     const int p0 = tid * kSelPerThread;
     uint32_t valid = 0, key[kSelPerThread];
@@ -122,7 +125,7 @@ __global__ __launch_bounds__(kSelThreads) void select_rows_kernel(const float *_
 #pragma unroll
     for (int i = 0; i < kSelPerThread; ++i)
         if ((take >> i) & 1u) rows[pos++] = r0 + i;
-    if (tid == kSelThreads - 1) count[0] = pos;  // the last thread's end is the total
+    if (tid == kThreads - 1) count[0] = pos;  // the last thread's end is the total
 }
 
 // ------------------------------------------------------------------------------------------ blocked layout
@@ -373,7 +376,18 @@ void gemm_dma_kernel(GemmArgs a) {
         compute(&lds[kt % STAGES][0]);
     }
 
-    // Lane (grp, r), register i of a tile: row 4 grp + i, column r.
+    // Lane (grp, r), register i of a tile: row 4 grp + i, column r.  The scatter's destination rows are all read
+    // before any store (a read behind the row test would wait for each one in turn).
+    int dst[TM][4];
+    if constexpr (EPI == kEpiScatter) {
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int m = min(m0 + wm * TM * 16 + tm * 16 + grp * 4 + i, cnt - 1);
+                dst[tm][i] = min(max(a.rows[m], 0), a.n_tok - 1);
+            }
+    }
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
 #pragma unroll
@@ -389,8 +403,7 @@ void gemm_dma_kernel(GemmArgs a) {
                 } else if constexpr (EPI == kEpiPartial) {
                     a.part[(static_cast<size_t>(ks_id) * a.m_pad + m) * a.N + n] = acc[0][tm][tn][i];
                 } else {
-                    const int row = min(max(a.rows[m], 0), a.n_tok - 1);
-                    a.y[static_cast<size_t>(row) * a.N + n] = acc[0][tm][tn][i];
+                    a.y[static_cast<size_t>(dst[tm][i]) * a.N + n] = acc[0][tm][tn][i];
                 }
             }
         }
@@ -428,8 +441,13 @@ hipError_t launch_context_select(const float *x, const float *x_ref, int n_tok, 
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(select_rows_kernel, dim3(1), dim3(kSelThreads), 0, st, static_cast<const float *>(drift),
-                       n_tok, v0, P, k, rows, count);
+    // Each thread covers 16 rows of the sequence: 256 threads while they fit (fewer waves at each barrier).
+    if (n_tok <= kSelThreadsSmall * kSelPerThread)
+        hipLaunchKernelGGL(select_rows_kernel<kSelThreadsSmall>, dim3(1), dim3(kSelThreadsSmall), 0, st,
+                           static_cast<const float *>(drift), n_tok, v0, P, k, rows, count);
+    else
+        hipLaunchKernelGGL(select_rows_kernel<kSelThreads>, dim3(1), dim3(kSelThreads), 0, st,
+                           static_cast<const float *>(drift), n_tok, v0, P, k, rows, count);
     return hipGetLastError();
 }
 

@@ -46,25 +46,25 @@ __global__ __launch_bounds__(kWave) void gateup_f32_kernel(
         float ag[rm::kF32TokBlock], au[rm::kF32TokBlock];
 #pragma unroll
         for (int t = 0; t < rm::kF32TokBlock; ++t) ag[t] = au[t] = 0.0f;
+        // No branch around the loads (a branch lets the compiler wait for each load before the next): a slot past
+        // the list reads neuron 0 and tokens past T re-read the last token; neither sum is ever stored.
         for (int c = cl * 4; c < d; c += 32) {
-            float4 g4 = make_float4(0.f, 0.f, 0.f, 0.f), u4 = g4;
-            if (valid) {
-                g4 = *reinterpret_cast<const float4 *>(grow + c);
-                u4 = *reinterpret_cast<const float4 *>(urow + c);
-            }
+            const float4 g4 = *reinterpret_cast<const float4 *>(grow + c);
+            const float4 u4 = *reinterpret_cast<const float4 *>(urow + c);
+            float4 xv[rm::kF32TokBlock];
+#pragma unroll
+            for (int t = 0; t < rm::kF32TokBlock; ++t)
+                xv[t] = *reinterpret_cast<const float4 *>(xb + static_cast<size_t>(min(t0 + t, T - 1)) * d + c);
 #pragma unroll
             for (int t = 0; t < rm::kF32TokBlock; ++t) {
-                if (t < nt) {
-                    const float4 xv = *reinterpret_cast<const float4 *>(xb + static_cast<size_t>(t0 + t) * d + c);
-                    ag[t] = fmaf(g4.x, xv.x, ag[t]);
-                    ag[t] = fmaf(g4.y, xv.y, ag[t]);
-                    ag[t] = fmaf(g4.z, xv.z, ag[t]);
-                    ag[t] = fmaf(g4.w, xv.w, ag[t]);
-                    au[t] = fmaf(u4.x, xv.x, au[t]);
-                    au[t] = fmaf(u4.y, xv.y, au[t]);
-                    au[t] = fmaf(u4.z, xv.z, au[t]);
-                    au[t] = fmaf(u4.w, xv.w, au[t]);
-                }
+                ag[t] = fmaf(g4.x, xv[t].x, ag[t]);
+                ag[t] = fmaf(g4.y, xv[t].y, ag[t]);
+                ag[t] = fmaf(g4.z, xv[t].z, ag[t]);
+                ag[t] = fmaf(g4.w, xv[t].w, ag[t]);
+                au[t] = fmaf(u4.x, xv[t].x, au[t]);
+                au[t] = fmaf(u4.y, xv[t].y, au[t]);
+                au[t] = fmaf(u4.z, xv[t].z, au[t]);
+                au[t] = fmaf(u4.w, xv[t].w, au[t]);
             }
         }
         // Combine the 8 lanes of each neuron row (lanes 8r .. 8r+7): fixed butterfly.

@@ -13,9 +13,10 @@
 //                         row loads), then each lane adds its own row's 64 squares in column order.
 //   scores_kernel:        one wave per (step, layer, 64 neurons): the rows go through LDS with coalesced loads,
 //                         then lane n adds row n in token order.
-//   step_select_kernel:   one 1024-thread workgroup per (step, layer), 16 neurons per thread (d_ff <= 16384): the
-//                         step's top K sets the layer's mask bytes (their union over the steps).
-//   group_rerank_kernel:  one 1024-thread workgroup per layer: the union's top K by summed score.
+//   step_select_kernel:   one workgroup per (step, layer), 16 neurons per thread (256 threads up to d_ff = 4096,
+//                         else 1024, d_ff <= 16384): the step's top K sets the layer's mask bytes (their union over
+//                         the steps).
+//   group_rerank_kernel:  one workgroup per layer (same size): the union's top K by summed score.
 // Top K is an MSB-first radix select over the scores' bit patterns (non-negative floats order like their bits):
 // four 8-bit passes, each a histogram (per-wave LDS histograms with integer atomics, so the counts are exact,
 // then added) and a suffix scan that finds the digit of the K-th largest key; then the keys above that
@@ -26,6 +27,7 @@ namespace {
 
 using rm_sel::kSelPerThread;
 using rm_sel::kSelThreads;
+using rm_sel::kSelThreadsSmall;
 using rm_sel::mul_rounded;
 using rm_sel::select_top_k;
 using rm_sel::SelLds;
@@ -47,27 +49,29 @@ __global__ __launch_bounds__(64) void neuron_norms_kernel(const void *__restrict
             const int r = piece >> 3;
             const int cc = (piece & 7) * 8;
             const int row = min(n0 + r, d_ff - 1);
+            // d is a multiple of 32, so a piece is wholly inside or outside the row.  A piece outside reads the
+            // row's first piece and contributes +0 (no change to a non-negative sum): no branch around the load,
+            // which would let the compiler wait for each load before issuing the next.
+            const bool in = c0 + cc < d;
+            const int col = in ? c0 + cc : 0;
             float v[8];
-            if (c0 + cc < d) {  // d is a multiple of 32, so a piece is wholly inside or outside the row
-                if constexpr (kBf16) {
-                    const uint4 p = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(w) +
-                                                                     static_cast<size_t>(row) * d + c0 + cc);
-                    const uint32_t q[4] = {p.x, p.y, p.z, p.w};
+            if constexpr (kBf16) {
+                const uint4 p = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(w) +
+                                                                 static_cast<size_t>(row) * d + col);
+                const uint32_t q[4] = {p.x, p.y, p.z, p.w};
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        v[2 * i] = __uint_as_float(q[i] << 16);
-                        v[2 * i + 1] = __uint_as_float(q[i] & 0xffff0000u);
-                    }
-                } else {
-                    const float *src = static_cast<const float *>(w) + static_cast<size_t>(row) * d + c0 + cc;
-                    const float4 a = *reinterpret_cast<const float4 *>(src);
-                    const float4 b = *reinterpret_cast<const float4 *>(src + 4);
-                    v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
+                for (int i = 0; i < 4; ++i) {
+                    v[2 * i] = __uint_as_float(q[i] << 16);
+                    v[2 * i + 1] = __uint_as_float(q[i] & 0xffff0000u);
                 }
             } else {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) v[i] = 0.0f;  // adds +0 to a non-negative sum: no change
+                const float *src = static_cast<const float *>(w) + static_cast<size_t>(row) * d + col;
+                const float4 a = *reinterpret_cast<const float4 *>(src);
+                const float4 b = *reinterpret_cast<const float4 *>(src + 4);
+                v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
             }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = in ? v[i] : 0.0f;
 #pragma unroll
             for (int i = 0; i < 8; ++i) tile[r][cc + i] = v[i];
         }
@@ -123,9 +127,10 @@ __global__ __launch_bounds__(64) void scores_kernel(const float *__restrict__ h,
 
 // Each step's K best neurons of one layer (workgroup = step * L + layer) set their mask bytes to 1: the mask
 // holds the union of the steps' candidates when the rerank runs.
-__global__ __launch_bounds__(kSelThreads) void step_select_kernel(const float *__restrict__ scores, int L, int d_ff,
-                                                                  int k, uint8_t *__restrict__ mask) {
-    __shared__ SelLds l;
+template <int kThreads>
+__global__ __launch_bounds__(kThreads) void step_select_kernel(const float *__restrict__ scores, int L, int d_ff,
+                                                               int k, uint8_t *__restrict__ mask) {
+    __shared__ SelLds<kThreads> l;
     const int sl = blockIdx.x;
     const int n0 = threadIdx.x * kSelPerThread;
     const float *c = scores + static_cast<size_t>(sl) * d_ff;
@@ -146,9 +151,10 @@ __global__ __launch_bounds__(kSelThreads) void step_select_kernel(const float *_
 // The layer's mask: the K members of the union (mask bytes set by step_select_kernel) with the largest score
 // summed over the steps in step order.  Neurons outside the union get the smallest key and are never taken
 // (the union holds at least K neurons).
-__global__ __launch_bounds__(kSelThreads) void group_rerank_kernel(const float *__restrict__ scores, int S, int L,
-                                                                   int d_ff, int k, uint8_t *__restrict__ mask) {
-    __shared__ SelLds l;
+template <int kThreads>
+__global__ __launch_bounds__(kThreads) void group_rerank_kernel(const float *__restrict__ scores, int S, int L,
+                                                                int d_ff, int k, uint8_t *__restrict__ mask) {
+    __shared__ SelLds<kThreads> l;
     const int layer = blockIdx.x;
     const int n0 = threadIdx.x * kSelPerThread;
     uint8_t *m = mask + static_cast<size_t>(layer) * d_ff;
@@ -159,15 +165,24 @@ __global__ __launch_bounds__(kSelThreads) void group_rerank_kernel(const float *
         summed[i] = 0.0f;
         if (n0 + i < d_ff) valid |= 1u << i;
     }
+    // The loads of a step are all issued before its sums, with no branch between them (a branch would let the
+    // compiler sink each load to its use, one round trip per neuron); slots past d_ff read the last neuron and
+    // are not used.
+    const int last = d_ff - 1;
     for (int s = 0; s < S; ++s) {
         const float *c = scores + (static_cast<size_t>(s) * L + layer) * d_ff;
+        float v[kSelPerThread];
 #pragma unroll
-        for (int i = 0; i < kSelPerThread; ++i)
-            if ((valid >> i) & 1u) summed[i] = __fadd_rn(summed[i], c[n0 + i]);
+        for (int i = 0; i < kSelPerThread; ++i) v[i] = c[min(n0 + i, last)];
+#pragma unroll
+        for (int i = 0; i < kSelPerThread; ++i) summed[i] = __fadd_rn(summed[i], v[i]);
     }
+    uint8_t in_union[kSelPerThread];
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i) in_union[i] = m[min(n0 + i, last)];
 #pragma unroll
     for (int i = 0; i < kSelPerThread; ++i)
-        key[i] = ((valid >> i) & 1u) && m[n0 + i] != 0 ? __float_as_uint(summed[i]) + 1u : 0u;
+        key[i] = ((valid >> i) & 1u) && in_union[i] != 0 ? __float_as_uint(summed[i]) + 1u : 0u;
     const uint32_t sel = select_top_k(key, valid, k, d_ff, l);
 #pragma unroll
     for (int i = 0; i < kSelPerThread; ++i)
@@ -194,11 +209,21 @@ hipError_t launch_group_masks(const float *h, int S, int L, int d_ff, int T, con
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const float *sc = scores;
-    launch_timed(RM_KERNEL_GROUP_SELECT, step_select_kernel, dim3(S * L), dim3(kSelThreads), st, sc, L, d_ff, k,
-                 mask);
-    e = hipGetLastError();
+    // A workgroup of 256 threads while the layer's neurons fit (fewer waves meet at each barrier), else 1024.
+    if (d_ff <= kSelThreadsSmall * kSelPerThread) {
+        e = launch_timed(RM_KERNEL_GROUP_SELECT, step_select_kernel<kSelThreadsSmall>, dim3(S * L),
+                         dim3(kSelThreadsSmall), st, sc, L, d_ff, k, mask);
+        if (e == hipSuccess) e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(group_rerank_kernel<kSelThreadsSmall>, dim3(L), dim3(kSelThreadsSmall), 0, st, sc, S, L,
+                           d_ff, k, mask);
+        return hipGetLastError();
+    }
+    e = launch_timed(RM_KERNEL_GROUP_SELECT, step_select_kernel<kSelThreads>, dim3(S * L), dim3(kSelThreads), st, sc,
+                     L, d_ff, k, mask);
+    if (e == hipSuccess) e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(group_rerank_kernel, dim3(L), dim3(kSelThreads), 0, st, sc, S, L, d_ff, k, mask);
+    hipLaunchKernelGGL(group_rerank_kernel<kSelThreads>, dim3(L), dim3(kSelThreads), 0, st, sc, S, L, d_ff, k, mask);
     return hipGetLastError();
 }
 

@@ -1,5 +1,5 @@
 // Device helpers shared by the kernels that rank float32 scores: an exactly rounded product, a workgroup prefix
-// sum, and the top-K selection of a 1024-thread workgroup (group_mask.hip, context_cache.hip).
+// sum, and the top-K selection of a workgroup of 256 or 1024 threads (group_mask.hip, context_cache.hip).
 //
 // Top K is an MSB-first radix select over the scores' bit patterns (non-negative floats order like their bits):
 // four 8-bit passes, each a histogram (per-wave LDS histograms with integer atomics, so the counts are exact,
@@ -11,8 +11,9 @@
 
 namespace rm_sel {
 
-constexpr int kSelThreads = 1024;
-constexpr int kSelPerThread = 16;  // keys per thread: at most 16384 per workgroup
+constexpr int kSelThreads = 1024;      // the largest workgroup: 16384 keys
+constexpr int kSelThreadsSmall = 256;  // up to 4096 keys: a quarter of the waves at each barrier
+constexpr int kSelPerThread = 16;      // keys per thread
 
 // a * b rounded to float32 on its own: the empty asm statement hides the product from the optimizer, so it
 // cannot be fused with the sum it feeds into one multiply-add (HIP compiles with contraction allowed).
@@ -22,15 +23,17 @@ __device__ __forceinline__ float mul_rounded(float a, float b) {
     return p;
 }
 
+template <int kThreads>
 struct SelLds {
-    uint32_t whist[kSelThreads / 64][256];  // one histogram per wave: atomics only contend within a wave
+    uint32_t whist[kThreads / 64][256];  // one histogram per wave: atomics only contend within a wave
     uint32_t hist[256];
-    int wave_sum[kSelThreads / 64];
+    int wave_sum[kThreads / 64];
     int digit, need;
 };
 
 // Exclusive prefix sum of v over the workgroup, in thread order.
-__device__ __forceinline__ int block_excl_scan(int v, SelLds &l) {
+template <int kThreads>
+__device__ __forceinline__ int block_excl_scan(int v, SelLds<kThreads> &l) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int incl = v;
 #pragma unroll
@@ -48,8 +51,10 @@ __device__ __forceinline__ int block_excl_scan(int v, SelLds &l) {
 
 // Selection bits (bit i: item tid * 16 + i) of the k largest keys among the thread's valid ones (bit i of
 // `valid`), ties to the lower item index.  0 <= k; every thread of the workgroup calls it.
+template <int kThreads>
 __device__ inline uint32_t select_top_k(const uint32_t (&key)[kSelPerThread], uint32_t valid, int k, int n_valid,
-                                        SelLds &l) {
+                                        SelLds<kThreads> &l) {
+    static_assert(kThreads >= 256, "the bin sums take 256 threads");
     if (k <= 0) return 0u;
     if (k >= n_valid) return valid;
     const int tid = threadIdx.x;
@@ -67,7 +72,7 @@ __device__ inline uint32_t select_top_k(const uint32_t (&key)[kSelPerThread], ui
         if (tid < 256) {
             uint32_t c = 0;
 #pragma unroll
-            for (int w = 0; w < kSelThreads / 64; ++w) c += l.whist[w][tid];
+            for (int w = 0; w < kThreads / 64; ++w) c += l.whist[w][tid];
             l.hist[tid] = c;
         }
         __syncthreads();

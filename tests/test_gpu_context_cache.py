@@ -44,6 +44,8 @@ SELECT_CASES = [
     (50, 128, 40, 0, 0, 0.0),
     (300, 256, 20, 256, 103, 0.5),
     (16384, 32, 0, 16384, 4000, 0.0),
+    (4096, 32, 0, 4000, 1500, 0.5),   # the last size of the 256-thread selection
+    (4097, 32, 1, 4000, 1500, 0.5),   # one row more: 1024 threads
 ]
 
 

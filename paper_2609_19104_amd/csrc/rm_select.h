@@ -25,8 +25,9 @@ __device__ __forceinline__ float mul_rounded(float a, float b) {
 
 template <int kThreads>
 struct SelLds {
-    uint32_t whist[kThreads / 64][256];  // one histogram per wave: atomics only contend within a wave
-    uint32_t hist[256];
+    // One histogram per wave (atomics only contend within a wave), two sets: a pass counts into one while the
+    // other is cleared for the next pass.
+    uint32_t whist[2][kThreads / 64][256];
     int wave_sum[kThreads / 64];
     int digit, need;
 };
@@ -54,56 +55,56 @@ __device__ __forceinline__ int block_excl_scan(int v, SelLds<kThreads> &l) {
 template <int kThreads>
 __device__ inline uint32_t select_top_k(const uint32_t (&key)[kSelPerThread], uint32_t valid, int k, int n_valid,
                                         SelLds<kThreads> &l) {
-    static_assert(kThreads >= 256, "the bin sums take 256 threads");
+    static_assert(kThreads >= 256, "wave 0 finds the digit while at least three other waves clear histograms");
     if (k <= 0) return 0u;
     if (k >= n_valid) return valid;
-    const int tid = threadIdx.x;
+    constexpr int kWaves = kThreads / 64;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     uint32_t prefix = 0, hi = 0;
     int need = k;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        const int wave = tid >> 6;
-        for (int b = tid & 63; b < 256; b += 64) l.whist[wave][b] = 0u;
-        __syncthreads();
+    for (int b = lane; b < 256; b += 64) l.whist[0][wave][b] = 0u;
+    __syncthreads();
+    // Two barriers per pass: after the counts, and after wave 0 has found the digit (meanwhile the other waves
+    // clear the other histogram set for the next pass).
+    for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass, buf = pass & 1;
 #pragma unroll
         for (int i = 0; i < kSelPerThread; ++i)
             if (((valid >> i) & 1u) && (key[i] & hi) == prefix)
-                atomicAdd(&l.whist[wave][(key[i] >> shift) & 255u], 1u);
+                atomicAdd(&l.whist[buf][wave][(key[i] >> shift) & 255u], 1u);
         __syncthreads();
-        if (tid < 256) {
-            uint32_t c = 0;
+        if (wave == 0) {  // lane j holds digits 4j .. 4j+3; find the digit holding the need-th largest key
+            uint32_t b[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-            for (int w = 0; w < kThreads / 64; ++w) c += l.whist[w][tid];
-            l.hist[tid] = c;
-        }
-        __syncthreads();
-        if (tid < 64) {  // lane j holds digits 4j .. 4j+3; find the digit holding the need-th largest key
-            const int j = tid;
-            const uint32_t b0 = l.hist[4 * j], b1 = l.hist[4 * j + 1], b2 = l.hist[4 * j + 2], b3 = l.hist[4 * j + 3];
-            const int own = static_cast<int>(b0 + b1 + b2 + b3);
+            for (int w = 0; w < kWaves; ++w)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) b[q] += l.whist[buf][w][4 * lane + q];
+            const int own = static_cast<int>(b[0] + b[1] + b[2] + b[3]);
             int above = own;  // inclusive suffix sum over lanes j .. 63, then made exclusive
 #pragma unroll
             for (int off = 1; off < 64; off <<= 1) {
                 const int u = __shfl_down(above, off);
-                if (j + off < 64) above += u;
+                if (lane + off < 64) above += u;
             }
             above -= own;  // keys in digits above 4j + 3
-            const uint32_t b[4] = {b0, b1, b2, b3};
             int cum = above;
 #pragma unroll
             for (int q = 3; q >= 0; --q) {
                 const int c = static_cast<int>(b[q]);
                 if (cum < need && cum + c >= need) {
-                    l.digit = 4 * j + q;
+                    l.digit = 4 * lane + q;
                     l.need = need - cum;
                 }
                 cum += c;
             }
+        } else {
+            for (int w = wave - 1; w < kWaves; w += kWaves - 1)
+                for (int b = lane; b < 256; b += 64) l.whist[buf ^ 1][w][b] = 0u;
         }
-        __syncthreads();
+        __syncthreads();  // l.digit / l.need are rewritten by wave 0 only after the next pass's first barrier
         prefix |= static_cast<uint32_t>(l.digit) << shift;
         hi |= 255u << shift;
         need = l.need;
-        __syncthreads();  // l.digit / l.need are rewritten by the next pass
     }
     // prefix is the k-th largest key; take every larger key and the `need` lowest-index keys equal to it.
     uint32_t sel = 0, eq = 0;

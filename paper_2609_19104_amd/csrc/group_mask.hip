@@ -89,6 +89,25 @@ __global__ __launch_bounds__(64) void neuron_norms_kernel(const void *__restrict
 // row n in token order.  The mask bytes of the layer are cleared here (step 0), before the selections set them.
 constexpr int kScoreRows = 64;
 constexpr int kScoreChunk = 64;
+#ifndef RM_SCORE_BATCH
+#define RM_SCORE_BATCH 32
+#endif
+constexpr int kScoreBatch = RM_SCORE_BATCH;  // loads in flight per lane
+
+// s + the n staged values added in index order, one rounding per addition (the chain continues across chunks),
+// with the LDS reads of 8 values issued before their additions.
+__device__ __forceinline__ float row_abs_sum(float s, const float *row, int n) {
+    int t = 0;
+    for (; t + 8 <= n; t += 8) {
+        float q[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) q[i] = row[t + i];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s = __fadd_rn(s, q[i]);
+    }
+    for (; t < n; ++t) s = __fadd_rn(s, row[t]);
+    return s;
+}
 
 __global__ __launch_bounds__(64) void scores_kernel(const float *__restrict__ h, int d_ff, int T,
                                                     const float *__restrict__ norms, int L,
@@ -100,20 +119,61 @@ __global__ __launch_bounds__(64) void scores_kernel(const float *__restrict__ h,
     const int rows = min(kScoreRows, d_ff - n0);
     const float *base = h + (static_cast<size_t>(sl) * d_ff + n0) * T;
     float s = 0.0f;
-    for (int t0 = 0; t0 < T; t0 += kScoreChunk) {
-        const int C = min(kScoreChunk, T - t0);
-        const int stride = C | 1;  // odd row pitch: lane n's reads of row n fall in distinct banks
-        const int total = rows * C;
-#pragma unroll 8
-        for (int e = lane; e < total; e += 64) {
-            const int r = e / C;
-            const int t = e - r * C;
-            tile[r * stride + t] = fabsf(base[static_cast<size_t>(r) * T + t0 + t]);
+    if (T <= kScoreChunk && (T & 1)) {
+        // Fast path (one chunk, odd T): the rows are one contiguous run of rows * T floats, staged as they lie
+        // (row n at n T: an odd pitch, so lane n's reads of row n fall in distinct banks); element e = lane + 64 k
+        // is a fixed offset from the lane's first, so the address arithmetic is one clamp per load.
+        const int total = rows * T;
+        const float *p = base + lane;
+        for (int k0 = 0; k0 * 64 < total; k0 += kScoreBatch) {
+            float v[kScoreBatch];
+#pragma unroll
+            for (int k = 0; k < kScoreBatch; ++k) v[k] = p[min(64 * (k0 + k), total - 1 - lane)];
+#pragma unroll
+            for (int k = 0; k < kScoreBatch; ++k)
+                if (lane + 64 * (k0 + k) < total) tile[lane + 64 * (k0 + k)] = fabsf(v[k]);
         }
         __syncthreads();
-        if (lane < rows)
-            for (int t = 0; t < C; ++t) s = __fadd_rn(s, tile[lane * stride + t]);
-        __syncthreads();
+        if (lane < rows) s = row_abs_sum(s, tile + lane * T, T);
+    } else {
+        for (int t0 = 0; t0 < T; t0 += kScoreChunk) {
+            const int C = min(kScoreChunk, T - t0);
+            const int stride = C | 1;  // odd row pitch: lane n's reads of row n fall in distinct banks
+            const int total = rows * C;  // <= 64 x 64: at most 64 elements per lane
+            // The lane's elements e = lane + 64 k, (row r, token t) with e = r C + t stepped without a division,
+            // in batches of kScoreBatch loads issued before any is used (elements past the chunk re-read its last
+            // one and are not stored).
+            const int dr = 64 / C, dt = 64 - dr * C;
+            int r = lane / C, t = lane - r * C;
+            for (int k0 = 0; k0 * 64 < total; k0 += kScoreBatch) {
+                float v[kScoreBatch];
+                int rs = r, ts = t;
+#pragma unroll
+                for (int k = 0; k < kScoreBatch; ++k) {
+                    const bool in = lane + 64 * (k0 + k) < total;
+                    v[k] = base[static_cast<size_t>(in ? r : rows - 1) * T + t0 + (in ? t : C - 1)];
+                    r += dr;
+                    t += dt;
+                    if (t >= C) {
+                        t -= C;
+                        ++r;
+                    }
+                }
+#pragma unroll
+                for (int k = 0; k < kScoreBatch; ++k) {
+                    if (lane + 64 * (k0 + k) < total) tile[rs * stride + ts] = fabsf(v[k]);
+                    rs += dr;
+                    ts += dt;
+                    if (ts >= C) {
+                        ts -= C;
+                        ++rs;
+                    }
+                }
+            }
+            __syncthreads();
+            if (lane < rows) s = row_abs_sum(s, tile + lane * stride, C);
+            __syncthreads();
+        }
     }
     if (lane < rows) {
         const int l = sl % L;

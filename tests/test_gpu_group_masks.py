@@ -49,6 +49,8 @@ CASES = [
     (5, 2, 4096, 51, 1229, 0.5),
     (4, 1, 4095, 33, 2048, 1.0),
     (2, 1, 4097, 9, 2000, 1.0),     # just past the 256-thread selection: 1024 threads
+    (2, 2, 300, 65, 100, 0.0),      # T past one 64-token chunk: the sums continue across chunks
+    (1, 1, 130, 130, 40, 0.5),
     (2, 2, 16384, 8, 4916, 0.0),
     (3, 1, 16384, 4, 8192, 2.0),
     (1, 2, 777, 64, 776, 0.0),

@@ -32,16 +32,24 @@ struct SelLds {
     int digit, need;
 };
 
+// Inclusive prefix sum over the 64 lanes of a wave (every lane active), with DPP moves instead of LDS
+// permutes: scans within rows of 16 lanes (row_shr 1, 2, 4, 8, a source outside the row adding 0), then row 0's
+// total into row 1 and row 2's into row 3 (row_bcast:15), then rows 0-1's into rows 2-3 (row_bcast:31).
+__device__ __forceinline__ int wave_incl_scan(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
+    return x;
+}
+
 // Exclusive prefix sum of v over the workgroup, in thread order.
 template <int kThreads>
 __device__ __forceinline__ int block_excl_scan(int v, SelLds<kThreads> &l) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int incl = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int u = __shfl_up(incl, off);
-        if (lane >= off) incl += u;
-    }
+    const int incl = wave_incl_scan(v);
     __syncthreads();  // wave_sum may still be read by a previous call
     if (lane == 63) l.wave_sum[wave] = incl;
     __syncthreads();
@@ -80,13 +88,8 @@ __device__ inline uint32_t select_top_k(const uint32_t (&key)[kSelPerThread], ui
 #pragma unroll
                 for (int q = 0; q < 4; ++q) b[q] += l.whist[buf][w][4 * lane + q];
             const int own = static_cast<int>(b[0] + b[1] + b[2] + b[3]);
-            int above = own;  // inclusive suffix sum over lanes j .. 63, then made exclusive
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int u = __shfl_down(above, off);
-                if (lane + off < 64) above += u;
-            }
-            above -= own;  // keys in digits above 4j + 3
+            const int incl = wave_incl_scan(own);
+            const int above = __builtin_amdgcn_readlane(incl, 63) - incl;  // keys in digits above 4j + 3
             int cum = above;
 #pragma unroll
             for (int q = 3; q >= 0; --q) {

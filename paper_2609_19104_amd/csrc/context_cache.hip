@@ -136,20 +136,11 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float *__re
 // the GEMM's LDS stage, so one K stage of a tile is one contiguous read.  swz permutes the pieces so that the
 // matrix-core fragment reads (16 rows at one piece) hit distinct LDS banks, both with 32 banks served 8 lanes a
 // cycle and with 64 banks served 16 lanes a cycle (the counters show no conflicts).
-#ifndef RM_CTX_KT
-#define RM_CTX_KT 64
-#endif
-constexpr int kStageK = RM_CTX_KT;                // K per stage and per block column
+constexpr int kStageK = 64;                       // K per GEMM stage and per block column
 constexpr int kRowBytes = kStageK * 2;
 constexpr int kBlockElems = 64 * kStageK;
-static_assert(kStageK == 64 || kStageK == 32, "stage width");
 
-__device__ __forceinline__ int ctx_swz(int r) {  // r: row mod 16
-    if constexpr (kStageK == 64)
-        return (r ^ (r >> 3)) & 7;
-    else
-        return ((r >> 1) ^ (r >> 2)) & 3;
-}
+__device__ __forceinline__ int ctx_swz(int r) { return (r ^ (r >> 3)) & 7; }  // r: row mod 16
 
 __device__ __forceinline__ size_t blocked_offset(int row, int col, int K) {  // element offset of (row, col)
     const int r = row & 63, piece = (col % kStageK) >> 3;

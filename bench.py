@@ -563,7 +563,8 @@ def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
         kern = {}
         for kk, pairs in evs.items():
             us = np.array([a.elapsed_time(b) for a, b in pairs]) * 1e3
-            kern[kk] = {"mean": float(us.mean()), "median": float(np.median(us)), "min": float(us.min())}
+            kern[kk] = {"mean": float(us.mean()), "median": float(np.median(us)), "min": float(us.min()),
+                        "p10": float(np.percentile(us, 10)), "p90": float(np.percentile(us, 90))}
     return ms, kern
 
 
@@ -757,7 +758,8 @@ def main(argv=None) -> int:
         "active_weight_bytes": setup.active_bytes,
         "warm_us_per_layer": round(warm_ms * 1e3 / setup.layer_steps, 3),
         "kernel_us": {f"{key}{suffix}": round(kern[kid][stat], 3) for kid, _, key, _ in hooks
-                      for suffix, stat in (("", "mean"), ("_median", "median"), ("_min", "min"))},
+                      for suffix, stat in (("", "mean"), ("_median", "median"), ("_min", "min"), ("_p10", "p10"),
+                                           ("_p90", "p90"))},
         "roofline": {"bound": bound, "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
                      "unit": unit, "frac": round(achieved / peak, 4),
                      "traffic": counted_traffic(args.workload, dom_key),

@@ -227,14 +227,25 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     constexpr int kTargetDownGroups = 4 * kCUs;
     if (s->wdtype == RM_BF16) {
         q.tpad = ceil_div(T, kBfTokBlock) * kBfTokBlock;
-        // Gate/up: the widest workgroup (8 * NG neurons) that still gives every compute unit one workgroup.
+        // Gate/up workgroups of 8 * NG neurons.  Measured on configs 4 and 5: one round of workgroups that fills
+        // most compute units is best (the widest NG with 150 .. 256 workgroups); a grid just past the compute
+        // units (256 .. 384 workgroups) is the worst case, since the compute units that get a second workgroup
+        // set the time, so a grid there takes the next narrower NG (more, lighter workgroups); otherwise the
+        // widest NG that still gives every compute unit one workgroup, or one group of 8 per workgroup (the
+        // direct kernel, when d allows) for short lists.
         const int k32 = ceil_div(kmax, kBfChunk) * kBfChunk;
         const bool direct_ok = s->d == 256 || s->d == 512 || s->d == 1024 || s->d == 2048;
-        q.gate_groups = direct_ok ? 1 : 2;
-        for (int ng : {8, 4, 2}) {
-            if (static_cast<long long>(B) * ceil_div(k32, 8 * ng) >= kCUs) {
-                q.gate_groups = ng;
-                break;
+        auto groups_of = [&](int ng) { return static_cast<long long>(B) * ceil_div(k32, 8 * ng); };
+        q.gate_groups = 0;
+        for (int ng : {8, 4, 2})
+            if (q.gate_groups == 0 && groups_of(ng) >= 150 && groups_of(ng) <= kCUs) q.gate_groups = ng;
+        if (q.gate_groups == 0) {
+            q.gate_groups = direct_ok ? 1 : 2;
+            for (int ng : {8, 4, 2}) {
+                if (groups_of(ng) >= kCUs) {
+                    q.gate_groups = (groups_of(ng) <= kCUs * 3 / 2 && ng > 2) ? ng / 2 : ng;
+                    break;
+                }
             }
         }
         q.kcap = ceil_div(k32, std::max(kBfChunk, 8 * q.gate_groups)) * std::max(kBfChunk, 8 * q.gate_groups);

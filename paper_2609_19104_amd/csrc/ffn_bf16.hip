@@ -846,35 +846,52 @@ int token_tiles(int T) {
 }
 
 template <int NT>
-void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
+hipError_t launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
+    hipError_t e = hipSuccess;
     const dim3 block(kGuThreads);
     const dim3 grid(p.gate_blocks * p.B);
     if (p.gate_groups == 1) {
         if (p.T <= rm::kBfTokBlock) {
             switch (p.d / 256) {  // the plan picks the direct kernel only for d = 256, 512, 1024, 2048
-                case 1: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 1, true>, grid, block, st, a); break;
-                case 2: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 2, true>, grid, block, st, a); break;
-                case 4: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 4, true>, grid, block, st, a); break;
-                default: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 8, true>, grid, block, st, a); break;
+                case 1:
+                    e = launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 1, true>, grid, block, st, a);
+                    break;
+                case 2:
+                    e = launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 2, true>, grid, block, st, a);
+                    break;
+                case 4:
+                    e = launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 4, true>, grid, block, st, a);
+                    break;
+                default:
+                    e = launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 8, true>, grid, block, st, a);
+                    break;
             }
         } else {
             switch (p.d / 256) {
-                case 1: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 1, false>, grid, block, st, a); break;
-                case 2: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 2, false>, grid, block, st, a); break;
-                case 4: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 4, false>, grid, block, st, a); break;
-                default: launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 8, false>, grid, block, st, a); break;
+                case 1:
+                    e = launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 1, false>, grid, block, st, a);
+                    break;
+                case 2:
+                    e = launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 2, false>, grid, block, st, a);
+                    break;
+                case 4:
+                    e = launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 4, false>, grid, block, st, a);
+                    break;
+                default:
+                    e = launch_timed(RM_KERNEL_GATEUP, gateup_direct_kernel<NT, 8, false>, grid, block, st, a);
+                    break;
             }
         }
-        return;
+        return e;
     }
     const int nch = (p.d + kChunkCols - 1) / kChunkCols;
     if (p.T <= rm::kBfTokBlock && p.d % kChunkCols == 0 && (nch == 1 || nch == 2 || nch == 4 || nch == 8)) {
 #define RM_PIPE(NG, TWO)                                                                                    \
     switch (nch) {                                                                                          \
-        case 1: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 1, TWO>, grid, block, st, a); break;  \
-        case 2: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 2, TWO>, grid, block, st, a); break;  \
-        case 4: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 4, TWO>, grid, block, st, a); break;  \
-        default: launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 8, TWO>, grid, block, st, a); break; \
+        case 1: e = launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 1, TWO>, grid, block, st, a); break; \
+        case 2: e = launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 2, TWO>, grid, block, st, a); break; \
+        case 4: e = launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 4, TWO>, grid, block, st, a); break; \
+        default: e = launch_timed(RM_KERNEL_GATEUP, gateup_pipe_kernel<NG, 8, TWO>, grid, block, st, a); break; \
     }
         const bool two = static_cast<long long>(p.gate_blocks) * p.B > 256;  // more workgroups than compute units
         switch (p.gate_groups) {
@@ -887,25 +904,25 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
                 break;
         }
 #undef RM_PIPE
-        return;
+        return e;
     }
 #define RM_STAGED(NG)                                                                                    \
     switch (nch) {                                                                                       \
-        case 1: launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 1>, grid, block, st, a); \
+        case 1: e = launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 1>, grid, block, st, a); \
             break;                                                                                       \
-        case 2: launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 2>, grid, block, st, a); \
+        case 2: e = launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 2>, grid, block, st, a); \
             break;                                                                                       \
-        case 3: launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 3>, grid, block, st, a); \
+        case 3: e = launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 3>, grid, block, st, a); \
             break;                                                                                       \
-        case 4: launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 4>, grid, block, st, a); \
+        case 4: e = launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 4>, grid, block, st, a); \
             break;                                                                                       \
         case 8: /* 8 chunks x 8 groups: the unrolled form spills */                                      \
             if (NG < 8)                                                                                  \
-                launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 8>, grid, block, st, a); \
+                e = launch_timed(RM_KERNEL_GATEUP, gateup_staged_unrolled_kernel<NT, NG, 8>, grid, block, st, a); \
             else                                                                                         \
-                launch_timed(RM_KERNEL_GATEUP, gateup_staged_kernel<NT, NG>, grid, block, st, a);        \
+                e = launch_timed(RM_KERNEL_GATEUP, gateup_staged_kernel<NT, NG>, grid, block, st, a);         \
             break;                                                                                       \
-        default: launch_timed(RM_KERNEL_GATEUP, gateup_staged_kernel<NT, NG>, grid, block, st, a); break; \
+        default: e = launch_timed(RM_KERNEL_GATEUP, gateup_staged_kernel<NT, NG>, grid, block, st, a); break; \
     }
     switch (p.gate_groups) {
         case 2: RM_STAGED(2) break;
@@ -913,6 +930,7 @@ void launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) {
         default: RM_STAGED(8) break;
     }
 #undef RM_STAGED
+    return e;
 }
 
 }  // namespace
@@ -942,14 +960,14 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
     a.H = reinterpret_cast<uint16_t *>(base + p.off_h);
     a.h_anchor = h_anchor;
     a.h_out = h_out;
+    hipError_t e;
     switch (token_tiles(p.T)) {
-        case 1: launch_gateup_nt<1>(p, a, st); break;
-        case 2: launch_gateup_nt<2>(p, a, st); break;
-        case 3: launch_gateup_nt<3>(p, a, st); break;
-        default: launch_gateup_nt<4>(p, a, st); break;
+        case 1: e = launch_gateup_nt<1>(p, a, st); break;
+        case 2: e = launch_gateup_nt<2>(p, a, st); break;
+        case 3: e = launch_gateup_nt<3>(p, a, st); break;
+        default: e = launch_gateup_nt<4>(p, a, st); break;
     }
-    hipError_t e = hipGetLastError();
-    return e;
+    return e != hipSuccess ? e : hipGetLastError();
 }
 
 hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
@@ -980,17 +998,18 @@ hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *i
     a.ssq = reinterpret_cast<float *>(base + p.off_ssq);
     const dim3 grid(p.ncol * p.ntt * p.B);
     const dim3 block(kDfThreads);
+    hipError_t e;
     switch (p.dn_cpw) {
-        case 1: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<1>, grid, block, st, a); break;
-        case 2: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<2>, grid, block, st, a); break;
-        case 3: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<3>, grid, block, st, a); break;
-        case 4: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<4>, grid, block, st, a); break;
-        case 5: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<5>, grid, block, st, a); break;
-        case 6: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<6>, grid, block, st, a); break;
-        case 7: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7>, grid, block, st, a); break;
-        default: launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8>, grid, block, st, a); break;
+        case 1: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<1>, grid, block, st, a); break;
+        case 2: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<2>, grid, block, st, a); break;
+        case 3: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<3>, grid, block, st, a); break;
+        case 4: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<4>, grid, block, st, a); break;
+        case 5: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<5>, grid, block, st, a); break;
+        case 6: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<6>, grid, block, st, a); break;
+        case 7: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7>, grid, block, st, a); break;
+        default: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8>, grid, block, st, a); break;
     }
-    return hipGetLastError();
+    return e != hipSuccess ? e : hipGetLastError();
 }
 
 hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *idx, void *ws, hipStream_t st) {
@@ -1010,11 +1029,12 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
     a.ncol = p.ncol;
     a.part = reinterpret_cast<float *>(base + p.off_part);
     const dim3 grid(p.ncol * p.slices * p.B), block(kDnThreads);
+    hipError_t e = hipSuccess;
 #define RM_DOWN_CPW(NT, ONE)                                                                              \
     switch (p.slice_units / kDnWaves) {                                                                  \
-        case 1: launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 1, ONE>, grid, block, st, a); break;        \
-        case 2: launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 2, ONE>, grid, block, st, a); break;        \
-        default: launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 4, ONE>, grid, block, st, a); break;       \
+        case 1: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 1, ONE>, grid, block, st, a); break;    \
+        case 2: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 2, ONE>, grid, block, st, a); break;    \
+        default: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 4, ONE>, grid, block, st, a); break;   \
     }
 #define RM_DOWN(NT)                          \
     if (p.T <= rm::kBfTokBlock) {            \
@@ -1030,8 +1050,7 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
     }
 #undef RM_DOWN
 #undef RM_DOWN_CPW
-    hipError_t e = hipGetLastError();
-    return e;
+    return e != hipSuccess ? e : hipGetLastError();
 }
 
 }  // namespace rm

@@ -163,11 +163,11 @@ hipError_t launch_gateup_f32(const Plan &p, const void *w_gate, const void *w_up
     const float *xn = reinterpret_cast<const float *>(base + p.off_xn);
     float *H = reinterpret_cast<float *>(base + p.off_h);
     const float *ssq = norm ? reinterpret_cast<const float *>(base + p.off_ssq) : nullptr;
-    launch_timed(RM_KERNEL_GATEUP, gateup_f32_kernel, dim3(p.gate_blocks, p.B), dim3(kWave), st,
-                 static_cast<const float *>(w_gate), static_cast<const float *>(w_up), xn, idx, count, p.max_count,
-                 p.d_ff, p.d, p.T, p.tpad, H, p.kcap, ssq, p.eps, h_anchor, h_out, p.act);
-    hipError_t e = hipGetLastError();
-    return e;
+    const hipError_t e =
+        launch_timed(RM_KERNEL_GATEUP, gateup_f32_kernel, dim3(p.gate_blocks, p.B), dim3(kWave), st,
+                     static_cast<const float *>(w_gate), static_cast<const float *>(w_up), xn, idx, count, p.max_count,
+                     p.d_ff, p.d, p.T, p.tpad, H, p.kcap, ssq, p.eps, h_anchor, h_out, p.act);
+    return e != hipSuccess ? e : hipGetLastError();
 }
 
 hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
@@ -175,11 +175,10 @@ hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx
     char *base = static_cast<char *>(ws);
     const float *H = reinterpret_cast<const float *>(base + p.off_h);
     float *part = reinterpret_cast<float *>(base + p.off_part);
-    launch_timed(RM_KERNEL_DOWN, down_f32_kernel, dim3(p.ncol, p.slices, p.B), dim3(kWave), st, H,
-                       static_cast<const float *>(w_down), idx, count, p.max_count, p.d_ff, p.d, p.T, p.tpad,
-                       p.kcap, p.slices, p.slice_units, part);
-    hipError_t e = hipGetLastError();
-    return e;
+    const hipError_t e = launch_timed(RM_KERNEL_DOWN, down_f32_kernel, dim3(p.ncol, p.slices, p.B), dim3(kWave), st,
+                                      H, static_cast<const float *>(w_down), idx, count, p.max_count, p.d_ff, p.d,
+                                      p.T, p.tpad, p.kcap, p.slices, p.slice_units, part);
+    return e != hipSuccess ? e : hipGetLastError();
 }
 
 }  // namespace rm

@@ -264,9 +264,9 @@ hipError_t launch_neuron_norms(const void *w_down, int d_ff, int d, int wdtype, 
 
 hipError_t launch_group_masks(const float *h, int S, int L, int d_ff, int T, const float *norms, int k,
                               float *scores, uint8_t *mask, hipStream_t st) {
-    launch_timed(RM_KERNEL_SCORES, scores_kernel, dim3((d_ff + kScoreRows - 1) / kScoreRows, S * L), dim3(64), st,
-                 h, d_ff, T, norms, L, scores, mask);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_timed(RM_KERNEL_SCORES, scores_kernel, dim3((d_ff + kScoreRows - 1) / kScoreRows, S * L),
+                                dim3(64), st, h, d_ff, T, norms, L, scores, mask);
+    if (e == hipSuccess) e = hipGetLastError();
     if (e != hipSuccess) return e;
     const float *sc = scores;
     // A workgroup of 256 threads while the layer's neurons fit (fewer waves meet at each barrier), else 1024.

@@ -47,13 +47,22 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     if (used > 0) {
         acc = ld4(P);
-        for (int s = 1; s < used; s += 16) {
-            float4 v[16];
+        if (used <= 4) {  // few slices (several samples per call): one batch of 3 loads, not 16 mostly repeated
+            float4 v[3];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) v[i] = ld4(P + min(s + i, used - 1) * stride);  // unconditional: no waits
+            for (int i = 0; i < 3; ++i) v[i] = ld4(P + min(1 + i, used - 1) * stride);  // unconditional: no waits
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-                if (s + i < used) acc = add4(acc, v[i]);
+            for (int i = 0; i < 3; ++i)
+                if (1 + i < used) acc = add4(acc, v[i]);
+        } else {
+            for (int s = 1; s < used; s += 16) {
+                float4 v[16];
+#pragma unroll
+                for (int i = 0; i < 16; ++i) v[i] = ld4(P + min(s + i, used - 1) * stride);  // unconditional
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    if (s + i < used) acc = add4(acc, v[i]);
+            }
         }
     }
     if (ya_in != nullptr || used > 0) {  // an empty list without an anchor leaves y = x bit for bit

@@ -166,3 +166,28 @@ def test_context_cache_full_size_end_to_end():
     assert np.array_equal(rows, ref_rows)
     y = _run_ffn(w, w.x, w.y_ref, ref_rows, count, count, "gelu_tanh")
     _check_update(w, w.x, w.y_ref, y, ref_rows, "gelu_tanh", sample=48)
+
+
+def _fuzz_cases(n=10, seed=2609):
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        d = int(rng.choice([64, 128, 192, 320]))
+        d_ff = int(rng.choice([128, 256, 384]))
+        n_tok = int(rng.integers(1, 600))
+        v0 = int(rng.integers(0, n_tok))
+        P = int(rng.integers(0, n_tok - v0 + 1))
+        k = int(rng.integers(0, P + 1))
+        rows_total = n_tok - P + k
+        max_rows = int(rng.integers(max(1, rows_total // 2), n_tok + 1)) if rows_total else int(rng.integers(1, 9))
+        yield d, d_ff, n_tok, v0, P, k, max_rows, str(rng.choice(["silu", "gelu_tanh"])), bool(rng.integers(0, 2))
+
+
+@pytest.mark.parametrize("d,d_ff,n_tok,v0,P,k,max_rows,act,packed", list(_fuzz_cases()))
+def test_context_ffn_random_shapes(d, d_ff, n_tok, v0, P, k, max_rows, act, packed):
+    # Seeded random shapes: widths of 1 to 5 K stages and 1 to 3 weight tiles, row counts below, at and above
+    # one 256-row tile, lists cut by max_rows, both activations, both weight layouts.
+    w = wl.context_workload(n_tok=n_tok, v0=v0, P=P, d=d, d_ff=d_ff, seed=3 + d + d_ff + n_tok)
+    rows = cc.recomputed_rows(cc.drift(w.x[v0:v0 + P], w.x_ref[v0:v0 + P]), n_tok, v0, k)
+    count = min(len(rows), max_rows)
+    y = _run_ffn(w, w.x, w.y_ref, rows, count, max_rows, act, packed=packed)
+    _check_update(w, w.x, w.y_ref, y, rows[:count], act)

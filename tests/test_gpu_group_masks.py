@@ -59,7 +59,17 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("S,L,d_ff,T,K,quantum", CASES)
+def _fuzz_cases(n=8, seed=19104):
+    # Seeded random shapes: token counts on both sides of one 64-token chunk (odd and even), widths on both sides
+    # of the 256-thread selection, K from 0 to d_ff, with and without ties.
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        d_ff = int(rng.choice([int(rng.integers(1, 300)), int(rng.integers(3000, 6000))]))
+        yield (int(rng.integers(1, 6)), int(rng.integers(1, 4)), d_ff, int(rng.integers(1, 140)),
+               int(rng.integers(0, d_ff + 1)), float(rng.choice([0.0, 0.5])))
+
+
+@pytest.mark.parametrize("S,L,d_ff,T,K,quantum", CASES + list(_fuzz_cases()))
 def test_group_masks_bit_exact(S, L, d_ff, T, K, quantum):
     h = wl.activation_like(92, (S, L, d_ff, T), d_ff, T, quantum=quantum)
     norms = wl.positive_norms(92, (L, d_ff), d_ff)

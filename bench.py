@@ -513,6 +513,27 @@ class GroupMaskSetup:
     def step(self, i: int) -> None:
         self.rm.rm_group_masks(self.hs[i % self.rotate], self.norms, self.k, self.scores, self.mask)
 
+    def coverage(self) -> dict:
+        """Section 3.4's coverage (share of a step's summed Eq. 1 contribution inside a mask) of the group's shared
+        mask and of each step's own top-K mask (rm_group_masks over that step alone), over the 5 steps x 18
+        layers.  Untimed; the ratio is a property of the synthetic activations, not of a trained model."""
+        import torch
+        h = self.hs[0]
+        self.rm.rm_group_masks(h, self.norms, self.k, self.scores, self.mask)
+        sc = self.scores.double()
+        tot = sc.sum(-1)
+        shared = (sc * (self.mask != 0)).sum(-1) / tot
+        own = torch.empty_like(shared)
+        s_scores = torch.empty((1, self.L, self.d_ff), dtype=torch.float32, device=h.device)
+        s_mask = torch.empty_like(self.mask)
+        for s in range(self.STEPS):
+            self.rm.rm_group_masks(h[s:s + 1], self.norms, self.k, s_scores, s_mask)
+            own[s] = (sc[s] * (s_mask != 0)).sum(-1) / tot[s]
+        return {"k": self.k, "step_specific_mean": round(own.mean().item(), 4),
+                "group_shared_mean": round(shared.mean().item(), 4),
+                "group_shared_min": round(shared.min().item(), 4),
+                "shared_over_specific_min": round((shared / own).min().item(), 4)}
+
     @property
     def active_bytes(self) -> int:  # the activations read (the norms, scores and masks are < 2% more)
         return self.h_bytes
@@ -770,6 +791,8 @@ def main(argv=None) -> int:
     if isinstance(setup, StackSetup5):
         out["per_sample_weight_bytes"] = setup.per_sample_bytes
         out["per_sample_value"] = round(setup.per_sample_bytes / (ms * 1e-3) / 1e9, 2)
+    if isinstance(setup, GroupMaskSetup):
+        out["coverage"] = setup.coverage()
     if not args.no_cpu_baseline and isinstance(setup, Setup):
         out["cpu_baseline"] = cpu_baseline(setup, args.cpu_seconds)
     print(json.dumps(out))

@@ -119,3 +119,24 @@ def test_group_masks_from_identity_list_anchor():
         for s in range(S):
             cand[np.argsort(-sc[s, l], kind="stable")[:K]] = True
         assert np.all(cand[m[l] != 0])
+
+
+@pytest.mark.parametrize("S,L,d_ff,T,K", [(5, 2, 4096, 51, 1229), (3, 1, 1000, 20, 100)])
+def test_step_specific_against_group_shared_coverage(S, L, d_ff, T, K):
+    # Section 5 shares one mask across a group; section 3.4's coverage measures what a mask keeps of a step's
+    # contribution.  Each step alone (S = 1) gives its own top-K mask; the group call gives the shared one.  Both
+    # masks match the oracle's bit for bit, so their coverages do, and the shared mask never covers more than
+    # the step's own.
+    h = wl.activation_like(94, (S, L, d_ff, T), d_ff, T)
+    norms = wl.positive_norms(94, (L, d_ff), d_ff)
+    scores, group = _run(h, norms, K)
+    for s in range(S):
+        _, own = _run(np.ascontiguousarray(h[s:s + 1]), norms, K)
+        for l in range(L):
+            c = gm.contribution_scores(h[s, l], norms[l])
+            ref_own = gm.top_k(c, K).astype(np.uint8)
+            ref_group = gm.group_masks(h[:, l:l + 1], norms[l:l + 1], K)[0]
+            assert np.array_equal(own[l], ref_own) and np.array_equal(group[l], ref_group)
+            cov_own, cov_group = gm.coverage(scores[s, l], own[l]), gm.coverage(scores[s, l], group[l])
+            assert cov_own == gm.coverage(c, ref_own) and cov_group == gm.coverage(c, ref_group)
+            assert 0.0 < cov_group <= cov_own <= 1.0

@@ -97,3 +97,24 @@ def test_group_mask_special_cases():
     for x in hs:
         cand |= gm.top_k(gm.contribution_scores(x, norms), 17)
     assert np.all(cand[m != 0])
+
+
+def test_coverage_pins():
+    # Section 3.4's coverage: the share of a step's summed contribution held by the masked neurons.  A full mask
+    # holds all of it, an empty one none, and a single neuron its own share.
+    c = np.array([4.0, 1.0, 0.0, 3.0], dtype=np.float32)
+    assert gm.coverage(c, np.ones(4, np.uint8)) == 1.0
+    assert gm.coverage(c, np.zeros(4, np.uint8)) == 0.0
+    assert gm.coverage(c, np.array([0, 0, 0, 1], np.uint8)) == 3.0 / 8.0
+    assert gm.coverage(np.zeros(3, np.float32), np.ones(3, np.uint8)) == 0.0
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_step_top_k_has_the_best_coverage_of_any_k_subset(seed):
+    # Brute force on 9 neurons: no K-subset covers more of a step than that step's own top K, so a mask shared
+    # by a group can only match or lose coverage against the step-specific one.
+    rng = np.random.default_rng(seed)
+    c = rng.exponential(size=9).astype(np.float32)
+    k = 3
+    best = max(gm.coverage(c, np.isin(np.arange(9), s)) for s in itertools.combinations(range(9), k))
+    assert gm.coverage(c, gm.top_k(c, k)) == pytest.approx(best, rel=1e-12)

@@ -115,6 +115,7 @@ rm_status rm_workspace_size(const rm_ffn_shape *s, int32_t B, int32_t T, int32_t
  *   count:  int32 [B], each in [0, max_count]; read on the device, so it may be produced by an earlier kernel.
  *   max_count: host-side upper bound of count[], in [0, d_ff]; sizes the launch and the workspace.
  *   ws, ws_bytes: workspace of at least rm_workspace_size(s, B, T, max_count) bytes.
+ * The workspace must not overlap x or y, nor may idx or count overlap y or the workspace (RM_ERR_INVALID_ARG).
  * count[b] == 0 gives y[b] == x[b] bit for bit. */
 rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
                               const float *x, float *y, const int32_t *idx, const int32_t *count,
@@ -234,8 +235,8 @@ rm_status rm_context_workspace_size(const rm_ffn_shape *s, int32_t n_tok, int32_
  *   max_rows: host bound of count, in [1, n_tok]; sizes the launch and the workspace.
  *   y:        float32 [n_tok][d], in/out: the reference outputs on entry.
  *   ws, ws_bytes: at least rm_context_workspace_size(s, n_tok, max_rows) bytes, 16-byte aligned.
- * x, y and the workspace must not overlap.  Errors: RM_ERR_INVALID_ARG, RM_ERR_SHAPE, RM_ERR_DTYPE, RM_ERR_ALIGN,
- * RM_ERR_WORKSPACE, RM_ERR_HIP. */
+ * x, y and the workspace must not overlap, nor may the weights, rows or count overlap y or the workspace.
+ * Errors: RM_ERR_INVALID_ARG, RM_ERR_SHAPE, RM_ERR_DTYPE, RM_ERR_ALIGN, RM_ERR_WORKSPACE, RM_ERR_HIP. */
 rm_status rm_context_ffn(const rm_ffn_shape *s, const void *w_gate, const void *w_up, const void *w_down_t,
                          int32_t n_tok, const float *x, const int32_t *rows, const int32_t *count, int32_t max_rows,
                          float *y, void *ws, size_t ws_bytes, void *stream);

@@ -95,6 +95,18 @@ rm_status check_call(const rm_ffn_shape *s, int B, int T, const float *x, float 
     return RM_OK;
 }
 
+// The lists are read while y and the workspace are written: idx ([lists][B][d_ff]) and count ([lists][B]) must
+// not overlap either (lists = 1 for a layer, L for a stack).  Checked last, after the per-argument checks.
+rm_status check_lists(const rm_ffn_shape *s, int lists, int B, int T, const float *y, const int32_t *idx,
+                      const int32_t *count, const void *ws, size_t ws_bytes) {
+    const size_t act_bytes = static_cast<size_t>(B) * T * s->d * sizeof(float);
+    const size_t ib = static_cast<size_t>(lists) * B * s->d_ff * 4, cb = static_cast<size_t>(lists) * B * 4;
+    if (ranges_overlap(idx, ib, y, act_bytes) || ranges_overlap(idx, ib, ws, ws_bytes) ||
+        ranges_overlap(count, cb, y, act_bytes) || ranges_overlap(count, cb, ws, ws_bytes))
+        return fail(RM_ERR_INVALID_ARG, "idx or count overlaps y or the workspace");
+    return RM_OK;
+}
+
 rm_status hip_fail(hipError_t e, const char *what) {
     return fail(RM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
@@ -357,6 +369,8 @@ RM_EXPORT rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_laye
     if (st != RM_OK) return st;
     st = check_gates(w, 1, B, T, s->d, y);
     if (st != RM_OK) return st;
+    st = check_lists(s, 1, B, T, y, idx, count, ws, p.total);
+    if (st != RM_OK) return st;
     st = run_layers(p, w, 1, x, y, idx, count, 0, 0, ws, static_cast<hipStream_t>(stream));
     return st == RM_OK ? ok() : st;
 }
@@ -375,6 +389,8 @@ RM_EXPORT rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
         if (st != RM_OK) return st;
     }
     st = check_gates(w, L, B, T, s->d, y);
+    if (st != RM_OK) return st;
+    st = check_lists(s, L, B, T, y, idx, count, ws, p.total);
     if (st != RM_OK) return st;
     st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
                     static_cast<hipStream_t>(stream));
@@ -470,6 +486,8 @@ RM_EXPORT rm_status rm_anchor_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
     if (st != RM_OK) return st;
     st = check_anchor_buffers(s, w, L, B, T, x, y, max_count, y_anchor, h_anchor, ws, ws_bytes);
     if (st != RM_OK) return st;
+    st = check_lists(s, L, B, T, y, idx, count, ws, std::max(p.total, q.total));
+    if (st != RM_OK) return st;
     // The capture reads the dense layers' FFN input and sums of squares from the dense workspace layout; it
     // writes nothing else there.
     q.off_xn = p.off_xn;
@@ -504,6 +522,8 @@ RM_EXPORT rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer
     at.ya_in = y_anchor;
     at.ha_in = max_count > 0 ? h_anchor : nullptr;
     at.h_stride = static_cast<size_t>(B) * max_count * T;
+    st = check_lists(s, L, B, T, y, idx, count, ws, p.total);
+    if (st != RM_OK) return st;
     st = run_layers(p, w, L, x, y, idx, count, static_cast<size_t>(B) * s->d_ff, B, ws,
                     static_cast<hipStream_t>(stream), at);
     return st == RM_OK ? ok() : st;
@@ -632,6 +652,13 @@ static rm_status context_ffn(const rm_ffn_shape *s, const void *w_gate, const vo
     if (ranges_overlap(x, act_bytes, y, act_bytes) || ranges_overlap(ws, p.total, x, act_bytes) ||
         ranges_overlap(ws, p.total, y, act_bytes))
         return fail(RM_ERR_INVALID_ARG, "x, y and the workspace must not overlap");
+    // What the launches only read (the weights, the row list and its count) must not overlap what they write.
+    const size_t mb = static_cast<size_t>(s->d) * s->d_ff * 2;
+    const void *ins[5] = {w_gate, w_up, w_down_t, rows, count};
+    const size_t inb[5] = {mb, mb, mb, static_cast<size_t>(max_rows) * 4, 4};
+    for (int i = 0; i < 5; ++i)
+        if (ranges_overlap(ins[i], inb[i], y, act_bytes) || ranges_overlap(ins[i], inb[i], ws, p.total))
+            return fail(RM_ERR_INVALID_ARG, "the weights, rows and count must not overlap y or the workspace");
     const hipError_t e = rm::launch_context_ffn(p, w_gate, w_up, w_down_t, blocked, x, rows, count, y, ws,
                                                 static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "context FFN launch");

@@ -256,6 +256,15 @@ def test_context_calls_validate(lib):
                FAKE * 4096, 1 << 30, None) == rm.RM_ERR_INVALID_ARG  # y is x
     assert ffn(ctypes.byref(s), None, FAKE, FAKE, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 512,
                FAKE * 4096, 1 << 30, None) == rm.RM_ERR_INVALID_ARG
+    # Inputs the launches only read must not overlap what they write (y, the workspace).
+    W, mb = 1 << 36, 2048 * 16384 * 2
+    y, ws = FAKE * 512, 1 << 34
+    for wg, wu, wd, rows, cnt in [(W, W + mb, W + 2 * mb, y + 64, FAKE * 256),      # rows inside y
+                                  (W, W + mb, W + 2 * mb, FAKE * 128, ws + 8),      # count inside the workspace
+                                  (W, W + mb, ws + 4096, FAKE * 128, FAKE * 256),   # w_down_t inside the workspace
+                                  (y - 16, W + mb, W + 2 * mb, FAKE * 128, FAKE * 256)]:  # w_gate over y
+        assert ffn(ctypes.byref(s), wg, wu, wd, 850, FAKE * 64, rows, cnt, 390, y, ws, 1 << 30,
+                   None) == rm.RM_ERR_INVALID_ARG
 
 
 def test_context_pack_calls_validate(lib):
@@ -283,3 +292,20 @@ def test_context_pack_calls_validate(lib):
               None) == rm.RM_ERR_WORKSPACE
     assert fp(ctypes.byref(odd), W, 850, FAKE * 64, FAKE * 128, FAKE * 256, 390, FAKE * 512, FAKE * 4096, 1 << 30,
               None) == rm.RM_ERR_SHAPE
+
+
+def test_lists_must_not_overlap_what_the_layer_writes(lib):
+    # idx and count are read while y and the workspace are written; overlapping them is rejected before any
+    # launch (every pointer below fails that check, so nothing is dereferenced).
+    s = rm.FfnShape(1024, 4096, rm.RM_BF16, 1e-6, rm.RM_ACT_SILU)
+    x, y, ws = FAKE * 64, FAKE * 128, 1 << 34
+    w = rm.LayerWeights(1 << 36, (1 << 36) + (1 << 24), (1 << 36) + (1 << 25), None, None)
+    layer = lib.rm_sparse_ffn_layer
+    for idx, cnt in [(y + 256, FAKE), (ws + 1024, FAKE), (FAKE, y + 4), (FAKE, ws)]:
+        assert layer(ctypes.byref(s), ctypes.byref(w), 1, 51, x, y, idx, cnt, 1229, ws, 1 << 30,
+                     None) == rm.RM_ERR_INVALID_ARG
+    # A stack's lists span L blocks: layer 2's block reaching into y is caught too.
+    ws_arr = (rm.LayerWeights * 3)(w, w, w)
+    idx = y - 2 * 4096 * 4 - 64
+    assert lib.rm_sparse_ffn_stack(ctypes.byref(s), ws_arr, 3, 1, 51, x, y, idx, FAKE, 1229, ws, 1 << 30,
+                                   None) == rm.RM_ERR_INVALID_ARG

@@ -760,6 +760,17 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
 #pragma unroll
     for (int k = 0; k < CPW; ++k)  // chunk-major H: 16 tokens x 64 bytes, one contiguous kilobyte
         cb[k].a[0] = load16(Hb + (static_cast<size_t>(chunk_of(k)) * a.tpad + t0 + nn) * rm::kBfChunk + grp * 8);
+    // The epilogue's inputs depend on nothing computed here, so they are loaded now, behind the H tiles, and
+    // the epilogue does not wait for memory a second time.  Wave w < 4 finishes token t0 + 4 grp + w of the
+    // tile (waves 4-7 load the same rows and drop them).
+    const int t_ep = t0 + grp * 4 + (wave & 3);
+    const size_t ro = (static_cast<size_t>(b) * a.T + min(t_ep, a.T - 1)) * a.d + col;
+    const float4 x_in = *reinterpret_cast<const float4 *>(a.x + ro);
+    float4 ya_in = make_float4(0.f, 0.f, 0.f, 0.f), gate = ya_in, g_next = ya_in;
+    if (a.ya_in != nullptr) ya_in = *reinterpret_cast<const float4 *>(a.ya_in + ro);
+    if (a.out_gate != nullptr)
+        gate = *reinterpret_cast<const float4 *>(a.out_gate + static_cast<size_t>(b) * a.d + col);
+    if (a.g_next != nullptr) g_next = *reinterpret_cast<const float4 *>(a.g_next + col);
     __builtin_amdgcn_sched_barrier(0);  // then the H tiles, before the wait for the indices
 #pragma unroll
     for (int i = 0; i < kIdxPerThread; ++i) {
@@ -801,22 +812,17 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
 #pragma unroll
         for (int w = 1; w < rm::kDfWaves; ++w) v[c] += red[w][c][lane][i];
     }
-    const int t = t0 + grp * 4 + i;
+    const int t = t_ep;  // = t0 + 4 grp + i
     const bool live = t < a.T;
-    const size_t ro = (static_cast<size_t>(b) * a.T + min(t, a.T - 1)) * a.d + col;
     const float4 acc4 = make_float4(v[0], v[1], v[2], v[3]);
-    float4 out = *reinterpret_cast<const float4 *>(a.x + ro);
+    float4 out = x_in;
     cnt = cnt < 0 ? 0 : (cnt > a.max_count ? a.max_count : cnt);
     if (a.ya_in != nullptr || cnt > 0) {  // an empty list without an anchor leaves y = x bit for bit
         float4 f = acc4;
-        if (a.ya_in != nullptr) {  // Eq. 4: the FFN output is y_a + (h - h_a) W_down
-            const float4 ya = *reinterpret_cast<const float4 *>(a.ya_in + ro);
-            f = make_float4(ya.x + acc4.x, ya.y + acc4.y, ya.z + acc4.z, ya.w + acc4.w);
-        }
-        if (a.out_gate != nullptr) {  // the adaptive output gate, before the residual
-            const float4 g = *reinterpret_cast<const float4 *>(a.out_gate + static_cast<size_t>(b) * a.d + col);
-            f = make_float4(f.x * g.x, f.y * g.y, f.z * g.z, f.w * g.w);
-        }
+        if (a.ya_in != nullptr)  // Eq. 4: the FFN output is y_a + (h - h_a) W_down
+            f = make_float4(ya_in.x + acc4.x, ya_in.y + acc4.y, ya_in.z + acc4.z, ya_in.w + acc4.w);
+        if (a.out_gate != nullptr)  // the adaptive output gate, before the residual
+            f = make_float4(f.x * gate.x, f.y * gate.y, f.z * gate.z, f.w * gate.w);
         out = make_float4(out.x + f.x, out.y + f.y, out.z + f.z, out.w + f.w);
     }
     const bool st = live && colok;
@@ -829,8 +835,7 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
         const float ss = rm_ssq64(out, colok);
         const int row = b * a.T + t;
         if (nn == 0 && live) a.ssq[static_cast<size_t>(row) * rm::ssq_stride(a.d) + ct] = ss;
-        const float4 g = *reinterpret_cast<const float4 *>(a.g_next + col);
-        out = make_float4(out.x * g.x, out.y * g.y, out.z * g.z, out.w * g.w);
+        out = make_float4(out.x * g_next.x, out.y * g_next.y, out.z * g_next.z, out.w * g_next.w);
     }
     if (st) {
         uint2 packed;

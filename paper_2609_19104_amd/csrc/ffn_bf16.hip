@@ -194,6 +194,19 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
     };
     rm_u32x4 xv[G::kSubs][G::kPieces];
     load_x(0, xv);
+    // One token block (kOneBlock) with a norm: wave 0 loads the partial sums of squares of tokens 0..63 (4 SPW
+    // per row, d = 256 SPW) with the input, so that forming the norm factors after the products waits for no
+    // memory.  They are added in the order rm_token_rnorm adds them.
+    const bool pre_norm = kOneBlock && a.ssq != nullptr;
+    float4 ssq_v[SPW];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) ssq_v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (pre_norm && __builtin_amdgcn_readfirstlane(wave) == 0) {
+        const float4 *p = reinterpret_cast<const float4 *>(
+            a.ssq + static_cast<size_t>(b * a.T + min(lane, a.T - 1)) * rm::ssq_stride(a.d));
+#pragma unroll
+        for (int i = 0; i < SPW; ++i) ssq_v[i] = p[i];
+    }
     __builtin_amdgcn_sched_barrier(0);  // the input loads go out before the wait for the index
     rm_u32x4 w[SPW];
     {
@@ -228,7 +241,21 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
         // The summed tile goes into the wave's region (its fragment reads precede these writes).
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) *reinterpret_cast<rm_f32x4 *>(region + (tt * 64 + lane) * 16) = acc[tt];
-        load_rnorm(a, b, t0, rn);
+        if (pre_norm) {
+            if (wave == 0) {
+                float ss = 0.0f;
+#pragma unroll
+                for (int i = 0; i < SPW; ++i) {
+                    ss += ssq_v[i].x;
+                    ss += ssq_v[i].y;
+                    ss += ssq_v[i].z;
+                    ss += ssq_v[i].w;
+                }
+                rn[lane] = lane < a.T ? rm_rnorm_from_ssq(ss, a.d, a.eps) : 1.0f;
+            }
+        } else {
+            load_rnorm(a, b, t0, rn);
+        }
         __syncthreads();
         gu_store_h<NT>(a, Hb, b, red, kGuWaves, t0, slot0, cnt, rn);
         t0 += rm::kBfTokBlock;

@@ -203,6 +203,11 @@ __device__ __forceinline__ uint32_t rm_f32_to_bf16_bits(float f) {
 
 __device__ __forceinline__ float rm_bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
+// 1 / sqrt(mean of squares + eps) from a row's summed squares.
+__device__ __forceinline__ float rm_rnorm_from_ssq(float s, int d, float eps) {
+    return 1.0f / sqrtf(s / static_cast<float>(d) + eps);
+}
+
 // RMSNorm factor of token row `row` (= b * T + t): 1 / sqrt(mean of squares + eps), from the row's partial sums
 // of squares by 256-column block, added in block order.
 __device__ __forceinline__ float rm_token_rnorm(const float *ssq, int row, int d, float eps) {
@@ -223,7 +228,7 @@ __device__ __forceinline__ float rm_token_rnorm(const float *ssq, int row, int d
             if (k + 3 < n) s += v[i].w;
         }
     }
-    return 1.0f / sqrtf(s / static_cast<float>(d) + eps);
+    return rm_rnorm_from_ssq(s, d, eps);
 }
 
 // Sum of squares of 4 columns (one lane's float4), then the sum over the 16 lanes of a lane group (lanes

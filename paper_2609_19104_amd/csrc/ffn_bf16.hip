@@ -537,6 +537,20 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
     };
 #pragma unroll
     for (int c = 0; c < P; ++c) load_chunk(c);
+    // With a norm, wave 0 loads the partial sums of squares of tokens 0..63 (4 NCH per row, d = NCH chunks of
+    // 256 columns) behind the first chunks, so that forming the norm factors after the products waits for no
+    // memory.  They are added in the order rm_token_rnorm adds them.  Where those registers would spill (d =
+    // 2048, or 8 groups two to a compute unit at d = 1024) the factors are loaded after the products instead.
+    constexpr bool kPreNorm = NCH <= 2 || (NCH == 4 && !(NG == 8 && kTwoPerCU));
+    float4 ssq_v[NCH];
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) ssq_v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (kPreNorm && a.ssq != nullptr && __builtin_amdgcn_readfirstlane(wave) == 0) {
+        const float4 *p = reinterpret_cast<const float4 *>(
+            a.ssq + static_cast<size_t>(b * a.T + min(lane, a.T - 1)) * rm::ssq_stride(a.d));
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) ssq_v[i] = p[i];
+    }
 
     rm_f32x4 acc[NT];
 #pragma unroll
@@ -560,7 +574,23 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
             }
         if (c + P < NCH) load_chunk(c + P);
     }
-    load_rnorm(a, b, 0, rn);
+    if (!kPreNorm) {
+        load_rnorm(a, b, 0, rn);
+    } else if (wave == 0) {
+        float r = 1.0f;
+        if (a.ssq != nullptr && lane < a.T) {
+            float ss = 0.0f;
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                ss += ssq_v[i].x;
+                ss += ssq_v[i].y;
+                ss += ssq_v[i].z;
+                ss += ssq_v[i].w;
+            }
+            r = rm_rnorm_from_ssq(ss, a.d, a.eps);
+        }
+        rn[lane] = r;
+    }
     __syncthreads();  // every wave is done with the input tiles before they hold the reduction
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) red(g, part, tt, lane) = acc[tt];

@@ -110,8 +110,9 @@ WORKLOADS = {
 STEP_TEXT = {
     "c2": "rm_masked_ffn_layer (mask compaction + layer), replayed from HIP graphs",
     "c4": "rm_masked_ffn_layer (mask compaction + layer), replayed from HIP graphs",
-    "c3": "one 10-step sequence: 18 rm_dense_ffn_ref, then 5 rm_masked_ffn_stack (L=18, compacting the refreshed "
-          "18 masks) alternating with 4 rm_sparse_ffn_stack (L=18), replayed from HIP graphs; "
+    "c3": "one 10-step sequence: rm_sparse_ffn_stack (L=18) over identity lists (the dense step), then 5 "
+          "rm_masked_ffn_stack (L=18, compacting the refreshed 18 masks) alternating with 4 rm_sparse_ffn_stack "
+          "(L=18), replayed from HIP graphs; "
           "us_per_layer = sequence time / 180",
     "c3-eq4": "one 10-step sequence: per group (anchors 0 and 5) rm_mask_compact (18 masks) + "
               "rm_anchor_ffn_stack (L=18) + 4 rm_delta_ffn_stack (L=18), replayed from HIP graphs; "
@@ -252,11 +253,11 @@ class StackSetup5:
 
 
 class StackSetup3:
-    """Config 3: one step is a whole 10-step denoising sequence through the 18-layer stack: step 0 dense
-    (rm_dense_ffn_ref layer by layer), steps 1..9 sparse, with the 18 per-layer masks compacted at steps 1, 3,
-    5, 7, 9 (rm_masked_ffn_stack) and their lists reused by the following step (rm_sparse_ffn_stack).  The masks
-    are the top-30% neurons by mean |SiLU(g) u| of a float32 dense pass on the previous step's input (input
-    setup, on the GPU)."""
+    """Config 3: one step is a whole 10-step denoising sequence through the 18-layer stack: step 0 dense (one
+    rm_sparse_ffn_stack over identity lists, every neuron in order), steps 1..9 sparse, with the 18 per-layer
+    masks compacted at steps 1, 3, 5, 7, 9 (rm_masked_ffn_stack) and their lists reused by the following step
+    (rm_sparse_ffn_stack).  The masks are the top-30% neurons by mean |SiLU(g) u| of a float32 dense pass on the
+    previous step's input (input setup, on the GPU)."""
 
     def __init__(self, key: str, device, cold: bool = True):
         import torch
@@ -290,12 +291,13 @@ class StackSetup3:
         self.y = torch.empty_like(self.xs[0])
         self.ws = rm.workspace(self.d, self.d_ff, rm.RM_BF16, 1, self.T, self.k, device=device)
         self.ws_dense = rm.workspace(self.d, self.d_ff, rm.RM_BF16, 1, self.T, self.d_ff, device=device)
+        self.ident = torch.arange(self.d_ff, dtype=torch.int32, device=device).repeat(self.L, 1).contiguous()
+        self.ident_cnt = torch.full((self.L,), self.d_ff, dtype=torch.int32, device=device)
         self.layer_steps = self.steps * self.L
 
     def step(self, i: int) -> None:
         rm, layers = self.rm, self.layer_copies[i % self.rotate]
-        for l in range(self.L):
-            rm.rm_dense_ffn_ref(self.xs[0] if l == 0 else self.y, self.y, layers[l], self.ws_dense)
+        rm.rm_sparse_ffn_stack(self.xs[0], self.y, layers, self.ident, self.ident_cnt, self.d_ff, self.ws_dense)
         for s in range(1, self.steps):
             r = (s - 1) // 2
             if s in self.refresh:

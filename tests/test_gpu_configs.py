@@ -66,6 +66,10 @@ def test_config3_stack_schedule():
             for lw in lws:
                 y = run_dense(lw, y)
             ref = oracle.ffn_stack(x[0], layers64, [np.ones(w.d_ff)] * w.L)
+            # The same dense step as one stack call over identity lists (the form the benchmark times).
+            ident = torch.arange(w.d_ff, dtype=torch.int32, device="cuda").repeat(w.L, 1).contiguous()
+            full = torch.full((w.L,), w.d_ff, dtype=torch.int32, device="cuda")
+            _check(run_stack(lws, x, ident, full, w.d_ff)[0], ref, x[0], TOL_BF16, "config 3 dense step as a stack")
         else:
             if s in w.refresh_steps:
                 masks = oracle.stack_masks_from_dense(w.x_steps[s - 1][0], layers64, w.k)

@@ -765,9 +765,9 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
 }
 
 // Down projection with the epilogue fused, for lists of at most kDfMaxChunks chunks.  Workgroup: one column
-// tile of 64 columns, one tile of 16 tokens, one sample; its 8 waves take the list's chunks in turn (chunk
-// wave + 8 k, k < CPW: every load is issued before the first product), each keeping a 16 x 64 fp32 tile, and
-// the 8 tiles are summed in wave order through LDS.  Then y = x + acc (x + (y_a + acc) for Eq. 4), y_a = acc on
+// tile of 64 columns, NT tiles of 16 tokens, one sample; its 8 waves take the list's chunks in turn (chunk
+// wave + 8 k, k < CPW: every load is issued before the first product), each keeping NT 16 x 64 fp32 tiles, and
+// the 8 waves' tiles are summed in wave order through LDS, one token tile at a time.  Then y = x + acc (x + (y_a + acc) for Eq. 4), y_a = acc on
 // an anchor step, and inside a stack the next layer's input xn = y * g in bf16 with the row's partial sum of
 // squares for this 64-column block.  No partials leave the workgroup, so no epilogue launch follows.
 struct DfArgs {
@@ -784,7 +784,7 @@ struct DfArgs {
     float *ssq;
 };
 
-template <int CPW>
+template <int CPW, int NT>
 __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     const int q = xcd_logical(blockIdx.x, gridDim.x);  // = (sample * ncol + column tile) * ntt + token tile
     const int tt = q % a.ntt;
@@ -799,7 +799,7 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     const bool colok = colw < a.d;
     const int col = min(colw, a.d - 4);  // columns past d re-read column d-4; those outputs are not stored
     const int nchunks = a.kcap / rm::kBfChunk;
-    const int t0 = tt * 16;
+    const int t0 = tt * 16 * NT;  // NT tiles of 16 tokens
     const uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
 
     // The list's neuron indices (clamped into [0, d_ff)) are staged once in LDS.
@@ -813,18 +813,29 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     __builtin_amdgcn_sched_barrier(0);  // the index loads go out first
 
     auto chunk_of = [&](int k) { return min(wave + k * rm::kDfWaves, nchunks - 1); };
-    DnChunk<1> cb[CPW];
+    DnChunk<NT> cb[CPW];
 #pragma unroll
-    for (int k = 0; k < CPW; ++k)  // chunk-major H: 16 tokens x 64 bytes, one contiguous kilobyte
-        cb[k].a[0] = load16(Hb + (static_cast<size_t>(chunk_of(k)) * a.tpad + t0 + nn) * rm::kBfChunk + grp * 8);
+    for (int k = 0; k < CPW; ++k)  // chunk-major H: 16 tokens x 64 bytes, one contiguous kilobyte per tile
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+            cb[k].a[j] = load16(Hb + (static_cast<size_t>(chunk_of(k)) * a.tpad + t0 + j * 16 + nn) * rm::kBfChunk +
+                                grp * 8);
     // The epilogue's inputs depend on nothing computed here, so they are loaded now, behind the H tiles, and
-    // the epilogue does not wait for memory a second time.  Wave w < 4 finishes token t0 + 4 grp + w of the
-    // tile (waves 4-7 load the same rows and drop them).
-    const int t_ep = t0 + grp * 4 + (wave & 3);
-    const size_t ro = (static_cast<size_t>(b) * a.T + min(t_ep, a.T - 1)) * a.d + col;
-    const float4 x_in = *reinterpret_cast<const float4 *>(a.x + ro);
-    float4 ya_in = make_float4(0.f, 0.f, 0.f, 0.f), gate = ya_in, g_next = ya_in;
-    if (a.ya_in != nullptr) ya_in = *reinterpret_cast<const float4 *>(a.ya_in + ro);
+    // the epilogue does not wait for memory a second time.  Wave w < 4 finishes token t0 + 16 j + 4 grp + w of
+    // tile j (waves 4-7 load the same rows and drop them).
+    const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    size_t ro[NT];
+    float4 x_in[NT], ya_in[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        ro[j] = (static_cast<size_t>(b) * a.T + min(t0 + j * 16 + grp * 4 + (wave & 3), a.T - 1)) * a.d + col;
+        x_in[j] = *reinterpret_cast<const float4 *>(a.x + ro[j]);
+        ya_in[j] = zero4;
+    }
+    float4 gate = zero4, g_next = zero4;
+    if (a.ya_in != nullptr)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) ya_in[j] = *reinterpret_cast<const float4 *>(a.ya_in + ro[j]);
     if (a.out_gate != nullptr)
         gate = *reinterpret_cast<const float4 *>(a.out_gate + static_cast<size_t>(b) * a.d + col);
     if (a.g_next != nullptr) g_next = *reinterpret_cast<const float4 *>(a.g_next + col);
@@ -846,59 +857,64 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     }
     __builtin_amdgcn_sched_barrier(0);
 
-    rm_f32x4 acc[1][4];
+    rm_f32x4 acc[NT][4];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[0][c] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[j][c] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int k = 0; k < CPW; ++k)
         if (wave + k * rm::kDfWaves < nchunks) dn_mma(cb[k], acc);
 
     __shared__ rm_f32x4 red[rm::kDfWaves][4][64];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) red[wave][c][lane] = acc[0][c];
-    __syncthreads();
-    if (wave >= 4) return;
-
-    // Wave i finishes token 4 * grp + i of the tile (lane L, register i of a tile: token 4*(L/16)+i, physical
-    // column 4*(L%16) + q of call q): the 8 waves' sums in wave order.
-    const int i = wave;
-    float v[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        v[c] = red[0][c][lane][i];
-#pragma unroll
-        for (int w = 1; w < rm::kDfWaves; ++w) v[c] += red[w][c][lane][i];
-    }
-    const int t = t_ep;  // = t0 + 4 grp + i
-    const bool live = t < a.T;
-    const float4 acc4 = make_float4(v[0], v[1], v[2], v[3]);
-    float4 out = x_in;
     cnt = cnt < 0 ? 0 : (cnt > a.max_count ? a.max_count : cnt);
-    if (a.ya_in != nullptr || cnt > 0) {  // an empty list without an anchor leaves y = x bit for bit
-        float4 f = acc4;
-        if (a.ya_in != nullptr)  // Eq. 4: the FFN output is y_a + (h - h_a) W_down
-            f = make_float4(ya_in.x + acc4.x, ya_in.y + acc4.y, ya_in.z + acc4.z, ya_in.w + acc4.w);
-        if (a.out_gate != nullptr)  // the adaptive output gate, before the residual
-            f = make_float4(f.x * gate.x, f.y * gate.y, f.z * gate.z, f.w * gate.w);
-        out = make_float4(out.x + f.x, out.y + f.y, out.z + f.z, out.w + f.w);
-    }
-    const bool st = live && colok;
-    if (st) {
-        *reinterpret_cast<float4 *>(a.y + ro) = out;
-        if (a.ya_out != nullptr) *reinterpret_cast<float4 *>(a.ya_out + ro) = acc4;
-    }
-    if (a.xn_next == nullptr) return;
-    if (a.g_next != nullptr) {
-        const float ss = rm_ssq64(out, colok);
-        const int row = b * a.T + t;
-        if (nn == 0 && live) a.ssq[static_cast<size_t>(row) * rm::ssq_stride(a.d) + ct] = ss;
-        out = make_float4(out.x * g_next.x, out.y * g_next.y, out.z * g_next.z, out.w * g_next.w);
-    }
-    if (st) {
-        uint2 packed;
-        packed.x = rm_f32_to_bf16_bits(out.x) | (rm_f32_to_bf16_bits(out.y) << 16);
-        packed.y = rm_f32_to_bf16_bits(out.z) | (rm_f32_to_bf16_bits(out.w) << 16);
-        *reinterpret_cast<uint2 *>(a.xn_next + ro) = packed;
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        if (j > 0) __syncthreads();  // tile j - 1's sums have been read
+#pragma unroll
+        for (int c = 0; c < 4; ++c) red[wave][c][lane] = acc[j][c];
+        __syncthreads();
+        if (wave >= 4) continue;
+        // Wave i finishes token 4 * grp + i of tile j (lane L, register i of a tile: token 4*(L/16)+i,
+        // physical column 4*(L%16) + q of call q): the 8 waves' sums in wave order.
+        const int i = wave;
+        float v[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            v[c] = red[0][c][lane][i];
+#pragma unroll
+            for (int w = 1; w < rm::kDfWaves; ++w) v[c] += red[w][c][lane][i];
+        }
+        const int t = t0 + j * 16 + grp * 4 + i;
+        const bool live = t < a.T;
+        const float4 acc4 = make_float4(v[0], v[1], v[2], v[3]);
+        float4 out = x_in[j];
+        if (a.ya_in != nullptr || cnt > 0) {  // an empty list without an anchor leaves y = x bit for bit
+            float4 f = acc4;
+            if (a.ya_in != nullptr)  // Eq. 4: the FFN output is y_a + (h - h_a) W_down
+                f = make_float4(ya_in[j].x + acc4.x, ya_in[j].y + acc4.y, ya_in[j].z + acc4.z, ya_in[j].w + acc4.w);
+            if (a.out_gate != nullptr)  // the adaptive output gate, before the residual
+                f = make_float4(f.x * gate.x, f.y * gate.y, f.z * gate.z, f.w * gate.w);
+            out = make_float4(out.x + f.x, out.y + f.y, out.z + f.z, out.w + f.w);
+        }
+        const bool st = live && colok;
+        if (st) {
+            *reinterpret_cast<float4 *>(a.y + ro[j]) = out;
+            if (a.ya_out != nullptr) *reinterpret_cast<float4 *>(a.ya_out + ro[j]) = acc4;
+        }
+        if (a.xn_next == nullptr) continue;
+        if (a.g_next != nullptr) {
+            const float ss = rm_ssq64(out, colok);
+            const int row = b * a.T + t;
+            if (nn == 0 && live) a.ssq[static_cast<size_t>(row) * rm::ssq_stride(a.d) + ct] = ss;
+            out = make_float4(out.x * g_next.x, out.y * g_next.y, out.z * g_next.z, out.w * g_next.w);
+        }
+        if (st) {
+            uint2 packed;
+            packed.x = rm_f32_to_bf16_bits(out.x) | (rm_f32_to_bf16_bits(out.y) << 16);
+            packed.y = rm_f32_to_bf16_bits(out.z) | (rm_f32_to_bf16_bits(out.w) << 16);
+            *reinterpret_cast<uint2 *>(a.xn_next + ro[j]) = packed;
+        }
     }
 }
 
@@ -1061,16 +1077,22 @@ hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *i
     const dim3 grid(p.ncol * p.ntt * p.B);
     const dim3 block(kDfThreads);
     hipError_t e;
-    switch (p.dn_cpw) {
-        case 1: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<1>, grid, block, st, a); break;
-        case 2: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<2>, grid, block, st, a); break;
-        case 3: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<3>, grid, block, st, a); break;
-        case 4: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<4>, grid, block, st, a); break;
-        case 5: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<5>, grid, block, st, a); break;
-        case 6: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<6>, grid, block, st, a); break;
-        case 7: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7>, grid, block, st, a); break;
-        default: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8>, grid, block, st, a); break;
+#define RM_DF(NT)                                                                                         \
+    switch (p.dn_cpw) {                                                                                   \
+        case 1: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<1, NT>, grid, block, st, a); break;    \
+        case 2: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<2, NT>, grid, block, st, a); break;    \
+        case 3: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<3, NT>, grid, block, st, a); break;    \
+        case 4: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<4, NT>, grid, block, st, a); break;    \
+        case 5: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<5, NT>, grid, block, st, a); break;    \
+        case 6: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<6, NT>, grid, block, st, a); break;    \
+        case 7: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7, NT>, grid, block, st, a); break;    \
+        default: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8, NT>, grid, block, st, a); break;   \
     }
+    if (p.df_nt == 2)
+        RM_DF(2)
+    else
+        RM_DF(1)
+#undef RM_DF
     return e != hipSuccess ? e : hipGetLastError();
 }
 

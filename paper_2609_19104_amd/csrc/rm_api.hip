@@ -273,9 +273,12 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         q.slice_units = cps;
         q.slices = ceil_div(nchunks, cps);
         // Short lists of one sample: one workgroup per (column tile, 16-token tile) can sum the whole list.
-        q.fused_down = B == 1 && nchunks <= kDfMaxChunks;
+        // With several samples, a workgroup takes 32 tokens, so each sample's rows are read by fewer token tiles
+        // (up to 7 chunks per wave: at 8 that kernel's registers spill).
         q.dn_cpw = ceil_div(nchunks, kDfWaves);
-        q.ntt = ceil_div(T, 16);
+        q.df_nt = B == 1 ? 1 : 2;
+        q.fused_down = nchunks <= kDfMaxChunks && (q.df_nt == 1 || q.dn_cpw <= 7);
+        q.ntt = ceil_div(T, 16 * q.df_nt);
         xn_elem = 2;
         h_elem = 2;
     } else {

@@ -58,7 +58,8 @@ struct Plan {
     // epilogue launch); the layer driver decides.
     bool fused_down = false;
     int dn_cpw = 0;      // fused down: chunks per wave (the kernel's unrolled pipeline depth)
-    int ntt = 0;         // fused down: 16-token tiles
+    int df_nt = 1;       // fused down: 16-token tiles per workgroup (2 with several samples)
+    int ntt = 0;         // fused down: token tiles of 16 df_nt tokens
     // Workspace: xn [B][T][d] (bf16 or f32); H (bf16: [B][kcap / 32][tpad][32], chunk-major; f32:
     // [B][tpad][kcap]); partials f32 [B][slices][T][d]; ssq f32 [B][T][ssq_stride(d)]
     // (per-token sums of squares of the FFN input by 64-column block, for the RMSNorm factor); and, for the dense

@@ -225,7 +225,10 @@ def test_stack_equals_layer_sequence():
     y = x
     for l in range(L):
         y = run_layer(lws[l], y, idx[l * B:(l + 1) * B].contiguous(), cnt[l * B:(l + 1) * B].contiguous(), 200)
-    assert np.array_equal(y_stack, y)
+    # Inside a stack the down projection runs fused (one workgroup sums the whole list in wave order), a single
+    # layer splits it over K-slices: the same terms, added in another order, so the two agree to rounding.
+    ey, ed = errors(y_stack, y, x)
+    assert ey <= 1e-5 and ed <= 1e-5, (ey, ed)
     ref = np.stack([oracle.ffn_stack(x[b], [lay.f64() for lay in layers],
                                      [masks[l, b].astype(np.float64) for l in range(L)]) for b in range(B)])
     _check(y_stack, ref, x, TOL_BF16, "stack")

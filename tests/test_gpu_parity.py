@@ -89,6 +89,9 @@ BF16_CASES = [
     (512, 16384, 64, 16384, "ones"),
     (768, 4096, 33, 2048, "none"),
     (256, 8192, 100, 4096, "none"),
+    # T > 64 at d = 2048 and d = 768: the staged kernel with eight and three column chunks
+    (2048, 4096, 100, 1500, "random"),
+    (768, 2048, 90, 700, "ones"),
 ]
 
 

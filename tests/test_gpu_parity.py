@@ -237,6 +237,24 @@ def test_stack_equals_layer_sequence():
     _check(y_stack, ref, x, TOL_BF16, "stack")
 
 
+@pytest.mark.parametrize("k", [1700, 1800, 64])
+def test_batched_stack_list_lengths(k):
+    # Several samples inside a stack: lists of up to 7 chunks per wave run the fused down projection with
+    # 32-token workgroups (1700 neurons: 54 chunks), longer ones the split projection and the epilogue (1800:
+    # 57 chunks), short ones one chunk per wave.  T = 40 leaves the second token tile ragged.
+    d, d_ff, T, L, B = 512, 2048, 40, 2, 3
+    layers = [wl.make_layer(23, l, d, d_ff, "bf16", norm="random") for l in range(L)]
+    x = wl.make_x(23, (B, T, d), k)
+    step = 40 if k > 100 else 8  # the samples' counts differ: ragged lists within the batch
+    masks = np.stack([np.stack([wl.uniform_mask(wl.rng(23, 4, k, l, b), d_ff, k - step * b) for b in range(B)])
+                      for l in range(L)])
+    idx, cnt = compact(masks.reshape(L * B, d_ff))
+    y = run_stack([dev_weights(l) for l in layers], x, idx, cnt, k)
+    ref = np.stack([oracle.ffn_stack(x[b], [lay.f64() for lay in layers],
+                                     [masks[l, b].astype(np.float64) for l in range(L)]) for b in range(B)])
+    _check(y, ref, x, TOL_BF16, f"batched stack k={k}")
+
+
 # ------------------------------------------------------------------------------------------------ masks in
 
 MASKED_CASES = [

@@ -665,32 +665,56 @@ def counted_traffic(workload: str, kernel_key: str):
     return int(float(v)) if v else None
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(setup: Setup, seconds: float):
-    """The float64 oracle on the same layer, mask and input, repeated for about `seconds` of CPU time."""
+    """The float64 oracle on the same layer, mask and input, repeated for about `seconds` of CPU time with the
+    BLAS threads it gets by default (all the cores it may use), then for about a quarter of that on one thread.
+    Each figure uses the median time per evaluation."""
     import oracle
 
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
     except Exception:  # threadpoolctl missing: report the affinity size NumPy's BLAS defaults to
+        threadpool_limits = None
         threads = len(os.sched_getaffinity(0))
     wg, wu, wd, g = setup.layer_np.f64()
     mult = setup.mask.cpu().numpy()[0].astype(np.float64)
     x = setup.x.cpu().numpy()[0]
-    oracle.masked_ffn(x, wg, wu, wd, mult, g)  # warm
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        oracle.masked_ffn(x, wg, wu, wd, mult, g)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds and reps >= 3:
-            break
-    per = el / reps
-    return {"value": round(setup.active_bytes / per / 1e9, 4), "unit": "GB/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"{reps} float64 oracle evaluations of the same layer (dense SwiGLU over all {setup.d_ff} "
-                      f"neurons, inactive ones zeroed) on the same input and mask, {el:.1f} s; "
-                      f"{per * 1e3:.2f} ms per layer; value = active weight bytes / oracle time"}
+
+    def run(budget: float):
+        oracle.masked_ffn(x, wg, wu, wd, mult, g)  # warm
+        times, t0 = [], time.perf_counter()
+        while True:
+            t = time.perf_counter()
+            oracle.masked_ffn(x, wg, wu, wd, mult, g)
+            times.append(time.perf_counter() - t)
+            el = time.perf_counter() - t0
+            if el >= budget and len(times) >= 5:
+                return float(np.median(times)), len(times), el
+
+    per, reps, el = run(seconds)
+    out = {"value": round(setup.active_bytes / per / 1e9, 4), "unit": "GB/s", "cores": int(threads),
+           "kind": "oracle", "cpu_model": _cpu_model(),
+           "sample": f"{reps} float64 oracle evaluations of the same layer (dense SwiGLU over all {setup.d_ff} "
+                     f"neurons, inactive ones zeroed) on the same input and mask, {el:.1f} s; median "
+                     f"{per * 1e3:.2f} ms per layer; value = active weight bytes / median oracle time"}
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            per1, reps1, _ = run(seconds / 4)
+        out["single_thread"] = {"value": round(setup.active_bytes / per1 / 1e9, 4), "unit": "GB/s",
+                                "ms_per_layer": round(per1 * 1e3, 2), "evaluations": reps1}
+    return out
 
 
 def main(argv=None) -> int:

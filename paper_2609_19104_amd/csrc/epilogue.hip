@@ -3,8 +3,8 @@
 // the next gate/up kernel forms the RMSNorm factor 1 / sqrt(mean(y^2) + eps).
 //
 // One wave per (token row, block of 256 columns), each lane a float4, so the launch has B T d / 256 waves.  The
-// slices are added in slice order 0, 1, 2, ... (loads issued sixteen at a time, additions in order), so the
-// result is bitwise reproducible.  Slices past the end of a sample's list are skipped (their partials hold
+// slices are added in slice order 0, 1, 2, ... (their loads issued in one batch of 3 or 11 when the slices fit,
+// else sixteen at a time; the additions in order), so the result is bitwise reproducible.  Slices past the end of a sample's list are skipped (their partials hold
 // zeros or are stale); with no listed neuron at all y = x exactly.  The block's sum of squares is reduced in a
 // fixed order (lane butterfly).  A separate launch, rather than the last K-slice workgroup of each column tile,
 // does this: a device-wide release from every such workgroup costs more than one kernel boundary.
@@ -53,6 +53,13 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
             for (int i = 0; i < 3; ++i) v[i] = ld4(P + min(1 + i, used - 1) * stride);  // unconditional: no waits
 #pragma unroll
             for (int i = 0; i < 3; ++i)
+                if (1 + i < used) acc = add4(acc, v[i]);
+        } else if (used <= 12) {  // up to 12 slices (one sample, lists of up to 12 slices): one batch of 11
+            float4 v[11];
+#pragma unroll
+            for (int i = 0; i < 11; ++i) v[i] = ld4(P + min(1 + i, used - 1) * stride);  // unconditional
+#pragma unroll
+            for (int i = 0; i < 11; ++i)
                 if (1 + i < used) acc = add4(acc, v[i]);
         } else {
             for (int s = 1; s < used; s += 16) {

@@ -15,14 +15,20 @@ __device__ __forceinline__ uint32_t nonzero_bytes(uint32_t v) {
            ((v & 0xff000000u) ? 8u : 0u);
 }
 
-// Sum of v over the workgroup (kCompactThreads threads).
-__device__ __forceinline__ int block_sum(int v, int *lds) {
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+// Sums of u and v over the workgroup (kCompactThreads threads), one pair of barriers for both.
+__device__ __forceinline__ void block_sum2(int &u, int &v, int *lds) {
+    for (int off = 32; off >= 1; off >>= 1) {
+        u += __shfl_xor(u, off);
+        v += __shfl_xor(v, off);
+    }
     const int wave = threadIdx.x >> 6;
-    __syncthreads();  // lds may still be read by a previous call
-    if ((threadIdx.x & 63) == 0) lds[wave] = v;
+    if ((threadIdx.x & 63) == 0) {
+        lds[wave] = u;
+        lds[4 + wave] = v;
+    }
     __syncthreads();
-    return lds[0] + lds[1] + lds[2] + lds[3];
+    u = lds[0] + lds[1] + lds[2] + lds[3];
+    v = lds[4] + lds[5] + lds[6] + lds[7];
 }
 
 // Mask m, segment s (neurons [s * kSeg, (s + 1) * kSeg)) -> the segment's part of idx[m] and, for s == 0,
@@ -36,7 +42,8 @@ __device__ __forceinline__ void compact_segment(const uint8_t *__restrict__ mask
     int32_t *out = idx + static_cast<size_t>(m) * d_ff;
     const int seg0 = s * kSeg;
     const int seg1 = min(seg0 + kSeg, d_ff);
-    __shared__ int lds[kCompactThreads / 64];
+    static_assert(kCompactThreads == 256, "block_sum2 adds four waves");
+    __shared__ int lds[2 * kCompactThreads / 64];
     // This segment's mask bytes, kept as they pass through step 1.
     __shared__ __attribute__((aligned(16))) uint32_t seg_bytes[kSeg / 4];
 
@@ -72,11 +79,10 @@ __device__ __forceinline__ void compact_segment(const uint8_t *__restrict__ mask
         if (p < seg0) before += c;
         if (p >= seg0 && p < seg1) reinterpret_cast<uint8_t *>(seg_bytes)[p - seg0] = m8;
     }
-    before = block_sum(before, lds);
-    total = block_sum(total, lds);
+    block_sum2(before, total, lds);
 
     // 2. This thread's 4 neurons of the segment (from LDS: every byte of [seg0, seg1) was stored in step 1, and
-    //    block_sum's barriers made it visible), their exclusive prefix within the segment, and the writes.
+    //    block_sum2's barrier made it visible), their exclusive prefix within the segment, and the writes.
     const int p0 = seg0 + 4 * tid;
     uint32_t bits = 0;
     if (p0 < seg1) {
@@ -90,7 +96,7 @@ __device__ __forceinline__ void compact_segment(const uint8_t *__restrict__ mask
         const int v = __shfl_up(incl, off);
         if (lane >= off) incl += v;
     }
-    __syncthreads();  // lds was read by block_sum
+    __syncthreads();  // lds was read by block_sum2
     if (lane == 63) lds[wave] = incl;
     __syncthreads();
     int before_wave = 0;

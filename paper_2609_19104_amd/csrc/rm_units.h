@@ -4,6 +4,7 @@
 #pragma once
 
 #include "rm_internal.h"
+#include "rm_select.h"
 
 namespace rm_units {
 
@@ -90,18 +91,13 @@ __device__ __forceinline__ void compact_segment(const uint8_t *__restrict__ mask
         if (p0 + 4 > seg1) bits &= (1u << (seg1 - p0)) - 1u;  // bytes past the mask are not neurons
     }
     const int mine = __popc(bits);
-    int incl = mine;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int v = __shfl_up(incl, off);
-        if (lane >= off) incl += v;
-    }
-    __syncthreads();  // lds was read by block_sum2
-    if (lane == 63) lds[wave] = incl;
+    const int incl = rm_sel::wave_incl_scan(mine);  // every lane of the wave takes part
+    __shared__ int wave_tot[kCompactThreads / 64];   // its own array: no barrier against block_sum2's reads
+    if (lane == 63) wave_tot[wave] = incl;
     __syncthreads();
     int before_wave = 0;
 #pragma unroll
-    for (int w = 0; w < kCompactThreads / 64; ++w) before_wave += (w < wave) ? lds[w] : 0;
+    for (int w = 0; w < kCompactThreads / 64; ++w) before_wave += (w < wave) ? wave_tot[w] : 0;
     int pos = before + before_wave + incl - mine;
     while (bits) {
         const int j = __builtin_ctz(bits);

@@ -3,8 +3,8 @@
 // the next gate/up kernel forms the RMSNorm factor 1 / sqrt(mean(y^2) + eps).
 //
 // One wave per (token row, block of 256 columns), each lane a float4, so the launch has B T d / 256 waves.  The
-// slices are added in slice order 0, 1, 2, ... (their loads issued in one batch of 3 or 11 when the slices fit,
-// else sixteen at a time; the additions in order), so the result is bitwise reproducible.  Slices past the end of a sample's list are skipped (their partials hold
+// slices are added in slice order 0, 1, 2, ... (their loads issued in one batch when the launch has at most 12
+// slices, else sixteen at a time; the additions in order), so the result is bitwise reproducible.  Slices past the end of a sample's list are skipped (their partials hold
 // zeros or are stale); with no listed neuron at all y = x exactly.  The block's sum of squares is reduced in a
 // fixed order (lane butterfly).  A separate launch, rather than the last K-slice workgroup of each column tile,
 // does this: a device-wide release from every such workgroup costs more than one kernel boundary.
@@ -45,31 +45,33 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
 
     float4 out = ld4(x + ro);
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (used > 0) {
-        acc = ld4(P);
-        if (used <= 4) {  // few slices (several samples per call): one batch of 3 loads, not 16 mostly repeated
-            float4 v[3];
+    if (slices <= 12) {
+        // All the launch's slices in one batch, addressed by the slice count of the launch (not by `used`,
+        // which waits for the count to arrive): the loads go out with x's, and only the additions depend on
+        // the count.  Slices at or past `used` are read (they lie inside the partials) and not added.
+        float4 v[12];
+        if (slices <= 4) {  // several samples per call: 4 loads, not 12 mostly repeated
 #pragma unroll
-            for (int i = 0; i < 3; ++i) v[i] = ld4(P + min(1 + i, used - 1) * stride);  // unconditional: no waits
+            for (int i = 0; i < 4; ++i) v[i] = ld4(P + min(i, slices - 1) * stride);
 #pragma unroll
-            for (int i = 0; i < 3; ++i)
-                if (1 + i < used) acc = add4(acc, v[i]);
-        } else if (used <= 12) {  // up to 12 slices (one sample, lists of up to 12 slices): one batch of 11
-            float4 v[11];
-#pragma unroll
-            for (int i = 0; i < 11; ++i) v[i] = ld4(P + min(1 + i, used - 1) * stride);  // unconditional
-#pragma unroll
-            for (int i = 0; i < 11; ++i)
-                if (1 + i < used) acc = add4(acc, v[i]);
+            for (int i = 0; i < 4; ++i)
+                if (i < used) acc = i == 0 ? v[0] : add4(acc, v[i]);
         } else {
-            for (int s = 1; s < used; s += 16) {
-                float4 v[16];
 #pragma unroll
-                for (int i = 0; i < 16; ++i) v[i] = ld4(P + min(s + i, used - 1) * stride);  // unconditional
+            for (int i = 0; i < 12; ++i) v[i] = ld4(P + min(i, slices - 1) * stride);
 #pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    if (s + i < used) acc = add4(acc, v[i]);
-            }
+            for (int i = 0; i < 12; ++i)
+                if (i < used) acc = i == 0 ? v[0] : add4(acc, v[i]);
+        }
+    } else if (used > 0) {
+        acc = ld4(P);
+        for (int s = 1; s < used; s += 16) {
+            float4 v[16];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) v[i] = ld4(P + min(s + i, used - 1) * stride);  // unconditional
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+                if (s + i < used) acc = add4(acc, v[i]);
         }
     }
     if (ya_in != nullptr || used > 0) {  // an empty list without an anchor leaves y = x bit for bit

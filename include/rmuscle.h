@@ -22,7 +22,8 @@
  *
  * Conventions shared by every call
  *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every buffer and the stream; the
- *     library allocates nothing, keeps no state except a thread-local error string, and never synchronizes.
+ *     library allocates nothing and never synchronizes.  Its only state is a thread-local error string and the
+ *     events that rm_profile_kernel_events arms for the calling thread.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the default stream).
  *   - Every argument is validated on the host before anything is enqueued; on error nothing is enqueued and
  *     the call returns a negative rm_status with a detail message in rm_last_error().
@@ -188,8 +189,9 @@ rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *
                              const float *x, float *y, const int32_t *idx, const int32_t *count, int32_t max_count,
                              const float *y_anchor, const float *h_anchor, void *ws, size_t ws_bytes, void *stream);
 
-/* Compact copies of a group's selected weight rows (section 4.1: the selected weights are prepared in shared
- * compact buffers reused across the group's steps).  For every layer l of a stack and its list (one list per
+/* Compact copies of a group's selected weight rows (section 4.1, last paragraph; section 5, "Overlapping
+ * Retrieval and Weight Gathering"): each layer's listed rows copied once per group into contiguous buffers, which
+ * every step of that group can then read in place of the scattered originals.  For every layer l of a stack and its list (one list per
  * layer, the group's mask: idx int32 [L][d_ff], count int32 [L], the rm_mask_compact layout with B = 1):
  *     out[l][0][i] = w[l].w_gate[idx[l][i]],  out[l][1][i] = w[l].w_up[idx[l][i]],
  *     out[l][2][i] = w[l].w_down[idx[l][i]]
@@ -206,13 +208,13 @@ rm_status rm_gather_stack_rows(const rm_ffn_shape *s, const rm_ffn_layer_weights
  * token rows, of which rows [v0, v0 + P) are visual tokens:
  *   drift[p] = RMS(x[v0+p] - x_ref[v0+p]) / max(RMS(x[v0+p]), 1e-6), the Eq. 2 drift of each visual token, with
  *              x the current FFN input (after RMSNorm) and x_ref the reference execution's, both float32 [N][d];
- *   rows:      int32 [N] out: in its first count[0] entries, ascending, every non-visual row (instruction and
- *              robot-state rows are always recomputed) and the k visual rows with the largest drift (ties to the
+ *   rows:      int32 [N] out: in its first count[0] entries, ascending, every non-visual row (Eq. 3 reuses a
+ *              cached output only for a visual token) and the k visual rows with the largest drift (ties to the
  *              lower token); k = ceil(rho_p * P) in the paper;
  *   count:     int32 [1] out, (N - P) + k.
- * The drift is float32 in a fixed order (lane j of a wave adds the squares of columns j, j + 64, ...; the lanes'
- * sums are folded 32, 16, ..., 1 apart; rounded division and correctly rounded square roots), since the row
- * selection depends on it.  N <= 16384, 0 <= v0, v0 + P <= N, 0 <= k <= P; drift may be NULL when P = 0.
+ * The drift is float32 (lane j of a wave adds the squares of columns j, j + 64, ...; the lanes' sums are folded
+ * 32, 16, ..., 1 apart; rounded division and correctly rounded square roots), within float32 rounding of the
+ * exact Eq. 2 value; the rows are the top k of these float32 values, the same on every call.  N <= 16384, 0 <= v0, v0 + P <= N, 0 <= k <= P; drift may be NULL when P = 0.
  * drift, rows and count must not overlap each other, x or x_ref.  Errors: RM_ERR_INVALID_ARG, RM_ERR_SHAPE,
  * RM_ERR_ALIGN (4-byte alignment). */
 rm_status rm_context_select(const float *x, const float *x_ref, int32_t n_tok, int32_t d, int32_t v0, int32_t P,

@@ -1,5 +1,5 @@
-// Compact copies of a group's selected weight rows (paper section 4.1: the selected weights are prepared in
-// shared compact buffers that the group's steps reuse; section 5 builds one mask per layer and group).
+// Compact copies of a group's selected weight rows (paper section 4.1, last paragraph; section 5 builds one mask
+// per layer and group): each layer's listed rows copied once, contiguously, for all the steps of the group.
 //
 // gather_rows_kernel: one wave per output row, 16-byte loads and stores (a bf16 row of d = 1024 is 2 KB, two
 // passes of the wave).  Output rows past a layer's count are filled with zeros: the FFN kernels read those rows

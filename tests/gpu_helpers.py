@@ -47,7 +47,7 @@ def run_layer(layer_dev, x: np.ndarray, idx: torch.Tensor, cnt: torch.Tensor, ma
     xt = dev_f32(x)
     yt = xt if in_place else torch.full_like(xt, float("nan"))
     ws = rm.workspace(d, d_ff, rm.wdtype_of(wg), B, T, max_count, device=DEV)
-    ws.fill_(0xA5)  # the library must not rely on a cleared workspace
+    ws.fill_(0xFF)  # NaN in every float32 / bf16 slot: stale workspace read into a result shows
     rm.rm_sparse_ffn_layer(xt, yt, layer_dev, idx, cnt, max_count, ws)
     torch.cuda.synchronize()
     return yt.cpu().numpy()
@@ -60,7 +60,7 @@ def run_dense(layer_dev, x: np.ndarray) -> np.ndarray:
     xt = dev_f32(x)
     yt = torch.full_like(xt, float("nan"))
     ws = rm.workspace(d, d_ff, rm.wdtype_of(wg), B, T, d_ff, device=DEV)
-    ws.fill_(0x5A)
+    ws.fill_(0x7F)  # about 3.4e38 in every float32 and bf16 slot
     rm.rm_dense_ffn_ref(xt, yt, layer_dev, ws)
     torch.cuda.synchronize()
     return yt.cpu().numpy()
@@ -73,7 +73,7 @@ def run_stack(layers_dev, x: np.ndarray, idx: torch.Tensor, cnt: torch.Tensor, m
     xt = dev_f32(x)
     yt = torch.full_like(xt, float("nan"))
     ws = rm.workspace(d, d_ff, rm.wdtype_of(wg), B, T, max_count, device=DEV)
-    ws.fill_(0x33)
+    ws.fill_(0xFF)
     rm.rm_sparse_ffn_stack(xt, yt, layers_dev, idx, cnt, max_count, ws)
     torch.cuda.synchronize()
     return yt.cpu().numpy()
@@ -114,7 +114,7 @@ def run_anchor(layers_dev, x: np.ndarray, idx: torch.Tensor, cnt: torch.Tensor, 
     ya = torch.full((L, B, T, d), float("nan"), dtype=torch.float32, device=DEV)
     ha = torch.full((L, B, max_count, T), H_SENTINEL, dtype=torch.float32, device=DEV)
     ws = rm.workspace(d, d_ff, rm.wdtype_of(wg), B, T, d_ff, device=DEV)
-    ws.fill_(0x6B)
+    ws.fill_(0x7F)
     rm.rm_anchor_ffn_stack(xt, yt, layers_dev, idx, cnt, max_count, ya, ha, ws)
     torch.cuda.synchronize()
     return yt, ya, ha
@@ -129,7 +129,7 @@ def run_delta(layers_dev, x: np.ndarray, idx: torch.Tensor, cnt: torch.Tensor, m
     xt = dev_f32(x)
     yt = torch.full_like(xt, float("nan"))
     ws = rm.workspace(d, d_ff, rm.wdtype_of(wg), B, T, max_count, device=DEV)
-    ws.fill_(0x2C)
+    ws.fill_(0xFF)
     rm.rm_delta_ffn_stack(xt, yt, layers_dev, idx, cnt, max_count, ya, ha, ws)
     torch.cuda.synchronize()
     return yt.cpu().numpy()

@@ -1,9 +1,15 @@
 """GPU parity of the Context Cache's visual-token recomputation (section 4.1, Eq. 2 and Eq. 3) against the oracle
 (oracle.context_cache) on the same seeded inputs.
 
-Bars: the Eq. 2 drift and the recomputed row list bit-exact (both sides take the top-k decision on the same
-float32 values); the recomputed rows of y within max-abs relative error 2e-2 of the float64 FFN (bf16 weights,
-inputs rounded to bf16, float32 accumulation); every other row of y left bit for bit as the reference output."""
+Bars:
+- the float32 Eq. 2 drift within `drift_rel_bound(d)` of the float64 value (a rounding bound that holds for any
+  summation order);
+- the recomputed row list exactly the top-k of the GPU's own float32 drifts (ties to the lower token; an integer
+  decision on the values it returns), and a valid top-k of the float64 drifts given that bound
+  (`check_recomputed_rows`: the count, every non-visual row, ascending, no dropped row above a chosen one);
+- repeated calls bit for bit equal;
+- every recomputed row of y within max-abs relative error 2e-2 of the float64 FFN (bf16 weights, inputs rounded to
+  bf16, float32 accumulation); every other row of y left bit for bit as the reference output."""
 import numpy as np
 import pytest
 import torch
@@ -49,8 +55,23 @@ SELECT_CASES = [
 ]
 
 
+def _check_selection(x, x_ref, v0, P, k, drift, rows, count):
+    n_tok, d = x.shape
+    ref = cc.drift(x[v0:v0 + P], x_ref[v0:v0 + P])
+    bound = cc.drift_rel_bound(d)
+    got = drift.astype(np.float64)
+    zero = ref == 0.0
+    assert np.all(got[zero] == 0.0)
+    err = float(np.max(np.abs(got[~zero] - ref[~zero]) / ref[~zero])) if np.any(~zero) else 0.0
+    print(f"drift: max rel err {err:.2e} against float64 (bound {bound:.2e})")
+    assert err <= bound
+    assert count == n_tok - P + k
+    assert np.array_equal(rows, cc.recomputed_rows(got, n_tok, v0, k))  # the decision on its own values
+    cc.check_recomputed_rows(rows, ref, n_tok, v0, k, rel=bound)
+
+
 @pytest.mark.parametrize("n_tok,d,v0,P,k,quantum", SELECT_CASES)
-def test_drift_and_row_selection_bit_exact(n_tok, d, v0, P, k, quantum):
+def test_drift_and_row_selection(n_tok, d, v0, P, k, quantum):
     r = np.random.default_rng(n_tok + d)
     x_ref = r.standard_normal((n_tok, d)).astype(np.float32)
     delta = r.standard_normal((n_tok, d)) * np.exp(r.standard_normal((n_tok, 1)))
@@ -59,11 +80,10 @@ def test_drift_and_row_selection_bit_exact(n_tok, d, v0, P, k, quantum):
         delta[::3] = 0.0  # rows without drift: exact zeros, tied
     x = (x_ref + delta).astype(np.float32)
     drift, rows, count = _select(x, x_ref, v0, P, k)
-    ref = cc.drift(x[v0:v0 + P], x_ref[v0:v0 + P])
-    assert np.array_equal(drift.view(np.uint32), ref.view(np.uint32))
-    ref_rows = cc.recomputed_rows(ref, n_tok, v0, k)
-    assert count == len(ref_rows) == n_tok - P + k
-    assert np.array_equal(rows, ref_rows)
+    _check_selection(x, x_ref, v0, P, k, drift, rows, count)
+    drift2, rows2, count2 = _select(x, x_ref, v0, P, k)
+    assert np.array_equal(drift.view(np.uint32), drift2.view(np.uint32))
+    assert count2 == count and np.array_equal(rows2, rows)
 
 
 def _run_ffn(w, x, y_ref, rows, count, max_rows, act, packed=False):
@@ -82,10 +102,10 @@ def _run_ffn(w, x, y_ref, rows, count, max_rows, act, packed=False):
     return yt.cpu().numpy()
 
 
-def _check_update(w, x, y_ref, y, rows, act, sample=None):
+def _check_update(w, x, y_ref, y, rows, act):
     keep = np.setdiff1d(np.arange(w.n_tok), rows)
     assert np.array_equal(y[keep].view(np.uint32), y_ref[keep].view(np.uint32))
-    chk = rows if sample is None else rows[np.linspace(0, len(rows) - 1, sample).astype(int)]
+    chk = rows
     if len(chk) == 0:
         return
     wg, wu, _, _ = w.layer.f64()
@@ -158,14 +178,14 @@ def test_context_ffn_with_no_rows_leaves_y():
 
 def test_context_cache_full_size_end_to_end():
     # The VLM layer of a pi0.5-style model: 850 rows (768 visual), rho_p = 0.4 -> 308 + 82 rows recomputed,
-    # d = 2048, d_ff = 16384, GeGLU.  Selection on the GPU, checked bit for bit; the FFN checked on 48 sampled
-    # recomputed rows and on every kept row.
+    # d = 2048, d_ff = 16384, GeGLU.  Selection on the GPU, checked against float64 Eq. 2; the FFN run on the rows
+    # the GPU chose and every one of them checked, as is every kept row.
     w = wl.context_workload()
     drift, rows, count = _select(w.x, w.x_ref, w.v0, w.P, w.k)
-    ref_rows = cc.recomputed_rows(cc.drift(w.x[w.v0:w.v0 + w.P], w.x_ref[w.v0:w.v0 + w.P]), w.n_tok, w.v0, w.k)
-    assert np.array_equal(rows, ref_rows)
-    y = _run_ffn(w, w.x, w.y_ref, ref_rows, count, count, "gelu_tanh")
-    _check_update(w, w.x, w.y_ref, y, ref_rows, "gelu_tanh", sample=48)
+    _check_selection(w.x, w.x_ref, w.v0, w.P, w.k, drift, rows, count)
+    assert count == 390
+    y = _run_ffn(w, w.x, w.y_ref, rows, count, count, "gelu_tanh")
+    _check_update(w, w.x, w.y_ref, y, rows, "gelu_tanh")
 
 
 def _fuzz_cases(n=10, seed=2609):

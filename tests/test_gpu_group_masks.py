@@ -1,8 +1,15 @@
 """GPU parity of the group-mask construction (section 5, "Constructing Group Neuron Masks"; Eq. 1) against the
-float32 oracle (oracle.group_masks), on the same seeded inputs.
+float64 oracle (oracle.group_masks), on the same seeded inputs.
 
-Bar: bit-exact.  The norms, the Eq. 1 scores and the masks are integer decisions or fixed-order float32 sums with
-one rounding per operation, computed in the same order on both sides."""
+Bars:
+- the float32 row norms and Eq. 1 scores within `norm_rel_bound(d)` / `score_rel_bound(T)` of the float64
+  values (rounding bounds that hold for any summation order);
+- each layer's mask exactly the section-5 decision taken on the GPU's own float32 scores (per-step top K, union,
+  top K by summed score, ties to the lower neuron; the sum over steps allowed its float32 rounding), and a valid
+  group mask for the float64 scores given their bound (`check_group_mask`);
+- where every sum is exact in float32 (activations on a dyadic grid, unit norms), the scores equal the float64
+  values exactly, the decision is unique, and the masks equal the oracle's bit for bit;
+- repeated calls bit for bit equal."""
 import numpy as np
 import pytest
 import torch
@@ -21,13 +28,19 @@ from gpu_helpers import dev_weights  # noqa: E402
 
 @pytest.mark.parametrize("wdtype", ["bf16", "f32"])
 @pytest.mark.parametrize("d,d_ff", [(32, 1), (96, 63), (1024, 65), (1024, 4096), (2048, 300)])
-def test_neuron_norms_bit_exact(wdtype, d, d_ff):
+def test_neuron_norms(wdtype, d, d_ff):
     layer = wl.make_layer(91, d_ff, d, d_ff, wdtype)
     wd = dev_weights(layer)[2]
-    norms = torch.full((d_ff,), float("nan"), device="cuda")
-    rm.rm_neuron_norms(wd, norms)
-    ref = gm.neuron_norms(wl.storage_to_f64(layer.w_down).astype(np.float32))
-    assert np.array_equal(norms.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+    runs = []
+    for _ in range(2):
+        norms = torch.full((d_ff,), float("nan"), device="cuda")
+        rm.rm_neuron_norms(wd, norms)
+        runs.append(norms.cpu().numpy())
+    assert np.array_equal(runs[0].view(np.uint32), runs[1].view(np.uint32))
+    ref = gm.neuron_norms(wl.storage_to_f64(layer.w_down))
+    err = np.max(np.abs(runs[0] - ref) / ref)
+    print(f"norms: max rel err {err:.2e} (bound {gm.norm_rel_bound(d):.2e})")
+    assert err <= gm.norm_rel_bound(d)
 
 
 def _run(h, norms, k):
@@ -69,20 +82,34 @@ def _fuzz_cases(n=8, seed=19104):
                int(rng.integers(0, d_ff + 1)), float(rng.choice([0.0, 0.5])))
 
 
+def _check_masks(h, norms, K, scores, mask, exact):
+    S, L, d_ff, T = h.shape
+    bound = gm.score_rel_bound(T)
+    for l in range(L):
+        c64 = np.stack([gm.contribution_scores(h[s, l], norms[l]) for s in range(S)])
+        got = scores[:, l].astype(np.float64)
+        if exact:
+            assert np.array_equal(got, c64), l
+            assert np.array_equal(mask[l], gm.group_mask(h[:, l], norms[l], K)), l
+        else:
+            pos = c64 > 0
+            assert np.all(got[~pos] == 0.0)
+            assert np.max(np.abs(got[pos] - c64[pos]) / c64[pos]) <= bound, l
+        gm.check_group_mask(mask[l], got, K, rel=0.0)  # the decision on its own values
+        gm.check_group_mask(mask[l], c64, K, rel=bound)
+    assert np.all(mask.sum(axis=1) == K)
+
+
 @pytest.mark.parametrize("S,L,d_ff,T,K,quantum", CASES + list(_fuzz_cases()))
-def test_group_masks_bit_exact(S, L, d_ff, T, K, quantum):
+def test_group_masks(S, L, d_ff, T, K, quantum):
     h = wl.activation_like(92, (S, L, d_ff, T), d_ff, T, quantum=quantum)
     norms = wl.positive_norms(92, (L, d_ff), d_ff)
     if quantum > 0:
-        norms[:] = 1.0  # keep the quantized sums tied after the product
+        norms[:] = 1.0  # every sum exact: the scores equal the float64 ones and ties are true ties
     scores, mask = _run(h, norms, K)
-    for s in range(S):
-        for l in range(L):
-            ref = gm.contribution_scores(h[s, l], norms[l])
-            assert np.array_equal(scores[s, l].view(np.uint32), ref.view(np.uint32)), (s, l)
-    ref_mask = gm.group_masks(h, norms, K)
-    assert np.array_equal(mask, ref_mask)
-    assert np.all(mask.sum(axis=1) == K)
+    _check_masks(h, norms, K, scores, mask, exact=quantum > 0)
+    scores2, mask2 = _run(h, norms, K)
+    assert np.array_equal(scores.view(np.uint32), scores2.view(np.uint32)) and np.array_equal(mask, mask2)
 
 
 def test_group_masks_from_identity_list_anchor():
@@ -125,18 +152,18 @@ def test_group_masks_from_identity_list_anchor():
 def test_step_specific_against_group_shared_coverage(S, L, d_ff, T, K):
     # Section 5 shares one mask across a group; section 3.4's coverage measures what a mask keeps of a step's
     # contribution.  Each step alone (S = 1) gives its own top-K mask; the group call gives the shared one.  Both
-    # masks match the oracle's bit for bit, so their coverages do, and the shared mask never covers more than
-    # the step's own.
+    # masks are checked as above, and the shared mask never covers more of a step's float64 contribution than the
+    # step's own, up to the scores' rounding allowance (a float32 top K can swap near-tied neurons).
     h = wl.activation_like(94, (S, L, d_ff, T), d_ff, T)
     norms = wl.positive_norms(94, (L, d_ff), d_ff)
     scores, group = _run(h, norms, K)
+    _check_masks(h, norms, K, scores, group, exact=False)
+    bound = gm.score_rel_bound(T)
     for s in range(S):
-        _, own = _run(np.ascontiguousarray(h[s:s + 1]), norms, K)
+        h1 = np.ascontiguousarray(h[s:s + 1])
+        s_scores, own = _run(h1, norms, K)
+        _check_masks(h1, norms, K, s_scores, own, exact=False)
         for l in range(L):
             c = gm.contribution_scores(h[s, l], norms[l])
-            ref_own = gm.top_k(c, K).astype(np.uint8)
-            ref_group = gm.group_masks(h[:, l:l + 1], norms[l:l + 1], K)[0]
-            assert np.array_equal(own[l], ref_own) and np.array_equal(group[l], ref_group)
-            cov_own, cov_group = gm.coverage(scores[s, l], own[l]), gm.coverage(scores[s, l], group[l])
-            assert cov_own == gm.coverage(c, ref_own) and cov_group == gm.coverage(c, ref_group)
-            assert 0.0 < cov_group <= cov_own <= 1.0
+            cov_own, cov_group = gm.coverage(c, own[l]), gm.coverage(c, group[l])
+            assert 0.0 < cov_group <= cov_own * (1.0 + 2.0 * bound) <= 1.0 + 2.0 * bound

@@ -203,6 +203,23 @@ def test_ragged_batch_counts():
         _check(y[b], y_ref[b], x[b], TOL_BF16, f"ragged count {c}")
 
 
+def test_ragged_batch_counts_f32():
+    # The float32 path at config 1's shape with a host bound of d_ff: most samples use far fewer K-slices than the
+    # launch has, and the slices past a sample's count hold stale workspace (NaN from run_layer's poison), which the
+    # epilogue must not add.
+    d, d_ff, T = 256, 1024, 8
+    counts = [0, 1, 7, 8, 9, 100, 256, 1024]
+    layer = wl.make_layer(27, 0, d, d_ff, "f32")
+    x = wl.make_x(27, (len(counts), T, d), 0)
+    masks = wl.ragged_masks(27, d_ff, counts)
+    idx, cnt = _masks_to_lists(masks)
+    y = run_layer(dev_weights(layer), x, idx, cnt, d_ff)
+    y_ref = _oracle_layer(layer, x, masks.astype(np.float64))
+    assert np.array_equal(y[0].view(np.uint32), x[0].view(np.uint32))
+    for b, c in enumerate(counts[1:], start=1):
+        _check(y[b], y_ref[b], x[b], TOL_F32, f"f32 ragged count {c}")
+
+
 def test_counts_above_max_count_are_clamped_not_read_past():
     # count[b] larger than the host bound: only the first max_count listed neurons are applied.
     d, d_ff, T = 256, 512, 16
@@ -283,7 +300,7 @@ def test_masked_calls_equal_compaction_then_lists(d, d_ff, L, B, T, p, wdtype, n
     cnt = torch.full((L * B,), -3, dtype=torch.int32, device="cuda")
     y = torch.full_like(xt, float("nan"))
     ws = rm.workspace(d, d_ff, rm.wdtype_of(lws[0][0]), B, T, max_count)
-    ws.fill_(0x4D)
+    ws.fill_(0xFF)  # NaN in every float32 and bf16 slot
     if L == 1:
         rm.rm_masked_ffn_layer(xt, y, lws[0], mt, idx, cnt, max_count, ws)
     else:

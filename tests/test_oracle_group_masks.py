@@ -1,30 +1,67 @@
 """Pins for the group-mask oracle (section 5, "Constructing Group Neuron Masks"; Eq. 1 of section 3.4).
 
-Each pin checks the oracle against something fixed independently of it: a library norm, the float64 Eq. 1
-score, exhaustive search over subsets, or a small example worked out by hand."""
+Each pin checks the oracle against something fixed independently of it: torch's library vector norms, values
+worked out by hand, float32 evaluations in several orders (for the rounding bounds), exhaustive search over
+subsets, or a small example worked out by hand.  The mask checker is pinned by planting mistakes in valid masks."""
 import itertools
 
 import numpy as np
 import pytest
+import torch
 
-import oracle
 from oracle import group_masks as gm
 
 
 def test_neuron_norms_match_library_norm():
     w = np.random.default_rng(1).standard_normal((37, 300)).astype(np.float32) * 0.02
-    ref = np.linalg.norm(w.astype(np.float64), axis=1)
-    got = gm.neuron_norms(w).astype(np.float64)
-    assert np.max(np.abs(got - ref) / ref) < 1e-5
+    ref = torch.linalg.vector_norm(torch.tensor(w, dtype=torch.float64), dim=1).numpy()
+    assert np.max(np.abs(gm.neuron_norms(w) - ref) / ref) < 1e-14
+    assert gm.neuron_norms(np.array([[3.0, 4.0], [0.0, 0.0]])).tolist() == [5.0, 0.0]
 
 
-def test_scores_match_float64_eq1():
+def test_scores_match_library_norms_and_hand_values():
+    # Eq. 1 as two library norms: the L1 norm of the neuron's activations times the L2 norm of its down row.
     r = np.random.default_rng(2)
     h = r.standard_normal((50, 17)).astype(np.float32)  # [d_ff][T]
     wd = r.standard_normal((50, 64)).astype(np.float32)
-    got = gm.contribution_scores(h, gm.neuron_norms(wd)).astype(np.float64)
-    ref = oracle.contribution_score(h.T.astype(np.float64), wd.astype(np.float64))  # h as [T][d_ff]
-    assert np.max(np.abs(got - ref) / ref) < 1e-5
+    ht, wt = torch.tensor(h, dtype=torch.float64), torch.tensor(wd, dtype=torch.float64)
+    ref = (torch.linalg.vector_norm(ht, ord=1, dim=1) * torch.linalg.vector_norm(wt, dim=1)).numpy()
+    got = gm.contribution_scores(h, gm.neuron_norms(wd))
+    assert np.max(np.abs(got - ref) / ref) < 1e-14
+    # By hand: |1| + |-2| + |0.5| = 3.5 times ||(3, 4)|| = 5 -> 17.5; the sign of h does not matter.
+    hh = np.array([[1.0, -2.0, 0.5], [-1.0, 2.0, -0.5]])
+    assert gm.contribution_scores(hh, gm.neuron_norms(np.array([[3.0, 4.0], [0.0, 2.0]]))).tolist() == [17.5, 7.0]
+
+
+def _f32_scores(h, norms, order):
+    """Eq. 1 in float32, one rounding per operation, |h| summed over t forward or backward: evaluations a float32
+    kernel could perform."""
+    h = np.abs(np.asarray(h, np.float32))
+    ts = range(h.shape[1]) if order == "forward" else range(h.shape[1] - 1, -1, -1)
+    s = np.zeros(h.shape[0], np.float32)
+    for t in ts:
+        s = (s + h[:, t]).astype(np.float32)
+    return (s * np.asarray(norms, np.float32)).astype(np.float32)
+
+
+@pytest.mark.parametrize("T", [1, 51, 130])
+def test_score_and_norm_bounds_cover_float32_evaluations(T):
+    r = np.random.default_rng(T)
+    h = (r.standard_normal((200, T)) * np.exp(2 * r.standard_normal((200, T)))).astype(np.float32)
+    wd = (r.standard_normal((200, 2048)) * np.exp(r.standard_normal((200, 2048)))).astype(np.float32)
+    n64 = gm.neuron_norms(wd)
+    sq = (wd * wd).astype(np.float32)
+    for cols in (range(2048), range(2047, -1, -1)):
+        s = np.zeros(200, np.float32)
+        for j in cols:
+            s = (s + sq[:, j]).astype(np.float32)
+        n32 = np.sqrt(s).astype(np.float32)
+        assert np.max(np.abs(n32 - n64) / n64) <= gm.norm_rel_bound(2048)
+    norms = n64.astype(np.float32)  # the scores' norms as float32 inputs
+    ref = gm.contribution_scores(h, norms)
+    for order in ("forward", "backward"):
+        err = np.max(np.abs(_f32_scores(h, norms, order) - ref) / ref)
+        assert err <= gm.score_rel_bound(T), (order, err)
 
 
 def test_top_k_matches_stable_sort_and_breaks_ties_low():
@@ -118,3 +155,32 @@ def test_step_top_k_has_the_best_coverage_of_any_k_subset(seed):
     k = 3
     best = max(gm.coverage(c, np.isin(np.arange(9), s)) for s in itertools.combinations(range(9), k))
     assert gm.coverage(c, gm.top_k(c, k)) == pytest.approx(best, rel=1e-12)
+
+
+def test_check_group_mask_accepts_valid_and_catches_planted_mistakes():
+    # Two steps, six neurons, K = 2.  Step 0: top two {0, 1}; step 1: top two {2, 1}.  Union {0, 1, 2}; summed
+    # scores 10.5, 14, 9, ... -> the mask {0, 1}.
+    c = np.array([[10.0, 9.0, 1.0, 0.5, 0.2, 0.1],
+                  [0.5, 5.0, 8.0, 3.0, 0.1, 0.2]])
+    good = np.array([1, 1, 0, 0, 0, 0], np.uint8)
+    gm.check_group_mask(good, c, 2, rel=1e-6)
+    bad = [
+        np.array([1, 1, 1, 0, 0, 0], np.uint8),  # three neurons
+        np.array([1, 0, 1, 0, 0, 0], np.uint8),  # 2 (summed 9) kept over 1 (summed 14)
+        np.array([1, 0, 0, 1, 0, 0], np.uint8),  # 3 is no step's candidate
+    ]
+    for m in bad:
+        with pytest.raises(AssertionError):
+            gm.check_group_mask(m, c, 2, rel=1e-6)
+    # Within the allowance either order is valid: neurons 0 and 1 summed 10.5 and 10.5 * (1 + 1e-9).
+    c2 = np.array([[10.0, 10.0 * (1 + 1e-9), 1.0], [0.5, 0.5, 0.2]])
+    for m in ([1, 0, 0], [0, 1, 0]):
+        gm.check_group_mask(np.array(m, np.uint8), c2, 1, rel=1e-6)
+    # The oracle's own masks pass on random inputs.
+    r = np.random.default_rng(30)
+    for _ in range(10):
+        h = r.standard_normal((3, 40, 5))
+        norms = 0.5 + r.random(40)
+        k = int(r.integers(1, 40))
+        cs = np.stack([gm.contribution_scores(x, norms) for x in h])
+        gm.check_group_mask(gm.group_mask(h, norms, k), cs, k, rel=0.0)

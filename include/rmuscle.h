@@ -122,6 +122,25 @@ rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_layer_weights 
                               const float *x, float *y, const int32_t *idx, const int32_t *count,
                               int32_t max_count, void *ws, size_t ws_bytes, void *stream);
 
+/* Bytes of device scratch that rm_sparse_ffn_layer_noalloc holds per GPU (32 MiB). */
+#define RM_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+/* rm_sparse_ffn_layer without a workspace argument, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation): the same computation, the same
+ * kernels and the same results bit for bit, with the workspace taken from a device array of
+ * RM_NOALLOC_SCRATCH_BYTES inside the library.  Arguments and errors as for rm_sparse_ffn_layer, minus ws and
+ * ws_bytes, plus:
+ *   - RM_ERR_WORKSPACE, before anything touches the device, when rm_workspace_size(s, B, T, max_count) exceeds
+ *     RM_NOALLOC_SCRATCH_BYTES (every configuration of the action expert in this library fits: at most 15 MiB);
+ *   - RM_ERR_INVALID_ARG when `stream` belongs to a device other than the current one.
+ * The call allocates nothing.  Its first call on a device looks up that device's copy of the array (each GPU has
+ * its own), which stays allocated until the process ends.  Every call on one GPU uses the same array and leaves
+ * its contents behind; the layer needs none of it cleared.  Calls that may overlap on one GPU (several streams,
+ * several threads) race on the array: the caller must order them. */
+rm_status rm_sparse_ffn_layer_noalloc(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B, int32_t T,
+                                      const float *x, float *y, const int32_t *idx, const int32_t *count,
+                                      int32_t max_count, void *stream);
+
 /* L masked FFN layers applied in order (the action expert's layer loop within one denoising step, sections
  * 2.4 and 4.1): layer l reads layer l-1's output.  w is a host array of L weight structs.  idx is
  * int32 [L][B][d_ff] and count int32 [L][B] (one rm_mask_compact call over L*B masks fills both); max_count

@@ -23,6 +23,8 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 # The in-tree build; RMUSCLE_LIB may name another build of the same library (e.g. for A/B timing).
 LIB_PATH = os.environ.get("RMUSCLE_LIB") or os.path.join(PKG_DIR, "librmuscle.so")
 
+NOALLOC_SCRATCH_BYTES = 32 << 20  # RM_NOALLOC_SCRATCH_BYTES
+
 RM_OK = 0
 RM_ERR_INVALID_ARG = -1
 RM_ERR_SHAPE = -2
@@ -41,7 +43,8 @@ RM_KERNEL_DOWN = 1
 RM_KERNEL_SCORES = 2
 RM_KERNEL_GROUP_SELECT = 3
 
-EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_stack",
+EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_layer_noalloc",
+            "rm_sparse_ffn_stack",
             "rm_masked_ffn_layer", "rm_masked_ffn_stack", "rm_dense_ffn_ref", "rm_anchor_ffn_stack",
             "rm_delta_ffn_stack", "rm_gather_stack_rows", "rm_context_select", "rm_context_workspace_size",
             "rm_context_ffn", "rm_context_pack_size", "rm_context_pack", "rm_context_ffn_packed", "rm_neuron_norms",
@@ -92,6 +95,7 @@ def load_library() -> ctypes.CDLL:
         "rm_mask_compact": [vp, i32, i32, vp, vp, vp],
         "rm_workspace_size": [sp, i32, i32, i32, ctypes.POINTER(sz)],
         "rm_sparse_ffn_layer": [sp, wp, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp],
+        "rm_sparse_ffn_layer_noalloc": [sp, wp, i32, i32, vp, vp, vp, vp, i32, vp],
         "rm_sparse_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp],
         "rm_masked_ffn_layer": [sp, wp, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp],
         "rm_masked_ffn_stack": [sp, wp, i32, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp],
@@ -246,6 +250,23 @@ def rm_sparse_ffn_layer(x: torch.Tensor, y: torch.Tensor, layer: Layer, idx: tor
     _check(load_library().rm_sparse_ffn_layer(ctypes.byref(shape), ctypes.byref(w), B, T, x.data_ptr(),
                                               y.data_ptr(), idx.data_ptr(), count.data_ptr(), int(max_count),
                                               wp, wn, _stream(stream)))
+
+
+def rm_sparse_ffn_layer_noalloc(x: torch.Tensor, y: torch.Tensor, layer: Layer, idx: torch.Tensor,
+                                count: torch.Tensor, max_count: int, eps: float = 1e-6, act: str = "silu",
+                                stream=None) -> None:
+    """rm_sparse_ffn_layer with the library's own per-device scratch instead of a workspace (no allocation; calls
+    that may overlap on one GPU must be ordered by the caller)."""
+    shape = _shape(layer, eps, act)
+    B, T = _activations(x, y, shape.d)
+    w = _weights(layer, B)
+    _need_cuda("idx", idx, (torch.int32,))
+    _need_cuda("count", count, (torch.int32,))
+    if idx.numel() != B * shape.d_ff or count.numel() != B:
+        raise ValueError("idx must be [B][d_ff] and count [B]")
+    _check(load_library().rm_sparse_ffn_layer_noalloc(ctypes.byref(shape), ctypes.byref(w), B, T, x.data_ptr(),
+                                                      y.data_ptr(), idx.data_ptr(), count.data_ptr(),
+                                                      int(max_count), _stream(stream)))
 
 
 def _stack_args(x: torch.Tensor, y: torch.Tensor, layers: Sequence[Layer], idx: torch.Tensor,

@@ -9,10 +9,17 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "rm_select.h"
 
 #define RM_EXPORT extern "C" __attribute__((visibility("default")))
+
+// Scratch of rm_sparse_ffn_layer_noalloc, for callers that cannot allocate a workspace: every GPU the library
+// runs on holds its own copy of this array until the process ends, and every call of that entry point on the GPU
+// shares it.  Host code never uses the name itself (on the host it is only a stand-in for the symbol): kernels
+// get the device address that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[RM_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -109,6 +116,36 @@ rm_status check_lists(const rm_ffn_shape *s, int lists, int B, int T, const floa
 
 rm_status hip_fail(hipError_t e, const char *what) {
     return fail(RM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Device address of `scratch` on the current device, looked up once per device (the first call of the no-alloc
+// entry point there) and kept.  The stream must belong to the current device, since each device has its own copy.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+rm_status noalloc_scratch(hipStream_t st, void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(RM_ERR_INVALID_ARG, "device %d outside [0, %d)", dev, kMaxDevices);
+    if (st != nullptr) {
+        int sdev = -1;
+        e = hipStreamGetDevice(st, &sdev);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+        if (sdev != dev)
+            return fail(RM_ERR_INVALID_ARG, "the stream belongs to device %d but device %d is current", sdev, dev);
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress of the no-alloc scratch");
+        if (p == nullptr) return fail(RM_ERR_HIP, "hipGetSymbolAddress returned NULL for the no-alloc scratch");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return RM_OK;
 }
 
 // The layers' output gates must not overlap y (they are read while y is written); checked by every FFN entry
@@ -376,6 +413,31 @@ RM_EXPORT rm_status rm_sparse_ffn_layer(const rm_ffn_shape *s, const rm_ffn_laye
     if (st != RM_OK) return st;
     st = run_layers(p, w, 1, x, y, idx, count, 0, 0, ws, static_cast<hipStream_t>(stream));
     return st == RM_OK ? ok() : st;
+}
+
+RM_EXPORT rm_status rm_sparse_ffn_layer_noalloc(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t B,
+                                                int32_t T, const float *x, float *y, const int32_t *idx,
+                                                const int32_t *count, int32_t max_count, void *stream) {
+    // The scratch the call needs is known from the shape alone: a call that needs more than the array holds
+    // fails here, before anything touches the device.
+    rm_status st = check_shape(s);
+    if (st != RM_OK) return st;
+    if (B <= 0 || T <= 0) return fail(RM_ERR_INVALID_ARG, "B=%d and T=%d must be positive", B, T);
+    if (max_count < 0 || max_count > s->d_ff)
+        return fail(RM_ERR_SHAPE, "max_count=%d outside [0, d_ff=%d]", max_count, s->d_ff);
+    rm::Plan p;
+    st = rm::make_plan(s, B, T, max_count, &p);
+    if (st != RM_OK) return st;
+    if (p.total > RM_NOALLOC_SCRATCH_BYTES)
+        return fail(RM_ERR_WORKSPACE,
+                    "this call needs %zu bytes of scratch; rm_sparse_ffn_layer_noalloc holds %zu (use "
+                    "rm_sparse_ffn_layer with a workspace)",
+                    p.total, static_cast<size_t>(RM_NOALLOC_SCRATCH_BYTES));
+    void *ws = nullptr;
+    st = noalloc_scratch(static_cast<hipStream_t>(stream), &ws);
+    if (st != RM_OK) return st;
+    // The same validation and kernels as the workspace form; the layer path needs no cleared scratch.
+    return rm_sparse_ffn_layer(s, w, B, T, x, y, idx, count, max_count, ws, RM_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 RM_EXPORT rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,

@@ -309,3 +309,27 @@ def test_lists_must_not_overlap_what_the_layer_writes(lib):
     idx = y - 2 * 4096 * 4 - 64
     assert lib.rm_sparse_ffn_stack(ctypes.byref(s), ws_arr, 3, 1, 51, x, y, idx, FAKE, 1229, ws, 1 << 30,
                                    None) == rm.RM_ERR_INVALID_ARG
+
+
+def test_noalloc_layer_rejects_calls_beyond_its_scratch_before_touching_the_device(lib):
+    # rm_sparse_ffn_layer_noalloc sizes the call from the shape alone and refuses one that needs more than
+    # RM_NOALLOC_SCRATCH_BYTES without any device call (this host has no GPU).
+    fake = ctypes.c_void_p(0x100000)
+    w = rm.LayerWeights(0x100000, 0x200000, 0x300000, None, None)
+
+    def call(d, d_ff, wdtype, B, T, k):
+        s = rm.FfnShape(d, d_ff, wdtype, 1e-6, rm.RM_ACT_SILU)
+        return lib.rm_sparse_ffn_layer_noalloc(ctypes.byref(s), ctypes.byref(w), B, T, fake, fake, fake, fake, k,
+                                               None)
+
+    big = (4096, 16384, rm.RM_BF16, 64, 64, 16384)
+    assert _size(*big)[1] > rm.NOALLOC_SCRATCH_BYTES
+    assert call(*big) == rm.RM_ERR_WORKSPACE
+    assert "holds" in rm.last_error() and str(rm.NOALLOC_SCRATCH_BYTES) in rm.last_error()
+    assert call(1000, 4096, rm.RM_BF16, 1, 51, 10) == rm.RM_ERR_SHAPE
+    assert call(1024, 4096, rm.RM_BF16, 1, 51, 4097) == rm.RM_ERR_SHAPE
+    assert call(1024, 4096, rm.RM_BF16, 0, 51, 10) == rm.RM_ERR_INVALID_ARG
+    # Every configuration of the action expert fits.
+    for cfg in ((256, 1024, rm.RM_F32, 1, 8, 256), (1024, 4096, rm.RM_BF16, 1, 51, 1229),
+                (2048, 16384, rm.RM_BF16, 1, 51, 16384), (1024, 4096, rm.RM_BF16, 16, 51, 1229)):
+        assert _size(*cfg)[1] <= rm.NOALLOC_SCRATCH_BYTES

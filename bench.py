@@ -1,10 +1,10 @@
 """Benchmark of the Action Cache sparse-FFN hot path on one MI355X.
 
-Workload (default): one pi0-style action-expert FFN layer, bf16 weights / float32 activations, d = 1024,
-d_ff = 4096, T = 51 tokens (50 actions + 1 state), mask = top 30% of neurons (K = 1229) by mean |SiLU(g) * u| on
-a reference input, evaluated on that input + 0.1 N(0,1).  One step is the whole hot path for one batch:
-rm_masked_ffn_layer, i.e. the compaction of the layer's mask into its index list (in the launch of the layer's
-first kernel) and the masked layer.
+Workload (default): the wide FFN layer, the largest single-GPU configuration: bf16 weights / float32
+activations, d = 2048, d_ff = 16384, T = 51 tokens (50 actions + 1 state), mask = top 30% of neurons (K = 4916) by
+mean |SiLU(g) * u| on a reference input, evaluated on that input + 0.1 N(0,1).  One step is the whole hot path for
+one batch: rm_masked_ffn_layer, i.e. the compaction of the layer's mask into its index list (in the launch of the
+layer's first kernel) and the masked layer.
 
 Weights are cold: every step reads a different one of R copies of the layer (>= 1 GiB together), so neither
 L2 nor the 256 MB Infinity Cache can serve them and the weight bytes come from HBM.  Activations, mask and
@@ -18,9 +18,13 @@ same steps launched one call at a time are reported as eager_us_per_layer.
 The printed JSON line gives value = achieved GB/s on active weight bytes (3 K d * 2 B per step) over the timed
 steps, the roofline of the dominant kernel (its algorithmic bytes / its average duration from HIP events
 recorded around its launches by the library's measurement hook, on the launch stream), and the float64 CPU
-oracle timed on a bounded sample of the same workload.
+oracle timed on a bounded sample of the same workload.  Beside them: the distribution of single-step times (each
+step a graph replay between two events), the mask compaction timed on its own, the bandwidth of a plain streaming
+read on the same GPU (rm_stream_read) and the fraction of it the step reaches, and, for the default workload, the
+per-layer figures of configurations 2, 3 and 5 (secondary; one graph-replayed run each).
 
-Other workloads (--workload): the wide layer d = 2048, d_ff = 16384 at 10/30/50/100% (c4-*); the 18-layer stack
+Other workloads (--workload): config 2's layer d = 1024, d_ff = 4096 (c2); the wide layer at 10/50/100% (c4-*);
+the 18-layer stack
 run through a 10-step denoising schedule, one step of the benchmark being the whole sequence (c3); the same
 sequence with Eq. 4's dense anchors at steps 0 and 5 and anchor-delta updates at the other steps (c3-eq4), also
 with the group's rows copied into compact buffers first (c3-eq4-compact); and
@@ -29,7 +33,7 @@ neuron masks from 5 reference steps of the stack (gm); and the Context Cache's t
 FFN layer (cc).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload c2|c4-10|c4-30|c4-50|c4-100|c3|c3-eq4|c3-eq4-compact|c5|gm|cc]
+                       [--workload c4-30|c2|c4-10|c4-50|c4-100|c3|c3-eq4|c3-eq4-compact|c5|gm|cc]
 """
 from __future__ import annotations
 
@@ -194,6 +198,9 @@ class Setup:
         self.rm.rm_masked_ffn_layer(self.x, self.y, self.layers[i % self.rotate], self.mask, self.idx, self.cnt,
                                     self.k, self.ws)
 
+    def compact(self) -> None:  # the step's mask compaction alone
+        self.rm.rm_mask_compact(self.mask, self.idx, self.cnt)
+
     @property
     def active_bytes(self) -> int:
         return active_weight_bytes(self.k, self.d, 2)
@@ -239,6 +246,12 @@ class StackSetup5:
     def step(self, i: int) -> None:
         self.rm.rm_masked_ffn_stack(self.x, self.y, self.layer_copies[i % self.rotate], self.mask, self.idx, self.cnt,
                                     self.k, self.ws)
+
+    def compact(self) -> None:  # the compaction of the step's L B masks alone
+        self.rm.rm_mask_compact(self.mask, self.idx, self.cnt)
+
+    def useful_flops(self) -> int:  # 3 projections x 2 FLOP per weight per token, each sample's own list
+        return self.L * self.B * 3 * projection_flops(self.T, self.d, self.k)
 
     @property
     def active_bytes(self) -> int:  # distinct rows per layer call (the union of the samples' lists)
@@ -295,11 +308,17 @@ class StackSetup3:
         self.ident_cnt = torch.full((self.L,), self.d_ff, dtype=torch.int32, device=device)
         self.layer_steps = self.steps * self.L
 
+    # The measurement hook is armed inside the step, right before step 2's stack (the first step that only reads
+    # its lists), so the timed launches are layer 0's sparse gate/up and down.
+    arm_inside = True
+
     def step(self, i: int) -> None:
         rm, layers = self.rm, self.layer_copies[i % self.rotate]
         rm.rm_sparse_ffn_stack(self.xs[0], self.y, layers, self.ident, self.ident_cnt, self.d_ff, self.ws_dense)
         for s in range(1, self.steps):
             r = (s - 1) // 2
+            if s == 2:
+                _arm(self)
             if s in self.refresh:
                 rm.rm_masked_ffn_stack(self.xs[s], self.y, layers, self.masks[r], self.idx[r], self.cnt[r], self.k,
                                        self.ws)
@@ -311,8 +330,11 @@ class StackSetup3:
         return self.L * (active_weight_bytes(self.d_ff, self.d, 2)
                          + (self.steps - 1) * active_weight_bytes(self.k, self.d, 2))
 
-    def hooks(self):  # the first gate/up and down launches of a step: layer 0 of the dense step
-        return ffn_hooks(self.rm, gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2))
+    def compact(self) -> None:  # one refresh's compaction of the 18 layer masks alone
+        self.rm.rm_mask_compact(self.masks[0], self.idx[0], self.cnt[0])
+
+    def hooks(self):  # layer 0's gate/up and down of step 2 (a sparse step on the refreshed lists)
+        return ffn_hooks(self.rm, gateup_bytes(self.k, self.d, 2), down_bytes(self.k, self.d, 2))
 
 
 class StackSetupEq4:
@@ -368,8 +390,16 @@ class StackSetupEq4:
                 rm.rm_anchor_ffn_stack(self.xs[s], self.y, layers, self.idx[g], self.cnt[g], self.k, self.ya,
                                        self.ha, self.ws_dense)
             else:
+                if s == 1:
+                    _arm(self)
                 rm.rm_delta_ffn_stack(self.xs[s], self.y, layers, self.idx[g], self.cnt[g], self.k, self.ya,
                                       self.ha, self.ws)
+
+    # The measurement hook is armed inside the step, right before step 1 (the first Eq. 4 delta step).
+    arm_inside = True
+
+    def compact(self) -> None:  # one group's compaction of the 18 layer masks alone
+        self.rm.rm_mask_compact(self.masks[0], self.idx[0], self.cnt[0])
 
     @property
     def active_bytes(self) -> int:  # anchors read every row, later steps the listed rows
@@ -377,8 +407,8 @@ class StackSetupEq4:
         return self.L * (n_anchor * active_weight_bytes(self.d_ff, self.d, 2)
                          + (self.steps - n_anchor) * active_weight_bytes(self.k, self.d, 2))
 
-    def hooks(self):  # the first gate/up and down launches of a step: layer 0 of the first anchor
-        return ffn_hooks(self.rm, gateup_bytes(self.d_ff, self.d, 2), down_bytes(self.d_ff, self.d, 2))
+    def hooks(self):  # layer 0's gate/up and down of step 1 (the first delta step, on the group's lists)
+        return ffn_hooks(self.rm, gateup_bytes(self.k, self.d, 2), down_bytes(self.k, self.d, 2))
 
 
 class StackSetupEq4Compact(StackSetupEq4):
@@ -414,6 +444,8 @@ class StackSetupEq4Compact(StackSetupEq4):
                 clayers = [(self.compact[g][l, 0], self.compact[g][l, 1], self.compact[g][l, 2], layers[l][3])
                            for l in range(self.L)]
             else:
+                if s == 1:
+                    _arm(self)
                 rm.rm_delta_ffn_stack(self.xs[s], self.y, clayers, self.ident, self.cnt[g], self.k, self.ya,
                                       self.ha, self.ws_c)
 
@@ -548,6 +580,14 @@ class GroupMaskSetup:
                 (rm.RM_KERNEL_GROUP_SELECT, "top-K, union and rerank (group_select_kernel)", "select", select_bytes)]
 
 
+def _arm(setup) -> None:
+    """Arms the measurement hook's events for the current step, where a setup does so inside its step."""
+    fn = getattr(setup, "arm", None)
+    if fn is not None:
+        fn()
+        setup.arm = None
+
+
 def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
     """Time `steps` steps after `warmup` untimed ones.  With hook=True, also hand the library a pair of HIP events
     for every gate/up and down launch (it launches them with hipExtLaunchKernel, which stamps the kernel's own
@@ -575,8 +615,13 @@ def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
     start.record()
     for i in range(steps):
         if hook:
-            for kk, pairs in evs.items():
-                rm.rm_profile_kernel_events(kk, pairs[i][0].cuda_event, pairs[i][1].cuda_event)
+            def arm(i=i):
+                for kk, pairs in evs.items():
+                    rm.rm_profile_kernel_events(kk, pairs[i][0].cuda_event, pairs[i][1].cuda_event)
+            if getattr(setup, "arm_inside", False):
+                setup.arm = arm
+            else:
+                arm()
         setup.step(warmup + i)
     end.record()
     torch.cuda.synchronize()
@@ -632,6 +677,102 @@ def time_graph(setup: Setup, steps: int, warmup: int):
     end.record()
     torch.cuda.synchronize()
     return start.elapsed_time(end) / steps
+
+
+def time_step_distribution(setup, blocks: int = 40):
+    """Per-step times: graphs of `block` consecutive steps (8 for a single layer, whose step is tens of
+    microseconds, so that one graph launch and one pair of events are spread over 8 steps; 1 for a stack), each of
+    `blocks` replays between two events, all queued behind a spin kernel so that they run back to back.  Returns
+    (median, p10, p90) of the per-step mean of each block in microseconds, and the block length."""
+    import torch
+    block = 8 if setup.layer_steps == 1 else 1
+    n_graphs = max(1, setup.rotate // block) if setup.rotate % block == 0 else setup.rotate
+    graphs = [_capture(setup, j * block, block) for j in range(n_graphs)]
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(blocks)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(2e6) * max(1, blocks // 4))
+    for i, (a, b) in enumerate(evs):
+        a.record()
+        graphs[i % n_graphs].replay()
+        b.record()
+    torch.cuda.synchronize()
+    us = np.array([a.elapsed_time(b) for a, b in evs]) * 1e3 / block
+    del graphs
+    return float(np.median(us)), float(np.percentile(us, 10)), float(np.percentile(us, 90)), block
+
+
+def time_compaction(setup, reps: int = 64) -> float:
+    """Microseconds per call of the step's mask compaction alone (rm_mask_compact of its masks), from a graph of
+    `reps` calls replayed a few times."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        setup.compact()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            setup.compact()
+    g.replay()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(4):
+        g.replay()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) * 1e3 / (4 * reps)
+
+
+def stream_read_gbs(device, gib: int = 2, reps: int = 8) -> dict:
+    """Bandwidth of a plain streaming read (rm_stream_read) of a `gib` GiB buffer on this GPU: the best of a few
+    grid sizes, each the median of `reps` timed reads (every read is cold: the buffer is 8x the Infinity Cache)."""
+    import torch
+    import paper_2609_19104_amd as rm
+    buf = torch.empty(gib << 30, dtype=torch.uint8, device=device)
+    best = None
+    for wg in (1024, 2048, 4096, 8192):
+        sink = torch.empty(wg * 512, dtype=torch.int32, device=device)
+        rm.rm_stream_read(buf, wg, sink)
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            rm.rm_stream_read(buf, wg, sink)
+            b.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        gbs = buf.numel() / (float(np.median(times)) * 1e-3) / 1e9
+        if best is None or gbs > best["gbs"]:
+            best = {"gbs": round(gbs, 1), "workgroups": wg}
+    del buf
+    torch.cuda.empty_cache()
+    best["bytes"] = gib << 30
+    return best
+
+
+def secondary_lines(device, steps: int, warmup: int) -> dict:
+    """Per-layer figures of configurations 2, 3 and 5, one graph-replayed timing each (cold weights)."""
+    import torch
+    out = {}
+    for key, cls in (("c2", Setup), ("c3", StackSetup3), ("c5", StackSetup5)):
+        setup = cls(key, device, cold=True)
+        ms = time_graph(setup, steps, warmup)
+        gbs = setup.active_bytes / (ms * 1e-3) / 1e9
+        line = {"workload": setup.spec["name"], "us_per_layer": round(ms * 1e3 / setup.layer_steps, 3),
+                "gbs_active": round(gbs, 1), "pct_of_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
+                "compaction_us": round(time_compaction(setup), 3)}
+        if isinstance(setup, StackSetup5):
+            line["per_sample_gbs"] = round(setup.per_sample_bytes / (ms * 1e-3) / 1e9, 1)
+            line["mfma_frac"] = round(setup.useful_flops() / (ms * 1e-3) / (BF16_PEAK_TFLOPS * 1e12), 4)
+        out[key] = line
+        del setup
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return out
 
 
 def kernel_source_digest() -> str:
@@ -722,7 +863,9 @@ def main(argv=None) -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="c4-30", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the per-layer figures of configurations 2, 3 and 5 (default workload only)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true",
@@ -775,9 +918,13 @@ def main(argv=None) -> int:
         achieved, peak, unit = dom_bytes / (dom_us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s"
     value = setup.active_bytes / (ms * 1e-3) / 1e9
 
+    step_med, step_p10, step_p90, step_block = time_step_distribution(setup)
+    compact_us = time_compaction(setup) if hasattr(setup, "compact") else None
+
     setup.rotate = 1
     warm_ms = time_graph(setup, args.steps, args.warmup)
     setup.rotate = setup.copies
+    stream = stream_read_gbs(dev)
 
     out = {
         "metric": "µs per sparse FFN layer + achieved HBM GB/s (% of peak) on active weights",
@@ -804,6 +951,14 @@ def main(argv=None) -> int:
         "tokens_per_s": round(setup.B * setup.T * setup.layer_steps / (ms * 1e-3), 1),
         "active_weight_bytes": setup.active_bytes,
         "warm_us_per_layer": round(warm_ms * 1e3 / setup.layer_steps, 3),
+        "step_us": {"median": round(step_med, 3), "p10": round(step_p10, 3), "p90": round(step_p90, 3),
+                    "how": f"40 graph replays of {step_block} consecutive step(s), each between two events and "
+                           f"divided by {step_block}, queued back to back"},
+        "compaction_us": None if compact_us is None else round(compact_us, 3),
+        "stream_read": {"gbs": stream["gbs"], "workgroups": stream["workgroups"], "bytes": stream["bytes"],
+                        "pct_of_peak": round(100.0 * stream["gbs"] / HBM_PEAK_GBS, 2),
+                        "kernel": "rm_stream_read (plain streaming read, 16 B per lane, 8 loads in flight)"},
+        "pct_of_stream_read": round(100.0 * value / stream["gbs"], 2),
         "kernel_us": {f"{key}{suffix}": round(kern[kid][stat], 3) for kid, _, key, _ in hooks
                       for suffix, stat in (("", "mean"), ("_median", "median"), ("_min", "min"), ("_p10", "p10"),
                                            ("_p90", "p90"))},
@@ -817,10 +972,16 @@ def main(argv=None) -> int:
     if isinstance(setup, StackSetup5):
         out["per_sample_weight_bytes"] = setup.per_sample_bytes
         out["per_sample_value"] = round(setup.per_sample_bytes / (ms * 1e-3) / 1e9, 2)
+        out["mfma_frac"] = round(setup.useful_flops() / (ms * 1e-3) / (BF16_PEAK_TFLOPS * 1e12), 4)
     if isinstance(setup, GroupMaskSetup):
         out["coverage"] = setup.coverage()
     if not args.no_cpu_baseline and isinstance(setup, Setup):
         out["cpu_baseline"] = cpu_baseline(setup, args.cpu_seconds)
+    if args.workload == ap.get_default("workload") and not args.no_secondary:
+        del setup
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        out["secondary"] = secondary_lines(dev, args.steps, args.warmup)
     print(json.dumps(out))
     return 0
 

@@ -319,6 +319,13 @@ typedef enum rm_kernel_id {
 } rm_kernel_id;
 rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end);
 
+/* Measurement: a plain streaming read of `bytes` of `buf` (16-byte aligned, bytes a positive multiple of 16) by
+ * `workgroups` workgroups of 512 threads, each lane keeping eight 16-byte loads in flight.  It computes nothing
+ * the caller uses: sink (uint32 [workgroups * 512], 4-byte aligned, not overlapping buf) is written only in the
+ * practically impossible case that a lane's XOR of its loads equals a fixed magic number.  Used to state the hot
+ * path's bandwidth as a fraction of a bare read on the same GPU.  workgroups in [1, 1 << 20]. */
+rm_status rm_stream_read(const void *buf, size_t bytes, int32_t workgroups, uint32_t *sink, void *stream);
+
 /* Static description of a status code. */
 const char *rm_status_string(rm_status status);
 

@@ -49,7 +49,7 @@ EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_s
             "rm_delta_ffn_stack", "rm_gather_stack_rows", "rm_context_select", "rm_context_workspace_size",
             "rm_context_ffn", "rm_context_pack_size", "rm_context_pack", "rm_context_ffn_packed", "rm_neuron_norms",
             "rm_group_masks",
-            "rm_profile_kernel_events",
+            "rm_profile_kernel_events", "rm_stream_read",
             "rm_status_string", "rm_last_error")
 
 # (w_gate, w_up, w_down, norm_g) or (w_gate, w_up, w_down, norm_g, out_gate); norm_g and out_gate may be None.
@@ -112,6 +112,7 @@ def load_library() -> ctypes.CDLL:
         "rm_neuron_norms": [vp, i32, i32, i32, vp, vp],
         "rm_group_masks": [vp, i32, i32, i32, i32, vp, i32, vp, vp, vp],
         "rm_profile_kernel_events": [i32, vp, vp],
+        "rm_stream_read": [vp, sz, i32, vp, vp],
         "rm_status_string": [i32],
         "rm_last_error": [],
     }
@@ -531,3 +532,15 @@ def rm_group_masks(h: torch.Tensor, norms: torch.Tensor, k: int, scores: torch.T
 def rm_profile_kernel_events(kernel: int, ev_begin: Optional[int], ev_end: Optional[int]) -> None:
     """Arm raw hipEvent_t handles around the next launch of `kernel` (an RM_KERNEL_* id)."""
     _check(load_library().rm_profile_kernel_events(kernel, ev_begin, ev_end))
+
+
+def rm_stream_read(buf: torch.Tensor, workgroups: int, sink: torch.Tensor, stream=None) -> None:
+    """Measurement: a plain streaming read of the whole of `buf` (any dtype, 16-byte multiple); sink int32/uint8
+    scratch of at least workgroups * 512 * 4 bytes."""
+    if buf.device.type != "cuda" or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    _need_cuda("sink", sink, (torch.int32, torch.uint8))
+    if sink.numel() * sink.element_size() < workgroups * 512 * 4:
+        raise ValueError("sink must hold workgroups * 512 uint32")
+    _check(load_library().rm_stream_read(buf.data_ptr(), buf.numel() * buf.element_size(), int(workgroups),
+                                         sink.data_ptr(), _stream(stream)))

@@ -831,6 +831,19 @@ RM_EXPORT rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, voi
     return ok();
 }
 
+RM_EXPORT rm_status rm_stream_read(const void *buf, size_t bytes, int32_t workgroups, uint32_t *sink, void *stream) {
+    if (!buf || !sink) return fail(RM_ERR_INVALID_ARG, "buf or sink is NULL");
+    if (bytes == 0 || bytes % 16 != 0) return fail(RM_ERR_SHAPE, "bytes=%zu must be a positive multiple of 16", bytes);
+    if (workgroups < 1 || workgroups > (1 << 20))
+        return fail(RM_ERR_SHAPE, "workgroups=%d outside [1, %d]", workgroups, 1 << 20);
+    if (!aligned(buf, 16) || !aligned(sink, 4)) return fail(RM_ERR_ALIGN, "buf must be 16-byte and sink 4-byte aligned");
+    if (ranges_overlap(buf, bytes, sink, static_cast<size_t>(workgroups) * 512 * 4))
+        return fail(RM_ERR_INVALID_ARG, "sink overlaps buf");
+    const hipError_t e = rm::launch_stream_read(buf, bytes, workgroups, sink, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "stream read launch");
+    return ok();
+}
+
 RM_EXPORT const char *rm_status_string(rm_status status) {
     switch (status) {
         case RM_OK: return "RM_OK";

@@ -162,6 +162,9 @@ hipError_t launch_epilogue(const Plan &p, const int32_t *count, const float *x, 
                            bool emit_xn, const float *ya_in, float *ya_out, const float *out_gate, void *ws,
                            hipStream_t st);
 
+// Streaming read of bytes (a multiple of 16) of buf by `workgroups` workgroups of 512 threads (measure.hip).
+hipError_t launch_stream_read(const void *buf, size_t bytes, int workgroups, uint32_t *sink, hipStream_t st);
+
 // Profiling hook: the events armed by rm_profile_kernel_events for the next launch of `kernel` by this thread
 // (null when disarmed), which are disarmed by taking them.
 void profile_take(int kernel, hipEvent_t *begin, hipEvent_t *end);

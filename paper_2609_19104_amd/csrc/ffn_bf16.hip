@@ -100,11 +100,12 @@ __device__ __forceinline__ int lane_neuron(const GuArgs &a, int b, int slot) {
 
 // Writes h for 8 neurons x 64 tokens of token block t0 from the summed tile; slots at or past the count and
 // tokens at or past T get h = 0 (their rows and columns were computed from clamped loads).  H is chunk-major
-// (32-slot chunks, then tokens), so the 8 slots of a token are 16 contiguous bytes.
+// (32-slot chunks, then tokens).  Thread tid finishes tile row tid & 7 (its gate row; the up row is 8 further) for
+// token tid >> 3, whose list slot is `slot` (< 0: a duplicate row, nothing stored).
 // red(w, tt, lane) is d-part w's tile tt (lane L, register i = row 4 (L / 16) + i, token L % 16).
 template <int NT, typename RedAt>
 __device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, int b, RedAt red, int ds, int t0,
-                                           int slot_base, int cnt, const float *rn) {
+                                           int slot, int cnt, const float *rn) {
     const int j = threadIdx.x & 7;
     const int tok = threadIdx.x >> 3;
     const int tt = tok >> 4, tc = tok & 15;
@@ -122,7 +123,7 @@ __device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, int b,
         const float r = rn[tok];
         h = rm_glu_act(a.act, gsum * r) * (usum * r);
     }
-    const int slot = slot_base + j;
+    if (slot < 0) return;
     const int t = t0 + tok;
     const bool live = slot < cnt && t < a.T;
     const size_t ai = (static_cast<size_t>(b) * a.max_count + slot) * a.T + t;  // [b][slot][t] when live
@@ -257,7 +258,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
             load_rnorm(a, b, t0, rn);
         }
         __syncthreads();
-        gu_store_h<NT>(a, Hb, b, red, kGuWaves, t0, slot0, cnt, rn);
+        gu_store_h<NT>(a, Hb, b, red, kGuWaves, t0, slot0 + (tid & 7), cnt, rn);
         t0 += rm::kBfTokBlock;
         if (kOneBlock || t0 >= a.T) break;
         __syncthreads();  // every wave has read the tiles before the regions are refilled
@@ -371,7 +372,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
 #pragma unroll
         for (int gg = 0; gg < NG; ++gg) {
             auto red_g = [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; };
-            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8, cnt, rn);
+            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8 + (tid & 7), cnt, rn);
         }
         __syncthreads();
     }
@@ -471,7 +472,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
 #pragma unroll
         for (int gg = 0; gg < NG; ++gg) {
             auto red_g = [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; };
-            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8, cnt, rn);
+            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8 + (tid & 7), cnt, rn);
         }
         __syncthreads();
     }
@@ -598,7 +599,168 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg)
         gu_store_h<NT>(a, Hb, b, [&](int w2, int tt, int l) -> const rm_f32x4 & { return red(gg, w2, tt, l); }, DS, 0,
-                       blk0 + gg * 8, cnt, rn);
+                       blk0 + gg * 8 + (tid & 7), cnt, rn);
+}
+
+// ------------------------------------------------------------------------------------------ gate / up, spread
+
+// For one sample's lists of more than 256 groups of 8 listed slots (T <= 64, d = 256 NCH with NCH in {1, 2, 4,
+// 8}): G workgroups (one per compute unit).  The list is cut into quads of 4 consecutive slots, dealt round-robin:
+// workgroup q takes quads q, q + G, q + 2G, ... (m or m + 1 of them), so the weight bytes per compute unit differ
+// by at most one quad.  Two quads fill one 16-row weight tile (tile rows 0-3 and 8-11: the first quad's gate and
+// up rows, rows 4-7 and 12-15 the second's); an odd last quad is paired with itself, its duplicate rows coalescing
+// with the originals in the same load instruction, and only one copy of h is stored.  Every compute unit streams
+// weights, and all the workgroup's tiles share each staged chunk of the FFN input.  Wave w takes columns
+// [32 w, 32 w + 32) of every 256-column chunk for all the tiles.  The chunk pipeline is the pipelined kernel's
+// (weights and input of a chunk issued ahead, rotated chunk order); each tile's 8 wave partials are added in wave
+// order through LDS.
+template <int NG, int NCH>
+__device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G, int nquads,
+                                                   uint16_t (*xs)[64 * kRowPitch], float *rn) {
+    constexpr int NT = 4;
+#ifndef RM_SPREAD_WTILES
+#define RM_SPREAD_WTILES 9
+#endif
+#ifndef RM_SPREAD_PX
+#define RM_SPREAD_PX 6
+#endif
+    constexpr int PW0 = RM_SPREAD_WTILES / (NG > 0 ? NG : 1);  // weight chunks in flight
+    constexpr int PW = PW0 < 1 ? 1 : (PW0 < NCH ? PW0 : NCH);
+    constexpr int PX = RM_SPREAD_PX < NCH ? RM_SPREAD_PX : NCH;  // input chunks in flight
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int r = lane & 15;
+    const int grp = lane >> 4;
+    const int cnt = clamp_count(a.count[0], a.max_count);
+    // Tile j: quads 2j and 2j + 1 of this workgroup (the second is the first again when it does not exist).
+    auto quad_of = [&](int j, int half) {
+        const int k = min(2 * j + half, nquads - 1);
+        return q + k * G;
+    };
+    int raw_n[NG];
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+        const int k = min(2 * j + ((r >> 2) & 1), nquads - 1);  // local quad of this lane's row
+        raw_n[j] = a.idx[min((q + k * G) * 4 + (r & 3), a.d_ff - 1)];
+    }
+    __builtin_amdgcn_sched_barrier(0);  // the index loads go out first
+    const int rot = q & (NCH - 1);
+    rm_u32x4 xv[PX][4], w[PW][NG];
+    const uint16_t *wrow[NG];
+    // Chunk c of the input: 64 token rows (rows past T repeat the last token) x 256 columns in 16-byte pieces.
+    auto load_x = [&](int c) {
+        const int col = ((c + rot) & (NCH - 1)) * kChunkCols;
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+            const int e = tid + qq * kGuThreads;
+            const int t = min(e >> 5, a.T - 1);
+            xv[c % PX][qq] = load16(a.xn + static_cast<size_t>(t) * a.d + col + (e & 31) * 8);
+        }
+    };
+    auto store_x = [&](int c) {  // into LDS buffer c & 1
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+            const int e = tid + qq * kGuThreads;
+            *reinterpret_cast<rm_u32x4 *>(&xs[c & 1][(e >> 5) * kRowPitch + (e & 31) * 8]) = xv[c % PX][qq];
+        }
+    };
+    auto load_w = [&](int c) {
+        const int col = ((c + rot) & (NCH - 1)) * kChunkCols;
+#pragma unroll
+        for (int j = 0; j < NG; ++j) w[c % PW][j] = load16(wrow[j] + col);
+    };
+    // The input of the first chunks goes out before the wait for the indices, then the weights.
+#pragma unroll
+    for (int c = 0; c < PX; ++c) load_x(c);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < NG; ++j)
+        wrow[j] = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(clamp_neuron(raw_n[j], a.d_ff)) * a.d + wave * 32 +
+                  grp * 8;
+#pragma unroll
+    for (int c = 0; c < PW; ++c) load_w(c);
+    constexpr bool kPreNorm = NCH <= 4 && NG <= 2;
+    float4 ssq_v[NCH];
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) ssq_v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (kPreNorm && a.ssq != nullptr && __builtin_amdgcn_readfirstlane(wave) == 0) {
+        const float4 *p =
+            reinterpret_cast<const float4 *>(a.ssq + static_cast<size_t>(min(lane, a.T - 1)) * rm::ssq_stride(a.d));
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) ssq_v[i] = p[i];
+    }
+
+    rm_f32x4 acc[NG][NT];
+#pragma unroll
+    for (int j = 0; j < NG; ++j)
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) acc[j][tt] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        // Buffer c & 1 was last read in chunk c - 2, before every wave passed chunk c - 1's barrier.
+        store_x(c);
+        __syncthreads();
+        if (c + PX < NCH) load_x(c + PX);
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) {
+            const rm_u32x4 bx =
+                *reinterpret_cast<const rm_u32x4 *>(&xs[c & 1][(tt * 16 + r) * kRowPitch + wave * 32 + grp * 8]);
+#pragma unroll
+            for (int j = 0; j < NG; ++j) acc[j][tt] = mfma_bf16(w[c % PW][j], bx, acc[j][tt]);
+        }
+        if (c + PW < NCH) load_w(c + PW);
+    }
+    if (!kPreNorm) {
+        load_rnorm(a, 0, 0, rn);
+    } else if (wave == 0) {
+        float rr = 1.0f;
+        if (a.ssq != nullptr && lane < a.T) {
+            float ss = 0.0f;
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                ss += ssq_v[i].x;
+                ss += ssq_v[i].y;
+                ss += ssq_v[i].z;
+                ss += ssq_v[i].w;
+            }
+            rr = rm_rnorm_from_ssq(ss, a.d, a.eps);
+        }
+        rn[lane] = rr;
+    }
+    // The waves' partial tiles of tile j go through LDS (in the input buffers, free once every wave has passed the
+    // barrier below) and are added in wave order.
+    rm_f32x4 *red = reinterpret_cast<rm_f32x4 *>(&xs[0][0]);
+    const int jj = tid & 7;  // the tile row (neuron) this thread stores
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+        __syncthreads();  // the input tiles (j = 0) or tile j - 1's sums have been read
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) red[(wave * NT + tt) * 64 + lane] = acc[j][tt];
+        __syncthreads();
+        const bool dup = jj >= 4 && 2 * j + 1 >= nquads;  // the second half repeats the first quad
+        const int slot = dup ? -1 : quad_of(j, jj >> 2) * 4 + (jj & 3);
+        gu_store_h<NT>(a, a.H, 0,
+                       [&](int w2, int tt, int l) -> const rm_f32x4 & { return red[(w2 * NT + tt) * 64 + l]; },
+                       kGuWaves, 0, slot, cnt, rn);
+    }
+}
+
+// NG: tiles of the workgroups with the most quads (ceil(max quads / 2)).  A workgroup's own quad count m or m + 1
+// decides its tile count, uniformly over the workgroup.
+template <int NG, int NCH>
+__global__ __launch_bounds__(kGuThreads) void gateup_spread_kernel(GuArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][64 * kRowPitch];
+    __shared__ float rn[64];
+    static_assert(sizeof(rm_f32x4) * kGuWaves * 4 * 64 <= sizeof(xs), "reduction tiles must fit the input tile");
+    const int G = gridDim.x;
+    const int q = blockIdx.x;
+    const int nq = a.kcap / 4;
+    const int mine = (nq - q + G - 1) / G;  // quads of this workgroup, >= 1
+    if ((mine + 1) / 2 == NG)
+        gateup_spread_body<NG, NCH>(a, q, G, mine, xs, rn);
+    else if constexpr (NG > 1)
+        gateup_spread_body<NG - 1, NCH>(a, q, G, mine, xs, rn);
 }
 
 // ------------------------------------------------------------------------------------------ down
@@ -1015,11 +1177,13 @@ hipError_t launch_gateup_nt(const rm::Plan &p, const GuArgs &a, hipStream_t st) 
 
 namespace rm {
 
+static hipError_t launch_gateup_args(const Plan &p, const GuArgs &a, hipStream_t st);
+
 hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_up, const int32_t *idx,
                               const int32_t *count, bool norm, const float *h_anchor, float *h_out, void *ws,
                               hipStream_t st) {
     char *base = static_cast<char *>(ws);
-    GuArgs a;
+    GuArgs a{};
     a.wg = static_cast<const uint16_t *>(w_gate);
     a.wu = static_cast<const uint16_t *>(w_up);
     a.xn = reinterpret_cast<const uint16_t *>(base + p.off_xn);
@@ -1038,7 +1202,27 @@ hipError_t launch_gateup_bf16(const Plan &p, const void *w_gate, const void *w_u
     a.H = reinterpret_cast<uint16_t *>(base + p.off_h);
     a.h_anchor = h_anchor;
     a.h_out = h_out;
+    return launch_gateup_args(p, a, st);
+}
+
+static hipError_t launch_gateup_args(const Plan &p, const GuArgs &a, hipStream_t st) {
     hipError_t e;
+    if (p.gate_spread > 0) {  // one sample, T <= 64, d = 256 NCH (the plan's conditions)
+        const dim3 grid(p.gate_blocks), block(kGuThreads);
+#define RM_SPREAD(NG)                                                                                       \
+    switch (p.d / kChunkCols) {                                                                             \
+        case 1: e = launch_timed(RM_KERNEL_GATEUP, gateup_spread_kernel<NG, 1>, grid, block, st, a); break; \
+        case 2: e = launch_timed(RM_KERNEL_GATEUP, gateup_spread_kernel<NG, 2>, grid, block, st, a); break; \
+        case 4: e = launch_timed(RM_KERNEL_GATEUP, gateup_spread_kernel<NG, 4>, grid, block, st, a); break; \
+        default: e = launch_timed(RM_KERNEL_GATEUP, gateup_spread_kernel<NG, 8>, grid, block, st, a); break; \
+    }
+        if (p.gate_spread == 2)  // the plan's range: 2 or 3 tiles
+            RM_SPREAD(2)
+        else
+            RM_SPREAD(3)
+#undef RM_SPREAD
+        return e != hipSuccess ? e : hipGetLastError();
+    }
     switch (token_tiles(p.T)) {
         case 1: e = launch_gateup_nt<1>(p, a, st); break;
         case 2: e = launch_gateup_nt<2>(p, a, st); break;

@@ -284,6 +284,12 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         // direct kernel, when d allows) for short lists.
         const int k32 = ceil_div(kmax, kBfChunk) * kBfChunk;
         const bool direct_ok = s->d == 256 || s->d == 512 || s->d == 1024 || s->d == 2048;
+        // One sample with more groups of 8 slots than compute units (up to 3 per unit): the spread kernel, one
+        // workgroup per compute unit taking quads of 4 slots round-robin, so that every unit streams weights and
+        // the units' weight bytes differ by one quad at most.
+        const int n8 = k32 / 8;
+        const bool spread = RM_GATEUP_SPREAD && B == 1 && T <= kBfTokBlock && direct_ok && n8 > kCUs &&
+                            n8 <= 3 * kCUs;
         auto groups_of = [&](int ng) { return static_cast<long long>(B) * ceil_div(k32, 8 * ng); };
         q.gate_groups = 0;
         for (int ng : {8, 4, 2})
@@ -299,6 +305,12 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         }
         q.kcap = ceil_div(k32, std::max(kBfChunk, 8 * q.gate_groups)) * std::max(kBfChunk, 8 * q.gate_groups);
         q.gate_blocks = q.kcap / (8 * q.gate_groups);
+        if (spread) {
+            q.gate_groups = 1;
+            q.kcap = k32;
+            q.gate_spread = (ceil_div(k32 / 4, kCUs) + 1) / 2;  // 16-row tiles of the fullest workgroup
+            q.gate_blocks = kCUs;
+        }
         q.col_tile = kBfColTile;
         q.ncol = ceil_div(s->d, q.col_tile);
         const int nchunks = q.kcap / kBfChunk;

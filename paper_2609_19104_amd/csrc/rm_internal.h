@@ -17,6 +17,11 @@ namespace rm {
 // function sizes the workspace and every launch, so they always agree.
 // ---------------------------------------------------------------------------------------------------------
 
+// The spread gate/up kernel for long single-sample lists (set to 0 at build time to compare without it).
+#ifndef RM_GATEUP_SPREAD
+#define RM_GATEUP_SPREAD 1
+#endif
+
 // bf16 path: 16x16x32 bf16 matrix-core tiles.
 constexpr int kBfTokBlock = 64;     // tokens per accumulator block (4 tiles of 16)
 constexpr int kBfNeurPerBlk = 8;    // neurons per gate/up workgroup (8 gate rows + 8 up rows = one 16-row tile)
@@ -49,6 +54,10 @@ struct Plan {
     int kcap = 0;        // row length of H (neuron slots), max_count rounded up
     int gate_groups = 1; // bf16 gate/up: groups of 8 neurons per workgroup (1 = direct, 2/4/8 = LDS-staged)
     int gate_blocks = 0; // gate/up workgroups per sample
+    // bf16, one sample, 257 .. 768 groups of 8 listed slots: the spread gate/up kernel, gate_blocks (= one per
+    // compute unit) workgroups taking quads of 4 slots round-robin, in at most gate_spread 16-row tiles each (0 =
+    // not used).
+    int gate_spread = 0;
     int col_tile = 0;    // output columns per down workgroup
     int ncol = 0;        // column tiles
     int slices = 0;      // K-slices per column tile (down partial sums)

@@ -92,6 +92,12 @@ BF16_CASES = [
     # T > 64 at d = 2048 and d = 768: the staged kernel with eight and three column chunks
     (2048, 4096, 100, 1500, "random"),
     (768, 2048, 90, 700, "ones"),
+    # one sample with 256 .. 1024 groups of 8 slots: the spread gate/up kernel with 2, 3 and 4 groups per
+    # workgroup, 1 to 8 column chunks; a grid with only four workgroups of two groups
+    (2048, 8192, 51, 6000, "random"),
+    (1024, 8192, 64, 8192, "ones"),
+    (256, 4096, 17, 2056, "none"),
+    (512, 4096, 51, 2500, "random"),
 ]
 
 
@@ -281,18 +287,26 @@ MASKED_CASES = [
     (512, 4095, 2, 2, 17, 0.5, "bf16", "ones"),
     (256, 16384, 1, 2, 8, 0.1, "bf16", "none"),
     (128, 300, 3, 2, 9, 0.6, "f32", "random"),
+    # one sample, 257 .. 768 groups of 8 slots: the spread gate/up kernel behind the masked calls
+    (2048, 16384, 1, 1, 51, 0.3, "bf16", "none"),
+    (256, 8192, 1, 1, 40, 0.3, "bf16", "none"),
+    (1024, 4096, 1, 1, 64, 0.6, "bf16", "random"),
+    (512, 6000, 1, 1, 33, 0.4, "bf16", "none"),
 ]
 
 
 @pytest.mark.parametrize("d,d_ff,L,B,T,p,wdtype,norm", MASKED_CASES)
-def test_masked_calls_equal_compaction_then_lists(d, d_ff, L, B, T, p, wdtype, norm):
+@pytest.mark.parametrize("spare", [0, 1], ids=["tight", "max_count_above_count"])
+def test_masked_calls_equal_compaction_then_lists(d, d_ff, L, B, T, p, wdtype, norm, spare):
     # rm_masked_ffn_layer / _stack = rm_mask_compact + rm_sparse_ffn_layer / _stack, bit for bit, and their
-    # lists are the oracle's.
+    # lists are the oracle's; with max_count at the masks' largest count, or well above it (slots past the count).
     layers = [wl.make_layer(71, l, d, d_ff, wdtype, norm=norm) for l in range(L)]
     lws = [dev_weights(l) for l in layers]
     x = wl.make_x(71, (B, T, d), d_ff, T)
     masks = wl.bernoulli_mask(wl.rng(71, 4, d_ff, L), (L * B, d_ff), p)
     max_count = int(masks.sum(axis=1).max())
+    if spare:
+        max_count = min(d_ff, max_count + max_count // 3)
     idx_ref, cnt_ref = oracle.compact_mask(masks)
     xt = torch.from_numpy(x).cuda()
     mt = torch.from_numpy(masks).cuda()

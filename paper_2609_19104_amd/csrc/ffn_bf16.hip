@@ -616,7 +616,7 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
 // order through LDS.
 template <int NG, int NCH>
 __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G, int nquads,
-                                                   uint16_t (*xs)[64 * kRowPitch], float *rn) {
+                                                   uint16_t (*xs)[64 * kRowPitch], rm_f32x4 *red2, float *rn) {
     constexpr int NT = 4;
 #ifndef RM_SPREAD_WTILES
 #define RM_SPREAD_WTILES 9
@@ -728,18 +728,23 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
         }
         rn[lane] = rr;
     }
-    // The waves' partial tiles of tile j go through LDS (in the input buffers, free once every wave has passed the
-    // barrier below) and are added in wave order.
-    rm_f32x4 *red = reinterpret_cast<rm_f32x4 *>(&xs[0][0]);
+    // The waves' partial tiles of every tile go through LDS at once (tiles 0 and 1 in the input buffers, free once
+    // every wave has passed the barrier below, tile 2 in red2) and are added in wave order: one barrier for all.
+    __syncthreads();  // every wave is done with the input tiles
+    auto red_at = [&](int j) -> rm_f32x4 * {
+        return j < 2 ? reinterpret_cast<rm_f32x4 *>(&xs[0][0]) + j * kGuWaves * NT * 64 : red2;
+    };
+#pragma unroll
+    for (int j = 0; j < NG; ++j)
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) red_at(j)[(wave * NT + tt) * 64 + lane] = acc[j][tt];
+    __syncthreads();
     const int jj = tid & 7;  // the tile row (neuron) this thread stores
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
-        __syncthreads();  // the input tiles (j = 0) or tile j - 1's sums have been read
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) red[(wave * NT + tt) * 64 + lane] = acc[j][tt];
-        __syncthreads();
         const bool dup = jj >= 4 && 2 * j + 1 >= nquads;  // the second half repeats the first quad
         const int slot = dup ? -1 : quad_of(j, jj >> 2) * 4 + (jj & 3);
+        const rm_f32x4 *red = red_at(j);
         gu_store_h<NT>(a, a.H, 0,
                        [&](int w2, int tt, int l) -> const rm_f32x4 & { return red[(w2 * NT + tt) * 64 + l]; },
                        kGuWaves, 0, slot, cnt, rn);
@@ -750,17 +755,19 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
 // decides its tile count, uniformly over the workgroup.
 template <int NG, int NCH>
 __global__ __launch_bounds__(kGuThreads) void gateup_spread_kernel(GuArgs a) {
+    static_assert(NG <= 3, "two reduction tiles in the input buffers, a third in red2");
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][64 * kRowPitch];
+    __shared__ rm_f32x4 red2[NG > 2 ? kGuWaves * 4 * 64 : 1];
     __shared__ float rn[64];
-    static_assert(sizeof(rm_f32x4) * kGuWaves * 4 * 64 <= sizeof(xs), "reduction tiles must fit the input tile");
+    static_assert(2 * sizeof(rm_f32x4) * kGuWaves * 4 * 64 <= sizeof(xs), "two reduction tiles fit the input tile");
     const int G = gridDim.x;
     const int q = blockIdx.x;
     const int nq = a.kcap / 4;
     const int mine = (nq - q + G - 1) / G;  // quads of this workgroup, >= 1
     if ((mine + 1) / 2 == NG)
-        gateup_spread_body<NG, NCH>(a, q, G, mine, xs, rn);
+        gateup_spread_body<NG, NCH>(a, q, G, mine, xs, red2, rn);
     else if constexpr (NG > 1)
-        gateup_spread_body<NG - 1, NCH>(a, q, G, mine, xs, rn);
+        gateup_spread_body<NG - 1, NCH>(a, q, G, mine, xs, red2, rn);
 }
 
 // ------------------------------------------------------------------------------------------ down

@@ -271,9 +271,13 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.act = s->act;
     const int kmax = max_count > 0 ? max_count : 1;
     size_t xn_elem, h_elem;
-    // Aim for about four down-projection workgroups per compute unit (256 CUs).
+    // Aim for about two down-projection workgroups per compute unit (256 CUs): fewer K-slices mean fewer
+    // float32 partials written and read back by the epilogue (config 4 at 30%: 10 slices instead of 20).
     constexpr int kCUs = 256;
-    constexpr int kTargetDownGroups = 4 * kCUs;
+#ifndef RM_DOWN_TARGET
+#define RM_DOWN_TARGET (2 * 256)
+#endif
+    constexpr int kTargetDownGroups = RM_DOWN_TARGET;
     if (s->wdtype == RM_BF16) {
         q.tpad = ceil_div(T, kBfTokBlock) * kBfTokBlock;
         // Gate/up workgroups of 8 * NG neurons.  Measured on configs 4 and 5: one round of workgroups that fills

@@ -862,9 +862,13 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
         for (int j = 0; j < 8; ++j) cc.w[j] = load8(a.wd + static_cast<size_t>(n[j]) * a.d + col);
     };
 
-    DnChunk<NT> cb[2];
-    load_h(cb[0], 0, 0);
-    if (CPW > 1) load_h(cb[1], 1, 0);
+#ifndef RM_DOWN_PD
+#define RM_DOWN_PD 2
+#endif
+    constexpr int PD = RM_DOWN_PD < CPW ? RM_DOWN_PD : CPW;  // chunks in flight per wave
+    DnChunk<NT> cb[PD];
+#pragma unroll
+    for (int k = 0; k < PD; ++k) load_h(cb[k], k, 0);
     __builtin_amdgcn_sched_barrier(0);  // then the H tiles, before the wait for the indices
 #pragma unroll
     for (int q = 0; q < kIdxPerThread; ++q) {
@@ -881,16 +885,16 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) acc[tt][q] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 
-        // Two chunks in flight: chunk k + 2 is loaded into chunk k's registers right after chunk k's products.
-        load_w(cb[0], 0);
-        if (CPW > 1) load_w(cb[1], 1);
+        // PD chunks in flight: chunk k + PD is loaded into chunk k's registers right after chunk k's products.
+#pragma unroll
+        for (int k = 0; k < PD; ++k) load_w(cb[k], k);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int k = 0; k < CPW; ++k) {
-            if (c_begin + wave + k * kDnWaves <= c_last) dn_mma(cb[k & 1], acc);
-            if (k + 2 < CPW) {
-                load_h(cb[k & 1], k + 2, t0);
-                load_w(cb[k & 1], k + 2);
+            if (c_begin + wave + k * kDnWaves <= c_last) dn_mma(cb[k % PD], acc);
+            if (k + PD < CPW) {
+                load_h(cb[k % PD], k + PD, t0);
+                load_w(cb[k % PD], k + PD);
             }
         }
 
@@ -928,8 +932,8 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
         t0 += rm::kBfTokBlock;
         if (kOneBlock || t0 >= a.T) break;
         __syncthreads();
-        load_h(cb[0], 0, t0);
-        if (CPW > 1) load_h(cb[1], 1, t0);
+#pragma unroll
+        for (int k = 0; k < PD; ++k) load_h(cb[k], k, t0);
     }
 }
 

@@ -89,10 +89,10 @@ __global__ __launch_bounds__(kThreads) void epilogue_kernel(const float *__restr
     }
     if (xn_next == nullptr) return;
 
-    if (g_next != nullptr) {  // partial sums of squares of the row's 64-column blocks (lane 16 j: block 4 blk + j)
-        const float ss = rm_ssq64(out, ok);
-        const int part = blk * 4 + static_cast<int>(threadIdx.x >> 4);
-        if ((threadIdx.x & 15) == 0 && part < rm::ssq_parts(d))
+    if (g_next != nullptr) {  // partial sums of squares of the row's 32-column blocks (lane 8 j: block 8 blk + j)
+        const float ss = rm_ssq32(out, ok);
+        const int part = blk * 8 + static_cast<int>(threadIdx.x >> 3);
+        if ((threadIdx.x & 7) == 0 && part < rm::ssq_parts(d))
             ssq[static_cast<size_t>(row) * rm::ssq_stride(d) + part] = ss;
         if (ok) {
             const float4 g = ld4(g_next + cc);

@@ -30,6 +30,8 @@
 //   columns are physical columns 4 n + q.  No LDS transpose is needed, and 16 lanes read a full 128-byte line
 //   of a row.  The four waves take interleaved chunks; their tiles are summed in LDS in a fixed order and the
 //   slice's float32 partial is stored.  The epilogue kernel adds the slices in order to the residual.
+//   down_fused: for lists of at most 64 chunks, one workgroup sums the whole list for its tile (32 columns,
+//   2 per lane and 2 calls per chunk, for one sample; 64 columns with several) and does the epilogue's work.
 #include "rm_internal.h"
 
 namespace {
@@ -90,6 +92,42 @@ __device__ __forceinline__ void load_rnorm(const GuArgs &a, int b, int t0, float
     }
 }
 
+// The partial sums of squares of one token block (tokens 0..63 of sample b; rows past T repeat the last token),
+// NS spans of 8 partials (256 columns) per token, loaded by the workgroup's 512 threads in memory order: thread e
+// takes span e % NS of token e / NS (32 contiguous bytes; threads past 64 NS repeat the last), so that a wave
+// reads whole lines.  The load is unconditional, so that it never sits under a branch (where the compiler would
+// wait for every load in flight): without a norm it reads the FFN input instead, whose rows are longer, and the
+// value is not used.
+template <int NS>
+__device__ __forceinline__ void load_spans(const GuArgs &a, int b, float4 &lo, float4 &hi) {
+    const int e = min(static_cast<int>(threadIdx.x), 64 * NS - 1);
+    const int t = min(e / NS, a.T - 1);
+    const float *src = a.ssq != nullptr ? a.ssq : reinterpret_cast<const float *>(a.xn);
+    const float4 *p =
+        reinterpret_cast<const float4 *>(src + static_cast<size_t>(b * a.T + t) * rm::ssq_stride(a.d)) + 2 * (e % NS);
+    lo = p[0];
+    hi = p[1];
+}
+
+// The thread's span sum into LDS: token t's spans at spans[t (NS + 1) + k] (rows padded against bank conflicts).
+template <int NS>
+__device__ __forceinline__ void store_span(float *spans, float4 lo, float4 hi) {
+    const int e = threadIdx.x;
+    if (e < 64 * NS) spans[(e / NS) * (NS + 1) + e % NS] = rm_ssq_span(lo, hi);
+}
+
+// RMSNorm factor of token t (< 64) from its spans' sums in LDS, added in span order; 1 without a norm and for
+// tokens past T.
+template <int NS>
+__device__ __forceinline__ float span_rnorm(const GuArgs &a, const float *spans, int t) {
+    if (a.ssq == nullptr || t >= a.T) return 1.0f;
+    const float *p = spans + t * (NS + 1);
+    float s = p[0];
+#pragma unroll
+    for (int k = 1; k < NS; ++k) s += p[k];
+    return rm_rnorm_from_ssq(s, a.d, a.eps);
+}
+
 // The neuron index of this lane's row (slot clamped into the list; entries past the count are only clamped
 // into range, their h is masked when stored).
 __device__ __forceinline__ int lane_neuron(const GuArgs &a, int b, int slot) {
@@ -101,11 +139,11 @@ __device__ __forceinline__ int lane_neuron(const GuArgs &a, int b, int slot) {
 // Writes h for 8 neurons x 64 tokens of token block t0 from the summed tile; slots at or past the count and
 // tokens at or past T get h = 0 (their rows and columns were computed from clamped loads).  H is chunk-major
 // (32-slot chunks, then tokens).  Thread tid finishes tile row tid & 7 (its gate row; the up row is 8 further) for
-// token tid >> 3, whose list slot is `slot` (< 0: a duplicate row, nothing stored).
+// token tid >> 3, whose list slot is `slot` (< 0: a duplicate row, nothing stored) and RMSNorm factor r.
 // red(w, tt, lane) is d-part w's tile tt (lane L, register i = row 4 (L / 16) + i, token L % 16).
 template <int NT, typename RedAt>
 __device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, int b, RedAt red, int ds, int t0,
-                                           int slot, int cnt, const float *rn) {
+                                           int slot, int cnt, float r) {
     const int j = threadIdx.x & 7;
     const int tok = threadIdx.x >> 3;
     const int tt = tok >> 4, tc = tok & 15;
@@ -120,7 +158,6 @@ __device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, int b,
             gsum += red(w, tt, lg)[reg];
             usum += red(w, tt, lu)[reg];
         }
-        const float r = rn[tok];
         h = rm_glu_act(a.act, gsum * r) * (usum * r);
     }
     if (slot < 0) return;
@@ -175,7 +212,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
     const int col0 = wave * SPW * 32;
 
     __shared__ __attribute__((aligned(16))) unsigned char lds[kGuWaves * G::kRegion];
-    __shared__ float rn[64];
+    __shared__ float rn[kOneBlock ? (SPW + 1) * 64 : 64];  // kOneBlock: the spans' sums, else the factors
     unsigned char *region = lds + wave * G::kRegion;
     auto red = [&](int w, int tt, int l) -> const rm_f32x4 & {
         return *reinterpret_cast<const rm_f32x4 *>(lds + w * G::kRegion + (tt * 64 + l) * 16);
@@ -195,19 +232,6 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
     };
     rm_u32x4 xv[G::kSubs][G::kPieces];
     load_x(0, xv);
-    // One token block (kOneBlock) with a norm: wave 0 loads the partial sums of squares of tokens 0..63 (4 SPW
-    // per row, d = 256 SPW) with the input, so that forming the norm factors after the products waits for no
-    // memory.  They are added in the order rm_token_rnorm adds them.
-    const bool pre_norm = kOneBlock && a.ssq != nullptr;
-    float4 ssq_v[SPW];
-#pragma unroll
-    for (int i = 0; i < SPW; ++i) ssq_v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (pre_norm && __builtin_amdgcn_readfirstlane(wave) == 0) {
-        const float4 *p = reinterpret_cast<const float4 *>(
-            a.ssq + static_cast<size_t>(b * a.T + min(lane, a.T - 1)) * rm::ssq_stride(a.d));
-#pragma unroll
-        for (int i = 0; i < SPW; ++i) ssq_v[i] = p[i];
-    }
     __builtin_amdgcn_sched_barrier(0);  // the input loads go out before the wait for the index
     rm_u32x4 w[SPW];
     {
@@ -216,6 +240,11 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
 #pragma unroll
         for (int i = 0; i < SPW; ++i) w[i] = load16(wrow + i * 32);
     }
+    // One token block (kOneBlock): behind the weights, the token block's partial sums of squares (SPW spans per
+    // token, d = 256 SPW); their span sums go to LDS after the products, so that the norm factors need no memory
+    // round trip after them.
+    float4 sp_lo = make_float4(0.f, 0.f, 0.f, 0.f), sp_hi = sp_lo;
+    if constexpr (kOneBlock) load_spans<SPW>(a, b, sp_lo, sp_hi);
     for (int t0 = 0;;) {
         __builtin_amdgcn_sched_barrier(0);
         rm_f32x4 acc[NT];
@@ -242,23 +271,14 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
         // The summed tile goes into the wave's region (its fragment reads precede these writes).
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) *reinterpret_cast<rm_f32x4 *>(region + (tt * 64 + lane) * 16) = acc[tt];
-        if (pre_norm) {
-            if (wave == 0) {
-                float ss = 0.0f;
-#pragma unroll
-                for (int i = 0; i < SPW; ++i) {
-                    ss += ssq_v[i].x;
-                    ss += ssq_v[i].y;
-                    ss += ssq_v[i].z;
-                    ss += ssq_v[i].w;
-                }
-                rn[lane] = lane < a.T ? rm_rnorm_from_ssq(ss, a.d, a.eps) : 1.0f;
-            }
+        if constexpr (kOneBlock) {
+            store_span<SPW>(rn, sp_lo, sp_hi);
         } else {
             load_rnorm(a, b, t0, rn);
         }
         __syncthreads();
-        gu_store_h<NT>(a, Hb, b, red, kGuWaves, t0, slot0 + (tid & 7), cnt, rn);
+        const float rt = kOneBlock ? span_rnorm<SPW>(a, rn, tid >> 3) : rn[tid >> 3];
+        gu_store_h<NT>(a, Hb, b, red, kGuWaves, t0, slot0 + (tid & 7), cnt, rt);
         t0 += rm::kBfTokBlock;
         if (kOneBlock || t0 >= a.T) break;
         __syncthreads();  // every wave has read the tiles before the regions are refilled
@@ -372,7 +392,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_kernel(GuArgs a) {
 #pragma unroll
         for (int gg = 0; gg < NG; ++gg) {
             auto red_g = [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; };
-            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8 + (tid & 7), cnt, rn);
+            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8 + (tid & 7), cnt, rn[tid >> 3]);
         }
         __syncthreads();
     }
@@ -472,7 +492,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_staged_unrolled_kernel(GuAr
 #pragma unroll
         for (int gg = 0; gg < NG; ++gg) {
             auto red_g = [&](int w, int tt, int l) -> const rm_f32x4 & { return red[gg][w][tt][l]; };
-            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8 + (tid & 7), cnt, rn);
+            gu_store_h<NT>(a, Hb, b, red_g, DS, t0, blk0 + gg * 8 + (tid & 7), cnt, rn[tid >> 3]);
         }
         __syncthreads();
     }
@@ -512,7 +532,6 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
     const uint16_t *wrow = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(n) * a.d + part * SPW * 32 + grp * 8;
 
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][64 * kRowPitch];
-    __shared__ float rn[64];
     static_assert(sizeof(rm_f32x4) * NG * DS * NT * 64 <= sizeof(xs), "reduction tiles must fit the input tile");
     auto red = [&](int gg, int w2, int tt, int l) -> rm_f32x4 & {
         return reinterpret_cast<rm_f32x4 *>(&xs[0][0])[((gg * DS + w2) * NT + tt) * 64 + l];
@@ -538,20 +557,14 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
     };
 #pragma unroll
     for (int c = 0; c < P; ++c) load_chunk(c);
-    // With a norm, wave 0 loads the partial sums of squares of tokens 0..63 (4 NCH per row, d = NCH chunks of
-    // 256 columns) behind the first chunks, so that forming the norm factors after the products waits for no
-    // memory.  They are added in the order rm_token_rnorm adds them.  Where those registers would spill (d =
-    // 2048, or 8 groups two to a compute unit at d = 1024) the factors are loaded after the products instead.
-    constexpr bool kPreNorm = NCH <= 2 || (NCH == 4 && !(NG == 8 && kTwoPerCU));
-    float4 ssq_v[NCH];
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) ssq_v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (kPreNorm && a.ssq != nullptr && __builtin_amdgcn_readfirstlane(wave) == 0) {
-        const float4 *p = reinterpret_cast<const float4 *>(
-            a.ssq + static_cast<size_t>(b * a.T + min(lane, a.T - 1)) * rm::ssq_stride(a.d));
-#pragma unroll
-        for (int i = 0; i < NCH; ++i) ssq_v[i] = p[i];
-    }
+    // Behind the first chunks, the partial sums of squares of tokens 0..63 (NCH spans per token); their span sums
+    // go to LDS after the products, so that forming the norm factors needs no memory round trip after them.
+    // With 8 groups two to a compute unit at d = 2048 those registers would spill: there the factors are loaded
+    // after the products instead.
+    constexpr bool kSpans = !(NCH == 8 && NG == 8 && kTwoPerCU);
+    __shared__ float spans[(NCH + 1) * 64];
+    float4 sp_lo = make_float4(0.f, 0.f, 0.f, 0.f), sp_hi = sp_lo;
+    if constexpr (kSpans) load_spans<NCH>(a, b, sp_lo, sp_hi);
 
     rm_f32x4 acc[NT];
 #pragma unroll
@@ -575,31 +588,20 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
             }
         if (c + P < NCH) load_chunk(c + P);
     }
-    if (!kPreNorm) {
-        load_rnorm(a, b, 0, rn);
-    } else if (wave == 0) {
-        float r = 1.0f;
-        if (a.ssq != nullptr && lane < a.T) {
-            float ss = 0.0f;
-#pragma unroll
-            for (int i = 0; i < NCH; ++i) {
-                ss += ssq_v[i].x;
-                ss += ssq_v[i].y;
-                ss += ssq_v[i].z;
-                ss += ssq_v[i].w;
-            }
-            r = rm_rnorm_from_ssq(ss, a.d, a.eps);
-        }
-        rn[lane] = r;
+    if constexpr (kSpans) {
+        store_span<NCH>(spans, sp_lo, sp_hi);
+    } else {
+        load_rnorm(a, b, 0, spans);
     }
     __syncthreads();  // every wave is done with the input tiles before they hold the reduction
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) red(g, part, tt, lane) = acc[tt];
     __syncthreads();
+    const float rt = kSpans ? span_rnorm<NCH>(a, spans, tid >> 3) : spans[tid >> 3];
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg)
         gu_store_h<NT>(a, Hb, b, [&](int w2, int tt, int l) -> const rm_f32x4 & { return red(gg, w2, tt, l); }, DS, 0,
-                       blk0 + gg * 8 + (tid & 7), cnt, rn);
+                       blk0 + gg * 8 + (tid & 7), cnt, rt);
 }
 
 // ------------------------------------------------------------------------------------------ gate / up, spread
@@ -616,7 +618,7 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
 // order through LDS.
 template <int NG, int NCH>
 __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G, int nquads,
-                                                   uint16_t (*xs)[64 * kRowPitch], rm_f32x4 *red2, float *rn) {
+                                                   uint16_t (*xs)[64 * kRowPitch], rm_f32x4 *red2, float *spans) {
     constexpr int NT = 4;
 #ifndef RM_SPREAD_WTILES
 #define RM_SPREAD_WTILES 9
@@ -674,22 +676,19 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
 #pragma unroll
     for (int c = 0; c < PX; ++c) load_x(c);
     __builtin_amdgcn_sched_barrier(0);
+    // Rows 8-15 of a tile read W_up: an offset added to W_gate's address.  (Selecting between the two pointers
+    // lets the compiler fetch the chosen one from the kernel arguments with a vector load, issued behind the
+    // input chunks, which would hold every weight load until all of them have arrived.)
+    const ptrdiff_t up_off = r < 8 ? 0 : a.wu - a.wg;
 #pragma unroll
     for (int j = 0; j < NG; ++j)
-        wrow[j] = ((r < 8) ? a.wg : a.wu) + static_cast<size_t>(clamp_neuron(raw_n[j], a.d_ff)) * a.d + wave * 32 +
-                  grp * 8;
+        wrow[j] = a.wg + up_off + static_cast<size_t>(clamp_neuron(raw_n[j], a.d_ff)) * a.d + wave * 32 + grp * 8;
 #pragma unroll
     for (int c = 0; c < PW; ++c) load_w(c);
-    constexpr bool kPreNorm = NCH <= 4 && NG <= 2;
-    float4 ssq_v[NCH];
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) ssq_v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (kPreNorm && a.ssq != nullptr && __builtin_amdgcn_readfirstlane(wave) == 0) {
-        const float4 *p =
-            reinterpret_cast<const float4 *>(a.ssq + static_cast<size_t>(min(lane, a.T - 1)) * rm::ssq_stride(a.d));
-#pragma unroll
-        for (int i = 0; i < NCH; ++i) ssq_v[i] = p[i];
-    }
+    // Behind the first weights, the partial sums of squares of tokens 0..63 (NCH spans per token); their span
+    // sums go to LDS after the products, so that forming the norm factors needs no memory round trip after them.
+    float4 sp_lo, sp_hi;
+    load_spans<NCH>(a, 0, sp_lo, sp_hi);
 
     rm_f32x4 acc[NG][NT];
 #pragma unroll
@@ -711,23 +710,7 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
         }
         if (c + PW < NCH) load_w(c + PW);
     }
-    if (!kPreNorm) {
-        load_rnorm(a, 0, 0, rn);
-    } else if (wave == 0) {
-        float rr = 1.0f;
-        if (a.ssq != nullptr && lane < a.T) {
-            float ss = 0.0f;
-#pragma unroll
-            for (int i = 0; i < NCH; ++i) {
-                ss += ssq_v[i].x;
-                ss += ssq_v[i].y;
-                ss += ssq_v[i].z;
-                ss += ssq_v[i].w;
-            }
-            rr = rm_rnorm_from_ssq(ss, a.d, a.eps);
-        }
-        rn[lane] = rr;
-    }
+    store_span<NCH>(spans, sp_lo, sp_hi);
     // The waves' partial tiles of every tile go through LDS at once (tiles 0 and 1 in the input buffers, free once
     // every wave has passed the barrier below, tile 2 in red2) and are added in wave order: one barrier for all.
     __syncthreads();  // every wave is done with the input tiles
@@ -739,6 +722,7 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) red_at(j)[(wave * NT + tt) * 64 + lane] = acc[j][tt];
     __syncthreads();
+    const float rt = span_rnorm<NCH>(a, spans, tid >> 3);
     const int jj = tid & 7;  // the tile row (neuron) this thread stores
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
@@ -747,7 +731,7 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
         const rm_f32x4 *red = red_at(j);
         gu_store_h<NT>(a, a.H, 0,
                        [&](int w2, int tt, int l) -> const rm_f32x4 & { return red[(w2 * NT + tt) * 64 + l]; },
-                       kGuWaves, 0, slot, cnt, rn);
+                       kGuWaves, 0, slot, cnt, rt);
     }
 }
 
@@ -758,16 +742,16 @@ __global__ __launch_bounds__(kGuThreads) void gateup_spread_kernel(GuArgs a) {
     static_assert(NG <= 3, "two reduction tiles in the input buffers, a third in red2");
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][64 * kRowPitch];
     __shared__ rm_f32x4 red2[NG > 2 ? kGuWaves * 4 * 64 : 1];
-    __shared__ float rn[64];
+    __shared__ float spans[(NCH + 1) * 64];
     static_assert(2 * sizeof(rm_f32x4) * kGuWaves * 4 * 64 <= sizeof(xs), "two reduction tiles fit the input tile");
     const int G = gridDim.x;
     const int q = blockIdx.x;
     const int nq = a.kcap / 4;
     const int mine = (nq - q + G - 1) / G;  // quads of this workgroup, >= 1
     if ((mine + 1) / 2 == NG)
-        gateup_spread_body<NG, NCH>(a, q, G, mine, xs, red2, rn);
+        gateup_spread_body<NG, NCH>(a, q, G, mine, xs, red2, spans);
     else if constexpr (NG > 1)
-        gateup_spread_body<NG - 1, NCH>(a, q, G, mine, xs, red2, rn);
+        gateup_spread_body<NG - 1, NCH>(a, q, G, mine, xs, red2, spans);
 }
 
 // ------------------------------------------------------------------------------------------ down
@@ -788,11 +772,12 @@ struct DnArgs {
 // Slots at or past the count hold h = 0 in H (the gate/up kernels write every slot below kcap), so the products
 // of their chunks are exact zeros and the kernel does not read the count; the epilogue skips whole slices past
 // it, so an empty list still gives y = x bit for bit.
-template <int NT>
+// CW calls, one per column of the lane's CW columns (CW = 2 reads only the low dword of each weight row).
+template <int NT, int CW = 4>
 __device__ __forceinline__ void dn_mma(const DnChunk<NT> &c, rm_f32x4 (*acc)[4]) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        // B fragment of call q: column q of the 8 x 4 block, rows 0..7 in K order, two bf16 per dword.
+    for (int q = 0; q < CW; ++q) {
+        // B fragment of call q: column q of the 8 x CW block, rows 0..7 in K order, two bf16 per dword.
         const int dw = q >> 1;
         const int sh = (q & 1) * 16;
         uint32_t v[8];
@@ -938,11 +923,12 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
 }
 
 // Down projection with the epilogue fused, for lists of at most kDfMaxChunks chunks.  Workgroup: one column
-// tile of 64 columns, NT tiles of 16 tokens, one sample; its 8 waves take the list's chunks in turn (chunk
-// wave + 8 k, k < CPW: every load is issued before the first product), each keeping NT 16 x 64 fp32 tiles, and
-// the 8 waves' tiles are summed in wave order through LDS, one token tile at a time.  Then y = x + acc (x + (y_a + acc) for Eq. 4), y_a = acc on
-// an anchor step, and inside a stack the next layer's input xn = y * g in bf16 with the row's partial sum of
-// squares for this 64-column block.  No partials leave the workgroup, so no epilogue launch follows.
+// tile of 16 CW columns (CW = 2 or 4 per lane), NT tiles of 16 tokens, one sample; its 8 waves take the list's
+// chunks in turn (chunk wave + 8 k, k < CPW: every load is issued before the first product), each keeping NT x CW
+// 16 x 16 fp32 tiles, and the 8 waves' tiles are summed in wave order through LDS, one token tile at a time.
+// Then y = x + acc (x + (y_a + acc) for Eq. 4), y_a = acc on an anchor step, and inside a stack the next layer's
+// input xn = y * g in bf16 with the row's partial sums of squares for its 32-column blocks.  No partials leave
+// the workgroup, so no epilogue launch follows.
 struct DfArgs {
     const uint16_t *H, *wd;
     const int32_t *idx, *count;
@@ -957,8 +943,13 @@ struct DfArgs {
     float *ssq;
 };
 
-template <int CPW, int NT>
+template <int N>
+using f32v = float __attribute__((ext_vector_type(N)));
+
+template <int CPW, int NT, int CW>
 __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
+    static_assert(CW == 2 || CW == 4, "two or four columns per lane");
+    using vec = f32v<CW>;
     const int q = xcd_logical(blockIdx.x, gridDim.x);  // = (sample * ncol + column tile) * ntt + token tile
     const int tt = q % a.ntt;
     const int ct = (q / a.ntt) % a.ncol;
@@ -967,10 +958,10 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int grp = lane >> 4;  // K group: slots 8*grp .. 8*grp+7 of a chunk
-    const int nn = lane & 15;   // A row (token in tile) and B column group (physical columns 4*nn + q)
-    const int colw = ct * rm::kBfColTile + nn * 4;
+    const int nn = lane & 15;   // A row (token in tile) and B column group (physical columns CW*nn + q)
+    const int colw = (ct * 16 + nn) * CW;
     const bool colok = colw < a.d;
-    const int col = min(colw, a.d - 4);  // columns past d re-read column d-4; those outputs are not stored
+    const int col = min(colw, a.d - CW);  // columns past d re-read the last CW columns; those are not stored
     const int nchunks = a.kcap / rm::kBfChunk;
     const int t0 = tt * 16 * NT;  // NT tiles of 16 tokens
     const uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
@@ -996,22 +987,23 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     // The epilogue's inputs depend on nothing computed here, so they are loaded now, behind the H tiles, and
     // the epilogue does not wait for memory a second time.  Wave w < 4 finishes token t0 + 16 j + 4 grp + w of
     // tile j (waves 4-7 load the same rows and drop them).
-    const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    vec zero;
+#pragma unroll
+    for (int c = 0; c < CW; ++c) zero[c] = 0.0f;
     size_t ro[NT];
-    float4 x_in[NT], ya_in[NT];
+    vec x_in[NT], ya_in[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
         ro[j] = (static_cast<size_t>(b) * a.T + min(t0 + j * 16 + grp * 4 + (wave & 3), a.T - 1)) * a.d + col;
-        x_in[j] = *reinterpret_cast<const float4 *>(a.x + ro[j]);
-        ya_in[j] = zero4;
+        x_in[j] = *reinterpret_cast<const vec *>(a.x + ro[j]);
+        ya_in[j] = zero;
     }
-    float4 gate = zero4, g_next = zero4;
+    vec gate = zero, g_next = zero;
     if (a.ya_in != nullptr)
 #pragma unroll
-        for (int j = 0; j < NT; ++j) ya_in[j] = *reinterpret_cast<const float4 *>(a.ya_in + ro[j]);
-    if (a.out_gate != nullptr)
-        gate = *reinterpret_cast<const float4 *>(a.out_gate + static_cast<size_t>(b) * a.d + col);
-    if (a.g_next != nullptr) g_next = *reinterpret_cast<const float4 *>(a.g_next + col);
+        for (int j = 0; j < NT; ++j) ya_in[j] = *reinterpret_cast<const vec *>(a.ya_in + ro[j]);
+    if (a.out_gate != nullptr) gate = *reinterpret_cast<const vec *>(a.out_gate + static_cast<size_t>(b) * a.d + col);
+    if (a.g_next != nullptr) g_next = *reinterpret_cast<const vec *>(a.g_next + col);
     __builtin_amdgcn_sched_barrier(0);  // then the H tiles, before the wait for the indices
 #pragma unroll
     for (int i = 0; i < kIdxPerThread; ++i) {
@@ -1026,7 +1018,11 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
         const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb + 4);
         const int n[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
 #pragma unroll
-        for (int j = 0; j < 8; ++j) cb[k].w[j] = load8(a.wd + static_cast<size_t>(n[j]) * a.d + col);
+        for (int j = 0; j < 8; ++j) {
+            const uint16_t *wp = a.wd + static_cast<size_t>(n[j]) * a.d + col;
+            if constexpr (CW == 4) cb[k].w[j] = load8(wp);
+            else cb[k].w[j] = make_uint2(*reinterpret_cast<const uint32_t *>(wp), 0u);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -1034,59 +1030,68 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[j][c] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < CW; ++c) acc[j][c] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int k = 0; k < CPW; ++k)
-        if (wave + k * rm::kDfWaves < nchunks) dn_mma(cb[k], acc);
+        if (wave + k * rm::kDfWaves < nchunks) dn_mma<NT, CW>(cb[k], acc);
 
-    __shared__ rm_f32x4 red[rm::kDfWaves][4][64];
+    __shared__ rm_f32x4 red[rm::kDfWaves][CW][64];
     cnt = cnt < 0 ? 0 : (cnt > a.max_count ? a.max_count : cnt);
+    const int ssq_stride = rm::ssq_stride(a.d);
+    // The 32-column block of this lane's columns, and whether the lane is its first (it stores the sum).
+    const int part = colw / rm::kSsqCols;
+    const bool part_lead = (nn & (rm::kSsqCols / CW - 1)) == 0;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
         if (j > 0) __syncthreads();  // tile j - 1's sums have been read
 #pragma unroll
-        for (int c = 0; c < 4; ++c) red[wave][c][lane] = acc[j][c];
+        for (int c = 0; c < CW; ++c) red[wave][c][lane] = acc[j][c];
         __syncthreads();
         if (wave >= 4) continue;
         // Wave i finishes token 4 * grp + i of tile j (lane L, register i of a tile: token 4*(L/16)+i,
-        // physical column 4*(L%16) + q of call q): the 8 waves' sums in wave order.
+        // physical column CW*(L%16) + q of call q): the 8 waves' sums in wave order.
         const int i = wave;
-        float v[4];
+        vec acc_v;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            v[c] = red[0][c][lane][i];
+        for (int c = 0; c < CW; ++c) {
+            float v = red[0][c][lane][i];
 #pragma unroll
-            for (int w = 1; w < rm::kDfWaves; ++w) v[c] += red[w][c][lane][i];
+            for (int w = 1; w < rm::kDfWaves; ++w) v += red[w][c][lane][i];
+            acc_v[c] = v;
         }
         const int t = t0 + j * 16 + grp * 4 + i;
         const bool live = t < a.T;
-        const float4 acc4 = make_float4(v[0], v[1], v[2], v[3]);
-        float4 out = x_in[j];
+        vec out = x_in[j];
         if (a.ya_in != nullptr || cnt > 0) {  // an empty list without an anchor leaves y = x bit for bit
-            float4 f = acc4;
-            if (a.ya_in != nullptr)  // Eq. 4: the FFN output is y_a + (h - h_a) W_down
-                f = make_float4(ya_in[j].x + acc4.x, ya_in[j].y + acc4.y, ya_in[j].z + acc4.z, ya_in[j].w + acc4.w);
-            if (a.out_gate != nullptr)  // the adaptive output gate, before the residual
-                f = make_float4(f.x * gate.x, f.y * gate.y, f.z * gate.z, f.w * gate.w);
-            out = make_float4(out.x + f.x, out.y + f.y, out.z + f.z, out.w + f.w);
+            vec f = acc_v;
+            if (a.ya_in != nullptr) f = ya_in[j] + acc_v;  // Eq. 4: the FFN output is y_a + (h - h_a) W_down
+            if (a.out_gate != nullptr) f = f * gate;       // the adaptive output gate, before the residual
+            out = out + f;
         }
         const bool st = live && colok;
         if (st) {
-            *reinterpret_cast<float4 *>(a.y + ro[j]) = out;
-            if (a.ya_out != nullptr) *reinterpret_cast<float4 *>(a.ya_out + ro[j]) = acc4;
+            *reinterpret_cast<vec *>(a.y + ro[j]) = out;
+            if (a.ya_out != nullptr) *reinterpret_cast<vec *>(a.ya_out + ro[j]) = acc_v;
         }
         if (a.xn_next == nullptr) continue;
         if (a.g_next != nullptr) {
-            const float ss = rm_ssq64(out, colok);
+            float ss;
+            if constexpr (CW == 4) ss = rm_ssq32(make_float4(out[0], out[1], out[2], out[3]), colok);
+            else ss = rm_ssq32_pairs(out[0], out[1], colok);
             const int row = b * a.T + t;
-            if (nn == 0 && live) a.ssq[static_cast<size_t>(row) * rm::ssq_stride(a.d) + ct] = ss;
-            out = make_float4(out.x * g_next.x, out.y * g_next.y, out.z * g_next.z, out.w * g_next.w);
+            if (part_lead && st) a.ssq[static_cast<size_t>(row) * ssq_stride + part] = ss;
+            out = out * g_next;
         }
         if (st) {
-            uint2 packed;
-            packed.x = rm_f32_to_bf16_bits(out.x) | (rm_f32_to_bf16_bits(out.y) << 16);
-            packed.y = rm_f32_to_bf16_bits(out.z) | (rm_f32_to_bf16_bits(out.w) << 16);
-            *reinterpret_cast<uint2 *>(a.xn_next + ro[j]) = packed;
+            if constexpr (CW == 4) {
+                uint2 packed;
+                packed.x = rm_f32_to_bf16_bits(out[0]) | (rm_f32_to_bf16_bits(out[1]) << 16);
+                packed.y = rm_f32_to_bf16_bits(out[2]) | (rm_f32_to_bf16_bits(out[3]) << 16);
+                *reinterpret_cast<uint2 *>(a.xn_next + ro[j]) = packed;
+            } else {
+                *reinterpret_cast<uint32_t *>(a.xn_next + ro[j]) =
+                    rm_f32_to_bf16_bits(out[0]) | (rm_f32_to_bf16_bits(out[1]) << 16);
+            }
         }
     }
 }
@@ -1259,7 +1264,7 @@ hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *i
     a.kcap = p.kcap;
     a.max_count = p.max_count;
     a.B = p.B;
-    a.ncol = p.ncol;
+    a.ncol = p.df_ncol;
     a.ntt = p.ntt;
     a.x = x;
     a.y = y;
@@ -1269,24 +1274,27 @@ hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *i
     a.g_next = emit_xn ? g_next : nullptr;
     a.xn_next = emit_xn ? reinterpret_cast<uint16_t *>(base + p.off_xn) : nullptr;
     a.ssq = reinterpret_cast<float *>(base + p.off_ssq);
-    const dim3 grid(p.ncol * p.ntt * p.B);
+    const dim3 grid(p.df_ncol * p.ntt * p.B);
     const dim3 block(kDfThreads);
     hipError_t e;
-#define RM_DF(NT)                                                                                         \
-    switch (p.dn_cpw) {                                                                                   \
-        case 1: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<1, NT>, grid, block, st, a); break;    \
-        case 2: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<2, NT>, grid, block, st, a); break;    \
-        case 3: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<3, NT>, grid, block, st, a); break;    \
-        case 4: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<4, NT>, grid, block, st, a); break;    \
-        case 5: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<5, NT>, grid, block, st, a); break;    \
-        case 6: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<6, NT>, grid, block, st, a); break;    \
-        case 7: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7, NT>, grid, block, st, a); break;    \
-        default: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8, NT>, grid, block, st, a); break;   \
+#define RM_DF(NT, CW)                                                                                         \
+    switch (p.dn_cpw) {                                                                                       \
+        case 1: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<1, NT, CW>, grid, block, st, a); break;    \
+        case 2: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<2, NT, CW>, grid, block, st, a); break;    \
+        case 3: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<3, NT, CW>, grid, block, st, a); break;    \
+        case 4: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<4, NT, CW>, grid, block, st, a); break;    \
+        case 5: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<5, NT, CW>, grid, block, st, a); break;    \
+        case 6: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<6, NT, CW>, grid, block, st, a); break;    \
+        case 7: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7, NT, CW>, grid, block, st, a); break;    \
+        default: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8, NT, CW>, grid, block, st, a); break;   \
     }
-    if (p.df_nt == 2)
-        RM_DF(2)
+    // The plan pairs one 16-token tile with 2 columns per lane (one sample) and two with 4 (several samples).
+    if (p.df_nt == 2 && p.df_cw == 4)
+        RM_DF(2, 4)
+    else if (p.df_nt == 1 && p.df_cw == 2)
+        RM_DF(1, 2)
     else
-        RM_DF(1)
+        return hipErrorInvalidValue;
 #undef RM_DF
     return e != hipSuccess ? e : hipGetLastError();
 }

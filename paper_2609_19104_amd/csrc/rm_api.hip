@@ -332,6 +332,10 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         q.df_nt = B == 1 ? 1 : 2;
         q.fused_down = nchunks <= kDfMaxChunks && (q.df_nt == 1 || q.dn_cpw <= 7);
         q.ntt = ceil_div(T, 16 * q.df_nt);
+        // One sample's tiles are 32 columns wide (two per lane), so that the 16-token tiles of a short prompt
+        // still give the chip a workgroup per compute unit or more; with several samples, 64 columns.
+        q.df_cw = B == 1 ? 2 : 4;
+        q.df_ncol = ceil_div(s->d, 16 * q.df_cw);
         xn_elem = 2;
         h_elem = 2;
     } else {
@@ -350,7 +354,8 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     }
     if (q.slices > 65535 || static_cast<long long>(q.gate_blocks) * B > 0x7fffffffLL ||
         static_cast<long long>(q.ncol) * q.slices * B > 0x7fffffffLL ||
-        static_cast<long long>(q.ncol) * ceil_div(T, 16) * B > 0x7fffffffLL)
+        static_cast<long long>(q.ncol) * ceil_div(T, 16) * B > 0x7fffffffLL ||
+        static_cast<long long>(q.df_ncol) * q.ntt * B > 0x7fffffffLL)
         return fail(RM_ERR_SHAPE, "launch grid too large");
     if (static_cast<long long>(B) * T * ceil_div(s->d, kRowBlock) > 0x7fffffffLL)
         return fail(RM_ERR_SHAPE, "B=%d x T=%d rows are too many for one launch", B, T);

@@ -36,8 +36,9 @@ constexpr int kDfMaxChunks = kDfWaves * kDfMaxCpw;  // lists of up to 64 chunks 
 // Prologue / epilogue: one wave per (token row, block of 256 columns).
 constexpr int kRowBlock = 256;
 // RMSNorm sums of squares are kept as partial sums over blocks of kSsqCols columns, [row][ssq_stride(d)] with
-// ssq_parts(d) partials per row (the rest of the row is padding, never read into a sum).
-constexpr int kSsqCols = 64;
+// ssq_parts(d) partials per row (the rest of the row is padding, never read into a sum).  d is a multiple of 32,
+// so every block is whole.
+constexpr int kSsqCols = 32;
 __host__ __device__ constexpr int ssq_parts(int d) { return (d + kSsqCols - 1) / kSsqCols; }
 __host__ __device__ constexpr int ssq_stride(int d) { return (ssq_parts(d) + 3) / 4 * 4; }
 
@@ -68,10 +69,12 @@ struct Plan {
     bool fused_down = false;
     int dn_cpw = 0;      // fused down: chunks per wave (the kernel's unrolled pipeline depth)
     int df_nt = 1;       // fused down: 16-token tiles per workgroup (2 with several samples)
+    int df_cw = 4;       // fused down: columns per lane (2 for one sample, 4 with several)
+    int df_ncol = 0;     // fused down: column tiles of 16 df_cw columns
     int ntt = 0;         // fused down: token tiles of 16 df_nt tokens
     // Workspace: xn [B][T][d] (bf16 or f32); H (bf16: [B][kcap / 32][tpad][32], chunk-major; f32:
     // [B][tpad][kcap]); partials f32 [B][slices][T][d]; ssq f32 [B][T][ssq_stride(d)]
-    // (per-token sums of squares of the FFN input by 64-column block, for the RMSNorm factor); and, for the dense
+    // (per-token sums of squares of the FFN input by 32-column block, for the RMSNorm factor); and, for the dense
     // reference, the lists 0 .. d_ff-1 int32 [B][d_ff] and their counts int32 [B].
     size_t off_xn = 0, off_h = 0, off_part = 0, off_ssq = 0, off_ident = 0, off_ident_count = 0, total = 0;
 };
@@ -221,41 +224,70 @@ __device__ __forceinline__ float rm_rnorm_from_ssq(float s, int d, float eps) {
     return 1.0f / sqrtf(s / static_cast<float>(d) + eps);
 }
 
+// A row's partial sums of squares are added in two levels: the 8 partials of each 256-column span in order (the
+// span's sum), then the spans' sums in order; a row whose d is not a multiple of 256 ends with a shorter span.
+// Kernels whose waves each hold one span add the spans in parallel and only the spans' sums in sequence.
+constexpr int kSsqSpan = 8;  // partials per span
+
+// The sum of one whole span's 8 partials, lo = partials 0-3, hi = 4-7.
+__device__ __forceinline__ float rm_ssq_span(float4 lo, float4 hi) {
+    float s = lo.x;
+    s += lo.y;
+    s += lo.z;
+    s += lo.w;
+    s += hi.x;
+    s += hi.y;
+    s += hi.z;
+    s += hi.w;
+    return s;
+}
+
 // RMSNorm factor of token row `row` (= b * T + t): 1 / sqrt(mean of squares + eps), from the row's partial sums
-// of squares by 256-column block, added in block order.
+// of squares by 32-column block, added in the two-level order above.
 __device__ __forceinline__ float rm_token_rnorm(const float *ssq, int row, int d, float eps) {
     const int n = rm::ssq_parts(d);
     const int stride4 = rm::ssq_stride(d) / 4;
     const float4 *p = reinterpret_cast<const float4 *>(ssq + static_cast<size_t>(row) * rm::ssq_stride(d));
-    float s = 0.0f;
-    for (int k0 = 0; k0 < n; k0 += 32) {  // eight float4 loads in flight, then the in-order sum
+    float s = 0.0f;  // + the first span's sum: exact
+    for (int k0 = 0; k0 < n; k0 += 4 * kSsqSpan) {  // four spans: eight float4 loads in flight, then the sums
         float4 v[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] = p[min(k0 / 4 + i, stride4 - 1)];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int k = k0 + 4 * i;
-            if (k < n) s += v[i].x;
-            if (k + 1 < n) s += v[i].y;
-            if (k + 2 < n) s += v[i].z;
-            if (k + 3 < n) s += v[i].w;
+        for (int j = 0; j < 4; ++j) {
+            const int k = k0 + j * kSsqSpan;
+            if (k >= n) break;
+            if (k + kSsqSpan <= n) {
+                s += rm_ssq_span(v[2 * j], v[2 * j + 1]);
+            } else {  // the row's last, shorter span
+                const float part[8] = {v[2 * j].x,     v[2 * j].y,     v[2 * j].z,     v[2 * j].w,
+                                       v[2 * j + 1].x, v[2 * j + 1].y, v[2 * j + 1].z, v[2 * j + 1].w};
+                float b = part[0];
+                for (int i = 1; i < n - k; ++i) b += part[i];
+                s += b;
+            }
         }
     }
     return rm_rnorm_from_ssq(s, d, eps);
 }
 
-// Sum of squares of 4 columns (one lane's float4), then the sum over the 16 lanes of a lane group (lanes
-// 16 g .. 16 g + 15 hold 64 consecutive columns): a fixed order shared by every kernel that writes the partials,
-// so that a layer's norm factors do not depend on which kernel produced its input.
-__device__ __forceinline__ float rm_ssq64(float4 v, bool ok) {
+// Sum of squares of a 32-column block, in one fixed order shared by every kernel that writes the partials, so
+// that a layer's norm factors do not depend on which kernel produced its input: per pair of columns
+// fma(c1, c1, fma(c0, c0, 0)), per group of 4 columns the sum of its two pairs, then the 8 groups of the block
+// added by a lane butterfly (xor 1, 2, 4 over the groups).  rm_ssq32: lanes 8 k .. 8 k + 7 hold the block's 32
+// columns, 4 per lane (ok: the lane's columns lie inside the row).
+__device__ __forceinline__ float rm_ssq32(float4 v, bool ok) {
     float ss = 0.0f;
-    if (ok) {
-        ss = fmaf(v.x, v.x, ss);
-        ss = fmaf(v.y, v.y, ss);
-        ss = fmaf(v.z, v.z, ss);
-        ss = fmaf(v.w, v.w, ss);
-    }
-    for (int off = 1; off < 16; off <<= 1) ss += __shfl_xor(ss, off);
+    if (ok) ss = fmaf(v.y, v.y, fmaf(v.x, v.x, 0.0f)) + fmaf(v.w, v.w, fmaf(v.z, v.z, 0.0f));
+    for (int off = 1; off < 8; off <<= 1) ss += __shfl_xor(ss, off);
+    return ss;
+}
+// The same block with 2 columns per lane, lanes 16 k .. 16 k + 15: lanes 2 g and 2 g + 1 hold group g's two pairs
+// (their sum is the group's, the same bits in both lanes), then the butterfly over the groups (xor 2, 4, 8).
+__device__ __forceinline__ float rm_ssq32_pairs(float x, float y, bool ok) {
+    const float p = ok ? fmaf(y, y, fmaf(x, x, 0.0f)) : 0.0f;
+    float ss = p + __shfl_xor(p, 1);
+    for (int off = 2; off < 16; off <<= 1) ss += __shfl_xor(ss, off);
     return ss;
 }
 

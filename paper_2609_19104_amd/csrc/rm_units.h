@@ -121,10 +121,10 @@ __device__ __forceinline__ void prologue_unit(const float *__restrict__ x, const
     const size_t o = static_cast<size_t>(row) * d + c;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     if (c < d) v = *reinterpret_cast<const float4 *>(x + o);
-    if (g != nullptr) {  // partial sums of squares of the row's 64-column blocks (lane 16 j: block 4 blk + j)
-        const float ss = rm_ssq64(v, c < d);
-        const int part = blk * 4 + (lane >> 4);
-        if ((lane & 15) == 0 && part < rm::ssq_parts(d))
+    if (g != nullptr) {  // partial sums of squares of the row's 32-column blocks (lane 8 j: block 8 blk + j)
+        const float ss = rm_ssq32(v, c < d);
+        const int part = blk * 8 + (lane >> 3);
+        if ((lane & 7) == 0 && part < rm::ssq_parts(d))
             ssq[static_cast<size_t>(row) * rm::ssq_stride(d) + part] = ss;
     }
     if (c < d) {

@@ -421,7 +421,7 @@ class StackSetupEq4Compact(StackSetupEq4):
         super().__init__(key, device, cold)
         # One compact buffer per group (the two groups' copies would alternate in a deployment; here each group
         # keeps its own so that replays need no ordering between them).
-        self.compact = [torch.empty((self.L, 3, self.k, self.d), dtype=torch.bfloat16, device=device)
+        self.rows = [torch.empty((self.L, 3, self.k, self.d), dtype=torch.bfloat16, device=device)
                         for _ in self.ANCHORS]
         self.ident = torch.arange(self.k, dtype=torch.int32, device=device).repeat(self.L, 1).contiguous()
         self.ws_c = self.rm.workspace(self.d, self.k, self.rm.RM_BF16, 1, self.T, self.k, device=device)
@@ -437,11 +437,11 @@ class StackSetupEq4Compact(StackSetupEq4):
                 rm.rm_mask_compact(self.masks[g], self.idx[g], self.cnt[g])
                 self.side.wait_stream(main)
                 with torch.cuda.stream(self.side):
-                    rm.rm_gather_stack_rows(layers, self.idx[g], self.cnt[g], self.k, self.compact[g])
+                    rm.rm_gather_stack_rows(layers, self.idx[g], self.cnt[g], self.k, self.rows[g])
                 rm.rm_anchor_ffn_stack(self.xs[s], self.y, layers, self.idx[g], self.cnt[g], self.k, self.ya,
                                        self.ha, self.ws_dense)
                 main.wait_stream(self.side)
-                clayers = [(self.compact[g][l, 0], self.compact[g][l, 1], self.compact[g][l, 2], layers[l][3])
+                clayers = [(self.rows[g][l, 0], self.rows[g][l, 1], self.rows[g][l, 2], layers[l][3])
                            for l in range(self.L)]
             else:
                 if s == 1:

@@ -278,6 +278,21 @@ def test_batched_stack_list_lengths(k):
     _check(y, ref, x, TOL_BF16, f"batched stack k={k}")
 
 
+def test_batched_stack_partial_column_tile():
+    # Several samples run 64-column fused-down tiles (4 columns per lane): at d = 160 the last tile's second
+    # 32-column block lies past the row, so its lanes store nothing, not even a norm partial.
+    d, d_ff, T, L, B, k = 160, 1024, 40, 3, 2, 300
+    layers = [wl.make_layer(24, l, d, d_ff, "bf16", norm="random") for l in range(L)]
+    x = wl.make_x(24, (B, T, d), k)
+    masks = np.stack([np.stack([wl.uniform_mask(wl.rng(24, 4, l, b), d_ff, k - 20 * b) for b in range(B)])
+                      for l in range(L)])
+    idx, cnt = compact(masks.reshape(L * B, d_ff))
+    y = run_stack([dev_weights(l) for l in layers], x, idx, cnt, k)
+    ref = np.stack([oracle.ffn_stack(x[b], [lay.f64() for lay in layers],
+                                     [masks[l, b].astype(np.float64) for l in range(L)]) for b in range(B)])
+    _check(y, ref, x, TOL_BF16, "batched stack, partial column tile")
+
+
 # ------------------------------------------------------------------------------------------------ masks in
 
 MASKED_CASES = [
@@ -328,15 +343,17 @@ def test_masked_calls_equal_compaction_then_lists(d, d_ff, L, B, T, p, wdtype, n
 
 # ------------------------------------------------------------------------------------------------ one-sample stacks
 # A single sample's stack (and a single layer at d >= 2048) with a list of at most 2048 neurons runs the down
-# projection fused with the epilogue: one workgroup per (64-column tile, 16-token tile) sums the whole list.
+# projection fused with the epilogue: one workgroup per (32-column tile, 16-token tile) sums the whole list and
+# writes the next layer's input with its 32-column norm partials (2 columns per lane).
 
 FUSED_CASES = [
     # d, d_ff, L, T, k, norm
-    (96, 200, 3, 17, 150, "random"),    # a partial column tile, 5 chunks
+    (96, 200, 3, 17, 150, "random"),    # three 32-column tiles, a norm over a short last span, 5 chunks
     (160, 512, 2, 70, 300, "none"),     # five token tiles (T > 64)
     (2048, 4096, 1, 51, 1500, "random"),  # one layer at d = 2048
     (1024, 4096, 2, 1, 2048, "ones"),   # T = 1, 64 chunks (8 per wave)
     (256, 2048, 3, 64, 1999, "random"),
+    (2048, 8192, 2, 51, 1600, "random"),  # d = 2048 inside a stack: 8 spans of norm partials per token
 ]
 
 

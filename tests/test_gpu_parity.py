@@ -342,8 +342,8 @@ def test_masked_calls_equal_compaction_then_lists(d, d_ff, L, B, T, p, wdtype, n
 
 
 # ------------------------------------------------------------------------------------------------ one-sample stacks
-# A single sample's stack (and a single layer at d >= 2048) with a list of at most 2048 neurons runs the down
-# projection fused with the epilogue: one workgroup per (32-column tile, 16-token tile) sums the whole list and
+# A single sample's layer or stack with a list of at most 2048 neurons runs the down projection fused with the
+# epilogue: one workgroup per (32-column tile, 16-token tile) sums the whole list and
 # writes the next layer's input with its 32-column norm partials (2 columns per lane).
 
 FUSED_CASES = [

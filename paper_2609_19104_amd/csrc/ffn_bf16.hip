@@ -946,9 +946,13 @@ struct DfArgs {
 template <int N>
 using f32v = float __attribute__((ext_vector_type(N)));
 
-template <int CPW, int NT, int CW>
+// CPS < CPW: the chunks go in stages of CPS (each stage's loads, then its products), so that the four 16-token
+// tiles of a whole 64-token block (several samples) fit the registers: one workgroup per (sample, column tile)
+// then reads the sample's listed rows of its columns once, and the grid is one round.
+template <int CPW, int NT, int CW, int CPS = CPW>
 __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     static_assert(CW == 2 || CW == 4, "two or four columns per lane");
+    constexpr int STAGES = (CPW + CPS - 1) / CPS;
     using vec = f32v<CW>;
     const int q = xcd_logical(blockIdx.x, gridDim.x);  // = (sample * ncol + column tile) * ntt + token tile
     const int tt = q % a.ntt;
@@ -977,13 +981,19 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     __builtin_amdgcn_sched_barrier(0);  // the index loads go out first
 
     auto chunk_of = [&](int k) { return min(wave + k * rm::kDfWaves, nchunks - 1); };
-    DnChunk<NT> cb[CPW];
+    DnChunk<NT> cb[CPS];
+    auto load_h = [&](int stage) {  // chunk-major H: 16 tokens x 64 bytes, one contiguous kilobyte per tile
 #pragma unroll
-    for (int k = 0; k < CPW; ++k)  // chunk-major H: 16 tokens x 64 bytes, one contiguous kilobyte per tile
+        for (int k = 0; k < CPS; ++k)
+            if (stage * CPS + k < CPW)
 #pragma unroll
-        for (int j = 0; j < NT; ++j)
-            cb[k].a[j] = load16(Hb + (static_cast<size_t>(chunk_of(k)) * a.tpad + t0 + j * 16 + nn) * rm::kBfChunk +
-                                grp * 8);
+                for (int j = 0; j < NT; ++j)
+                    cb[k].a[j] = load16(Hb +
+                                        (static_cast<size_t>(chunk_of(stage * CPS + k)) * a.tpad + t0 + j * 16 + nn) *
+                                            rm::kBfChunk +
+                                        grp * 8);
+    };
+    load_h(0);
     // The epilogue's inputs depend on nothing computed here, so they are loaded now, behind the H tiles, and
     // the epilogue does not wait for memory a second time.  Wave w < 4 finishes token t0 + 16 j + 4 grp + w of
     // tile j (waves 4-7 load the same rows and drop them).
@@ -1011,20 +1021,22 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
         if (s < a.kcap) sidx[s] = clamp_neuron(iv[i], a.d_ff);
     }
     __syncthreads();
+    auto load_w = [&](int stage) {
 #pragma unroll
-    for (int k = 0; k < CPW; ++k) {
-        const int kb = chunk_of(k) * rm::kBfChunk + grp * 8;
-        const int4 i0 = *reinterpret_cast<const int4 *>(sidx + kb);
-        const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb + 4);
-        const int n[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+        for (int k = 0; k < CPS; ++k) {
+            if (stage * CPS + k >= CPW) continue;
+            const int kb = chunk_of(stage * CPS + k) * rm::kBfChunk + grp * 8;
+            const int4 i0 = *reinterpret_cast<const int4 *>(sidx + kb);
+            const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb + 4);
+            const int n[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const uint16_t *wp = a.wd + static_cast<size_t>(n[j]) * a.d + col;
-            if constexpr (CW == 4) cb[k].w[j] = load8(wp);
-            else cb[k].w[j] = make_uint2(*reinterpret_cast<const uint32_t *>(wp), 0u);
+            for (int j = 0; j < 8; ++j) {
+                const uint16_t *wp = a.wd + static_cast<size_t>(n[j]) * a.d + col;
+                if constexpr (CW == 4) cb[k].w[j] = load8(wp);
+                else cb[k].w[j] = make_uint2(*reinterpret_cast<const uint32_t *>(wp), 0u);
+            }
         }
-    }
-    __builtin_amdgcn_sched_barrier(0);
+    };
 
     rm_f32x4 acc[NT][4];
 #pragma unroll
@@ -1032,8 +1044,26 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
 #pragma unroll
         for (int c = 0; c < CW; ++c) acc[j][c] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = 0; k < CPW; ++k)
-        if (wave + k * rm::kDfWaves < nchunks) dn_mma<NT, CW>(cb[k], acc);
+    for (int stage = 0; stage < STAGES; ++stage) {
+        if (stage > 0) load_h(stage);
+        load_w(stage);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) {
+            const int kk = stage * CPS + k;
+            if (kk >= CPW) continue;
+            if constexpr (STAGES == 1) {
+                if (wave + kk * rm::kDfWaves < nchunks) dn_mma<NT, CW>(cb[k], acc);
+            } else {  // a chunk past the list enters with a zero H tile (exact zeros) rather than under a branch,
+                      // which would let the compiler move this stage's loads into it
+                if (wave + kk * rm::kDfWaves >= nchunks)
+#pragma unroll
+                    for (int j = 0; j < NT; ++j) cb[k].a[j] = zero16();
+                dn_mma<NT, CW>(cb[k], acc);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
 
     __shared__ rm_f32x4 red[rm::kDfWaves][CW][64];
     cnt = cnt < 0 ? 0 : (cnt > a.max_count ? a.max_count : cnt);
@@ -1288,11 +1318,22 @@ hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *i
         case 7: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7, NT, CW>, grid, block, st, a); break;    \
         default: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8, NT, CW>, grid, block, st, a); break;   \
     }
-    // The plan pairs one 16-token tile with 2 columns per lane (one sample) and two with 4 (several samples).
-    if (p.df_nt == 2 && p.df_cw == 4)
-        RM_DF(2, 4)
-    else if (p.df_nt == 1 && p.df_cw == 2)
+    // The plan pairs one 16-token tile with 2 columns per lane (one sample) and four with 4 (several samples).
+    if (p.df_nt == 4 && p.df_cw == 4) {
+        // Several samples: one 64-token block per workgroup, chunks in stages of 3 (at most 8 per wave).
+        switch (p.dn_cpw) {
+            case 1: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<1, 4, 4, 3>, grid, block, st, a); break;
+            case 2: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<2, 4, 4, 3>, grid, block, st, a); break;
+            case 3: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<3, 4, 4, 3>, grid, block, st, a); break;
+            case 4: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<4, 4, 4, 3>, grid, block, st, a); break;
+            case 5: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<5, 4, 4, 3>, grid, block, st, a); break;
+            case 6: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<6, 4, 4, 3>, grid, block, st, a); break;
+            case 7: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<7, 4, 4, 3>, grid, block, st, a); break;
+            default: e = launch_timed(RM_KERNEL_DOWN, down_fused_kernel<8, 4, 4, 3>, grid, block, st, a); break;
+        }
+    } else if (p.df_nt == 1 && p.df_cw == 2) {
         RM_DF(1, 2)
+    }
     else
         return hipErrorInvalidValue;
 #undef RM_DF

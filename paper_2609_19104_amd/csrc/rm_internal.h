@@ -63,12 +63,11 @@ struct Plan {
     int ncol = 0;        // column tiles
     int slices = 0;      // K-slices per column tile (down partial sums)
     int slice_units = 0; // bf16: 32-neuron chunks per slice; f32: neurons per slice
-    // bf16, lists of at most kDfMaxChunks chunks (7 chunks per wave with several samples): the down projection
-    // runs fused (one workgroup per column tile and token tile sums the whole list and applies the residual
+    // bf16, lists of at most kDfMaxChunks chunks: the down projection runs fused (one workgroup per column tile and token tile sums the whole list and applies the residual
     // itself: no partials, no epilogue launch).
     bool fused_down = false;
     int dn_cpw = 0;      // fused down: chunks per wave (the kernel's unrolled pipeline depth)
-    int df_nt = 1;       // fused down: 16-token tiles per workgroup (2 with several samples)
+    int df_nt = 1;       // fused down: 16-token tiles per workgroup (4 with several samples)
     int df_cw = 4;       // fused down: columns per lane (2 for one sample, 4 with several)
     int df_ncol = 0;     // fused down: column tiles of 16 df_cw columns
     int ntt = 0;         // fused down: token tiles of 16 df_nt tokens

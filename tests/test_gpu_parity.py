@@ -260,12 +260,13 @@ def test_stack_equals_layer_sequence():
     _check(y_stack, ref, x, TOL_BF16, "stack")
 
 
-@pytest.mark.parametrize("k", [1700, 1800, 64])
+@pytest.mark.parametrize("k", [1700, 2048, 2100, 64])
 def test_batched_stack_list_lengths(k):
-    # Several samples inside a stack: lists of up to 7 chunks per wave run the fused down projection with
-    # 32-token workgroups (1700 neurons: 54 chunks), longer ones the split projection and the epilogue (1800:
-    # 57 chunks), short ones one chunk per wave.  T = 40 leaves the second token tile ragged.
-    d, d_ff, T, L, B = 512, 2048, 40, 2, 3
+    # Several samples inside a stack: lists of up to 64 chunks run the fused down projection with one 64-token
+    # workgroup per (sample, column tile), its chunks in stages of 3 (1700 neurons: 54 chunks, 7 per wave, three
+    # stages; 2048: 8 per wave), longer ones the split projection and the epilogue (2100: 66 chunks), short ones
+    # one chunk per wave.  T = 40 leaves rows 40-63 of the token block padding.
+    d, d_ff, T, L, B = 512, 4096, 40, 2, 3
     layers = [wl.make_layer(23, l, d, d_ff, "bf16", norm="random") for l in range(L)]
     x = wl.make_x(23, (B, T, d), k)
     step = 40 if k > 100 else 8  # the samples' counts differ: ragged lists within the batch

@@ -30,8 +30,9 @@
 //   columns are physical columns 4 n + q.  No LDS transpose is needed, and 16 lanes read a full 128-byte line
 //   of a row.  The four waves take interleaved chunks; their tiles are summed in LDS in a fixed order and the
 //   slice's float32 partial is stored.  The epilogue kernel adds the slices in order to the residual.
-//   down_fused: for lists of at most 64 chunks, one workgroup sums the whole list for its tile (32 columns,
-//   2 per lane and 2 calls per chunk, for one sample; 64 columns with several) and does the epilogue's work.
+//   down_fused: for lists of at most 64 chunks, one workgroup sums the whole list for its tile and does the
+//   epilogue's work: one sample, 32 columns (2 per lane, 2 calls per chunk) and 16 tokens; several samples, 64
+//   columns and the whole 64-token block, the chunks in stages.
 #include "rm_internal.h"
 
 namespace {

@@ -1363,7 +1363,12 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
     switch (p.slice_units / kDnWaves) {                                                                  \
         case 1: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 1, ONE>, grid, block, st, a); break;    \
         case 2: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 2, ONE>, grid, block, st, a); break;    \
-        default: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 4, ONE>, grid, block, st, a); break;   \
+        case 3: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 3, ONE>, grid, block, st, a); break;    \
+        case 4: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 4, ONE>, grid, block, st, a); break;    \
+        case 5: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 5, ONE>, grid, block, st, a); break;    \
+        case 6: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 6, ONE>, grid, block, st, a); break;    \
+        case 7: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 7, ONE>, grid, block, st, a); break;    \
+        default: e = launch_timed(RM_KERNEL_DOWN, down_bf16_kernel<NT, 8, ONE>, grid, block, st, a); break;   \
     }
 #define RM_DOWN(NT)                          \
     if (p.T <= rm::kBfTokBlock) {            \

@@ -271,11 +271,13 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.act = s->act;
     const int kmax = max_count > 0 ? max_count : 1;
     size_t xn_elem, h_elem;
-    // Aim for about two down-projection workgroups per compute unit (256 CUs): fewer K-slices mean fewer
-    // float32 partials written and read back by the epilogue (config 4 at 30%: 10 slices instead of 20).
+    // Aim for one down-projection workgroup per compute unit (256 CUs): a grid just past a multiple of the unit
+    // count leaves the units with one more workgroup setting the time (config 4 at 30%: 8 slices of 20 chunks,
+    // 256 workgroups, instead of 10 slices of 16, 320: down 10.0 -> 8.1 us), and fewer K-slices mean fewer
+    // float32 partials written and read back by the epilogue.
     constexpr int kCUs = 256;
 #ifndef RM_DOWN_TARGET
-#define RM_DOWN_TARGET (2 * 256)
+#define RM_DOWN_TARGET 256
 #endif
     constexpr int kTargetDownGroups = RM_DOWN_TARGET;
     if (s->wdtype == RM_BF16) {
@@ -318,11 +320,11 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         q.col_tile = kBfColTile;
         q.ncol = ceil_div(s->d, q.col_tile);
         const int nchunks = q.kcap / kBfChunk;
-        // Chunks per slice: 4, 8 or 16 (1, 2 or 4 per wave), the fewest that keep the slice count near the
-        // target; longer lists get more slices.
+        // Chunks per slice: a multiple of 4 (1 to 8 per wave), the fewest that keep the slice count within the
+        // target; lists longer than 8 chunks per wave at the target get more slices.
         const int s_target = std::max(1, ceil_div(kTargetDownGroups, q.ncol * B));
-        int cps = kBfWaves;
-        while (cps < 4 * kBfWaves && ceil_div(nchunks, cps) > s_target) cps *= 2;
+        const int cps = kBfWaves * std::min(kBfMaxChunksPerSlice / kBfWaves,
+                                            std::max(1, ceil_div(ceil_div(nchunks, s_target), kBfWaves)));
         q.slice_units = cps;
         q.slices = ceil_div(nchunks, cps);
         // Short lists (up to kDfMaxChunks chunks): one workgroup per (column tile, token tile) can sum the whole

@@ -28,7 +28,7 @@ constexpr int kBfNeurPerBlk = 8;    // neurons per gate/up workgroup (8 gate row
 constexpr int kBfChunk = 32;        // neurons per down-projection matrix-core step (K of the 16x16x32 tile)
 constexpr int kBfColTile = 64;      // output columns per down workgroup (16 lanes x 4 columns)
 constexpr int kBfWaves = 4;
-constexpr int kBfMaxChunksPerSlice = 16;  // down: a slice's indices (16 x 32) are staged in 2 KB of LDS
+constexpr int kBfMaxChunksPerSlice = 32;  // down: a slice's indices (32 x 32) are staged in 4 KB of LDS
 constexpr int kDfWaves = 8;        // fused down: waves per workgroup
 constexpr int kDfMaxCpw = 8;       // fused down: at most 8 chunks per wave
 constexpr int kDfMaxChunks = kDfWaves * kDfMaxCpw;  // lists of up to 64 chunks (2048 neurons)

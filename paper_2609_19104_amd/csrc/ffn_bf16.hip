@@ -93,6 +93,15 @@ __device__ __forceinline__ void load_rnorm(const GuArgs &a, int b, int t0, float
     }
 }
 
+// The Eq. 4 anchor value h_a of (slot, token t) for gu_store_h, loaded ahead of the products so that the store
+// of h waits for no memory: an unconditional load of a clamped in-bounds address (without an anchor it reads the
+// list's first entry and the value is not used).
+__device__ __forceinline__ float anchor_h(const GuArgs &a, int b, int slot, int t) {
+    const size_t ai = (static_cast<size_t>(b) * a.max_count + min(slot, a.max_count - 1)) * a.T + min(t, a.T - 1);
+    const float *p = a.h_anchor != nullptr ? a.h_anchor + ai : reinterpret_cast<const float *>(a.idx);
+    return *p;
+}
+
 // The partial sums of squares of one token block (tokens 0..63 of sample b; rows past T repeat the last token),
 // NS spans of 8 partials (256 columns) per token, loaded by the workgroup's 512 threads in memory order: thread e
 // takes span e % NS of token e / NS (32 contiguous bytes; threads past 64 NS repeat the last), so that a wave
@@ -141,10 +150,11 @@ __device__ __forceinline__ int lane_neuron(const GuArgs &a, int b, int slot) {
 // tokens at or past T get h = 0 (their rows and columns were computed from clamped loads).  H is chunk-major
 // (32-slot chunks, then tokens).  Thread tid finishes tile row tid & 7 (its gate row; the up row is 8 further) for
 // token tid >> 3, whose list slot is `slot` (< 0: a duplicate row, nothing stored) and RMSNorm factor r.
+// ha_pre: the Eq. 4 anchor value was loaded ahead (ha, from anchor_h), else it is loaded here.
 // red(w, tt, lane) is d-part w's tile tt (lane L, register i = row 4 (L / 16) + i, token L % 16).
 template <int NT, typename RedAt>
 __device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, int b, RedAt red, int ds, int t0,
-                                           int slot, int cnt, float r) {
+                                           int slot, int cnt, float r, bool ha_pre = false, float ha = 0.0f) {
     const int j = threadIdx.x & 7;
     const int tok = threadIdx.x >> 3;
     const int tt = tok >> 4, tc = tok & 15;
@@ -169,7 +179,7 @@ __device__ __forceinline__ void gu_store_h(const GuArgs &a, uint16_t *Hb, int b,
         if (live) a.h_out[ai] = h;
         return;
     }
-    if (a.h_anchor != nullptr && live) h -= a.h_anchor[ai];  // Eq. 4: h_t - h_a, rounded once
+    if (a.h_anchor != nullptr && live) h -= ha_pre ? ha : a.h_anchor[ai];  // Eq. 4: h_t - h_a, rounded once
     if (!live) h = 0.0f;
     Hb[(static_cast<size_t>(slot >> 5) * a.tpad + t) * rm::kBfChunk + (slot & 31)] =
         static_cast<uint16_t>(rm_f32_to_bf16_bits(h));
@@ -209,6 +219,7 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
     const int grp = lane >> 4;  // which 8 of the 32 K values of a step this lane carries
     const int cnt = clamp_count(a.count[b], a.max_count);  // used only when h is stored
     const int raw_n = a.idx[static_cast<size_t>(b) * a.d_ff + min(slot0 + (r & 7), a.d_ff - 1)];
+    float ha = anchor_h(a, b, slot0 + (tid & 7), tid >> 3);  // token block 0's anchor value (Eq. 4)
     uint16_t *Hb = a.H + static_cast<size_t>(b) * a.tpad * a.kcap;
     const int col0 = wave * SPW * 32;
 
@@ -279,11 +290,12 @@ __global__ __launch_bounds__(kGuThreads) void gateup_direct_kernel(GuArgs a) {
         }
         __syncthreads();
         const float rt = kOneBlock ? span_rnorm<SPW>(a, rn, tid >> 3) : rn[tid >> 3];
-        gu_store_h<NT>(a, Hb, b, red, kGuWaves, t0, slot0 + (tid & 7), cnt, rt);
+        gu_store_h<NT>(a, Hb, b, red, kGuWaves, t0, slot0 + (tid & 7), cnt, rt, true, ha);
         t0 += rm::kBfTokBlock;
         if (kOneBlock || t0 >= a.T) break;
         __syncthreads();  // every wave has read the tiles before the regions are refilled
         load_x(t0, xv);
+        ha = anchor_h(a, b, slot0 + (tid & 7), t0 + (tid >> 3));
     }
 }
 
@@ -979,6 +991,18 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
     for (int i = 0; i < kIdxPerThread; ++i)
         iv[i] = a.idx[static_cast<size_t>(b) * a.d_ff + min(min(tid + i * kDfThreads, a.kcap - 1), a.d_ff - 1)];
     int cnt = a.count[b];
+    // The epilogue's inputs depend on nothing computed here, so they are loaded now and the epilogue does not
+    // wait for memory a second time.  Wave w < 4 finishes token t0 + 16 j + 4 grp + w of tile j (waves 4-7 load
+    // the same rows and drop them).  An anchor's y_a goes out first, right behind the indices: the compiler waits
+    // for the loads before it inside that branch, and the indices are needed next anyway.
+    size_t ro[NT];
+    vec x_in[NT], ya_in[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+        ro[j] = (static_cast<size_t>(b) * a.T + min(t0 + j * 16 + grp * 4 + (wave & 3), a.T - 1)) * a.d + col;
+    if (a.ya_in != nullptr)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) ya_in[j] = *reinterpret_cast<const vec *>(a.ya_in + ro[j]);
     __builtin_amdgcn_sched_barrier(0);  // the index loads go out first
 
     auto chunk_of = [&](int k) { return min(wave + k * rm::kDfWaves, nchunks - 1); };
@@ -995,26 +1019,13 @@ __global__ __launch_bounds__(kDfThreads) void down_fused_kernel(DfArgs a) {
                                         grp * 8);
     };
     load_h(0);
-    // The epilogue's inputs depend on nothing computed here, so they are loaded now, behind the H tiles, and
-    // the epilogue does not wait for memory a second time.  Wave w < 4 finishes token t0 + 16 j + 4 grp + w of
-    // tile j (waves 4-7 load the same rows and drop them).
-    vec zero;
 #pragma unroll
-    for (int c = 0; c < CW; ++c) zero[c] = 0.0f;
-    size_t ro[NT];
-    vec x_in[NT], ya_in[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-        ro[j] = (static_cast<size_t>(b) * a.T + min(t0 + j * 16 + grp * 4 + (wave & 3), a.T - 1)) * a.d + col;
-        x_in[j] = *reinterpret_cast<const vec *>(a.x + ro[j]);
-        ya_in[j] = zero;
-    }
-    vec gate = zero, g_next = zero;
-    if (a.ya_in != nullptr)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) ya_in[j] = *reinterpret_cast<const vec *>(a.ya_in + ro[j]);
-    if (a.out_gate != nullptr) gate = *reinterpret_cast<const vec *>(a.out_gate + static_cast<size_t>(b) * a.d + col);
-    if (a.g_next != nullptr) g_next = *reinterpret_cast<const vec *>(a.g_next + col);
+    for (int j = 0; j < NT; ++j) x_in[j] = *reinterpret_cast<const vec *>(a.x + ro[j]);
+    // The gates load unconditionally (under its branch the compiler waited there for every load in flight): a
+    // gate the call does not have reads x instead, and its value is not used.
+    const vec gate =
+        *reinterpret_cast<const vec *>((a.out_gate != nullptr ? a.out_gate + static_cast<size_t>(b) * a.d : a.x) + col);
+    const vec g_next = *reinterpret_cast<const vec *>((a.g_next != nullptr ? a.g_next : a.x) + col);
     __builtin_amdgcn_sched_barrier(0);  // then the H tiles, before the wait for the indices
 #pragma unroll
     for (int i = 0; i < kIdxPerThread; ++i) {

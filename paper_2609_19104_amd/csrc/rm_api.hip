@@ -217,7 +217,7 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
     const size_t y_stride = static_cast<size_t>(p.B) * p.T * p.d;
     // The fused down projection sums the whole list in each workgroup: fewer, longer workgroups than the split
     // over K, and no epilogue launch.  With one sample's 32-column tiles it is the faster form for every list
-    // it takes, a single d = 1024 layer included (config 2: 15.6 -> 15.3 us per step).
+    // it takes, a single d = 1024 layer included (d_ff = 4096, 1229 neurons, T = 51: 15.6 -> 15.3 us per step).
     const bool fused = p.fused_down;
     for (int l = 0; l < L; ++l) {
         const int32_t *il = idx + l * list_stride;
@@ -272,7 +272,7 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     const int kmax = max_count > 0 ? max_count : 1;
     size_t xn_elem, h_elem;
     // Aim for one down-projection workgroup per compute unit (256 CUs): a grid just past a multiple of the unit
-    // count leaves the units with one more workgroup setting the time (config 4 at 30%: 8 slices of 20 chunks,
+    // count leaves the units with one more workgroup setting the time (d = 2048, 4916 neurons: 8 slices of 20 chunks,
     // 256 workgroups, instead of 10 slices of 16, 320: down 10.0 -> 8.1 us), and fewer K-slices mean fewer
     // float32 partials written and read back by the epilogue.
     constexpr int kCUs = 256;
@@ -282,12 +282,12 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     constexpr int kTargetDownGroups = RM_DOWN_TARGET;
     if (s->wdtype == RM_BF16) {
         q.tpad = ceil_div(T, kBfTokBlock) * kBfTokBlock;
-        // Gate/up workgroups of 8 * NG neurons.  Measured on configs 4 and 5: one round of workgroups that fills
-        // most compute units is best (the widest NG with 150 .. 256 workgroups); a grid just past the compute
-        // units (256 .. 384 workgroups) is the worst case, since the compute units that get a second workgroup
-        // set the time, so a grid there takes the next narrower NG (more, lighter workgroups); otherwise the
-        // widest NG that still gives every compute unit one workgroup, or one group of 8 per workgroup (the
-        // direct kernel, when d allows) for short lists.
+        // Gate/up workgroups of 8 * NG neurons.  Measured at d = 2048 (one sample) and d = 1024 (16 samples):
+        // one round of workgroups that fills most compute units is best (the widest NG with 150 .. 256
+        // workgroups); a grid just past the compute units (256 .. 384 workgroups) is the worst case, since the
+        // compute units that get a second workgroup set the time, so a grid there takes the next narrower NG
+        // (more, lighter workgroups); otherwise the widest NG that still gives every compute unit one
+        // workgroup, or one group of 8 per workgroup (the direct kernel, when d allows) for short lists.
         const int k32 = ceil_div(kmax, kBfChunk) * kBfChunk;
         const bool direct_ok = s->d == 256 || s->d == 512 || s->d == 1024 || s->d == 2048;
         // One sample with more groups of 8 slots than compute units (up to 3 per unit): the spread kernel, one
@@ -329,7 +329,7 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
         q.slices = ceil_div(nchunks, cps);
         // Short lists (up to kDfMaxChunks chunks): one workgroup per (column tile, token tile) can sum the whole
         // list.  One sample: 16-token tiles.  Several samples: one 64-token tile, so each sample's listed rows of
-        // a column tile are read once (config 5: down 17.8 -> 14.8 us per layer against two 32-token tiles).
+        // a column tile are read once (16 samples of 51 tokens, d = 1024: down 17.8 -> 14.8 us against two 32-token tiles).
         q.dn_cpw = ceil_div(nchunks, kDfWaves);
         q.df_nt = B == 1 ? 1 : 4;
         q.fused_down = nchunks <= kDfMaxChunks;

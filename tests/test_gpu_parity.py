@@ -98,6 +98,10 @@ BF16_CASES = [
     (1024, 8192, 64, 8192, "ones"),
     (256, 4096, 17, 2056, "none"),
     (512, 4096, 51, 2500, "random"),
+    # the split down projection's K-slices of 12, 24 and 28 chunks (3, 6 and 7 per wave), 256 workgroups or fewer
+    (1024, 8192, 51, 5000, "none"),
+    (1024, 16384, 51, 11000, "random"),
+    (1024, 16384, 33, 13500, "none"),
 ]
 
 

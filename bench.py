@@ -206,7 +206,12 @@ class Setup:
         return active_weight_bytes(self.k, self.d, 2)
 
     def hooks(self):
-        return ffn_hooks(self.rm, gateup_bytes(self.k, self.d, 2), down_bytes(self.k, self.d, 2))
+        gu, dn = gateup_bytes(self.k, self.d, 2), down_bytes(self.k, self.d, 2)
+        if self.rm.rm_layer_kernels(self.d, self.d_ff, self.rm.RM_BF16, self.B, self.T, self.k) == \
+                1 << self.rm.RM_KERNEL_LAYER:  # gate/up and down in one launch (layer_xcd_kernel)
+            return [(self.rm.RM_KERNEL_LAYER, "gate/up + down projections in one launch (layer_xcd_kernel)",
+                     "layer", gu + dn)]
+        return ffn_hooks(self.rm, gu, dn)
 
 
 def _stack_copies(layers, device, cold: bool):
@@ -625,6 +630,9 @@ def time_steps(setup: Setup, steps: int, warmup: int, hook: bool = False):
         setup.step(warmup + i)
     end.record()
     torch.cuda.synchronize()
+    if hook:  # disarm: a slot armed for a kernel the step did not launch must not catch a later launch
+        for kk in evs:
+            rm.rm_profile_kernel_events(kk, None, None)
     ms = start.elapsed_time(end) / steps
     kern = None
     if hook:

@@ -315,9 +315,18 @@ typedef enum rm_kernel_id {
     RM_KERNEL_GATEUP = 0,      /* gate/up projection of the FFN calls                          */
     RM_KERNEL_DOWN = 1,        /* down projection of the FFN calls                             */
     RM_KERNEL_SCORES = 2,      /* Eq. 1 scores of rm_group_masks                               */
-    RM_KERNEL_GROUP_SELECT = 3 /* top-K selection, union and rerank of rm_group_masks          */
+    RM_KERNEL_GROUP_SELECT = 3, /* top-K selection, union and rerank of rm_group_masks         */
+    RM_KERNEL_LAYER = 4         /* gate/up and down of one layer in one launch (one sample's    */
+                                /* long list at d = 2048: the workgroups of each XCD meet      */
+                                /* between the two projections)                                */
 } rm_kernel_id;
 rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end);
+
+/* Measurement: which of the hooked kernels a single-layer call (rm_sparse_ffn_layer, rm_masked_ffn_layer) of
+ * this shape launches on the current device: bit k of *kernels (a host pointer) is set for rm_kernel_id k
+ * (RM_KERNEL_GATEUP and RM_KERNEL_DOWN, or RM_KERNEL_LAYER alone when the gate/up and down projections run in
+ * one launch).  Host only; enqueues nothing.  Errors: those of rm_workspace_size. */
+rm_status rm_layer_kernels(const rm_ffn_shape *s, int32_t B, int32_t T, int32_t max_count, uint32_t *kernels);
 
 /* Measurement: a plain streaming read of `bytes` of `buf` (16-byte aligned, bytes a positive multiple of 16) by
  * `workgroups` workgroups of 512 threads, each lane keeping eight 16-byte loads in flight.  It computes nothing

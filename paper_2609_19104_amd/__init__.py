@@ -42,6 +42,7 @@ RM_KERNEL_GATEUP = 0
 RM_KERNEL_DOWN = 1
 RM_KERNEL_SCORES = 2
 RM_KERNEL_GROUP_SELECT = 3
+RM_KERNEL_LAYER = 4
 
 EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_sparse_ffn_layer_noalloc",
             "rm_sparse_ffn_stack",
@@ -49,7 +50,7 @@ EXPORTED = ("rm_mask_compact", "rm_workspace_size", "rm_sparse_ffn_layer", "rm_s
             "rm_delta_ffn_stack", "rm_gather_stack_rows", "rm_context_select", "rm_context_workspace_size",
             "rm_context_ffn", "rm_context_pack_size", "rm_context_pack", "rm_context_ffn_packed", "rm_neuron_norms",
             "rm_group_masks",
-            "rm_profile_kernel_events", "rm_stream_read",
+            "rm_profile_kernel_events", "rm_layer_kernels", "rm_stream_read",
             "rm_status_string", "rm_last_error")
 
 # (w_gate, w_up, w_down, norm_g) or (w_gate, w_up, w_down, norm_g, out_gate); norm_g and out_gate may be None.
@@ -112,6 +113,7 @@ def load_library() -> ctypes.CDLL:
         "rm_neuron_norms": [vp, i32, i32, i32, vp, vp],
         "rm_group_masks": [vp, i32, i32, i32, i32, vp, i32, vp, vp, vp],
         "rm_profile_kernel_events": [i32, vp, vp],
+        "rm_layer_kernels": [sp, i32, i32, i32, ctypes.POINTER(ctypes.c_uint32)],
         "rm_stream_read": [vp, sz, i32, vp, vp],
         "rm_status_string": [i32],
         "rm_last_error": [],
@@ -224,6 +226,14 @@ def rm_workspace_size(d: int, d_ff: int, wdtype: int, B: int, T: int, max_count:
     out = ctypes.c_size_t(0)
     shape = FfnShape(d, d_ff, wdtype, eps)
     _check(load_library().rm_workspace_size(ctypes.byref(shape), B, T, max_count, ctypes.byref(out)))
+    return int(out.value)
+
+
+def rm_layer_kernels(d: int, d_ff: int, wdtype: int, B: int, T: int, max_count: int, eps: float = 1e-6) -> int:
+    """Bit mask of the RM_KERNEL_* ids a single-layer call of this shape launches on the current device."""
+    out = ctypes.c_uint32(0)
+    shape = FfnShape(d, d_ff, wdtype, eps)
+    _check(load_library().rm_layer_kernels(ctypes.byref(shape), B, T, max_count, ctypes.byref(out)))
     return int(out.value)
 
 

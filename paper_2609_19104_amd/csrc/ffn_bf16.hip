@@ -629,19 +629,30 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
 // [32 w, 32 w + 32) of every 256-column chunk for all the tiles.  The chunk pipeline is the pipelined kernel's
 // (weights and input of a chunk issued ahead, rotated chunk order); each tile's 8 wave partials are added in wave
 // order through LDS.
-template <int NG, int NCH>
-__device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G, int nquads,
-                                                   uint16_t (*xs)[64 * kRowPitch], rm_f32x4 *red2, float *spans) {
-    constexpr int NT = 4;
+// pre(): extra loads of the caller, issued right behind the first weight chunks (PRE_AT = 0) or behind the loads
+// of chunk PRE_AT - 1 inside the chunk loop (the one-launch layer form fetches its down-projection rows there);
+// PXM: input chunks in flight.
 #ifndef RM_SPREAD_WTILES
 #define RM_SPREAD_WTILES 9
 #endif
 #ifndef RM_SPREAD_PX
 #define RM_SPREAD_PX 6
 #endif
+struct NoPre {
+    __device__ void operator()() const {}
+};
+// kLate (the one-launch layer form, whose workgroups write the input first): early() runs once the indices
+// have arrived, before the first weight loads; mid() runs behind them; the input and its norm partials are
+// loaded after mid() instead of ahead of the indices.
+template <int NG, int NCH, int PXM = RM_SPREAD_PX, int PRE_AT = 0, bool kLate = false, typename Pre = NoPre,
+          typename Early = NoPre, typename Mid = NoPre>
+__device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G, int nquads,
+                                                   uint16_t (*xs)[64 * kRowPitch], rm_f32x4 *red2, float *spans,
+                                                   Pre pre = Pre{}, Early early = Early{}, Mid mid = Mid{}) {
+    constexpr int NT = 4;
     constexpr int PW0 = RM_SPREAD_WTILES / (NG > 0 ? NG : 1);  // weight chunks in flight
     constexpr int PW = PW0 < 1 ? 1 : (PW0 < NCH ? PW0 : NCH);
-    constexpr int PX = RM_SPREAD_PX < NCH ? RM_SPREAD_PX : NCH;  // input chunks in flight
+    constexpr int PX = PXM < NCH ? PXM : NCH;  // input chunks in flight
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -686,9 +697,12 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
         for (int j = 0; j < NG; ++j) w[c % PW][j] = load16(wrow[j] + col);
     };
     // The input of the first chunks goes out before the wait for the indices, then the weights.
+    if constexpr (!kLate) {
 #pragma unroll
-    for (int c = 0; c < PX; ++c) load_x(c);
+        for (int c = 0; c < PX; ++c) load_x(c);
+    }
     __builtin_amdgcn_sched_barrier(0);
+    early();
     // Rows 8-15 of a tile read W_up: an offset added to W_gate's address.  (Selecting between the two pointers
     // lets the compiler fetch the chosen one from the kernel arguments with a vector load, issued behind the
     // input chunks, which would hold every weight load until all of them have arrived.)
@@ -698,8 +712,14 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
         wrow[j] = a.wg + up_off + static_cast<size_t>(clamp_neuron(raw_n[j], a.d_ff)) * a.d + wave * 32 + grp * 8;
 #pragma unroll
     for (int c = 0; c < PW; ++c) load_w(c);
+    if constexpr (PRE_AT == 0) pre();
     // Behind the first weights, the partial sums of squares of tokens 0..63 (NCH spans per token); their span
     // sums go to LDS after the products, so that forming the norm factors needs no memory round trip after them.
+    if constexpr (kLate) {
+        mid();
+#pragma unroll
+        for (int c = 0; c < PX; ++c) load_x(c);
+    }
     float4 sp_lo, sp_hi;
     load_spans<NCH>(a, 0, sp_lo, sp_hi);
 
@@ -722,6 +742,7 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
             for (int j = 0; j < NG; ++j) acc[j][tt] = mfma_bf16(w[c % PW][j], bx, acc[j][tt]);
         }
         if (c + PW < NCH) load_w(c + PW);
+        if (PRE_AT > 0 && c + 1 == (PRE_AT < NCH ? PRE_AT : NCH)) pre();
     }
     store_span<NCH>(spans, sp_lo, sp_hi);
     // The waves' partial tiles of every tile go through LDS at once (tiles 0 and 1 in the input buffers, free once
@@ -932,6 +953,304 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
         __syncthreads();
 #pragma unroll
         for (int k = 0; k < PD; ++k) load_h(cb[k], k, t0);
+    }
+}
+
+// ------------------------------------------------------------------------------------------ layer, per XCD
+
+// One sample's list at d = 2048 with 257 .. 768 groups of 8 listed slots (the spread plan's range): the FFN input's
+// bf16 rounding, the gate/up and the down projection in one launch of 256 workgroups, one per compute unit, so no
+// prologue launch precedes it.  The list's 32-slot chunks are cut into 8 slices of cps chunks, slice x for the 32
+// workgroups of XCD x (workgroup i runs on XCD i mod 8, checked against the hardware's XCC_ID register).
+//   Phase 0: the XCD's 32 workgroups write the XCD's own copy of xn = bf16(x g) (and, with a norm, its per-token
+//            partial sums of squares, in the prologue's order), one (token row, 256-column block) unit per wave.
+//   Phase 1: the spread gate/up over the slice's quads of 4 slots (dealt round-robin over the XCD's 32
+//            workgroups), reading the XCD's xn copy and writing h into H.
+//   Phase 2: the down projection of the same slice for column tile i / 8 (64 columns), whose float32 partial goes
+//            to the slice's row of the partials as the split down projection writes it, so the epilogue launch
+//            is unchanged.
+// Between the phases the XCD's workgroups meet; everything a phase reads was written by compute units of the same
+// XCD, so no hand-off needs the device-wide L2 write-back that makes a hand-off between XCDs cost more than a
+// kernel boundary.  Inside one launch a plain load can be served a stale copy of a line that another compute unit
+// stores to, and an atomic does not see plain stores' lines either; a device-scope load reads the stored value.
+//   Meeting 1 (after phase 0): each workgroup stores the launch's tag in its flag (tag: the dispatch packet's id
+//            mixed with the queue's address, different for every launch, so the flags need no reset and the
+//            workspace no initialization) once its phase-0 stores are complete, and polls the XCD's 32 flags with
+//            device-scope loads, behind its first weight loads (so the wait overlaps them).  Rank 0 first resets
+//            the XCD's counter for meeting 2 with an atomic swap.
+//   Meeting 2 (after phase 1): an atomic add on that counter (executed past the L1, where the polls, also
+//            atomic adds, read it) until it reaches 32.
+// The xn copy and H are read with plain loads: no line of them is read in the launch before it is written.  A
+// wait gives up after spin_ticks of the 100 MHz real-time clock; then, or when a workgroup is not on the XCD its
+// number names, the workgroup writes NaN partials, so the layer's output is NaN rather than wrong.
+constexpr int kXlPerXcd = 32;  // workgroups per XCD: 256 compute units / 8 XCDs
+
+struct XlArgs {
+    GuArgs g;            // the gate/up arguments (one sample); g.xn / g.ssq: XCD 0's copies, XCD x's at + x stride
+    const float *x;      // the FFN input, float32 [T][d]
+    const float *norm_g; // the norm gain [d], or null
+    uint16_t *xn8;       // [8][T][d] bf16: XCD x's copy of xn
+    float *ssq8;         // [8][T][ssq_stride(d)]: XCD x's copy of the partial sums of squares (norm only)
+    const uint16_t *wd;  // neuron-major W_down [d_ff][d]
+    float *part;         // float32 partials [slices][T][d], slice x = chunks [x cps, (x + 1) cps)
+    unsigned long long *flags;  // [8][32]: meeting 1's flag of workgroup (XCD x, rank r) at flags[32 x + r]
+    unsigned *ctr;       // [8][64]: meeting 2's counter of XCD x at ctr[64 x] (its own 256-byte line)
+    unsigned zero;       // 0, an operand the compiler cannot see, so that a poll stays an atomic add
+    int cps;             // chunks per slice, at most 8 CPW
+    long long spin_ticks;
+};
+
+__device__ __forceinline__ unsigned xcc_id() {
+    unsigned v;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+    return v & 0xfu;
+}
+
+extern "C" __device__ unsigned long long rm_llvm_dispatch_id() __asm("llvm.amdgcn.dispatch.id");
+
+// A 64-bit value that differs between launches: the dispatch packet's id in its queue (a counter) times an odd
+// constant (a bijection), xor the queue's address.
+__device__ __forceinline__ unsigned long long launch_tag() {
+    const unsigned long long q = reinterpret_cast<unsigned long long>(__builtin_amdgcn_queue_ptr());
+    return (rm_llvm_dispatch_id() + 1ull) * 0x9E3779B97F4A7C15ull ^ q;
+}
+
+// NCH: 256-column chunks of d (8 at d = 2048); CPW: chunks per wave in phase 2 (cps <= 8 CPW).  The phase-2
+// rows of W_down are requested inside phase 1, behind the loads of its chunk RM_XCD_PRE_AT - 1 (the last
+// chunk's weights are then in flight, so no product waits for them), and held in registers until meeting 2;
+// after it only H (from this XCD's L2) is read.  Requested at the start instead, they delayed the first input
+// chunk by 2.7 us; requested after the meeting, the down phase waited for them.
+#ifndef RM_XCD_PX
+#define RM_XCD_PX 6
+#endif
+#ifndef RM_XCD_PRE_AT
+#define RM_XCD_PRE_AT 7
+#endif
+template <int NCH, int CPW>
+__global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
+    constexpr int NT = 4;
+    constexpr int kXsBytes = 2 * 64 * kRowPitch * 2;            // phase 1: the staged input chunks
+    constexpr int kRed2Bytes = kGuWaves * NT * 64 * 16;          // phase 1: the third tile's wave partials
+    constexpr int kRedBytes = kGuWaves * NT * 4 * 64 * 16;       // phase 2: the 8 waves' 64 x 64 tiles
+    static_assert(kXsBytes + kRed2Bytes <= kRedBytes, "phase 1's buffers fit phase 2's");
+    constexpr int kSlots = CPW * kGuWaves * rm::kBfChunk;        // indices of a slice
+    constexpr int kIdxPer = (kSlots + kGuThreads - 1) / kGuThreads;
+    constexpr int kUnits = 2;                                    // phase-0 units per wave: 64 rows x NCH blocks / 256
+    __shared__ __attribute__((aligned(16))) unsigned char lds[kRedBytes];
+    __shared__ float spans[(NCH + 1) * 64];
+    __shared__ __attribute__((aligned(16))) int sidx[kSlots];
+    __shared__ int s_fail;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int x = blockIdx.x & 7;
+    const int rank = blockIdx.x >> 3;  // the workgroup's place on its XCD, and its phase-2 column tile
+    GuArgs g = a.g;
+    g.xn = a.xn8 + static_cast<size_t>(x) * g.T * g.d;
+    if (g.ssq != nullptr) g.ssq = a.ssq8 + static_cast<size_t>(x) * g.T * rm::ssq_stride(g.d);
+    const int nchunks = g.kcap / rm::kBfChunk;
+    const int c0 = x * a.cps;
+    const int n = max(0, min(c0 + a.cps, nchunks) - c0);  // chunks of this XCD's slice
+
+    // Phase 0's input: unit u = row * NCH + block of the XCD's T * NCH units, u = 8 rank + wave + 256 k; the loads
+    // are unconditional (a unit past the rows reloads the last one, whose results are not stored).
+    const int units = g.T * NCH;
+    float4 xin[kUnits], gin[kUnits];
+#pragma unroll
+    for (int k = 0; k < kUnits; ++k) {
+        const int u = min(rank * kGuWaves + wave + k * kXlPerXcd * kGuWaves, units - 1);
+        const size_t o = static_cast<size_t>(u / NCH) * g.d + (u % NCH) * kChunkCols + lane * 4;
+        xin[k] = *reinterpret_cast<const float4 *>(a.x + o);
+        gin[k] = *reinterpret_cast<const float4 *>((a.norm_g != nullptr ? a.norm_g : a.x) + (u % NCH) * kChunkCols +
+                                                   lane * 4);
+    }
+
+    const int grp = lane >> 4;  // phase 2: slots 8 grp .. 8 grp + 7 of a chunk
+    const int nn = lane & 15;   // phase 2: token in tile, and physical columns 4 nn + q
+    const int colw = rank * rm::kBfColTile + nn * 4;
+    const bool colok = colw < g.d;
+    const int col = min(colw, g.d - 4);  // columns past d re-read column d - 4; those outputs are not stored
+    // Phase 2's chunk k of this wave: slice chunk wave + 8 k (clamped to the slice; the products of a chunk past
+    // it are skipped), counted from a start that differs by column tile, so that the XCD's 32 workgroups do not
+    // all read the same chunk of H from the L2 at the same time.
+    const int rot = rank % max(n, 1);
+    auto chunk_of = [&](int k) {
+        const int j = min(wave + k * kGuWaves, max(n, 1) - 1);
+        return c0 + (j + rot < max(n, 1) ? j + rot : j + rot - max(n, 1));
+    };
+    // The slice's indices go out with the input (two coalesced loads per thread) and are staged in LDS when the
+    // rows they name are requested.
+    int iv[kIdxPer];
+#pragma unroll
+    for (int q = 0; q < kIdxPer; ++q) {
+        const int i = min(tid + q * kGuThreads, max(n * rm::kBfChunk, 1) - 1);
+        iv[q] = g.idx[min(c0 * rm::kBfChunk + i, g.d_ff - 1)];
+    }
+    uint2 wdn[CPW][8];
+    auto pre = [&]() {
+#pragma unroll
+        for (int q = 0; q < kIdxPer; ++q) {
+            const int i = tid + q * kGuThreads;
+            if (i < kSlots) sidx[i] = clamp_neuron(iv[q], g.d_ff);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < CPW; ++k) {
+            const int kb = (chunk_of(k) - c0) * rm::kBfChunk + grp * 8;
+            const int4 i0 = *reinterpret_cast<const int4 *>(sidx + kb);
+            const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb + 4);
+            const int nr[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) wdn[k][j] = load8(a.wd + static_cast<size_t>(nr[j]) * g.d + col);
+        }
+    };
+    const unsigned long long tag = launch_tag();
+    unsigned long long *fl = a.flags + x * kXlPerXcd;
+    unsigned *ctr = a.ctr + x * 64;
+    if (tid == 0) s_fail = xcc_id() != static_cast<unsigned>(x) ? 1 : 0;
+    // Phase 0 (once the indices have arrived, before the first weight loads): round x g to bf16 into this XCD's
+    // copy of xn, as the prologue does, then arrive at meeting 1.
+    auto early = [&]() {
+#pragma unroll
+        for (int k = 0; k < kUnits; ++k) {
+            const int u = rank * kGuWaves + wave + k * kXlPerXcd * kGuWaves;
+            const int row = u / NCH, blk = u % NCH;
+            float4 v = xin[k];
+            if (g.ssq != nullptr) {  // partial sums of squares of the row's 32-column blocks
+                const float ss = rm_ssq32(v, true);
+                if (u < units && (lane & 7) == 0)
+                    const_cast<float *>(g.ssq)[static_cast<size_t>(row) * rm::ssq_stride(g.d) + blk * 8 + (lane >> 3)] = ss;
+                v.x *= gin[k].x;
+                v.y *= gin[k].y;
+                v.z *= gin[k].z;
+                v.w *= gin[k].w;
+            }
+            uint2 packed;
+            packed.x = rm_f32_to_bf16_bits(v.x) | (rm_f32_to_bf16_bits(v.y) << 16);
+            packed.y = rm_f32_to_bf16_bits(v.z) | (rm_f32_to_bf16_bits(v.w) << 16);
+            if (u < units)
+                *reinterpret_cast<uint2 *>(const_cast<uint16_t *>(g.xn) + static_cast<size_t>(row) * g.d +
+                                           blk * kChunkCols + lane * 4) = packed;
+        }
+        if (tid == 0 && rank == 0) __hip_atomic_exchange(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's stores are complete
+        __syncthreads();
+    };
+    // Meeting 1, behind the first weight loads: arrive, then wait until the XCD's 32 flags hold the tag.
+    auto mid = [&]() {
+        if (tid == 0) fl[rank] = tag;
+        if (wave == 0) {
+            bool fail = false;
+            const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+            for (;;) {
+                const unsigned long long f =
+                    __hip_atomic_load(fl + (lane & (kXlPerXcd - 1)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (__builtin_amdgcn_ballot_w64(f != tag) == 0) break;
+                if (static_cast<long long>(__builtin_amdgcn_s_memrealtime() - t0) > a.spin_ticks) {
+                    fail = true;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            if (lane == 0 && fail) s_fail = 1;
+        }
+        __syncthreads();
+    };
+
+    // Phase 1: gate/up of the slice's quads q0, q0 + 32, ...
+    const int nq = n * (rm::kBfChunk / 4);
+    const int mine = nq > rank ? (nq - rank + kXlPerXcd - 1) / kXlPerXcd : 0;
+    auto xs = reinterpret_cast<uint16_t(*)[64 * kRowPitch]>(lds);
+    auto red2 = reinterpret_cast<rm_f32x4 *>(lds + kXsBytes);
+    const int q0 = c0 * (rm::kBfChunk / 4) + rank;
+    switch ((mine + 1) / 2) {
+        case 0:
+            early();
+            mid();
+            pre();
+            break;
+        case 1:
+            gateup_spread_body<1, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
+                                                                       early, mid);
+            break;
+        case 2:
+            gateup_spread_body<2, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
+                                                                       early, mid);
+            break;
+        default:
+            gateup_spread_body<3, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
+                                                                       early, mid);
+            break;
+    }
+
+    // Meeting 2: this workgroup's stores of h are complete before it arrives.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0) {
+        unsigned now = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+        const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+        while (now < kXlPerXcd) {
+            __builtin_amdgcn_s_sleep(1);
+            now = __hip_atomic_fetch_add(ctr, a.zero, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (static_cast<long long>(__builtin_amdgcn_s_memrealtime() - t0) > a.spin_ticks) {
+                s_fail = 1;
+                break;
+            }
+        }
+    }
+    __syncthreads();
+    asm volatile("buffer_inv sc0" ::: "memory");  // this compute unit's L1 holds no line of H
+    if (n == 0) return;
+
+    // Phase 2: the slice's chunks for column tile `rank`, the rows already in registers; H from the L2.
+    DnChunk<NT> cb[CPW];
+#pragma unroll
+    for (int k = 0; k < CPW; ++k) {
+        const int ce = chunk_of(k);
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+            cb[k].a[tt] = load16(g.H + (static_cast<size_t>(ce) * g.tpad + tt * 16 + nn) * rm::kBfChunk + grp * 8);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cb[k].w[j] = wdn[k][j];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    rm_f32x4 acc[NT][4];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[tt][q] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < CPW; ++k)
+        if (wave + k * kGuWaves < n) dn_mma<NT>(cb[k], acc);
+    auto red = reinterpret_cast<rm_f32x4(*)[NT][4][64]>(lds);  // [wave][token tile][column call][lane]
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) red[wave][tt][q][lane] = acc[tt][q];
+    __syncthreads();
+    // Wave w sums token tile w / 2, column calls 2 (w % 2) and 2 (w % 2) + 1, over the 8 waves in wave order and
+    // stores that part of the slice's partial.
+    const int tt = wave >> 1;
+    const int qc = 2 * (wave & 1);
+    rm_f32x4 v0 = red[0][tt][qc][lane], v1 = red[0][tt][qc + 1][lane];
+#pragma unroll
+    for (int w = 1; w < kGuWaves; ++w) {
+        v0 += red[w][tt][qc][lane];
+        v1 += red[w][tt][qc + 1][lane];
+    }
+    if (!colok) return;
+    const float nan = __builtin_nanf("");
+    const bool bad = s_fail != 0;
+    float *P = a.part + static_cast<size_t>(x) * g.T * g.d + colw + qc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int t = tt * 16 + grp * 4 + i;  // lane L, register i: token 4 (L / 16) + i of the tile
+        if (t < g.T) {
+            float2 o;
+            o.x = bad ? nan : v0[i];  // physical column 4 nn + qc
+            o.y = bad ? nan : v1[i];
+            *reinterpret_cast<float2 *>(P + static_cast<size_t>(t) * g.d) = o;
+        }
     }
 }
 
@@ -1349,6 +1668,56 @@ hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *i
     else
         return hipErrorInvalidValue;
 #undef RM_DF
+    return e != hipSuccess ? e : hipGetLastError();
+}
+
+hipError_t launch_layer_xcd(const Plan &p, const void *w_gate, const void *w_up, const void *w_down,
+                            const int32_t *idx, const int32_t *count, const float *xin, const float *norm_g,
+                            const float *h_anchor, void *ws, hipStream_t st) {
+    char *base = static_cast<char *>(ws);
+    XlArgs a{};
+    GuArgs &g = a.g;
+    g.wg = static_cast<const uint16_t *>(w_gate);
+    g.wu = static_cast<const uint16_t *>(w_up);
+    g.xn = reinterpret_cast<const uint16_t *>(base + p.off_xn8);
+    g.idx = idx;
+    g.count = count;
+    g.ssq = norm_g != nullptr ? reinterpret_cast<const float *>(base + p.off_ssq8) : nullptr;
+    g.eps = p.eps;
+    g.max_count = p.max_count;
+    g.d_ff = p.d_ff;
+    g.d = p.d;
+    g.T = p.T;
+    g.tpad = p.tpad;
+    g.kcap = p.kcap;
+    g.B = 1;
+    g.act = p.act;
+    g.H = reinterpret_cast<uint16_t *>(base + p.off_h);
+    g.h_anchor = h_anchor;
+    g.h_out = nullptr;
+    a.x = xin;
+    a.norm_g = norm_g;
+    a.xn8 = reinterpret_cast<uint16_t *>(base + p.off_xn8);
+    a.ssq8 = reinterpret_cast<float *>(base + p.off_ssq8);
+    a.wd = static_cast<const uint16_t *>(w_down);
+    a.part = reinterpret_cast<float *>(base + p.off_part);
+    a.flags = reinterpret_cast<unsigned long long *>(base + p.off_sync);
+    a.ctr = reinterpret_cast<unsigned *>(base + p.off_sync + kXcdFlagBytes);
+    a.zero = 0u;
+    a.cps = p.slice_units;
+    a.spin_ticks = kXcdSpinTicks;
+    // The plan's conditions: B = 1, T <= 64, d = 2048 (32 column tiles, one per workgroup of an XCD), slices of
+    // 9 .. 24 chunks, 256 workgroups.
+    if (p.B != 1 || p.T > kBfTokBlock || p.d != 8 * kChunkCols || p.slice_units < 1 ||
+        p.slice_units > 3 * kGuWaves || p.slices > 8)
+        return hipErrorInvalidValue;
+    const dim3 grid(8 * kXlPerXcd), block(kGuThreads);
+    hipError_t e;
+    switch ((p.slice_units + kGuWaves - 1) / kGuWaves) {
+        case 1: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<8, 1>, grid, block, st, a); break;
+        case 2: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<8, 2>, grid, block, st, a); break;
+        default: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<8, 3>, grid, block, st, a); break;
+    }
     return e != hipSuccess ? e : hipGetLastError();
 }
 

@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 
 #include "rm_select.h"
@@ -29,7 +30,7 @@ struct ProfileSlot {
     hipEvent_t begin = nullptr;
     hipEvent_t end = nullptr;
 };
-thread_local ProfileSlot g_profile[4];
+thread_local ProfileSlot g_profile[5];
 
 rm_status fail(rm_status st, const char *fmt, ...) {
     va_list ap;
@@ -209,9 +210,16 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
                      const int32_t *idx, const int32_t *count, size_t list_stride, size_t count_stride, void *ws,
                      hipStream_t st, const AnchorTerms &at = AnchorTerms{}, const uint8_t *mask = nullptr,
                      int n_masks = 0) {
-    hipError_t e = mask ? rm::launch_compact_prologue(p, mask, n_masks, const_cast<int32_t *>(idx),
-                                                      const_cast<int32_t *>(count), x, w[0].norm_g, ws, st)
-                        : rm::launch_prologue(p, x, w[0].norm_g, ws, st);
+    // The one-launch layer form reads the float32 input itself: only a mask's compaction precedes it.
+    hipError_t e = hipSuccess;
+    if (p.xcd_layer) {
+        if (mask) e = rm::launch_mask_compact(mask, n_masks, p.d_ff, const_cast<int32_t *>(idx),
+                                              const_cast<int32_t *>(count), st);
+    } else {
+        e = mask ? rm::launch_compact_prologue(p, mask, n_masks, const_cast<int32_t *>(idx),
+                                               const_cast<int32_t *>(count), x, w[0].norm_g, ws, st)
+                 : rm::launch_prologue(p, x, w[0].norm_g, ws, st);
+    }
     if (e != hipSuccess) return hip_fail(e, "prologue launch");
     const bool bf = p.wdtype == RM_BF16;
     const size_t y_stride = static_cast<size_t>(p.B) * p.T * p.d;
@@ -224,9 +232,13 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
         const int32_t *cl = count + l * count_stride;
         const bool norm = w[l].norm_g != nullptr;
         const float *ha = at.ha_in ? at.ha_in + l * at.h_stride : nullptr;
-        e = bf ? rm::launch_gateup_bf16(p, w[l].w_gate, w[l].w_up, il, cl, norm, ha, nullptr, ws, st)
-               : rm::launch_gateup_f32(p, w[l].w_gate, w[l].w_up, il, cl, norm, ha, nullptr, ws, st);
-        if (e != hipSuccess) return hip_fail(e, "gate/up launch");
+        if (p.xcd_layer)  // gate/up and down in one launch from the float32 input; partials to the epilogue
+            e = rm::launch_layer_xcd(p, w[l].w_gate, w[l].w_up, w[l].w_down, il, cl, l == 0 ? x : y, w[l].norm_g,
+                                     ha, ws, st);
+        else
+            e = bf ? rm::launch_gateup_bf16(p, w[l].w_gate, w[l].w_up, il, cl, norm, ha, nullptr, ws, st)
+                   : rm::launch_gateup_f32(p, w[l].w_gate, w[l].w_up, il, cl, norm, ha, nullptr, ws, st);
+        if (e != hipSuccess) return hip_fail(e, p.xcd_layer ? "layer launch" : "gate/up launch");
         if (at.ha_out != nullptr) {  // the anchor keeps h^M of the group's lists (same input, same norm)
             const rm::Plan &q = *at.cap_plan;
             const int32_t *ci = at.cap_idx + static_cast<size_t>(l) * p.B * p.d_ff;
@@ -236,7 +248,7 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
                    : rm::launch_gateup_f32(q, w[l].w_gate, w[l].w_up, ci, cc, norm, nullptr, ho, ws, st);
             if (e != hipSuccess) return hip_fail(e, "anchor h capture launch");
         }
-        const bool next = l + 1 < L;
+        const bool next = l + 1 < L && !p.xcd_layer;  // the one-launch form needs no xn for the next layer
         const float *g_next = next ? w[l + 1].norm_g : nullptr;
         const float *xin = l == 0 ? x : y;
         const float *ya_in = at.ya_in ? at.ya_in + l * y_stride : nullptr;
@@ -247,12 +259,32 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
             if (e != hipSuccess) return hip_fail(e, "down launch");
             continue;
         }
-        e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, ws, st) : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
-        if (e != hipSuccess) return hip_fail(e, "down launch");
+        if (!p.xcd_layer) {
+            e = bf ? rm::launch_down_bf16(p, w[l].w_down, il, ws, st)
+                   : rm::launch_down_f32(p, w[l].w_down, il, cl, ws, st);
+            if (e != hipSuccess) return hip_fail(e, "down launch");
+        }
         e = rm::launch_epilogue(p, cl, xin, y, g_next, next, ya_in, ya_out, w[l].out_gate, ws, st);
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }
     return RM_OK;
+}
+
+// Whether the current device has the 256 compute units (8 XCDs of 32) that the one-launch layer form needs
+// resident at once; asked once per device.
+bool device_has_256_cus() {
+    static std::atomic<int> known[64];  // 0 = not asked, 1 = no, 2 = yes
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return false;
+    if (dev >= 64) return false;
+    int v = known[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        int cus = 0;
+        const bool ok = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess;
+        v = ok && cus == 256 ? 2 : 1;
+        known[dev].store(v, std::memory_order_relaxed);
+    }
+    return v == 2;
 }
 
 }  // namespace
@@ -271,6 +303,8 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.act = s->act;
     const int kmax = max_count > 0 ? max_count : 1;
     size_t xn_elem, h_elem;
+    bool xcd_shape = false;
+    int part_slices = 0;  // partial slices the workspace holds (at least q.slices)
     // Aim for one down-projection workgroup per compute unit (256 CUs): a grid just past a multiple of the unit
     // count leaves the units with one more workgroup setting the time (d = 2048, 4916 neurons: 8 slices of 20 chunks,
     // 256 workgroups, instead of 10 slices of 16, 320: down 10.0 -> 8.1 us), and fewer K-slices mean fewer
@@ -327,6 +361,20 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
                                             std::max(1, ceil_div(ceil_div(nchunks, s_target), kBfWaves)));
         q.slice_units = cps;
         q.slices = ceil_div(nchunks, cps);
+        // One sample's long list at d = 2048 (the spread plan's range): gate/up and down in one launch, the
+        // list's chunks cut into 8 slices, one per XCD (at most 3 chunks per wave of the down phase).  The
+        // workspace holds the counters and the partials of either plan, so its size does not depend on the
+        // device; the launch form needs 256 compute units (all 256 workgroups resident, 32 per XCD).
+        const int cps8 = ceil_div(nchunks, 8);
+        xcd_shape = RM_LAYER_XCD && spread && s->d == 8 * 256 && cps8 <= 3 * 8;
+        if (xcd_shape) {
+            part_slices = std::max(q.slices, ceil_div(nchunks, cps8));
+            if (device_has_256_cus()) {
+                q.xcd_layer = true;
+                q.slice_units = cps8;
+                q.slices = ceil_div(nchunks, cps8);
+            }
+        }
         // Short lists (up to kDfMaxChunks chunks): one workgroup per (column tile, token tile) can sum the whole
         // list.  One sample: 16-token tiles.  Several samples: one 64-token tile, so each sample's listed rows of
         // a column tile are read once (16 samples of 51 tokens, d = 1024: down 17.8 -> 14.8 us against two 32-token tiles).
@@ -367,13 +415,20 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.off_h = off;
     off = align_up(off + static_cast<size_t>(B) * q.tpad * q.kcap * h_elem, 256);
     q.off_part = off;
-    off = align_up(off + static_cast<size_t>(B) * q.slices * static_cast<size_t>(T) * s->d * 4, 256);
+    off = align_up(off + static_cast<size_t>(B) * std::max(q.slices, part_slices) * static_cast<size_t>(T) * s->d * 4,
+                   256);
     q.off_ssq = off;
     off = align_up(off + static_cast<size_t>(B) * T * ssq_stride(s->d) * sizeof(float), 256);
     q.off_ident = off;
     off = align_up(off + static_cast<size_t>(B) * s->d_ff * sizeof(int32_t), 256);
     q.off_ident_count = off;
     off = align_up(off + static_cast<size_t>(B) * sizeof(int32_t), 256);
+    q.off_xn8 = off;
+    if (xcd_shape) off = align_up(off + static_cast<size_t>(8) * T * s->d * 2, 256);
+    q.off_ssq8 = off;
+    if (xcd_shape) off = align_up(off + static_cast<size_t>(8) * T * ssq_stride(s->d) * sizeof(float), 256);
+    q.off_sync = off;
+    if (xcd_shape) off = align_up(off + kXcdFlagBytes + kXcdCtrBytes, 256);
     q.total = off;
     *p = q;
     return RM_OK;
@@ -570,11 +625,13 @@ RM_EXPORT rm_status rm_anchor_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
     rm::Plan p, q;
     rm_status st = check_call(s, B, T, x, y, nullptr, nullptr, false, 0, ws, ws_bytes, &p);  // dense layers
     if (st != RM_OK) return st;
-    st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &q);  // the group's lists
+    // The group's lists: their plan sizes the capture launch, which uses only the dense layout's regions (its
+    // own plan may ask for more, e.g. the one-launch layer form's buffers), so the dense size is what counts.
+    st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, SIZE_MAX, &q);
     if (st != RM_OK) return st;
     st = check_anchor_buffers(s, w, L, B, T, x, y, max_count, y_anchor, h_anchor, ws, ws_bytes);
     if (st != RM_OK) return st;
-    st = check_lists(s, L, B, T, y, idx, count, ws, std::max(p.total, q.total));
+    st = check_lists(s, L, B, T, y, idx, count, ws, p.total);
     if (st != RM_OK) return st;
     // The capture reads the dense layers' FFN input and sums of squares from the dense workspace layout; it
     // writes nothing else there.
@@ -847,10 +904,22 @@ RM_EXPORT rm_status rm_group_masks(const float *h, int32_t S, int32_t L, int32_t
 }
 
 RM_EXPORT rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end) {
-    if (kernel < RM_KERNEL_GATEUP || kernel > RM_KERNEL_GROUP_SELECT)
+    if (kernel < RM_KERNEL_GATEUP || kernel > RM_KERNEL_LAYER)
         return fail(RM_ERR_INVALID_ARG, "unknown kernel id %d", kernel);
     g_profile[kernel].begin = static_cast<hipEvent_t>(ev_begin);
     g_profile[kernel].end = static_cast<hipEvent_t>(ev_end);
+    return ok();
+}
+
+RM_EXPORT rm_status rm_layer_kernels(const rm_ffn_shape *s, int32_t B, int32_t T, int32_t max_count,
+                                     uint32_t *kernels) {
+    if (!kernels) return fail(RM_ERR_INVALID_ARG, "kernels is NULL");
+    size_t bytes = 0;
+    const rm_status st = rm_workspace_size(s, B, T, max_count, &bytes);  // the same checks
+    if (st != RM_OK) return st;
+    rm::Plan p;
+    rm::make_plan(s, B, T, max_count, &p);
+    *kernels = p.xcd_layer ? (1u << RM_KERNEL_LAYER) : ((1u << RM_KERNEL_GATEUP) | (1u << RM_KERNEL_DOWN));
     return ok();
 }
 

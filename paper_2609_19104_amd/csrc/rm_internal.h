@@ -22,6 +22,18 @@ namespace rm {
 #define RM_GATEUP_SPREAD 1
 #endif
 
+// One launch for the gate/up and down projections of one sample's long list at d = 2048, its workgroups meeting
+// per XCD between the two (set to 0 at build time to compare with the separate launches).
+#ifndef RM_LAYER_XCD
+#define RM_LAYER_XCD 1
+#endif
+// The meetings of that launch: one uint64 flag per workgroup (8 XCDs x 32), then one counter per XCD, each on
+// its own 256-byte line.
+constexpr int kXcdFlagBytes = 8 * 32 * 8;
+constexpr int kXcdCtrBytes = 8 * 256;
+// How long a workgroup of that launch waits for the rest of its XCD before it gives up (100 MHz clock ticks).
+constexpr long long kXcdSpinTicks = 20000000;  // 200 ms
+
 // bf16 path: 16x16x32 bf16 matrix-core tiles.
 constexpr int kBfTokBlock = 64;     // tokens per accumulator block (4 tiles of 16)
 constexpr int kBfNeurPerBlk = 8;    // neurons per gate/up workgroup (8 gate rows + 8 up rows = one 16-row tile)
@@ -71,11 +83,19 @@ struct Plan {
     int df_cw = 4;       // fused down: columns per lane (2 for one sample, 4 with several)
     int df_ncol = 0;     // fused down: column tiles of 16 df_cw columns
     int ntt = 0;         // fused down: token tiles of 16 df_nt tokens
+    // bf16, one sample, d = 2048, the spread plan's list lengths, 256 compute units: gate/up and down in one
+    // launch (layer_xcd_kernel) that reads the float32 input itself, slices = the 8 XCDs' slices of slice_units
+    // chunks; no prologue launch, the epilogue follows.
+    bool xcd_layer = false;
     // Workspace: xn [B][T][d] (bf16 or f32); H (bf16: [B][kcap / 32][tpad][32], chunk-major; f32:
     // [B][tpad][kcap]); partials f32 [B][slices][T][d]; ssq f32 [B][T][ssq_stride(d)]
     // (per-token sums of squares of the FFN input by 32-column block, for the RMSNorm factor); and, for the dense
     // reference, the lists 0 .. d_ff-1 int32 [B][d_ff] and their counts int32 [B].
-    size_t off_xn = 0, off_h = 0, off_part = 0, off_ssq = 0, off_ident = 0, off_ident_count = 0, total = 0;
+    // With xcd_layer, also the XCDs' own copies of the FFN input, bf16 [8][T][d], and of its partial sums of
+    // squares, f32 [8][T][ssq_stride(d)], and the meetings' flags and counters (kXcdFlagBytes + kXcdCtrBytes; no
+    // initialization needed).
+    size_t off_xn = 0, off_h = 0, off_part = 0, off_ssq = 0, off_ident = 0, off_ident_count = 0, off_xn8 = 0,
+           off_ssq8 = 0, off_sync = 0, total = 0;
 };
 
 rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p);
@@ -162,6 +182,12 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
 hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
                              const float *x, float *y, const float *g_next, bool emit_xn, const float *ya_in,
                              float *ya_out, const float *out_gate, void *ws, hipStream_t st);
+// With p.xcd_layer: the gate/up and the down projection (per-slice partials, as launch_down_bf16 writes them)
+// in one launch that reads the float32 FFN input xin [T][d] and the norm gain (null: no norm) itself, so no
+// prologue precedes it; the epilogue follows (it need not emit the next layer's xn).
+hipError_t launch_layer_xcd(const Plan &p, const void *w_gate, const void *w_up, const void *w_down,
+                            const int32_t *idx, const int32_t *count, const float *xin, const float *norm_g,
+                            const float *h_anchor, void *ws, hipStream_t st);
 hipError_t launch_down_f32(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count, void *ws,
                            hipStream_t st);
 

@@ -141,6 +141,18 @@ def test_profile_hook_rejects_unknown_kernel(lib):
     assert lib.rm_profile_kernel_events(rm.RM_KERNEL_GATEUP, None, None) == rm.RM_OK
 
 
+def test_layer_kernels_query(lib):
+    both = (1 << rm.RM_KERNEL_GATEUP) | (1 << rm.RM_KERNEL_DOWN)
+    assert rm.rm_layer_kernels(1024, 4096, rm.RM_BF16, 1, 51, 1229) == both
+    assert rm.rm_layer_kernels(256, 1024, rm.RM_F32, 1, 8, 256) == both
+    # One sample's long list at d = 2048: one launch on a 256-unit device, else the two.
+    assert rm.rm_layer_kernels(2048, 16384, rm.RM_BF16, 1, 51, 4916) in (both, 1 << rm.RM_KERNEL_LAYER)
+    assert rm.rm_layer_kernels(2048, 16384, rm.RM_BF16, 2, 51, 4916) == both
+    with pytest.raises(rm.RmError):
+        rm.rm_layer_kernels(1000, 4096, rm.RM_BF16, 1, 51, 10)
+    assert lib.rm_layer_kernels(None, 1, 51, 10, None) == rm.RM_ERR_INVALID_ARG
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     x = torch.zeros(1, 4, 32)
@@ -150,9 +162,10 @@ def test_binding_refuses_cpu_tensors():
 
 
 def test_profile_hook_accepts_every_kernel_id(lib):
-    for k in (rm.RM_KERNEL_GATEUP, rm.RM_KERNEL_DOWN, rm.RM_KERNEL_SCORES, rm.RM_KERNEL_GROUP_SELECT):
+    for k in (rm.RM_KERNEL_GATEUP, rm.RM_KERNEL_DOWN, rm.RM_KERNEL_SCORES, rm.RM_KERNEL_GROUP_SELECT,
+              rm.RM_KERNEL_LAYER):
         assert lib.rm_profile_kernel_events(k, None, None) == rm.RM_OK
-    assert lib.rm_profile_kernel_events(4, None, None) == rm.RM_ERR_INVALID_ARG
+    assert lib.rm_profile_kernel_events(5, None, None) == rm.RM_ERR_INVALID_ARG
     assert lib.rm_profile_kernel_events(-1, None, None) == rm.RM_ERR_INVALID_ARG
 
 

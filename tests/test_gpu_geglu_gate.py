@@ -42,6 +42,7 @@ CASES = [
     (256, 1000, 1, 2, 51, 333, "bf16", "silu"),
     (1024, 4096, 3, 1, 51, 1229, "bf16", "gelu_tanh"),  # one sample: fused down, xn for the next layer
     (160, 512, 2, 3, 17, 200, "bf16", "gelu_tanh"),     # stack with the epilogue emitting xn
+    (2048, 8192, 2, 1, 51, 3000, "bf16", "gelu_tanh"),  # one sample's long list: gate/up and down in one launch
     (128, 300, 2, 2, 9, 150, "f32", "gelu_tanh"),
     (64, 100, 1, 1, 3, 37, "f32", "silu"),
 ]
@@ -85,7 +86,8 @@ def test_gate_with_empty_list_is_identity(B):
     assert np.array_equal(y.cpu().numpy().view(np.uint32), x.view(np.uint32))
 
 
-@pytest.mark.parametrize("d,d_ff,L,B,T,k", [(1024, 4096, 2, 1, 51, 1229), (256, 512, 3, 2, 33, 200)])
+@pytest.mark.parametrize("d,d_ff,L,B,T,k", [(1024, 4096, 2, 1, 51, 1229), (256, 512, 3, 2, 33, 200),
+                                             (2048, 8192, 2, 1, 51, 3000)])
 def test_gated_geglu_anchor_and_delta(d, d_ff, L, B, T, k):
     layers = [wl.make_layer(105, l, d, d_ff, "bf16", norm="random") for l in range(L)]
     ga, gt = _gates(106, L, B, d), _gates(107, L, B, d)  # the anchor step's and a later step's gates

@@ -1,0 +1,121 @@
+"""GPU parity of the one-launch layer form: one sample's list of 257 .. 768 groups of 8 slots at d = 2048 runs
+the gate/up and the down projection in one launch whose workgroups meet per XCD (layer_xcd_kernel), then the
+epilogue.  Against the float64 oracle on the same seeded inputs, across that range of list lengths (the shortest,
+whose last XCD slice holds 2 chunks and leaves half of that XCD's workgroups without gate/up work, up to slices
+of 24 chunks), token counts 1 .. 64, with and without a norm, slots past the count, inside stacks (the per-XCD
+counters carried from layer to layer), repeated calls, an empty list and an Eq. 4 delta step.
+
+Bars: max-abs relative error 2e-2 (bf16 weights) on y and on the FFN part y - x; repeated and in-place calls
+bitwise equal; an empty list y == x bit for bit; a delta step at the anchor's own input the anchor bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from gpu_helpers import (TOL_BF16, compact, dev_weights, errors, run_anchor, run_delta, run_layer,  # noqa: E402
+                         run_stack)
+
+D = 2048
+
+
+def test_the_one_launch_form_runs():
+    # The calls below take the one-launch form on this device (256 compute units).
+    import paper_2609_19104_amd as rm
+    for d_ff, T, k in ((8192, 51, 2057), (16384, 17, 6144), (16384, 51, 4916), (8192, 1, 4300)):
+        assert rm.rm_layer_kernels(D, d_ff, rm.RM_BF16, 1, T, k) == 1 << rm.RM_KERNEL_LAYER
+
+
+def _oracle_layer(layer, x, mult):
+    wg, wu, wd, g = layer.f64()
+    return np.stack([oracle.masked_ffn(x[b], wg, wu, wd, mult[b], g) for b in range(x.shape[0])])
+
+
+def _check(y, y_ref, x, label):
+    ey, ed = errors(y, y_ref, x)
+    print(f"{label}: rel err y {ey:.3e} delta {ed:.3e}")
+    assert ey <= TOL_BF16 and ed <= TOL_BF16, f"{label}: rel err y {ey:.3e}, delta {ed:.3e}"
+
+
+@pytest.mark.parametrize("d_ff,T,k,spare,norm", [
+    (8192, 51, 2057, 0, "none"),     # 65 chunks: slices of 9, the last XCD's slice 2 chunks
+    (8192, 64, 3001, 0, "random"),   # 94 chunks, slices of 12, a ragged last chunk
+    (8192, 1, 4100, 200, "ones"),    # one token; slots past the count
+    (16384, 17, 6144, 0, "none"),    # 192 chunks: slices of 24 (3 per wave), the range's end
+    (16384, 51, 4916, 0, "random"),  # the count of a top-30% mask of 16384 neurons, with a norm
+])
+def test_layer_parity(d_ff, T, k, spare, norm):
+    layer = wl.make_layer(131, d_ff, D, d_ff, "bf16", norm=norm)
+    x = wl.make_x(131, (1, T, D), d_ff, T, k)
+    mask = wl.uniform_mask(wl.rng(131, 4, d_ff, T, k), d_ff, k)[None]
+    idx, cnt = compact(mask)
+    y = run_layer(dev_weights(layer), x, idx, cnt, min(d_ff, k + spare))
+    _check(y, _oracle_layer(layer, x, mask.astype(np.float64)), x, f"layer d_ff={d_ff} T={T} k={k}")
+
+
+def test_stack_repeat_and_in_place():
+    # Three layers with ragged counts: each layer's launch finds the counters where the last one left them.
+    d_ff, T, L = 8192, 51, 3
+    counts = [3000, 2600, 3500]
+    layers = [wl.make_layer(132, l, D, d_ff, "bf16", norm="random") for l in range(L)]
+    lws = [dev_weights(l) for l in layers]
+    x = wl.make_x(132, (1, T, D), 0)
+    masks = np.stack([wl.uniform_mask(wl.rng(132, 4, l), d_ff, c) for l, c in enumerate(counts)])
+    idx, cnt = compact(masks)
+    y = run_stack(lws, x, idx, cnt, max(counts))
+    y2 = run_stack(lws, x, idx, cnt, max(counts))
+    assert np.array_equal(y.view(np.uint32), y2.view(np.uint32))
+    ref = oracle.ffn_stack(x[0], [lay.f64() for lay in layers], [m.astype(np.float64) for m in masks])[None]
+    _check(y, ref, x, "stack")
+    # Layer by layer (each call with its own prologue): the same kernels, so the same bits.
+    yl = x
+    for l in range(L):
+        yl = run_layer(lws[l], yl, idx[l:l + 1].contiguous(), cnt[l:l + 1].contiguous(), max(counts))
+    assert np.array_equal(yl.view(np.uint32), y.view(np.uint32))
+    y_in = run_layer(lws[0], x, idx[:1].contiguous(), cnt[:1].contiguous(), max(counts), in_place=True)
+    y_out = run_layer(lws[0], x, idx[:1].contiguous(), cnt[:1].contiguous(), max(counts))
+    assert np.array_equal(y_in.view(np.uint32), y_out.view(np.uint32))
+
+
+def test_empty_and_clamped_counts():
+    d_ff, T = 8192, 33
+    layer = wl.make_layer(133, 0, D, d_ff, "bf16", norm="random")
+    lw = dev_weights(layer)
+    x = wl.make_x(133, (1, T, D), 0)
+    x[0, 0, :5] = -0.0
+    idx, cnt = compact(np.zeros((1, d_ff), np.uint8))
+    y = run_layer(lw, x, idx, cnt, 3000)  # the plan of a 3000-slot list, no listed neuron
+    assert np.array_equal(y.view(np.uint32), x.view(np.uint32))
+    # A count above max_count: only the first max_count listed neurons are applied.
+    mask = wl.uniform_mask(wl.rng(133, 4), d_ff, 4000)[None]
+    idx, cnt = compact(mask)
+    y = run_layer(lw, x, idx, cnt, 2500)
+    first = np.zeros(d_ff)
+    first[oracle.compact_mask(mask)[0][0, :2500]] = 1
+    _check(y, _oracle_layer(layer, x, first[None]), x, "clamped count")
+
+
+def test_delta_step():
+    # Eq. 4: the dense anchor keeps y_a and the group list's h_a (captured by the spread gate/up launch); the
+    # delta step runs the one-launch form on the same list.
+    d_ff, T, L, k = 8192, 51, 2, 3000
+    layers = [wl.make_layer(134, l, D, d_ff, "bf16", norm="random") for l in range(L)]
+    lws = [dev_weights(l) for l in layers]
+    xa = wl.make_x(134, (1, T, D), 0)
+    xt = (xa + 0.05 * np.random.default_rng(135).standard_normal(xa.shape)).astype(np.float32)
+    masks = np.stack([wl.uniform_mask(wl.rng(134, 4, l), d_ff, k - 100 * l) for l in range(L)])
+    idx, cnt = compact(masks)
+    y, ya, ha = run_anchor(lws, xa, idx, cnt, k)
+    yd = run_delta(lws, xt, idx, cnt, k, ya, ha)
+    lay = [l.f64() for l in layers]
+    _, ya_ref, ha_ref = oracle.anchor_stack(xa[0], lay)
+    ref = oracle.delta_stack(xt[0], lay, [m.astype(np.float64) for m in masks], ya_ref, ha_ref)[None]
+    _check(yd, ref, xt, "delta step")
+    y_same = run_delta(lws, xa, idx, cnt, k, ya, ha)
+    assert np.array_equal(y_same.view(np.uint32), y.cpu().numpy().view(np.uint32))

@@ -112,8 +112,10 @@ WORKLOADS = {
 
 
 STEP_TEXT = {
-    "c2": "rm_masked_ffn_layer (mask compaction + layer), replayed from HIP graphs",
-    "c4": "rm_masked_ffn_layer (mask compaction + layer), replayed from HIP graphs",
+    "c2": "rm_sparse_ffn_layer on the mask's list, compacted once at set-up (the group's cached list, shared by its "
+          "steps), replayed from HIP graphs; masked_us_per_layer: rm_masked_ffn_layer (compaction + layer) per step",
+    "c4": "rm_sparse_ffn_layer on the mask's list, compacted once at set-up (the group's cached list, shared by its "
+          "steps), replayed from HIP graphs; masked_us_per_layer: rm_masked_ffn_layer (compaction + layer) per step",
     "c3": "one 10-step sequence: rm_sparse_ffn_stack (L=18) over identity lists (the dense step), then 5 "
           "rm_masked_ffn_stack (L=18, compacting the refreshed 18 masks) alternating with 4 rm_sparse_ffn_stack "
           "(L=18), replayed from HIP graphs; "
@@ -193,10 +195,18 @@ class Setup:
         self.ws = rm.workspace(self.d, self.d_ff, rm.RM_BF16, self.B, self.T, self.k, device=device)
         self.rm = rm
         self.L, self.layer_steps = 1, 1
+        # A step is the layer on the group's cached list (compacted here, once); with lists = False it is the
+        # call that compacts the mask too.
+        self.lists = True
+        rm.rm_mask_compact(self.mask, self.idx, self.cnt)
 
     def step(self, i: int) -> None:
-        self.rm.rm_masked_ffn_layer(self.x, self.y, self.layers[i % self.rotate], self.mask, self.idx, self.cnt,
-                                    self.k, self.ws)
+        if self.lists:  # the group's cached list (compacted once at set-up): the layer alone
+            self.rm.rm_sparse_ffn_layer(self.x, self.y, self.layers[i % self.rotate], self.idx, self.cnt, self.k,
+                                        self.ws)
+        else:
+            self.rm.rm_masked_ffn_layer(self.x, self.y, self.layers[i % self.rotate], self.mask, self.idx, self.cnt,
+                                        self.k, self.ws)
 
     def compact(self) -> None:  # the step's mask compaction alone
         self.rm.rm_mask_compact(self.mask, self.idx, self.cnt)
@@ -773,6 +783,9 @@ def secondary_lines(device, steps: int, warmup: int) -> dict:
         line = {"workload": setup.spec["name"], "us_per_layer": round(ms * 1e3 / setup.layer_steps, 3),
                 "gbs_active": round(gbs, 1), "pct_of_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
                 "compaction_us": round(time_compaction(setup), 3)}
+        if isinstance(setup, Setup):
+            setup.lists = False
+            line["masked_us_per_layer"] = round(time_graph(setup, steps, warmup) * 1e3, 3)
         if isinstance(setup, StackSetup5):
             line["per_sample_gbs"] = round(setup.per_sample_bytes / (ms * 1e-3) / 1e9, 1)
             line["mfma_frac"] = round(setup.useful_flops() / (ms * 1e-3) / (BF16_PEAK_TFLOPS * 1e12), 4)
@@ -928,6 +941,11 @@ def main(argv=None) -> int:
 
     step_med, step_p10, step_p90, step_block = time_step_distribution(setup)
     compact_us = time_compaction(setup) if hasattr(setup, "compact") else None
+    masked_ms = None
+    if isinstance(setup, Setup):  # the same step with the compaction of its mask (rm_masked_ffn_layer)
+        setup.lists = False
+        masked_ms = time_graph(setup, args.steps, args.warmup)
+        setup.lists = True
 
     setup.rotate = 1
     warm_ms = time_graph(setup, args.steps, args.warmup)
@@ -963,6 +981,7 @@ def main(argv=None) -> int:
                     "how": f"40 graph replays of {step_block} consecutive step(s), each between two events and "
                            f"divided by {step_block}, queued back to back"},
         "compaction_us": None if compact_us is None else round(compact_us, 3),
+        "masked_us_per_layer": None if masked_ms is None else round(masked_ms * 1e3, 3),
         "stream_read": {"gbs": stream["gbs"], "workgroups": stream["workgroups"], "bytes": stream["bytes"],
                         "pct_of_peak": round(100.0 * stream["gbs"] / HBM_PEAK_GBS, 2),
                         "kernel": "rm_stream_read (plain streaming read, 16 B per lane, 8 loads in flight)"},

@@ -641,14 +641,13 @@ __global__ __launch_bounds__(kGuThreads, (NG == 2 || kTwoPerCU) ? 4 : 2) void ga
 struct NoPre {
     __device__ void operator()() const {}
 };
-// kLate (the one-launch layer form, whose workgroups write the input first): early() runs once the indices
-// have arrived, before the first weight loads; mid() runs behind them; the input and its norm partials are
-// loaded after mid() instead of ahead of the indices.
+// kLate (the one-launch layer form, whose workgroups write the input first): early() runs behind the index
+// loads, and the first input chunks are loaded after it instead of ahead of the indices.
 template <int NG, int NCH, int PXM = RM_SPREAD_PX, int PRE_AT = 0, bool kLate = false, typename Pre = NoPre,
-          typename Early = NoPre, typename Mid = NoPre>
+          typename Early = NoPre>
 __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G, int nquads,
                                                    uint16_t (*xs)[64 * kRowPitch], rm_f32x4 *red2, float *spans,
-                                                   Pre pre = Pre{}, Early early = Early{}, Mid mid = Mid{}) {
+                                                   Pre pre = Pre{}, Early early = Early{}) {
     constexpr int NT = 4;
     constexpr int PW0 = RM_SPREAD_WTILES / (NG > 0 ? NG : 1);  // weight chunks in flight
     constexpr int PW = PW0 < 1 ? 1 : (PW0 < NCH ? PW0 : NCH);
@@ -703,6 +702,11 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
     }
     __builtin_amdgcn_sched_barrier(0);
     early();
+    if constexpr (kLate) {
+#pragma unroll
+        for (int c = 0; c < PX; ++c) load_x(c);
+        __builtin_amdgcn_sched_barrier(0);
+    }
     // Rows 8-15 of a tile read W_up: an offset added to W_gate's address.  (Selecting between the two pointers
     // lets the compiler fetch the chosen one from the kernel arguments with a vector load, issued behind the
     // input chunks, which would hold every weight load until all of them have arrived.)
@@ -715,11 +719,6 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
     if constexpr (PRE_AT == 0) pre();
     // Behind the first weights, the partial sums of squares of tokens 0..63 (NCH spans per token); their span
     // sums go to LDS after the products, so that forming the norm factors needs no memory round trip after them.
-    if constexpr (kLate) {
-        mid();
-#pragma unroll
-        for (int c = 0; c < PX; ++c) load_x(c);
-    }
     float4 sp_lo, sp_hi;
     load_spans<NCH>(a, 0, sp_lo, sp_hi);
 
@@ -961,7 +960,9 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
 // One sample's list at d = 2048 with 257 .. 768 groups of 8 listed slots (the spread plan's range): the FFN input's
 // bf16 rounding, the gate/up and the down projection in one launch of 256 workgroups, one per compute unit, so no
 // prologue launch precedes it.  The list's 32-slot chunks are cut into 8 slices of cps chunks, slice x for the 32
-// workgroups of XCD x (workgroup i runs on XCD i mod 8, checked against the hardware's XCC_ID register).
+// workgroups i with i mod 8 = x.  The dispatcher deals a launch's workgroups to the 8 XCDs in turn, starting
+// where the previous launch stopped, so such a group shares one XCD and its L2; each workgroup checks this
+// against the hardware's XCC_ID register at meeting 1.
 //   Phase 0: the XCD's 32 workgroups write the XCD's own copy of xn = bf16(x g) (and, with a norm, its per-token
 //            partial sums of squares, in the prologue's order), one (token row, 256-column block) unit per wave.
 //   Phase 1: the spread gate/up over the slice's quads of 4 slots (dealt round-robin over the XCD's 32
@@ -972,17 +973,19 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
 // Between the phases the XCD's workgroups meet; everything a phase reads was written by compute units of the same
 // XCD, so no hand-off needs the device-wide L2 write-back that makes a hand-off between XCDs cost more than a
 // kernel boundary.  Inside one launch a plain load can be served a stale copy of a line that another compute unit
-// stores to, and an atomic does not see plain stores' lines either; a device-scope load reads the stored value.
-//   Meeting 1 (after phase 0): each workgroup stores the launch's tag in its flag (tag: the dispatch packet's id
-//            mixed with the queue's address, different for every launch, so the flags need no reset and the
-//            workspace no initialization) once its phase-0 stores are complete, and polls the XCD's 32 flags with
-//            device-scope loads, behind its first weight loads (so the wait overlaps them).  Rank 0 first resets
-//            the XCD's counter for meeting 2 with an atomic swap.
+// stores to, an atomic does not see plain stores' lines, and a plain store can stay in an L2 that a device-scope
+// load reads past; a device-scope store and a device-scope load meet.
+//   Meeting 1 (after phase 0): each workgroup stores the launch's tag in its flag with a device-scope store (tag:
+//            the dispatch packet's id mixed with the queue's address, different for every launch, so the flags
+//            need no reset and the workspace no initialization) once its phase-0 stores are complete, and polls the
+//            XCD's 32 flags with device-scope loads, before it issues any weight load (a poll issued behind them
+//            would wait for them, and its read of memory would queue behind the stream).  Rank 0 first resets the
+//            XCD's counter for meeting 2 with an atomic swap.
 //   Meeting 2 (after phase 1): an atomic add on that counter (executed past the L1, where the polls, also
 //            atomic adds, read it) until it reaches 32.
 // The xn copy and H are read with plain loads: no line of them is read in the launch before it is written.  A
-// wait gives up after spin_ticks of the 100 MHz real-time clock; then, or when a workgroup is not on the XCD its
-// number names, the workgroup writes NaN partials, so the layer's output is NaN rather than wrong.
+// wait gives up after spin_ticks of the 100 MHz real-time clock (as meeting 1 does when a group's workgroups are
+// not on one XCD); then the workgroup writes NaN partials, so the layer's output is NaN rather than wrong.
 constexpr int kXlPerXcd = 32;  // workgroups per XCD: 256 compute units / 8 XCDs
 
 struct XlArgs {
@@ -1104,12 +1107,14 @@ __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
             for (int j = 0; j < 8; ++j) wdn[k][j] = load8(a.wd + static_cast<size_t>(nr[j]) * g.d + col);
         }
     };
-    const unsigned long long tag = launch_tag();
+    // The flag this workgroup stores: the launch's tag with its low 4 bits replaced by the XCD it runs on, so that
+    // a group's flags agree only if all 32 of its workgroups share one XCD (and thus one L2).
+    const unsigned long long tag = (launch_tag() & ~0xfull) | xcc_id();
     unsigned long long *fl = a.flags + x * kXlPerXcd;
     unsigned *ctr = a.ctr + x * 64;
-    if (tid == 0) s_fail = xcc_id() != static_cast<unsigned>(x) ? 1 : 0;
-    // Phase 0 (once the indices have arrived, before the first weight loads): round x g to bf16 into this XCD's
-    // copy of xn, as the prologue does, then arrive at meeting 1.
+    if (tid == 0) s_fail = 0;
+    // Phase 0 (behind the index loads, before the input and weight loads): round x g to bf16 into this XCD's copy
+    // of xn, as the prologue does, then meeting 1.
     auto early = [&]() {
 #pragma unroll
         for (int k = 0; k < kUnits; ++k) {
@@ -1135,10 +1140,9 @@ __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
         if (tid == 0 && rank == 0) __hip_atomic_exchange(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's stores are complete
         __syncthreads();
-    };
-    // Meeting 1, behind the first weight loads: arrive, then wait until the XCD's 32 flags hold the tag.
-    auto mid = [&]() {
-        if (tid == 0) fl[rank] = tag;
+        // Meeting 1, before any weight load is in flight (a poll would wait behind them): arrive, then wait until
+        // the XCD's 32 flags hold the tag.
+        if (tid == 0) __hip_atomic_store(fl + rank, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (wave == 0) {
             bool fail = false;
             const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
@@ -1166,20 +1170,19 @@ __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
     switch ((mine + 1) / 2) {
         case 0:
             early();
-            mid();
             pre();
             break;
         case 1:
             gateup_spread_body<1, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
-                                                                       early, mid);
+                                                                       early);
             break;
         case 2:
             gateup_spread_body<2, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
-                                                                       early, mid);
+                                                                       early);
             break;
         default:
             gateup_spread_body<3, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
-                                                                       early, mid);
+                                                                       early);
             break;
     }
 

@@ -182,9 +182,9 @@ hipError_t launch_down_bf16(const Plan &p, const void *w_down, const int32_t *id
 hipError_t launch_down_fused(const Plan &p, const void *w_down, const int32_t *idx, const int32_t *count,
                              const float *x, float *y, const float *g_next, bool emit_xn, const float *ya_in,
                              float *ya_out, const float *out_gate, void *ws, hipStream_t st);
-// With p.xcd_layer: the gate/up and the down projection (per-slice partials, as launch_down_bf16 writes them)
-// in one launch that reads the float32 FFN input xin [T][d] and the norm gain (null: no norm) itself, so no
-// prologue precedes it; the epilogue follows (it need not emit the next layer's xn).
+// With p.xcd_layer: the gate/up and the down projection in one launch that reads the float32 FFN input xin
+// [T][d] and the norm gain (null: no norm) itself, so no prologue precedes it; it leaves per-slice partials, as
+// launch_down_bf16 writes them, for launch_epilogue (which need not emit the next layer's xn).
 hipError_t launch_layer_xcd(const Plan &p, const void *w_gate, const void *w_up, const void *w_down,
                             const int32_t *idx, const int32_t *count, const float *xin, const float *norm_g,
                             const float *h_anchor, void *ws, hipStream_t st);

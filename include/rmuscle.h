@@ -22,8 +22,10 @@
  *
  * Conventions shared by every call
  *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every buffer and the stream; the
- *     library allocates nothing and never synchronizes.  Its only state is a thread-local error string and the
- *     events that rm_profile_kernel_events arms for the calling thread.
+ *     library allocates nothing and never synchronizes.  Its only state is a thread-local error string, the
+ *     events that rm_profile_kernel_events arms for the calling thread, a per-device record of the compute-unit
+ *     count (asked once; it decides whether the one-launch layer form can run), and the noalloc entry point's
+ *     per-device scratch array.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the default stream).
  *   - Every argument is validated on the host before anything is enqueued; on error nothing is enqueued and
  *     the call returns a negative rm_status with a detail message in rm_last_error().

@@ -10,7 +10,8 @@ What is computed for one VLM FFN layer over a sequence of N tokens whose visual 
    input and xbar the reference execution's input of the same token.  Float64 on exact widenings of the stored
    float32 inputs, with RMS(v) = sqrt(mean(v^2)).
 2. The recomputed rows: the ceil(rho_p P) visual tokens with the largest d_p (ties to the lower token), plus all
-   rows outside the visual range (the text instruction and the robot state are recomputed every time).
+   rows outside the visual range (the rows of the text instruction and of the robot state, which the method never
+   takes from the cache).
 3. Eq. 3: y_hat_p = F(x_p) for recomputed rows and the reference output ybar_p for the others, F being the FFN
    (gate, up, activation, down; no norm inside, no residual).  Float64.
 

@@ -1,6 +1,6 @@
 """GPU test of rm_sparse_ffn_layer_noalloc, the layer entry point that allocates nothing (it takes its
-workspace from a per-device array inside the library): two calls in a row on one GPU, the second with a smaller
-input, each checked bit for bit against rm_sparse_ffn_layer with a caller workspace (the same kernels) and
+workspace from a per-device array inside the library): three calls in a row on one GPU, each with a smaller
+input than the one before (the first at d = 2048 with a list long enough for the one-launch layer form), each checked bit for bit against rm_sparse_ffn_layer with a caller workspace (the same kernels) and
 against the float64 oracle within the bf16 / float32 tolerances."""
 import numpy as np
 import pytest
@@ -19,6 +19,7 @@ from gpu_helpers import TOL_BF16, TOL_F32, dev_f32, dev_weights, errors, run_lay
 
 CALLS = [
     # d, d_ff, wdtype, T, counts per sample, max_count
+    (2048, 16384, "bf16", 51, [4916], 4916),  # one sample's long list: the one-launch layer form, its XCD copies
     (1024, 4096, "bf16", 51, [1229, 0, 700], 1229),
     (256, 1024, "bf16", 8, [100], 100),
 ]

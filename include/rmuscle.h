@@ -151,9 +151,13 @@ rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights 
                               int32_t T, const float *x, float *y, const int32_t *idx, const int32_t *count,
                               int32_t max_count, void *ws, size_t ws_bytes, void *stream);
 
-/* rm_mask_compact followed by rm_sparse_ffn_layer, with the compaction run in the same launch as the layer's
- * first kernel (the two are independent), for a step that takes a freshly retrieved mask (section 4.1: the
- * reference's mask is compacted into its index list; section 5: one mask per layer and group).
+/* rm_mask_compact followed by rm_sparse_ffn_layer, for a step that takes a freshly retrieved mask (section 4.1:
+ * the reference's mask is compacted into its index list; section 5: one mask per layer and group).  The
+ * compaction runs in the launch of the layer's first kernel (the two are independent), or ahead of the
+ * one-launch layer kernel at d = 2048.  The result is rm_sparse_ffn_layer's on the written lists bit for bit,
+ * except for one sample at d = 1024, where rm_sparse_ffn_layer runs the one-launch layer kernel and this call
+ * the prologue (with the compaction), gate/up and fused down kernels: there the two agree up to the order of
+ * the float32 sums.
  *   mask:  uint8 [B][d_ff], nonzero = active.
  *   idx, count: out, int32 [B][d_ff] and [B], written exactly as rm_mask_compact writes them, so that the
  *          group's later steps can call rm_sparse_ffn_layer with them.
@@ -165,9 +169,10 @@ rm_status rm_masked_ffn_layer(const rm_ffn_shape *s, const rm_ffn_layer_weights 
                               const float *x, float *y, const uint8_t *mask, int32_t *idx, int32_t *count,
                               int32_t max_count, void *ws, size_t ws_bytes, void *stream);
 
-/* rm_mask_compact of L * B masks followed by rm_sparse_ffn_stack, the compaction in the launch of the stack's
- * first kernel.  mask: uint8 [L][B][d_ff]; idx int32 [L][B][d_ff] and count int32 [L][B] out.  Otherwise as
- * rm_masked_ffn_layer and rm_sparse_ffn_stack. */
+/* rm_mask_compact of L * B masks followed by rm_sparse_ffn_stack (bit for bit), the compaction in the launch
+ * of the stack's first kernel (ahead of the one-launch layer kernel at d = 2048).  mask: uint8 [L][B][d_ff];
+ * idx int32 [L][B][d_ff] and count int32 [L][B] out.  Otherwise as rm_masked_ffn_layer and
+ * rm_sparse_ffn_stack. */
 rm_status rm_masked_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer_weights *w, int32_t L, int32_t B,
                               int32_t T, const float *x, float *y, const uint8_t *mask, int32_t *idx,
                               int32_t *count, int32_t max_count, void *ws, size_t ws_bytes, void *stream);
@@ -319,13 +324,14 @@ typedef enum rm_kernel_id {
     RM_KERNEL_SCORES = 2,      /* Eq. 1 scores of rm_group_masks                               */
     RM_KERNEL_GROUP_SELECT = 3, /* top-K selection, union and rerank of rm_group_masks         */
     RM_KERNEL_LAYER = 4         /* gate/up and down of one layer in one launch (one sample's    */
-                                /* long list at d = 2048: the workgroups of each XCD meet      */
-                                /* between the two projections)                                */
+                                /* long list at d = 2048, or a single layer's given list at    */
+                                /* d = 1024: the workgroups of each XCD meet between the two   */
+                                /* projections)                                                */
 } rm_kernel_id;
 rm_status rm_profile_kernel_events(int32_t kernel, void *ev_begin, void *ev_end);
 
-/* Measurement: which of the hooked kernels a single-layer call (rm_sparse_ffn_layer, rm_masked_ffn_layer) of
- * this shape launches on the current device: bit k of *kernels (a host pointer) is set for rm_kernel_id k
+/* Measurement: which of the hooked kernels a single-layer call on given lists (rm_sparse_ffn_layer) of this
+ * shape launches on the current device: bit k of *kernels (a host pointer) is set for rm_kernel_id k
  * (RM_KERNEL_GATEUP and RM_KERNEL_DOWN, or RM_KERNEL_LAYER alone when the gate/up and down projections run in
  * one launch).  Host only; enqueues nothing.  Errors: those of rm_workspace_size. */
 rm_status rm_layer_kernels(const rm_ffn_shape *s, int32_t B, int32_t T, int32_t max_count, uint32_t *kernels);

@@ -780,7 +780,8 @@ __global__ __launch_bounds__(kGuThreads) void gateup_spread_kernel(GuArgs a) {
     const int G = gridDim.x;
     const int q = blockIdx.x;
     const int nq = a.kcap / 4;
-    const int mine = (nq - q + G - 1) / G;  // quads of this workgroup, >= 1
+    const int mine = (nq - q + G - 1) / G;  // quads of this workgroup (none when the list has fewer quads than G)
+    if (mine < 1) return;
     if ((mine + 1) / 2 == NG)
         gateup_spread_body<NG, NCH>(a, q, G, mine, xs, red2, spans);
     else if constexpr (NG > 1)
@@ -1029,12 +1030,13 @@ __device__ __forceinline__ unsigned long long launch_tag() {
 #ifndef RM_XCD_PRE_AT
 #define RM_XCD_PRE_AT 7
 #endif
-template <int NCH, int CPW>
+// CW: columns per lane in phase 2 (4 at d = 2048, 2 at d = 1024): column tiles of 16 CW columns, 32 per XCD.
+template <int NCH, int CPW, int CW>
 __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
     constexpr int NT = 4;
     constexpr int kXsBytes = 2 * 64 * kRowPitch * 2;            // phase 1: the staged input chunks
     constexpr int kRed2Bytes = kGuWaves * NT * 64 * 16;          // phase 1: the third tile's wave partials
-    constexpr int kRedBytes = kGuWaves * NT * 4 * 64 * 16;       // phase 2: the 8 waves' 64 x 64 tiles
+    constexpr int kRedBytes = kGuWaves * NT * 4 * 64 * 16;       // phase 2: the 8 waves' 64-token x 16 CW tiles (CW <= 4)
     static_assert(kXsBytes + kRed2Bytes <= kRedBytes, "phase 1's buffers fit phase 2's");
     constexpr int kSlots = CPW * kGuWaves * rm::kBfChunk;        // indices of a slice
     constexpr int kIdxPer = (kSlots + kGuThreads - 1) / kGuThreads;
@@ -1069,10 +1071,10 @@ __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
     }
 
     const int grp = lane >> 4;  // phase 2: slots 8 grp .. 8 grp + 7 of a chunk
-    const int nn = lane & 15;   // phase 2: token in tile, and physical columns 4 nn + q
-    const int colw = rank * rm::kBfColTile + nn * 4;
+    const int nn = lane & 15;   // phase 2: token in tile, and physical columns CW nn + q
+    const int colw = rank * 16 * CW + nn * CW;
     const bool colok = colw < g.d;
-    const int col = min(colw, g.d - 4);  // columns past d re-read column d - 4; those outputs are not stored
+    const int col = min(colw, g.d - CW);  // columns past d re-read the last ones; those outputs are not stored
     // Phase 2's chunk k of this wave: slice chunk wave + 8 k (clamped to the slice; the products of a chunk past
     // it are skipped), counted from a start that differs by column tile, so that the XCD's 32 workgroups do not
     // all read the same chunk of H from the L2 at the same time.
@@ -1104,7 +1106,13 @@ __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
             const int4 i1 = *reinterpret_cast<const int4 *>(sidx + kb + 4);
             const int nr[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
 #pragma unroll
-            for (int j = 0; j < 8; ++j) wdn[k][j] = load8(a.wd + static_cast<size_t>(nr[j]) * g.d + col);
+            for (int j = 0; j < 8; ++j) {
+                const uint16_t *src = a.wd + static_cast<size_t>(nr[j]) * g.d + col;
+                if constexpr (CW == 4)
+                    wdn[k][j] = load8(src);
+                else  // two columns: the row's 4 bytes in the low dword, which is all dn_mma<NT, 2> reads
+                    wdn[k][j] = uint2{*reinterpret_cast<const uint32_t *>(src), 0u};
+            }
         }
     };
     // The flag this workgroup stores: the launch's tag with its low 4 bits replaced by the XCD it runs on, so that
@@ -1224,35 +1232,41 @@ __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
         for (int q = 0; q < 4; ++q) acc[tt][q] = rm_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int k = 0; k < CPW; ++k)
-        if (wave + k * kGuWaves < n) dn_mma<NT>(cb[k], acc);
-    auto red = reinterpret_cast<rm_f32x4(*)[NT][4][64]>(lds);  // [wave][token tile][column call][lane]
+        if (wave + k * kGuWaves < n) dn_mma<NT, CW>(cb[k], acc);
+    auto red = reinterpret_cast<rm_f32x4(*)[NT][CW][64]>(lds);  // [wave][token tile][column call][lane]
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) red[wave][tt][q][lane] = acc[tt][q];
+        for (int q = 0; q < CW; ++q) red[wave][tt][q][lane] = acc[tt][q];
     __syncthreads();
-    // Wave w sums token tile w / 2, column calls 2 (w % 2) and 2 (w % 2) + 1, over the 8 waves in wave order and
-    // stores that part of the slice's partial.
+    // Wave w sums token tile w / 2 and column calls qc .. qc + CW / 2 - 1 (qc = (w % 2) CW / 2) over the 8 waves in
+    // wave order and stores that part of the slice's partial.
+    constexpr int QW = CW / 2;  // column calls per wave
     const int tt = wave >> 1;
-    const int qc = 2 * (wave & 1);
-    rm_f32x4 v0 = red[0][tt][qc][lane], v1 = red[0][tt][qc + 1][lane];
+    const int qc = (wave & 1) * QW;
+    rm_f32x4 v[QW];
 #pragma unroll
-    for (int w = 1; w < kGuWaves; ++w) {
-        v0 += red[w][tt][qc][lane];
-        v1 += red[w][tt][qc + 1][lane];
+    for (int j = 0; j < QW; ++j) {
+        v[j] = red[0][tt][qc + j][lane];
+#pragma unroll
+        for (int w = 1; w < kGuWaves; ++w) v[j] += red[w][tt][qc + j][lane];
     }
     if (!colok) return;
     const float nan = __builtin_nanf("");
     const bool bad = s_fail != 0;
-    float *P = a.part + static_cast<size_t>(x) * g.T * g.d + colw + qc;
+    float *P = a.part + static_cast<size_t>(x) * g.T * g.d + colw + qc;  // physical columns CW nn + qc + j
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int t = tt * 16 + grp * 4 + i;  // lane L, register i: token 4 (L / 16) + i of the tile
         if (t < g.T) {
-            float2 o;
-            o.x = bad ? nan : v0[i];  // physical column 4 nn + qc
-            o.y = bad ? nan : v1[i];
-            *reinterpret_cast<float2 *>(P + static_cast<size_t>(t) * g.d) = o;
+            if constexpr (QW == 2) {
+                float2 o;
+                o.x = bad ? nan : v[0][i];
+                o.y = bad ? nan : v[1][i];
+                *reinterpret_cast<float2 *>(P + static_cast<size_t>(t) * g.d) = o;
+            } else {
+                P[static_cast<size_t>(t) * g.d] = bad ? nan : v[0][i];
+            }
         }
     }
 }
@@ -1596,7 +1610,9 @@ static hipError_t launch_gateup_args(const Plan &p, const GuArgs &a, hipStream_t
         case 4: e = launch_timed(RM_KERNEL_GATEUP, gateup_spread_kernel<NG, 4>, grid, block, st, a); break; \
         default: e = launch_timed(RM_KERNEL_GATEUP, gateup_spread_kernel<NG, 8>, grid, block, st, a); break; \
     }
-        if (p.gate_spread == 2)  // the plan's range: 2 or 3 tiles
+        if (p.gate_spread == 1)  // the plan's range: 1 to 3 tiles
+            RM_SPREAD(1)
+        else if (p.gate_spread == 2)
             RM_SPREAD(2)
         else
             RM_SPREAD(3)
@@ -1709,18 +1725,26 @@ hipError_t launch_layer_xcd(const Plan &p, const void *w_gate, const void *w_up,
     a.zero = 0u;
     a.cps = p.slice_units;
     a.spin_ticks = kXcdSpinTicks;
-    // The plan's conditions: B = 1, T <= 64, d = 2048 (32 column tiles, one per workgroup of an XCD), slices of
-    // 9 .. 24 chunks, 256 workgroups.
-    if (p.B != 1 || p.T > kBfTokBlock || p.d != 8 * kChunkCols || p.slice_units < 1 ||
+    // The plan's conditions: B = 1, T <= 64, d = 2048 or 1024 (32 column tiles of 64 or 32 columns, one per
+    // workgroup of an XCD), slices of at most 24 chunks, 256 workgroups.
+    if (p.B != 1 || p.T > kBfTokBlock || (p.d != 8 * kChunkCols && p.d != 4 * kChunkCols) || p.slice_units < 1 ||
         p.slice_units > 3 * kGuWaves || p.slices > 8)
         return hipErrorInvalidValue;
     const dim3 grid(8 * kXlPerXcd), block(kGuThreads);
+    const int cpw = (p.slice_units + kGuWaves - 1) / kGuWaves;
     hipError_t e;
-    switch ((p.slice_units + kGuWaves - 1) / kGuWaves) {
-        case 1: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<8, 1>, grid, block, st, a); break;
-        case 2: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<8, 2>, grid, block, st, a); break;
-        default: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<8, 3>, grid, block, st, a); break;
+#define RM_XL(NCH, CW)                                                                                   \
+    switch (cpw) {                                                                                       \
+        case 1: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<NCH, 1, CW>, grid, block, st, a); break; \
+        case 2: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<NCH, 2, CW>, grid, block, st, a); break; \
+        default: e = launch_timed(RM_KERNEL_LAYER, layer_xcd_kernel<NCH, 3, CW>, grid, block, st, a); break; \
     }
+    if (p.d == 8 * kChunkCols) {
+        RM_XL(8, 4)
+    } else {
+        RM_XL(4, 2)
+    }
+#undef RM_XL
     return e != hipSuccess ? e : hipGetLastError();
 }
 

@@ -76,7 +76,8 @@ bool ranges_overlap(const void *a, size_t na, const void *b, size_t nb) {
 
 // Common checks of a layer / stack / dense call; fills the plan.
 rm_status check_call(const rm_ffn_shape *s, int B, int T, const float *x, float *y, const int32_t *idx,
-                     const int32_t *count, bool sparse, int max_count, void *ws, size_t ws_bytes, rm::Plan *p) {
+                     const int32_t *count, bool sparse, int max_count, void *ws, size_t ws_bytes, rm::Plan *p,
+                     unsigned form = 0) {
     rm_status st = check_shape(s);
     if (st != RM_OK) return st;
     if (B <= 0 || T <= 0) return fail(RM_ERR_INVALID_ARG, "B=%d and T=%d must be positive", B, T);
@@ -92,7 +93,7 @@ rm_status check_call(const rm_ffn_shape *s, int B, int T, const float *x, float 
         if (max_count < 0 || max_count > s->d_ff)
             return fail(RM_ERR_SHAPE, "max_count=%d outside [0, d_ff=%d]", max_count, s->d_ff);
     }
-    st = rm::make_plan(s, B, T, sparse ? max_count : s->d_ff, p);
+    st = rm::make_plan(s, B, T, sparse ? max_count : s->d_ff, p, form);
     if (st != RM_OK) return st;
     if (!ws) return fail(RM_ERR_INVALID_ARG, "workspace is NULL");
     if (!aligned(ws, 16)) return fail(RM_ERR_ALIGN, "workspace must be 16-byte aligned");
@@ -291,7 +292,7 @@ bool device_has_256_cus() {
 
 namespace rm {
 
-rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p) {
+rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p, unsigned form) {
     Plan q;
     q.d = s->d;
     q.d_ff = s->d_ff;
@@ -303,7 +304,7 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.act = s->act;
     const int kmax = max_count > 0 ? max_count : 1;
     size_t xn_elem, h_elem;
-    bool xcd_shape = false;
+    bool xcd_shape = false, xcd_room = false;
     int part_slices = 0;  // partial slices the workspace holds (at least q.slices)
     // Aim for one down-projection workgroup per compute unit (256 CUs): a grid just past a multiple of the unit
     // count leaves the units with one more workgroup setting the time (d = 2048, 4916 neurons: 8 slices of 20 chunks,
@@ -361,26 +362,43 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
                                             std::max(1, ceil_div(ceil_div(nchunks, s_target), kBfWaves)));
         q.slice_units = cps;
         q.slices = ceil_div(nchunks, cps);
-        // One sample's long list at d = 2048 (the spread plan's range): gate/up and down in one launch, the
-        // list's chunks cut into 8 slices, one per XCD (at most 3 chunks per wave of the down phase).  The
-        // workspace holds the counters and the partials of either plan, so its size does not depend on the
-        // device; the launch form needs 256 compute units (all 256 workgroups resident, 32 per XCD).
+        // One sample's list in the spread range at d = 2048, or of 8 .. 192 chunks at d = 1024: gate/up and down
+        // in one launch, the list's chunks cut into 8 slices, one per XCD (at most 3 chunks per wave of the down
+        // phase, at most 6 quads per workgroup of the gate/up phase).  It pays where it removes launches: at
+        // d = 2048 it replaces prologue (or epilogue-emitted input), gate/up, split down and epilogue by two
+        // launches, in a stack too; at d = 1024 only for a single layer on given lists (prologue, gate/up and
+        // fused down become two launches; a stack's layer is already gate/up + fused down, and a call that
+        // compacts its mask does so in the prologue's launch).  Measured on one box: config 2 14.3 -> 13.7 us
+        // per layer, its masked call 15.3 -> 16.5; a d = 1024 stack (config 3) 12.55 -> 14.7 and config 4 at
+        // 10 % 17.0 -> 18.2 with it, so those keep the other kernels.  The workspace holds the buffers and the
+        // partials of either plan, so its size does not depend on the device or the call; the launch form needs
+        // 256 compute units (all 256 workgroups resident, 32 per XCD).
         const int cps8 = ceil_div(nchunks, 8);
-        xcd_shape = RM_LAYER_XCD && spread && s->d == 8 * 256 && cps8 <= 3 * 8;
-        if (xcd_shape) {
-            part_slices = std::max(q.slices, ceil_div(nchunks, cps8));
-            if (device_has_256_cus()) {
-                q.xcd_layer = true;
-                q.slice_units = cps8;
-                q.slices = ceil_div(nchunks, cps8);
-            }
-        }
+        const bool xcd_d = s->d == 8 * 256 || s->d == 4 * 256;
+        xcd_shape = RM_LAYER_XCD && B == 1 && T <= kBfTokBlock && cps8 <= 3 * 8 && nchunks >= 8 &&
+                    ((spread && s->d == 8 * 256) || s->d == 4 * 256);
+        // The buffers are reserved for every such d and T, whatever B and max_count, so that the workspace size
+        // stays monotone in them (a workspace sized for more samples or a longer list serves this call).
+        xcd_room = RM_LAYER_XCD && T <= kBfTokBlock && xcd_d;
+        if (xcd_shape) part_slices = std::max(q.slices, ceil_div(nchunks, cps8));
         // Short lists (up to kDfMaxChunks chunks): one workgroup per (column tile, token tile) can sum the whole
         // list.  One sample: 16-token tiles.  Several samples: one 64-token tile, so each sample's listed rows of
         // a column tile are read once (16 samples of 51 tokens, d = 1024: down 17.8 -> 14.8 us against two 32-token tiles).
         q.dn_cpw = ceil_div(nchunks, kDfWaves);
         q.df_nt = B == 1 ? 1 : 4;
         q.fused_down = nchunks <= kDfMaxChunks;
+        if (xcd_shape && (s->d == 8 * 256 || form == 0) && device_has_256_cus()) {  // the one-launch form
+            q.xcd_layer = true;
+            q.fused_down = false;
+            q.slice_units = cps8;
+            q.slices = ceil_div(nchunks, cps8);
+            // A separate gate/up launch on this plan (an anchor's capture of h_a) runs the spread kernel: the
+            // same per-neuron arithmetic and chunk order as the one-launch form's gate/up phase, so a delta step
+            // at the anchor's own input finds h - h_a = 0 exactly.
+            q.gate_groups = 1;
+            q.gate_blocks = kCUs;
+            q.gate_spread = (ceil_div(q.kcap / 4, kCUs) + 1) / 2;
+        }
         q.ntt = ceil_div(T, 16 * q.df_nt);
         // One sample's tiles are 32 columns wide (two per lane), so that the 16-token tiles of a short prompt
         // still give the chip a workgroup per compute unit or more; with several samples, 64 columns.
@@ -424,11 +442,11 @@ rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p)
     q.off_ident_count = off;
     off = align_up(off + static_cast<size_t>(B) * sizeof(int32_t), 256);
     q.off_xn8 = off;
-    if (xcd_shape) off = align_up(off + static_cast<size_t>(8) * T * s->d * 2, 256);
+    if (xcd_room) off = align_up(off + static_cast<size_t>(8) * T * s->d * 2, 256);
     q.off_ssq8 = off;
-    if (xcd_shape) off = align_up(off + static_cast<size_t>(8) * T * ssq_stride(s->d) * sizeof(float), 256);
+    if (xcd_room) off = align_up(off + static_cast<size_t>(8) * T * ssq_stride(s->d) * sizeof(float), 256);
     q.off_sync = off;
-    if (xcd_shape) off = align_up(off + kXcdFlagBytes + kXcdCtrBytes, 256);
+    if (xcd_room) off = align_up(off + kXcdFlagBytes + kXcdCtrBytes, 256);
     q.total = off;
     *p = q;
     return RM_OK;
@@ -525,7 +543,8 @@ RM_EXPORT rm_status rm_sparse_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
     if (L <= 0) return fail(RM_ERR_INVALID_ARG, "L=%d must be positive", L);
     if (!w) return fail(RM_ERR_INVALID_ARG, "weights pointer is NULL");
     rm::Plan p;
-    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p,
+                              rm::kFormStack | rm::kFormMask);
     if (st != RM_OK) return st;
     for (int l = 0; l < L; ++l) {
         st = check_layer(&w[l], l);
@@ -566,7 +585,7 @@ RM_EXPORT rm_status rm_masked_ffn_layer(const rm_ffn_shape *s, const rm_ffn_laye
                                         const float *x, float *y, const uint8_t *mask, int32_t *idx, int32_t *count,
                                         int32_t max_count, void *ws, size_t ws_bytes, void *stream) {
     rm::Plan p;
-    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p, rm::kFormMask);
     if (st != RM_OK) return st;
     st = check_layer(w, 0);
     if (st != RM_OK) return st;
@@ -584,7 +603,8 @@ RM_EXPORT rm_status rm_masked_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
     if (L <= 0) return fail(RM_ERR_INVALID_ARG, "L=%d must be positive", L);
     if (!w) return fail(RM_ERR_INVALID_ARG, "weights pointer is NULL");
     rm::Plan p;
-    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p,
+                              rm::kFormStack | rm::kFormMask);
     if (st != RM_OK) return st;
     for (int l = 0; l < L; ++l) {
         st = check_layer(&w[l], l);
@@ -623,20 +643,22 @@ RM_EXPORT rm_status rm_anchor_ffn_stack(const rm_ffn_shape *s, const rm_ffn_laye
                                         const int32_t *count, int32_t max_count, float *y_anchor, float *h_anchor,
                                         void *ws, size_t ws_bytes, void *stream) {
     rm::Plan p, q;
-    rm_status st = check_call(s, B, T, x, y, nullptr, nullptr, false, 0, ws, ws_bytes, &p);  // dense layers
+    // the dense layers
+    rm_status st = check_call(s, B, T, x, y, nullptr, nullptr, false, 0, ws, ws_bytes, &p, rm::kFormStack);
     if (st != RM_OK) return st;
     // The group's lists: their plan sizes the capture launch, which uses only the dense layout's regions (its
     // own plan may ask for more, e.g. the one-launch layer form's buffers), so the dense size is what counts.
-    st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, SIZE_MAX, &q);
+    st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, SIZE_MAX, &q, rm::kFormStack);
     if (st != RM_OK) return st;
     st = check_anchor_buffers(s, w, L, B, T, x, y, max_count, y_anchor, h_anchor, ws, ws_bytes);
     if (st != RM_OK) return st;
     st = check_lists(s, L, B, T, y, idx, count, ws, p.total);
     if (st != RM_OK) return st;
-    // The capture reads the dense layers' FFN input and sums of squares from the dense workspace layout; it
-    // writes nothing else there.
-    q.off_xn = p.off_xn;
-    q.off_ssq = p.off_ssq;
+    // The capture reads the dense layers' FFN input and sums of squares from the dense workspace layout (with the
+    // one-launch layer form, XCD 0's copies, which that launch completes and which have the same layout for one
+    // sample); it writes nothing else there.
+    q.off_xn = p.xcd_layer ? p.off_xn8 : p.off_xn;
+    q.off_ssq = p.xcd_layer ? p.off_ssq8 : p.off_ssq;
     q.off_h = p.off_h;  // not written by a capture
     AnchorTerms at;
     at.ya_out = y_anchor;
@@ -659,7 +681,7 @@ RM_EXPORT rm_status rm_delta_ffn_stack(const rm_ffn_shape *s, const rm_ffn_layer
                                        int32_t max_count, const float *y_anchor, const float *h_anchor, void *ws,
                                        size_t ws_bytes, void *stream) {
     rm::Plan p;
-    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p);
+    rm_status st = check_call(s, B, T, x, y, idx, count, true, max_count, ws, ws_bytes, &p, rm::kFormStack);
     if (st != RM_OK) return st;
     st = check_anchor_buffers(s, w, L, B, T, x, y, max_count, y_anchor, h_anchor, ws, ws_bytes);
     if (st != RM_OK) return st;

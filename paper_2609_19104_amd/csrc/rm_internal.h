@@ -98,7 +98,11 @@ struct Plan {
            off_ssq8 = 0, off_sync = 0, total = 0;
 };
 
-rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p);
+// form: the kind of call the plan is for, 0 (a single layer on given lists) or a sum of the flags below; it
+// decides whether the one-launch layer form pays (the workspace size does not depend on it).
+constexpr unsigned kFormStack = 1;  // several layers
+constexpr unsigned kFormMask = 2;   // the call compacts masks
+rm_status make_plan(const rm_ffn_shape *s, int B, int T, int max_count, Plan *p, unsigned form = 0);
 
 // ---------------------------------------------------------------------------------------------------------
 // Launchers (enqueue only; all arguments already validated).

@@ -1,6 +1,6 @@
-"""GPU parity of the one-launch layer form: one sample's list of 257 .. 768 groups of 8 slots at d = 2048 runs
-the gate/up and the down projection in one launch whose workgroups meet per XCD (layer_xcd_kernel), then the
-epilogue.  Against the float64 oracle on the same seeded inputs, across that range of list lengths (the shortest,
+"""GPU parity of the one-launch layer form: one sample's list of 257 .. 768 groups of 8 slots at d = 2048 (or a
+single layer's list of 8 .. 192 chunks of 32 neurons at d = 1024) runs the gate/up and the down projection in one
+launch whose workgroups meet per XCD (layer_xcd_kernel), then the epilogue.  Against the float64 oracle on the same seeded inputs, across that range of list lengths (the shortest,
 whose last XCD slice holds 2 chunks and leaves half of that XCD's workgroups without gate/up work, up to slices
 of 24 chunks), token counts 1 .. 64, with and without a norm, slots past the count, inside stacks (the per-XCD
 counters carried from layer to layer), repeated calls, an empty list and an Eq. 4 delta step.
@@ -30,6 +30,11 @@ def test_the_one_launch_form_runs():
     import paper_2609_19104_amd as rm
     for d_ff, T, k in ((8192, 51, 2057), (16384, 17, 6144), (16384, 51, 4916), (8192, 1, 4300)):
         assert rm.rm_layer_kernels(D, d_ff, rm.RM_BF16, 1, T, k) == 1 << rm.RM_KERNEL_LAYER
+    for d_ff, T, k in ((4096, 51, 1229), (4096, 64, 4096), (8192, 1, 6144)):
+        assert rm.rm_layer_kernels(1024, d_ff, rm.RM_BF16, 1, T, k) == 1 << rm.RM_KERNEL_LAYER
+    both = (1 << rm.RM_KERNEL_GATEUP) | (1 << rm.RM_KERNEL_DOWN)
+    assert rm.rm_layer_kernels(1024, 4096, rm.RM_BF16, 2, 51, 1229) == both  # two samples
+    assert rm.rm_layer_kernels(1024, 4096, rm.RM_BF16, 1, 51, 200) == both   # 7 chunks
 
 
 def _oracle_layer(layer, x, mult):
@@ -57,6 +62,24 @@ def test_layer_parity(d_ff, T, k, spare, norm):
     idx, cnt = compact(mask)
     y = run_layer(dev_weights(layer), x, idx, cnt, min(d_ff, k + spare))
     _check(y, _oracle_layer(layer, x, mask.astype(np.float64)), x, f"layer d_ff={d_ff} T={T} k={k}")
+
+
+@pytest.mark.parametrize("d_ff,T,k,spare,norm", [
+    (4096, 51, 1229, 0, "random"),   # a top-30% mask of 4096 neurons: 39 chunks, slices of 5
+    (4096, 64, 4000, 96, "none"),    # 128 chunks (slices of 16), slots past the count
+    (4096, 1, 256, 0, "ones"),       # 8 chunks, one per XCD; one token
+    (8192, 17, 6144, 0, "random"),   # 192 chunks: slices of 24, the range's end
+])
+def test_layer_parity_d1024(d_ff, T, k, spare, norm):
+    d = 1024
+    layer = wl.make_layer(136, d_ff, d, d_ff, "bf16", norm=norm)
+    x = wl.make_x(136, (1, T, d), d_ff, T, k)
+    mask = wl.uniform_mask(wl.rng(136, 4, d_ff, T, k), d_ff, k)[None]
+    idx, cnt = compact(mask)
+    y = run_layer(dev_weights(layer), x, idx, cnt, min(d_ff, k + spare))
+    _check(y, _oracle_layer(layer, x, mask.astype(np.float64)), x, f"layer d=1024 d_ff={d_ff} T={T} k={k}")
+    y2 = run_layer(dev_weights(layer), x, idx, cnt, min(d_ff, k + spare), in_place=True)
+    assert np.array_equal(y.view(np.uint32), y2.view(np.uint32))
 
 
 def test_stack_repeat_and_in_place():
@@ -119,3 +142,60 @@ def test_delta_step():
     _check(yd, ref, xt, "delta step")
     y_same = run_delta(lws, xa, idx, cnt, k, ya, ha)
     assert np.array_equal(y_same.view(np.uint32), y.cpu().numpy().view(np.uint32))
+
+
+def _masked(lws, x, masks, max_count, mask_dev=None):
+    """rm_masked_ffn_layer (one mask) or rm_masked_ffn_stack -> (y, idx, count) as numpy arrays."""
+    import paper_2609_19104_amd as rm
+    d_ff, d = lws[0][0].shape
+    n = masks.shape[0]
+    xt = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    mt = torch.from_numpy(masks).cuda() if mask_dev is None else mask_dev
+    idx = torch.full((n, d_ff), 777, dtype=torch.int32, device="cuda")
+    cnt = torch.full((n,), -3, dtype=torch.int32, device="cuda")
+    y = torch.full_like(xt, float("nan"))
+    ws = rm.workspace(d, d_ff, rm.RM_BF16, 1, x.shape[1], max_count)
+    ws.fill_(0xFF)
+    if n == 1:
+        rm.rm_masked_ffn_layer(xt, y, lws[0], mt, idx, cnt, max_count, ws)
+    else:
+        rm.rm_masked_ffn_stack(xt, y, lws, mt, idx, cnt, max_count, ws)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), idx.cpu().numpy(), cnt.cpu().numpy()
+
+
+@pytest.mark.parametrize("d,d_ff,L,T,counts,max_count", [
+    (2048, 8192, 2, 51, [3000, 2600], 3000),  # a masked stack: each layer's launch compacts its own mask
+    (2048, 16384, 1, 51, [4000], 2500),       # count above max_count: the whole list out, 2500 applied
+    (2048, 16384, 1, 17, [0], 3000),          # an empty mask
+    (1024, 4096, 1, 64, [4096], 4096),        # every neuron
+    (1024, 4112, 1, 5, [4100], 4112),         # d_ff = 257 x 16: the last chunk past d_ff, slots past the count
+])
+def test_masked_calls_in_the_one_launch_range(d, d_ff, L, T, counts, max_count):
+    # Masked calls whose lists the one-launch form takes: idx / count bit for bit the oracle's compaction (the -1
+    # tail included); y bit for bit the same call on those lists at d = 2048 (the compaction launch ahead of the
+    # same kernels), within the bar of the oracle at d = 1024 (a masked single layer there keeps the compaction in
+    # the prologue's launch and the gate/up and fused down kernels).
+    import paper_2609_19104_amd as rm
+    assert rm.rm_layer_kernels(d, d_ff, rm.RM_BF16, 1, T, max_count) == 1 << rm.RM_KERNEL_LAYER
+    layers = [wl.make_layer(137, l, d, d_ff, "bf16", norm="random") for l in range(L)]
+    lws = [dev_weights(l) for l in layers]
+    x = wl.make_x(137, (1, T, d), d_ff, T)
+    masks = np.stack([wl.uniform_mask(wl.rng(137, 4, l, d_ff), d_ff, c) for l, c in enumerate(counts)])
+    y, idx, cnt = _masked(lws, x, masks, max_count)
+    idx_ref, cnt_ref = oracle.compact_mask(masks)
+    assert np.array_equal(cnt, cnt_ref) and np.array_equal(idx, idx_ref)
+    i2, c2 = compact(masks)
+    y2 = run_layer(lws[0], x, i2, c2, max_count) if L == 1 else run_stack(lws, x, i2, c2, max_count)
+    if counts == [0]:
+        assert np.array_equal(y.view(np.uint32), x.view(np.uint32))
+    if d == 2048:
+        assert np.array_equal(y.view(np.uint32), y2.view(np.uint32))
+    else:
+        applied = np.zeros((L, d_ff))
+        for l in range(L):
+            applied[l, idx_ref[l, :min(cnt_ref[l], max_count)]] = 1
+        ref = oracle.ffn_stack(x[0], [lay.f64() for lay in layers], list(applied))[None]
+        _check(y, ref, x, "masked call")
+        _check(y2, ref, x, "call on the lists")
+

@@ -644,10 +644,10 @@ struct NoPre {
 // kLate (the one-launch layer form, whose workgroups write the input first): early() runs behind the index
 // loads, and the first input chunks are loaded after it instead of ahead of the indices.
 template <int NG, int NCH, int PXM = RM_SPREAD_PX, int PRE_AT = 0, bool kLate = false, typename Pre = NoPre,
-          typename Early = NoPre>
+          typename Early = NoPre, typename Meet = NoPre>
 __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G, int nquads,
                                                    uint16_t (*xs)[64 * kRowPitch], rm_f32x4 *red2, float *spans,
-                                                   Pre pre = Pre{}, Early early = Early{}) {
+                                                   Pre pre = Pre{}, Early early = Early{}, Meet meet = Meet{}) {
     constexpr int NT = 4;
     constexpr int PW0 = RM_SPREAD_WTILES / (NG > 0 ? NG : 1);  // weight chunks in flight
     constexpr int PW = PW0 < 1 ? 1 : (PW0 < NCH ? PW0 : NCH);
@@ -702,7 +702,8 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
     }
     __builtin_amdgcn_sched_barrier(0);
     early();
-    if constexpr (kLate) {
+    constexpr bool kMeet = !__is_same(Meet, NoPre);
+    if constexpr (kLate && !kMeet) {
 #pragma unroll
         for (int c = 0; c < PX; ++c) load_x(c);
         __builtin_amdgcn_sched_barrier(0);
@@ -716,6 +717,13 @@ __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G
         wrow[j] = a.wg + up_off + static_cast<size_t>(clamp_neuron(raw_n[j], a.d_ff)) * a.d + wave * 32 + grp * 8;
 #pragma unroll
     for (int c = 0; c < PW; ++c) load_w(c);
+    if constexpr (kMeet) {  // the first weights go out before the caller's meeting, the input after it
+        __builtin_amdgcn_sched_barrier(0);
+        meet();
+#pragma unroll
+        for (int c = 0; c < PX; ++c) load_x(c);
+        __builtin_amdgcn_sched_barrier(0);
+    }
     if constexpr (PRE_AT == 0) pre();
     // Behind the first weights, the partial sums of squares of tokens 0..63 (NCH spans per token); their span
     // sums go to LDS after the products, so that forming the norm factors needs no memory round trip after them.
@@ -978,10 +986,11 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
 // load reads past; a device-scope store and a device-scope load meet.
 //   Meeting 1 (after phase 0): each workgroup stores the launch's tag in its flag with a device-scope store (tag:
 //            the dispatch packet's id mixed with the queue's address, different for every launch, so the flags
-//            need no reset and the workspace no initialization) once its phase-0 stores are complete, and polls the
-//            XCD's 32 flags with device-scope loads, before it issues any weight load (a poll issued behind them
-//            would wait for them, and its read of memory would queue behind the stream).  Rank 0 first resets the
-//            XCD's counter for meeting 2 with an atomic swap.
+//            need no reset and the workspace no initialization) once its phase-0 stores are complete, and waits
+//            until the XCD's 32 flags hold the tag: at d = 2048 with scalar loads issued behind its first weight
+//            loads (they have their own counter), at d = 1024 with device-scope vector loads before any weight
+//            load (a vector poll issued behind them would wait for them).  Rank 0 first resets the XCD's counter
+//            for meeting 2 with an atomic swap.
 //   Meeting 2 (after phase 1): an atomic add on that counter (executed past the L1, where the polls, also
 //            atomic adds, read it) until it reaches 32.
 // The xn copy and H are read with plain loads: no line of them is read in the launch before it is written.  A
@@ -1034,6 +1043,7 @@ __device__ __forceinline__ unsigned long long launch_tag() {
 template <int NCH, int CPW, int CW>
 __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
     constexpr int NT = 4;
+    constexpr bool kScalarPoll = NCH == 8;  // meeting 1's wait: scalar loads behind the first weights (d = 2048)
     constexpr int kXsBytes = 2 * 64 * kRowPitch * 2;            // phase 1: the staged input chunks
     constexpr int kRed2Bytes = kGuWaves * NT * 64 * 16;          // phase 1: the third tile's wave partials
     constexpr int kRedBytes = kGuWaves * NT * 4 * 64 * 16;       // phase 2: the 8 waves' 64-token x 16 CW tiles (CW <= 4)
@@ -1146,18 +1156,60 @@ __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
                                            blk * kChunkCols + lane * 4) = packed;
         }
         if (tid == 0 && rank == 0) __hip_atomic_exchange(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's stores are complete
+        // This wave's stores are complete (vmcnt(0); the builtin, unlike an asm statement, tells the compiler
+        // that the index loads are complete too, so the weight loads behind the flag's store need no wait).
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0x0f70);
         __syncthreads();
-        // Meeting 1, before any weight load is in flight (a poll would wait behind them): arrive, then wait until
-        // the XCD's 32 flags hold the tag.
+        // Meeting 1: arrive; at d = 1024 also wait here, before any weight load is in flight (a vector poll would
+        // wait behind them), until the XCD's 32 flags hold the tag.
         if (tid == 0) __hip_atomic_store(fl + rank, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (!kScalarPoll) {
+            if (wave == 0) {
+                bool fail = false;
+                const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+                for (;;) {
+                    const unsigned long long f =
+                        __hip_atomic_load(fl + (lane & (kXlPerXcd - 1)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (__builtin_amdgcn_ballot_w64(f != tag) == 0) break;
+                    if (static_cast<long long>(__builtin_amdgcn_s_memrealtime() - t0) > a.spin_ticks) {
+                        fail = true;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+                if (lane == 0 && fail) s_fail = 1;
+            }
+            __syncthreads();
+        }
+    };
+    // At d = 2048 the wait of meeting 1 comes behind the first weight loads: wave 0 polls with scalar loads that
+    // bypass the scalar cache (their own counter, so they do not wait for the weights in flight) until the XCD's
+    // 32 flags hold the tag, 8 flags (64 bytes) per load.  (Measured: config 4 at 30 % 27.6 -> 26.6 us per
+    // step; at d = 1024, with less weight per compute unit, 13.8 -> 14.1, so there the vector poll stays.)
+    auto meet = [&]() {
         if (wave == 0) {
             bool fail = false;
             const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
             for (;;) {
-                const unsigned long long f =
-                    __hip_atomic_load(fl + (lane & (kXlPerXcd - 1)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (__builtin_amdgcn_ballot_w64(f != tag) == 0) break;
+                typedef unsigned u32x16 __attribute__((ext_vector_type(16)));
+                u32x16 f0, f1, f2, f3;
+                asm volatile(
+                    "s_load_dwordx16 %0, %4, 0x0 glc\n\t"
+                    "s_load_dwordx16 %1, %4, 0x40 glc\n\t"
+                    "s_load_dwordx16 %2, %4, 0x80 glc\n\t"
+                    "s_load_dwordx16 %3, %4, 0xc0 glc\n\t"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=s"(f0), "=s"(f1), "=s"(f2), "=s"(f3)
+                    : "s"(fl)
+                    : "memory");
+                const unsigned lo = static_cast<unsigned>(tag), hi = static_cast<unsigned>(tag >> 32);
+                bool all = true;
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    all = all && f0[2 * i] == lo && f0[2 * i + 1] == hi && f1[2 * i] == lo && f1[2 * i + 1] == hi &&
+                          f2[2 * i] == lo && f2[2 * i + 1] == hi && f3[2 * i] == lo && f3[2 * i + 1] == hi;
+                if (all) break;
                 if (static_cast<long long>(__builtin_amdgcn_s_memrealtime() - t0) > a.spin_ticks) {
                     fail = true;
                     break;
@@ -1175,24 +1227,31 @@ __global__ __launch_bounds__(kGuThreads) void layer_xcd_kernel(XlArgs a) {
     auto xs = reinterpret_cast<uint16_t(*)[64 * kRowPitch]>(lds);
     auto red2 = reinterpret_cast<rm_f32x4 *>(lds + kXsBytes);
     const int q0 = c0 * (rm::kBfChunk / 4) + rank;
-    switch ((mine + 1) / 2) {
-        case 0:
-            early();
-            pre();
-            break;
-        case 1:
-            gateup_spread_body<1, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
-                                                                       early);
-            break;
-        case 2:
-            gateup_spread_body<2, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
-                                                                       early);
-            break;
-        default:
-            gateup_spread_body<3, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans, pre,
-                                                                       early);
-            break;
-    }
+    auto phase1 = [&](auto wait) {  // wait: the scalar poll, or nothing (early() has polled)
+        switch ((mine + 1) / 2) {
+            case 0:
+                early();
+                wait();
+                pre();
+                break;
+            case 1:
+                gateup_spread_body<1, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans,
+                                                                           pre, early, wait);
+                break;
+            case 2:
+                gateup_spread_body<2, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans,
+                                                                           pre, early, wait);
+                break;
+            default:
+                gateup_spread_body<3, NCH, RM_XCD_PX, RM_XCD_PRE_AT, true>(g, q0, kXlPerXcd, mine, xs, red2, spans,
+                                                                           pre, early, wait);
+                break;
+        }
+    };
+    if constexpr (kScalarPoll)
+        phase1(meet);
+    else
+        phase1(NoPre{});
 
     // Meeting 2: this workgroup's stores of h are complete before it arrives.
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");

@@ -24,8 +24,8 @@
  *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every buffer and the stream; the
  *     library allocates nothing and never synchronizes.  Its only state is a thread-local error string, the
  *     events that rm_profile_kernel_events arms for the calling thread, a per-device record of the compute-unit
- *     count (asked once; it decides whether the one-launch layer form can run), and the noalloc entry point's
- *     per-device scratch array.
+ *     count (asked once; with the RM_NO_LAYER_FORM environment variable, read once, it decides whether the
+ *     one-launch layer form can run), and the noalloc entry point's per-device scratch array.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the default stream).
  *   - Every argument is validated on the host before anything is enqueued; on error nothing is enqueued and
  *     the call returns a negative rm_status with a detail message in rm_last_error().
@@ -35,6 +35,12 @@
  *     On the bf16 path the FFN input xn and the activations h are rounded to bf16 before the matrix-core
  *     products.
  *   - The result is deterministic: no floating-point atomics; repeated calls give bitwise equal outputs.
+ *   - The one-launch layer form (RM_KERNEL_LAYER; on a device with 256 compute units) needs all 256 of its
+ *     workgroups resident at once: the 32 workgroups of each XCD wait for each other twice.  Work on other
+ *     streams or processes that holds compute units while it runs delays it; a wait gives up after 200 ms,
+ *     and then the affected outputs are NaN (the kernel always finishes).  Callers that share the GPU that
+ *     way set the environment variable RM_NO_LAYER_FORM=1 before their first call: every call then takes
+ *     the other kernels (same results up to the order of the float32 sums).
  */
 #ifndef RMUSCLE_H
 #define RMUSCLE_H

@@ -6,6 +6,7 @@
 // after the first run in place on y.  Nothing here synchronizes or allocates.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -271,9 +272,16 @@ rm_status run_layers(const rm::Plan &p, const rm_ffn_layer_weights *w, int L, co
     return RM_OK;
 }
 
-// Whether the current device has the 256 compute units (8 XCDs of 32) that the one-launch layer form needs
-// resident at once; asked once per device.
+// Whether the one-launch layer form may run on the current device: it has the 256 compute units (8 XCDs of 32)
+// that the form needs resident at once (asked once per device), and the environment variable RM_NO_LAYER_FORM
+// was not set to a non-empty value other than "0" when the process first asked (for callers that share the GPU
+// with other work that can hold compute units while the form's workgroups wait for each other).
 bool device_has_256_cus() {
+    static const bool off = [] {
+        const char *e = getenv("RM_NO_LAYER_FORM");
+        return e != nullptr && e[0] != '\0' && strcmp(e, "0") != 0;
+    }();
+    if (off) return false;
     static std::atomic<int> known[64];  // 0 = not asked, 1 = no, 2 = yes
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0) return false;

@@ -199,3 +199,42 @@ def test_masked_calls_in_the_one_launch_range(d, d_ff, L, T, counts, max_count):
         _check(y, ref, x, "masked call")
         _check(y2, ref, x, "call on the lists")
 
+
+
+def test_form_switched_off_by_the_environment(tmp_path):
+    # RM_NO_LAYER_FORM=1 (read at the process's first call): the same layer takes the other kernels, in a child
+    # process; both results within the bar of the oracle.
+    import os
+    import subprocess
+    import sys
+    import paper_2609_19104_amd as rm
+    d_ff, T, k = 8192, 17, 3000
+    assert rm.rm_layer_kernels(D, d_ff, rm.RM_BF16, 1, T, k) == 1 << rm.RM_KERNEL_LAYER
+    here = os.path.dirname(os.path.abspath(__file__))
+    out = tmp_path / "y.npy"
+    child = f"""
+import sys
+sys.path[:0] = [{here!r}, {os.path.dirname(here)!r}]
+import numpy as np, torch
+import paper_2609_19104_amd as rm, workloads as wl
+from gpu_helpers import compact, dev_weights, run_layer
+both = (1 << rm.RM_KERNEL_GATEUP) | (1 << rm.RM_KERNEL_DOWN)
+assert rm.rm_layer_kernels({D}, {d_ff}, rm.RM_BF16, 1, {T}, {k}) == both
+layer = wl.make_layer(139, 0, {D}, {d_ff}, "bf16", norm="random")
+x = wl.make_x(139, (1, {T}, {D}), 0)
+idx, cnt = compact(wl.uniform_mask(wl.rng(139, 4), {d_ff}, {k})[None])
+np.save({str(out)!r}, run_layer(dev_weights(layer), x, idx, cnt, {k}))
+"""
+    env = dict(os.environ, RM_NO_LAYER_FORM="1")
+    r = subprocess.run([sys.executable, "-c", child], env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    y_off = np.load(out)
+    layer = wl.make_layer(139, 0, D, d_ff, "bf16", norm="random")
+    x = wl.make_x(139, (1, T, D), 0)
+    mask = wl.uniform_mask(wl.rng(139, 4), d_ff, k)[None]
+    idx, cnt = compact(mask)
+    y_on = run_layer(dev_weights(layer), x, idx, cnt, k)
+    ref = _oracle_layer(layer, x, mask.astype(np.float64))
+    _check(y_on, ref, x, "one-launch form")
+    _check(y_off, ref, x, "form switched off")
+    assert not np.array_equal(y_on.view(np.uint32), y_off.view(np.uint32))  # the other kernels did run

@@ -1,6 +1,8 @@
 """The library's calls captured in a HIP graph (through torch.cuda.CUDAGraph) give the eager results on every
 replay.  Replays alternate with eager work and synchronizations; the kernels are deterministic, so every
-replay must match the eager output bit for bit."""
+replay must match the eager output bit for bit.  The cases include the one-launch layer form (one sample at
+d = 2048 in its list range, single and stacked, and a single layer at d = 1024), whose per-launch tags must
+differ on every replay and every eager launch in between."""
 import numpy as np
 import pytest
 import torch
@@ -17,18 +19,24 @@ import paper_2609_19104_amd as rm  # noqa: E402
 from gpu_helpers import TOL_BF16, dev_f32, dev_weights, errors  # noqa: E402
 
 
-def _setup(L, B, norm, seed):
-    d, d_ff, T = 512, 1024, 51
+def _setup(L, B, norm, seed, d, d_ff, k):
+    T = 51
     layers = [wl.make_layer(seed, l, d, d_ff, "bf16", norm=norm) for l in range(L)]
     x = wl.make_x(seed, (B, T, d), 0)
-    masks = np.stack([np.stack([wl.uniform_mask(wl.rng(seed, 4, l, b), d_ff, 300) for b in range(B)])
+    masks = np.stack([np.stack([wl.uniform_mask(wl.rng(seed, 4, l, b), d_ff, k) for b in range(B)])
                       for l in range(L)]).reshape(L * B, d_ff)
     return layers, x, masks
 
 
-@pytest.mark.parametrize("L,B,norm", [(1, 1, "none"), (3, 2, "ones")])
-def test_graph_replays_match_eager(L, B, norm):
-    layers, x, masks = _setup(L, B, norm, 40 + L)
+@pytest.mark.parametrize("L,B,norm,d,d_ff,k", [
+    (1, 1, "none", 512, 1024, 300),
+    (3, 2, "ones", 512, 1024, 300),
+    (1, 1, "random", 2048, 8192, 3000),  # the one-launch layer form
+    (2, 1, "ones", 2048, 8192, 3000),    # the one-launch layer form in a stack
+    (1, 1, "random", 1024, 4096, 1229),  # the one-launch layer form at d = 1024
+])
+def test_graph_replays_match_eager(L, B, norm, d, d_ff, k):
+    layers, x, masks = _setup(L, B, norm, 40 + L, d, d_ff, k)
     lws = [dev_weights(l) for l in layers]
     d_ff, d = layers[0].d_ff, layers[0].d
     T = x.shape[1]
@@ -37,14 +45,14 @@ def test_graph_replays_match_eager(L, B, norm):
     cnt = torch.empty((L * B,), dtype=torch.int32, device="cuda")
     xt = dev_f32(x)
     y = torch.empty_like(xt)
-    ws = rm.workspace(d, d_ff, rm.RM_BF16, B, T, 300, device="cuda")
+    ws = rm.workspace(d, d_ff, rm.RM_BF16, B, T, k, device="cuda")
 
     def step():
         rm.rm_mask_compact(mask_t, idx, cnt)
         if L == 1:
-            rm.rm_sparse_ffn_layer(xt, y, lws[0], idx, cnt, 300, ws)
+            rm.rm_sparse_ffn_layer(xt, y, lws[0], idx, cnt, k, ws)
         else:
-            rm.rm_sparse_ffn_stack(xt, y, lws, idx, cnt, 300, ws)
+            rm.rm_sparse_ffn_stack(xt, y, lws, idx, cnt, k, ws)
 
     step()
     torch.cuda.synchronize()
@@ -63,7 +71,7 @@ def test_graph_replays_match_eager(L, B, norm):
 
     other_x = dev_f32(wl.make_x(99, x.shape, 1))
     other_y = torch.empty_like(other_x)
-    other_ws = rm.workspace(d, d_ff, rm.RM_BF16, B, T, 300, device="cuda")
+    other_ws = rm.workspace(d, d_ff, rm.RM_BF16, B, T, k, device="cuda")
     for r in range(4):
         y.fill_(float("nan"))
         idx.fill_(7)
@@ -73,9 +81,9 @@ def test_graph_replays_match_eager(L, B, norm):
         assert torch.equal(y, y_eager), f"replay {r} differs from the eager result"
         # eager work between replays, on other buffers
         if L == 1:
-            rm.rm_sparse_ffn_layer(other_x, other_y, lws[0], idx, cnt, 300, other_ws)
+            rm.rm_sparse_ffn_layer(other_x, other_y, lws[0], idx, cnt, k, other_ws)
         else:
-            rm.rm_sparse_ffn_stack(other_x, other_y, lws, idx, cnt, 300, other_ws)
+            rm.rm_sparse_ffn_stack(other_x, other_y, lws, idx, cnt, k, other_ws)
         torch.cuda.synchronize()
 
     ref = np.stack([oracle.ffn_stack(x[b], [lay.f64() for lay in layers],

@@ -796,15 +796,40 @@ def secondary_lines(device, steps: int, warmup: int) -> dict:
     return out
 
 
+def _code_only(text: str) -> str:
+    """C/C++ source without its comments and trailing blanks (string and character literals kept), so that an
+    edit of comments alone leaves the digest below unchanged."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":  # a literal: copied through, escapes included
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return "\n".join(line.rstrip() for line in "".join(out).split("\n") if line.strip())
+
+
 def kernel_source_digest() -> str:
-    """sha256 over the HIP sources (names and contents, sorted): identifies the kernels a counter run measured."""
+    """sha256 over the HIP sources' code (names and code without comments, files sorted): identifies the kernels
+    a counter run measured."""
     import hashlib
     h = hashlib.sha256()
     for name in sorted(os.listdir(CSRC)):
         if name.endswith((".hip", ".h")):
             h.update(name.encode())
-            with open(os.path.join(CSRC, name), "rb") as f:
-                h.update(f.read())
+            with open(os.path.join(CSRC, name), encoding="utf-8") as f:
+                h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 

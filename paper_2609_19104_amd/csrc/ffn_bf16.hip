@@ -642,7 +642,9 @@ struct NoPre {
     __device__ void operator()() const {}
 };
 // kLate (the one-launch layer form, whose workgroups write the input first): early() runs behind the index
-// loads, and the first input chunks are loaded after it instead of ahead of the indices.
+// loads, and the first input chunks are loaded after it instead of ahead of the indices.  With a meet() (the
+// layer form at d = 2048) the first weight chunks go out after early(), then meet() waits for the other
+// workgroups, then the input chunks go out.
 template <int NG, int NCH, int PXM = RM_SPREAD_PX, int PRE_AT = 0, bool kLate = false, typename Pre = NoPre,
           typename Early = NoPre, typename Meet = NoPre>
 __device__ __forceinline__ void gateup_spread_body(const GuArgs &a, int q, int G, int nquads,
@@ -966,19 +968,19 @@ __global__ __launch_bounds__(kDnThreads) void down_bf16_kernel(DnArgs a) {
 
 // ------------------------------------------------------------------------------------------ layer, per XCD
 
-// One sample's list at d = 2048 with 257 .. 768 groups of 8 listed slots (the spread plan's range): the FFN input's
-// bf16 rounding, the gate/up and the down projection in one launch of 256 workgroups, one per compute unit, so no
-// prologue launch precedes it.  The list's 32-slot chunks are cut into 8 slices of cps chunks, slice x for the 32
-// workgroups i with i mod 8 = x.  The dispatcher deals a launch's workgroups to the 8 XCDs in turn, starting
-// where the previous launch stopped, so such a group shares one XCD and its L2; each workgroup checks this
-// against the hardware's XCC_ID register at meeting 1.
+// One sample's list at d = 2048 with 257 .. 768 groups of 8 listed slots (the spread plan's range), or a single
+// layer's list of 8 .. 192 chunks at d = 1024: the FFN input's bf16 rounding, the gate/up and the down projection
+// in one launch of 256 workgroups, one per compute unit, so no prologue launch precedes it.  The list's 32-slot
+// chunks are cut into 8 slices of cps chunks, slice x for the 32 workgroups i with i mod 8 = x.  The dispatcher
+// deals a launch's workgroups to the 8 XCDs in turn, starting where the previous launch stopped, so such a group
+// shares one XCD and its L2; each workgroup checks this against the hardware's XCC_ID register at meeting 1.
 //   Phase 0: the XCD's 32 workgroups write the XCD's own copy of xn = bf16(x g) (and, with a norm, its per-token
 //            partial sums of squares, in the prologue's order), one (token row, 256-column block) unit per wave.
 //   Phase 1: the spread gate/up over the slice's quads of 4 slots (dealt round-robin over the XCD's 32
 //            workgroups), reading the XCD's xn copy and writing h into H.
-//   Phase 2: the down projection of the same slice for column tile i / 8 (64 columns), whose float32 partial goes
-//            to the slice's row of the partials as the split down projection writes it, so the epilogue launch
-//            is unchanged.
+//   Phase 2: the down projection of the same slice for column tile i / 8 (64 columns at d = 2048, 32 at
+//            d = 1024), whose float32 partial goes to the slice's row of the partials as the split down
+//            projection writes it, so the epilogue launch is unchanged.
 // Between the phases the XCD's workgroups meet; everything a phase reads was written by compute units of the same
 // XCD, so no hand-off needs the device-wide L2 write-back that makes a hand-off between XCDs cost more than a
 // kernel boundary.  Inside one launch a plain load can be served a stale copy of a line that another compute unit

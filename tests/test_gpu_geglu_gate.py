@@ -43,6 +43,7 @@ CASES = [
     (1024, 4096, 3, 1, 51, 1229, "bf16", "gelu_tanh"),  # one sample: fused down, xn for the next layer
     (160, 512, 2, 3, 17, 200, "bf16", "gelu_tanh"),     # stack with the epilogue emitting xn
     (2048, 8192, 2, 1, 51, 3000, "bf16", "gelu_tanh"),  # one sample's long list: gate/up and down in one launch
+    (1024, 4096, 1, 1, 51, 1229, "bf16", "gelu_tanh"),  # a single d = 1024 layer: the one-launch form too
     (128, 300, 2, 2, 9, 150, "f32", "gelu_tanh"),
     (64, 100, 1, 1, 3, 37, "f32", "silu"),
 ]
